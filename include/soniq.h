@@ -1,0 +1,207 @@
+/*
+ * soniq.h -- C ABI of libsoniq, a gfx950 (MI355X) implementation of the
+ * inference hot path of SONIQ (arXiv 2311.14114): a per-channel two-level
+ * mixed-precision integer matrix multiply
+ *
+ *     Y[m, n] = bf16( s_w[n] * sum_g s_a[g] * ACC[g][m][n] ),
+ *     ACC[g][m][n] = sum over input channels k of precision group g of
+ *                    q_a[m, k] * q_w[n, k]                   (exact, int32)
+ *
+ * used for linear layers and for convolutions lowered to a GEMM (im2col).
+ *
+ * Paper passages the calls implement:
+ *   - Sec. 2.4, constraints C1 (one precision per SIMD/tile block), C2 (one
+ *     scale per fused dot product), C3 (few precision levels: at most two
+ *     widths per operand here), C5 (coalesced channel-packed layout);
+ *   - Sec. 3, Phase I "Dynamic channel re-ordering" and Alg. 1 (channels of
+ *     equal precision made contiguous), Fig. "normalization" (each
+ *     equal-precision block padded to the vector width without changing
+ *     results);
+ *   - Sec. 3, "Enabling Low-Cost Fixed-Point Operations": group max-abs scale
+ *     (item 1), unsigned activation codes (item 2), signed two's-complement
+ *     weight codes (item 3, Eq. 1);
+ *   - Alg. 1 Phase II: the forward pass as integer MAC execution.
+ *
+ * Conventions for every call:
+ *   - "device" pointers are HIP device allocations on the current device;
+ *     "host" pointers are ordinary host memory.  All matrices are row-major
+ *     with the given leading dimension in elements.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued on it asynchronously unless stated otherwise.
+ *   - Arguments are validated synchronously before anything is enqueued; on
+ *     a non-OK status nothing was enqueued and outputs are untouched.  The
+ *     message of the last failure on this thread is soniq_last_error().
+ *   - No call throws; HIP errors are returned as SONIQ_ERR_HIP, and faults of
+ *     earlier asynchronous work may be reported by a later call.
+ */
+#ifndef SONIQ_H_
+#define SONIQ_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SONIQ_OK = 0,
+  SONIQ_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, width or handle */
+  SONIQ_ERR_UNSUPPORTED = 2,      /* valid but outside this build's limits */
+  SONIQ_ERR_OUT_OF_MEMORY = 3,    /* a device or host allocation failed */
+  SONIQ_ERR_HIP = 4               /* a HIP runtime call failed */
+} soniq_status;
+
+/* Opaque handles.  A weights handle owns the packed weights, their scales
+ * and the channel plans; it is immutable after packing and may be shared by
+ * streams and threads.  An activation handle owns one packed activation
+ * buffer and its group scales; use it from one stream at a time. */
+typedef struct soniq_weights_s* soniq_weights;
+typedef struct soniq_act_s* soniq_act;
+
+/* Weight code grid (Sec. 3 codec, item 3).
+ *   SONIQ_WQ_SYMMETRIC: codes in [-(2^(b-1)-1), 2^(b-1)-1], step
+ *       max-abs/(2^(b-1)-1); 1-bit channels are sign x max-abs (codes +-1,
+ *       the XNOR/popcount semantics of Sec. 4.2).
+ *   SONIQ_WQ_TWOS_FRACTION: the two's-complement fraction grid of Eq. (1):
+ *       codes in [-2^(b-1), 2^(b-1)-1], step max-abs/2^(b-1). */
+enum { SONIQ_WQ_SYMMETRIC = 0, SONIQ_WQ_TWOS_FRACTION = 1 };
+
+/* Largest supported input-channel count (padded): keeps every int32
+ * accumulator exact. */
+#define SONIQ_MAX_K 65536
+
+/*
+ * soniq_pack_weights -- quantize, re-order and bit-pack one layer's weights.
+ * Passages: codec items 1 and 3 (scale and codes per output channel), Alg. 1
+ * channel permutation and Fig. "normalization" (grouping and padding),
+ * Sec. 2.4 C5 (packed layout).
+ *
+ *   W_dev      device, float32 [N, ldw]; row n holds output channel n over
+ *              the K input channels (the nn.Linear / im2col weight layout).
+ *   N, K       output and input channel counts, N >= 1, 1 <= K and the
+ *              padded K <= SONIQ_MAX_K.
+ *   ldw        row stride of W in elements, ldw >= K.
+ *   w_bits     host, uint8 [N]: width of each output channel, 1..8, at most
+ *              two distinct values.  Copied during the call.
+ *   a_bits     host, uint8 [K]: width of each input (activation) channel,
+ *              1..8, at most two distinct values.  Fixes the activation
+ *              precision groups used by every activation handle created
+ *              from these weights.  Copied during the call.
+ *   a_signed   1: activations use the signed symmetric grid; 0: the unsigned
+ *              codec of codec item 2 (e.g. post-ReLU inputs).
+ *   stream     W is read on this stream.  The call returns after the packed
+ *              weights are complete (it synchronizes this stream).
+ *   out        receives the new handle; release with soniq_weights_destroy.
+ *
+ * Widths 3, 5, 6 and 7 are stored in the next power-of-two container.
+ * Errors: INVALID_ARGUMENT (null pointer, N/K < 1, ldw < K, width outside
+ * 1..8, more than two widths), UNSUPPORTED (padded K > SONIQ_MAX_K),
+ * OUT_OF_MEMORY, HIP.
+ */
+soniq_status soniq_pack_weights(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                const uint8_t* w_bits, const uint8_t* a_bits,
+                                int a_signed, void* stream, soniq_weights* out);
+
+/* As soniq_pack_weights, with the weight grid chosen by wq_mode
+ * (SONIQ_WQ_SYMMETRIC or SONIQ_WQ_TWOS_FRACTION). */
+soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                   const uint8_t* w_bits, const uint8_t* a_bits,
+                                   int a_signed, int wq_mode, void* stream,
+                                   soniq_weights* out);
+
+/*
+ * soniq_act_create -- allocate a packed activation buffer for up to max_M
+ * rows, laid out for the input-channel plan of `w` (activation groups,
+ * permutation and padding are fixed at weight-packing time, Alg. 1).
+ * Errors: INVALID_ARGUMENT (null, max_M < 1), OUT_OF_MEMORY, HIP.
+ */
+soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out);
+
+/*
+ * soniq_quantize_act -- quantize, re-order and pack M activation rows.
+ * Passages: codec items 1 and 2 (group max-abs scale; unsigned codes) or the
+ * symmetric signed grid; Sec. 2.4 C2 (one scale per precision group, shared
+ * by all rows of the call); Alg. 1 channel permutation.
+ *
+ *   A_dev   device, float32 [M, lda]; row m is one input vector over K
+ *           channels in the original channel order.  Finite values only.
+ *   M       1 <= M <= max_M of the handle.
+ *   lda     row stride in elements, lda >= K.
+ * Enqueued on `stream`; the packed codes and the group scales s_a stay in
+ * the handle for the next soniq_mp_gemm on the same stream.
+ * Errors: INVALID_ARGUMENT, HIP.
+ */
+soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, int64_t lda,
+                                void* stream);
+
+/*
+ * soniq_mp_gemm -- Y = bf16(s_w * sum_g s_a[g] * ACC[g]) for the M rows last
+ * quantized into `act` (Alg. 1 Phase II integer MAC forward; C2: the scales
+ * are applied once per output, after the exact integer sums).
+ *
+ *   act      a handle created from `w`, after soniq_quantize_act.
+ *   Y_dev    device, bf16 bit patterns (uint16) [M, ldy], columns in the
+ *            original output-channel order; fully overwritten.
+ *   ldy      row stride in elements, ldy >= N.
+ *   acc_dev  optional device int32 [S][M][N] (S = number of activation
+ *            groups, soniq_weights_info): receives the exact accumulators
+ *            ACC[g][m][n] in original order.  NULL skips the dump.
+ * Enqueued on `stream`.  M <= 8 uses a bandwidth-bound kernel without matrix
+ * cores; larger M uses int8 MFMA tiles.
+ * Errors: INVALID_ARGUMENT (null, mismatched handles, nothing quantized),
+ * HIP.
+ */
+soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int64_t ldy,
+                           int32_t* acc_dev, void* stream);
+
+/* Description of a packed weights handle. */
+typedef struct {
+  int64_t N, K;               /* logical sizes */
+  int32_t S;                  /* activation precision groups (1 or 2) */
+  int32_t a_signed, wq_mode;
+  uint8_t a_bits[2];          /* width of each activation group, ascending */
+  uint8_t w_bits[2];          /* weight widths, ascending (w_bits[1]=0 if one) */
+  int64_t a_count[2];         /* input channels per activation group */
+  int64_t a_count_padded[2];  /* after padding each group to 64 channels */
+  int64_t w_count[2];         /* output channels per weight width */
+  int64_t packed_w_bytes;     /* bytes of the packed weight buffer */
+  int64_t packed_w_bytes_algorithmic; /* sum over rows of container*K/8 */
+} soniq_weights_info_t;
+
+/* Fill *out.  Errors: INVALID_ARGUMENT. */
+soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
+
+/*
+ * soniq_plan_input_channels -- the input-channel plan for a_bits, computed
+ * on the host (no device needed): pos[k] receives the position of input
+ * channel k in the packed, group-ordered and padded channel axis (group 0,
+ * the narrower width, first; original order within a group; each group
+ * padded to a multiple of 64).  seg_len[2] and seg_pad[2] receive the group
+ * sizes before and after padding (second entries 0 when S = 1).
+ * Returns INVALID_ARGUMENT for bad widths or pointers.
+ */
+soniq_status soniq_plan_input_channels(const uint8_t* a_bits, int64_t K, int64_t* pos,
+                                       int64_t seg_len[2], int64_t seg_pad[2], int32_t* S);
+
+/*
+ * Debug readback (synchronous: waits for the device).  Codes are returned as
+ * int32 in the original channel order; scales as float32.
+ *   soniq_weights_unpack_debug: codes [N, K], s_w [N].
+ *   soniq_act_unpack_debug:     codes [M, K] of the last soniq_quantize_act,
+ *                               s_a [S].
+ * Either output pointer may be NULL.  Errors: INVALID_ARGUMENT, HIP.
+ */
+soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* s_w);
+soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a);
+
+/* Release a handle (NULL is ignored).  Waits for the device first. */
+void soniq_weights_destroy(soniq_weights w);
+void soniq_act_destroy(soniq_act act);
+
+/* Message of the last non-OK status returned on the calling thread. */
+const char* soniq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SONIQ_H_ */

@@ -1,0 +1,254 @@
+"""Python binding of libsoniq (gfx950): SONIQ's per-channel mixed-precision
+quantized matrix multiply (arXiv 2311.14114, Sec. 3 codec and Alg. 1 Phase II
+integer MAC).
+
+The functions carry the C-ABI names of ``include/soniq.h`` and only marshal
+arguments: torch tensors provide device pointers and the current HIP stream;
+every step runs in the library's HIP kernels.  There is no CPU fallback: if
+``libsoniq.so`` is missing, importing the binding's entry points raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsoniq.so")
+
+SONIQ_OK = 0
+SONIQ_ERR_INVALID_ARGUMENT = 1
+SONIQ_ERR_UNSUPPORTED = 2
+SONIQ_ERR_OUT_OF_MEMORY = 3
+SONIQ_ERR_HIP = 4
+SONIQ_WQ_SYMMETRIC = 0
+SONIQ_WQ_TWOS_FRACTION = 1
+SONIQ_MAX_K = 65536
+
+# Every symbol include/soniq.h declares.
+EXPORTED = [
+    "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_act_create",
+    "soniq_quantize_act", "soniq_mp_gemm", "soniq_weights_info",
+    "soniq_plan_input_channels", "soniq_weights_unpack_debug",
+    "soniq_act_unpack_debug", "soniq_weights_destroy", "soniq_act_destroy",
+    "soniq_last_error",
+]
+
+
+class SoniqError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"soniq status {status}: {msg}")
+        self.status = status
+
+
+class WeightsInfo(ctypes.Structure):
+    _fields_ = [
+        ("N", ctypes.c_int64), ("K", ctypes.c_int64), ("S", ctypes.c_int32),
+        ("a_signed", ctypes.c_int32), ("wq_mode", ctypes.c_int32),
+        ("a_bits", ctypes.c_uint8 * 2), ("w_bits", ctypes.c_uint8 * 2),
+        ("a_count", ctypes.c_int64 * 2), ("a_count_padded", ctypes.c_int64 * 2),
+        ("w_count", ctypes.c_int64 * 2), ("packed_w_bytes", ctypes.c_int64),
+        ("packed_w_bytes_algorithmic", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsoniq.so (fails loudly when it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                              "or python -m paper_2311_14114_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32, st = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int
+        L.soniq_pack_weights.restype = st
+        L.soniq_pack_weights.argtypes = [vp, i64, i64, i64, vp, vp, i32, vp, ctypes.POINTER(vp)]
+        L.soniq_pack_weights_ex.restype = st
+        L.soniq_pack_weights_ex.argtypes = [vp, i64, i64, i64, vp, vp, i32, i32, vp, ctypes.POINTER(vp)]
+        L.soniq_act_create.restype = st
+        L.soniq_act_create.argtypes = [vp, i64, ctypes.POINTER(vp)]
+        L.soniq_quantize_act.restype = st
+        L.soniq_quantize_act.argtypes = [vp, vp, i64, i64, vp]
+        L.soniq_mp_gemm.restype = st
+        L.soniq_mp_gemm.argtypes = [vp, vp, vp, i64, vp, vp]
+        L.soniq_weights_info.restype = st
+        L.soniq_weights_info.argtypes = [vp, ctypes.POINTER(WeightsInfo)]
+        L.soniq_plan_input_channels.restype = st
+        L.soniq_plan_input_channels.argtypes = [vp, i64, vp, vp, vp, vp]
+        L.soniq_weights_unpack_debug.restype = st
+        L.soniq_weights_unpack_debug.argtypes = [vp, vp, vp]
+        L.soniq_act_unpack_debug.restype = st
+        L.soniq_act_unpack_debug.argtypes = [vp, vp, vp]
+        L.soniq_weights_destroy.restype = None
+        L.soniq_weights_destroy.argtypes = [vp]
+        L.soniq_act_destroy.restype = None
+        L.soniq_act_destroy.argtypes = [vp]
+        L.soniq_last_error.restype = ctypes.c_char_p
+        L.soniq_last_error.argtypes = []
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != SONIQ_OK:
+        raise SoniqError(status, lib().soniq_last_error().decode())
+
+
+def _u8(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a), dtype=np.uint8)
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(int(stream))
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, dtype_name: str):
+    import torch
+    if not (isinstance(t, torch.Tensor) and t.is_cuda):
+        raise TypeError(f"expected a device tensor ({dtype_name})")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Weights:
+    """Owner of a packed weights handle (soniq_weights)."""
+
+    def __init__(self, handle: ctypes.c_void_p, N: int, K: int):
+        self.handle = handle
+        self.N, self.K = N, K
+        self.info = soniq_weights_info(self)
+        self.S = self.info.S
+
+    def close(self):
+        if self.handle:
+            lib().soniq_weights_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Activations:
+    """Owner of a packed activation handle (soniq_act)."""
+
+    def __init__(self, handle: ctypes.c_void_p, weights: Weights, max_M: int):
+        self.handle = handle
+        self.weights = weights      # keeps the weights alive
+        self.max_M = max_M
+        self.M = 0
+
+    def close(self):
+        if self.handle:
+            lib().soniq_act_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_WQ_SYMMETRIC,
+                       stream=None) -> Weights:
+    """Quantize, re-order and bit-pack W (device float32 [N, K], row-major)."""
+    import torch
+    if W.dtype != torch.float32 or W.dim() != 2 or W.stride(1) != 1:
+        raise TypeError("W must be a 2-D float32 device tensor with unit column stride")
+    N, K = W.shape
+    wb, ab = _u8(w_bits), _u8(a_bits)
+    if wb.shape != (N,) or ab.shape != (K,):
+        raise ValueError("w_bits must have N entries and a_bits K entries")
+    h = ctypes.c_void_p()
+    _check(lib().soniq_pack_weights_ex(_dev(W, "float32"), N, K, W.stride(0),
+                                       wb.ctypes.data_as(ctypes.c_void_p),
+                                       ab.ctypes.data_as(ctypes.c_void_p),
+                                       1 if a_signed else 0, int(wq_mode), _stream(stream),
+                                       ctypes.byref(h)))
+    return Weights(h, N, K)
+
+
+def soniq_act_create(weights: Weights, max_M: int) -> Activations:
+    h = ctypes.c_void_p()
+    _check(lib().soniq_act_create(weights.handle, int(max_M), ctypes.byref(h)))
+    return Activations(h, weights, int(max_M))
+
+
+def soniq_quantize_act(act: Activations, A, stream=None) -> None:
+    """Quantize and pack A (device float32 [M, K], row-major) into `act`."""
+    import torch
+    if A.dtype != torch.float32 or A.dim() != 2 or A.stride(1) != 1:
+        raise TypeError("A must be a 2-D float32 device tensor with unit column stride")
+    if A.shape[1] != act.weights.K:
+        raise ValueError("A has the wrong number of input channels")
+    _check(lib().soniq_quantize_act(act.handle, _dev(A, "float32"), A.shape[0], A.stride(0),
+                                    _stream(stream)))
+    act.M = A.shape[0]
+
+
+def soniq_mp_gemm(act: Activations, weights: Weights, out=None, acc=None, stream=None):
+    """Y[M, N] (bf16) from the last quantized activations; optional int32
+    accumulator dump acc[S, M, N].  Returns Y."""
+    import torch
+    M, N = act.M, weights.N
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or out.shape[0] < M:
+        raise TypeError("out must be a bf16 [M, >=N] device tensor with unit column stride")
+    accp = None
+    if acc is not None:
+        if acc.dtype != torch.int32 or not acc.is_contiguous() or tuple(acc.shape) != (weights.S, M, N):
+            raise TypeError("acc must be a contiguous int32 [S, M, N] device tensor")
+        accp = _dev(acc, "int32")
+    _check(lib().soniq_mp_gemm(act.handle, weights.handle, _dev(out, "bf16"), out.stride(0),
+                               accp, _stream(stream)))
+    return out
+
+
+def soniq_weights_info(weights: Weights) -> WeightsInfo:
+    info = WeightsInfo()
+    _check(lib().soniq_weights_info(weights.handle, ctypes.byref(info)))
+    return info
+
+
+def soniq_plan_input_channels(a_bits):
+    """Host-only input-channel plan: (pos[K], seg_len[2], seg_pad[2], S)."""
+    ab = _u8(a_bits)
+    K = ab.shape[0]
+    pos = np.empty(K, np.int64)
+    seg_len = np.zeros(2, np.int64)
+    seg_pad = np.zeros(2, np.int64)
+    S = ctypes.c_int32()
+    _check(lib().soniq_plan_input_channels(ab.ctypes.data_as(ctypes.c_void_p), K,
+                                           pos.ctypes.data_as(ctypes.c_void_p),
+                                           seg_len.ctypes.data_as(ctypes.c_void_p),
+                                           seg_pad.ctypes.data_as(ctypes.c_void_p),
+                                           ctypes.byref(S)))
+    return pos, seg_len, seg_pad, S.value
+
+
+def soniq_weights_unpack_debug(weights: Weights):
+    """Codes int32 [N, K] (original order) and scales float32 [N]."""
+    codes = np.empty((weights.N, weights.K), np.int32)
+    s_w = np.empty(weights.N, np.float32)
+    _check(lib().soniq_weights_unpack_debug(weights.handle, codes.ctypes.data_as(ctypes.c_void_p),
+                                            s_w.ctypes.data_as(ctypes.c_void_p)))
+    return codes, s_w
+
+
+def soniq_act_unpack_debug(act: Activations):
+    """Codes int32 [M, K] (original order) and group scales float32 [S]."""
+    codes = np.empty((act.M, act.weights.K), np.int32)
+    s_a = np.zeros(2, np.float32)
+    _check(lib().soniq_act_unpack_debug(act.handle, codes.ctypes.data_as(ctypes.c_void_p),
+                                        s_a.ctypes.data_as(ctypes.c_void_p)))
+    return codes, s_a[: act.weights.S].copy()

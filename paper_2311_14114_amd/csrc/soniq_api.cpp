@@ -1,0 +1,597 @@
+// Host side of libsoniq: argument validation, the input-channel and
+// output-channel plans, device buffers, dispatch and debug readback.
+//
+// Input-channel plan (Alg. 1 channel permutation; Fig. "normalization"):
+// the activation widths define at most two groups (C3), ordered narrow then
+// wide; within a group channels keep their original order; each group is
+// padded with zero channels to a multiple of 64 so every group starts on a
+// fresh 64-element unit of every packed row.
+//
+// Output-channel plan: channels are cut into tiles of 64 consecutive
+// original channels; inside a tile the narrow-width channels are stored
+// first (stable), so each tile holds two runs of uniform container width
+// (C1 at tile granularity) while every tile still covers a contiguous range
+// of output columns, which keeps the output stores local.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "soniq.h"
+#include "soniq_internal.h"
+
+using namespace soniq;
+
+namespace {
+
+thread_local std::string g_err;
+
+soniq_status fail(soniq_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+soniq_status fail_hip(hipError_t e, const char* what) {
+  return fail(e == hipErrorOutOfMemory ? SONIQ_ERR_OUT_OF_MEMORY : SONIQ_ERR_HIP,
+              "%s failed: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr)                                   \
+  do {                                                  \
+    hipError_t e_ = (expr);                             \
+    if (e_ != hipSuccess) return fail_hip(e_, #expr);   \
+  } while (0)
+
+constexpr uint32_t kMagicW = 0x57514E53u;  // live weights handle
+constexpr uint32_t kMagicA = 0x41514E53u;  // live activation handle
+constexpr uint32_t kDead = 0xDEADBEEFu;
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+int pow2_container(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
+
+// Weight container: 1-bit symmetric channels are sign bits; the Eq. (1)
+// 1-bit grid {-1, 0} is two's complement and needs two bits.
+int w_container(int b, int wq_mode) {
+  if (b == 1) return wq_mode == SONIQ_WQ_TWOS_FRACTION ? 2 : 1;
+  return pow2_container(b);
+}
+
+// Activation container: unsigned 1-bit codes {0, 1} go in a 2-bit field.
+int a_container(int b, int is_signed) {
+  if (b == 1) return is_signed ? 1 : 2;
+  return pow2_container(b);
+}
+
+int unpack_shift(int c) { return c == 8 ? 0 : c == 4 ? 4 : 6; }
+
+QParam w_qparam(int b, int wq_mode) {
+  QParam q{};
+  if (wq_mode == SONIQ_WQ_TWOS_FRACTION) {
+    q.qdiv = (float)(1 << (b - 1));
+    q.lo = -(1 << (b - 1));
+    q.hi = (1 << (b - 1)) - 1;
+  } else if (b == 1) {
+    q.sign1 = 1;
+    q.qdiv = 1.0f;
+    q.lo = -1;
+    q.hi = 1;
+  } else {
+    const int Q = (1 << (b - 1)) - 1;
+    q.qdiv = (float)Q;
+    q.lo = -Q;
+    q.hi = Q;
+  }
+  return q;
+}
+
+QParam a_qparam(int b, int is_signed) {
+  if (is_signed) return w_qparam(b, SONIQ_WQ_SYMMETRIC);
+  QParam q{};
+  q.qdiv = (float)((1 << b) - 1);
+  q.lo = 0;
+  q.hi = (1 << b) - 1;
+  return q;
+}
+
+// Unsigned codes that fill their container are stored shifted by 2^(c-1).
+int a_zero_point(int b, int is_signed, int c) {
+  return (!is_signed && b == c) ? (1 << (c - 1)) : 0;
+}
+
+struct KPlan {
+  int S = 0;
+  int bits[2] = {0, 0};
+  int64_t len[2] = {0, 0}, pad[2] = {0, 0};
+  int64_t Kp = 0;
+  std::vector<int32_t> pos;
+  std::vector<uint8_t> seg;
+};
+
+// Distinct widths (ascending) of a bit vector; false if a width is outside
+// 1..8 or there are more than two.
+bool distinct_widths(const uint8_t* bits, int64_t n, int out[2], int* count) {
+  bool seen[9] = {false};
+  for (int64_t i = 0; i < n; ++i) {
+    if (bits[i] < 1 || bits[i] > 8) return false;
+    seen[bits[i]] = true;
+  }
+  int c = 0;
+  out[0] = out[1] = 0;
+  for (int b = 1; b <= 8; ++b)
+    if (seen[b]) {
+      if (c == 2) return false;
+      out[c++] = b;
+    }
+  *count = c;
+  return true;
+}
+
+bool plan_k(const uint8_t* a_bits, int64_t K, KPlan& kp) {
+  if (!distinct_widths(a_bits, K, kp.bits, &kp.S)) return false;
+  kp.pos.resize(K);
+  kp.seg.resize(K);
+  kp.len[0] = kp.len[1] = 0;
+  for (int64_t k = 0; k < K; ++k) kp.len[a_bits[k] == kp.bits[0] ? 0 : 1]++;
+  kp.pad[0] = round_up(kp.len[0], kGran);
+  kp.pad[1] = round_up(kp.len[1], kGran);
+  kp.Kp = kp.pad[0] + kp.pad[1];
+  int64_t r0 = 0, r1 = 0;
+  for (int64_t k = 0; k < K; ++k) {
+    if (a_bits[k] == kp.bits[0]) {
+      kp.seg[k] = 0;
+      kp.pos[k] = (int32_t)r0++;
+    } else {
+      kp.seg[k] = 1;
+      kp.pos[k] = (int32_t)(kp.pad[0] + r1++);
+    }
+  }
+  return true;
+}
+
+template <class T>
+hipError_t dev_alloc(T** p, size_t count) {
+  *p = nullptr;
+  if (count == 0) count = 1;
+  return hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T));
+}
+
+}  // namespace
+
+struct soniq_weights_s {
+  uint32_t magic = 0;
+  int refs = 1;          // 1 for the owner + 1 per live activation handle
+  bool released = false;  // soniq_weights_destroy was called
+  int64_t N = 0, K = 0;
+  int a_signed = 1, wq_mode = SONIQ_WQ_SYMMETRIC;
+  KPlan kp;
+  int nw = 0;
+  int wb[2] = {0, 0};
+  int64_t w_cnt[2] = {0, 0};
+  WPlan wp{};
+  std::vector<TileDesc> tiles_h;
+  std::vector<int32_t> phys_h;
+  std::vector<int64_t> row_off_h;
+  int64_t packed_bytes = 0;
+  uint8_t* packed = nullptr;
+  TileDesc* tiles = nullptr;
+  ColInfo* colinfo = nullptr;
+  uint8_t* shw = nullptr;
+  int32_t* pos = nullptr;
+  uint8_t* seg = nullptr;
+};
+
+struct soniq_act_s {
+  uint32_t magic = 0;
+  soniq_weights w = nullptr;
+  int64_t max_M = 0, M_alloc = 0, M = 0;
+  ActPlan ap{};
+  int64_t packed_bytes = 0;
+  uint8_t* packed = nullptr;
+  float* partial = nullptr;
+  unsigned int* counter = nullptr;
+  float* s_a = nullptr;
+};
+
+namespace {
+
+void free_weights(soniq_weights w) {
+  (void)hipDeviceSynchronize();
+  (void)hipFree(w->packed);
+  (void)hipFree(w->tiles);
+  (void)hipFree(w->colinfo);
+  (void)hipFree(w->shw);
+  (void)hipFree(w->pos);
+  (void)hipFree(w->seg);
+  w->magic = kDead;
+  delete w;
+}
+
+void release_weights(soniq_weights w) {
+  if (--w->refs == 0) free_weights(w);
+}
+
+bool live_w(soniq_weights w) { return w && w->magic == kMagicW && !w->released; }
+bool live_a(soniq_act a) { return a && a->magic == kMagicA; }
+
+ActPlan make_act_plan(const soniq_weights_s& w, int64_t M_alloc) {
+  ActPlan ap{};
+  ap.S = w.kp.S;
+  int64_t off = 0;
+  for (int g = 0; g < 2; ++g) {
+    if (g < ap.S) {
+      const int b = w.kp.bits[g];
+      ap.c[g] = a_container(b, w.a_signed);
+      ap.sh[g] = unpack_shift(ap.c[g]);
+      ap.zp[g] = a_zero_point(b, w.a_signed, ap.c[g]);
+      ap.kpad[g] = (int)w.kp.pad[g];
+      ap.row_bytes[g] = round_up(w.kp.pad[g] * ap.c[g] / 8, 16);
+      ap.seg_off[g] = off;
+      off = round_up(off + M_alloc * ap.row_bytes[g], 256);
+      ap.q[g] = a_qparam(b, w.a_signed);
+      ap.padcnt[g] = (int)(w.kp.pad[g] - w.kp.len[g]);
+    } else {
+      ap.c[g] = 8;
+      ap.q[g] = a_qparam(8, 1);
+    }
+  }
+  ap.Kp = (int)w.kp.Kp;
+  return ap;
+}
+
+int64_t act_bytes(const ActPlan& ap, int64_t M_alloc) {
+  int64_t off = 0;
+  for (int g = 0; g < ap.S; ++g) off = round_up(off + M_alloc * ap.row_bytes[g], 256);
+  return off;
+}
+
+// Field f (container c) of element e of a packed row.
+uint32_t field_of(const uint8_t* row, int64_t e, int c) {
+  const int per = 32 / c;
+  uint32_t word;
+  memcpy(&word, row + (e / per) * 4, 4);
+  const int ee = (int)(e % per);
+  const int j = ee / 4, b = ee % 4;
+  return (word >> (8 * b + c * j)) & ((1u << c) - 1u);
+}
+
+int decode_signed(uint32_t f, int c) {
+  if (c == 1) return f ? -1 : 1;
+  return (f >> (c - 1)) ? (int)f - (1 << c) : (int)f;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* soniq_last_error(void) { return g_err.c_str(); }
+
+soniq_status soniq_plan_input_channels(const uint8_t* a_bits, int64_t K, int64_t* pos,
+                                       int64_t seg_len[2], int64_t seg_pad[2], int32_t* S) {
+  if (!a_bits || !pos || !seg_len || !seg_pad || !S)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_plan_input_channels: null pointer");
+  if (K < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_plan_input_channels: K < 1");
+  KPlan kp;
+  if (!plan_k(a_bits, K, kp))
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_plan_input_channels: widths must be 1..8 with at most two values");
+  for (int64_t k = 0; k < K; ++k) pos[k] = kp.pos[k];
+  for (int g = 0; g < 2; ++g) {
+    seg_len[g] = kp.len[g];
+    seg_pad[g] = kp.pad[g];
+  }
+  *S = kp.S;
+  return SONIQ_OK;
+}
+
+soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                   const uint8_t* w_bits, const uint8_t* a_bits,
+                                   int a_signed, int wq_mode, void* stream,
+                                   soniq_weights* out) {
+  if (!W_dev || !w_bits || !a_bits || !out)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: null pointer");
+  if (N < 1 || K < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: N, K must be >= 1");
+  if (ldw < K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: ldw < K");
+  if (a_signed != 0 && a_signed != 1)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: a_signed must be 0 or 1");
+  if (wq_mode != SONIQ_WQ_SYMMETRIC && wq_mode != SONIQ_WQ_TWOS_FRACTION)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: unknown wq_mode %d", wq_mode);
+  int wb[2], nw = 0;
+  if (!distinct_widths(w_bits, N, wb, &nw))
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_pack_weights: w_bits must be 1..8 with at most two distinct values");
+  KPlan kp;
+  if (!plan_k(a_bits, K, kp))
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_pack_weights: a_bits must be 1..8 with at most two distinct values");
+  if (kp.Kp > SONIQ_MAX_K)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_pack_weights: padded K %lld exceeds %d",
+                (long long)kp.Kp, SONIQ_MAX_K);
+  if (N > (int64_t)1 << 24)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_pack_weights: N %lld exceeds 2^24", (long long)N);
+
+  soniq_weights w = new (std::nothrow) soniq_weights_s();
+  if (!w) return fail(SONIQ_ERR_OUT_OF_MEMORY, "soniq_pack_weights: host allocation");
+  w->N = N;
+  w->K = K;
+  w->a_signed = a_signed;
+  w->wq_mode = wq_mode;
+  w->kp = std::move(kp);
+  w->nw = nw;
+  w->wb[0] = wb[0];
+  w->wb[1] = nw == 2 ? wb[1] : 0;
+
+  // Output-channel plan.
+  const int b_lo = wb[0], b_hi = nw == 2 ? wb[1] : wb[0];
+  WPlan& wp = w->wp;
+  wp.c_lo = w_container(b_lo, wq_mode);
+  wp.c_hi = w_container(b_hi, wq_mode);
+  wp.sh_lo = unpack_shift(wp.c_lo);
+  wp.sh_hi = unpack_shift(wp.c_hi);
+  wp.rb_lo = round_up(w->kp.Kp * wp.c_lo / 8, 16);
+  wp.rb_hi = round_up(w->kp.Kp * wp.c_hi / 8, 16);
+  wp.ntiles = (int)((N + kNTile - 1) / kNTile);
+  wp.ntiles += wp.ntiles & 1;  // even, so 128-column GEMM tiles stay in range
+  wp.Np = wp.ntiles * kNTile;
+  w->tiles_h.assign(wp.ntiles, TileDesc{0, 0, 0});
+  w->phys_h.assign(N, 0);
+  w->row_off_h.assign(N, 0);
+  std::vector<ColInfo> colinfo_h(wp.Np, ColInfo{-1, 0.0f, {0, 0}});
+  std::vector<uint8_t> shw_h(wp.Np, 0);
+  uint64_t base = 0;
+  for (int t = 0; t < wp.ntiles; ++t) {
+    const int64_t n0 = (int64_t)t * kNTile;
+    const int64_t n1 = std::min<int64_t>(n0 + kNTile, N);
+    TileDesc td{base, 0, 0};
+    if (n0 < N) {
+      int rank = 0;
+      for (int64_t n = n0; n < n1; ++n)
+        if (w_bits[n] == b_lo) {
+          w->phys_h[n] = (int32_t)(n0 + rank);
+          w->row_off_h[n] = (int64_t)base + (int64_t)rank * wp.rb_lo;
+          ++rank;
+        }
+      td.n_lo = rank;
+      for (int64_t n = n0; n < n1; ++n)
+        if (w_bits[n] != b_lo) {
+          w->phys_h[n] = (int32_t)(n0 + rank);
+          w->row_off_h[n] = (int64_t)base + (int64_t)td.n_lo * wp.rb_lo +
+                            (int64_t)(rank - td.n_lo) * wp.rb_hi;
+          ++rank;
+        }
+      td.n_rows = rank;
+      for (int64_t n = n0; n < n1; ++n) {
+        colinfo_h[w->phys_h[n]].n = (int32_t)n;
+        const int c = w_bits[n] == b_lo ? wp.c_lo : wp.c_hi;
+        shw_h[w->phys_h[n]] = (uint8_t)(unpack_shift(c) | (c == 1 ? kShwSign : 0));
+      }
+    }
+    w->tiles_h[t] = td;
+    base = (uint64_t)round_up((int64_t)base + (int64_t)td.n_lo * wp.rb_lo +
+                                  (int64_t)(td.n_rows - td.n_lo) * wp.rb_hi,
+                              256);
+  }
+  w->packed_bytes = (int64_t)base;
+  for (int64_t n = 0; n < N; ++n) w->w_cnt[w_bits[n] == b_lo ? 0 : 1]++;
+
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  soniq_status rc = SONIQ_OK;
+  uint8_t* wbits_dev = nullptr;
+  int64_t* row_off_dev = nullptr;
+  int32_t* phys_dev = nullptr;
+  hipError_t e = hipSuccess;
+#define STEP(expr)                              \
+  if (e == hipSuccess) {                        \
+    e = (expr);                                 \
+    if (e != hipSuccess) rc = fail_hip(e, #expr); \
+  }
+  STEP(dev_alloc(&w->packed, (size_t)w->packed_bytes));
+  STEP(dev_alloc(&w->tiles, (size_t)wp.ntiles));
+  STEP(dev_alloc(&w->colinfo, (size_t)wp.Np));
+  STEP(dev_alloc(&w->shw, (size_t)wp.Np));
+  STEP(dev_alloc(&w->pos, (size_t)K));
+  STEP(dev_alloc(&w->seg, (size_t)K));
+  STEP(dev_alloc(&wbits_dev, (size_t)N));
+  STEP(dev_alloc(&row_off_dev, (size_t)N));
+  STEP(dev_alloc(&phys_dev, (size_t)N));
+  STEP(hipMemsetAsync(w->packed, 0, (size_t)w->packed_bytes, st));
+  STEP(hipMemcpyAsync(w->tiles, w->tiles_h.data(), wp.ntiles * sizeof(TileDesc), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->colinfo, colinfo_h.data(), wp.Np * sizeof(ColInfo), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->shw, shw_h.data(), wp.Np, hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->pos, w->kp.pos.data(), K * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->seg, w->kp.seg.data(), K, hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(wbits_dev, w_bits, N, hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(row_off_dev, w->row_off_h.data(), N * sizeof(int64_t), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(phys_dev, w->phys_h.data(), N * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  STEP(launch_wpack(W_dev, N, K, ldw, wbits_dev, w->pos, w->seg, row_off_dev, phys_dev,
+                    w_qparam(b_lo, wq_mode), w_qparam(b_hi, wq_mode), b_lo, wp.c_lo, wp.c_hi,
+                    (int)w->kp.Kp, (int)w->kp.pad[0], wp.rb_lo, wp.rb_hi, w->packed,
+                    w->colinfo, st));
+  STEP(hipStreamSynchronize(st));
+#undef STEP
+  (void)hipFree(wbits_dev);
+  (void)hipFree(row_off_dev);
+  (void)hipFree(phys_dev);
+  if (rc != SONIQ_OK) {
+    free_weights(w);
+    return rc;
+  }
+  w->magic = kMagicW;
+  *out = w;
+  return SONIQ_OK;
+}
+
+soniq_status soniq_pack_weights(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                const uint8_t* w_bits, const uint8_t* a_bits, int a_signed,
+                                void* stream, soniq_weights* out) {
+  return soniq_pack_weights_ex(W_dev, N, K, ldw, w_bits, a_bits, a_signed,
+                               SONIQ_WQ_SYMMETRIC, stream, out);
+}
+
+soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out) {
+  if (!live_w(w) || !out) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_weights_info: bad handle or null");
+  memset(out, 0, sizeof *out);
+  out->N = w->N;
+  out->K = w->K;
+  out->S = w->kp.S;
+  out->a_signed = w->a_signed;
+  out->wq_mode = w->wq_mode;
+  for (int g = 0; g < 2; ++g) {
+    out->a_bits[g] = (uint8_t)w->kp.bits[g];
+    out->a_count[g] = w->kp.len[g];
+    out->a_count_padded[g] = w->kp.pad[g];
+    out->w_bits[g] = (uint8_t)w->wb[g];
+    out->w_count[g] = w->w_cnt[g];
+  }
+  out->packed_w_bytes = w->packed_bytes;
+  out->packed_w_bytes_algorithmic =
+      (w->w_cnt[0] * w->wp.c_lo + w->w_cnt[1] * w->wp.c_hi) * w->K / 8;
+  return SONIQ_OK;
+}
+
+soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
+  if (!live_w(w) || !out) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create: bad handle or null");
+  if (max_M < 1 || max_M > ((int64_t)1 << 31) - 128)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create: max_M out of range");
+  soniq_act a = new (std::nothrow) soniq_act_s();
+  if (!a) return fail(SONIQ_ERR_OUT_OF_MEMORY, "soniq_act_create: host allocation");
+  a->w = w;
+  a->max_M = max_M;
+  a->M_alloc = round_up(max_M, kGemmBM);
+  a->ap = make_act_plan(*w, a->M_alloc);
+  a->packed_bytes = act_bytes(a->ap, a->M_alloc);
+  hipError_t e = dev_alloc(&a->packed, (size_t)a->packed_bytes);
+  if (e == hipSuccess) e = dev_alloc(&a->partial, 2 * kAbsmaxBlocks);
+  if (e == hipSuccess) e = dev_alloc(&a->counter, 1);
+  if (e == hipSuccess) e = dev_alloc(&a->s_a, 2);
+  if (e == hipSuccess) e = hipMemset(a->counter, 0, sizeof(unsigned int));
+  if (e == hipSuccess) e = hipMemset(a->s_a, 0, 2 * sizeof(float));
+  if (e == hipSuccess) e = hipMemset(a->packed, 0, (size_t)a->packed_bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    soniq_status rc = fail_hip(e, "soniq_act_create");
+    (void)hipFree(a->packed);
+    (void)hipFree(a->partial);
+    (void)hipFree(a->counter);
+    (void)hipFree(a->s_a);
+    delete a;
+    return rc;
+  }
+  w->refs++;
+  a->magic = kMagicA;
+  *out = a;
+  return SONIQ_OK;
+}
+
+soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, int64_t lda,
+                                void* stream) {
+  if (!live_a(act) || !A_dev) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: bad handle or null");
+  const soniq_weights w = act->w;
+  if (M < 1 || M > act->max_M)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: M=%lld outside [1, %lld]",
+                (long long)M, (long long)act->max_M);
+  if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: lda < K");
+  HIP_TRY(launch_act_quant(A_dev, M, w->K, lda, act->ap, w->pos, w->seg, act->partial,
+                           act->counter, act->s_a, act->packed,
+                           reinterpret_cast<hipStream_t>(stream)));
+  act->M = M;
+  return SONIQ_OK;
+}
+
+soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int64_t ldy,
+                           int32_t* acc_dev, void* stream) {
+  if (!live_a(act) || !live_w(w) || !Y_dev)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: bad handle or null");
+  if (act->w != w)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: activation handle belongs to other weights");
+  if (act->M < 1)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: no activations quantized yet");
+  if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: ldy < N");
+  const int64_t M = act->M;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (gemv_fits(M, act->ap.Kp)) {
+    HIP_TRY(launch_mp_gemv(act->packed, act->s_a, act->ap, w->packed, w->tiles, w->colinfo,
+                           w->shw, w->wp, M, w->N, Y_dev, ldy, acc_dev, st));
+  } else {
+    if ((M + kGemmBM - 1) / kGemmBM > 65535)
+      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: M too large for one launch");
+    HIP_TRY(launch_mp_gemm(act->packed, act->s_a, act->ap, w->packed, w->tiles, w->colinfo,
+                           w->shw, w->wp, M, w->N, Y_dev, ldy, acc_dev, st));
+  }
+  return SONIQ_OK;
+}
+
+soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* s_w) {
+  if (!live_w(w)) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_weights_unpack_debug: bad handle");
+  HIP_TRY(hipDeviceSynchronize());
+  std::vector<uint8_t> packed(w->packed_bytes);
+  std::vector<ColInfo> ci(w->wp.Np);
+  HIP_TRY(hipMemcpy(packed.data(), w->packed, w->packed_bytes, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(ci.data(), w->colinfo, ci.size() * sizeof(ColInfo), hipMemcpyDeviceToHost));
+  const int b_lo = w->wb[0];
+  (void)b_lo;
+  for (int64_t n = 0; n < w->N; ++n) {
+    const int32_t p = w->phys_h[n];
+    const int t = p / kNTile, j = p % kNTile;
+    const bool lo = j < w->tiles_h[t].n_lo;
+    const int c = lo ? w->wp.c_lo : w->wp.c_hi;
+    const uint8_t* row = packed.data() + w->row_off_h[n];
+    if (codes)
+      for (int64_t k = 0; k < w->K; ++k)
+        codes[n * w->K + k] = decode_signed(field_of(row, w->kp.pos[k], c), c);
+    if (s_w) s_w[n] = ci[p].s_w;
+  }
+  return SONIQ_OK;
+}
+
+soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a) {
+  if (!live_a(act)) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_unpack_debug: bad handle");
+  if (act->M < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_unpack_debug: nothing quantized");
+  HIP_TRY(hipDeviceSynchronize());
+  const ActPlan& ap = act->ap;
+  const soniq_weights w = act->w;
+  std::vector<uint8_t> packed(act->packed_bytes);
+  float sa[2] = {0, 0};
+  HIP_TRY(hipMemcpy(packed.data(), act->packed, act->packed_bytes, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(sa, act->s_a, sizeof sa, hipMemcpyDeviceToHost));
+  if (codes)
+    for (int64_t m = 0; m < act->M; ++m)
+      for (int64_t k = 0; k < w->K; ++k) {
+        const int g = w->kp.seg[k];
+        const int64_t e = w->kp.pos[k] - (g ? ap.kpad[0] : 0);
+        const uint8_t* row = packed.data() + ap.seg_off[g] + m * ap.row_bytes[g];
+        codes[m * w->K + k] = decode_signed(field_of(row, e, ap.c[g]), ap.c[g]) + ap.zp[g];
+      }
+  if (s_a)
+    for (int g = 0; g < ap.S; ++g) s_a[g] = sa[g];
+  return SONIQ_OK;
+}
+
+void soniq_weights_destroy(soniq_weights w) {
+  if (!live_w(w)) return;
+  w->released = true;
+  release_weights(w);
+}
+
+void soniq_act_destroy(soniq_act act) {
+  if (!live_a(act)) return;
+  (void)hipDeviceSynchronize();
+  (void)hipFree(act->packed);
+  (void)hipFree(act->partial);
+  (void)hipFree(act->counter);
+  (void)hipFree(act->s_a);
+  act->magic = kDead;
+  soniq_weights w = act->w;
+  delete act;
+  release_weights(w);
+}
+
+}  // extern "C"

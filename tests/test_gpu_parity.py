@@ -1,0 +1,226 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle.
+
+Bar: weight and activation codes, scales and every int32 accumulator are
+bit-exact; bf16 outputs equal the oracle's fixed-order fp32 replay bit for
+bit and lie within the tolerance of the fp64 reference (relative 1e-2, or
+2^-15 of the magnitude sum where cancellation makes the output tiny).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2311_14114_amd as sq
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16_bits(t):
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def gpu_run(case, wq_mode=0, ldw_pad=0, lda_pad=0, ldy_pad=0, with_acc=True, debug=True):
+    M, N, K = case["M"], case["N"], case["K"]
+    print(f"[gpu] {case['name']} M={M} N={N} K={K} wq_mode={wq_mode}", flush=True)
+    Wb = torch.zeros((N, K + ldw_pad), dtype=torch.float32, device="cuda")
+    Wb[:, :K] = torch.from_numpy(case["W"]).cuda()
+    Ab = torch.zeros((M, K + lda_pad), dtype=torch.float32, device="cuda")
+    Ab[:, :K] = torch.from_numpy(case["A"]).cuda()
+    W, A = Wb[:, :K], Ab[:, :K]
+    w = sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"], wq_mode)
+    act = sq.soniq_act_create(w, M)
+    sq.soniq_quantize_act(act, A)
+    Yb = torch.empty((M, N + ldy_pad), dtype=torch.bfloat16, device="cuda")
+    acc = torch.empty((w.S, M, N), dtype=torch.int32, device="cuda") if with_acc else None
+    sq.soniq_mp_gemm(act, w, out=Yb[:, :N], acc=acc)
+    torch.cuda.synchronize()
+    out = dict(S=w.S, y=_bf16_bits(Yb[:, :N]), w=w, act=act)
+    if with_acc:
+        out["acc"] = acc.cpu().numpy()
+    if debug:
+        out["q_w"], out["s_w"] = sq.soniq_weights_unpack_debug(w)
+        out["q_a"], out["s_a"] = sq.soniq_act_unpack_debug(act)
+    return out
+
+
+def oracle_run(case, wq_mode=0):
+    mode = oracle.TWOS_FRACTION if wq_mode == 1 else oracle.SIGNED
+    return oracle.run(case["A"], case["W"], case["a_bits"], case["w_bits"], case["a_signed"], mode)
+
+
+def check_y(y, y_ref, acc, s_a, s_w):
+    yg = oracle.bf16_to_f32(y).astype(np.float64)
+    yr = oracle.bf16_to_f32(y_ref).astype(np.float64)
+    T = np.abs(s_w.astype(np.float64))[None, :] * sum(
+        np.abs(float(s_a[g]) * acc[g].astype(np.float64)) for g in range(acc.shape[0]))
+    tol = np.maximum(1e-2 * np.abs(yr), 2.0 ** -15 * T)
+    bad = np.abs(yg - yr) > tol
+    assert not bad.any(), f"{bad.sum()} outputs outside tolerance"
+
+
+def compare_full(g, r):
+    assert g["S"] == r["S"]
+    np.testing.assert_array_equal(g["s_w"], r["s_w"])
+    np.testing.assert_array_equal(g["q_w"], r["q_w"])
+    np.testing.assert_array_equal(g["s_a"], r["s_a"])
+    np.testing.assert_array_equal(g["q_a"], r["q_a"])
+    np.testing.assert_array_equal(g["acc"], r["acc"])
+    np.testing.assert_array_equal(g["y"], r["y_replay"])
+    check_y(g["y"], r["y_ref"], r["acc"], r["s_a"], r["s_w"])
+
+
+FULL = ["tiny_linear", "conv3x3_im2col", "xfmr_qkv", "xfmr_ffn_up", "xfmr_ffn_down",
+        "decode_11008_m1", "decode_4096_m1", "decode_11008_m8", "decode_4096_m8"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_workload_parity_full(name):
+    case = workloads.make(name)
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+def test_square_8192_sampled():
+    """Full-size 8192^3 at the benchmark's launch configuration: all codes and
+    scales bit-exact; accumulators and outputs on 4096 sampled positions."""
+    case = workloads.square_8192()
+    g = gpu_run(case, with_acc=False, debug=True)
+    q_w, s_w = oracle.quantize_weights(case["W"], case["w_bits"])
+    q_a, s_a, seg_bits, seg_of = oracle.quantize_act(case["A"], case["a_bits"], case["a_signed"])
+    np.testing.assert_array_equal(g["s_w"], s_w)
+    np.testing.assert_array_equal(g["s_a"], s_a)
+    np.testing.assert_array_equal(g["q_w"], q_w)
+    np.testing.assert_array_equal(g["q_a"], q_a)
+    del g["q_w"], g["q_a"]
+    # accumulators at sampled positions, through a second call with the dump
+    w, act = g["w"], g["act"]
+    acc = torch.empty((w.S, case["M"], case["N"]), dtype=torch.int32, device="cuda")
+    Y = sq.soniq_mp_gemm(act, w, acc=acc)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    ms = np.concatenate([rng.integers(0, case["M"], 4088), [0, 0, 8191, 8191, 127, 128, 4095, 4096]])
+    ns = np.concatenate([rng.integers(0, case["N"], 4088), [0, 8191, 0, 8191, 128, 127, 4096, 4095]])
+    ref = oracle.mac_at(q_a, q_w, seg_of, len(seg_bits), ms, ns)
+    mi, ni = torch.from_numpy(ms).cuda(), torch.from_numpy(ns).cuda()
+    got = acc[:, mi, ni].cpu().numpy().T.astype(np.int64)
+    np.testing.assert_array_equal(got, ref)
+    y = _bf16_bits(Y[mi, ni])
+    acc_s = ref.T.astype(np.int32)[:, None, :]          # [S, 1, count]
+    yr = oracle.epilogue_replay(acc_s, s_a, s_w[ns]).ravel()
+    np.testing.assert_array_equal(y, yr)
+    # also the same bits as the call without the dump
+    np.testing.assert_array_equal(g["y"][ms, ns], y)
+
+
+EDGE = [  # (M, N, K, a_lo, a_hi, w_lo, w_hi, a_signed)
+    (1, 1, 1, 4, 8, 2, 4, True),
+    (1, 65, 63, 4, 8, 2, 4, True),
+    (2, 130, 65, 2, 8, 1, 4, False),
+    (7, 63, 200, 4, 4, 4, 8, True),
+    (8, 300, 129, 1, 8, 1, 2, True),
+    (9, 63, 200, 4, 8, 2, 8, True),
+    (129, 257, 130, 4, 8, 2, 4, False),
+    (200, 1, 64, 8, 8, 8, 8, True),
+    (131, 129, 1000, 3, 6, 5, 7, True),
+    (257, 200, 333, 1, 2, 1, 3, False),
+    (3, 64, 4095, 4, 8, 2, 4, True),
+    (150, 100, 129, 1, 8, 1, 2, True),     # sign-bit x sign-bit padding, GEMM path
+    (20, 70, 65, 1, 1, 1, 1, True),        # all channels 1-bit
+]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=lambda s: "x".join(map(str, s[:3])) + f"_a{s[3]}{s[4]}w{s[5]}{s[6]}{'s' if s[7] else 'u'}")
+def test_edge_shapes(shape):
+    M, N, K, alo, ahi, wlo, whi, sgn = shape
+    case = workloads.generic(M, N, K, a_lo=alo, a_hi=ahi, a_frac_lo=0.6, w_lo=wlo, w_hi=whi,
+                             w_frac_lo=0.7, a_signed=sgn, seed=M * 1000 + N + K,
+                             a_abs=not sgn, name="edge")
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+@pytest.mark.parametrize("alo,ahi", [(1, 8), (2, 4), (3, 5), (6, 7), (1, 2)])
+@pytest.mark.parametrize("sgn", [True, False])
+@pytest.mark.parametrize("M", [3, 150])
+def test_activation_widths(alo, ahi, sgn, M):
+    case = workloads.generic(M, 96, 250, a_lo=alo, a_hi=ahi, a_frac_lo=0.5, w_lo=2, w_hi=8,
+                             w_frac_lo=0.5, a_signed=sgn, seed=alo * 10 + ahi + M, name="awidth")
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+@pytest.mark.parametrize("wlo,whi", [(1, 8), (2, 3), (4, 5), (6, 7), (1, 1), (8, 8)])
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("M", [5, 140])
+def test_weight_widths_and_grids(wlo, whi, mode, M):
+    case = workloads.generic(M, 150, 190, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=wlo, w_hi=whi,
+                             w_frac_lo=0.5, seed=wlo * 10 + whi + M + 100 * mode, name="wwidth")
+    compare_full(gpu_run(case, wq_mode=mode), oracle_run(case, wq_mode=mode))
+
+
+def test_strides_and_unaligned_rows():
+    case = workloads.generic(70, 100, 131, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
+                             w_frac_lo=0.5, seed=5, name="strides")
+    compare_full(gpu_run(case, ldw_pad=3, lda_pad=5, ldy_pad=7), oracle_run(case))
+    case = workloads.generic(5, 100, 132, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
+                             w_frac_lo=0.5, seed=6, name="strides2")
+    compare_full(gpu_run(case, ldw_pad=1, lda_pad=1, ldy_pad=1), oracle_run(case))
+
+
+def test_zero_inputs():
+    case = workloads.generic(40, 70, 100, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=1, w_hi=4,
+                             w_frac_lo=0.5, seed=9, name="zeros")
+    case["A"][:] = 0.0
+    case["W"][::3] = 0.0
+    compare_full(gpu_run(case), oracle_run(case))
+    case = workloads.generic(4, 70, 100, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=1, w_hi=4,
+                             w_frac_lo=0.5, seed=10, name="zeros-group")
+    case["A"][:, case["a_bits"] == 8] = 0.0       # one activation group all zero
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+def test_tiny_and_huge_magnitudes():
+    case = workloads.generic(33, 40, 77, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=8,
+                             w_frac_lo=0.5, seed=11, a_std=1e-30, w_std=1e30, name="scale")
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+def test_repeat_calls_and_smaller_batch():
+    """Results do not depend on an earlier, larger call through the same
+    handles, and repeated calls are bit-identical (no races)."""
+    big = workloads.generic(300, 130, 260, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
+                            w_frac_lo=0.5, seed=12, name="big")
+    W = torch.from_numpy(big["W"]).cuda()
+    w = sq.soniq_pack_weights(W, big["w_bits"], big["a_bits"], True)
+    act = sq.soniq_act_create(w, 300)
+    ys = []
+    for M in (300, 300, 7, 131, 7):
+        A = torch.from_numpy(big["A"][:M].copy()).cuda()
+        sq.soniq_quantize_act(act, A)
+        acc = torch.empty((w.S, M, 130), dtype=torch.int32, device="cuda")
+        Y = sq.soniq_mp_gemm(act, w, acc=acc)
+        torch.cuda.synchronize()
+        r = oracle.run(big["A"][:M], big["W"], big["a_bits"], big["w_bits"], True)
+        np.testing.assert_array_equal(acc.cpu().numpy(), r["acc"])
+        np.testing.assert_array_equal(_bf16_bits(Y), r["y_replay"])
+        ys.append(_bf16_bits(Y))
+    np.testing.assert_array_equal(ys[0], ys[1])
+    np.testing.assert_array_equal(ys[2], ys[4])
+
+
+def test_api_errors_on_device():
+    case = workloads.tiny_linear()
+    W = torch.from_numpy(case["W"]).cuda()
+    w = sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], True)
+    w2 = sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], True)
+    act = sq.soniq_act_create(w, 16)
+    with pytest.raises(sq.SoniqError):
+        sq.soniq_mp_gemm(act, w)                 # nothing quantized yet
+    A = torch.from_numpy(case["A"]).cuda()
+    with pytest.raises(sq.SoniqError):
+        sq.soniq_quantize_act(act, A)            # M = 64 > max_M = 16
+    sq.soniq_quantize_act(act, A[:16])
+    with pytest.raises(sq.SoniqError):
+        sq.soniq_mp_gemm(act, w2)                # activations of other weights
+    info = sq.soniq_weights_info(w)
+    assert info.N == 256 and info.K == 256 and info.S == 2
+    assert list(info.a_bits) == [4, 8] and list(info.w_bits) == [2, 4]
+    assert info.packed_w_bytes_algorithmic == (192 * 2 + 64 * 4) * 256 // 8
