@@ -4,14 +4,16 @@
 // Input-channel plan (Alg. 1 channel permutation; Fig. "normalization"):
 // the activation widths define at most two groups (C3), ordered narrow then
 // wide; within a group channels keep their original order; each group is
-// padded with zero channels to a multiple of 64 so every group starts on a
-// fresh 64-element unit of every packed row.
+// padded with zero channels to a multiple of 64 (one MFMA k-step) so every
+// group starts on a fresh granule of every packed row.
 //
-// Output-channel plan: channels are cut into tiles of 64 consecutive
-// original channels; inside a tile the narrow-width channels are stored
-// first (stable), so each tile holds two runs of uniform container width
-// (C1 at tile granularity) while every tile still covers a contiguous range
-// of output columns, which keeps the output stores local.
+// Output-channel plan (C1: one width per 16-row block): the channels of
+// each weight width, in original order, are cut into blocks of 16 (the
+// last block of a width padded with empty rows).  The blocks of the two
+// widths are then merged by their first original channel, so any run of
+// consecutive blocks covers a nearly contiguous range of output columns and
+// the GEMM's output stores stay local.  The block count is padded to a
+// multiple of 8 (one 128-column GEMM tile).
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
@@ -177,16 +179,21 @@ struct soniq_weights_s {
   int wb[2] = {0, 0};
   int64_t w_cnt[2] = {0, 0};
   WPlan wp{};
-  std::vector<TileDesc> tiles_h;
+  std::vector<uint64_t> blk_off_h;
+  std::vector<uint8_t> blk_c_h;
   std::vector<int32_t> phys_h;
-  std::vector<int64_t> row_off_h;
   int64_t packed_bytes = 0;
   uint8_t* packed = nullptr;
-  TileDesc* tiles = nullptr;
+  uint64_t* blk_off = nullptr;
+  uint8_t* blk_c = nullptr;
   ColInfo* colinfo = nullptr;
   uint8_t* shw = nullptr;
+  int32_t* tile_cols = nullptr;
+  uint8_t* colrank = nullptr;
   int32_t* pos = nullptr;
   uint8_t* seg = nullptr;
+
+  WDev dev() const { return WDev{packed, blk_off, blk_c, colinfo, shw, tile_cols, colrank}; }
 };
 
 struct soniq_act_s {
@@ -206,9 +213,12 @@ namespace {
 void free_weights(soniq_weights w) {
   (void)hipDeviceSynchronize();
   (void)hipFree(w->packed);
-  (void)hipFree(w->tiles);
+  (void)hipFree(w->blk_off);
+  (void)hipFree(w->blk_c);
   (void)hipFree(w->colinfo);
   (void)hipFree(w->shw);
+  (void)hipFree(w->tile_cols);
+  (void)hipFree(w->colrank);
   (void)hipFree(w->pos);
   (void)hipFree(w->seg);
   w->magic = kDead;
@@ -233,11 +243,12 @@ ActPlan make_act_plan(const soniq_weights_s& w, int64_t M_alloc) {
       ap.sh[g] = unpack_shift(ap.c[g]);
       ap.zp[g] = a_zero_point(b, w.a_signed, ap.c[g]);
       ap.kpad[g] = (int)w.kp.pad[g];
-      ap.row_bytes[g] = round_up(w.kp.pad[g] * ap.c[g] / 8, 16);
-      ap.seg_off[g] = off;
-      off = round_up(off + M_alloc * ap.row_bytes[g], 256);
-      ap.q[g] = a_qparam(b, w.a_signed);
+      ap.ng[g] = (int)(w.kp.pad[g] / kGran);
       ap.padcnt[g] = (int)(w.kp.pad[g] - w.kp.len[g]);
+      ap.mblk_bytes[g] = (int64_t)ap.ng[g] * 128 * ap.c[g];
+      ap.seg_off[g] = off;
+      off = round_up(off + (M_alloc / kBlk) * ap.mblk_bytes[g], 256);
+      ap.q[g] = a_qparam(b, w.a_signed);
     } else {
       ap.c[g] = 8;
       ap.q[g] = a_qparam(8, 1);
@@ -249,18 +260,36 @@ ActPlan make_act_plan(const soniq_weights_s& w, int64_t M_alloc) {
 
 int64_t act_bytes(const ActPlan& ap, int64_t M_alloc) {
   int64_t off = 0;
-  for (int g = 0; g < ap.S; ++g) off = round_up(off + M_alloc * ap.row_bytes[g], 256);
+  for (int g = 0; g < ap.S; ++g) off = round_up(off + (M_alloc / kBlk) * ap.mblk_bytes[g], 256);
   return off;
 }
 
-// Field f (container c) of element e of a packed row.
-uint32_t field_of(const uint8_t* row, int64_t e, int c) {
-  const int per = 32 / c;
+// Field of element e (0..15) of a unit of container c at p.
+uint32_t unit_field(const uint8_t* p, int e, int c) {
+  const int j = e / 4, b = e % 4;
+  if (c == 8) return p[e];
+  if (c == 1) {
+    const uint32_t h = (uint32_t)p[0] | ((uint32_t)p[1] << 8);
+    return (h >> (4 * b + j)) & 1u;
+  }
   uint32_t word;
-  memcpy(&word, row + (e / per) * 4, 4);
-  const int ee = (int)(e % per);
-  const int j = ee / 4, b = ee % 4;
-  return (word >> (8 * b + c * j)) & ((1u << c) - 1u);
+  if (c == 4) {
+    memcpy(&word, p + 4 * (e / 8), 4);
+    const int jj = (e % 8) / 4;
+    return (word >> (8 * b + 4 * jj)) & 0xFu;
+  }
+  memcpy(&word, p, 4);
+  return (word >> (8 * b + 2 * j)) & 0x3u;
+}
+
+// Field of row r, channel position e (in the group-ordered padded axis of
+// one group) of a fragment-major region whose block-granules are `gstride`
+// = 128*c bytes apart.
+uint32_t block_field(const uint8_t* blk, int r, int64_t e, int c) {
+  const int64_t q = e / kGran;
+  const int within = (int)(e % kGran);
+  const int kg = within / 16, el = within % 16;
+  return unit_field(blk + q * 128 * c + (kg * 16 + r) * 2 * c, el, c);
 }
 
 int decode_signed(uint32_t f, int c) {
@@ -334,58 +363,68 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
   WPlan& wp = w->wp;
   wp.c_lo = w_container(b_lo, wq_mode);
   wp.c_hi = w_container(b_hi, wq_mode);
-  wp.sh_lo = unpack_shift(wp.c_lo);
-  wp.sh_hi = unpack_shift(wp.c_hi);
-  wp.rb_lo = round_up(w->kp.Kp * wp.c_lo / 8, 16);
-  wp.rb_hi = round_up(w->kp.Kp * wp.c_hi / 8, 16);
-  wp.ntiles = (int)((N + kNTile - 1) / kNTile);
-  wp.ntiles += wp.ntiles & 1;  // even, so 128-column GEMM tiles stay in range
-  wp.Np = wp.ntiles * kNTile;
-  w->tiles_h.assign(wp.ntiles, TileDesc{0, 0, 0});
+  wp.ngt = (int)(w->kp.Kp / kGran);
+  std::vector<int32_t> rows_lo, rows_hi;
+  for (int64_t n = 0; n < N; ++n) (w_bits[n] == b_lo ? rows_lo : rows_hi).push_back((int32_t)n);
+  w->w_cnt[0] = (int64_t)rows_lo.size();
+  w->w_cnt[1] = (int64_t)rows_hi.size();
+  const int64_t nb_lo = (w->w_cnt[0] + kBlk - 1) / kBlk, nb_hi = (w->w_cnt[1] + kBlk - 1) / kBlk;
+  int64_t nblk = nb_lo + nb_hi;
+  nblk = round_up(nblk, kGemmBN / kBlk);
+  wp.nblk = (int)nblk;
+  wp.Np = (int)(nblk * kBlk);
+  w->blk_off_h.assign(nblk, 0);
+  w->blk_c_h.assign(nblk, (uint8_t)wp.c_lo);
   w->phys_h.assign(N, 0);
-  w->row_off_h.assign(N, 0);
   std::vector<ColInfo> colinfo_h(wp.Np, ColInfo{-1, 0.0f, {0, 0}});
   std::vector<uint8_t> shw_h(wp.Np, 0);
-  uint64_t base = 0;
-  for (int t = 0; t < wp.ntiles; ++t) {
-    const int64_t n0 = (int64_t)t * kNTile;
-    const int64_t n1 = std::min<int64_t>(n0 + kNTile, N);
-    TileDesc td{base, 0, 0};
-    if (n0 < N) {
-      int rank = 0;
-      for (int64_t n = n0; n < n1; ++n)
-        if (w_bits[n] == b_lo) {
-          w->phys_h[n] = (int32_t)(n0 + rank);
-          w->row_off_h[n] = (int64_t)base + (int64_t)rank * wp.rb_lo;
-          ++rank;
-        }
-      td.n_lo = rank;
-      for (int64_t n = n0; n < n1; ++n)
-        if (w_bits[n] != b_lo) {
-          w->phys_h[n] = (int32_t)(n0 + rank);
-          w->row_off_h[n] = (int64_t)base + (int64_t)td.n_lo * wp.rb_lo +
-                            (int64_t)(rank - td.n_lo) * wp.rb_hi;
-          ++rank;
-        }
-      td.n_rows = rank;
-      for (int64_t n = n0; n < n1; ++n) {
-        colinfo_h[w->phys_h[n]].n = (int32_t)n;
-        const int c = w_bits[n] == b_lo ? wp.c_lo : wp.c_hi;
-        shw_h[w->phys_h[n]] = (uint8_t)(unpack_shift(c) | (c == 1 ? kShwSign : 0));
+  {
+    int64_t il = 0, ih = 0, b = 0;
+    uint64_t off = 0;
+    auto place = [&](const std::vector<int32_t>& rows, int64_t blk_in_width, int c) {
+      for (int r = 0; r < kBlk; ++r) {
+        const int64_t idx = blk_in_width * kBlk + r;
+        if (idx >= (int64_t)rows.size()) break;
+        const int32_t n = rows[idx];
+        const int32_t p = (int32_t)(b * kBlk + r);
+        w->phys_h[n] = p;
+        colinfo_h[p].n = n;
+        shw_h[p] = (uint8_t)(unpack_shift(c) | (c == 1 ? kShwSign : 0));
       }
+      w->blk_c_h[b] = (uint8_t)c;
+      w->blk_off_h[b] = off;
+      off += (uint64_t)wp.ngt * 128 * c;  // blocks are contiguous (the GEMM relies on it)
+      ++b;
+    };
+    while (il < nb_lo || ih < nb_hi) {
+      const bool take_lo = ih >= nb_hi || (il < nb_lo && rows_lo[il * kBlk] < rows_hi[ih * kBlk]);
+      if (take_lo) place(rows_lo, il++, wp.c_lo);
+      else place(rows_hi, ih++, wp.c_hi);
     }
-    w->tiles_h[t] = td;
-    base = (uint64_t)round_up((int64_t)base + (int64_t)td.n_lo * wp.rb_lo +
-                                  (int64_t)(td.n_rows - td.n_lo) * wp.rb_hi,
-                              256);
+    static const std::vector<int32_t> none;
+    while (b < nblk) place(none, 0, wp.c_lo);
+    w->packed_bytes = (int64_t)off;
   }
-  w->packed_bytes = (int64_t)base;
-  for (int64_t n = 0; n < N; ++n) w->w_cnt[w_bits[n] == b_lo ? 0 : 1]++;
+  // Output order inside each 128-column tile, for coalesced stores.
+  const int ntile = wp.Np / kGemmBN;
+  std::vector<int32_t> tile_cols_h((size_t)wp.Np, -1);
+  std::vector<uint8_t> colrank_h((size_t)wp.Np, 255);
+  for (int t = 0; t < ntile; ++t) {
+    std::vector<std::pair<int32_t, int32_t>> cols;  // (n, physical position)
+    for (int j = 0; j < kGemmBN; ++j) {
+      const int32_t p = t * kGemmBN + j;
+      if (colinfo_h[p].n >= 0) cols.emplace_back(colinfo_h[p].n, p);
+    }
+    std::sort(cols.begin(), cols.end());
+    for (size_t r = 0; r < cols.size(); ++r) {
+      tile_cols_h[(size_t)t * kGemmBN + r] = cols[r].first;
+      colrank_h[cols[r].second] = (uint8_t)r;
+    }
+  }
 
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   soniq_status rc = SONIQ_OK;
   uint8_t* wbits_dev = nullptr;
-  int64_t* row_off_dev = nullptr;
   int32_t* phys_dev = nullptr;
   hipError_t e = hipSuccess;
 #define STEP(expr)                              \
@@ -394,31 +433,33 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
     if (e != hipSuccess) rc = fail_hip(e, #expr); \
   }
   STEP(dev_alloc(&w->packed, (size_t)w->packed_bytes));
-  STEP(dev_alloc(&w->tiles, (size_t)wp.ntiles));
+  STEP(dev_alloc(&w->blk_off, (size_t)wp.nblk));
+  STEP(dev_alloc(&w->blk_c, (size_t)wp.nblk));
   STEP(dev_alloc(&w->colinfo, (size_t)wp.Np));
   STEP(dev_alloc(&w->shw, (size_t)wp.Np));
+  STEP(dev_alloc(&w->tile_cols, (size_t)wp.Np));
+  STEP(dev_alloc(&w->colrank, (size_t)wp.Np));
   STEP(dev_alloc(&w->pos, (size_t)K));
   STEP(dev_alloc(&w->seg, (size_t)K));
   STEP(dev_alloc(&wbits_dev, (size_t)N));
-  STEP(dev_alloc(&row_off_dev, (size_t)N));
   STEP(dev_alloc(&phys_dev, (size_t)N));
   STEP(hipMemsetAsync(w->packed, 0, (size_t)w->packed_bytes, st));
-  STEP(hipMemcpyAsync(w->tiles, w->tiles_h.data(), wp.ntiles * sizeof(TileDesc), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->blk_off, w->blk_off_h.data(), wp.nblk * sizeof(uint64_t), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->blk_c, w->blk_c_h.data(), wp.nblk, hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->colinfo, colinfo_h.data(), wp.Np * sizeof(ColInfo), hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->shw, shw_h.data(), wp.Np, hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->tile_cols, tile_cols_h.data(), wp.Np * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->colrank, colrank_h.data(), wp.Np, hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->pos, w->kp.pos.data(), K * sizeof(int32_t), hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->seg, w->kp.seg.data(), K, hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(wbits_dev, w_bits, N, hipMemcpyHostToDevice, st));
-  STEP(hipMemcpyAsync(row_off_dev, w->row_off_h.data(), N * sizeof(int64_t), hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(phys_dev, w->phys_h.data(), N * sizeof(int32_t), hipMemcpyHostToDevice, st));
-  STEP(launch_wpack(W_dev, N, K, ldw, wbits_dev, w->pos, w->seg, row_off_dev, phys_dev,
-                    w_qparam(b_lo, wq_mode), w_qparam(b_hi, wq_mode), b_lo, wp.c_lo, wp.c_hi,
-                    (int)w->kp.Kp, (int)w->kp.pad[0], wp.rb_lo, wp.rb_hi, w->packed,
-                    w->colinfo, st));
+  STEP(launch_wpack(W_dev, N, K, ldw, wbits_dev, w->pos, w->seg, phys_dev, w->blk_off, w->blk_c,
+                    w_qparam(b_lo, wq_mode), w_qparam(b_hi, wq_mode), b_lo, (int)w->kp.Kp,
+                    w->packed, w->colinfo, st));
   STEP(hipStreamSynchronize(st));
 #undef STEP
   (void)hipFree(wbits_dev);
-  (void)hipFree(row_off_dev);
   (void)hipFree(phys_dev);
   if (rc != SONIQ_OK) {
     free_weights(w);
@@ -459,13 +500,13 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out) {
 
 soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
   if (!live_w(w) || !out) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create: bad handle or null");
-  if (max_M < 1 || max_M > ((int64_t)1 << 31) - 128)
+  if (max_M < 1 || max_M > ((int64_t)1 << 31) - kMAlign)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create: max_M out of range");
   soniq_act a = new (std::nothrow) soniq_act_s();
   if (!a) return fail(SONIQ_ERR_OUT_OF_MEMORY, "soniq_act_create: host allocation");
   a->w = w;
   a->max_M = max_M;
-  a->M_alloc = round_up(max_M, kGemmBM);
+  a->M_alloc = round_up(max_M, kMAlign);
   a->ap = make_act_plan(*w, a->M_alloc);
   a->packed_bytes = act_bytes(a->ap, a->M_alloc);
   hipError_t e = dev_alloc(&a->packed, (size_t)a->packed_bytes);
@@ -517,14 +558,15 @@ soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int6
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: ldy < N");
   const int64_t M = act->M;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (gemv_fits(M, act->ap.Kp)) {
-    HIP_TRY(launch_mp_gemv(act->packed, act->s_a, act->ap, w->packed, w->tiles, w->colinfo,
-                           w->shw, w->wp, M, w->N, Y_dev, ldy, acc_dev, st));
+  if (gemv_fits(M, act->ap, w->wp)) {
+    HIP_TRY(launch_mp_gemv(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                           acc_dev, st));
   } else {
-    if ((M + kGemmBM - 1) / kGemmBM > 65535)
-      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: M too large for one launch");
-    HIP_TRY(launch_mp_gemm(act->packed, act->s_a, act->ap, w->packed, w->tiles, w->colinfo,
-                           w->shw, w->wp, M, w->N, Y_dev, ldy, acc_dev, st));
+    const int64_t tiles = ((M + 63) / 64) * (w->wp.Np / kGemmBN);
+    if (tiles > 0x7FFFFFFFLL)
+      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
+    HIP_TRY(launch_mp_gemm(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                           acc_dev, st));
   }
   return SONIQ_OK;
 }
@@ -536,17 +578,14 @@ soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* 
   std::vector<ColInfo> ci(w->wp.Np);
   HIP_TRY(hipMemcpy(packed.data(), w->packed, w->packed_bytes, hipMemcpyDeviceToHost));
   HIP_TRY(hipMemcpy(ci.data(), w->colinfo, ci.size() * sizeof(ColInfo), hipMemcpyDeviceToHost));
-  const int b_lo = w->wb[0];
-  (void)b_lo;
   for (int64_t n = 0; n < w->N; ++n) {
     const int32_t p = w->phys_h[n];
-    const int t = p / kNTile, j = p % kNTile;
-    const bool lo = j < w->tiles_h[t].n_lo;
-    const int c = lo ? w->wp.c_lo : w->wp.c_hi;
-    const uint8_t* row = packed.data() + w->row_off_h[n];
+    const int b = p / kBlk, r = p % kBlk;
+    const int c = w->blk_c_h[b];
+    const uint8_t* blk = packed.data() + w->blk_off_h[b];
     if (codes)
       for (int64_t k = 0; k < w->K; ++k)
-        codes[n * w->K + k] = decode_signed(field_of(row, w->kp.pos[k], c), c);
+        codes[n * w->K + k] = decode_signed(block_field(blk, r, w->kp.pos[k], c), c);
     if (s_w) s_w[n] = ci[p].s_w;
   }
   return SONIQ_OK;
@@ -567,8 +606,8 @@ soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a) {
       for (int64_t k = 0; k < w->K; ++k) {
         const int g = w->kp.seg[k];
         const int64_t e = w->kp.pos[k] - (g ? ap.kpad[0] : 0);
-        const uint8_t* row = packed.data() + ap.seg_off[g] + m * ap.row_bytes[g];
-        codes[m * w->K + k] = decode_signed(field_of(row, e, ap.c[g]), ap.c[g]) + ap.zp[g];
+        const uint8_t* blk = packed.data() + ap.seg_off[g] + (m / kBlk) * ap.mblk_bytes[g];
+        codes[m * w->K + k] = decode_signed(block_field(blk, (int)(m % kBlk), e, ap.c[g]), ap.c[g]) + ap.zp[g];
       }
   if (s_a)
     for (int g = 0; g < ap.S; ++g) s_a[g] = sa[g];

@@ -1,23 +1,28 @@
 // gfx950 (CDNA4) kernels of the SONIQ inference hot path.
 //
-//   k_wpack      quantize one output channel, place its codes on the
-//                group-ordered, padded channel axis, bit-pack it and record
-//                its scale and per-group code sums            (once per layer)
-//   k_absmax     per-activation-group max-abs over all rows, finished by the
-//                last workgroup, which also writes the group scales
-//   k_act_pack   quantize, re-order and bit-pack activation rows
-//   k_gemm<S>    int8 MFMA GEMM on the packed operands: 128x128 block tile,
-//                LDS double buffer filled through a register stage that
-//                unpacks 1/2/4-bit fields to int8, one int32 accumulator set
-//                per activation group, fixed-order fp32 epilogue to bf16
-//   k_gemv<MT>   batch <= 8 decode without matrix cores: the activation rows
-//                are unpacked once per workgroup into LDS, 16 lanes stream
-//                one packed weight row with 128-bit loads and v_dot4_i32_i8
+//   k_wpack         quantize one output channel, place its codes on the
+//                   group-ordered padded channel axis and write its units
+//                   into its 16-row block; record scale and code sums
+//   k_absmax_*      per-activation-group max-abs over all rows; the last
+//                   workgroup writes the group scales
+//   k_act_pack      quantize, re-order and pack one activation row
+//   k_act_small     small batches in one launch (max, quantize, pack)
+//   k_gemm          int8 MFMA GEMM on packed operands: a 3-stage ring of
+//                   LDS buffers filled by direct global->LDS loads of packed
+//                   fragments, unpacked to int8 in registers right before
+//                   v_mfma_i32_16x16x64_i8, one int32 accumulator set per
+//                   activation group, fixed-order fp32 epilogue to bf16
+//   k_gemv          batch <= 8 decode without matrix cores: one workgroup
+//                   streams one 16-row weight block with 128-bit loads and
+//                   v_dot4_i32_i8 against activations unpacked in LDS
 //
-// Paper passages: Sec. 2.4 C1/C2/C5; Sec. 3 codec (scale, unsigned codes,
-// Eq. 1 weight codes); Alg. 1 channel permutation and Phase II integer MAC;
-// Fig. "normalization" (group by width, pad to the vector width).
+// Paper passages: Sec. 2.4 C1/C2/C5; Sec. 3 codec (group max-abs scale,
+// unsigned codes, Eq. 1 weight codes); Alg. 1 channel permutation and Phase
+// II integer MAC; Fig. "normalization" (group by width, pad to the vector
+// width).
 #include "soniq_internal.h"
+
+#include <cstdlib>
 
 namespace soniq {
 namespace {
@@ -25,107 +30,32 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- codec --
-__device__ __forceinline__ int quant_code(float x, float s, const QParam& q) {
+// Code of x under step s.  The quotient is taken as one IEEE fp32 division
+// rounded to nearest even.  When `fast` (s normal and not tiny) the
+// quotient is first estimated with a reciprocal; the estimate is within
+// 2^-14 of the true quotient (|x/s| <= 256), so rint of the estimate equals
+// rint of the correctly rounded quotient unless the estimate lies within
+// 2^-9 of a half-integer, where the exact division decides.
+__device__ __forceinline__ int quant_code(float x, float s, float rs, bool fast,
+                                          const QParam& q) {
   if (q.sign1) return x < 0.0f ? -1 : 1;
   if (s == 0.0f) return 0;
-  float t = __builtin_rintf(__fdiv_rn(x, s));
+  float t;
+  if (fast) {
+    const float e = x * rs;
+    t = __builtin_rintf(e);
+    if (fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f) t = __builtin_rintf(__fdiv_rn(x, s));
+  } else {
+    t = __builtin_rintf(__fdiv_rn(x, s));
+  }
   t = fminf(fmaxf(t, (float)q.lo), (float)q.hi);
   return (int)t;
 }
 
+__device__ __forceinline__ bool fast_ok(float s) { return s >= 0x1p-100f && s <= 0x1p100f; }
+
 __device__ __forceinline__ float group_scale(float maxabs, const QParam& q) {
   return q.sign1 ? maxabs : __fdiv_rn(maxabs, q.qdiv);
-}
-
-// One packed word from E = 32/c stored int8 codes (E/4 dwords, natural order).
-__device__ __forceinline__ uint32_t pack_word(const uint32_t* d, int c) {
-  if (c == 8) return d[0];
-  if (c == 4) return (d[0] & 0x0F0F0F0Fu) | ((d[1] & 0x0F0F0F0Fu) << 4);
-  if (c == 2)
-    return (d[0] & 0x03030303u) | ((d[1] & 0x03030303u) << 2) |
-           ((d[2] & 0x03030303u) << 4) | ((d[3] & 0x03030303u) << 6);
-  uint32_t w = 0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) w |= ((d[j] >> 7) & 0x01010101u) << j;
-  return w;
-}
-
-// A "unit" is 64 consecutive elements of one row: 8*c packed bytes, or 64
-// unpacked int8.  Held in four 128-bit registers (no arrays, so it stays in
-// VGPRs whatever the container).
-struct Unit {
-  uint4 v0, v1, v2, v3;
-};
-
-__device__ __forceinline__ uint4 u4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
-  return make_uint4(a, b, c, d);
-}
-
-// Load a unit (8-byte aligned for c = 1, 16-byte aligned otherwise).
-__device__ __forceinline__ Unit load_unit(const uint8_t* p, int c) {
-  Unit u;
-  const uint4 z = u4(0, 0, 0, 0);
-  u.v0 = z; u.v1 = z; u.v2 = z; u.v3 = z;
-  const uint4* q = reinterpret_cast<const uint4*>(p);
-  if (c == 1) {
-    const uint2 t = *reinterpret_cast<const uint2*>(p);
-    u.v0.x = t.x;
-    u.v0.y = t.y;
-  } else {
-    u.v0 = q[0];
-    if (c >= 4) u.v1 = q[1];
-    if (c == 8) {
-      u.v2 = q[2];
-      u.v3 = q[3];
-    }
-  }
-  return u;
-}
-
-// Four consecutive elements per output dword, see unpack_word.
-__device__ __forceinline__ uint4 unpack2(uint32_t w) {
-  return u4((w << 6) & 0xC0C0C0C0u, (w << 4) & 0xC0C0C0C0u, (w << 2) & 0xC0C0C0C0u,
-            w & 0xC0C0C0C0u);
-}
-__device__ __forceinline__ uint4 unpack4(uint32_t w0, uint32_t w1) {
-  return u4((w0 << 4) & 0xF0F0F0F0u, w0 & 0xF0F0F0F0u, (w1 << 4) & 0xF0F0F0F0u,
-            w1 & 0xF0F0F0F0u);
-}
-__device__ __forceinline__ uint32_t sgn1(uint32_t w, int j) {
-  return ((w << (7 - j)) & 0x80808080u) | 0x40404040u;
-}
-__device__ __forceinline__ uint4 unpack1_lo(uint32_t w) {
-  return u4(sgn1(w, 0), sgn1(w, 1), sgn1(w, 2), sgn1(w, 3));
-}
-__device__ __forceinline__ uint4 unpack1_hi(uint32_t w) {
-  return u4(sgn1(w, 4), sgn1(w, 5), sgn1(w, 6), sgn1(w, 7));
-}
-
-// Unpack a loaded unit to 64 scaled int8 elements; zeros when !valid.
-__device__ __forceinline__ Unit unpack_unit(const Unit& w, int c, bool valid) {
-  Unit d;
-  if (!valid) {
-    const uint4 z = u4(0, 0, 0, 0);
-    d.v0 = z; d.v1 = z; d.v2 = z; d.v3 = z;
-  } else if (c == 8) {
-    d = w;
-  } else if (c == 4) {
-    d.v0 = unpack4(w.v0.x, w.v0.y);
-    d.v1 = unpack4(w.v0.z, w.v0.w);
-    d.v2 = unpack4(w.v1.x, w.v1.y);
-    d.v3 = unpack4(w.v1.z, w.v1.w);
-  } else if (c == 2) {
-    d.v0 = unpack2(w.v0.x);
-    d.v1 = unpack2(w.v0.y);
-    d.v2 = unpack2(w.v0.z);
-    d.v3 = unpack2(w.v0.w);
-  } else {
-    d.v0 = unpack1_lo(w.v0.x);
-    d.v1 = unpack1_hi(w.v0.x);
-    d.v2 = unpack1_lo(w.v0.y);
-    d.v3 = unpack1_hi(w.v0.y);
-  }
-  return d;
 }
 
 __device__ __forceinline__ uint16_t bf16_rne(float x) {
@@ -142,21 +72,81 @@ __device__ __forceinline__ float epilogue(int t0, int t1, int S, float sa0, floa
 }
 
 // Exact accumulator of one activation group from the raw dot product of
-// unpacked bytes: undo the unpack scales, remove the products of padding
-// channels (only sign-bit x sign-bit padding is nonzero: both decode to +1,
-// each product 64*64), add the unsigned zero point times the code sum.
+// unpacked bytes: remove the products of padding channels (only sign-bit x
+// sign-bit padding is nonzero: both decode to +1, each product 64*64), undo
+// the unpack scales, add the unsigned zero point times the code sum.
 __device__ __forceinline__ int true_acc(int raw, int sha, int ca, int padcnt, int zp,
                                         uint8_t shw, int colsum) {
   if (ca == 1 && (shw & kShwSign)) raw -= padcnt << 12;
   return (raw >> (sha + (shw & 0x7F))) + zp * colsum;
 }
 
-// Stored activation code of x in group g (code minus the group zero point).
-__device__ __forceinline__ uint8_t store_code(float x, int g, float s0, float s1,
-                                              const QParam& q0, const QParam& q1, int zp0,
-                                              int zp1) {
-  const int code = g ? quant_code(x, s1, q1) - zp1 : quant_code(x, s0, q0) - zp0;
-  return (uint8_t)(int8_t)code;
+// ------------------------------------------------------ unit pack/unpack --
+// Pack 16 stored int8 codes (4 dwords, natural order) into one unit.
+// Returns the unit's words; the unit occupies 2*c bytes.
+__device__ __forceinline__ uint4 pack_unit(uint32_t d0, uint32_t d1, uint32_t d2, uint32_t d3,
+                                           int c) {
+  if (c == 8) return make_uint4(d0, d1, d2, d3);
+  if (c == 4)
+    return make_uint4((d0 & 0x0F0F0F0Fu) | ((d1 & 0x0F0F0F0Fu) << 4),
+                      (d2 & 0x0F0F0F0Fu) | ((d3 & 0x0F0F0F0Fu) << 4), 0u, 0u);
+  if (c == 2)
+    return make_uint4((d0 & 0x03030303u) | ((d1 & 0x03030303u) << 2) |
+                          ((d2 & 0x03030303u) << 4) | ((d3 & 0x03030303u) << 6),
+                      0u, 0u, 0u);
+  const uint32_t y = ((d0 >> 7) & 0x01010101u) | (((d1 >> 7) & 0x01010101u) << 1) |
+                     (((d2 >> 7) & 0x01010101u) << 2) | (((d3 >> 7) & 0x01010101u) << 3);
+  const uint32_t h = (y & 0xFu) | ((y >> 4) & 0xF0u) | ((y >> 8) & 0xF00u) | ((y >> 12) & 0xF000u);
+  return make_uint4(h, 0u, 0u, 0u);
+}
+
+__device__ __forceinline__ void store_unit(uint8_t* p, uint4 u, int c) {
+  if (c == 8) *reinterpret_cast<uint4*>(p) = u;
+  else if (c == 4) *reinterpret_cast<uint2*>(p) = make_uint2(u.x, u.y);
+  else if (c == 2) *reinterpret_cast<uint32_t*>(p) = u.x;
+  else *reinterpret_cast<uint16_t*>(p) = (uint16_t)u.x;
+}
+
+__device__ __forceinline__ uint4 load_unit(const uint8_t* p, int c) {
+  if (c == 8) return *reinterpret_cast<const uint4*>(p);
+  if (c == 4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    return make_uint4(v.x, v.y, 0u, 0u);
+  }
+  if (c == 2) return make_uint4(*reinterpret_cast<const uint32_t*>(p), 0u, 0u, 0u);
+  return make_uint4(*reinterpret_cast<const uint16_t*>(p), 0u, 0u, 0u);
+}
+
+__device__ __forceinline__ uint4 unpack4(uint32_t w0, uint32_t w1) {
+  return make_uint4((w0 << 4) & 0xF0F0F0F0u, w0 & 0xF0F0F0F0u, (w1 << 4) & 0xF0F0F0F0u,
+                    w1 & 0xF0F0F0F0u);
+}
+__device__ __forceinline__ uint4 unpack2(uint32_t w) {
+  return make_uint4((w << 6) & 0xC0C0C0C0u, (w << 4) & 0xC0C0C0C0u, (w << 2) & 0xC0C0C0C0u,
+                    w & 0xC0C0C0C0u);
+}
+__device__ __forceinline__ uint32_t sgn1(uint32_t y, int j) {
+  return ((y << (7 - j)) & 0x80808080u) | 0x40404040u;
+}
+__device__ __forceinline__ uint4 unpack1(uint32_t h) {
+  uint32_t x = (h | (h << 8)) & 0x00FF00FFu;
+  const uint32_t y = (x | (x << 4)) & 0x0F0F0F0Fu;  // byte b = nibble b of h
+  return make_uint4(sgn1(y, 0), sgn1(y, 1), sgn1(y, 2), sgn1(y, 3));
+}
+
+// Unit (raw, low 2*c bytes valid) -> 16 scaled int8 elements.
+template <int C>
+__device__ __forceinline__ uint4 unpack_unit(uint4 raw) {
+  if constexpr (C == 8) return raw;
+  else if constexpr (C == 4) return unpack4(raw.x, raw.y);
+  else if constexpr (C == 2) return unpack2(raw.x);
+  else return unpack1(raw.x & 0xFFFFu);
+}
+__device__ __forceinline__ uint4 unpack_unit_rt(uint4 raw, int c) {
+  if (c == 8) return raw;
+  if (c == 4) return unpack4(raw.x, raw.y);
+  if (c == 2) return unpack2(raw.x);
+  return unpack1(raw.x & 0xFFFFu);
 }
 
 // ------------------------------------------------------------ reductions --
@@ -189,8 +179,8 @@ __device__ __forceinline__ int block_sum(int v, int* red) {
 __global__ __launch_bounds__(256) void k_wpack(
     const float* __restrict__ W, int64_t K, int64_t ldw, const uint8_t* __restrict__ w_bits,
     const int32_t* __restrict__ pos, const uint8_t* __restrict__ seg,
-    const int64_t* __restrict__ row_off, const int32_t* __restrict__ phys, QParam q_lo,
-    QParam q_hi, int b_lo, int c_lo, int c_hi, int Kp, int64_t rb_lo, int64_t rb_hi,
+    const int32_t* __restrict__ phys, const uint64_t* __restrict__ blk_off,
+    const uint8_t* __restrict__ blk_c, QParam q_lo, QParam q_hi, int b_lo, int Kp,
     uint8_t* __restrict__ packed, ColInfo* __restrict__ colinfo) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float redf[4];
@@ -203,31 +193,32 @@ __global__ __launch_bounds__(256) void k_wpack(
   for (int64_t k = tid; k < K; k += blockDim.x) m = fmaxf(m, fabsf(row[k]));
   m = block_max(m, redf);
 
-  const bool lo = w_bits[n] == b_lo;
-  const QParam q = lo ? q_lo : q_hi;
-  const int c = lo ? c_lo : c_hi;
+  const QParam q = w_bits[n] == b_lo ? q_lo : q_hi;
   const float s = group_scale(m, q);
+  const bool fast = fast_ok(s);
+  const float rs = fast ? __builtin_amdgcn_rcpf(s) : 0.0f;
 
   uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
   for (int i = tid; i < Kp / 4; i += blockDim.x) codes32[i] = 0;
   __syncthreads();
   int cs0 = 0, cs1 = 0;
   for (int64_t k = tid; k < K; k += blockDim.x) {
-    int code = quant_code(row[k], s, q);
+    const int code = quant_code(row[k], s, rs, fast, q);
     codes[pos[k]] = (uint8_t)(int8_t)code;
     if (seg[k] == 0) cs0 += code; else cs1 += code;
   }
   cs0 = block_sum(cs0, redi);
   cs1 = block_sum(cs1, redi);  // block_sum syncs, so the code writes are visible
 
-  const int per = 32 / c;
-  const int nwords = Kp / per;
-  const int rwords = (int)((lo ? rb_lo : rb_hi) >> 2);
-  uint32_t* dst = reinterpret_cast<uint32_t*>(packed + row_off[n]);
-  for (int w = tid; w < rwords; w += blockDim.x) {
-    uint32_t word = 0;
-    if (w < nwords) word = pack_word(codes32 + w * (per / 4), c);
-    dst[w] = word;
+  const int p = phys[n];
+  const int blk = p / kBlk, r = p % kBlk;
+  const int c = blk_c[blk];
+  uint8_t* dst = packed + blk_off[blk];
+  const int nunits = (Kp / kGran) * 4;
+  for (int u = tid; u < nunits; u += blockDim.x) {
+    const int qg = u >> 2, kg = u & 3;
+    const uint4 d = *reinterpret_cast<const uint4*>(codes + qg * kGran + kg * 16);
+    store_unit(dst + (int64_t)qg * 128 * c + (kg * 16 + r) * 2 * c, pack_unit(d.x, d.y, d.z, d.w, c), c);
   }
   if (tid == 0) {
     ColInfo ci;
@@ -235,49 +226,16 @@ __global__ __launch_bounds__(256) void k_wpack(
     ci.s_w = s;
     ci.colsum[0] = cs0;
     ci.colsum[1] = cs1;
-    colinfo[phys[n]] = ci;
+    colinfo[p] = ci;
   }
 }
 
 // -------------------------------------------------------------- k_absmax --
-// Max-abs of every activation group over all M rows.  Each workgroup
-// writes its partial maxima; the last one to finish reduces them, writes
-// the group scales s_a[g] and re-arms the counter for the next call.
-// Contiguous rows (lda == K, K % 4 == 0, 16-byte aligned) are read as one
-// flat float4 stream with kAbsU loads in flight per thread.
+// Max-abs of every activation group over all M rows, in two launches: each
+// workgroup here writes its partial maxima (no atomics, no fences: a
+// per-workgroup device-scope fence costs tens of nanoseconds each on a chip
+// with per-XCD L2s); the pack kernel that follows reduces the partials.
 constexpr int kAbsU = 8;
-
-__device__ __forceinline__ void absmax_finish(float mx0, float mx1, const ActPlan& ap,
-                                              float* __restrict__ partial,
-                                              unsigned int* __restrict__ counter,
-                                              float* __restrict__ s_a, float* red,
-                                              int* is_last) {
-  const int tid = threadIdx.x;
-  mx0 = block_max(mx0, red);
-  mx1 = block_max(mx1, red);
-  if (tid == 0) {
-    partial[2 * blockIdx.x] = mx0;
-    partial[2 * blockIdx.x + 1] = mx1;
-    __threadfence();
-    unsigned int ticket = atomicAdd(counter, 1u);
-    *is_last = (ticket == gridDim.x - 1);
-  }
-  __syncthreads();
-  if (!*is_last) return;
-  __threadfence();
-  float r0 = 0.0f, r1 = 0.0f;
-  for (int b = tid; b < (int)gridDim.x; b += blockDim.x) {
-    r0 = fmaxf(r0, __hip_atomic_load(&partial[2 * b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    r1 = fmaxf(r1, __hip_atomic_load(&partial[2 * b + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-  }
-  r0 = block_max(r0, red);
-  r1 = block_max(r1, red);
-  if (tid == 0) {
-    s_a[0] = group_scale(r0, ap.q[0]);
-    s_a[1] = ap.S == 2 ? group_scale(r1, ap.q[1]) : 0.0f;
-    *counter = 0u;
-  }
-}
 
 __device__ __forceinline__ void max4(float4 v, uchar4 g, float& mx0, float& mx1) {
   const float a0 = fabsf(v.x), a1 = fabsf(v.y), a2 = fabsf(v.z), a3 = fabsf(v.w);
@@ -285,13 +243,23 @@ __device__ __forceinline__ void max4(float4 v, uchar4 g, float& mx0, float& mx1)
   mx1 = fmaxf(mx1, fmaxf(fmaxf(g.x ? a0 : 0.0f, g.y ? a1 : 0.0f), fmaxf(g.z ? a2 : 0.0f, g.w ? a3 : 0.0f)));
 }
 
+__device__ __forceinline__ void write_partial(float mx0, float mx1, float* red,
+                                              float* __restrict__ partial) {
+  mx0 = block_max(mx0, red);
+  mx1 = block_max(mx1, red);
+  if (threadIdx.x == 0) {
+    partial[2 * blockIdx.x] = mx0;
+    partial[2 * blockIdx.x + 1] = mx1;
+  }
+}
+
+// Contiguous rows (lda == K, K % 4 == 0, 16-byte aligned): one flat float4
+// stream, kAbsU loads in flight per thread.  Out-of-range lanes re-read the
+// last element (always in bounds) and contribute nothing.
 __global__ __launch_bounds__(256) void k_absmax_flat(const float4* __restrict__ A, uint32_t total4,
                                                      uint32_t K4, const uchar4* __restrict__ seg4,
-                                                     ActPlan ap, float* __restrict__ partial,
-                                                     unsigned int* __restrict__ counter,
-                                                     float* __restrict__ s_a) {
+                                                     float* __restrict__ partial) {
   __shared__ float red[4];
-  __shared__ int is_last;
   float mx0 = 0.0f, mx1 = 0.0f;
   const uint32_t step = gridDim.x * 256u * kAbsU;
   for (uint32_t base = blockIdx.x * 256u * kAbsU + threadIdx.x; base < total4; base += step) {
@@ -299,30 +267,25 @@ __global__ __launch_bounds__(256) void k_absmax_flat(const float4* __restrict__ 
     uchar4 g[kAbsU];
 #pragma unroll
     for (int j = 0; j < kAbsU; ++j) {
-      const uint32_t i = base + 256u * j;
-      if (i < total4) {
-        v[j] = A[i];
-        g[j] = seg4[i % K4];
-      } else {
-        v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-        g[j] = make_uchar4(0, 0, 0, 0);
-      }
+      const uint32_t i = min(base + 256u * j, total4 - 1u);
+      v[j] = A[i];
+      g[j] = seg4[i % K4];
     }
 #pragma unroll
-    for (int j = 0; j < kAbsU; ++j) max4(v[j], g[j], mx0, mx1);
+    for (int j = 0; j < kAbsU; ++j) {
+      const bool ok = base + 256u * j < total4;
+      max4(ok ? v[j] : make_float4(0.f, 0.f, 0.f, 0.f), g[j], mx0, mx1);
+    }
   }
-  absmax_finish(mx0, mx1, ap, partial, counter, s_a, red, &is_last);
+  write_partial(mx0, mx1, red, partial);
 }
 
 // Any stride or width: one row at a time, scalar loads.
 __global__ __launch_bounds__(256) void k_absmax_rows(const float* __restrict__ A, int64_t M,
                                                      int64_t K, int64_t lda,
-                                                     const uint8_t* __restrict__ seg, ActPlan ap,
-                                                     float* __restrict__ partial,
-                                                     unsigned int* __restrict__ counter,
-                                                     float* __restrict__ s_a) {
+                                                     const uint8_t* __restrict__ seg,
+                                                     float* __restrict__ partial) {
   __shared__ float red[4];
-  __shared__ int is_last;
   float mx0 = 0.0f, mx1 = 0.0f;
   for (int64_t m = blockIdx.x; m < M; m += gridDim.x) {
     const float* row = A + m * lda;
@@ -331,159 +294,220 @@ __global__ __launch_bounds__(256) void k_absmax_rows(const float* __restrict__ A
       if (seg[k]) mx1 = fmaxf(mx1, a); else mx0 = fmaxf(mx0, a);
     }
   }
-  absmax_finish(mx0, mx1, ap, partial, counter, s_a, red, &is_last);
+  write_partial(mx0, mx1, red, partial);
 }
 
-// ------------------------------------------------------------ k_act_pack --
-// Codes of a block of rows, scattered to their group-ordered positions in
-// LDS, then assembled into packed words and stored 16 bytes at a time.
-__device__ __forceinline__ void pack_rows_from_lds(const uint32_t* codes32, int nrows,
-                                                   int64_t m0, const ActPlan& ap,
-                                                   uint8_t* __restrict__ packed) {
-  const int Kp4 = ap.Kp / 4;
+// Group scales from the partial maxima (every pack workgroup computes the
+// same values; workgroup 0 also stores them for the GEMM epilogue).
+__device__ __forceinline__ void scales_from_partials(const float* __restrict__ partial, int nparts,
+                                                     const ActPlan& ap, float* red, float& s0,
+                                                     float& s1, float* __restrict__ s_a_out) {
+  float r0 = 0.0f, r1 = 0.0f;
+  for (int b = threadIdx.x; b < nparts; b += blockDim.x) {
+    const float2 v = reinterpret_cast<const float2*>(partial)[b];
+    r0 = fmaxf(r0, v.x);
+    r1 = fmaxf(r1, v.y);
+  }
+  r0 = block_max(r0, red);
+  r1 = block_max(r1, red);
+  s0 = group_scale(r0, ap.q[0]);
+  s1 = ap.S == 2 ? group_scale(r1, ap.q[1]) : 0.0f;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    s_a_out[0] = s0;
+    s_a_out[1] = s1;
+  }
+}
+
+// Quantizer state of both activation groups.
+struct ActQ {
+  float s0, s1, rs0, rs1;
+  bool f0, f1;
+  QParam q0, q1;
+  int zp0, zp1;
+};
+
+__device__ __forceinline__ ActQ make_actq(const ActPlan& ap, float s0, float s1) {
+  ActQ a;
+  a.s0 = s0;
+  a.s1 = s1;
+  a.f0 = fast_ok(s0);
+  a.f1 = fast_ok(s1);
+  a.rs0 = a.f0 ? __builtin_amdgcn_rcpf(s0) : 0.0f;
+  a.rs1 = a.f1 ? __builtin_amdgcn_rcpf(s1) : 0.0f;
+  a.q0 = ap.q[0];
+  a.q1 = ap.q[1];
+  a.zp0 = ap.zp[0];
+  a.zp1 = ap.zp[1];
+  return a;
+}
+
+// Stored activation code of x in group g (code minus the group zero point).
+__device__ __forceinline__ uint8_t store_code(float x, int g, const ActQ& a) {
+  const int code = g ? quant_code(x, a.s1, a.rs1, a.f1, a.q1) - a.zp1
+                     : quant_code(x, a.s0, a.rs0, a.f0, a.q0) - a.zp0;
+  return (uint8_t)(int8_t)code;
+}
+
+// Write the units of `nrows` rows whose stored codes sit in LDS (row r at
+// codes + r*Kp) to rows m0.. of the packed activation buffer, one 2*c-byte
+// unit per store.  Used when a workgroup holds fewer than 16 rows.
+__device__ __forceinline__ void write_act_units(const uint8_t* codes, int nrows, int64_t m0,
+                                                const ActPlan& ap, uint8_t* __restrict__ packed) {
   for (int g = 0; g < ap.S; ++g) {
     const int c = g ? ap.c[1] : ap.c[0];
-    const int per = 32 / c;
-    const int nwords = (g ? ap.kpad[1] : ap.kpad[0]) / per;
-    const int64_t rb = g ? ap.row_bytes[1] : ap.row_bytes[0];
-    const int rquads = (int)(rb >> 4);
-    const int gbase = g ? ap.kpad[0] / 4 : 0;
+    const int ng = g ? ap.ng[1] : ap.ng[0];
+    const int gbase = g ? ap.kpad[0] : 0;
+    const int64_t mblk = g ? ap.mblk_bytes[1] : ap.mblk_bytes[0];
     uint8_t* dst0 = packed + (g ? ap.seg_off[1] : ap.seg_off[0]);
-    for (int u = threadIdx.x; u < nrows * rquads; u += blockDim.x) {
-      const int r = u / rquads, q = u - r * rquads;
-      const uint32_t* src = codes32 + r * Kp4 + gbase;
-      uint32_t w[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int wi = 4 * q + i;
-        w[i] = wi < nwords ? pack_word(src + wi * (per / 4), c) : 0u;
-      }
-      *reinterpret_cast<uint4*>(dst0 + (m0 + r) * rb + (int64_t)q * 16) =
-          make_uint4(w[0], w[1], w[2], w[3]);
+    const int per_row = ng * 4;
+    for (int u = threadIdx.x; u < nrows * per_row; u += blockDim.x) {
+      const int r = u / per_row, rest = u - r * per_row;
+      const int qg = rest >> 2, kg = rest & 3;
+      const int64_t m = m0 + r;
+      const uint4 d = *reinterpret_cast<const uint4*>(codes + (int64_t)r * ap.Kp + gbase + qg * kGran + kg * 16);
+      uint8_t* p = dst0 + (m / kBlk) * mblk + (int64_t)qg * 128 * c + (kg * 16 + (int)(m % kBlk)) * 2 * c;
+      store_unit(p, pack_unit(d.x, d.y, d.z, d.w, c), c);
     }
   }
 }
 
-// One workgroup per activation row.  Dynamic LDS: Kp bytes of stored codes.
-constexpr int kPackU = 4;
-__global__ __launch_bounds__(256) void k_act_pack(const float* __restrict__ A, int64_t K,
-                                                  int64_t lda, const int32_t* __restrict__ pos,
+// ------------------------------------------------------------ k_act_rows --
+// R activation rows per workgroup: reduce the partial maxima, quantize the
+// rows into LDS at their group-ordered positions, write their units.
+// Dynamic LDS: R*Kp bytes.
+constexpr int kPackU = 8;
+__global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, int64_t M,
+                                                  int64_t K, int64_t lda, int R,
+                                                  const int32_t* __restrict__ pos,
                                                   const uint8_t* __restrict__ seg, ActPlan ap,
-                                                  const float* __restrict__ s_a,
+                                                  const float* __restrict__ partial, int nparts,
+                                                  float* __restrict__ s_a_out,
                                                   uint8_t* __restrict__ packed, int vec4) {
   extern __shared__ __align__(16) uint8_t codes[];
-  const int64_t m = blockIdx.x;
+  __shared__ float red[4];
+  const int64_t m0 = (int64_t)blockIdx.x * R;
+  const int rows = (int)min((int64_t)R, M - m0);
   const int tid = threadIdx.x;
-  const float* row = A + m * lda;
-  const float s0 = s_a[0], s1 = s_a[1];
-  const QParam q0 = ap.q[0], q1 = ap.q[1];
-  const int zp0 = ap.zp[0], zp1 = ap.zp[1];
   uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
-  for (int i = tid; i < ap.Kp / 4; i += blockDim.x) codes32[i] = 0;
-  __syncthreads();
+  for (int i = tid; i < rows * ap.Kp / 4; i += blockDim.x) codes32[i] = 0;
+  float s0, s1;
+  scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
+  const ActQ aq = make_actq(ap, s0, s1);
   if (vec4) {
     const int K4 = (int)(K / 4);
-    const float4* row4 = reinterpret_cast<const float4*>(row);
-    for (int base = tid; base < K4; base += 256 * kPackU) {
+    const int total = rows * K4;
+    for (int base = tid; base < total; base += 256 * kPackU) {
       float4 v[kPackU];
       int4 p[kPackU];
       uchar4 g[kPackU];
+      int rr[kPackU];
 #pragma unroll
       for (int j = 0; j < kPackU; ++j) {
-        const int i = base + 256 * j;
-        if (i < K4) {
-          v[j] = row4[i];
-          p[j] = reinterpret_cast<const int4*>(pos)[i];
-          g[j] = reinterpret_cast<const uchar4*>(seg)[i];
-        }
+        const int i = min(base + 256 * j, total - 1);
+        const int r = i / K4, k4 = i - r * K4;
+        rr[j] = r;
+        v[j] = *reinterpret_cast<const float4*>(A + (m0 + r) * lda + 4 * k4);
+        p[j] = reinterpret_cast<const int4*>(pos)[k4];
+        g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
       }
 #pragma unroll
       for (int j = 0; j < kPackU; ++j) {
-        if (base + 256 * j < K4) {
-          codes[p[j].x] = store_code(v[j].x, g[j].x, s0, s1, q0, q1, zp0, zp1);
-          codes[p[j].y] = store_code(v[j].y, g[j].y, s0, s1, q0, q1, zp0, zp1);
-          codes[p[j].z] = store_code(v[j].z, g[j].z, s0, s1, q0, q1, zp0, zp1);
-          codes[p[j].w] = store_code(v[j].w, g[j].w, s0, s1, q0, q1, zp0, zp1);
+        if (base + 256 * j < total) {
+          uint8_t* row = codes + rr[j] * ap.Kp;
+          row[p[j].x] = store_code(v[j].x, g[j].x, aq);
+          row[p[j].y] = store_code(v[j].y, g[j].y, aq);
+          row[p[j].z] = store_code(v[j].z, g[j].z, aq);
+          row[p[j].w] = store_code(v[j].w, g[j].w, aq);
         }
       }
     }
   } else {
-    for (int64_t k = tid; k < K; k += blockDim.x)
-      codes[pos[k]] = store_code(row[k], seg[k], s0, s1, q0, q1, zp0, zp1);
+    for (int64_t i = tid; i < (int64_t)rows * K; i += blockDim.x) {
+      const int r = (int)(i / K);
+      const int64_t k = i - (int64_t)r * K;
+      codes[(int64_t)r * ap.Kp + pos[k]] = store_code(A[(m0 + r) * lda + k], seg[k], aq);
+    }
   }
   __syncthreads();
-  pack_rows_from_lds(codes32, 1, m, ap, packed);
+  write_act_units(codes, rows, m0, ap, packed);
 }
 
 // ----------------------------------------------------------- k_act_small --
-// Small batches (M * K <= kSmallElems, M * Kp <= 64 KB): one workgroup of
-// 1024 threads holds the whole batch in registers, reduces the group
-// maxima, quantizes and packs -- one pass over A, one launch.
-constexpr int kSmallU = 8;
-constexpr int kSmallThreads = 1024;
-constexpr int kSmallElems = kSmallThreads * kSmallU * 4;
+// Small batches (M <= 64, M*K <= kSmallElems, contiguous aligned rows): one
+// launch.  Every workgroup reduces the group maxima of the whole batch
+// itself (at most 256 KB, L2-resident after the first pass), then
+// quantizes and packs its own row.  Dynamic LDS: Kp bytes.
+constexpr int kSmallElems = 65536;
+constexpr int kSmallU = 4;
 
-__global__ __launch_bounds__(1024) void k_act_small(const float* __restrict__ A, int M, int K,
-                                                    int64_t lda, const int32_t* __restrict__ pos,
-                                                    const uint8_t* __restrict__ seg, ActPlan ap,
-                                                    float* __restrict__ s_a_out,
-                                                    uint8_t* __restrict__ packed) {
+__global__ __launch_bounds__(256) void k_act_small(const float* __restrict__ A, int M, int K,
+                                                   int64_t lda, const int32_t* __restrict__ pos,
+                                                   const uint8_t* __restrict__ seg, ActPlan ap,
+                                                   float* __restrict__ s_a_out,
+                                                   uint8_t* __restrict__ packed) {
   extern __shared__ __align__(16) uint8_t codes[];
-  __shared__ float red[16];
+  __shared__ float red[4];
   const int tid = threadIdx.x;
   const int K4 = K / 4;
   const int total4 = M * K4;
-  float4 v[kSmallU];
-  int4 p[kSmallU];
-  uchar4 g[kSmallU];
   float mx0 = 0.0f, mx1 = 0.0f;
+  for (int base = tid; base < total4; base += 256 * kSmallU) {
+    float4 v[kSmallU];
+    uchar4 g[kSmallU];
 #pragma unroll
-  for (int j = 0; j < kSmallU; ++j) {
-    const int i = tid + kSmallThreads * j;
-    if (i < total4) {
+    for (int j = 0; j < kSmallU; ++j) {
+      const int i = min(base + 256 * j, total4 - 1);  // repeats change no max
       const int m = i / K4, k4 = i - m * K4;
       v[j] = *reinterpret_cast<const float4*>(A + (int64_t)m * lda + 4 * k4);
-      p[j] = reinterpret_cast<const int4*>(pos)[k4];
       g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
-      max4(v[j], g[j], mx0, mx1);
     }
+#pragma unroll
+    for (int j = 0; j < kSmallU; ++j) max4(v[j], g[j], mx0, mx1);
   }
   uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
-  for (int i = tid; i < M * ap.Kp / 4; i += kSmallThreads) codes32[i] = 0;
+  for (int i = tid; i < ap.Kp / 4; i += 256) codes32[i] = 0;
   mx0 = block_max(mx0, red);
   mx1 = block_max(mx1, red);
   const float s0 = group_scale(mx0, ap.q[0]);
   const float s1 = ap.S == 2 ? group_scale(mx1, ap.q[1]) : 0.0f;
-  if (tid == 0) {
+  if (blockIdx.x == 0 && tid == 0) {
     s_a_out[0] = s0;
     s_a_out[1] = s1;
   }
-  const QParam q0 = ap.q[0], q1 = ap.q[1];
-  const int zp0 = ap.zp[0], zp1 = ap.zp[1];
+  const ActQ aq = make_actq(ap, s0, s1);
+  const int m = blockIdx.x;
+  const float* row = A + (int64_t)m * lda;
+  for (int base = tid; base < K4; base += 256 * kSmallU) {
+    float4 v[kSmallU];
+    int4 p[kSmallU];
+    uchar4 g[kSmallU];
 #pragma unroll
-  for (int j = 0; j < kSmallU; ++j) {
-    const int i = tid + kSmallThreads * j;
-    if (i < total4) {
-      uint8_t* row = codes + (i / K4) * ap.Kp;
-      row[p[j].x] = store_code(v[j].x, g[j].x, s0, s1, q0, q1, zp0, zp1);
-      row[p[j].y] = store_code(v[j].y, g[j].y, s0, s1, q0, q1, zp0, zp1);
-      row[p[j].z] = store_code(v[j].z, g[j].z, s0, s1, q0, q1, zp0, zp1);
-      row[p[j].w] = store_code(v[j].w, g[j].w, s0, s1, q0, q1, zp0, zp1);
+    for (int j = 0; j < kSmallU; ++j) {
+      const int k4 = min(base + 256 * j, K4 - 1);
+      v[j] = reinterpret_cast<const float4*>(row)[k4];
+      p[j] = reinterpret_cast<const int4*>(pos)[k4];
+      g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
+    }
+#pragma unroll
+    for (int j = 0; j < kSmallU; ++j) {
+      if (base + 256 * j < K4) {
+        codes[p[j].x] = store_code(v[j].x, g[j].x, aq);
+        codes[p[j].y] = store_code(v[j].y, g[j].y, aq);
+        codes[p[j].z] = store_code(v[j].z, g[j].z, aq);
+        codes[p[j].w] = store_code(v[j].w, g[j].w, aq);
+      }
     }
   }
   __syncthreads();
-  pack_rows_from_lds(codes32, M, 0, ap, packed);
+  write_act_units(codes, 1, m, ap, packed);
 }
 
-// ---------------------------------------------------------------- k_gemm --
+// ------------------------------------------------------------ GEMM/GEMV --
 struct GemmArgs {
   const uint8_t* act;
   const float* s_a;
   ActPlan ap;
-  const uint8_t* w;
-  const TileDesc* tiles;
-  const ColInfo* colinfo;
-  const uint8_t* shw;
+  WDev wd;
   WPlan wp;
   int64_t M, N;
   uint16_t* Y;
@@ -491,173 +515,314 @@ struct GemmArgs {
   int32_t* acc;
 };
 
-constexpr int kTK = 128;            // channels per LDS stage (two units)
-constexpr int kRowB = kTK;          // LDS bytes per tile row (int8)
-constexpr int kTileB = 128 * kRowB; // bytes of one operand tile in LDS
+// s_waitcnt immediate for vmcnt(n) (gfx9 encoding), expcnt/lgkmcnt untouched.
+#define SONIQ_VMCNT_IMM(n) (((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
 
-// 16-byte chunk `ch` of LDS row r, XOR-swizzled so that the 16 rows read by
-// one MFMA fragment spread over all banks.
-__device__ __forceinline__ int lds_off(int r, int ch) {
-  return r * kRowB + ((ch ^ ((r >> 1) & 7)) << 4);
+// Workgroup barrier without a memory fence: the LDS ring is filled by
+// direct loads whose completion each wave has already awaited with
+// wait_vmcnt; the compiler fences keep LDS accesses on their side.
+__device__ __forceinline__ void bar_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-template <int S>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-  __shared__ __align__(16) uint8_t lds[2][2][kTileB];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * 128;
-  const int n0 = blockIdx.x * 128;
-  const ActPlan& ap = a.ap;
-  const WPlan& wp = a.wp;
+// 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
+__device__ __forceinline__ void load_lds16(const uint8_t* src, uint8_t* lds_dst_uniform) {
+  __builtin_amdgcn_global_load_lds(
+      reinterpret_cast<const void*>(src),
+      reinterpret_cast<__attribute__((address_space(3))) void*>(
+          reinterpret_cast<uintptr_t>(lds_dst_uniform)),
+      16, 0, 0);
+}
 
-  // Stage list: group 0 stages, then group 1 stages.
-  const int ng0 = ap.kpad[0] / kGran;
-  const int ng1 = S == 2 ? ap.kpad[1] / kGran : 0;
-  const int ns0 = (ng0 + 1) / 2;
-  const int ns1 = (ng1 + 1) / 2;
-  const int nst = ns0 + ns1;
+template <int C>
+__device__ __forceinline__ v4i read_frag(const uint8_t* p, int lane) {
+  uint4 raw;
+  if constexpr (C == 8) {
+    raw = *reinterpret_cast<const uint4*>(p + lane * 16);
+  } else if constexpr (C == 4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p + lane * 8);
+    raw = make_uint4(v.x, v.y, 0u, 0u);
+  } else if constexpr (C == 2) {
+    raw = make_uint4(*reinterpret_cast<const uint32_t*>(p + lane * 4), 0u, 0u, 0u);
+  } else {
+    raw = make_uint4(*reinterpret_cast<const uint16_t*>(p + lane * 2), 0u, 0u, 0u);
+  }
+  const uint4 d = unpack_unit<C>(raw);
+  return v4i{(int)d.x, (int)d.y, (int)d.z, (int)d.w};
+}
 
-  // Loader roles: thread -> (tile row, unit within the stage).
-  const int lrow = tid >> 1, lq = tid & 1;
-  // Activation row pointer per group.
-  const uint8_t* arow0 = a.act + ap.seg_off[0] + (m0 + lrow) * ap.row_bytes[0];
-  const uint8_t* arow1 = a.act + ap.seg_off[1] + (m0 + lrow) * ap.row_bytes[1];
-  // Weight row pointer and container.
-  const int p = n0 + lrow;
-  const int t = p >> 6, j = p & 63;
-  bool wvalid = false;
-  int wc = 8;
-  const uint8_t* wrow = a.w;
-  if (t < wp.ntiles) {
-    TileDesc td = a.tiles[t];
-    if (j < td.n_rows) {
-      wvalid = true;
-      const bool lo = j < td.n_lo;
-      wc = lo ? wp.c_lo : wp.c_hi;
-      wrow = a.w + td.base +
-             (lo ? (int64_t)j * wp.rb_lo : (int64_t)td.n_lo * wp.rb_lo + (int64_t)(j - td.n_lo) * wp.rb_hi);
+__device__ __forceinline__ v4i read_frag_rt(const uint8_t* p, int lane, int c) {
+  if (c == 8) return read_frag<8>(p, lane);
+  if (c == 4) return read_frag<4>(p, lane);
+  if (c == 2) return read_frag<2>(p, lane);
+  return read_frag<1>(p, lane);
+}
+
+template <int CA>
+__device__ __forceinline__ v4i read_frag_a(const uint8_t* p, int lane, int c) {
+  if constexpr (CA != 0) return read_frag<CA>(p, lane);
+  else return read_frag_rt(p, lane, c);
+}
+
+// Weight-block fragment: the container is one of two per handle; CBL/CBH
+// fix them at compile time (0 = decided at run time).
+template <int CBL, int CBH>
+__device__ __forceinline__ v4i read_frag_w(const uint8_t* p, int lane, int c) {
+  if constexpr (CBL != 0 && CBL == CBH) {
+    return read_frag<CBL>(p, lane);
+  } else if constexpr (CBL != 0 && CBH != 0) {
+    if (c == CBL) return read_frag<CBL>(p, lane);
+    return read_frag<CBH>(p, lane);
+  } else {
+    return read_frag_rt(p, lane, c);
+  }
+}
+
+constexpr int kBSlot = 128 * 16 * 8;  // B stage bytes at c = 8 (8 blocks, 2 granules)
+constexpr int kLB = 4;                // B loads per stage (kBSlot / 4 KB)
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(SONIQ_VMCNT_IMM(N));
+}
+
+// One activation group's K loop of a BM x 128 tile (BM = 32*WFM; waves 2x2,
+// wave tile (16*WFM) x 64), through an NST-deep LDS ring.  Stage = 2
+// granules.  A stage in LDS: m-block i granule kk at (2i + kk)*128*ca; B
+// stage: block j at bpre[j]*16, granule kk at +kk*128*c_j.  Every wave
+// issues exactly WFM + kLB direct loads per stage (lanes past the data
+// re-load one valid chunk into an unused slot), so each wait is a
+// compile-time vmcnt.
+template <int CA, int CBL, int CBH, int WFM, int NST>
+__device__ __forceinline__ void gemm_group(uint8_t* lds, const uint8_t* abase, int64_t mstride,
+                                           int ca_rt, int ng, const uint8_t* wtile, int ngt,
+                                           const int (&bc)[8], const int (&bpre)[9], int qbase,
+                                           v4i (&acc)[WFM][4], int tid, int lane, int wid,
+                                           int wm, int wn) {
+  constexpr int BM = 32 * WFM;
+  constexpr int ASLOT = BM * 16 * 8;
+  constexpr int SLOT = ASLOT + kBSlot;
+  constexpr int L = WFM + kLB;
+  const int ca = CA ? CA : ca_rt;
+  const int ach = BM * ca;  // A chunks (16 B) per full stage
+  const int TB = bpre[8];
+  const int nst = (ng + 1) >> 1;
+
+  // Per-lane source offsets, fixed for the whole group: stage st adds
+  // st*256*ca (A, uniform) or st*256*c_j (B, per lane).
+  uint32_t aoff[WFM];
+#pragma unroll
+  for (int i = 0; i < WFM; ++i) {
+    const int ci = min(i * 256 + tid, ach - 1);
+    const int mb = ci / (16 * ca);
+    aoff[i] = (uint32_t)(mb * mstride + (ci - mb * 16 * ca) * 16);
+  }
+  uint32_t boffs[kLB], bstr[kLB];
+#pragma unroll
+  for (int i = 0; i < kLB; ++i) {
+    const int ci = min(i * 256 + tid, TB - 1);
+    int pj = 0, cj = bc[0];
+#pragma unroll
+    for (int t = 1; t < 8; ++t) {
+      const bool in = ci >= bpre[t];
+      pj += in ? bpre[t] - bpre[t - 1] : 0;
+      cj += in ? bc[t] - bc[t - 1] : 0;
     }
+    // Blocks are contiguous: block j starts ngt*128*(sum of earlier c) bytes in.
+    boffs[i] = (uint32_t)(ngt * 8 * pj + qbase * 128 * cj + (ci - pj) * 16);
+    bstr[i] = 256 * cj;
   }
 
-  Unit ra, rb;
-  bool va = false, vb = false;
-  int ca = 8;
-
-  auto stage_info = [&](int st, int& g, int& gi0, int& ngv) {
-    if (st < ns0) { g = 0; gi0 = 2 * st; ngv = min(2, ng0 - gi0); }
-    else { g = 1; gi0 = 2 * (st - ns0); ngv = min(2, ng1 - gi0); }
-  };
-  const int ca0 = ap.c[0], ca1 = ap.c[1], kp0 = ap.kpad[0];
-  auto gload = [&](int st) {
-    int g, gi0, ngv;
-    stage_info(st, g, gi0, ngv);
-    const int gi = gi0 + lq;
-    ca = g ? ca1 : ca0;
-    va = lq < ngv;
-    if (va) ra = load_unit((g ? arow1 : arow0) + (int64_t)gi * 8 * ca, ca);
-    vb = wvalid && lq < ngv;
-    if (vb) {
-      const int64_t e0 = (int64_t)(g ? kp0 : 0) + (int64_t)gi * kGran;
-      rb = load_unit(wrow + e0 * wc / 8, wc);
-    }
-  };
-  auto lwrite = [&](int buf) {
-    const Unit da = unpack_unit(ra, ca, va);
-    uint8_t* la = lds[buf][0];
-    *reinterpret_cast<uint4*>(la + lds_off(lrow, lq * 4 + 0)) = da.v0;
-    *reinterpret_cast<uint4*>(la + lds_off(lrow, lq * 4 + 1)) = da.v1;
-    *reinterpret_cast<uint4*>(la + lds_off(lrow, lq * 4 + 2)) = da.v2;
-    *reinterpret_cast<uint4*>(la + lds_off(lrow, lq * 4 + 3)) = da.v3;
-    const Unit db = unpack_unit(rb, wc, vb);
-    uint8_t* lb = lds[buf][1];
-    *reinterpret_cast<uint4*>(lb + lds_off(lrow, lq * 4 + 0)) = db.v0;
-    *reinterpret_cast<uint4*>(lb + lds_off(lrow, lq * 4 + 1)) = db.v1;
-    *reinterpret_cast<uint4*>(lb + lds_off(lrow, lq * 4 + 2)) = db.v2;
-    *reinterpret_cast<uint4*>(lb + lds_off(lrow, lq * 4 + 3)) = db.v3;
-  };
-
-  v4i acc0[4][4], acc1[4][4];
+  auto issue = [&](int st, int slot) {
+    uint8_t* As = lds + slot * SLOT;
+    uint8_t* Bs = As + ASLOT;
+    const uint8_t* ast = abase + (int64_t)st * 256 * ca;
+    if (2 * st + 1 < ng) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < WFM; ++i) load_lds16(ast + aoff[i], As + (i * 256 + wid * 64) * 16);
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      acc0[i][jj] = v4i{0, 0, 0, 0};
-      acc1[i][jj] = v4i{0, 0, 0, 0};
-    }
-
-  auto compute = [&](int buf, int ngv, v4i (&acc)[4][4]) {
-    const uint8_t* la = lds[buf][0];
-    const uint8_t* lb = lds[buf][1];
+      for (int i = 0; i < kLB; ++i)
+        load_lds16(wtile + boffs[i] + (uint32_t)st * bstr[i], Bs + (i * 256 + wid * 64) * 16);
+    } else {
+      // Final half stage: second-granule chunks re-load a first-granule chunk
+      // (same slot layout; those slots are never read as data).
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      if (kk < ngv) {
-        v4i af[4], bf[4];
-        const int ch = kk * 4 + (lane >> 4);
+      for (int i = 0; i < WFM; ++i) {
+        const int ci = min(i * 256 + tid, ach - 1);
+        const int mb = ci / (16 * ca);
+        const int off = ci - mb * 16 * ca;
+        load_lds16(ast + aoff[i] - (off >= 8 * ca ? 8 * ca * 16 : 0), As + (i * 256 + wid * 64) * 16);
+      }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          af[i] = *reinterpret_cast<const v4i*>(la + lds_off(wm * 64 + i * 16 + (lane & 15), ch));
+      for (int i = 0; i < kLB; ++i) {
+        const uint32_t cj = bstr[i] >> 8;
+        const int ci = min(i * 256 + tid, TB - 1);
+        int pj = 0;
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          bf[jj] = *reinterpret_cast<const v4i*>(lb + lds_off(wn * 64 + jj * 16 + (lane & 15), ch));
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-            acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[jj], acc[i][jj], 0, 0, 0);
+        for (int t = 1; t < 8; ++t) pj += ci >= bpre[t] ? bpre[t] - bpre[t - 1] : 0;
+        const int off = ci - pj;
+        load_lds16(wtile + boffs[i] + (uint32_t)st * bstr[i] - (off >= 8 * (int)cj ? 8 * cj * 16 : 0),
+                   Bs + (i * 256 + wid * 64) * 16);
       }
     }
   };
 
-  if (nst > 0) {
-    gload(0);
-    lwrite(0);
-  }
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) gload(st + 1);
-    int g, gi0, ngv;
-    stage_info(st, g, gi0, ngv);
-    if (S == 1 || g == 0) compute(st & 1, ngv, acc0);
-    else compute(st & 1, ngv, acc1);
-    if (st + 1 < nst) lwrite((st + 1) & 1);
-    __syncthreads();
+  // The wave's four weight blocks: LDS offset of this lane's unit in
+  // granule 0 of the stage, and the block's container (wave-uniform).
+  int wcj[4], wlo[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    wcj[jj] = __builtin_amdgcn_readfirstlane(wn ? bc[4 + jj] : bc[jj]);
+    wlo[jj] = (wn ? bpre[4 + jj] : bpre[jj]) * 16 + lane * 2 * wcj[jj];
   }
 
-  // Epilogue: exact int32 per group, fixed-order fp32 scaling, bf16.
+  int issued = 0;
+  for (; issued < NST - 1 && issued < nst; ++issued) issue(issued, issued);
+  for (int st = 0; st < nst; ++st) {
+    // Stages issued after st: at most NST - 2.
+    const int later = issued - st - 1;
+    if constexpr (NST >= 4) {
+      if (later >= 2) wait_vm<2 * L>();
+      else if (later == 1) wait_vm<L>();
+      else wait_vm<0>();
+    } else if constexpr (NST == 3) {
+      if (later >= 1) wait_vm<L>();
+      else wait_vm<0>();
+    } else {
+      wait_vm<0>();
+    }
+    bar_nofence();
+    if (issued < nst) {
+      issue(issued, issued % NST);
+      ++issued;
+    }
+    const int slot = st % NST;
+    const uint8_t* As = lds + slot * SLOT + lane * 2 * ca;
+    const uint8_t* Bs = lds + slot * SLOT + ASLOT;
+    // Both granules of the stage run unconditionally; in a final half stage
+    // the second granule's A fragments are zeroed, so its products vanish
+    // whatever its slot holds.
+    const bool second = 2 * st + 1 < ng;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      v4i af[WFM], bf[4];
+#pragma unroll
+      for (int i = 0; i < WFM; ++i) {
+        const v4i f = read_frag_a<CA>(As + ((wm * WFM + i) * 2 + kk) * 128 * ca, 0, ca);
+        af[i] = (kk == 0 || second) ? f : v4i{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        bf[jj] = read_frag_w<CBL, CBH>(Bs + wlo[jj] + kk * 128 * wcj[jj], 0, wcj[jj]);
+#pragma unroll
+      for (int i = 0; i < WFM; ++i)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[jj], acc[i][jj], 0, 0, 0);
+    }
+  }
+  // Everyone is done reading the ring before the next group refills it.
+  bar_nofence();
+}
+
+template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  constexpr int BM = 32 * WFM;
+  constexpr int SLOT = BM * 16 * 8 + kBSlot;
+  __shared__ __align__(16) uint8_t lds[NST * SLOT];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;
+  const ActPlan& ap = a.ap;
+  const int ntn = a.wp.Np / kGemmBN;
+  const int mt = blockIdx.x / ntn, nt = blockIdx.x - mt * ntn;
+  const int64_t m0 = (int64_t)mt * BM;
+  const int jb0 = nt * 8;
+
+  int bc[8], bpre[9];
+  bpre[0] = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    bc[j] = a.wd.blk_c[jb0 + j];
+    bpre[j + 1] = bpre[j] + 16 * bc[j];
+  }
+  const uint8_t* wtile = a.wd.packed + a.wd.blk_off[jb0];
+
+  v4i acc0[WFM][4];
+#pragma unroll
+  for (int i = 0; i < WFM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) acc0[i][jj] = v4i{0, 0, 0, 0};
+  gemm_group<CA0, CBL, CBH, WFM, NST>(lds, a.act + ap.seg_off[0] + (m0 / kBlk) * ap.mblk_bytes[0],
+                                      ap.mblk_bytes[0], ap.c[0], ap.ng[0], wtile, a.wp.ngt, bc,
+                                      bpre, 0, acc0, tid, lane, wid, wm, wn);
+  v4i acc1[WFM][4];
+#pragma unroll
+  for (int i = 0; i < WFM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) acc1[i][jj] = v4i{0, 0, 0, 0};
+  if constexpr (S == 2)
+    gemm_group<CA1, CBL, CBH, WFM, NST>(lds, a.act + ap.seg_off[1] + (m0 / kBlk) * ap.mblk_bytes[1],
+                                        ap.mblk_bytes[1], ap.c[1], ap.ng[1], wtile, a.wp.ngt, bc,
+                                        bpre, ap.ng[0], acc1, tid, lane, wid, wm, wn);
+
+  // Epilogue: exact int32 per group, fixed-order fp32 scaling, bf16.  The
+  // tile is staged in LDS (the ring is free: gemm_group ended with a
+  // barrier) with its columns in ascending original order, then stored so
+  // that consecutive lanes write consecutive output columns.
+  uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
+  static_assert(BM * kGemmBN * 2 <= NST * SLOT, "output staging fits the ring");
   const float sa0 = a.s_a[0];
   const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
-    const int pc = n0 + wn * 64 + jj * 16 + (lane & 15);
-    if (pc >= wp.Np) continue;
-    const ColInfo ci = a.colinfo[pc];
+    const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
+    const ColInfo ci = a.wd.colinfo[pc];
     if (ci.n < 0) continue;
-    const uint8_t shw = a.shw[pc];
+    const uint8_t shw = a.wd.shw[pc];
+    const int slot = a.wd.colrank[pc];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < WFM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
-        if (m >= a.M) continue;
+        const int row = (wm * WFM + i) * 16 + (lane >> 4) * 4 + r;
         const int t0 = true_acc(acc0[i][jj][r], ap.sh[0], ap.c[0], ap.padcnt[0], ap.zp[0], shw,
                                 ci.colsum[0]);
         const int t1 = S == 2 ? true_acc(acc1[i][jj][r], ap.sh[1], ap.c[1], ap.padcnt[1],
                                          ap.zp[1], shw, ci.colsum[1])
                               : 0;
-        a.Y[m * a.ldy + ci.n] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, ci.s_w));
+        ys[row * kGemmBN + slot] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, ci.s_w));
         if (a.acc) {
-          a.acc[m * a.N + ci.n] = t0;
-          if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
+          const int64_t m = m0 + row;
+          if (m < a.M) {
+            a.acc[m * a.N + ci.n] = t0;
+            if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
+          }
         }
       }
+  }
+  __syncthreads();
+  const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
+  if (n >= 0) {
+    for (int row = tid / kGemmBN; row < BM; row += 256 / kGemmBN) {
+      const int64_t m = m0 + row;
+      if (m < a.M) a.Y[m * a.ldy + n] = ys[row * kGemmBN + (tid & (kGemmBN - 1))];
+    }
   }
 }
 
 // ---------------------------------------------------------------- k_gemv --
-// Dot of NV*16 unpacked elements (k0 .. k0 + 16*NV) with every staged
-// activation row; the sum goes to the accumulator of the group of k0.
+// One workgroup (4 waves) per 16-row weight block.  The block's bytes are a
+// contiguous run of 16-byte chunks; wave w takes chunk rows i = w, w+4, ...
+// (64 chunks each).  A chunk of container C holds U = 8/C units that share
+// one granule and one 16-channel group and belong to U different rows, so
+// each lane keeps U row accumulators per activation group and row.
+constexpr int kGemvB = 8;  // chunk rows in flight per wave
+
 __device__ __forceinline__ int dot16(uint4 d, uint4 x, int v) {
   v = __builtin_amdgcn_sdot4((int)d.x, (int)x.x, v, false);
   v = __builtin_amdgcn_sdot4((int)d.y, (int)x.y, v, false);
@@ -665,152 +830,159 @@ __device__ __forceinline__ int dot16(uint4 d, uint4 x, int v) {
   return __builtin_amdgcn_sdot4((int)d.w, (int)x.w, v, false);
 }
 
-template <int NV, int MT>
-__device__ __forceinline__ void dot_rows(const Unit& d, int k0, const uint8_t* xs, int Kp,
-                                         int kp0, int M, int (&acc0)[MT], int (&acc1)[MT]) {
-  if (k0 >= Kp) return;
-  const bool g1 = k0 >= kp0;
+template <int C>
+__device__ __forceinline__ uint4 chunk_unit(uint4 raw, int u) {
+  if constexpr (C == 8) return raw;
+  else if constexpr (C == 4) return u == 0 ? unpack4(raw.x, raw.y) : unpack4(raw.z, raw.w);
+  else if constexpr (C == 2) {
+    const uint32_t w = u == 0 ? raw.x : u == 1 ? raw.y : u == 2 ? raw.z : raw.w;
+    return unpack2(w);
+  } else {
+    const uint32_t w = (u >> 1) == 0 ? raw.x : (u >> 1) == 1 ? raw.y : (u >> 1) == 2 ? raw.z : raw.w;
+    return unpack1((w >> (16 * (u & 1))) & 0xFFFFu);
+  }
+}
+
+// Unpack the activation rows (block 0 of the packed buffer) into LDS.
+__device__ __forceinline__ void gemv_stage_x(const GemmArgs& a, uint8_t* xs) {
+  const ActPlan& ap = a.ap;
+  const int M = (int)a.M, ngt = a.wp.ngt, ng0 = ap.ng[0];
+  for (int u = threadIdx.x; u < M * ngt * 4; u += blockDim.x) {
+    const int m = u / (ngt * 4), rest = u - m * ngt * 4;
+    const int q = rest >> 2, kg = rest & 3;
+    const bool g1 = q >= ng0;
+    const int qq = g1 ? q - ng0 : q;
+    const int c = g1 ? ap.c[1] : ap.c[0];
+    const uint8_t* src = a.act + (g1 ? ap.seg_off[1] : ap.seg_off[0]) + (int64_t)qq * 128 * c +
+                         (kg * 16 + m) * 2 * c;
+    *reinterpret_cast<uint4*>(xs + m * ap.Kp + q * kGran + kg * 16) =
+        unpack_unit_rt(load_unit(src, c), c);
+  }
+}
+
+template <int MT, int C>
+__device__ __forceinline__ void gemv_block(const GemmArgs& a, uint8_t* xs, int blk,
+                                           int (&red)[4][kBlk][2][8]) {
+  constexpr int U = 8 / C;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const ActPlan& ap = a.ap;
+  const int M = (int)a.M, Kp = ap.Kp, ng0 = ap.ng[0];
+  const uint8_t* base = a.wd.packed + a.wd.blk_off[blk];
+  const int nchunks = a.wp.ngt * 8 * C;
+  const int NI = (nchunks + 63) >> 6;
+  const int kg = ((U * lane) & 63) >> 4;
+  const int qoff = (U * lane) >> 6;
+
+  int acc0[U][MT], acc1[U][MT];
 #pragma unroll
-  for (int mm = 0; mm < MT; ++mm) {
-    if (mm < M) {
-      const uint4* x = reinterpret_cast<const uint4*>(xs + (int64_t)mm * Kp + k0);
-      int v = dot16(d.v0, x[0], 0);
-      if (NV > 1) v = dot16(d.v1, x[1], v);
-      if (NV > 2) {
-        v = dot16(d.v2, x[2], v);
-        v = dot16(d.v3, x[3], v);
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm) {
+      acc0[u][mm] = 0;
+      acc1[u][mm] = 0;
+    }
+
+  // The first batch of weight chunks is in flight while the activations are
+  // unpacked into LDS.
+  uint4 raw[kGemvB];
+  int i0 = wid;
+#pragma unroll
+  for (int b = 0; b < kGemvB; ++b) {
+    const int ci = min((i0 + 4 * b) * 64 + lane, nchunks - 1);
+    raw[b] = *reinterpret_cast<const uint4*>(base + (int64_t)ci * 16);
+  }
+  gemv_stage_x(a, xs);
+  __syncthreads();
+
+  for (; i0 < NI; i0 += 4 * kGemvB) {
+    if (i0 != wid) {
+#pragma unroll
+      for (int b = 0; b < kGemvB; ++b) {
+        const int ci = min((i0 + 4 * b) * 64 + lane, nchunks - 1);
+        raw[b] = *reinterpret_cast<const uint4*>(base + (int64_t)ci * 16);
       }
-      if (g1) acc1[mm] += v; else acc0[mm] += v;
+    }
+#pragma unroll
+    for (int b = 0; b < kGemvB; ++b) {
+      const int i = i0 + 4 * b;
+      if (i * 64 + lane < nchunks) {
+        const int q = U * i + qoff;
+        const int k0 = q * kGran + 16 * kg;
+        const bool g1 = q >= ng0;
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm) {
+          if (mm < M) {
+            const uint4 x = *reinterpret_cast<const uint4*>(xs + mm * Kp + k0);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+              const int v = dot16(chunk_unit<C>(raw[b], u), x, 0);
+              if (g1) acc1[u][mm] += v; else acc0[u][mm] += v;
+            }
+          }
+        }
+      }
+    }
+  }
+
+  // Lanes that share rows: equal lane mod (16/U).
+#pragma unroll
+  for (int o = 16 / U; o < 64; o <<= 1)
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) {
+        acc0[u][mm] += __shfl_xor(acc0[u][mm], o, 64);
+        acc1[u][mm] += __shfl_xor(acc1[u][mm], o, 64);
+      }
+
+  // Across the four waves, through LDS; then one thread per (row, m).
+  if (lane < 16 / U) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) {
+        red[wid][U * lane + u][0][mm] = acc0[u][mm];
+        red[wid][U * lane + u][1][mm] = acc1[u][mm];
+      }
+  }
+  __syncthreads();
+  if (tid < kBlk * M) {
+    const int r = tid / M, m = tid - r * M;
+    int s0 = 0, s1 = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      s0 += red[w][r][0][m];
+      s1 += red[w][r][1][m];
+    }
+    const int p = blk * kBlk + r;
+    const ColInfo ci = a.wd.colinfo[p];
+    if (ci.n >= 0) {
+      const uint8_t shw = a.wd.shw[p];
+      const int S = ap.S;
+      const int t0 = true_acc(s0, ap.sh[0], ap.c[0], ap.padcnt[0], ap.zp[0], shw, ci.colsum[0]);
+      const int t1 = S == 2 ? true_acc(s1, ap.sh[1], ap.c[1], ap.padcnt[1], ap.zp[1], shw, ci.colsum[1])
+                            : 0;
+      const float sa0 = a.s_a[0], sa1 = S == 2 ? a.s_a[1] : 0.0f;
+      a.Y[(int64_t)m * a.ldy + ci.n] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, ci.s_w));
+      if (a.acc) {
+        a.acc[(int64_t)m * a.N + ci.n] = t0;
+        if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
+      }
     }
   }
 }
 
-// Workgroup = 4 waves = 16 physical output rows; each row is streamed by 16
-// lanes with 128-bit loads.  Dynamic LDS: M * Kp bytes of unpacked
-// activations.
-constexpr int kGemvU = 8;  // weight chunks in flight per lane
-
+// Dynamic LDS: M * Kp bytes of unpacked activations.
 template <int MT>
 __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
   extern __shared__ __align__(16) uint8_t xs[];
-  const int tid = threadIdx.x;
-  const ActPlan& ap = a.ap;
-  const WPlan& wp = a.wp;
-  const int M = (int)a.M;
-  const int Kp = ap.Kp;
-  const int ng0 = ap.kpad[0] / kGran;
-  const int ngt = Kp / kGran;
-
-  // This lane's weight row (16 lanes per row, 4 rows per wave).
-  const int lane = tid & 63, wid = tid >> 6;
-  const int s = lane & 15;
-  const int p = blockIdx.x * kGemvRows + wid * 4 + (lane >> 4);
-  const int t = p >> 6, j = p & 63;
-  const TileDesc td = a.tiles[t];
-  const bool valid = j < td.n_rows;
-  const bool lo = j < td.n_lo;
-  const int c = lo ? wp.c_lo : wp.c_hi;
-  const uint8_t* row = a.w + td.base +
-                       (lo ? (int64_t)j * wp.rb_lo : (int64_t)td.n_lo * wp.rb_lo + (int64_t)(j - td.n_lo) * wp.rb_hi);
-  const int nch = valid ? (int)((lo ? wp.rb_lo : wp.rb_hi) >> 4) : 0;
-  const int kp0 = ap.kpad[0];
-
-  // First batch of weight chunks in flight before the activations are staged.
-  uint4 cur[kGemvU];
-#pragma unroll
-  for (int u = 0; u < kGemvU; ++u) {
-    const int ch = s + 16 * u;
-    cur[u] = ch < nch ? *reinterpret_cast<const uint4*>(row + (int64_t)ch * 16) : make_uint4(0, 0, 0, 0);
-  }
-
-  // Stage the activation rows, unpacked, in LDS.
-  for (int u = tid; u < M * ngt; u += blockDim.x) {
-    const int m = u / ngt, ga = u - m * ngt;
-    const bool g1 = ga >= ng0;
-    const int gi = g1 ? ga - ng0 : ga;
-    const int cx = g1 ? ap.c[1] : ap.c[0];
-    const int64_t off = g1 ? ap.seg_off[1] + (int64_t)m * ap.row_bytes[1]
-                           : ap.seg_off[0] + (int64_t)m * ap.row_bytes[0];
-    const Unit d = unpack_unit(load_unit(a.act + off + (int64_t)gi * 8 * cx, cx), cx, true);
-    uint4* dst = reinterpret_cast<uint4*>(xs + (int64_t)m * Kp + (int64_t)ga * kGran);
-    dst[0] = d.v0;
-    dst[1] = d.v1;
-    dst[2] = d.v2;
-    dst[3] = d.v3;
-  }
-  __syncthreads();
-
-  int acc0[MT], acc1[MT];
-#pragma unroll
-  for (int mm = 0; mm < MT; ++mm) { acc0[mm] = 0; acc1[mm] = 0; }
-
-  for (int base = s; base < nch; base += 16 * kGemvU) {
-    uint4 nxt[kGemvU];
-    const bool more = base + 16 * kGemvU < nch;
-    if (more) {
-#pragma unroll
-      for (int u = 0; u < kGemvU; ++u) {
-        const int ch = base + 16 * (kGemvU + u);
-        nxt[u] = ch < nch ? *reinterpret_cast<const uint4*>(row + (int64_t)ch * 16) : make_uint4(0, 0, 0, 0);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kGemvU; ++u) {
-      const int ch = base + 16 * u;
-      if (ch < nch) {
-        const uint4 v = cur[u];
-        Unit d;
-        if (c == 2) {
-          d.v0 = unpack2(v.x); d.v1 = unpack2(v.y); d.v2 = unpack2(v.z); d.v3 = unpack2(v.w);
-          dot_rows<4, MT>(d, ch * 64, xs, Kp, kp0, M, acc0, acc1);
-        } else if (c == 4) {
-          d.v0 = unpack4(v.x, v.y); d.v1 = unpack4(v.z, v.w);
-          dot_rows<2, MT>(d, ch * 32, xs, Kp, kp0, M, acc0, acc1);
-        } else if (c == 8) {
-          d.v0 = v;
-          dot_rows<1, MT>(d, ch * 16, xs, Kp, kp0, M, acc0, acc1);
-        } else {
-          d.v0 = unpack1_lo(v.x); d.v1 = unpack1_hi(v.x); d.v2 = unpack1_lo(v.y); d.v3 = unpack1_hi(v.y);
-          dot_rows<4, MT>(d, ch * 128, xs, Kp, kp0, M, acc0, acc1);
-          d.v0 = unpack1_lo(v.z); d.v1 = unpack1_hi(v.z); d.v2 = unpack1_lo(v.w); d.v3 = unpack1_hi(v.w);
-          dot_rows<4, MT>(d, ch * 128 + 64, xs, Kp, kp0, M, acc0, acc1);
-        }
-      }
-    }
-    if (more) {
-#pragma unroll
-      for (int u = 0; u < kGemvU; ++u) cur[u] = nxt[u];
-    }
-  }
-
-  // Sum over the 16 lanes of the row; every lane ends with the totals.
-#pragma unroll
-  for (int mm = 0; mm < MT; ++mm) {
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      acc0[mm] += __shfl_xor(acc0[mm], o, 16);
-      acc1[mm] += __shfl_xor(acc1[mm], o, 16);
-    }
-  }
-  if (!valid || s >= M) return;
-  const ColInfo ci = a.colinfo[p];
-  if (ci.n < 0) return;
-  int r0 = 0, r1 = 0;
-#pragma unroll
-  for (int mm = 0; mm < MT; ++mm)
-    if (mm == s) { r0 = acc0[mm]; r1 = acc1[mm]; }
-  const uint8_t shw = a.shw[p];
-  const int S = ap.S;
-  const int t0 = true_acc(r0, ap.sh[0], ap.c[0], ap.padcnt[0], ap.zp[0], shw, ci.colsum[0]);
-  const int t1 = S == 2 ? true_acc(r1, ap.sh[1], ap.c[1], ap.padcnt[1], ap.zp[1], shw, ci.colsum[1])
-                        : 0;
-  const float sa0 = a.s_a[0], sa1 = S == 2 ? a.s_a[1] : 0.0f;
-  const int64_t m = s;
-  a.Y[m * a.ldy + ci.n] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, ci.s_w));
-  if (a.acc) {
-    a.acc[m * a.N + ci.n] = t0;
-    if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
-  }
+  __shared__ int red[4][kBlk][2][8];
+  const int blk = blockIdx.x;
+  const int c = a.wd.blk_c[blk];
+  if (c == 2) gemv_block<MT, 2>(a, xs, blk, red);
+  else if (c == 4) gemv_block<MT, 4>(a, xs, blk, red);
+  else if (c == 8) gemv_block<MT, 8>(a, xs, blk, red);
+  else gemv_block<MT, 1>(a, xs, blk, red);
 }
 
 }  // namespace
@@ -818,15 +990,13 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
 // ------------------------------------------------------------- launchers --
 hipError_t launch_wpack(const float* W, int64_t N, int64_t K, int64_t ldw,
                         const uint8_t* w_bits_dev, const int32_t* pos_dev,
-                        const uint8_t* seg_dev, const int64_t* row_off_dev,
-                        const int32_t* phys_dev, QParam q_lo, QParam q_hi, int b_lo,
-                        int c_lo, int c_hi, int Kp, int kpad0, int64_t rb_lo,
-                        int64_t rb_hi, uint8_t* packed, ColInfo* colinfo,
+                        const uint8_t* seg_dev, const int32_t* phys_dev,
+                        const uint64_t* blk_off, const uint8_t* blk_c, QParam q_lo,
+                        QParam q_hi, int b_lo, int Kp, uint8_t* packed, ColInfo* colinfo,
                         hipStream_t stream) {
-  (void)kpad0;
   hipLaunchKernelGGL(k_wpack, dim3((unsigned)N), dim3(256), (size_t)Kp, stream, W, K, ldw,
-                     w_bits_dev, pos_dev, seg_dev, row_off_dev, phys_dev, q_lo, q_hi, b_lo,
-                     c_lo, c_hi, Kp, rb_lo, rb_hi, packed, colinfo);
+                     w_bits_dev, pos_dev, seg_dev, phys_dev, blk_off, blk_c, q_lo, q_hi, b_lo,
+                     Kp, packed, colinfo);
   return hipGetLastError();
 }
 
@@ -835,68 +1005,119 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const uint8_t* seg_dev, float* partial,
                             unsigned int* counter, float* s_a, uint8_t* packed,
                             hipStream_t stream) {
+  (void)counter;
   const bool aligned = (K % 4 == 0) && (lda % 4 == 0) &&
                        (reinterpret_cast<uintptr_t>(A) % 16 == 0);
-  if (aligned && M * K <= kSmallElems && M * (int64_t)ap.Kp <= 64 * 1024) {
-    hipLaunchKernelGGL(k_act_small, dim3(1), dim3(kSmallThreads), (size_t)(M * ap.Kp), stream, A,
+  if (aligned && M <= 64 && M * K <= kSmallElems) {
+    hipLaunchKernelGGL(k_act_small, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A,
                        (int)M, (int)K, lda, pos_dev, seg_dev, ap, s_a, packed);
     return hipGetLastError();
   }
+  int nparts;
   if (aligned && lda == K && M * K / 4 < (int64_t)UINT32_MAX) {
     const int64_t total4 = M * K / 4;
     int64_t blocks = (total4 + 256 * kAbsU - 1) / (256 * kAbsU);
     if (blocks > kAbsmaxBlocks) blocks = kAbsmaxBlocks;
+    nparts = (int)blocks;
     hipLaunchKernelGGL(k_absmax_flat, dim3((unsigned)blocks), dim3(256), 0, stream,
                        reinterpret_cast<const float4*>(A), (uint32_t)total4, (uint32_t)(K / 4),
-                       reinterpret_cast<const uchar4*>(seg_dev), ap, partial, counter, s_a);
+                       reinterpret_cast<const uchar4*>(seg_dev), partial);
   } else {
-    int64_t blocks = M < kAbsmaxBlocks ? M : kAbsmaxBlocks;
+    const int64_t blocks = M < kAbsmaxBlocks ? M : kAbsmaxBlocks;
+    nparts = (int)blocks;
     hipLaunchKernelGGL(k_absmax_rows, dim3((unsigned)blocks), dim3(256), 0, stream, A, M, K, lda,
-                       seg_dev, ap, partial, counter, s_a);
+                       seg_dev, partial);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_act_pack, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A, K,
-                     lda, pos_dev, seg_dev, ap, s_a, packed, aligned ? 1 : 0);
+  const int R = 4 * (int64_t)ap.Kp <= 64 * 1024 ? 4 : 1;
+  hipLaunchKernelGGL(k_act_rows, dim3((unsigned)((M + R - 1) / R)), dim3(256), (size_t)R * ap.Kp,
+                     stream, A, M, K, lda, R, pos_dev, seg_dev, ap, partial, nparts, s_a, packed,
+                     aligned ? 1 : 0);
   return hipGetLastError();
 }
 
 static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
-                          const uint8_t* w_packed, const TileDesc* tiles,
-                          const ColInfo* colinfo, const uint8_t* shw, const WPlan& wp,
-                          int64_t M, int64_t N, uint16_t* Y, int64_t ldy, int32_t* acc) {
+                          const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
+                          int64_t ldy, int32_t* acc) {
   GemmArgs a;
-  a.act = act_packed; a.s_a = s_a; a.ap = ap; a.w = w_packed; a.tiles = tiles;
-  a.colinfo = colinfo; a.shw = shw; a.wp = wp; a.M = M; a.N = N; a.Y = Y; a.ldy = ldy;
+  a.act = act_packed;
+  a.s_a = s_a;
+  a.ap = ap;
+  a.wd = wd;
+  a.wp = wp;
+  a.M = M;
+  a.N = N;
+  a.Y = Y;
+  a.ldy = ldy;
   a.acc = acc;
   return a;
 }
 
+// Tile shape: 0 = 256x128 (WFM 8, 3-deep ring), 1 = 128x128 (WFM 4, 3-deep),
+// 2 = 64x128 (WFM 2, 3-deep), 3 = 128x128 (WFM 4, 2-deep, two workgroups
+// per CU).
+template <int S, int CA0, int CA1, int CBL, int CBH>
+static void launch_gemm_t(const GemmArgs& a, int64_t M, int shape, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  const dim3 blk(256);
+  switch (shape) {
+    case 0:
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 8, 3>), dim3((unsigned)(((M + 255) / 256) * ntn)), blk, 0, stream, a);
+      break;
+    case 1:
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 4, 3>), dim3((unsigned)(((M + 127) / 128) * ntn)), blk, 0, stream, a);
+      break;
+    case 3:
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 4, 2>), dim3((unsigned)(((M + 127) / 128) * ntn)), blk, 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 3>), dim3((unsigned)(((M + 63) / 64) * ntn)), blk, 0, stream, a);
+      break;
+  }
+}
+
+static int gemm_shape(int64_t M, int ntn) {
+  if (const char* e = getenv("SONIQ_GEMM_SHAPE")) return atoi(e);
+  // 128x128 tiles, two workgroups per CU, when there are enough of them to
+  // fill the chip twice; otherwise 64x128 tiles for more workgroups.
+  if (((M + 127) / 128) * ntn >= 512) return 3;
+  return 2;
+}
+
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
-                          const uint8_t* w_packed, const TileDesc* tiles,
-                          const ColInfo* colinfo, const uint8_t* shw, const WPlan& wp,
-                          int64_t M, int64_t N, uint16_t* Y, int64_t ldy, int32_t* acc,
-                          hipStream_t stream) {
-  GemmArgs a = make_args(act_packed, s_a, ap, w_packed, tiles, colinfo, shw, wp, M, N, Y, ldy, acc);
-  dim3 grid((unsigned)((wp.Np + 127) / 128), (unsigned)((M + 127) / 128));
-  if (ap.S == 2)
-    hipLaunchKernelGGL(k_gemm<2>, grid, dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(k_gemm<1>, grid, dim3(256), 0, stream, a);
+                          const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
+                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
+  const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  const int shape = gemm_shape(M, wp.Np / kGemmBN);
+  const int ca0 = ap.c[0], ca1 = ap.S == 2 ? ap.c[1] : 0;
+  const int cl = wp.c_lo, ch = wp.c_hi;
+  if (ap.S == 2 && ca0 == 4 && ca1 == 8) {
+    if (cl == 4 && ch == 8) launch_gemm_t<2, 4, 8, 4, 8>(a, M, shape, stream);
+    else if (cl == 2 && ch == 8) launch_gemm_t<2, 4, 8, 2, 8>(a, M, shape, stream);
+    else if (cl == 1 && ch == 4) launch_gemm_t<2, 4, 8, 1, 4>(a, M, shape, stream);
+    else if (cl == 2 && ch == 4) launch_gemm_t<2, 4, 8, 2, 4>(a, M, shape, stream);
+    else launch_gemm_t<2, 4, 8, 0, 0>(a, M, shape, stream);
+  } else if (ap.S == 2) {
+    launch_gemm_t<2, 0, 0, 0, 0>(a, M, shape, stream);
+  } else {
+    launch_gemm_t<1, 0, 0, 0, 0>(a, M, shape, stream);
+  }
   return hipGetLastError();
 }
 
-bool gemv_fits(int64_t M, int Kp) {
-  return M >= 1 && M <= kGemvMaxM && M * (int64_t)Kp <= 64 * 1024;
+bool gemv_fits(int64_t M, const ActPlan& ap, const WPlan& wp) {
+  if (M < 1 || M > 8 || M * (int64_t)ap.Kp > 64 * 1024) return false;
+  // 1-bit weight blocks keep 8 rows per lane: at most 4 activation rows.
+  if ((wp.c_lo == 1 || wp.c_hi == 1) && M > 4) return false;
+  return true;
 }
 
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
-                          const uint8_t* w_packed, const TileDesc* tiles,
-                          const ColInfo* colinfo, const uint8_t* shw, const WPlan& wp,
-                          int64_t M, int64_t N, uint16_t* Y, int64_t ldy, int32_t* acc,
-                          hipStream_t stream) {
-  GemmArgs a = make_args(act_packed, s_a, ap, w_packed, tiles, colinfo, shw, wp, M, N, Y, ldy, acc);
-  dim3 grid((unsigned)(wp.Np / kGemvRows));
+                          const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
+                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
+  const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  dim3 grid((unsigned)wp.nblk);
   const size_t lds = (size_t)M * ap.Kp;
   if (M == 1)
     hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
