@@ -22,6 +22,8 @@
 // width).
 #include "soniq_internal.h"
 
+#include <hip/hip_bf16.h>
+
 #include <cstdlib>
 
 namespace soniq {
@@ -320,32 +322,48 @@ __device__ __forceinline__ void scales_from_partials(const float* __restrict__ p
 
 // Quantizer state of both activation groups.
 struct ActQ {
-  float s0, s1, rs0, rs1;
-  bool f0, f1;
-  QParam q0, q1;
-  int zp0, zp1;
+  float s[2], rs[2], lo[2], hi[2];
+  int zp[2];
+  bool fast[2], sign1[2];
 };
 
 __device__ __forceinline__ ActQ make_actq(const ActPlan& ap, float s0, float s1) {
   ActQ a;
-  a.s0 = s0;
-  a.s1 = s1;
-  a.f0 = fast_ok(s0);
-  a.f1 = fast_ok(s1);
-  a.rs0 = a.f0 ? __builtin_amdgcn_rcpf(s0) : 0.0f;
-  a.rs1 = a.f1 ? __builtin_amdgcn_rcpf(s1) : 0.0f;
-  a.q0 = ap.q[0];
-  a.q1 = ap.q[1];
-  a.zp0 = ap.zp[0];
-  a.zp1 = ap.zp[1];
+  const float sv[2] = {s0, s1};
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    const QParam& q = g ? ap.q[1] : ap.q[0];
+    a.s[g] = sv[g];
+    a.fast[g] = fast_ok(sv[g]);
+    a.rs[g] = a.fast[g] ? __builtin_amdgcn_rcpf(sv[g]) : 0.0f;
+    a.lo[g] = (float)q.lo;
+    a.hi[g] = (float)q.hi;
+    a.zp[g] = g ? ap.zp[1] : ap.zp[0];
+    a.sign1[g] = q.sign1 != 0;
+  }
   return a;
 }
 
-// Stored activation code of x in group g (code minus the group zero point).
+// Stored activation code of x in group g (code minus the group zero
+// point): the group's parameters are selected first, then one quantizer
+// runs (see quant_code for the reciprocal fast path).
 __device__ __forceinline__ uint8_t store_code(float x, int g, const ActQ& a) {
-  const int code = g ? quant_code(x, a.s1, a.rs1, a.f1, a.q1) - a.zp1
-                     : quant_code(x, a.s0, a.rs0, a.f0, a.q0) - a.zp0;
-  return (uint8_t)(int8_t)code;
+  const float s = g ? a.s[1] : a.s[0];
+  const float rs = g ? a.rs[1] : a.rs[0];
+  const bool fast = g ? a.fast[1] : a.fast[0];
+  int code;
+  if (g ? a.sign1[1] : a.sign1[0]) {
+    code = x < 0.0f ? -1 : 1;
+  } else if (s == 0.0f) {
+    code = 0;
+  } else {
+    const float e = x * rs;
+    float t = __builtin_rintf(e);
+    if (!fast || fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f) t = __builtin_rintf(__fdiv_rn(x, s));
+    t = fminf(fmaxf(t, g ? a.lo[1] : a.lo[0]), g ? a.hi[1] : a.hi[0]);
+    code = (int)t;
+  }
+  return (uint8_t)(int8_t)(code - (g ? a.zp[1] : a.zp[0]));
 }
 
 // Write the units of `nrows` rows whose stored codes sit in LDS (row r at
@@ -375,9 +393,10 @@ __device__ __forceinline__ void write_act_units(const uint8_t* codes, int nrows,
 // R activation rows per workgroup: reduce the partial maxima, quantize the
 // rows into LDS at their group-ordered positions, write their units.
 // Dynamic LDS: R*Kp bytes.
-constexpr int kPackU = 8;
+constexpr int kPackJ = 2;  // float4 positions per thread per pass
+template <int R>
 __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, int64_t M,
-                                                  int64_t K, int64_t lda, int R,
+                                                  int64_t K, int64_t lda,
                                                   const int32_t* __restrict__ pos,
                                                   const uint8_t* __restrict__ seg, ActPlan ap,
                                                   const float* __restrict__ partial, int nparts,
@@ -394,30 +413,37 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
   scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
   const ActQ aq = make_actq(ap, s0, s1);
   if (vec4) {
+    // Each thread owns float4 positions k4 = tid + 256*j for every row of
+    // the workgroup: one position/group lookup serves all rows.
     const int K4 = (int)(K / 4);
-    const int total = rows * K4;
-    for (int base = tid; base < total; base += 256 * kPackU) {
-      float4 v[kPackU];
-      int4 p[kPackU];
-      uchar4 g[kPackU];
-      int rr[kPackU];
+    for (int base = tid; base < K4; base += 256 * kPackJ) {
+      int4 p[kPackJ];
+      uchar4 g[kPackJ];
+      float4 v[R][kPackJ];
 #pragma unroll
-      for (int j = 0; j < kPackU; ++j) {
-        const int i = min(base + 256 * j, total - 1);
-        const int r = i / K4, k4 = i - r * K4;
-        rr[j] = r;
-        v[j] = *reinterpret_cast<const float4*>(A + (m0 + r) * lda + 4 * k4);
+      for (int j = 0; j < kPackJ; ++j) {
+        const int k4 = min(base + 256 * j, K4 - 1);
         p[j] = reinterpret_cast<const int4*>(pos)[k4];
         g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int rc = min(r, rows - 1);
+          v[r][j] = *reinterpret_cast<const float4*>(A + (m0 + rc) * lda + 4 * k4);
+        }
       }
 #pragma unroll
-      for (int j = 0; j < kPackU; ++j) {
-        if (base + 256 * j < total) {
-          uint8_t* row = codes + rr[j] * ap.Kp;
-          row[p[j].x] = store_code(v[j].x, g[j].x, aq);
-          row[p[j].y] = store_code(v[j].y, g[j].y, aq);
-          row[p[j].z] = store_code(v[j].z, g[j].z, aq);
-          row[p[j].w] = store_code(v[j].w, g[j].w, aq);
+      for (int j = 0; j < kPackJ; ++j) {
+        if (base + 256 * j < K4) {
+#pragma unroll
+          for (int r = 0; r < R; ++r) {
+            if (r < rows) {
+              uint8_t* row = codes + r * ap.Kp;
+              row[p[j].x] = store_code(v[r][j].x, g[j].x, aq);
+              row[p[j].y] = store_code(v[r][j].y, g[j].y, aq);
+              row[p[j].z] = store_code(v[r][j].z, g[j].z, aq);
+              row[p[j].w] = store_code(v[r][j].w, g[j].w, aq);
+            }
+          }
         }
       }
     }
@@ -773,9 +799,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   // Epilogue: exact int32 per group, fixed-order fp32 scaling, bf16.  The
   // tile is staged in LDS (the ring is free: gemm_group ended with a
   // barrier) with its columns in ascending original order, then stored so
-  // that consecutive lanes write consecutive output columns.
+  // that consecutive lanes write consecutive output columns.  Staging rows
+  // are padded by 8 halfwords so the four row quads of a wave's store land
+  // in different banks.
+  constexpr int YS = kGemmBN + 8;
   uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
-  static_assert(BM * kGemmBN * 2 <= NST * SLOT, "output staging fits the ring");
+  static_assert(BM * YS * 2 <= NST * SLOT, "output staging fits the ring");
   const float sa0 = a.s_a[0];
   const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
 #pragma unroll
@@ -783,35 +812,53 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
     const ColInfo ci = a.wd.colinfo[pc];
     if (ci.n < 0) continue;
+    // Exact accumulator of group g: (raw >> sh_g) + add_g, where add_g folds
+    // the zero-point term and the sign x sign padding products (padcnt
+    // products of +1 each, exact multiples of 2^sh_g in the raw sum).
     const uint8_t shw = a.wd.shw[pc];
-    const int slot = a.wd.colrank[pc];
+    const bool sgn = (shw & kShwSign) != 0;
+    const int sh0 = ap.sh[0] + (shw & 0x7F);
+    const int add0 = ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
+    const int sh1 = ap.sh[1] + (shw & 0x7F);
+    const int add1 = ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0);
+    uint16_t* ycol = ys + a.wd.colrank[pc];
 #pragma unroll
-    for (int i = 0; i < WFM; ++i)
+    for (int i = 0; i < WFM; ++i) {
+      const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = (wm * WFM + i) * 16 + (lane >> 4) * 4 + r;
-        const int t0 = true_acc(acc0[i][jj][r], ap.sh[0], ap.c[0], ap.padcnt[0], ap.zp[0], shw,
-                                ci.colsum[0]);
-        const int t1 = S == 2 ? true_acc(acc1[i][jj][r], ap.sh[1], ap.c[1], ap.padcnt[1],
-                                         ap.zp[1], shw, ci.colsum[1])
-                              : 0;
-        ys[row * kGemmBN + slot] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, ci.s_w));
+      for (int r = 0; r < 4; r += 2) {
+        int t0[2], t1[2];
+        float y[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          t0[h] = (acc0[i][jj][r + h] >> sh0) + add0;
+          t1[h] = S == 2 ? (acc1[i][jj][r + h] >> sh1) + add1 : 0;
+          y[h] = epilogue(t0[h], t1[h], S, sa0, sa1, ci.s_w);
+        }
+        // v_cvt_pk_bf16_f32: round to nearest even, as bf16_rne.
+        const __hip_bfloat162 pr = __float22bfloat162_rn(make_float2(y[0], y[1]));
+        ycol[(row0 + r) * YS] = __builtin_bit_cast(uint16_t, pr.x);
+        ycol[(row0 + r + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
         if (a.acc) {
-          const int64_t m = m0 + row;
-          if (m < a.M) {
-            a.acc[m * a.N + ci.n] = t0;
-            if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int64_t m = m0 + row0 + r + h;
+            if (m < a.M) {
+              a.acc[m * a.N + ci.n] = t0[h];
+              if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1[h];
+            }
           }
         }
       }
+    }
   }
   __syncthreads();
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
-    for (int row = tid / kGemmBN; row < BM; row += 256 / kGemmBN) {
-      const int64_t m = m0 + row;
-      if (m < a.M) a.Y[m * a.ldy + n] = ys[row * kGemmBN + (tid & (kGemmBN - 1))];
-    }
+    const int mrem = (int)min((int64_t)BM, a.M - m0);
+    uint16_t* yout = a.Y + m0 * a.ldy + n;
+    for (int row = tid / kGemmBN; row < mrem; row += 256 / kGemmBN)
+      yout[(int64_t)row * a.ldy] = ys[row * YS + (tid & (kGemmBN - 1))];
   }
 }
 
@@ -1030,10 +1077,15 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int R = 4 * (int64_t)ap.Kp <= 64 * 1024 ? 4 : 1;
-  hipLaunchKernelGGL(k_act_rows, dim3((unsigned)((M + R - 1) / R)), dim3(256), (size_t)R * ap.Kp,
-                     stream, A, M, K, lda, R, pos_dev, seg_dev, ap, partial, nparts, s_a, packed,
-                     aligned ? 1 : 0);
+  if (4 * (int64_t)ap.Kp <= 64 * 1024) {
+    hipLaunchKernelGGL(k_act_rows<4>, dim3((unsigned)((M + 3) / 4)), dim3(256),
+                       (size_t)4 * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,
+                       nparts, s_a, packed, aligned ? 1 : 0);
+  } else {
+    hipLaunchKernelGGL(k_act_rows<1>, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A, M,
+                       K, lda, pos_dev, seg_dev, ap, partial, nparts, s_a, packed,
+                       aligned ? 1 : 0);
+  }
   return hipGetLastError();
 }
 
