@@ -1,18 +1,26 @@
 """Benchmark of the SONIQ mixed-precision quantized GEMM on one MI355X.
 
-One step = the whole per-call hot path on one batch: quantize + permute +
-pack the fp32 activations (soniq_quantize_act) and the packed x packed
-integer MAC with the bf16 epilogue (soniq_mp_gemm).  Weights are packed once
+One step = the whole per-call hot path on one batch: quantize, permute and
+pack the fp32 activations (soniq_quantize_act), then the packed x packed
+integer MAC with the bf16 epilogue (soniq_mp_gemm).  Weights are packed
 before timing (they are static per layer); their packing time is reported
-separately.  Inputs are resident in HBM before timing starts; the fp32
-activation batch rotates over enough distinct copies that every step reads
-it from HBM rather than from the 256 MB Infinity Cache.
+separately.  Inputs are resident in HBM when timing starts.  Both operands
+rotate over distinct copies (fp32 activations up to 512 MB, packed weights
+up to 1 GiB), so every step reads them from HBM rather than from the 256 MB
+Infinity Cache, as a layer of a real network would.
 
-Prints one JSON line.  `value` is TOPS (2*M*N*K integer ops per step).
+Prints one JSON line.  `value` is TOPS: 2*M*N*K integer ops per step over
+the whole step.  `roofline` covers the dominant kernel of a step, timed with
+HIP events on the stream it runs on.  `cpu_baseline` is the CPU oracle on a
+bounded sample of the same workload.
+
+`--copy-calibration` instead runs a plain 1 GiB device copy, whose
+FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic figures.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -26,24 +34,38 @@ sys.path.insert(0, ROOT)
 
 METRIC = "mixed-precision GEMM TOPS & GEMV HBM GB/s (1 MI355X); speedup vs bf16 GEMM"
 DEFAULT_WORKLOAD = "conv3x3_im2col"
-HBM_PEAK_GBS = 8000.0
-INT8_PEAK_TOPS = 5000.0
-ROTATE_BYTES = 512 << 20
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E
+INT8_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA
+ROTATE_A_BYTES = 512 << 20
+ROTATE_W_BYTES = 1 << 30
+MAX_W_COPIES = 96
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2311_14114_amd", "csrc", "soniq_kernels.hip")
+
+
+def container(b: int) -> int:
+    return 1 if b <= 1 else 2 if b <= 2 else 4 if b <= 4 else 8
 
 
 def algorithmic(case, info):
-    """Algorithmic bytes and ops of one step (no padding, no debug dumps)."""
+    """Algorithmic bytes and ops of one step: no padding, no debug dumps."""
     M, N, K = case["M"], case["N"], case["K"]
     ab = case["a_bits"]
-    cont = lambda b: 1 if b <= 1 else 2 if b <= 2 else 4 if b <= 4 else 8
-    act_packed = sum(M * int((ab == b).sum()) * cont(int(b)) // 8 for b in np.unique(ab))
+    act_packed = sum(M * int((ab == b).sum()) * container(int(b)) // 8 for b in np.unique(ab))
+    S = len(np.unique(ab))
     return dict(
         ops=2 * M * N * K,
         a_fp32=M * K * 4,
         a_packed=act_packed,
         w_packed=int(info.packed_w_bytes_algorithmic),
+        # per output channel: scale and one code sum per activation group
+        w_side=N * (4 + 4 * S),
         y=M * N * 2,
     )
+
+
+def uses_gemv(case) -> bool:
+    return case["M"] <= 8
 
 
 def run_gpu(case, steps, warmup, rotate=True):
@@ -53,24 +75,35 @@ def run_gpu(case, steps, warmup, rotate=True):
     torch.cuda.set_device(0)
     dev = torch.device("cuda")
     M, N, K = case["M"], case["N"], case["K"]
+    stream = torch.cuda.current_stream()
     W = torch.from_numpy(case["W"]).to(dev)
     A0 = torch.from_numpy(case["A"]).to(dev)
-    nrot = max(1, min(8, math.ceil(ROTATE_BYTES / A0.numel() / 4))) if rotate else 1
-    As = [A0] + [A0.clone() for _ in range(nrot - 1)]
-    stream = torch.cuda.current_stream()
 
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
-    w = sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"])
+    ws = [sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"])]
     e1.record(stream)
     torch.cuda.synchronize()
     pack_ms = e0.elapsed_time(e1)
-    act = sq.soniq_act_create(w, M)
+    info = ws[0].info
+    nw = 1
+    if rotate:
+        nw = max(1, min(MAX_W_COPIES, math.ceil(ROTATE_W_BYTES / int(info.packed_w_bytes))))
+    for _ in range(nw - 1):
+        ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"]))
+    acts = [sq.soniq_act_create(w, M) for w in ws]
+    na = max(1, min(8, math.ceil(ROTATE_A_BYTES / (A0.numel() * 4)))) if rotate else 1
+    As = [A0] + [A0.clone() for _ in range(na - 1)]
     Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
 
+    def step(i):
+        act = acts[i % nw]
+        sq.soniq_quantize_act(act, As[i % na])
+        return act, ws[i % nw]
+
     for i in range(warmup):
-        sq.soniq_quantize_act(act, As[i % nrot])
+        act, w = step(i)
         sq.soniq_mp_gemm(act, w, out=Y)
     torch.cuda.synchronize()
 
@@ -81,7 +114,7 @@ def run_gpu(case, steps, warmup, rotate=True):
     start.record(stream)
     for i in range(steps):
         evs[i][0].record(stream)
-        sq.soniq_quantize_act(act, As[i % nrot])
+        act, w = step(i)
         evs[i][1].record(stream)
         sq.soniq_mp_gemm(act, w, out=Y)
         evs[i][2].record(stream)
@@ -91,57 +124,140 @@ def run_gpu(case, steps, warmup, rotate=True):
     total_ms = start.elapsed_time(end)
     q_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    del acts, ws
 
-    # bf16 comparator: torch's GEMM (hipBLASLt) on the same shapes, same protocol
+    # bf16 comparator: torch's GEMM (hipBLASLt) on the same shapes, the same
+    # protocol, operands rotated the same way.
     Ab = [a.to(torch.bfloat16) for a in As]
-    Wb = W.to(torch.bfloat16)
+    nwb = max(1, min(nw, math.ceil(ROTATE_W_BYTES / (N * K * 2))))
+    Wb = [W.to(torch.bfloat16) for _ in range(nwb)]
     for i in range(warmup):
-        torch.nn.functional.linear(Ab[i % nrot], Wb)
+        torch.nn.functional.linear(Ab[i % na], Wb[i % nwb])
     torch.cuda.synchronize()
     s2, t2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s2.record(stream)
     for i in range(steps):
-        torch.nn.functional.linear(Ab[i % nrot], Wb)
+        torch.nn.functional.linear(Ab[i % na], Wb[i % nwb])
     t2.record(stream)
     torch.cuda.synchronize()
     bf16_ms = s2.elapsed_time(t2) / steps
-    info = w.info
     del Ab, Wb
     return dict(total_ms=total_ms, wall_s=wall, q_ms=q_ms, g_ms=g_ms, pack_ms=pack_ms,
-                bf16_ms=bf16_ms, info=info, nrot=nrot,
-                gemm_kernel="k_gemv" if (M <= 8) else "k_gemm")
+                bf16_ms=bf16_ms, info=info, na=na, nw=nw)
 
 
-def cpu_baseline(case, budget_s=10.0):
-    """The oracle as it stands (plain C + OpenMP) on the same workload."""
+def source_digest() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    it is missing or was taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    digest = source_digest()
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            kv = dict(t.split("=", 1) for t in line.split() if "=" in t)
+            if kv.get("kernel") == kernel and kv.get("workload") == workload:
+                if kv.get("source") != digest:
+                    return None
+                return int(float(kv["traffic_bytes"]))
+    return None
+
+
+def roofline(case, alg, r):
+    """Roofline of the dominant kernel of one step."""
+    if r["q_ms"] >= r["g_ms"]:
+        kernel = "soniq_quantize_act"
+        byt = alg["a_fp32"] + alg["a_packed"]
+        t = r["q_ms"] * 1e-3
+        ach = byt / t / 1e9
+        return dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=ach / HBM_PEAK_GBS, traffic=measured_traffic(kernel, case["name"]),
+                    kernel=kernel, algorithmic_bytes=byt, launch_us=t * 1e6)
+    t = r["g_ms"] * 1e-3
+    byt = alg["a_packed"] + alg["w_packed"] + alg["w_side"] + alg["y"]
+    kernel = "k_gemv" if uses_gemv(case) else "k_gemm"
+    traffic = measured_traffic(kernel, case["name"])
+    # the bound is whichever resource needs longer at its peak
+    if uses_gemv(case) or byt / (HBM_PEAK_GBS * 1e9) >= alg["ops"] / (INT8_PEAK_TOPS * 1e12):
+        ach = byt / t / 1e9
+        return dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=ach / HBM_PEAK_GBS, traffic=traffic, kernel=kernel,
+                    algorithmic_bytes=byt, launch_us=t * 1e6)
+    ach = alg["ops"] / t / 1e12
+    return dict(bound="mfma", achieved=ach, peak=INT8_PEAK_TOPS, unit="TFLOP/s",
+                frac=ach / INT8_PEAK_TOPS, traffic=traffic, kernel=kernel,
+                algorithmic_ops=alg["ops"], launch_us=t * 1e6)
+
+
+def cpu_baseline(case, budget_s=12.0):
+    """The CPU oracle, as it stands, on a bounded sample of the workload: the
+    weights are quantized once, untimed (as the GPU packs them once); each
+    timed run quantizes the first `rows` activation rows, runs the integer
+    MAC and the epilogue.  Rows grow until one run takes about a second."""
     import oracle
     oracle.lib()
-    reps, t0 = 0, time.perf_counter()
+    M, N, K = case["M"], case["N"], case["K"]
+    q_w, s_w = oracle.quantize_weights(case["W"], case["w_bits"])
+
+    def one(rows):
+        A = np.ascontiguousarray(case["A"][:rows])
+        t0 = time.perf_counter()
+        q_a, s_a, seg_bits, seg_of = oracle.quantize_act(A, case["a_bits"], case["a_signed"])
+        acc = oracle.mac(q_a, q_w, seg_of, len(seg_bits))
+        oracle.epilogue_replay(acc, s_a, s_w)
+        return time.perf_counter() - t0
+
+    rows = min(M, 8)
     while True:
-        oracle.run(case["A"], case["W"], case["a_bits"], case["w_bits"], case["a_signed"])
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 20:
+        dt = one(rows)
+        if rows == M or dt >= 1.0:
             break
-    ops = 2 * case["M"] * case["N"] * case["K"] * reps
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return dict(value=ops / el / 1e12, unit="TOPS", cores=cores, kind="oracle",
-                sample=f"full workload, {reps} run(s) of quantize+MAC+epilogue in {el:.1f} s")
+        rows = min(M, max(rows + 1, int(rows * min(8.0, 1.2 / max(dt, 1e-3)))))
+    reps, el = 1, dt
+    while el < budget_s:
+        el += one(rows)
+        reps += 1
+    ops = 2 * rows * N * K * reps
+    return dict(value=ops / el / 1e12, unit="TOPS", cores=oracle.threads(), kind="oracle",
+                sample=(f"{rows} of {M} activation rows x all {N} outputs, K={K}: "
+                        f"quantize_act + MAC + epilogue, {reps} runs in {el:.1f} s"))
+
+
+def copy_calibration(nbytes=1 << 30, reps=5):
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the quantized GEMM path runs on a single "
-              "MI355X (multi-GPU sharding is a design note only).", file=sys.stderr)
+        print("bench.py measures one GPU only: the quantized GEMM runs on a single MI355X; "
+              "how it would shard over several GPUs is a design note, not a measured path.",
+              file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import workloads
     case = workloads.make(args.workload)
@@ -150,25 +266,6 @@ def main():
     ms = r["total_ms"] / args.steps
     tops = alg["ops"] / (ms * 1e-3) / 1e12
 
-    # Roofline of the dominant kernel call of a step.
-    if r["q_ms"] >= r["g_ms"]:
-        byt = alg["a_fp32"] + alg["a_packed"]
-        ach = byt / (r["q_ms"] * 1e-3) / 1e9
-        roof = dict(kernel="soniq_quantize_act (k_absmax + k_act_pack)", bound="hbm",
-                    achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
-                    traffic=None, bytes_per_launch=byt, launch_ms=r["q_ms"])
-    elif case["M"] <= 8:
-        byt = alg["w_packed"]
-        ach = byt / (r["g_ms"] * 1e-3) / 1e9
-        roof = dict(kernel="k_gemv", bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=ach / HBM_PEAK_GBS, traffic=None, bytes_per_launch=byt,
-                    launch_ms=r["g_ms"])
-    else:
-        ach = alg["ops"] / (r["g_ms"] * 1e-3) / 1e12
-        roof = dict(kernel="k_gemm", bound="mfma", achieved=ach, peak=INT8_PEAK_TOPS,
-                    unit="TOP/s", frac=ach / INT8_PEAK_TOPS, traffic=None,
-                    ops_per_launch=alg["ops"], launch_ms=r["g_ms"])
-
     rec = {
         "metric": METRIC, "value": tops, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
@@ -176,11 +273,13 @@ def main():
         "config": {"workload": case["name"], "M": case["M"], "N": case["N"], "K": case["K"],
                    "a_bits": sorted(set(case["a_bits"].tolist())),
                    "w_bits": sorted(set(case["w_bits"].tolist())),
-                   "a_signed": bool(case["a_signed"]), "activation_copies": r["nrot"]},
-        "roofline": roof,
+                   "a_signed": bool(case["a_signed"]),
+                   "activation_copies": r["na"], "weight_copies": r["nw"]},
+        "roofline": roofline(case, alg, r),
         "breakdown_ms": {"quantize_act": r["q_ms"], "mp_gemm": r["g_ms"],
                          "pack_weights_once": r["pack_ms"]},
         "gemm_tops": alg["ops"] / (r["g_ms"] * 1e-3) / 1e12,
+        "packed_weight_gbs": alg["w_packed"] / (r["g_ms"] * 1e-3) / 1e9,
         "bf16_linear_ms": r["bf16_ms"],
         "speedup_vs_bf16": {"gemm": r["bf16_ms"] / r["g_ms"], "step": r["bf16_ms"] / ms},
     }

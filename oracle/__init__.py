@@ -55,6 +55,8 @@ def lib():
             build()
         L = ctypes.CDLL(_LIB)
         i64, i32, f32, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_void_p
+        L.orc_threads.restype = i32
+        L.orc_threads.argtypes = []
         L.orc_qmax.restype = i64
         L.orc_qmax.argtypes = [i32, i32]
         L.orc_scale.restype = f32
@@ -87,6 +89,11 @@ def lib():
         L.orc_unpack.argtypes = [vp, i64, i32, i32, vp]
         _lib = L
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(lib().orc_threads())
 
 
 def _p(a: np.ndarray):

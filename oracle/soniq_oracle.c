@@ -26,6 +26,7 @@
  * Compiled with: -O2 -fopenmp -ffp-contract=off -fno-fast-math.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -309,3 +310,6 @@ void orc_unpack(const uint32_t* words, int64_t n, int bits, int mode,
                                            : (int32_t)field;
   }
 }
+
+/* Threads an OpenMP region of the oracle runs on (for reporting only). */
+int orc_threads(void) { return omp_get_max_threads(); }
