@@ -9,11 +9,11 @@
 //
 // Output-channel plan (C1: one width per 16-row block): the channels of
 // each weight width, in original order, are cut into blocks of 16 (the
-// last block of a width padded with empty rows).  The blocks of the two
-// widths are then merged by their first original channel, so any run of
-// consecutive blocks covers a nearly contiguous range of output columns and
-// the GEMM's output stores stay local.  The block count is padded to a
-// multiple of 8 (one 128-column GEMM tile).
+// last block of a width padded with empty rows); all blocks of the narrow
+// width come first, then those of the wide width, then empty blocks up to a
+// multiple of 8 (one 128-column GEMM tile).  Blocks are contiguous, so a
+// kernel derives any block's container and byte offset from the plan alone
+// (WPlan::nlo, c_lo, c_hi, ngt) without reading a table.
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
@@ -278,8 +278,10 @@ uint32_t unit_field(const uint8_t* p, int e, int c) {
     const int jj = (e % 8) / 4;
     return (word >> (8 * b + 4 * jj)) & 0xFu;
   }
+  // c = 2: elements 4j+b with j = 0, 1 sit in the top two bits of nibble
+  // 2b+j, those with j = 2, 3 in the bottom two bits of nibble 2b+j-2.
   memcpy(&word, p, 4);
-  return (word >> (8 * b + 2 * j)) & 0x3u;
+  return (word >> (8 * b + 4 * (j & 1) + ((j >> 1) ? 0 : 2))) & 0x3u;
 }
 
 // Field of row r, channel position e (in the group-ordered padded axis of
@@ -372,6 +374,7 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
   int64_t nblk = nb_lo + nb_hi;
   nblk = round_up(nblk, kGemmBN / kBlk);
   wp.nblk = (int)nblk;
+  wp.nlo = (int)nb_lo;
   wp.Np = (int)(nblk * kBlk);
   w->blk_off_h.assign(nblk, 0);
   w->blk_c_h.assign(nblk, (uint8_t)wp.c_lo);
@@ -396,14 +399,17 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
       off += (uint64_t)wp.ngt * 128 * c;  // blocks are contiguous (the GEMM relies on it)
       ++b;
     };
-    while (il < nb_lo || ih < nb_hi) {
-      const bool take_lo = ih >= nb_hi || (il < nb_lo && rows_lo[il * kBlk] < rows_hi[ih * kBlk]);
-      if (take_lo) place(rows_lo, il++, wp.c_lo);
-      else place(rows_hi, ih++, wp.c_hi);
-    }
+    while (il < nb_lo) place(rows_lo, il++, wp.c_lo);
+    while (ih < nb_hi) place(rows_hi, ih++, wp.c_hi);
     static const std::vector<int32_t> none;
-    while (b < nblk) place(none, 0, wp.c_lo);
+    while (b < nblk) place(none, 0, wp.c_hi);
     w->packed_bytes = (int64_t)off;
+    // Kernels derive block offsets from the plan; the table must agree.
+    for (int64_t i = 0; i < nblk; ++i)
+      if (w->blk_off_h[i] != wblk_off(wp, (int)i) || w->blk_c_h[i] != wblk_c(wp, (int)i)) {
+        free_weights(w);
+        return fail(SONIQ_ERR_UNSUPPORTED, "soniq_pack_weights: block plan mismatch");
+      }
   }
   // Output order inside each 128-column tile, for coalesced stores.
   const int ntile = wp.Np / kGemmBN;

@@ -12,7 +12,11 @@
 // mask move four consecutive elements into the top bits of four bytes:
 //   c = 8: byte e                                (unpack scale 1)
 //   c = 4: two words, element 4j+b of a word at bits 8b+4j  (scale 2^4)
-//   c = 2: one word, element 4j+b at bits 8b+2j             (scale 2^6)
+//   c = 2: one word; element 4j+b at bits 8b+4(j&1)+2 for j < 2 and at
+//          bits 8b+4(j&1) for j >= 2 (the top / bottom half of nibble
+//          2b+(j&1)), so masking the word with 0xCCCCCCCC, directly and
+//          shifted left by 2, gives the c = 4 nibble arrangement
+//          (values x4) that v_dot8_i32_i4 consumes   (unpack scale 2^6)
 //   c = 1: 16 bits, element 4j+b at bit 4b+j; bit 1 = -1,
 //          bit 0 = +1, unpacked to -64 / +64                 (scale 2^6)
 // Integer dot products of unpacked bytes are exact multiples of
@@ -71,8 +75,19 @@ struct WPlan {
   int c_lo, c_hi;
   int ngt;   // granules over both groups (Kp / kGran)
   int nblk;  // 16-row blocks, a multiple of 8
+  int nlo;   // blocks [0, nlo) hold the narrow width, the rest the wide one
   int Np;    // kBlk * nblk physical output positions
 };
+
+// Container and byte offset of weight block `blk` (blocks are contiguous,
+// narrow ones first).
+__host__ __device__ inline int wblk_c(const WPlan& wp, int blk) {
+  return blk < wp.nlo ? wp.c_lo : wp.c_hi;
+}
+__host__ __device__ inline uint64_t wblk_off(const WPlan& wp, int blk) {
+  const int lo = blk < wp.nlo ? blk : wp.nlo;
+  return ((uint64_t)lo * wp.c_lo + (uint64_t)(blk - lo) * wp.c_hi) * (uint64_t)wp.ngt * 128u;
+}
 
 struct WDev {
   const uint8_t* packed;

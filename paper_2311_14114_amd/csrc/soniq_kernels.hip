@@ -93,8 +93,8 @@ __device__ __forceinline__ uint4 pack_unit(uint32_t d0, uint32_t d1, uint32_t d2
     return make_uint4((d0 & 0x0F0F0F0Fu) | ((d1 & 0x0F0F0F0Fu) << 4),
                       (d2 & 0x0F0F0F0Fu) | ((d3 & 0x0F0F0F0Fu) << 4), 0u, 0u);
   if (c == 2)
-    return make_uint4((d0 & 0x03030303u) | ((d1 & 0x03030303u) << 2) |
-                          ((d2 & 0x03030303u) << 4) | ((d3 & 0x03030303u) << 6),
+    return make_uint4(((d0 & 0x03030303u) << 2) | ((d1 & 0x03030303u) << 6) |
+                          (d2 & 0x03030303u) | ((d3 & 0x03030303u) << 4),
                       0u, 0u, 0u);
   const uint32_t y = ((d0 >> 7) & 0x01010101u) | (((d1 >> 7) & 0x01010101u) << 1) |
                      (((d2 >> 7) & 0x01010101u) << 2) | (((d3 >> 7) & 0x01010101u) << 3);
@@ -124,8 +124,8 @@ __device__ __forceinline__ uint4 unpack4(uint32_t w0, uint32_t w1) {
                     w1 & 0xF0F0F0F0u);
 }
 __device__ __forceinline__ uint4 unpack2(uint32_t w) {
-  return make_uint4((w << 6) & 0xC0C0C0C0u, (w << 4) & 0xC0C0C0C0u, (w << 2) & 0xC0C0C0C0u,
-                    w & 0xC0C0C0C0u);
+  return make_uint4((w << 4) & 0xC0C0C0C0u, w & 0xC0C0C0C0u, (w << 6) & 0xC0C0C0C0u,
+                    (w << 2) & 0xC0C0C0C0u);
 }
 __device__ __forceinline__ uint32_t sgn1(uint32_t y, int j) {
   return ((y << (7 - j)) & 0x80808080u) | 0x40404040u;
@@ -543,6 +543,8 @@ struct GemmArgs {
 
 // s_waitcnt immediate for vmcnt(n) (gfx9 encoding), expcnt/lgkmcnt untouched.
 #define SONIQ_VMCNT_IMM(n) (((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
+// s_waitcnt immediate for lgkmcnt(0) alone (vmcnt and expcnt at their maxima).
+#define SONIQ_LGKMCNT0_IMM (0xF | (3 << 14) | (0x7 << 4))
 
 // Workgroup barrier without a memory fence: the LDS ring is filled by
 // direct loads whose completion each wave has already awaited with
@@ -773,10 +775,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   bpre[0] = 0;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    bc[j] = a.wd.blk_c[jb0 + j];
+    bc[j] = wblk_c(a.wp, jb0 + j);
     bpre[j + 1] = bpre[j] + 16 * bc[j];
   }
-  const uint8_t* wtile = a.wd.packed + a.wd.blk_off[jb0];
+  const uint8_t* wtile = a.wd.packed + wblk_off(a.wp, jb0);
 
   v4i acc0[WFM][4];
 #pragma unroll
@@ -862,7 +864,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- k_gemv --
+// ------------------------------------------------------------ k_gemv_any --
+// Generic batch <= 8 path for any activation containers.
 // One workgroup (4 waves) per 16-row weight block.  The block's bytes are a
 // contiguous run of 16-byte chunks; wave w takes chunk rows i = w, w+4, ...
 // (64 chunks each).  A chunk of container C holds U = 8/C units that share
@@ -914,7 +917,7 @@ __device__ __forceinline__ void gemv_block(const GemmArgs& a, uint8_t* xs, int b
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const ActPlan& ap = a.ap;
   const int M = (int)a.M, Kp = ap.Kp, ng0 = ap.ng[0];
-  const uint8_t* base = a.wd.packed + a.wd.blk_off[blk];
+  const uint8_t* base = a.wd.packed + wblk_off(a.wp, blk);
   const int nchunks = a.wp.ngt * 8 * C;
   const int NI = (nchunks + 63) >> 6;
   const int kg = ((U * lane) & 63) >> 4;
@@ -1021,15 +1024,322 @@ __device__ __forceinline__ void gemv_block(const GemmArgs& a, uint8_t* xs, int b
 
 // Dynamic LDS: M * Kp bytes of unpacked activations.
 template <int MT>
-__global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
+__global__ __launch_bounds__(256) void k_gemv_any(GemmArgs a) {
   extern __shared__ __align__(16) uint8_t xs[];
   __shared__ int red[4][kBlk][2][8];
   const int blk = blockIdx.x;
-  const int c = a.wd.blk_c[blk];
+  const int c = wblk_c(a.wp, blk);
   if (c == 2) gemv_block<MT, 2>(a, xs, blk, red);
   else if (c == 4) gemv_block<MT, 4>(a, xs, blk, red);
   else if (c == 8) gemv_block<MT, 8>(a, xs, blk, red);
   else gemv_block<MT, 1>(a, xs, blk, red);
+}
+
+
+
+// ---------------------------------------------------------------- k_gemv --
+// Batch <= 8 decode with the first activation group in 4-bit containers and
+// the second (if any) in bytes.  One workgroup (256 threads) per 16-row
+// weight block.  A block is ngt granules of 8*CW 16-byte chunks; the first
+// ng0 granules meet activation group 0, the rest group 1.  Load slot b of
+// thread tid holds chunk tid + 256*b of group 0 for b < NB0, else chunk
+// tid + 256*(b - NB0) of group 1, so a slot's group is fixed at compile
+// time and the thread's place inside a granule is fixed too:
+// t = tid mod 8*CW, i.e. rows r0 .. r0+U-1 (U = 8/CW) of 16-channel group
+// kg.  Loads are raw buffer loads; chunks past a group's end read as zero
+// without touching memory, so all of a thread's loads are issued at once
+// and zero chunks add nothing (except 1-bit blocks, where they are masked).
+//   - group 0 x 2- or 4-bit weights: v_dot8_i32_i4 on packed nibbles (a
+//     2-bit word becomes two nibble words with two masks);
+//   - otherwise bytes and v_dot4_i32_i8.
+// Lanes of a 16-lane DPP row that share output rows are summed with
+// row_ror; the four rows of a wave and the four waves meet in LDS.
+constexpr uint32_t kOOB = 0x7FFFFFF0u;  // buffer offset past any block
+
+__device__ __forceinline__ int dot16n(uint32_t w0, uint32_t w1, uint2 x, int v) {
+  v = __builtin_amdgcn_sdot8((int)w0, (int)x.x, v, false);
+  return __builtin_amdgcn_sdot8((int)w1, (int)x.y, v, false);
+}
+
+template <int CW>
+__device__ __forceinline__ uint4 chunk_bytes(uint4 raw, int u) {
+  if constexpr (CW == 8) return raw;
+  else if constexpr (CW == 4) return u == 0 ? unpack4(raw.x, raw.y) : unpack4(raw.z, raw.w);
+  else if constexpr (CW == 2) {
+    const uint32_t w = u == 0 ? raw.x : u == 1 ? raw.y : u == 2 ? raw.z : raw.w;
+    return unpack2(w);
+  } else {
+    const uint32_t w = (u >> 1) == 0 ? raw.x : (u >> 1) == 1 ? raw.y : (u >> 1) == 2 ? raw.z : raw.w;
+    return unpack1((w >> (16 * (u & 1))) & 0xFFFFu);
+  }
+}
+
+// Nibble words (elements 0-7, 8-15 in the 4-bit unit arrangement) of unit u.
+template <int CW>
+__device__ __forceinline__ uint2 chunk_nibbles(uint4 raw, int u) {
+  if constexpr (CW == 4) {
+    return u == 0 ? make_uint2(raw.x, raw.y) : make_uint2(raw.z, raw.w);
+  } else {
+    const uint32_t w = u == 0 ? raw.x : u == 1 ? raw.y : u == 2 ? raw.z : raw.w;
+    return make_uint2(w & 0xCCCCCCCCu, (w << 2) & 0xCCCCCCCCu);
+  }
+}
+
+template <int CW>
+__device__ __forceinline__ int dpp_row_sum(int v) {
+  // lanes of a 16-lane row with equal index mod 2*CW hold the same rows
+  if constexpr (2 * CW <= 8) v += __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);
+  if constexpr (2 * CW <= 4) v += __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);
+  if constexpr (2 * CW <= 2) v += __builtin_amdgcn_update_dpp(0, v, 0x122, 0xF, 0xF, false);
+  return v;
+}
+
+// Batch row of flattened unit index u (rows of d units), M <= MT <= 8.
+template <int MT>
+__device__ __forceinline__ int gemv_row_of(int u, int d) {
+  int m = 0;
+#pragma unroll
+  for (int j = 1; j < MT; ++j) m += u >= j * d ? 1 : 0;
+  return m;
+}
+
+// Activation staging: rows 0..M-1 of block 0 of both groups go to LDS,
+// group 0 as packed 8-byte nibble units [m][q][kg] (NIB) or widened to
+// bytes, group 1 as bytes [m][q][kg] at nbase.  A unit is loaded as 16
+// bytes through a buffer resource over the activation buffer (group 0
+// units use the first half); indexes past the last unit read as zero.
+template <int MT>
+constexpr int gemv_xr() { return MT == 1 ? 2 : MT == 2 ? 3 : MT <= 4 ? 5 : 9; }
+
+template <int MT>
+__device__ __forceinline__ void gemv_load_x(const GemmArgs& a, __amdgpu_buffer_rsrc_t xr, int u0,
+                                            uint4 (&xl)[gemv_xr<MT>()]) {
+  const ActPlan& ap = a.ap;
+  const int d = a.wp.ngt * 4, d0 = ap.ng[0] * 4;
+  const int total = (int)a.M * d;
+  const uint32_t o0 = (uint32_t)ap.seg_off[0], o1 = (uint32_t)ap.seg_off[1];
+#pragma unroll
+  for (int i = 0; i < gemv_xr<MT>(); ++i) {
+    // unit rest = 4q + kg of row m: at rest*128 + 8m (4-bit group) or
+    // (rest - 4*ng0)*256 + 16m (byte group) from the group's base
+    const int u = u0 + i * 256 + (int)threadIdx.x;
+    const int m = gemv_row_of<MT>(u, d), rest = u - m * d;
+    const uint32_t off = rest < d0 ? o0 + (uint32_t)(rest * 128 + m * 8)
+                                   : o1 + (uint32_t)((rest - d0) * 256 + m * 16);
+    xl[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                          xr, u < total ? off : kOOB, 0, 0));
+  }
+}
+
+template <int MT, bool NIB>
+__device__ __forceinline__ void gemv_store_x(const GemmArgs& a, int u0,
+                                             const uint4 (&xl)[gemv_xr<MT>()], uint8_t* xs,
+                                             int nbase) {
+  const int d = a.wp.ngt * 4, d0 = a.ap.ng[0] * 4;
+  const int total = (int)a.M * d;
+#pragma unroll
+  for (int i = 0; i < gemv_xr<MT>(); ++i) {
+    const int u = u0 + i * 256 + (int)threadIdx.x;
+    if (u < total) {
+      const int m = gemv_row_of<MT>(u, d), rest = u - m * d;
+      if (rest < d0 && NIB) {
+        *reinterpret_cast<uint2*>(xs + m * d0 * 8 + rest * 8) = make_uint2(xl[i].x, xl[i].y);
+      } else {
+        const uint4 v = rest < d0 ? unpack4(xl[i].x, xl[i].y) : xl[i];
+        *reinterpret_cast<uint4*>(xs + nbase + (m * d + rest) * 16) = v;
+      }
+    }
+  }
+}
+
+template <int MT, int CW, bool NIB>
+__device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int blk,
+                                            int (&red)[4][4][kBlk][2][MT]) {
+  constexpr int U = 8 / CW;
+  constexpr int CPG = 8 * CW;    // chunks per granule
+  constexpr int QS = 256 / CPG;  // granules per slot of the workgroup
+  // load slots per batch for the two activation groups (sized so a 4096-
+  // channel row with a dominant narrow group needs one batch)
+  constexpr int NB0 = CW == 1 ? 2 : CW == 2 ? 4 : CW == 4 ? 8 : 8;
+  constexpr int NB1 = CW == 1 ? 1 : CW == 2 ? 2 : CW == 4 ? 4 : 4;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const ActPlan& ap = a.ap;
+  const int M = (int)a.M, ngt = a.wp.ngt, ng0 = ap.ng[0], ng1 = ngt - ng0;
+  const int nbase = NIB ? M * ng0 * 32 : 0;
+  const int nch0 = ng0 * CPG, nch1 = ng1 * CPG;
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.wd.packed + wblk_off(a.wp, blk)), (short)0, (nch0 + nch1) * 16, 0x00020000);
+  const int t = tid & (CPG - 1);
+  const int kg = (U * t) >> 4;
+  const int q0 = tid / CPG;
+  // Epilogue inputs of this thread's output (block row er, batch row em),
+  // fetched together with the first loads rather than after the reduction.
+  const int er = tid & (kBlk - 1), em = tid >> 4;
+  const int ep = blk * kBlk + er;
+  const ColInfo eci = a.wd.colinfo[ep];
+  const uint8_t eshw = a.wd.shw[ep];
+  const float sa0 = a.s_a[0], sa1 = ap.S == 2 ? a.s_a[1] : 0.0f;
+
+  int acc0[U][MT], acc1[U][MT];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm) acc0[u][mm] = acc1[u][mm] = 0;
+
+  // Group-0 slot b of batch i holds chunk tid + 256*(i*NB0 + b), group-1
+  // slot b of batch i chunk tid + 256*(i*NB1 + b) past the group-0 chunks.
+  auto issue0 = [&](int s0, uint4 (&raw)[NB0]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < NB0; ++b) {
+      const int c = tid + 256 * (s0 + b);
+      raw[b] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             wr, c < nch0 ? (uint32_t)c * 16 : kOOB, 0, 0));
+    }
+  };
+  auto issue1 = [&](int s0, uint4 (&raw)[NB1]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < NB1; ++b) {
+      const int c = tid + 256 * (s0 + b);
+      raw[b] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             wr, c < nch1 ? (uint32_t)(nch0 + c) * 16 : kOOB, 0, 0));
+    }
+  };
+  // Byte-path products of one chunk (zero chunks add nothing; 1-bit
+  // chunks, whose zero bits decode to +1, are masked).
+  auto bytes_into = [&](int (&acc)[U][MT], uint4 raw, int xq, bool ok) __attribute__((always_inline)) {
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm) {
+      if (mm < M) {
+        const uint4 x = *reinterpret_cast<const uint4*>(xs + nbase + (mm * ngt + xq) * 64 + kg * 16);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int v = dot16(chunk_bytes<CW>(raw, u), x, 0);
+          acc[u][mm] += (CW != 1 || ok) ? v : 0;
+        }
+      }
+    }
+  };
+  auto consume0 = [&](int s0, const uint4 (&raw)[NB0]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < NB0; ++b) {
+      if (256 * (s0 + b) >= nch0) break;  // the same for the whole workgroup
+      const int q = min(q0 + QS * (s0 + b), ng0 - 1);
+      if constexpr (NIB) {
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm) {
+          if (mm < M) {
+            const uint2 x = *reinterpret_cast<const uint2*>(xs + (mm * ng0 + q) * 32 + kg * 8);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+              const uint2 w = chunk_nibbles<CW>(raw[b], u);
+              acc0[u][mm] = dot16n(w.x, w.y, x, acc0[u][mm]);
+            }
+          }
+        }
+      } else {
+        bytes_into(acc0, raw[b], q, tid + 256 * (s0 + b) < nch0);
+      }
+    }
+  };
+  auto consume1 = [&](int s0, const uint4 (&raw)[NB1]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < NB1; ++b) {
+      if (256 * (s0 + b) >= nch1) break;  // the same for the whole workgroup
+      bytes_into(acc1, raw[b], ng0 + min(q0 + QS * (s0 + b), ng1 - 1), tid + 256 * (s0 + b) < nch1);
+    }
+  };
+
+  // The activation loads go first (they hit L2), then the first batch of
+  // both groups' chunks; staging waits only for the former.
+  {
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)a.act, (short)0,
+        (int)(ap.S == 2 ? ap.seg_off[1] + ap.mblk_bytes[1] : ap.seg_off[0] + ap.mblk_bytes[0]),
+        0x00020000);
+    uint4 xl[gemv_xr<MT>()];
+    gemv_load_x<MT>(a, xr, 0, xl);
+    uint4 raw0[NB0], raw1[NB1];
+    issue0(0, raw0);
+    issue1(0, raw1);
+    gemv_store_x<MT, NIB>(a, 0, xl, xs, nbase);
+    const int total_x = M * ngt * 4;
+    for (int u0 = 256 * gemv_xr<MT>(); u0 < total_x; u0 += 256 * gemv_xr<MT>()) {
+      gemv_load_x<MT>(a, xr, u0, xl);
+      gemv_store_x<MT, NIB>(a, u0, xl, xs, nbase);
+    }
+    // The staged rows must be visible to every wave, but the weight chunks
+    // may still be in flight: wait for LDS writes only, then a plain
+    // barrier (a full __syncthreads would also drain every chunk load).
+    __builtin_amdgcn_s_waitcnt(SONIQ_LGKMCNT0_IMM);
+    bar_nofence();
+    consume0(0, raw0);
+    if (nch1 > 0) consume1(0, raw1);
+  }
+  for (int s0 = NB0; 256 * s0 < nch0; s0 += NB0) {
+    uint4 raw[NB0];
+    issue0(s0, raw);
+    consume0(s0, raw);
+  }
+  for (int s0 = NB1; 256 * s0 < nch1; s0 += NB1) {
+    uint4 raw[NB1];
+    issue1(s0, raw);
+    consume1(s0, raw);
+  }
+
+  // Within each 16-lane row, then rows and waves through LDS.
+  const int row16 = lane >> 4, l16 = lane & 15;
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm) {
+      acc0[u][mm] = dpp_row_sum<CW>(acc0[u][mm]);
+      acc1[u][mm] = dpp_row_sum<CW>(acc1[u][mm]);
+    }
+  if (l16 < 2 * CW) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) {
+        red[wid][row16][U * l16 + u][0][mm] = acc0[u][mm];
+        red[wid][row16][U * l16 + u][1][mm] = acc1[u][mm];
+      }
+  }
+  __syncthreads();
+  if (tid < kBlk * M && eci.n >= 0) {
+    int s0 = 0, s1 = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        s0 += red[w][h][er][0][em];
+        s1 += red[w][h][er][1][em];
+      }
+    const int S = ap.S;
+    // group 0 sums are in units of 2^2 (2-bit nibbles) or 1 on the nibble
+    // path; byte-path sums carry both unpack scales
+    const int t0 = NIB ? (s0 >> (CW == 2 ? 2 : 0)) + ap.zp[0] * eci.colsum[0]
+                       : true_acc(s0, ap.sh[0], ap.c[0], ap.padcnt[0], ap.zp[0], eshw, eci.colsum[0]);
+    const int t1 = S == 2 ? true_acc(s1, ap.sh[1], ap.c[1], ap.padcnt[1], ap.zp[1], eshw, eci.colsum[1])
+                          : 0;
+    a.Y[(int64_t)em * a.ldy + eci.n] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, eci.s_w));
+    if (a.acc) {
+      a.acc[(int64_t)em * a.N + eci.n] = t0;
+      if (S == 2) a.acc[(a.M + em) * a.N + eci.n] = t1;
+    }
+  }
+}
+
+// Dynamic LDS: M * (Kp + 32 * ng0) bytes.
+template <int MT>
+__global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
+  extern __shared__ __align__(16) uint8_t xs[];
+  __shared__ int red[4][4][kBlk][2][MT];
+  const int blk = blockIdx.x;
+  const int c = wblk_c(a.wp, blk);
+  if (c == 2) gemv4_block<MT, 2, true>(a, xs, blk, red);
+  else if (c == 4) gemv4_block<MT, 4, true>(a, xs, blk, red);
+  else if (c == 8) gemv4_block<MT, 8, false>(a, xs, blk, red);
+  else gemv4_block<MT, 1, false>(a, xs, blk, red);
 }
 
 }  // namespace
@@ -1158,11 +1468,29 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
   return hipGetLastError();
 }
 
+static size_t gemv_lds(int64_t M, const ActPlan& ap);
+
 bool gemv_fits(int64_t M, const ActPlan& ap, const WPlan& wp) {
-  if (M < 1 || M > 8 || M * (int64_t)ap.Kp > 64 * 1024) return false;
+  if (M < 1 || M > 8) return false;
+  // dynamic LDS (activation rows) plus the static reduction buffer
+  if (gemv_lds(M, ap) + (size_t)2048 * 8 > 64 * 1024) return false;
   // 1-bit weight blocks keep 8 rows per lane: at most 4 activation rows.
   if ((wp.c_lo == 1 || wp.c_hi == 1) && M > 4) return false;
+  // buffer-resource offsets into the activation and weight buffers are 32-bit
+  const int64_t act_end = ap.S == 2 ? ap.seg_off[1] + ap.mblk_bytes[1] : ap.seg_off[0] + ap.mblk_bytes[0];
+  if (act_end >= ((int64_t)1 << 31) || (int64_t)wp.ngt * 128 * 8 * 16 >= ((int64_t)1 << 31))
+    return false;
   return true;
+}
+
+// The nibble GEMV needs the first activation group in 4-bit containers and
+// the second (if any) in bytes.
+static bool gemv_nibble_plan(const ActPlan& ap) {
+  return ap.c[0] == 4 && (ap.S == 1 || ap.c[1] == 8);
+}
+
+static size_t gemv_lds(int64_t M, const ActPlan& ap) {
+  return gemv_nibble_plan(ap) ? (size_t)M * (ap.Kp + 32 * ap.ng[0]) : (size_t)M * ap.Kp;
 }
 
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
@@ -1170,15 +1498,18 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
   const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   dim3 grid((unsigned)wp.nblk);
-  const size_t lds = (size_t)M * ap.Kp;
-  if (M == 1)
-    hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
-  else if (M == 2)
-    hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), lds, stream, a);
-  else if (M <= 4)
-    hipLaunchKernelGGL(k_gemv<4>, grid, dim3(256), lds, stream, a);
-  else
-    hipLaunchKernelGGL(k_gemv<8>, grid, dim3(256), lds, stream, a);
+  const size_t lds = gemv_lds(M, ap);
+  if (gemv_nibble_plan(ap)) {
+    if (M == 1) hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
+    else if (M == 2) hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), lds, stream, a);
+    else if (M <= 4) hipLaunchKernelGGL(k_gemv<4>, grid, dim3(256), lds, stream, a);
+    else hipLaunchKernelGGL(k_gemv<8>, grid, dim3(256), lds, stream, a);
+  } else {
+    if (M == 1) hipLaunchKernelGGL(k_gemv_any<1>, grid, dim3(256), lds, stream, a);
+    else if (M == 2) hipLaunchKernelGGL(k_gemv_any<2>, grid, dim3(256), lds, stream, a);
+    else if (M <= 4) hipLaunchKernelGGL(k_gemv_any<4>, grid, dim3(256), lds, stream, a);
+    else hipLaunchKernelGGL(k_gemv_any<8>, grid, dim3(256), lds, stream, a);
+  }
   return hipGetLastError();
 }
 

@@ -156,6 +156,31 @@ def test_weight_widths_and_grids(wlo, whi, mode, M):
     compare_full(gpu_run(case, wq_mode=mode), oracle_run(case, wq_mode=mode))
 
 
+GEMV_W = [(2, 4), (2, 8), (4, 8), (1, 4), (1, 2), (8, 8), (3, 4)]
+GEMV_A = [(4, 8, True), (4, 8, False), (4, 4, True), (3, 8, True), (2, 8, True), (8, 8, True)]
+
+
+@pytest.mark.parametrize("wlo,whi", GEMV_W)
+@pytest.mark.parametrize("alo,ahi,sgn", GEMV_A)
+@pytest.mark.parametrize("M", [1, 2, 5, 8])
+def test_small_batch_paths(wlo, whi, alo, ahi, sgn, M):
+    """Batch <= 8: nibble dot products (4-bit activation groups against 2- and
+    4-bit weight blocks), byte dot products otherwise, ragged N and K."""
+    case = workloads.generic(M, 333, 1000, a_lo=alo, a_hi=ahi, a_frac_lo=0.7, w_lo=wlo,
+                             w_hi=whi, w_frac_lo=0.6, a_signed=sgn, a_abs=not sgn,
+                             seed=wlo * 1000 + whi * 100 + alo * 10 + ahi + M * 7 + sgn,
+                             name="gemv")
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+@pytest.mark.parametrize("M,K", [(1, 9000), (2, 9000), (8, 3000)])
+def test_small_batch_long_rows(M, K):
+    """Several load batches per workgroup and several activation staging rounds."""
+    case = workloads.generic(M, 100, K, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=4, w_hi=8,
+                             w_frac_lo=0.5, seed=K + M, name="gemv_long")
+    compare_full(gpu_run(case), oracle_run(case))
+
+
 def test_strides_and_unaligned_rows():
     case = workloads.generic(70, 100, 131, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
                              w_frac_lo=0.5, seed=5, name="strides")
