@@ -35,7 +35,7 @@ constexpr int kGran = 64;     // channels per granule
 constexpr int kBlk = 16;      // rows per block
 constexpr int kGemmBN = 128;  // GEMM block tile columns (8 weight blocks)
 constexpr int kMAlign = 256;  // activation rows are allocated in multiples of this
-constexpr int kAbsmaxBlocks = 256;
+constexpr int kAbsmaxBlocks = 1024;  // max partial maxima (pairs) per activation batch
 
 // Quantizer of one width: code = sign1 ? (x < 0 ? -1 : +1)
 //                                : clamp(rint(x / s), lo, hi), s = max/qdiv.

@@ -237,7 +237,6 @@ __global__ __launch_bounds__(256) void k_wpack(
 // workgroup here writes its partial maxima (no atomics, no fences: a
 // per-workgroup device-scope fence costs tens of nanoseconds each on a chip
 // with per-XCD L2s); the pack kernel that follows reduces the partials.
-constexpr int kAbsU = 8;
 
 __device__ __forceinline__ void max4(float4 v, uchar4 g, float& mx0, float& mx1) {
   const float a0 = fabsf(v.x), a1 = fabsf(v.y), a2 = fabsf(v.z), a3 = fabsf(v.w);
@@ -255,29 +254,49 @@ __device__ __forceinline__ void write_partial(float mx0, float mx1, float* red,
   }
 }
 
-// Contiguous rows (lda == K, K % 4 == 0, 16-byte aligned): one flat float4
-// stream, kAbsU loads in flight per thread.  Out-of-range lanes re-read the
-// last element (always in bounds) and contribute nothing.
-__global__ __launch_bounds__(256) void k_absmax_flat(const float4* __restrict__ A, uint32_t total4,
-                                                     uint32_t K4, const uchar4* __restrict__ seg4,
-                                                     float* __restrict__ partial) {
+// Rows with K % 4 == 0, lda % 4 == 0, 16-byte aligned.  Workgroup b takes
+// RB consecutive rows (RB a multiple of 4); thread tid owns float4
+// positions k4 = base + 256*j of every row, keeps their running |max| over
+// the rows (one v_max per element, four rows of loads in flight), and folds
+// them into the two group maxima once per position batch.  Clamped rows and
+// positions re-read in-bounds data already counted, which a max ignores.
+template <int J>
+__global__ __launch_bounds__(256) void k_absmax_blk(const float4* __restrict__ A, int64_t M,
+                                                    int K4, int64_t lda4, int RB,
+                                                    const uchar4* __restrict__ seg4,
+                                                    float* __restrict__ partial) {
   __shared__ float red[4];
+  const int tid = threadIdx.x;
+  const int64_t m0 = (int64_t)blockIdx.x * RB;
+  const int rows = (int)min((int64_t)RB, M - m0);
   float mx0 = 0.0f, mx1 = 0.0f;
-  const uint32_t step = gridDim.x * 256u * kAbsU;
-  for (uint32_t base = blockIdx.x * 256u * kAbsU + threadIdx.x; base < total4; base += step) {
-    float4 v[kAbsU];
-    uchar4 g[kAbsU];
+  for (int base = 0; base < K4; base += 256 * J) {
+    int k4[J];
 #pragma unroll
-    for (int j = 0; j < kAbsU; ++j) {
-      const uint32_t i = min(base + 256u * j, total4 - 1u);
-      v[j] = A[i];
-      g[j] = seg4[i % K4];
+    for (int j = 0; j < J; ++j) k4[j] = min(base + 256 * j + tid, K4 - 1);
+    float4 mx[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) mx[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int r0 = 0; r0 < rows; r0 += 4) {
+      float4 v[4][J];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float4* row = A + (m0 + min(r0 + r, rows - 1)) * lda4;
+#pragma unroll
+        for (int j = 0; j < J; ++j) v[r][j] = row[k4[j]];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+          mx[j].x = fmaxf(mx[j].x, fabsf(v[r][j].x));
+          mx[j].y = fmaxf(mx[j].y, fabsf(v[r][j].y));
+          mx[j].z = fmaxf(mx[j].z, fabsf(v[r][j].z));
+          mx[j].w = fmaxf(mx[j].w, fabsf(v[r][j].w));
+        }
     }
 #pragma unroll
-    for (int j = 0; j < kAbsU; ++j) {
-      const bool ok = base + 256u * j < total4;
-      max4(ok ? v[j] : make_float4(0.f, 0.f, 0.f, 0.f), g[j], mx0, mx1);
-    }
+    for (int j = 0; j < J; ++j) max4(mx[j], seg4[k4[j]], mx0, mx1);
   }
   write_partial(mx0, mx1, red, partial);
 }
@@ -369,6 +388,23 @@ __device__ __forceinline__ uint8_t store_code(float x, int g, const ActQ& a) {
 // Write the units of `nrows` rows whose stored codes sit in LDS (row r at
 // codes + r*Kp) to rows m0.. of the packed activation buffer, one 2*c-byte
 // unit per store.  Used when a workgroup holds fewer than 16 rows.
+template <int C>
+__device__ __forceinline__ void write_group_units(const uint8_t* codes, int nrows, int64_t m0,
+                                                  int Kp, int ng, int gbase, int64_t mblk,
+                                                  uint8_t* __restrict__ dst0) {
+  const int per_row = ng * 4;
+  for (int r = 0; r < nrows; ++r) {
+    const int64_t m = m0 + r;
+    uint8_t* dst = dst0 + (m / kBlk) * mblk + (int)(m % kBlk) * 2 * C;
+    const uint8_t* src = codes + r * Kp + gbase;
+    for (int rest = threadIdx.x; rest < per_row; rest += blockDim.x) {
+      const int qg = rest >> 2, kg = rest & 3;
+      const uint4 d = *reinterpret_cast<const uint4*>(src + rest * 16);
+      store_unit(dst + qg * 128 * C + kg * 32 * C, pack_unit(d.x, d.y, d.z, d.w, C), C);
+    }
+  }
+}
+
 __device__ __forceinline__ void write_act_units(const uint8_t* codes, int nrows, int64_t m0,
                                                 const ActPlan& ap, uint8_t* __restrict__ packed) {
   for (int g = 0; g < ap.S; ++g) {
@@ -377,82 +413,142 @@ __device__ __forceinline__ void write_act_units(const uint8_t* codes, int nrows,
     const int gbase = g ? ap.kpad[0] : 0;
     const int64_t mblk = g ? ap.mblk_bytes[1] : ap.mblk_bytes[0];
     uint8_t* dst0 = packed + (g ? ap.seg_off[1] : ap.seg_off[0]);
-    const int per_row = ng * 4;
-    for (int u = threadIdx.x; u < nrows * per_row; u += blockDim.x) {
-      const int r = u / per_row, rest = u - r * per_row;
-      const int qg = rest >> 2, kg = rest & 3;
-      const int64_t m = m0 + r;
-      const uint4 d = *reinterpret_cast<const uint4*>(codes + (int64_t)r * ap.Kp + gbase + qg * kGran + kg * 16);
-      uint8_t* p = dst0 + (m / kBlk) * mblk + (int64_t)qg * 128 * c + (kg * 16 + (int)(m % kBlk)) * 2 * c;
-      store_unit(p, pack_unit(d.x, d.y, d.z, d.w, c), c);
-    }
+    if (c == 8) write_group_units<8>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
+    else if (c == 4) write_group_units<4>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
+    else if (c == 2) write_group_units<2>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
+    else write_group_units<1>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
   }
+}
+
+// Per-element quantizer parameters of one group, arranged so that the
+// common case needs no branch: code = clamp(rint(x*rs) - zp, lo - zp,
+// hi - zp).  rs is NaN where the reciprocal shortcut is not exact enough
+// (scale outside [2^-100, 2^100]), which sends every element of the group
+// through the exact division; a zero scale has rs = 0 and gives code 0.
+struct QElem {
+  float rs, lo, hi, zp, s;
+};
+
+__device__ __forceinline__ QElem qelem(float s, const QParam& q, int zp) {
+  QElem e;
+  e.s = s;
+  e.rs = s == 0.0f ? 0.0f : fast_ok(s) ? __builtin_amdgcn_rcpf(s) : __builtin_nanf("");
+  e.zp = (float)zp;
+  e.lo = (float)(q.lo - zp);
+  e.hi = (float)(q.hi - zp);
+  return e;
+}
+
+// Stored code (code - zp) of x.  The shortcut rint(x * rcp(s)) equals
+// rint(x / s) unless x/s lies near a rounding tie: v_rcp_f32 is within 1 ulp
+// and the product adds half an ulp, so for |x/s| <= 256 the two quotients
+// differ by less than 256 * 2^-22 = 2^-14; inside a band of 2^-12 around a
+// tie (or when the shortcut is off, rs NaN) the exact IEEE quotient decides.
+constexpr float kTieBand = 0x1p-12f;
+
+__device__ __forceinline__ int qstore(float x, float rs, float lo, float hi, float zp, float s) {
+  const float e = x * rs;
+  float t = __builtin_rintf(e);
+  if (!(fabsf(fabsf(e - t) - 0.5f) > kTieBand)) [[unlikely]]
+    t = s == 0.0f ? 0.0f : __builtin_rintf(__fdiv_rn(x, s));
+  return (int)__builtin_amdgcn_fmed3f(t - zp, lo, hi);
 }
 
 // ------------------------------------------------------------ k_act_rows --
 // R activation rows per workgroup: reduce the partial maxima, quantize the
 // rows into LDS at their group-ordered positions, write their units.
+// Thread tid owns float4 positions base + tid + 256*j (j < J) of every row;
+// their LDS positions and group parameters are looked up once for all R
+// rows.  The first batch of rows is loaded before the partial maxima are
+// reduced, so the two latencies overlap.  Groups of 1-bit sign codes, and
+// unaligned rows, take the generic per-element quantizer (J = 0).
 // Dynamic LDS: R*Kp bytes.
-constexpr int kPackJ = 2;  // float4 positions per thread per pass
-template <int R>
+template <int R, int J>
+__device__ __forceinline__ void act_rows_load(const float* __restrict__ A, int64_t m0, int rows,
+                                              int64_t lda, int K4, int base,
+                                              const int32_t* __restrict__ pos,
+                                              const uint8_t* __restrict__ seg, int4 (&p)[J],
+                                              uchar4 (&g)[J], float4 (&v)[R][J]) {
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int k4 = min(base + 256 * j, K4 - 1);
+    p[j] = reinterpret_cast<const int4*>(pos)[k4];
+    g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      v[r][j] = *reinterpret_cast<const float4*>(A + (m0 + min(r, rows - 1)) * lda + 4 * k4);
+  }
+}
+
+template <int R, int J>
+__device__ __forceinline__ void act_rows_quant(uint8_t* codes, int Kp, int rows, int K4, int base,
+                                               const int4 (&p)[J], const uchar4 (&g)[J],
+                                               const float4 (&v)[R][J], const QElem& q0,
+                                               const QElem& q1) {
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    if (base + 256 * j < K4) {
+      const uchar4 h = g[j];
+      const QElem& ex = h.x ? q1 : q0;
+      const QElem& ey = h.y ? q1 : q0;
+      const QElem& ez = h.z ? q1 : q0;
+      const QElem& ew = h.w ? q1 : q0;
+      const float rsx = ex.rs, lox = ex.lo, hix = ex.hi, zpx = ex.zp, sx = ex.s;
+      const float rsy = ey.rs, loy = ey.lo, hiy = ey.hi, zpy = ey.zp, sy = ey.s;
+      const float rsz = ez.rs, loz = ez.lo, hiz = ez.hi, zpz = ez.zp, sz = ez.s;
+      const float rsw = ew.rs, low = ew.lo, hiw = ew.hi, zpw = ew.zp, sw = ew.s;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (r < rows) {
+          uint8_t* row = codes + r * Kp;
+          row[p[j].x] = (uint8_t)qstore(v[r][j].x, rsx, lox, hix, zpx, sx);
+          row[p[j].y] = (uint8_t)qstore(v[r][j].y, rsy, loy, hiy, zpy, sy);
+          row[p[j].z] = (uint8_t)qstore(v[r][j].z, rsz, loz, hiz, zpz, sz);
+          row[p[j].w] = (uint8_t)qstore(v[r][j].w, rsw, low, hiw, zpw, sw);
+        }
+      }
+    }
+  }
+}
+
+template <int R, int J>
 __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, int64_t M,
                                                   int64_t K, int64_t lda,
                                                   const int32_t* __restrict__ pos,
                                                   const uint8_t* __restrict__ seg, ActPlan ap,
                                                   const float* __restrict__ partial, int nparts,
                                                   float* __restrict__ s_a_out,
-                                                  uint8_t* __restrict__ packed, int vec4) {
+                                                  uint8_t* __restrict__ packed) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[4];
   const int64_t m0 = (int64_t)blockIdx.x * R;
   const int rows = (int)min((int64_t)R, M - m0);
   const int tid = threadIdx.x;
-  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
-  for (int i = tid; i < rows * ap.Kp / 4; i += blockDim.x) codes32[i] = 0;
-  float s0, s1;
-  scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
-  const ActQ aq = make_actq(ap, s0, s1);
-  if (vec4) {
-    // Each thread owns float4 positions k4 = tid + 256*j for every row of
-    // the workgroup: one position/group lookup serves all rows.
+  if constexpr (J > 0) {
     const int K4 = (int)(K / 4);
-    for (int base = tid; base < K4; base += 256 * kPackJ) {
-      int4 p[kPackJ];
-      uchar4 g[kPackJ];
-      float4 v[R][kPackJ];
-#pragma unroll
-      for (int j = 0; j < kPackJ; ++j) {
-        const int k4 = min(base + 256 * j, K4 - 1);
-        p[j] = reinterpret_cast<const int4*>(pos)[k4];
-        g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          const int rc = min(r, rows - 1);
-          v[r][j] = *reinterpret_cast<const float4*>(A + (m0 + rc) * lda + 4 * k4);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < kPackJ; ++j) {
-        if (base + 256 * j < K4) {
-#pragma unroll
-          for (int r = 0; r < R; ++r) {
-            if (r < rows) {
-              uint8_t* row = codes + r * ap.Kp;
-              row[p[j].x] = store_code(v[r][j].x, g[j].x, aq);
-              row[p[j].y] = store_code(v[r][j].y, g[j].y, aq);
-              row[p[j].z] = store_code(v[r][j].z, g[j].z, aq);
-              row[p[j].w] = store_code(v[r][j].w, g[j].w, aq);
-            }
-          }
-        }
-      }
+    int4 p[J];
+    uchar4 g[J];
+    float4 v[R][J];
+    act_rows_load<R, J>(A, m0, rows, lda, K4, tid, pos, seg, p, g, v);
+    uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+    for (int i = tid; i < rows * ap.Kp / 4; i += blockDim.x) codes32[i] = 0;
+    float s0, s1;
+    scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
+    const QElem q0 = qelem(s0, ap.q[0], ap.zp[0]), q1 = qelem(s1, ap.q[1], ap.zp[1]);
+    act_rows_quant<R, J>(codes, ap.Kp, rows, K4, tid, p, g, v, q0, q1);
+    for (int base = tid + 256 * J; base < K4; base += 256 * J) {
+      act_rows_load<R, J>(A, m0, rows, lda, K4, base, pos, seg, p, g, v);
+      act_rows_quant<R, J>(codes, ap.Kp, rows, K4, base, p, g, v, q0, q1);
     }
   } else {
-    for (int64_t i = tid; i < (int64_t)rows * K; i += blockDim.x) {
-      const int r = (int)(i / K);
-      const int64_t k = i - (int64_t)r * K;
-      codes[(int64_t)r * ap.Kp + pos[k]] = store_code(A[(m0 + r) * lda + k], seg[k], aq);
-    }
+    uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+    for (int i = tid; i < rows * ap.Kp / 4; i += blockDim.x) codes32[i] = 0;
+    float s0, s1;
+    scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
+    const ActQ aq = make_actq(ap, s0, s1);
+    for (int r = 0; r < rows; ++r)
+      for (int64_t k = tid; k < K; k += blockDim.x)
+        codes[(int64_t)r * ap.Kp + pos[k]] = store_code(A[(m0 + r) * lda + k], seg[k], aq);
   }
   __syncthreads();
   write_act_units(codes, rows, m0, ap, packed);
@@ -1371,14 +1467,24 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
     return hipGetLastError();
   }
   int nparts;
-  if (aligned && lda == K && M * K / 4 < (int64_t)UINT32_MAX) {
-    const int64_t total4 = M * K / 4;
-    int64_t blocks = (total4 + 256 * kAbsU - 1) / (256 * kAbsU);
-    if (blocks > kAbsmaxBlocks) blocks = kAbsmaxBlocks;
+  if (aligned) {
+    // rows per workgroup: a multiple of 4 keeping the grid within the
+    // partial buffer (kAbsmaxBlocks workgroups)
+    const int K4 = (int)(K / 4);
+    const int64_t RB = 4 * ((M + 4 * kAbsmaxBlocks - 1) / (4 * kAbsmaxBlocks));
+    const int64_t blocks = (M + RB - 1) / RB;
     nparts = (int)blocks;
-    hipLaunchKernelGGL(k_absmax_flat, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       reinterpret_cast<const float4*>(A), (uint32_t)total4, (uint32_t)(K / 4),
-                       reinterpret_cast<const uchar4*>(seg_dev), partial);
+    const int J = K4 <= 256 ? 1 : K4 <= 512 ? 2 : K4 <= 768 ? 3 : 4;
+    const float4* A4 = reinterpret_cast<const float4*>(A);
+    const uchar4* s4 = reinterpret_cast<const uchar4*>(seg_dev);
+    if (J == 1)
+      hipLaunchKernelGGL(k_absmax_blk<1>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
+    else if (J == 2)
+      hipLaunchKernelGGL(k_absmax_blk<2>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
+    else if (J == 3)
+      hipLaunchKernelGGL(k_absmax_blk<3>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
+    else
+      hipLaunchKernelGGL(k_absmax_blk<4>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
   } else {
     const int64_t blocks = M < kAbsmaxBlocks ? M : kAbsmaxBlocks;
     nparts = (int)blocks;
@@ -1387,15 +1493,30 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // groups of 1-bit sign codes, and unaligned rows, take the generic
+  // per-element quantizer (J = 0); otherwise J float4 positions per thread
+  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
+  const int K4 = (int)(K / 4);
+  const int J = (sign || !aligned) ? 0 : K4 <= 256 ? 1 : K4 <= 512 ? 2 : K4 <= 768 ? 3 : 4;
+#define SONIQ_ACT_ROWS(R_, J_)                                                                  \
+  hipLaunchKernelGGL((k_act_rows<R_, J_>), dim3((unsigned)((M + R_ - 1) / R_)), dim3(256),      \
+                     (size_t)R_ * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,    \
+                     nparts, s_a, packed)
   if (4 * (int64_t)ap.Kp <= 64 * 1024) {
-    hipLaunchKernelGGL(k_act_rows<4>, dim3((unsigned)((M + 3) / 4)), dim3(256),
-                       (size_t)4 * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,
-                       nparts, s_a, packed, aligned ? 1 : 0);
+    switch (J) {
+      case 0: SONIQ_ACT_ROWS(4, 0); break;
+      case 1: SONIQ_ACT_ROWS(4, 1); break;
+      case 2: SONIQ_ACT_ROWS(4, 2); break;
+      case 3: SONIQ_ACT_ROWS(4, 3); break;
+      default: SONIQ_ACT_ROWS(4, 4); break;
+    }
   } else {
-    hipLaunchKernelGGL(k_act_rows<1>, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A, M,
-                       K, lda, pos_dev, seg_dev, ap, partial, nparts, s_a, packed,
-                       aligned ? 1 : 0);
+    switch (J) {
+      case 0: SONIQ_ACT_ROWS(1, 0); break;
+      default: SONIQ_ACT_ROWS(1, 4); break;
+    }
   }
+#undef SONIQ_ACT_ROWS
   return hipGetLastError();
 }
 
