@@ -10,8 +10,9 @@
 // Output-channel plan (C1: one width per 16-row block): the channels of
 // each weight width, in original order, are cut into blocks of 16 (the
 // last block of a width padded with empty rows); all blocks of the narrow
-// width come first, then those of the wide width, then empty blocks up to a
-// multiple of 8 (one 128-column GEMM tile).  Blocks are contiguous, so a
+// width come first, padded with empty blocks to a multiple of 8 (one
+// 128-column GEMM tile), then those of the wide width, padded the same way.
+// So every GEMM tile holds one width, and since blocks are contiguous a
 // kernel derives any block's container and byte offset from the plan alone
 // (WPlan::nlo, c_lo, c_hi, ngt) without reading a table.
 #include <algorithm>
@@ -371,10 +372,11 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
   w->w_cnt[0] = (int64_t)rows_lo.size();
   w->w_cnt[1] = (int64_t)rows_hi.size();
   const int64_t nb_lo = (w->w_cnt[0] + kBlk - 1) / kBlk, nb_hi = (w->w_cnt[1] + kBlk - 1) / kBlk;
-  int64_t nblk = nb_lo + nb_hi;
-  nblk = round_up(nblk, kGemmBN / kBlk);
+  // with two widths the narrow blocks are padded to whole tiles
+  const int64_t nlo = nw == 2 ? round_up(nb_lo, kGemmBN / kBlk) : nb_lo;
+  const int64_t nblk = round_up(nlo + nb_hi, kGemmBN / kBlk);
   wp.nblk = (int)nblk;
-  wp.nlo = (int)nb_lo;
+  wp.nlo = (int)nlo;
   wp.Np = (int)(nblk * kBlk);
   w->blk_off_h.assign(nblk, 0);
   w->blk_c_h.assign(nblk, (uint8_t)wp.c_lo);
@@ -399,9 +401,10 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
       off += (uint64_t)wp.ngt * 128 * c;  // blocks are contiguous (the GEMM relies on it)
       ++b;
     };
-    while (il < nb_lo) place(rows_lo, il++, wp.c_lo);
-    while (ih < nb_hi) place(rows_hi, ih++, wp.c_hi);
     static const std::vector<int32_t> none;
+    while (il < nb_lo) place(rows_lo, il++, wp.c_lo);
+    while (b < nlo) place(none, 0, wp.c_lo);
+    while (ih < nb_hi) place(rows_hi, ih++, wp.c_hi);
     while (b < nblk) place(none, 0, wp.c_hi);
     w->packed_bytes = (int64_t)off;
     // Kernels derive block offsets from the plan; the table must agree.

@@ -24,6 +24,9 @@
 
 #include <hip/hip_bf16.h>
 
+#include <type_traits>
+#include <utility>
+
 #include <cstdlib>
 
 namespace soniq {
@@ -713,6 +716,258 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt(SONIQ_VMCNT_IMM(N));
 }
 
+// Buffer-resource offset past any buffer: the load returns zero without
+// touching memory.
+constexpr uint32_t kOOB = 0x7FFFFFF0u;
+
+// Fragment reads from the LDS ring are issued as inline asm.  The ring is
+// filled by direct global->LDS loads whose completion each wave awaits with
+// an explicit vmcnt wait and a barrier; through plain C++ loads the
+// compiler cannot tell the ring slots apart and drains every in-flight
+// load (vmcnt(0)) before each read, which serializes the pipeline.
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t lds_off(const uint8_t* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint8_t*)p);
+}
+
+// Packed unit (2*C bytes) at LDS byte address a + OFF, in a register type
+// of its size.
+template <int C>
+struct RawT { using type = uint32_t; };
+template <>
+struct RawT<4> { using type = u32x2v; };
+template <>
+struct RawT<8> { using type = u32x4v; };
+template <int C>
+using raw_t = typename RawT<C>::type;
+
+template <int C, int OFF>
+__device__ __forceinline__ raw_t<C> lds_unit(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  raw_t<C> r{};
+#if defined(__HIP_DEVICE_COMPILE__)  // GPU asm; the host pass never runs it
+  if constexpr (C == 8) asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+  else if constexpr (C == 4) asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+  else if constexpr (C == 2) asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+  else asm volatile("ds_read_u16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+#else
+  (void)a;
+#endif
+  return r;
+}
+
+// Waits for every LDS read in flight; each fragment is then passed through
+// an empty asm so that nothing using it can be scheduled above the wait.
+__device__ __forceinline__ void lds_wait() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#endif
+}
+template <typename T>
+__device__ __forceinline__ void lds_touch(T& r) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(r));
+#else
+  (void)r;
+#endif
+}
+
+__device__ __forceinline__ v4i frag_of(uint4 d) { return v4i{(int)d.x, (int)d.y, (int)d.z, (int)d.w}; }
+
+template <int C>
+__device__ __forceinline__ v4i unpack_frag(raw_t<C> r) {
+  if constexpr (C == 8) return frag_of(make_uint4(r.x, r.y, r.z, r.w));
+  else if constexpr (C == 4) return frag_of(unpack4(r.x, r.y));
+  else if constexpr (C == 2) return frag_of(unpack2(r));
+  else return frag_of(unpack1(r & 0xFFFFu));
+}
+
+template <int CA, int KK, int WFM, int... I>
+__device__ __forceinline__ void read_a_units(raw_t<CA> (&ra)[WFM], uint32_t a,
+                                             std::integer_sequence<int, I...>) {
+  ((ra[I] = lds_unit<CA, (I * 2 + KK) * 128 * CA>(a)), ...);
+}
+
+// B fragment jj of a granule: the block's container is CBL or CBH.
+template <int CBL, int CBH, int KK>
+__device__ __forceinline__ v4i b_frag(uint32_t addr, int c, bool) {
+  if constexpr (CBL == CBH) {
+    raw_t<CBL> r = lds_unit<CBL, KK * 128 * CBL>(addr);
+    lds_wait();
+    lds_touch(r);
+    return unpack_frag<CBL>(r);
+  } else {
+    if (c == CBL) {
+      raw_t<CBL> r = lds_unit<CBL, KK * 128 * CBL>(addr);
+      lds_wait();
+      lds_touch(r);
+      return unpack_frag<CBL>(r);
+    }
+    raw_t<CBH> r = lds_unit<CBH, KK * 128 * CBH>(addr);
+    lds_wait();
+    lds_touch(r);
+    return unpack_frag<CBH>(r);
+  }
+}
+
+// Granule KK of a stage for containers fixed at compile time: read and
+// widen the wave's 4 B units, then read its WFM A units and per A fragment
+// widen and issue its 4 MFMAs (two waits keep fewer raw units live).
+template <int CA, int CBL, int CBH, int WFM, int KK>
+__device__ __forceinline__ void mma_granule(v4i (&acc)[WFM][4], uint32_t a_addr,
+                                            const uint32_t (&b_addr)[4], const int (&wcj)[4],
+                                            bool) {
+  v4i bf[4];
+  if constexpr (CBL == CBH) {
+    raw_t<CBL> rb[4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) rb[jj] = lds_unit<CBL, KK * 128 * CBL>(b_addr[jj]);
+    lds_wait();
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      lds_touch(rb[jj]);
+      bf[jj] = unpack_frag<CBL>(rb[jj]);
+    }
+  } else {
+    // the mixed-width tile: one wait per fragment (rare)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) bf[jj] = b_frag<CBL, CBH, KK>(b_addr[jj], wcj[jj], false);
+  }
+  raw_t<CA> ra[WFM];
+  read_a_units<CA, KK>(ra, a_addr, std::make_integer_sequence<int, WFM>{});
+  lds_wait();
+#pragma unroll
+  for (int i = 0; i < WFM; ++i) {
+    lds_touch(ra[i]);
+    const v4i af = unpack_frag<CA>(ra[i]);
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf[jj], acc[i][jj], 0, 0, 0);
+  }
+}
+
+// One activation group's K loop for containers fixed at compile time (A in
+// CA, the tile's weight blocks in CBL or CBH; CBL == CBH for tiles of one
+// width).  Tile BM x 128 (BM = 32*WFM), waves 2x2, wave tile (16*WFM) x 64,
+// NST-deep LDS ring, stage = 2 granules, same LDS stage layout as the
+// generic loop.  Loads go through buffer resources: each lane's offsets are
+// fixed for the group and a scalar stage offset advances them (per lane on
+// the mixed-width tile); chunks past the data read as zero, which also
+// zeroes the second granule of a final half stage, so its products vanish.
+template <int CA, int CBL, int CBH, int WFM, int NST>
+__device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* abase,
+                                                int64_t mstride, int ng, const uint8_t* wtile,
+                                                int wbytes, int ngt, const int (&bc)[8],
+                                                const int (&bpre)[9], int qbase,
+                                                v4i (&acc)[WFM][4], int tid, int lane, int wid,
+                                                int wm, int wn) {
+#if defined(__HIP_DEVICE_COMPILE__)  // GPU builtins; the host pass never runs it
+  static_assert(CA == 4 || CA == 8, "activation container");
+  constexpr int BM = 32 * WFM;
+  constexpr int ASLOT = BM * 16 * 8;
+  constexpr int SLOT = ASLOT + kBSlot;
+  constexpr int LA = BM * CA / 256;                      // A loads per stage
+  constexpr int LB = CBH >= 2 ? CBH / 2 : 1;             // B loads per stage
+  constexpr int L = LA + LB;
+  constexpr bool UNI = CBL == CBH;
+  const int nst = (ng + 1) >> 1;
+  const int TB = bpre[8];  // B chunks per full stage
+
+  const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)abase, (short)0, (int)min((int64_t)0x7FFFFFF0, (int64_t)(BM / kBlk) * mstride), 0x00020000);
+  const __amdgpu_buffer_rsrc_t br =
+      __builtin_amdgcn_make_buffer_rsrc((void*)wtile, (short)0, wbytes, 0x00020000);
+
+  // A chunk ci = i*256 + tid of a stage: m-block ci / (16*CA), byte
+  // (ci mod 16*CA)*16 of the stage's 256*CA bytes; second granule when that
+  // byte is >= 128*CA.
+  uint32_t aoff[LA];
+  bool asec[LA];
+#pragma unroll
+  for (int i = 0; i < LA; ++i) {
+    const int ci = i * 256 + tid;
+    const int mb = ci / (16 * CA), w = ci - mb * 16 * CA;
+    aoff[i] = (uint32_t)(mb * mstride + w * 16);
+    asec[i] = w >= 8 * CA;
+  }
+  // B chunk ci: block j (bpre[j] <= ci < bpre[j+1]), container c_j.
+  uint32_t boff[LB];
+  uint32_t bstep[LB];
+  bool bsec[LB], bval[LB];
+#pragma unroll
+  for (int i = 0; i < LB; ++i) {
+    const int ci = i * 256 + tid;
+    int pj = 0, cj = bc[0];
+#pragma unroll
+    for (int t = 1; t < 8; ++t) {
+      const bool in = ci >= bpre[t];
+      pj += in ? bpre[t] - bpre[t - 1] : 0;
+      cj += in ? bc[t] - bc[t - 1] : 0;
+    }
+    // block j starts ngt*128*(sum of earlier c) = ngt*8*pj bytes in
+    boff[i] = (uint32_t)(ngt * 8 * pj + qbase * 128 * cj + (ci - pj) * 16);
+    bstep[i] = 256 * cj;
+    bsec[i] = ci - pj >= 8 * cj;
+    bval[i] = ci < TB;
+  }
+
+  auto issue = [&](int st, int slot) __attribute__((always_inline)) {
+    const bool half = 2 * st + 1 >= ng;  // final stage holds one granule
+    const uint32_t ldsb = lds_off(lds) + (uint32_t)(slot * SLOT);
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ar, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + (i * 256 + wid * 64) * 16), 16,
+          half && asec[i] ? kOOB : aoff[i], st * 256 * CA, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+      const bool skip = !bval[i] || (half && bsec[i]);
+      const uint32_t vo = UNI ? boff[i] : boff[i] + (uint32_t)st * bstep[i];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          br, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + ASLOT + (i * 256 + wid * 64) * 16), 16,
+          skip ? kOOB : vo, UNI ? st * 256 * CBL : 0, 0, 0);
+    }
+  };
+
+  // The wave's four weight blocks: container (wave-uniform) and this lane's
+  // unit address in granule 0 of slot 0.
+  int wcj[4];
+  uint32_t b_lds[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    wcj[jj] = UNI ? CBL : __builtin_amdgcn_readfirstlane(wn ? bc[4 + jj] : bc[jj]);
+    b_lds[jj] = lds_off(lds) + (uint32_t)(ASLOT + (wn ? bpre[4 + jj] : bpre[jj]) * 16 + lane * 2 * wcj[jj]);
+  }
+  const uint32_t a_lds = lds_off(lds) + (uint32_t)(lane * 2 * CA + wm * WFM * 2 * 128 * CA);
+
+  int issued = 0;
+  for (; issued < NST - 1 && issued < nst; ++issued) issue(issued, issued);
+  for (int st = 0; st < nst; ++st) {
+    // Stages issued after st: at most NST - 2.
+    const int later = issued - st - 1;
+    if (NST >= 6 && later >= 4) wait_vm<(NST >= 6 ? 4 * L : 0)>();
+    else if (NST >= 5 && later == 3) wait_vm<(NST >= 5 ? 3 * L : 0)>();
+    else if (NST >= 4 && later == 2) wait_vm<(NST >= 4 ? 2 * L : 0)>();
+    else if (NST >= 3 && later == 1) wait_vm<(NST >= 3 ? L : 0)>();
+    else wait_vm<0>();
+    bar_nofence();
+    if (issued < nst) {
+      issue(issued, issued % NST);
+      ++issued;
+    }
+    const uint32_t soff = (uint32_t)((st % NST) * SLOT);
+    const uint32_t b_addr[4] = {b_lds[0] + soff, b_lds[1] + soff, b_lds[2] + soff, b_lds[3] + soff};
+    mma_granule<CA, CBL, CBH, WFM, 0>(acc, a_lds + soff, b_addr, wcj, false);
+    mma_granule<CA, CBL, CBH, WFM, 1>(acc, a_lds + soff, b_addr, wcj, false);
+  }
+  // Everyone is done reading the ring before the next group refills it.
+  bar_nofence();
+#endif
+}
+
 // One activation group's K loop of a BM x 128 tile (BM = 32*WFM; waves 2x2,
 // wave tile (16*WFM) x 64), through an NST-deep LDS ring.  Stage = 2
 // granules.  A stage in LDS: m-block i granule kk at (2i + kk)*128*ca; B
@@ -721,7 +976,7 @@ __device__ __forceinline__ void wait_vm() {
 // re-load one valid chunk into an unused slot), so each wait is a
 // compile-time vmcnt.
 template <int CA, int CBL, int CBH, int WFM, int NST>
-__device__ __forceinline__ void gemm_group(uint8_t* lds, const uint8_t* abase, int64_t mstride,
+__device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abase, int64_t mstride,
                                            int ca_rt, int ng, const uint8_t* wtile, int ngt,
                                            const int (&bc)[8], const int (&bpre)[9], int qbase,
                                            v4i (&acc)[WFM][4], int tid, int lane, int wid,
@@ -808,44 +1063,41 @@ __device__ __forceinline__ void gemm_group(uint8_t* lds, const uint8_t* abase, i
   for (int st = 0; st < nst; ++st) {
     // Stages issued after st: at most NST - 2.
     const int later = issued - st - 1;
-    if constexpr (NST >= 4) {
-      if (later >= 2) wait_vm<2 * L>();
-      else if (later == 1) wait_vm<L>();
-      else wait_vm<0>();
-    } else if constexpr (NST == 3) {
-      if (later >= 1) wait_vm<L>();
-      else wait_vm<0>();
-    } else {
-      wait_vm<0>();
-    }
+    if (NST >= 6 && later >= 4) wait_vm<(NST >= 6 ? 4 * L : 0)>();
+    else if (NST >= 5 && later == 3) wait_vm<(NST >= 5 ? 3 * L : 0)>();
+    else if (NST >= 4 && later == 2) wait_vm<(NST >= 4 ? 2 * L : 0)>();
+    else if (NST >= 3 && later == 1) wait_vm<(NST >= 3 ? L : 0)>();
+    else wait_vm<0>();
     bar_nofence();
     if (issued < nst) {
       issue(issued, issued % NST);
       ++issued;
     }
     const int slot = st % NST;
-    const uint8_t* As = lds + slot * SLOT + lane * 2 * ca;
-    const uint8_t* Bs = lds + slot * SLOT + ASLOT;
     // Both granules of the stage run unconditionally; in a final half stage
     // the second granule's A fragments are zeroed, so its products vanish
     // whatever its slot holds.
     const bool second = 2 * st + 1 < ng;
+    {
+      const uint8_t* As = lds + slot * SLOT + lane * 2 * ca;
+      const uint8_t* Bs = lds + slot * SLOT + ASLOT;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      v4i af[WFM], bf[4];
+      for (int kk = 0; kk < 2; ++kk) {
+        v4i af[WFM], bf[4];
 #pragma unroll
-      for (int i = 0; i < WFM; ++i) {
-        const v4i f = read_frag_a<CA>(As + ((wm * WFM + i) * 2 + kk) * 128 * ca, 0, ca);
-        af[i] = (kk == 0 || second) ? f : v4i{0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-        bf[jj] = read_frag_w<CBL, CBH>(Bs + wlo[jj] + kk * 128 * wcj[jj], 0, wcj[jj]);
-#pragma unroll
-      for (int i = 0; i < WFM; ++i)
+        for (int i = 0; i < WFM; ++i) {
+          const v4i f = read_frag_a<CA>(As + ((wm * WFM + i) * 2 + kk) * 128 * ca, 0, ca);
+          af[i] = (kk == 0 || second) ? f : v4i{0, 0, 0, 0};
+        }
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
-          acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[jj], acc[i][jj], 0, 0, 0);
+          bf[jj] = read_frag_w<CBL, CBH>(Bs + wlo[jj] + kk * 128 * wcj[jj], 0, wcj[jj]);
+#pragma unroll
+        for (int i = 0; i < WFM; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[jj], acc[i][jj], 0, 0, 0);
+      }
     }
   }
   // Everyone is done reading the ring before the next group refills it.
@@ -881,18 +1133,35 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   for (int i = 0; i < WFM; ++i)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) acc0[i][jj] = v4i{0, 0, 0, 0};
-  gemm_group<CA0, CBL, CBH, WFM, NST>(lds, a.act + ap.seg_off[0] + (m0 / kBlk) * ap.mblk_bytes[0],
-                                      ap.mblk_bytes[0], ap.c[0], ap.ng[0], wtile, a.wp.ngt, bc,
-                                      bpre, 0, acc0, tid, lane, wid, wm, wn);
+  // Every tile holds one weight width (the plan pads the narrow blocks to
+  // whole tiles), so the loop runs with that container fixed.
+  const int wbytes = (int)(wblk_off(a.wp, jb0 + 8) - wblk_off(a.wp, jb0));
+  const bool tile_lo = jb0 < a.wp.nlo;
+  auto run_group = [&](auto ca_tag, const uint8_t* abase, int64_t mstride, int ca_rt, int ng,
+                       int qbase, v4i (&acc)[WFM][4]) __attribute__((always_inline)) {
+    constexpr int CA = decltype(ca_tag)::value;
+    if constexpr (CA != 0 && CBL != 0 && CBH != 0) {
+      if (CBL == CBH || tile_lo)
+        gemm_group_fast<CA, CBL, CBL, WFM, NST>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
+                                                bc, bpre, qbase, acc, tid, lane, wid, wm, wn);
+      else
+        gemm_group_fast<CA, CBH, CBH, WFM, NST>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
+                                                bc, bpre, qbase, acc, tid, lane, wid, wm, wn);
+    } else {
+      gemm_group_any<CA, CBL, CBH, WFM, NST>(lds, abase, mstride, ca_rt, ng, wtile, a.wp.ngt, bc,
+                                             bpre, qbase, acc, tid, lane, wid, wm, wn);
+    }
+  };
+  run_group(std::integral_constant<int, CA0>{}, a.act + ap.seg_off[0] + (m0 / kBlk) * ap.mblk_bytes[0],
+            ap.mblk_bytes[0], ap.c[0], ap.ng[0], 0, acc0);
   v4i acc1[WFM][4];
 #pragma unroll
   for (int i = 0; i < WFM; ++i)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) acc1[i][jj] = v4i{0, 0, 0, 0};
   if constexpr (S == 2)
-    gemm_group<CA1, CBL, CBH, WFM, NST>(lds, a.act + ap.seg_off[1] + (m0 / kBlk) * ap.mblk_bytes[1],
-                                        ap.mblk_bytes[1], ap.c[1], ap.ng[1], wtile, a.wp.ngt, bc,
-                                        bpre, ap.ng[0], acc1, tid, lane, wid, wm, wn);
+    run_group(std::integral_constant<int, CA1>{}, a.act + ap.seg_off[1] + (m0 / kBlk) * ap.mblk_bytes[1],
+              ap.mblk_bytes[1], ap.c[1], ap.ng[1], ap.ng[0], acc1);
 
   // Epilogue: exact int32 per group, fixed-order fp32 scaling, bf16.  The
   // tile is staged in LDS (the ring is free: gemm_group ended with a
@@ -1150,7 +1419,6 @@ __global__ __launch_bounds__(256) void k_gemv_any(GemmArgs a) {
 //   - otherwise bytes and v_dot4_i32_i8.
 // Lanes of a 16-lane DPP row that share output rows are summed with
 // row_ror; the four rows of a wave and the four waves meet in LDS.
-constexpr uint32_t kOOB = 0x7FFFFFF0u;  // buffer offset past any block
 
 __device__ __forceinline__ int dot16n(uint32_t w0, uint32_t w1, uint2 x, int v) {
   v = __builtin_amdgcn_sdot8((int)w0, (int)x.x, v, false);
@@ -1537,35 +1805,33 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   return a;
 }
 
-// Tile shape: 0 = 256x128 (WFM 8, 3-deep ring), 1 = 128x128 (WFM 4, 3-deep),
-// 2 = 64x128 (WFM 2, 3-deep), 3 = 128x128 (WFM 4, 2-deep, two workgroups
-// per CU).
+// Tile shapes: 3 = 128x128 (WFM 4, 2-deep ring, two workgroups per CU),
+// 7 = 64x128 (WFM 2, 2-deep, three per CU), 2 = 64x128 (WFM 2, 3-deep).
 template <int S, int CA0, int CA1, int CBL, int CBH>
 static void launch_gemm_t(const GemmArgs& a, int64_t M, int shape, hipStream_t stream) {
   const int ntn = a.wp.Np / kGemmBN;
   const dim3 blk(256);
   switch (shape) {
-    case 0:
-      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 8, 3>), dim3((unsigned)(((M + 255) / 256) * ntn)), blk, 0, stream, a);
-      break;
-    case 1:
-      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 4, 3>), dim3((unsigned)(((M + 127) / 128) * ntn)), blk, 0, stream, a);
-      break;
     case 3:
       hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 4, 2>), dim3((unsigned)(((M + 127) / 128) * ntn)), blk, 0, stream, a);
       break;
-    default:
+    case 2:
       hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 3>), dim3((unsigned)(((M + 63) / 64) * ntn)), blk, 0, stream, a);
+      break;
+    default:
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2>), dim3((unsigned)(((M + 63) / 64) * ntn)), blk, 0, stream, a);
       break;
   }
 }
 
+// 128x128 tiles when there are enough of them to keep every CU busy for
+// several rounds; otherwise 64x128 tiles, three workgroups per CU, which
+// hide latency better on smaller problems.  SONIQ_GEMM_SHAPE (2, 3 or 7)
+// overrides the choice for measurement; results do not depend on it.
 static int gemm_shape(int64_t M, int ntn) {
   if (const char* e = getenv("SONIQ_GEMM_SHAPE")) return atoi(e);
-  // 128x128 tiles, two workgroups per CU, when there are enough of them to
-  // fill the chip twice; otherwise 64x128 tiles for more workgroups.
-  if (((M + 127) / 128) * ntn >= 512) return 3;
-  return 2;
+  if (((M + 127) / 128) * ntn >= 1024) return 3;
+  return 7;
 }
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
