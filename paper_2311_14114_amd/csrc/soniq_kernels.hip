@@ -167,6 +167,28 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   return r;
 }
 
+// Maxima of two values over the workgroup (one pair of barriers).
+__device__ __forceinline__ float2 block_max2(float2 v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    v.x = fmaxf(v.x, __shfl_xor(v.x, o, 64));
+    v.y = fmaxf(v.y, __shfl_xor(v.y, o, 64));
+  }
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) {
+    red[2 * wid] = v.x;
+    red[2 * wid + 1] = v.y;
+  }
+  __syncthreads();
+  float2 r = make_float2(red[0], red[1]);
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) {
+    r.x = fmaxf(r.x, red[2 * i]);
+    r.y = fmaxf(r.y, red[2 * i + 1]);
+  }
+  return r;
+}
+
 __device__ __forceinline__ int block_sum(int v, int* red) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -249,26 +271,25 @@ __device__ __forceinline__ void max4(float4 v, uchar4 g, float& mx0, float& mx1)
 
 __device__ __forceinline__ void write_partial(float mx0, float mx1, float* red,
                                               float* __restrict__ partial) {
-  mx0 = block_max(mx0, red);
-  mx1 = block_max(mx1, red);
+  const float2 m = block_max2(make_float2(mx0, mx1), red);
   if (threadIdx.x == 0) {
-    partial[2 * blockIdx.x] = mx0;
-    partial[2 * blockIdx.x + 1] = mx1;
+    partial[2 * blockIdx.x] = m.x;
+    partial[2 * blockIdx.x + 1] = m.y;
   }
 }
 
 // Rows with K % 4 == 0, lda % 4 == 0, 16-byte aligned.  Workgroup b takes
-// RB consecutive rows (RB a multiple of 4); thread tid owns float4
-// positions k4 = base + 256*j of every row, keeps their running |max| over
-// the rows (one v_max per element, four rows of loads in flight), and folds
-// them into the two group maxima once per position batch.  Clamped rows and
-// positions re-read in-bounds data already counted, which a max ignores.
-template <int J>
+// RB consecutive rows; thread tid owns float4 positions k4 = base + 256*j
+// of every row, loads all RB rows of them at once, keeps their |max| over
+// the rows (one v_max per element) and folds them into the two group
+// maxima once per position batch.  Clamped rows and positions re-read
+// in-bounds data already counted, which a max ignores.
+template <int J, int RB>
 __global__ __launch_bounds__(256) void k_absmax_blk(const float4* __restrict__ A, int64_t M,
-                                                    int K4, int64_t lda4, int RB,
+                                                    int K4, int64_t lda4,
                                                     const uchar4* __restrict__ seg4,
                                                     float* __restrict__ partial) {
-  __shared__ float red[4];
+  __shared__ float red[8];
   const int tid = threadIdx.x;
   const int64_t m0 = (int64_t)blockIdx.x * RB;
   const int rows = (int)min((int64_t)RB, M - m0);
@@ -277,27 +298,25 @@ __global__ __launch_bounds__(256) void k_absmax_blk(const float4* __restrict__ A
     int k4[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) k4[j] = min(base + 256 * j + tid, K4 - 1);
+    float4 v[RB][J];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      const float4* row = A + (m0 + min(r, rows - 1)) * lda4;
+#pragma unroll
+      for (int j = 0; j < J; ++j) v[r][j] = row[k4[j]];
+    }
     float4 mx[J];
 #pragma unroll
     for (int j = 0; j < J; ++j) mx[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int r0 = 0; r0 < rows; r0 += 4) {
-      float4 v[4][J];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float4* row = A + (m0 + min(r0 + r, rows - 1)) * lda4;
+    for (int r = 0; r < RB; ++r)
 #pragma unroll
-        for (int j = 0; j < J; ++j) v[r][j] = row[k4[j]];
+      for (int j = 0; j < J; ++j) {
+        mx[j].x = fmaxf(mx[j].x, fabsf(v[r][j].x));
+        mx[j].y = fmaxf(mx[j].y, fabsf(v[r][j].y));
+        mx[j].z = fmaxf(mx[j].z, fabsf(v[r][j].z));
+        mx[j].w = fmaxf(mx[j].w, fabsf(v[r][j].w));
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int j = 0; j < J; ++j) {
-          mx[j].x = fmaxf(mx[j].x, fabsf(v[r][j].x));
-          mx[j].y = fmaxf(mx[j].y, fabsf(v[r][j].y));
-          mx[j].z = fmaxf(mx[j].z, fabsf(v[r][j].z));
-          mx[j].w = fmaxf(mx[j].w, fabsf(v[r][j].w));
-        }
-    }
 #pragma unroll
     for (int j = 0; j < J; ++j) max4(mx[j], seg4[k4[j]], mx0, mx1);
   }
@@ -309,7 +328,7 @@ __global__ __launch_bounds__(256) void k_absmax_rows(const float* __restrict__ A
                                                      int64_t K, int64_t lda,
                                                      const uint8_t* __restrict__ seg,
                                                      float* __restrict__ partial) {
-  __shared__ float red[4];
+  __shared__ float red[8];
   float mx0 = 0.0f, mx1 = 0.0f;
   for (int64_t m = blockIdx.x; m < M; m += gridDim.x) {
     const float* row = A + m * lda;
@@ -332,8 +351,9 @@ __device__ __forceinline__ void scales_from_partials(const float* __restrict__ p
     r0 = fmaxf(r0, v.x);
     r1 = fmaxf(r1, v.y);
   }
-  r0 = block_max(r0, red);
-  r1 = block_max(r1, red);
+  const float2 rr = block_max2(make_float2(r0, r1), red);
+  r0 = rr.x;
+  r1 = rr.y;
   s0 = group_scale(r0, ap.q[0]);
   s1 = ap.S == 2 ? group_scale(r1, ap.q[1]) : 0.0f;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -449,12 +469,46 @@ __device__ __forceinline__ QElem qelem(float s, const QParam& q, int zp) {
 // tie (or when the shortcut is off, rs NaN) the exact IEEE quotient decides.
 constexpr float kTieBand = 0x1p-12f;
 
-__device__ __forceinline__ int qstore(float x, float rs, float lo, float hi, float zp, float s) {
+// Shortcut code (stored code = code - zp) and whether x/s lies in the band.
+__device__ __forceinline__ int qfast(float x, float rs, float lo, float hi, float zp, bool& near) {
   const float e = x * rs;
-  float t = __builtin_rintf(e);
-  if (!(fabsf(fabsf(e - t) - 0.5f) > kTieBand)) [[unlikely]]
-    t = s == 0.0f ? 0.0f : __builtin_rintf(__fdiv_rn(x, s));
+  const float t = __builtin_rintf(e);
+  near = !(fabsf(fabsf(e - t) - 0.5f) > kTieBand);
   return (int)__builtin_amdgcn_fmed3f(t - zp, lo, hi);
+}
+
+__device__ __forceinline__ int qexact(float x, float lo, float hi, float zp, float s) {
+  const float t = s == 0.0f ? 0.0f : __builtin_rintf(__fdiv_rn(x, s));
+  return (int)__builtin_amdgcn_fmed3f(t - zp, lo, hi);
+}
+
+__device__ __forceinline__ int qstore(float x, float rs, float lo, float hi, float zp, float s) {
+  bool near;
+  const int c = qfast(x, rs, lo, hi, zp, near);
+  return near ? qexact(x, lo, hi, zp, s) : c;
+}
+
+// Four elements sharing one branch for the rare exact path.
+struct QE4 {
+  float rs[4], lo[4], hi[4], zp[4], s[4];
+};
+
+__device__ __forceinline__ void qstore4(const float4& v, const QE4& q, uint8_t* row, int4 p) {
+  bool n0, n1, n2, n3;
+  int c0 = qfast(v.x, q.rs[0], q.lo[0], q.hi[0], q.zp[0], n0);
+  int c1 = qfast(v.y, q.rs[1], q.lo[1], q.hi[1], q.zp[1], n1);
+  int c2 = qfast(v.z, q.rs[2], q.lo[2], q.hi[2], q.zp[2], n2);
+  int c3 = qfast(v.w, q.rs[3], q.lo[3], q.hi[3], q.zp[3], n3);
+  if ((n0 | n1 | n2 | n3)) [[unlikely]] {
+    if (n0) c0 = qexact(v.x, q.lo[0], q.hi[0], q.zp[0], q.s[0]);
+    if (n1) c1 = qexact(v.y, q.lo[1], q.hi[1], q.zp[1], q.s[1]);
+    if (n2) c2 = qexact(v.z, q.lo[2], q.hi[2], q.zp[2], q.s[2]);
+    if (n3) c3 = qexact(v.w, q.lo[3], q.hi[3], q.zp[3], q.s[3]);
+  }
+  row[p.x] = (uint8_t)c0;
+  row[p.y] = (uint8_t)c1;
+  row[p.z] = (uint8_t)c2;
+  row[p.w] = (uint8_t)c3;
 }
 
 // ------------------------------------------------------------ k_act_rows --
@@ -492,24 +546,19 @@ __device__ __forceinline__ void act_rows_quant(uint8_t* codes, int Kp, int rows,
   for (int j = 0; j < J; ++j) {
     if (base + 256 * j < K4) {
       const uchar4 h = g[j];
-      const QElem& ex = h.x ? q1 : q0;
-      const QElem& ey = h.y ? q1 : q0;
-      const QElem& ez = h.z ? q1 : q0;
-      const QElem& ew = h.w ? q1 : q0;
-      const float rsx = ex.rs, lox = ex.lo, hix = ex.hi, zpx = ex.zp, sx = ex.s;
-      const float rsy = ey.rs, loy = ey.lo, hiy = ey.hi, zpy = ey.zp, sy = ey.s;
-      const float rsz = ez.rs, loz = ez.lo, hiz = ez.hi, zpz = ez.zp, sz = ez.s;
-      const float rsw = ew.rs, low = ew.lo, hiw = ew.hi, zpw = ew.zp, sw = ew.s;
+      QE4 q;
+      const bool hv[4] = {h.x != 0, h.y != 0, h.z != 0, h.w != 0};
 #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        if (r < rows) {
-          uint8_t* row = codes + r * Kp;
-          row[p[j].x] = (uint8_t)qstore(v[r][j].x, rsx, lox, hix, zpx, sx);
-          row[p[j].y] = (uint8_t)qstore(v[r][j].y, rsy, loy, hiy, zpy, sy);
-          row[p[j].z] = (uint8_t)qstore(v[r][j].z, rsz, loz, hiz, zpz, sz);
-          row[p[j].w] = (uint8_t)qstore(v[r][j].w, rsw, low, hiw, zpw, sw);
-        }
+      for (int e = 0; e < 4; ++e) {
+        q.rs[e] = hv[e] ? q1.rs : q0.rs;
+        q.lo[e] = hv[e] ? q1.lo : q0.lo;
+        q.hi[e] = hv[e] ? q1.hi : q0.hi;
+        q.zp[e] = hv[e] ? q1.zp : q0.zp;
+        q.s[e] = hv[e] ? q1.s : q0.s;
       }
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if (r < rows) qstore4(v[r][j], q, codes + r * Kp, p[j]);
     }
   }
 }
@@ -523,7 +572,7 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
                                                   float* __restrict__ s_a_out,
                                                   uint8_t* __restrict__ packed) {
   extern __shared__ __align__(16) uint8_t codes[];
-  __shared__ float red[4];
+  __shared__ float red[8];
   const int64_t m0 = (int64_t)blockIdx.x * R;
   const int rows = (int)min((int64_t)R, M - m0);
   const int tid = threadIdx.x;
@@ -571,7 +620,7 @@ __global__ __launch_bounds__(256) void k_act_small(const float* __restrict__ A, 
                                                    float* __restrict__ s_a_out,
                                                    uint8_t* __restrict__ packed) {
   extern __shared__ __align__(16) uint8_t codes[];
-  __shared__ float red[4];
+  __shared__ float red[8];
   const int tid = threadIdx.x;
   const int K4 = K / 4;
   const int total4 = M * K4;
@@ -1735,24 +1784,26 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
     return hipGetLastError();
   }
   int nparts;
-  if (aligned) {
-    // rows per workgroup: a multiple of 4 keeping the grid within the
-    // partial buffer (kAbsmaxBlocks workgroups)
+  if (aligned && M <= 16 * (int64_t)kAbsmaxBlocks) {
+    // 8 (or 16) rows per workgroup keep the grid within the partial buffer
     const int K4 = (int)(K / 4);
-    const int64_t RB = 4 * ((M + 4 * kAbsmaxBlocks - 1) / (4 * kAbsmaxBlocks));
+    const int RB = M <= 8 * (int64_t)kAbsmaxBlocks ? 8 : 16;
     const int64_t blocks = (M + RB - 1) / RB;
     nparts = (int)blocks;
     const int J = K4 <= 256 ? 1 : K4 <= 512 ? 2 : K4 <= 768 ? 3 : 4;
     const float4* A4 = reinterpret_cast<const float4*>(A);
     const uchar4* s4 = reinterpret_cast<const uchar4*>(seg_dev);
-    if (J == 1)
-      hipLaunchKernelGGL(k_absmax_blk<1>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
-    else if (J == 2)
-      hipLaunchKernelGGL(k_absmax_blk<2>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
-    else if (J == 3)
-      hipLaunchKernelGGL(k_absmax_blk<3>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
-    else
-      hipLaunchKernelGGL(k_absmax_blk<4>, dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, K4, lda / 4, (int)RB, s4, partial);
+#define SONIQ_ABSMAX(J_, RB_)                                                                   \
+  hipLaunchKernelGGL((k_absmax_blk<J_, RB_>), dim3((unsigned)blocks), dim3(256), 0, stream, A4, M, \
+                     K4, lda / 4, s4, partial)
+    if (RB == 8) {
+      if (J == 1) SONIQ_ABSMAX(1, 8); else if (J == 2) SONIQ_ABSMAX(2, 8);
+      else if (J == 3) SONIQ_ABSMAX(3, 8); else SONIQ_ABSMAX(4, 8);
+    } else {
+      if (J == 1) SONIQ_ABSMAX(1, 16); else if (J == 2) SONIQ_ABSMAX(2, 16);
+      else SONIQ_ABSMAX(2, 16);
+    }
+#undef SONIQ_ABSMAX
   } else {
     const int64_t blocks = M < kAbsmaxBlocks ? M : kAbsmaxBlocks;
     nparts = (int)blocks;
@@ -1770,7 +1821,16 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   hipLaunchKernelGGL((k_act_rows<R_, J_>), dim3((unsigned)((M + R_ - 1) / R_)), dim3(256),      \
                      (size_t)R_ * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,    \
                      nparts, s_a, packed)
-  if (4 * (int64_t)ap.Kp <= 64 * 1024) {
+  // 8 rows per workgroup when 4 would need more than about one round of
+  // workgroups on the chip (loads of all rows are issued at once)
+  const bool r8 = false;
+  if (r8) {
+    switch (J) {
+      case 1: SONIQ_ACT_ROWS(8, 1); break;
+      case 2: SONIQ_ACT_ROWS(8, 2); break;
+      default: SONIQ_ACT_ROWS(8, 3); break;
+    }
+  } else if (4 * (int64_t)ap.Kp <= 64 * 1024) {
     switch (J) {
       case 0: SONIQ_ACT_ROWS(4, 0); break;
       case 1: SONIQ_ACT_ROWS(4, 1); break;
