@@ -126,6 +126,9 @@ EDGE = [  # (M, N, K, a_lo, a_hi, w_lo, w_hi, a_signed)
     (3, 64, 4095, 4, 8, 2, 4, True),
     (150, 100, 129, 1, 8, 1, 2, True),     # sign-bit x sign-bit padding, GEMM path
     (20, 70, 65, 1, 1, 1, 1, True),        # all channels 1-bit
+    (1030, 100, 300, 4, 8, 2, 4, True),    # 16-row block quantizer, ragged last block
+    (1041, 70, 260, 4, 8, 1, 4, False),    # unsigned, ragged
+    (1024, 64, 1028, 4, 8, 4, 8, True),    # two position slots per thread
 ]
 
 
