@@ -610,17 +610,21 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
 // at codes + r*Kp + gbase): granule q holds units l = kg*16 + r of 2C bytes
 // (128C contiguous bytes); 16-byte piece w holds units w*U .. w*U+U-1
 // (U = 8/C), i.e. rows of one 16-channel group.
-template <int C>
+template <int C, int RB>
 __device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int Kp, int gbase, int ng,
-                                                   uint8_t* __restrict__ dst) {
-  constexpr int U = 8 / C;
-  const int npieces = ng * 8 * C;
+                                                   int r0, uint8_t* __restrict__ dst) {
+  constexpr int U = 8 / C;            // units per piece
+  constexpr int PK = RB / U > 0 ? RB / U : 1;  // pieces per 16-channel group
+  static_assert(RB % U == 0, "row range covers whole pieces");
+  const int npieces = ng * 4 * PK;
   for (int i = threadIdx.x; i < npieces; i += blockDim.x) {
-    const int q = i / (8 * C), w = i - q * 8 * C;
+    const int q = i / (4 * PK), rem = i - q * 4 * PK;
+    const int kg = rem / PK, pr = rem - kg * PK;
+    const int w = (kg * 16 + r0) / U + pr;  // piece within the granule
     uint32_t wd[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int l = w * U + u, kg = l >> 4, r = l & 15;
+      const int l = w * U + u, r = (l & 15) - r0;
       const uint4 d = *reinterpret_cast<const uint4*>(codes + r * Kp + gbase + q * kGran + kg * 16);
       const uint4 pk = pack_unit(d.x, d.y, d.z, d.w, C);
       if constexpr (C == 8) {
@@ -633,20 +637,20 @@ __device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int Kp,
         wd[u >> 1] |= (pk.x & 0xFFFFu) << (16 * (u & 1));
       }
     }
-    *reinterpret_cast<uint4*>(dst + (int64_t)i * 16) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+    *reinterpret_cast<uint4*>(dst + (int64_t)(q * 8 * C + w) * 16) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
   }
 }
 
 // ----------------------------------------------------------- k_act_blk16 --
-// One 16-row block per workgroup (aligned rows, no sign-code group): the
-// rows go through in four batches of four, the next batch's loads in
-// flight while the current one is quantized into LDS; the partial maxima
-// are reduced once per block; the block's packed units are then written as
-// whole 16-byte pieces of its contiguous granule runs (coalesced, full
-// lines).  Rows past M are clamped to row M-1 (in bounds) and their units
-// land in the block's padding rows, which no consumer reads.
-// Dynamic LDS: 16*Kp bytes.
-template <int J>
+// RB rows (8 or 16, aligned to a 16-row block) per workgroup, aligned rows,
+// no sign-code group: the rows go through in batches of four, the next
+// batch's loads in flight while the current one is quantized into LDS; the
+// partial maxima are reduced once; the rows' packed units are then written
+// as whole 16-byte pieces (each 16-channel group's units of these rows are
+// contiguous).  Rows past M are clamped to row M-1 (in bounds) and their
+// units land in padding rows, which no consumer reads.
+// Dynamic LDS: RB*Kp bytes.
+template <int J, int RB>
 __global__ __launch_bounds__(256) void k_act_blk16(const float* __restrict__ A, int64_t M,
                                                    int64_t K, int64_t lda,
                                                    const int32_t* __restrict__ pos,
@@ -654,16 +658,17 @@ __global__ __launch_bounds__(256) void k_act_blk16(const float* __restrict__ A, 
                                                    const float* __restrict__ partial, int nparts,
                                                    float* __restrict__ s_a_out,
                                                    uint8_t* __restrict__ packed) {
+  static_assert(RB == 8 || RB == 16, "row batch");
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
-  const int64_t m0 = (int64_t)blockIdx.x * kBlk;
-  const int rows = (int)min((int64_t)kBlk, M - m0);
+  const int64_t m0 = (int64_t)blockIdx.x * RB;
+  const int rows = (int)min((int64_t)RB, M - m0);
   const int tid = threadIdx.x;
   const int K4 = (int)(K / 4);
   int4 p[J];
   uchar4 g[J];
   float4 va[4][J], vb[4][J];
-  // batch b holds rows 4b..4b+3 (clamped into the block's valid rows)
+  // batch b holds rows 4b..4b+3 (clamped into the valid rows)
   auto load = [&](float4 (&v)[4][J], int b) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
@@ -682,28 +687,30 @@ __global__ __launch_bounds__(256) void k_act_blk16(const float* __restrict__ A, 
   }
   load(vb, 1);
   uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
-  for (int i = tid; i < kBlk * ap.Kp / 4; i += 256) codes32[i] = 0;
+  for (int i = tid; i < RB * ap.Kp / 4; i += 256) codes32[i] = 0;
   float s0, s1;
   scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
   const QElem q0 = qelem(s0, ap.q[0], ap.zp[0]), q1 = qelem(s1, ap.q[1], ap.zp[1]);
   act_rows_quant<4, J>(codes, ap.Kp, 4, K4, tid, p, g, va, q0, q1);
-  load(va, 2);
+  if constexpr (RB == 16) load(va, 2);
   act_rows_quant<4, J>(codes + 4 * ap.Kp, ap.Kp, 4, K4, tid, p, g, vb, q0, q1);
-  load(vb, 3);
-  act_rows_quant<4, J>(codes + 8 * ap.Kp, ap.Kp, 4, K4, tid, p, g, va, q0, q1);
-  act_rows_quant<4, J>(codes + 12 * ap.Kp, ap.Kp, 4, K4, tid, p, g, vb, q0, q1);
+  if constexpr (RB == 16) {
+    load(vb, 3);
+    act_rows_quant<4, J>(codes + 8 * ap.Kp, ap.Kp, 4, K4, tid, p, g, va, q0, q1);
+    act_rows_quant<4, J>(codes + 12 * ap.Kp, ap.Kp, 4, K4, tid, p, g, vb, q0, q1);
+  }
   __syncthreads();
-  // Group g's units of this block, written as whole 16-byte pieces.
+  const int r0 = (int)(m0 % kBlk);
   for (int gi = 0; gi < ap.S; ++gi) {
     const int c = gi ? ap.c[1] : ap.c[0];
     const int ng = gi ? ap.ng[1] : ap.ng[0];
     const int gbase = gi ? ap.kpad[0] : 0;
     uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
                    (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
-    if (c == 8) write_block_pieces<8>(codes, ap.Kp, gbase, ng, dst);
-    else if (c == 4) write_block_pieces<4>(codes, ap.Kp, gbase, ng, dst);
-    else if (c == 2) write_block_pieces<2>(codes, ap.Kp, gbase, ng, dst);
-    else write_block_pieces<1>(codes, ap.Kp, gbase, ng, dst);
+    if (c == 8) write_block_pieces<8, RB>(codes, ap.Kp, gbase, ng, r0, dst);
+    else if (c == 4) write_block_pieces<4, RB>(codes, ap.Kp, gbase, ng, r0, dst);
+    else if (c == 2) write_block_pieces<2, RB>(codes, ap.Kp, gbase, ng, r0, dst);
+    else write_block_pieces<1, RB>(codes, ap.Kp, gbase, ng, r0, dst);
   }
 }
 
@@ -1922,16 +1929,21 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   hipLaunchKernelGGL((k_act_rows<R_, J_>), dim3((unsigned)((M + R_ - 1) / R_)), dim3(256),      \
                      (size_t)R_ * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,    \
                      nparts, s_a, packed)
-  // whole 16-row blocks per workgroup for larger batches
-  if (J > 0 && J <= 3 && M >= 1024 && 16 * (int64_t)ap.Kp <= 64 * 1024) {
-    const dim3 grid((unsigned)((M + kBlk - 1) / kBlk));
-    const size_t lds = (size_t)kBlk * ap.Kp;
-    if (J == 1)
-      hipLaunchKernelGGL((k_act_blk16<1>), grid, dim3(256), lds, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial, nparts, s_a, packed);
-    else if (J == 2)
-      hipLaunchKernelGGL((k_act_blk16<2>), grid, dim3(256), lds, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial, nparts, s_a, packed);
-    else
-      hipLaunchKernelGGL((k_act_blk16<3>), grid, dim3(256), lds, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial, nparts, s_a, packed);
+  // whole 8- or 16-row block slices per workgroup for larger batches
+  // 16 rows per workgroup once that still gives ~1.5 workgroups per CU,
+  // else 8 (more workgroups in flight)
+  const int rbk = M >= 6144 ? 16 : 8;
+  if (J > 0 && J <= 3 && M >= 1024 && rbk * (int64_t)ap.Kp <= 64 * 1024) {
+    const size_t lds = (size_t)rbk * ap.Kp;
+#define SONIQ_BLK(J_, RB_)                                                                       \
+  hipLaunchKernelGGL((k_act_blk16<J_, RB_>), dim3((unsigned)((M + RB_ - 1) / RB_)), dim3(256), lds, \
+                     stream, A, M, K, lda, pos_dev, seg_dev, ap, partial, nparts, s_a, packed)
+    if (rbk == 8) {
+      if (J == 1) SONIQ_BLK(1, 8); else if (J == 2) SONIQ_BLK(2, 8); else SONIQ_BLK(3, 8);
+    } else {
+      if (J == 1) SONIQ_BLK(1, 16); else if (J == 2) SONIQ_BLK(2, 16); else SONIQ_BLK(3, 16);
+    }
+#undef SONIQ_BLK
   } else if (4 * (int64_t)ap.Kp <= 64 * 1024) {
     switch (J) {
       case 0: SONIQ_ACT_ROWS(4, 0); break;
