@@ -205,7 +205,7 @@ struct soniq_act_s {
   int64_t packed_bytes = 0;
   uint8_t* packed = nullptr;
   float* partial = nullptr;
-  unsigned int* counter = nullptr;
+  unsigned int* counter = nullptr;  // kActStateWords words: the single-pass quantizer's grid state
   float* s_a = nullptr;
 };
 
@@ -520,9 +520,9 @@ soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
   a->packed_bytes = act_bytes(a->ap, a->M_alloc);
   hipError_t e = dev_alloc(&a->packed, (size_t)a->packed_bytes);
   if (e == hipSuccess) e = dev_alloc(&a->partial, 2 * kAbsmaxBlocks);
-  if (e == hipSuccess) e = dev_alloc(&a->counter, 1);
+  if (e == hipSuccess) e = dev_alloc(&a->counter, kActStateWords);
   if (e == hipSuccess) e = dev_alloc(&a->s_a, 2);
-  if (e == hipSuccess) e = hipMemset(a->counter, 0, sizeof(unsigned int));
+  if (e == hipSuccess) e = hipMemset(a->counter, 0, kActStateWords * sizeof(unsigned int));
   if (e == hipSuccess) e = hipMemset(a->s_a, 0, 2 * sizeof(float));
   if (e == hipSuccess) e = hipMemset(a->packed, 0, (size_t)a->packed_bytes);
   if (e == hipSuccess) e = hipDeviceSynchronize();

@@ -36,6 +36,9 @@ constexpr int kBlk = 16;      // rows per block
 constexpr int kGemmBN = 128;  // GEMM block tile columns (8 weight blocks)
 constexpr int kMAlign = 256;  // activation rows are allocated in multiples of this
 constexpr int kAbsmaxBlocks = 1024;  // max partial maxima (pairs) per activation batch
+// 32-bit words of device state per activation handle (the single-pass
+// quantizer's grid counters and maxima); zero between calls.
+constexpr int kActStateWords = 2048;
 
 // Quantizer of one width: code = sign1 ? (x < 0 ? -1 : +1)
 //                                : clamp(rint(x / s), lo, hi), s = max/qdiv.

@@ -714,6 +714,389 @@ __global__ __launch_bounds__(256) void k_act_blk16(const float* __restrict__ A, 
   }
 }
 
+// ------------------------------------------------- wait and LDS helpers --
+// s_waitcnt immediate for vmcnt(n) (gfx9 encoding), expcnt/lgkmcnt untouched.
+#define SONIQ_VMCNT_IMM(n) (((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
+// s_waitcnt immediate for lgkmcnt(0) alone (vmcnt and expcnt at their maxima).
+#define SONIQ_LGKMCNT0_IMM (0xF | (3 << 14) | (0x7 << 4))
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(SONIQ_VMCNT_IMM(N));
+}
+
+// Buffer-resource offset past any buffer: the load returns zero without
+// touching memory.
+constexpr uint32_t kOOB = 0x7FFFFFF0u;
+
+// LDS byte address of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_off(const uint8_t* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint8_t*)p);
+}
+
+// ------------------------------------------------------------ k_act_coop --
+// One pass over HBM for batches that fit in the registers of the chip.
+// The grid is no larger than the number of workgroups that can be resident
+// at once, so every workgroup holds its rows while the group maxima meet.
+// Workgroup b holds the RB rows m0 = RB*b .. of one 16-row block
+// (RB = 4, 8 or 16): its RB*K4 float4 are spread evenly over the 256
+// threads, thread tid taking flat positions f = tid + 256*i (i < T) with
+// row f / K4 and position f % K4.  It folds its group maxima into the
+// grid's, waits until every workgroup has done so, quantizes the rows it
+// still holds into LDS and writes their units as whole pieces.  Rows past
+// M are clamped to row M-1 for the loads and left as zero codes, which
+// land in padding rows.  Dynamic LDS: RB*Kp code bytes, then the K
+// planned positions (group 1 starts at planned position kpad[0]), padded
+// to a multiple of 256, then TL*4 KB of row data.
+//
+// Grid state (zero when the handle is made, and left that way between
+// calls), in 32-bit words, each counter on a 128-byte line of its own:
+//   sub[x]     at 32*x          arrivals of workgroups b with b % 8 == x
+//   top        at kBarTop       groups x complete
+//   gen[x]     at kBarGen+32*x  generation, one copy per group (equal)
+//   max[p][x][g] at kBarMax+32*(8p+x)+g  group maxima (float bits) of
+//                               the call with generation parity p
+// Only relaxed agent-scope atomics touch this state, and each step waits
+// for the previous one's returned value before it issues, so a workgroup
+// that sees the generation move also sees every folded maximum.  No L2
+// write-back or invalidate is needed (the rows stay in registers).  The
+// last arrival of a group resets its sub counter, the last group resets
+// top and the other parity's maxima, then advances every gen copy.
+constexpr int kBarTop = 256, kBarGen = 288, kBarMax = 544;
+constexpr int kBarWords = kBarMax + 32 * 16;
+static_assert(kBarWords <= kActStateWords, "grid state fits the handle's words");
+
+// Spin limit of the wait: far beyond any real wait (a few tenths of a
+// second).  A workgroup that times out (its grid was not resident after
+// all) computes the maxima itself from the whole batch, so the result is
+// the same, only slower.
+constexpr unsigned kBarrierSpins = 1u << 18;
+
+__device__ __forceinline__ unsigned bar_load(const unsigned* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned bar_add(unsigned* p, unsigned v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void bar_store(unsigned* p, unsigned v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Make the following atomics wait for v (an atomic's returned value).
+__device__ __forceinline__ void bar_after(unsigned v) {
+  asm volatile("" ::"v"(v) : "memory");
+}
+
+// This workgroup's generation word; read it (thread 0) when the kernel
+// starts, since it cannot move before every workgroup has arrived.
+__device__ __forceinline__ unsigned* grid_gen_word(unsigned* st) {
+  return st + kBarGen + 32 * (blockIdx.x & 7);
+}
+
+// Fold (mx0, mx1) into the grid maxima and wait for every workgroup.
+// Thread 0 only, gen = this call's generation; returns false when the
+// wait timed out.
+__device__ __forceinline__ bool grid_fold_max(unsigned* st, unsigned gen, float mx0, float mx1,
+                                              float& g0, float& g1) {
+  const unsigned x = blockIdx.x & 7;
+  const unsigned ngroups = gridDim.x < 8 ? gridDim.x : 8;
+  const unsigned nx = (gridDim.x - x + 7) / 8;  // workgroups in group x
+  unsigned* genx = st + kBarGen + 32 * x;
+  bar_after(gen);
+  unsigned* mp = st + kBarMax + 32 * (8 * (gen & 1));
+  const unsigned o0 = __hip_atomic_fetch_max(mp + 32 * x, __float_as_uint(mx0), __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+  const unsigned o1 = __hip_atomic_fetch_max(mp + 32 * x + 1, __float_as_uint(mx1),
+                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  bar_after(o0 | o1);
+  bool ok = true, last = false;
+  const unsigned a1 = bar_add(st + 32 * x, 1u);
+  bar_after(a1);
+  if (a1 == nx - 1) {
+    bar_store(st + 32 * x, 0u);
+    const unsigned a2 = bar_add(st + kBarTop, 1u);
+    bar_after(a2);
+    if (a2 == ngroups - 1) {
+      bar_store(st + kBarTop, 0u);
+      unsigned* other = st + kBarMax + 32 * (8 * ((gen & 1) ^ 1));
+      for (int i = 0; i < 8; ++i) {
+        bar_store(other + 32 * i, 0u);
+        bar_store(other + 32 * i + 1, 0u);
+      }
+      // the maxima were folded before every arrival, so the copies can go
+      // out together
+      for (int i = 0; i < 8; ++i) bar_add(st + kBarGen + 32 * i, 1u);
+      last = true;
+    }
+  }
+  if (!last) {
+    unsigned n = 0;
+    unsigned now;
+    while ((now = bar_load(genx)) == gen) {
+      if (++n > kBarrierSpins) {
+        ok = false;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(20);
+    }
+    bar_after(now);
+  }
+  unsigned m0 = 0, m1 = 0;
+  for (int i = 0; i < 8; ++i) {
+    m0 = max(m0, bar_load(mp + 32 * i));
+    m1 = max(m1, bar_load(mp + 32 * i + 1));
+  }
+  g0 = __uint_as_float(m0);
+  g1 = __uint_as_float(m1);
+  return ok;
+}
+
+// Group maxima of the whole batch, by this workgroup alone (the timed-out
+// wait only).  pos4: LDS copy of the planned positions; group 1 starts at
+// planned position kp0.
+__device__ __forceinline__ void absmax_all(const float* __restrict__ A, int64_t M, int K4,
+                                           int64_t lda, const int4* pos4, int kp0, float* red,
+                                           float& g0, float& g1) {
+  float mx0 = 0.0f, mx1 = 0.0f;
+  for (int64_t m = 0; m < M; ++m)
+    for (int k = threadIdx.x; k < K4; k += 256) {
+      const int4 p = pos4[k];
+      max4(*reinterpret_cast<const float4*>(A + m * lda + 4 * k),
+           make_uchar4(p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0), mx0, mx1);
+    }
+  const float2 r = block_max2(make_float2(mx0, mx1), red);
+  g0 = r.x;
+  g1 = r.y;
+}
+
+// Step from flat position (r, k) to (r, k) + 256 within rows of K4 float4:
+// 256 = q256*K4 + r256.
+__device__ __forceinline__ void coop_step(int& r, int& k, int K4, int q256, int r256) {
+  k += r256;
+  r += q256;
+  if (k >= K4) {
+    k -= K4;
+    ++r;
+  }
+}
+
+__device__ __forceinline__ void coop_first(int& r, int& k, int K4) {
+  r = 0;
+  k = threadIdx.x;
+  if (k >= K4) {
+    r = k / K4;
+    k -= r * K4;
+  }
+}
+
+// Rounding by the 1.5*2^23 shift: for |e| < 2^22, e + (kShift - zp)
+// rounds to the integer kShift + rint(e) - zp, whose float bits are
+// kShiftBits + rint(e) - zp; it is clamped between kShift + the
+// stored-code bounds (exact integers too) and the low byte of its bits is
+// the stored code (no conversion, no zero-point subtraction).  Outside a rounding tie the sum
+// rounds to the nearest integer exactly as rint does; the tie band sends
+// ties to the exact division anyway.  Every element of a group has
+// |x * rcp(s)| <= qmax + 1 < 2^22.
+constexpr float kShift = 12582912.0f;  // 1.5 * 2^23
+
+// Both groups' quantizer parameters held in VGPRs, so that an element's
+// set costs one select per parameter (the empty asm keeps the compiler
+// from re-deriving them per element).
+struct QPair {
+  float rs0, rs1, mz0, mz1;  // reciprocal scale; kShift - zp
+  float lb0, lb1, hb0, hb1;  // kShift + stored-code bounds
+  float s0, s1, zp0, zp1;
+};
+
+__device__ __forceinline__ QPair qpair(const QElem& a, const QElem& b) {
+  QPair p{a.rs, b.rs, kShift - a.zp, kShift - b.zp, kShift + a.lo, kShift + b.lo,
+          kShift + a.hi, kShift + b.hi, a.s, b.s, a.zp, b.zp};
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(p.rs0), "+v"(p.rs1), "+v"(p.mz0), "+v"(p.mz1), "+v"(p.lb0), "+v"(p.lb1),
+               "+v"(p.hb0), "+v"(p.hb1));
+#endif
+  return p;
+}
+
+// Stored code of x (low byte of the result), and whether x/s lies in the
+// tie band (then the caller takes the exact division).
+__device__ __forceinline__ int qshift(float x, float rs, float mz, float lb, float hb, bool& near) {
+  const float e = x * rs;
+  const float t = e + mz;
+  near = !(fabsf(fabsf(e - (t - mz)) - 0.5f) > kTieBand);
+  return __float_as_int(__builtin_amdgcn_fmed3f(t, lb, hb));
+}
+
+// Stored codes of four elements whose groups are h (true: group 1) into
+// row[p.*] (same codes as qstore4).
+__device__ __forceinline__ void qstore4g(const float4& v, const bool (&h)[4], const QPair& q,
+                                         uint8_t* row, int4 p) {
+  const float xs[4] = {v.x, v.y, v.z, v.w};
+  int c[4];
+  bool n[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    c[e] = qshift(xs[e], h[e] ? q.rs1 : q.rs0, h[e] ? q.mz1 : q.mz0, h[e] ? q.lb1 : q.lb0,
+                  h[e] ? q.hb1 : q.hb0, n[e]);
+  if (n[0] | n[1] | n[2] | n[3]) [[unlikely]] {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n[e])
+        c[e] = qexact(xs[e], (h[e] ? q.lb1 : q.lb0) - kShift, (h[e] ? q.hb1 : q.hb0) - kShift,
+                      h[e] ? q.zp1 : q.zp0, h[e] ? q.s1 : q.s0);
+  }
+  row[p.x] = (uint8_t)c[0];
+  row[p.y] = (uint8_t)c[1];
+  row[p.z] = (uint8_t)c[2];
+  row[p.w] = (uint8_t)c[3];
+}
+
+// Waves per SIMD the register budget must allow: T <= 9 keeps seven
+// workgroups per CU resident (1568 four-row workgroups on 256 CUs), more
+// float4 per thread four.  TL of the T float4 per thread wait in LDS.
+template <int T, int TL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T <= 9 ? 7 : 4)))
+void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int RB,
+                const int32_t* __restrict__ pos, ActPlan ap, unsigned* __restrict__ st,
+                float* __restrict__ s_a_out, uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  __shared__ float red[8];
+  __shared__ float gmax[2];
+  __shared__ int flag;
+  const int tid = threadIdx.x;
+  const int64_t m0 = (int64_t)blockIdx.x * RB;
+  const int rows = (int)min((int64_t)RB, M - m0);
+  const int nf = RB * K4;  // flat positions of this workgroup (T*256 >= nf)
+  const int q256 = 256 / K4, r256 = 256 - q256 * K4;
+  const int kp0 = ap.kpad[0];  // planned positions >= kp0 belong to group 1
+  const float* A0 = A + m0 * lda;
+  int4* pos4 = reinterpret_cast<int4*>(codes + RB * ap.Kp);
+  unsigned gen = 0;
+  if (tid == 0) gen = bar_load(grid_gen_word(st));
+  // The position table goes global -> LDS directly (no registers), ahead
+  // of the row loads: entry k of wave wid's chunk j (k = 256j + 64wid +
+  // lane) lands at pos4[k]; lanes past K4 read zeros into the padding of
+  // the table's region (K4 rounded up to 64 entries).  RB >= 4 gives
+  // K4 <= 64*T <= 256*TJ.
+  constexpr int TJ = (T + 3) / 4;
+  {
+    const __amdgpu_buffer_rsrc_t pr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)pos, (short)0, K4 * 16, 0x00020000);
+    const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t base = lds_off(codes) + (uint32_t)(RB * ap.Kp);
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int k0 = 256 * j + 64 * wid;
+      const int k = k0 + (tid & 63);
+      if (k0 < K4)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            pr, (__attribute__((address_space(3))) void*)(uintptr_t)(base + 16 * k0), 16,
+            k < K4 ? 16u * k : kOOB, 0, 0, 0);
+    }
+    asm volatile("" ::: "memory");
+  }
+  // slots i < TV in registers; the last TL slots go global -> LDS (lane l
+  // of wave w: vlds + (i - TV)*4096 + (64w + l)*16) where the register
+  // budget cannot hold them
+  constexpr int TV = T - TL;
+  float4 v[TV];
+  float4* vlds = reinterpret_cast<float4*>(codes + RB * ap.Kp + 16 * ((K4 + 63) / 64 * 64));
+  {
+    // rows through a buffer resource based at row m0: 32-bit offsets
+    const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)A0, (short)0, (int)(((int64_t)(rows - 1) * lda + 4 * K4) * 4), 0x00020000);
+    const uint32_t ld4 = (uint32_t)lda * 4u;
+    const uint32_t vb = lds_off(reinterpret_cast<uint8_t*>(vlds)) +
+                        (uint32_t)__builtin_amdgcn_readfirstlane(tid >> 6) * 1024u;
+    int r, k;
+    coop_first(r, k, K4);
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+      // positions past nf re-read this workgroup's last element
+      const bool in = tid + 256 * i < nf;
+      const int rc = in ? min(r, rows - 1) : rows - 1;
+      const int kc = in ? k : K4 - 1;
+      const uint32_t off = (uint32_t)rc * ld4 + 16u * (uint32_t)kc;
+      if (i < TV)
+        v[i < TV ? i : 0] =
+            __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(ar, off, 0, 0));
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            ar, (__attribute__((address_space(3))) void*)(uintptr_t)(vb + (i - TV) * 4096), 16, off,
+            0, 0, 0);
+      coop_step(r, k, K4, q256, r256);
+    }
+  }
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < RB * ap.Kp / 4; i += 256) codes32[i] = 0;
+  wait_vm<T>();  // this wave's table chunks (issued before the T row loads)
+  __syncthreads();
+  // slot i's float4 (the LDS ones are read where they are used)
+  auto val = [&](int i) __attribute__((always_inline)) {
+    return i < TV ? v[i < TV ? i : 0] : vlds[(i - TV) * 256 + tid];
+  };
+  float mx0 = 0.0f, mx1 = 0.0f;
+  {
+    int r, k;
+    coop_first(r, k, K4);
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+      const int4 p = pos4[tid + 256 * i < nf ? k : K4 - 1];
+      max4(val(i), make_uchar4(p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0), mx0, mx1);
+      coop_step(r, k, K4, q256, r256);
+    }
+  }
+  {
+    const float2 m = block_max2(make_float2(mx0, mx1), red);
+    if (tid == 0) {
+      float g0, g1;
+      flag = grid_fold_max(st, gen, m.x, m.y, g0, g1);
+      gmax[0] = g0;
+      gmax[1] = g1;
+    }
+  }
+  __syncthreads();
+  float g0 = gmax[0], g1 = gmax[1];
+  if (!flag) absmax_all(A, M, K4, lda, pos4, kp0, red, g0, g1);
+  const float s0 = group_scale(g0, ap.q[0]);
+  const float s1 = ap.S == 2 ? group_scale(g1, ap.q[1]) : 0.0f;
+  if (blockIdx.x == 0 && tid == 0) {
+    s_a_out[0] = s0;
+    s_a_out[1] = s1;
+  }
+  const QPair q = qpair(qelem(s0, ap.q[0], ap.zp[0]), qelem(s1, ap.q[1], ap.zp[1]));
+  {
+    int r, k;
+    coop_first(r, k, K4);
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+      if (tid + 256 * i < nf && r < rows) {
+        const int4 p = pos4[k];
+        const bool h[4] = {p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0};
+        qstore4g(val(i), h, q, codes + r * ap.Kp, p);
+      }
+      coop_step(r, k, K4, q256, r256);
+    }
+  }
+  __syncthreads();
+  const int r0 = (int)(m0 % kBlk);
+  for (int gi = 0; gi < ap.S; ++gi) {
+    const int c = gi ? ap.c[1] : ap.c[0];
+    const int ng = gi ? ap.ng[1] : ap.ng[0];
+    const int gbase = gi ? ap.kpad[0] : 0;
+    uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
+                   (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
+#define SONIQ_PIECES(RB_)                                                         \
+  if (c == 8) write_block_pieces<8, RB_>(codes, ap.Kp, gbase, ng, r0, dst);        \
+  else if (c == 4) write_block_pieces<4, RB_>(codes, ap.Kp, gbase, ng, r0, dst);   \
+  else write_block_pieces<2, RB_>(codes, ap.Kp, gbase, ng, r0, dst)
+    if (RB == 4) { SONIQ_PIECES(4); }
+    else if (RB == 8) { SONIQ_PIECES(8); }
+    else { SONIQ_PIECES(16); }
+#undef SONIQ_PIECES
+  }
+}
+
 // ----------------------------------------------------------- k_act_small --
 // Small batches (M <= 64, M*K <= kSmallElems, contiguous aligned rows): one
 // launch.  Every workgroup reduces the group maxima of the whole batch
@@ -797,11 +1180,6 @@ struct GemmArgs {
   int32_t* acc;
 };
 
-// s_waitcnt immediate for vmcnt(n) (gfx9 encoding), expcnt/lgkmcnt untouched.
-#define SONIQ_VMCNT_IMM(n) (((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
-// s_waitcnt immediate for lgkmcnt(0) alone (vmcnt and expcnt at their maxima).
-#define SONIQ_LGKMCNT0_IMM (0xF | (3 << 14) | (0x7 << 4))
-
 // Workgroup barrier without a memory fence: the LDS ring is filled by
 // direct loads whose completion each wave has already awaited with
 // wait_vmcnt; the compiler fences keep LDS accesses on their side.
@@ -867,16 +1245,6 @@ __device__ __forceinline__ v4i read_frag_w(const uint8_t* p, int lane, int c) {
 constexpr int kBSlot = 128 * 16 * 8;  // B stage bytes at c = 8 (8 blocks, 2 granules)
 constexpr int kLB = 4;                // B loads per stage (kBSlot / 4 KB)
 
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt(SONIQ_VMCNT_IMM(N));
-}
-
-// Buffer-resource offset past any buffer: the load returns zero without
-// touching memory.
-constexpr uint32_t kOOB = 0x7FFFFFF0u;
-
 // Fragment reads from the LDS ring are issued as inline asm.  The ring is
 // filled by direct global->LDS loads whose completion each wave awaits with
 // an explicit vmcnt wait and a barrier; through plain C++ loads the
@@ -885,9 +1253,6 @@ constexpr uint32_t kOOB = 0x7FFFFFF0u;
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ uint32_t lds_off(const uint8_t* p) {
-  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint8_t*)p);
-}
 
 // Packed unit (2*C bytes) at LDS byte address a + OFF, in a register type
 // of its size.
@@ -1863,6 +2228,93 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
   else gemv4_block<MT, 1, false>(a, xs, blk, red);
 }
 
+
+// ------------------------------------------------- single-pass quantize --
+// Batches of at least kCoopMinElems elements whose rows fit the registers
+// of one resident grid take k_act_coop: RB rows per workgroup (4, 8 or 16,
+// the choice wasting the fewest register slots), T float4 per thread, and
+// at most as many workgroups as can be resident at once (by the occupancy
+// of k_act_coop<T> with this LDS size, times the CU count).
+// SONIQ_ACT_COOP=0 turns the path off for measurement; results do not
+// depend on it.
+constexpr int64_t kCoopMinElems = (int64_t)1 << 20;
+
+template <int T, int TL>
+int coop_capacity(size_t lds) {
+  // resident workgroups per CU for this T and LDS size, cached per device
+  struct Entry {
+    int dev = -1;
+    size_t lds = 0;
+    int per_cu = 0, cus = 0;
+  };
+  static thread_local Entry cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (cache.dev != dev || cache.lds != lds) {
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_act_coop<T, TL>, 256, lds) != hipSuccess)
+      return 0;
+    cache.dev = dev;
+    cache.lds = lds;
+    cache.per_cu = per_cu;
+    cache.cus = cus;
+  }
+  return cache.per_cu * cache.cus;
+}
+
+template <int T, int TL>
+bool coop_launch(const float* A, int64_t M, int64_t K, int64_t lda, int RB, const ActPlan& ap,
+                 const int32_t* pos_dev, unsigned* bar, float* s_a,
+                 uint8_t* packed, hipStream_t stream, hipError_t& e) {
+  const size_t lds = (size_t)RB * ap.Kp + 16 * (size_t)((K / 4 + 63) / 64 * 64) + 4096 * TL;
+  const int64_t blocks = (M + RB - 1) / RB;
+  // a workgroup's rows are addressed with 32-bit byte offsets
+  if ((int64_t)(RB - 1) * lda * 4 + K * 4 >= ((int64_t)1 << 31)) return false;
+  if (lds > 64 * 1024 || blocks > coop_capacity<T, TL>(lds)) return false;
+  hipLaunchKernelGGL((k_act_coop<T, TL>), dim3((unsigned)blocks), dim3(256), lds, stream, A, M,
+                     (int)(K / 4), lda, RB, pos_dev, ap, bar, s_a, packed);
+  e = hipGetLastError();
+  return true;
+}
+
+bool launch_act_coop(const float* A, int64_t M, int64_t K, int64_t lda, const ActPlan& ap,
+                     const int32_t* pos_dev, unsigned* bar, float* s_a,
+                     uint8_t* packed, hipStream_t stream, hipError_t& e) {
+  if (const char* env = getenv("SONIQ_ACT_COOP"))
+    if (atoi(env) == 0) return false;
+  const int64_t K4 = K / 4;
+  // candidates (RB, T) ordered by wasted register slots, more workgroups
+  // first (they spread the quantize work more evenly over the CUs)
+  struct Cand {
+    int rb, t;
+    int64_t waste;
+  } cand[3];
+  int nc = 0;
+  for (int rb : {4, 8, 16}) {
+    const int64_t need = (rb * K4 + 255) / 256;
+    const int t = need <= 6 ? 6 : need <= 9 ? 9 : need <= 12 ? 12 : need <= 18 ? 18 : 0;
+    if (t == 0) continue;
+    cand[nc++] = {rb, t, 256 * (int64_t)t - rb * K4};
+  }
+  for (int i = 1; i < nc; ++i)
+    for (int j = i; j > 0 && cand[j].waste < cand[j - 1].waste; --j) std::swap(cand[j], cand[j - 1]);
+  for (int i = 0; i < nc; ++i) {
+    const Cand& c = cand[i];
+    bool done = false;
+    if (c.t == 6)
+      done = coop_launch<6, 0>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
+    else if (c.t == 9)
+      done = coop_launch<9, 1>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
+    else if (c.t == 12)
+      done = coop_launch<12, 0>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
+    else
+      done = coop_launch<18, 0>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
+    if (done) return true;
+  }
+  return false;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------- launchers --
@@ -1883,13 +2335,18 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const uint8_t* seg_dev, float* partial,
                             unsigned int* counter, float* s_a, uint8_t* packed,
                             hipStream_t stream) {
-  (void)counter;
   const bool aligned = (K % 4 == 0) && (lda % 4 == 0) &&
                        (reinterpret_cast<uintptr_t>(A) % 16 == 0);
   if (aligned && M <= 64 && M * K <= kSmallElems) {
     hipLaunchKernelGGL(k_act_small, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A,
                        (int)M, (int)K, lda, pos_dev, seg_dev, ap, s_a, packed);
     return hipGetLastError();
+  }
+  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
+  if (aligned && !sign && M * K >= kCoopMinElems) {
+    hipError_t e = hipSuccess;
+    if (launch_act_coop(A, M, K, lda, ap, pos_dev, counter, s_a, packed, stream, e))
+      return e;
   }
   int nparts;
   if (aligned && M <= 16 * (int64_t)kAbsmaxBlocks) {
@@ -1922,7 +2379,6 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   if (e != hipSuccess) return e;
   // groups of 1-bit sign codes, and unaligned rows, take the generic
   // per-element quantizer (J = 0); otherwise J float4 positions per thread
-  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
   const int K4 = (int)(K / 4);
   const int J = (sign || !aligned) ? 0 : K4 <= 256 ? 1 : K4 <= 512 ? 2 : K4 <= 768 ? 3 : 4;
 #define SONIQ_ACT_ROWS(R_, J_)                                                                  \

@@ -252,3 +252,51 @@ def test_api_errors_on_device():
     assert info.N == 256 and info.K == 256 and info.S == 2
     assert list(info.a_bits) == [4, 8] and list(info.w_bits) == [2, 4]
     assert info.packed_w_bytes_algorithmic == (192 * 2 + 64 * 4) * 256 // 8
+
+
+# Batches of at least 2^20 elements that fit the registers of one resident
+# grid are quantized in one pass (rows per workgroup RB and float4 per
+# thread T chosen from K); each case below lands on a different (RB, T),
+# with a ragged last workgroup.  Both the single pass and the two-pass
+# path (SONIQ_ACT_COOP=0) must match the oracle.
+COOP = [  # (M, K, a_lo, a_hi, a_signed)      RB, T
+    (8200, 128, 4, 8, True),                # 16, 6 (K4 = 32: 8 rows per 256-step)
+    (1400, 768, 4, 8, False),               # 16, 12
+    (343, 3072, 2, 4, True),                # 4, 12 (2-bit pieces of 4 rows)
+    (460, 2304, 4, 8, False),               # 8, 18 (the conv row length)
+    (1100, 1000, 4, 8, True),               # 4, 6 (K4 = 250 < 256)
+    (4100, 260, 2, 8, False),               # 16, 6 (K4 = 65: three rows per step)
+]
+
+
+@pytest.mark.parametrize("coop", [True, False], ids=["single_pass", "two_pass"])
+@pytest.mark.parametrize("shape", COOP, ids=lambda s: f"{s[0]}x{s[1]}_a{s[2]}{s[3]}{'s' if s[4] else 'u'}")
+def test_single_pass_quantize(shape, coop, monkeypatch):
+    M, K, alo, ahi, sgn = shape
+    if not coop:
+        monkeypatch.setenv("SONIQ_ACT_COOP", "0")
+    case = workloads.generic(M, 64, K, a_lo=alo, a_hi=ahi, a_frac_lo=0.6, w_lo=2, w_hi=4,
+                             w_frac_lo=0.5, a_signed=sgn, a_abs=not sgn, seed=M + K,
+                             name="coop")
+    compare_full(gpu_run(case), oracle_run(case))
+
+
+def test_single_pass_repeat_calls():
+    """The grid barrier's counters reset themselves: repeated calls, a
+    smaller grid after a larger one and new data all stay bit-exact."""
+    big = workloads.generic(1400, 64, 768, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
+                            w_frac_lo=0.5, seed=21, name="coop-repeat")
+    W = torch.from_numpy(big["W"]).cuda()
+    w = sq.soniq_pack_weights(W, big["w_bits"], big["a_bits"], True)
+    act = sq.soniq_act_create(w, 1400)
+    for M, scale in ((1400, 1.0), (1400, 3.0), (1366, 0.5), (1400, 1.0)):
+        A_np = (big["A"][:M] * np.float32(scale)).copy()
+        sq.soniq_quantize_act(act, torch.from_numpy(A_np).cuda())
+        acc = torch.empty((w.S, M, 64), dtype=torch.int32, device="cuda")
+        Y = sq.soniq_mp_gemm(act, w, acc=acc)
+        torch.cuda.synchronize()
+        r = oracle.run(A_np, big["W"], big["a_bits"], big["w_bits"], True)
+        _, s_a = sq.soniq_act_unpack_debug(act)
+        np.testing.assert_array_equal(s_a, r["s_a"])
+        np.testing.assert_array_equal(acc.cpu().numpy(), r["acc"])
+        np.testing.assert_array_equal(_bf16_bits(Y), r["y_replay"])
