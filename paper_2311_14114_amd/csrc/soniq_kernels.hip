@@ -770,7 +770,8 @@ static_assert(kBarWords <= kActStateWords, "grid state fits the handle's words")
 // Spin limit of the wait: far beyond any real wait (a few tenths of a
 // second).  A workgroup that times out (its grid was not resident after
 // all) computes the maxima itself from the whole batch, so the result is
-// the same, only slower.
+// the same, only slower.  SONIQ_COOP_SPINS overrides the limit (tests set
+// it to 0 to run that path).
 constexpr unsigned kBarrierSpins = 1u << 18;
 
 __device__ __forceinline__ unsigned bar_load(const unsigned* p) {
@@ -796,8 +797,8 @@ __device__ __forceinline__ unsigned* grid_gen_word(unsigned* st) {
 // Fold (mx0, mx1) into the grid maxima and wait for every workgroup.
 // Thread 0 only, gen = this call's generation; returns false when the
 // wait timed out.
-__device__ __forceinline__ bool grid_fold_max(unsigned* st, unsigned gen, float mx0, float mx1,
-                                              float& g0, float& g1) {
+__device__ __forceinline__ bool grid_fold_max(unsigned* st, unsigned gen, unsigned spins,
+                                              float mx0, float mx1, float& g0, float& g1) {
   const unsigned x = blockIdx.x & 7;
   const unsigned ngroups = gridDim.x < 8 ? gridDim.x : 8;
   const unsigned nx = (gridDim.x - x + 7) / 8;  // workgroups in group x
@@ -833,7 +834,7 @@ __device__ __forceinline__ bool grid_fold_max(unsigned* st, unsigned gen, float 
     unsigned n = 0;
     unsigned now;
     while ((now = bar_load(genx)) == gen) {
-      if (++n > kBarrierSpins) {
+      if (++n > spins) {
         ok = false;
         break;
       }
@@ -958,7 +959,7 @@ template <int T, int TL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T <= 9 ? 7 : 4)))
 void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int RB,
                 const int32_t* __restrict__ pos, ActPlan ap, unsigned* __restrict__ st,
-                float* __restrict__ s_a_out, uint8_t* __restrict__ packed) {
+                unsigned spins, float* __restrict__ s_a_out, uint8_t* __restrict__ packed) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
   __shared__ float gmax[2];
@@ -1050,7 +1051,7 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     const float2 m = block_max2(make_float2(mx0, mx1), red);
     if (tid == 0) {
       float g0, g1;
-      flag = grid_fold_max(st, gen, m.x, m.y, g0, g1);
+      flag = grid_fold_max(st, gen, spins, m.x, m.y, g0, g1);
       gmax[0] = g0;
       gmax[1] = g1;
     }
@@ -2272,8 +2273,10 @@ bool coop_launch(const float* A, int64_t M, int64_t K, int64_t lda, int RB, cons
   // a workgroup's rows are addressed with 32-bit byte offsets
   if ((int64_t)(RB - 1) * lda * 4 + K * 4 >= ((int64_t)1 << 31)) return false;
   if (lds > 64 * 1024 || blocks > coop_capacity<T, TL>(lds)) return false;
+  unsigned spins = kBarrierSpins;
+  if (const char* env = getenv("SONIQ_COOP_SPINS")) spins = (unsigned)strtoul(env, nullptr, 10);
   hipLaunchKernelGGL((k_act_coop<T, TL>), dim3((unsigned)blocks), dim3(256), lds, stream, A, M,
-                     (int)(K / 4), lda, RB, pos_dev, ap, bar, s_a, packed);
+                     (int)(K / 4), lda, RB, pos_dev, ap, bar, spins, s_a, packed);
   e = hipGetLastError();
   return true;
 }

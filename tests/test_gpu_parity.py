@@ -300,3 +300,19 @@ def test_single_pass_repeat_calls():
         np.testing.assert_array_equal(s_a, r["s_a"])
         np.testing.assert_array_equal(acc.cpu().numpy(), r["acc"])
         np.testing.assert_array_equal(_bf16_bits(Y), r["y_replay"])
+
+
+@pytest.mark.parametrize("M,K", [(1400, 768), (460, 2304)])
+def test_single_pass_wait_timeout(M, K, monkeypatch):
+    """With a spin limit of zero every workgroup but the grid's last arrival
+    gives up waiting and takes the maxima from the whole batch itself; the
+    codes, scales and outputs are the same, and the next call (normal
+    limit) finds the grid state clean."""
+    case = workloads.generic(M, 64, K, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=4,
+                             w_frac_lo=0.5, a_signed=False, a_abs=True, seed=M * 3 + K,
+                             name="coop-timeout")
+    ref = oracle_run(case)
+    monkeypatch.setenv("SONIQ_COOP_SPINS", "0")
+    compare_full(gpu_run(case), ref)
+    monkeypatch.delenv("SONIQ_COOP_SPINS")
+    compare_full(gpu_run(case), ref)
