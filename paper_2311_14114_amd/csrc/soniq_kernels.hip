@@ -1246,6 +1246,21 @@ __device__ __forceinline__ v4i read_frag_w(const uint8_t* p, int lane, int c) {
 constexpr int kBSlot = 128 * 16 * 8;  // B stage bytes at c = 8 (8 blocks, 2 granules)
 constexpr int kLB = 4;                // B loads per stage (kBSlot / 4 KB)
 
+// Ring slot of a (32*WFM) x 128 tile: the A stage at the larger activation
+// container, then the B stage at the larger weight container (8-bit where
+// the containers are only known at run time).
+constexpr int gemm_aslot(int S, int CA0, int CA1, int CBL, int CBH, int WFM) {
+  return (CA0 == 0 || (S == 2 && CA1 == 0) || CBL == 0 || CBH == 0)
+             ? 32 * WFM * 16 * 8
+             : 32 * WFM * 16 * (S == 2 && CA1 > CA0 ? CA1 : CA0);
+}
+constexpr int gemm_slot(int S, int CA0, int CA1, int CBL, int CBH, int WFM) {
+  return gemm_aslot(S, CA0, CA1, CBL, CBH, WFM) +
+         ((CA0 == 0 || (S == 2 && CA1 == 0) || CBL == 0 || CBH == 0)
+              ? kBSlot
+              : 128 * 16 * (CBH > CBL ? CBH : CBL));
+}
+
 // Fragment reads from the LDS ring are issued as inline asm.  The ring is
 // filled by direct global->LDS loads whose completion each wave awaits with
 // an explicit vmcnt wait and a barrier; through plain C++ loads the
@@ -1286,6 +1301,16 @@ __device__ __forceinline__ raw_t<C> lds_unit(uint32_t a) {
 __device__ __forceinline__ void lds_wait() {
 #if defined(__HIP_DEVICE_COMPILE__)
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#endif
+}
+// Waits until at most N LDS reads (or scalar loads) are in flight; LDS
+// reads complete in order, so the earliest ones have landed.  A scalar
+// load still in flight only makes the wait longer.
+template <int N>
+__device__ __forceinline__ void lds_wait_n() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
 #endif
 }
 template <typename T>
@@ -1371,6 +1396,48 @@ __device__ __forceinline__ void mma_granule(v4i (&acc)[WFM][4], uint32_t a_addr,
   }
 }
 
+// Both granules of a stage on a tile of one weight width CB: every unit
+// read of the stage is issued first; granule 0 is widened and multiplied
+// once its reads have landed (the 4 + WFM reads of granule 1 may still be
+// in flight), then granule 1.
+template <int CA, int CB, int WFM>
+__device__ __forceinline__ void mma_stage(v4i (&acc)[WFM][4], uint32_t a_addr,
+                                          const uint32_t (&b_addr)[4]) {
+  raw_t<CB> rb0[4], rb1[4];
+  raw_t<CA> ra0[WFM], ra1[WFM];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) rb0[jj] = lds_unit<CB, 0>(b_addr[jj]);
+  read_a_units<CA, 0>(ra0, a_addr, std::make_integer_sequence<int, WFM>{});
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) rb1[jj] = lds_unit<CB, 128 * CB>(b_addr[jj]);
+  read_a_units<CA, 1>(ra1, a_addr, std::make_integer_sequence<int, WFM>{});
+  auto granule = [&](raw_t<CB> (&rb)[4], raw_t<CA> (&ra)[WFM]) __attribute__((always_inline)) {
+    v4i bf[4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      lds_touch(rb[jj]);
+      bf[jj] = unpack_frag<CB>(rb[jj]);
+    }
+#pragma unroll
+    for (int i = 0; i < WFM; ++i) {
+      lds_touch(ra[i]);
+      const v4i af = unpack_frag<CA>(ra[i]);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf[jj], acc[i][jj], 0, 0, 0);
+    }
+  };
+  lds_wait_n<4 + WFM>();
+  granule(rb0, ra0);
+#if defined(__HIP_DEVICE_COMPILE__)
+  // keep granule 0's products ahead of the wait (MFMAs are not memory
+  // operations, so the wait's memory clobber alone does not order them)
+  __builtin_amdgcn_sched_barrier(0);
+#endif
+  lds_wait();
+  granule(rb1, ra1);
+}
+
 // One activation group's K loop for containers fixed at compile time (A in
 // CA, the tile's weight blocks in CBL or CBH; CBL == CBH for tiles of one
 // width).  Tile BM x 128 (BM = 32*WFM), waves 2x2, wave tile (16*WFM) x 64,
@@ -1379,7 +1446,7 @@ __device__ __forceinline__ void mma_granule(v4i (&acc)[WFM][4], uint32_t a_addr,
 // fixed for the group and a scalar stage offset advances them (per lane on
 // the mixed-width tile); chunks past the data read as zero, which also
 // zeroes the second granule of a final half stage, so its products vanish.
-template <int CA, int CBL, int CBH, int WFM, int NST>
+template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT>
 __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* abase,
                                                 int64_t mstride, int ng, const uint8_t* wtile,
                                                 int wbytes, int ngt, const int (&bc)[8],
@@ -1389,8 +1456,7 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
 #if defined(__HIP_DEVICE_COMPILE__)  // GPU builtins; the host pass never runs it
   static_assert(CA == 4 || CA == 8, "activation container");
   constexpr int BM = 32 * WFM;
-  constexpr int ASLOT = BM * 16 * 8;
-  constexpr int SLOT = ASLOT + kBSlot;
+  static_assert(ASLOT >= BM * 16 * CA && SLOT - ASLOT >= 128 * 16 * CBH, "ring slot holds a stage");
   constexpr int LA = BM * CA / 256;                      // A loads per stage
   constexpr int LB = CBH >= 2 ? CBH / 2 : 1;             // B loads per stage
   constexpr int L = LA + LB;
@@ -1483,8 +1549,12 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
     }
     const uint32_t soff = (uint32_t)((st % NST) * SLOT);
     const uint32_t b_addr[4] = {b_lds[0] + soff, b_lds[1] + soff, b_lds[2] + soff, b_lds[3] + soff};
-    mma_granule<CA, CBL, CBH, WFM, 0>(acc, a_lds + soff, b_addr, wcj, false);
-    mma_granule<CA, CBL, CBH, WFM, 1>(acc, a_lds + soff, b_addr, wcj, false);
+    if constexpr (UNI) {
+      mma_stage<CA, CBL, WFM>(acc, a_lds + soff, b_addr);
+    } else {
+      mma_granule<CA, CBL, CBH, WFM, 0>(acc, a_lds + soff, b_addr, wcj, false);
+      mma_granule<CA, CBL, CBH, WFM, 1>(acc, a_lds + soff, b_addr, wcj, false);
+    }
   }
   // Everyone is done reading the ring before the next group refills it.
   bar_nofence();
@@ -1498,15 +1568,14 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
 // issues exactly WFM + kLB direct loads per stage (lanes past the data
 // re-load one valid chunk into an unused slot), so each wait is a
 // compile-time vmcnt.
-template <int CA, int CBL, int CBH, int WFM, int NST>
+template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT>
 __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abase, int64_t mstride,
                                            int ca_rt, int ng, const uint8_t* wtile, int ngt,
                                            const int (&bc)[8], const int (&bpre)[9], int qbase,
                                            v4i (&acc)[WFM][4], int tid, int lane, int wid,
                                            int wm, int wn) {
   constexpr int BM = 32 * WFM;
-  constexpr int ASLOT = BM * 16 * 8;
-  constexpr int SLOT = ASLOT + kBSlot;
+  static_assert(ASLOT == BM * 16 * 8 && SLOT == ASLOT + kBSlot, "runtime containers: 8-bit slots");
   constexpr int L = WFM + kLB;
   const int ca = CA ? CA : ca_rt;
   const int ach = BM * ca;  // A chunks (16 B) per full stage
@@ -1627,10 +1696,12 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
   bar_nofence();
 }
 
+// (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).
 template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int BM = 32 * WFM;
-  constexpr int SLOT = BM * 16 * 8 + kBSlot;
+  constexpr int SLOT = gemm_slot(S, CA0, CA1, CBL, CBH, WFM);
+  constexpr int ASLOT = gemm_aslot(S, CA0, CA1, CBL, CBH, WFM);
   __shared__ __align__(16) uint8_t lds[NST * SLOT];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -1651,6 +1722,11 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
   const uint8_t* wtile = a.wd.packed + wblk_off(a.wp, jb0);
 
+  // The activation scales (written by the quantize launch just before) are
+  // requested now, so that they have arrived when the epilogue needs them.
+  const float sa0 = a.s_a[0];
+  const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
+
   v4i acc0[WFM][4];
 #pragma unroll
   for (int i = 0; i < WFM; ++i)
@@ -1665,14 +1741,17 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     constexpr int CA = decltype(ca_tag)::value;
     if constexpr (CA != 0 && CBL != 0 && CBH != 0) {
       if (CBL == CBH || tile_lo)
-        gemm_group_fast<CA, CBL, CBL, WFM, NST>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
-                                                bc, bpre, qbase, acc, tid, lane, wid, wm, wn);
+        gemm_group_fast<CA, CBL, CBL, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ng, wtile, wbytes,
+                                                             a.wp.ngt, bc, bpre, qbase, acc, tid,
+                                                             lane, wid, wm, wn);
       else
-        gemm_group_fast<CA, CBH, CBH, WFM, NST>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
-                                                bc, bpre, qbase, acc, tid, lane, wid, wm, wn);
+        gemm_group_fast<CA, CBH, CBH, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ng, wtile, wbytes,
+                                                             a.wp.ngt, bc, bpre, qbase, acc, tid,
+                                                             lane, wid, wm, wn);
     } else {
-      gemm_group_any<CA, CBL, CBH, WFM, NST>(lds, abase, mstride, ca_rt, ng, wtile, a.wp.ngt, bc,
-                                             bpre, qbase, acc, tid, lane, wid, wm, wn);
+      gemm_group_any<CA, CBL, CBH, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ca_rt, ng, wtile,
+                                                          a.wp.ngt, bc, bpre, qbase, acc, tid,
+                                                          lane, wid, wm, wn);
     }
   };
   run_group(std::integral_constant<int, CA0>{}, a.act + ap.seg_off[0] + (m0 / kBlk) * ap.mblk_bytes[0],
@@ -1695,8 +1774,6 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int YS = kGemmBN + 8;
   uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
   static_assert(BM * YS * 2 <= NST * SLOT, "output staging fits the ring");
-  const float sa0 = a.s_a[0];
-  const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
@@ -2458,8 +2535,8 @@ static void launch_gemm_t(const GemmArgs& a, int64_t M, int shape, hipStream_t s
 }
 
 // 128x128 tiles when there are enough of them to keep every CU busy for
-// several rounds; otherwise 64x128 tiles, three workgroups per CU, which
-// hide latency better on smaller problems.  SONIQ_GEMM_SHAPE (2, 3 or 7)
+// several rounds; otherwise 64x128 tiles through a 2-deep ring, which hide
+// latency better on smaller problems.  SONIQ_GEMM_SHAPE (2, 3 or 7)
 // overrides the choice for measurement; results do not depend on it.
 static int gemm_shape(int64_t M, int ntn) {
   if (const char* e = getenv("SONIQ_GEMM_SHAPE")) return atoi(e);
@@ -2471,9 +2548,9 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
   const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
-  const int shape = gemm_shape(M, wp.Np / kGemmBN);
   const int ca0 = ap.c[0], ca1 = ap.S == 2 ? ap.c[1] : 0;
   const int cl = wp.c_lo, ch = wp.c_hi;
+  const int shape = gemm_shape(M, wp.Np / kGemmBN);
   if (ap.S == 2 && ca0 == 4 && ca1 == 8) {
     if (cl == 4 && ch == 8) launch_gemm_t<2, 4, 8, 4, 8>(a, M, shape, stream);
     else if (cl == 2 && ch == 8) launch_gemm_t<2, 4, 8, 2, 8>(a, M, shape, stream);
