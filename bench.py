@@ -121,20 +121,24 @@ def run_gpu(case, steps, warmup, rotate=True):
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(end)
 
-    # The per-call breakdown (and the roofline's launch durations) from a
-    # second pass over the same steps with an event around every call; the
-    # extra events would otherwise inflate the timed region.
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    # The per-call breakdown (and the roofline's launch durations): the same
+    # calls, each entry point back to back between two events (an event
+    # around every call would add its own overhead to each).
+    q0, q1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    q0.record(stream)
     for i in range(steps):
-        evs[i][0].record(stream)
-        act, w = step(i)
-        evs[i][1].record(stream)
-        sq.soniq_mp_gemm(act, w, out=Y)
-        evs[i][2].record(stream)
+        step(i)
+    q1.record(stream)
     torch.cuda.synchronize()
-    q_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    q_ms = q0.elapsed_time(q1) / steps
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for i in range(steps):
+        sq.soniq_mp_gemm(acts[i % nw], ws[i % nw], out=Y)
+    g1.record(stream)
+    torch.cuda.synchronize()
+    g_ms = g0.elapsed_time(g1) / steps
     del acts, ws
 
     # bf16 comparator: torch's GEMM (hipBLASLt) on the same shapes, the same
