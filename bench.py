@@ -68,7 +68,7 @@ def uses_gemv(case) -> bool:
     return case["M"] <= 8
 
 
-def run_gpu(case, steps, warmup, rotate=True):
+def run_gpu(case, steps, warmup, rotate=True, graph=True):
     import torch
     import paper_2311_14114_amd as sq
 
@@ -107,38 +107,48 @@ def run_gpu(case, steps, warmup, rotate=True):
         sq.soniq_mp_gemm(act, w, out=Y)
     torch.cuda.synchronize()
 
-    # The timed region: exactly `steps` steps between two events, nothing
-    # else on the stream.
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record(stream)
-    for i in range(steps):
+    def full(i):
         act, w = step(i)
         sq.soniq_mp_gemm(act, w, out=Y)
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    total_ms = start.elapsed_time(end)
 
-    # The per-call breakdown (and the roofline's launch durations): the same
-    # calls, each entry point back to back between two events (an event
-    # around every call would add its own overhead to each).
-    q0, q1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    q0.record(stream)
-    for i in range(steps):
-        step(i)
-    q1.record(stream)
-    torch.cuda.synchronize()
-    q_ms = q0.elapsed_time(q1) / steps
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    for i in range(steps):
+    def gemm_only(i):
         sq.soniq_mp_gemm(acts[i % nw], ws[i % nw], out=Y)
-    g1.record(stream)
-    torch.cuda.synchronize()
-    g_ms = g0.elapsed_time(g1) / steps
+
+    def timed(fn):
+        # ms per call of fn(0..steps-1) run back to back on the stream
+        # between two events, launched eagerly or as one captured HIP graph
+        # (the launch overhead of small calls otherwise starves the GPU)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if graph:
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(stream)
+            with torch.cuda.graph(g, stream=side):
+                for i in range(steps):
+                    fn(i)
+            torch.cuda.synchronize()
+            g.replay()  # first replay uploads the graph
+            torch.cuda.synchronize()
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+        else:
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for i in range(steps):
+                fn(i)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    # The timed region: exactly `steps` steps between two events, nothing
+    # else on the stream.  Then the per-call breakdown (and the roofline's
+    # launch durations): each entry point alone, back to back.
+    t0 = time.perf_counter()
+    total_ms = timed(full) * steps
+    wall = time.perf_counter() - t0
+    q_ms = timed(step)
+    g_ms = timed(gemm_only)
     del acts, ws
 
     # bf16 comparator: torch's GEMM (hipBLASLt) on the same shapes, the same
@@ -264,6 +274,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--launch", choices=["graph", "eager"], default="graph",
+                    help="replay the timed steps as one captured HIP graph (default) or "
+                         "launch every call from the host")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the quantized GEMM runs on a single MI355X; "
@@ -276,7 +289,8 @@ def main():
 
     import workloads
     case = workloads.make(args.workload)
-    r = run_gpu(case, args.steps, args.warmup, rotate=not args.no_rotate)
+    r = run_gpu(case, args.steps, args.warmup, rotate=not args.no_rotate,
+                graph=args.launch == "graph")
     alg = algorithmic(case, r["info"])
     ms = r["total_ms"] / args.steps
     tops = alg["ops"] / (ms * 1e-3) / 1e12
@@ -289,7 +303,8 @@ def main():
                    "a_bits": sorted(set(case["a_bits"].tolist())),
                    "w_bits": sorted(set(case["w_bits"].tolist())),
                    "a_signed": bool(case["a_signed"]),
-                   "activation_copies": r["na"], "weight_copies": r["nw"]},
+                   "activation_copies": r["na"], "weight_copies": r["nw"],
+                   "launch": args.launch},
         "roofline": roofline(case, alg, r),
         "breakdown_ms": {"quantize_act": r["q_ms"], "mp_gemm": r["g_ms"],
                          "pack_weights_once": r["pack_ms"]},

@@ -3,18 +3,22 @@
 //   k_wpack         quantize one output channel, place its codes on the
 //                   group-ordered padded channel axis and write its units
 //                   into its 16-row block; record scale and code sums
-//   k_absmax_*      per-activation-group max-abs over all rows; the last
-//                   workgroup writes the group scales
-//   k_act_pack      quantize, re-order and pack one activation row
+//   k_act_coop      activation quantize in one pass over HBM: a resident
+//                   grid holds its rows in registers, folds the group
+//                   maxima at a grid barrier, quantizes and packs
+//   k_absmax_*      two-pass form, pass 1: per-workgroup partial maxima
+//   k_act_blk16,    two-pass form, pass 2: reduce the partials, quantize,
+//   k_act_rows      pack 16- or 8-row slices (or rows)
 //   k_act_small     small batches in one launch (max, quantize, pack)
-//   k_gemm          int8 MFMA GEMM on packed operands: a 3-stage ring of
-//                   LDS buffers filled by direct global->LDS loads of packed
-//                   fragments, unpacked to int8 in registers right before
-//                   v_mfma_i32_16x16x64_i8, one int32 accumulator set per
-//                   activation group, fixed-order fp32 epilogue to bf16
-//   k_gemv          batch <= 8 decode without matrix cores: one workgroup
-//                   streams one 16-row weight block with 128-bit loads and
-//                   v_dot4_i32_i8 against activations unpacked in LDS
+//   k_act_row1      one row, from registers after a single load
+//   k_gemm          int8 MFMA GEMM on packed operands: an LDS ring filled by
+//                   direct global->LDS buffer loads, units widened to int8
+//                   in registers right before v_mfma_i32_16x16x64_i8, one
+//                   int32 accumulator set per activation group, fixed-order
+//                   fp32 epilogue to bf16
+//   k_gemv          batch <= 8 without matrix cores: one workgroup streams
+//                   one 16-row weight block, v_dot8_i32_i4 on nibbles or
+//                   v_dot4_i32_i8 on bytes against activations in LDS
 //
 // Paper passages: Sec. 2.4 C1/C2/C5; Sec. 3 codec (group max-abs scale,
 // unsigned codes, Eq. 1 weight codes); Alg. 1 channel permutation and Phase
@@ -1166,6 +1170,54 @@ __global__ __launch_bounds__(256) void k_act_small(const float* __restrict__ A, 
   }
   __syncthreads();
   write_act_units(codes, 1, m, ap, packed);
+}
+
+// ------------------------------------------------------------ k_act_row1 --
+// One row (a decode step), aligned, no sign-code group: a single workgroup
+// loads the row and its planned positions once (thread tid owns float4
+// positions tid + 256*j, j < J), reduces the group maxima, then quantizes
+// from registers (group 1 starts at planned position kpad[0]) into LDS and
+// writes the row's units.  One HBM round trip instead of two.
+// Dynamic LDS: Kp bytes.
+template <int J>
+__global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, int K4,
+                                                  const int32_t* __restrict__ pos, ActPlan ap,
+                                                  float* __restrict__ s_a_out,
+                                                  uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  __shared__ float red[8];
+  const int tid = threadIdx.x;
+  const int kp0 = ap.kpad[0];
+  float4 v[J];
+  int4 p[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int k4 = min(tid + 256 * j, K4 - 1);  // repeats change no max
+    v[j] = reinterpret_cast<const float4*>(A)[k4];
+    p[j] = reinterpret_cast<const int4*>(pos)[k4];
+  }
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < ap.Kp / 4; i += 256) codes32[i] = 0;
+  float mx0 = 0.0f, mx1 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+    max4(v[j], make_uchar4(p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0), mx0, mx1);
+  const float2 m = block_max2(make_float2(mx0, mx1), red);  // syncs
+  const float s0 = group_scale(m.x, ap.q[0]);
+  const float s1 = ap.S == 2 ? group_scale(m.y, ap.q[1]) : 0.0f;
+  if (tid == 0) {
+    s_a_out[0] = s0;
+    s_a_out[1] = s1;
+  }
+  const QPair q = qpair(qelem(s0, ap.q[0], ap.zp[0]), qelem(s1, ap.q[1], ap.zp[1]));
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+    if (tid + 256 * j < K4) {
+      const bool h[4] = {p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0};
+      qstore4g(v[j], h, q, codes, p[j]);
+    }
+  __syncthreads();
+  write_act_units(codes, 1, 0, ap, packed);
 }
 
 // ------------------------------------------------------------ GEMM/GEMV --
@@ -2417,12 +2469,26 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             hipStream_t stream) {
   const bool aligned = (K % 4 == 0) && (lda % 4 == 0) &&
                        (reinterpret_cast<uintptr_t>(A) % 16 == 0);
+  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
+  if (aligned && M == 1 && !sign && K / 4 <= 256 * 16) {
+    const int K4 = (int)(K / 4);
+    const int J = (K4 + 255) / 256;
+#define SONIQ_ROW1(J_)                                                                          \
+  hipLaunchKernelGGL((k_act_row1<J_>), dim3(1), dim3(256), (size_t)ap.Kp, stream, A, K4, pos_dev, \
+                     ap, s_a, packed)
+    if (J <= 1) SONIQ_ROW1(1);
+    else if (J <= 2) SONIQ_ROW1(2);
+    else if (J <= 4) SONIQ_ROW1(4);
+    else if (J <= 8) SONIQ_ROW1(8);
+    else SONIQ_ROW1(16);
+#undef SONIQ_ROW1
+    return hipGetLastError();
+  }
   if (aligned && M <= 64 && M * K <= kSmallElems) {
     hipLaunchKernelGGL(k_act_small, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A,
                        (int)M, (int)K, lda, pos_dev, seg_dev, ap, s_a, packed);
     return hipGetLastError();
   }
-  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
   if (aligned && !sign && M * K >= kCoopMinElems) {
     hipError_t e = hipSuccess;
     if (launch_act_coop(A, M, K, lda, ap, pos_dev, counter, s_a, packed, stream, e))
