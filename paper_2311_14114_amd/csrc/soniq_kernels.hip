@@ -1231,6 +1231,7 @@ struct GemmArgs {
   uint16_t* Y;
   int64_t ldy;
   int32_t* acc;
+  int xcd_tiles;  // GEMM: give each XCD a contiguous range of tiles
 };
 
 // Workgroup barrier without a memory fence: the LDS ring is filled by
@@ -1761,7 +1762,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const int wm = wid >> 1, wn = wid & 1;
   const ActPlan& ap = a.ap;
   const int ntn = a.wp.Np / kGemmBN;
-  const int mt = blockIdx.x / ntn, nt = blockIdx.x - mt * ntn;
+  // Workgroups go round-robin to the 8 XCDs (b mod 8), each with its own
+  // L2.  On grids of a few rounds XCD x takes a contiguous range of tiles,
+  // so the N tiles of one row block share that L2 for their activation
+  // reads and for the partial output lines they write (a tile's output
+  // columns are scattered); longer grids keep the launch order, whose
+  // concurrent tiles share weight tiles across XCDs.
+  const int G = (int)gridDim.x, x = (int)(blockIdx.x & 7), l = (int)(blockIdx.x >> 3);
+  const int tile = a.xcd_tiles ? x * (G >> 3) + min(x, G & 7) + l : (int)blockIdx.x;
+  const int mt = tile / ntn, nt = tile - mt * ntn;
   const int64_t m0 = (int64_t)mt * BM;
   const int jb0 = nt * 8;
 
@@ -2578,6 +2587,7 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.Y = Y;
   a.ldy = ldy;
   a.acc = acc;
+  a.xcd_tiles = 0;
   return a;
 }
 
@@ -2613,10 +2623,12 @@ static int gemm_shape(int64_t M, int ntn) {
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
-  const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const int ca0 = ap.c[0], ca1 = ap.S == 2 ? ap.c[1] : 0;
   const int cl = wp.c_lo, ch = wp.c_hi;
   const int shape = gemm_shape(M, wp.Np / kGemmBN);
+  const int64_t tiles = (shape == 3 ? (M + 127) / 128 : (M + 63) / 64) * (wp.Np / kGemmBN);
+  a.xcd_tiles = tiles <= 2048;  // a few rounds of two workgroups per CU
   if (ap.S == 2 && ca0 == 4 && ca1 == 8) {
     if (cl == 4 && ch == 8) launch_gemm_t<2, 4, 8, 4, 8>(a, M, shape, stream);
     else if (cl == 2 && ch == 8) launch_gemm_t<2, 4, 8, 2, 8>(a, M, shape, stream);
