@@ -10,7 +10,7 @@
 //   k_act_blk16,    two-pass form, pass 2: reduce the partials, quantize,
 //   k_act_rows      pack 16- or 8-row slices (or rows)
 //   k_act_small     small batches in one launch (max, quantize, pack)
-//   k_act_row1      one row, from registers after a single load
+//   k_act_row1      batches of up to 8 rows, from registers after one load
 //   k_gemm          int8 MFMA GEMM on packed operands: an LDS ring filled by
 //                   direct global->LDS buffer loads, units widened to int8
 //                   in registers right before v_mfma_i32_16x16x64_i8, one
@@ -1173,39 +1173,47 @@ __global__ __launch_bounds__(256) void k_act_small(const float* __restrict__ A, 
 }
 
 // ------------------------------------------------------------ k_act_row1 --
-// One row (a decode step), aligned, no sign-code group: a single workgroup
-// loads the row and its planned positions once (thread tid owns float4
-// positions tid + 256*j, j < J), reduces the group maxima, then quantizes
-// from registers (group 1 starts at planned position kpad[0]) into LDS and
-// writes the row's units.  One HBM round trip instead of two.
+// Batches of at most MT rows (decode steps), aligned, no sign-code group:
+// workgroup m loads every row of the batch and the planned positions once
+// (thread tid owns float4 positions tid + 256*j, j < J, of every row),
+// reduces the group maxima of the batch from registers, then quantizes
+// its own row m (group 1 starts at planned position kpad[0]) into LDS and
+// writes the row's units.  One HBM round trip instead of two; every
+// workgroup computes the same maxima from the same data.
 // Dynamic LDS: Kp bytes.
-template <int J>
-__global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, int K4,
-                                                  const int32_t* __restrict__ pos, ActPlan ap,
-                                                  float* __restrict__ s_a_out,
+template <int J, int MT>
+__global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, int M, int K4,
+                                                  int64_t lda, const int32_t* __restrict__ pos,
+                                                  ActPlan ap, float* __restrict__ s_a_out,
                                                   uint8_t* __restrict__ packed) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
   const int tid = threadIdx.x;
+  const int m = blockIdx.x;
   const int kp0 = ap.kpad[0];
-  float4 v[J];
+  float4 v[MT][J];
   int4 p[J];
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int k4 = min(tid + 256 * j, K4 - 1);  // repeats change no max
-    v[j] = reinterpret_cast<const float4*>(A)[k4];
     p[j] = reinterpret_cast<const int4*>(pos)[k4];
+#pragma unroll
+    for (int r = 0; r < MT; ++r)
+      v[r][j] = reinterpret_cast<const float4*>(A + (int64_t)min(r, M - 1) * lda)[k4];
   }
   uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
   for (int i = tid; i < ap.Kp / 4; i += 256) codes32[i] = 0;
   float mx0 = 0.0f, mx1 = 0.0f;
 #pragma unroll
-  for (int j = 0; j < J; ++j)
-    max4(v[j], make_uchar4(p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0), mx0, mx1);
-  const float2 m = block_max2(make_float2(mx0, mx1), red);  // syncs
-  const float s0 = group_scale(m.x, ap.q[0]);
-  const float s1 = ap.S == 2 ? group_scale(m.y, ap.q[1]) : 0.0f;
-  if (tid == 0) {
+  for (int j = 0; j < J; ++j) {
+    const uchar4 g = make_uchar4(p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0);
+#pragma unroll
+    for (int r = 0; r < MT; ++r) max4(v[r][j], g, mx0, mx1);
+  }
+  const float2 mm = block_max2(make_float2(mx0, mx1), red);  // syncs
+  const float s0 = group_scale(mm.x, ap.q[0]);
+  const float s1 = ap.S == 2 ? group_scale(mm.y, ap.q[1]) : 0.0f;
+  if (m == 0 && tid == 0) {
     s_a_out[0] = s0;
     s_a_out[1] = s1;
   }
@@ -1214,10 +1222,14 @@ __global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, i
   for (int j = 0; j < J; ++j)
     if (tid + 256 * j < K4) {
       const bool h[4] = {p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0};
-      qstore4g(v[j], h, q, codes, p[j]);
+      float4 x = v[0][j];
+#pragma unroll
+      for (int r = 1; r < MT; ++r)
+        if (r == m) x = v[r][j];
+      qstore4g(x, h, q, codes, p[j]);
     }
   __syncthreads();
-  write_act_units(codes, 1, 0, ap, packed);
+  write_act_units(codes, 1, m, ap, packed);
 }
 
 // ------------------------------------------------------------ GEMM/GEMV --
@@ -2128,11 +2140,13 @@ __device__ __forceinline__ int gemv_row_of(int u, int d) {
   return m;
 }
 
-// Activation staging: rows 0..M-1 of block 0 of both groups go to LDS,
-// group 0 as packed 8-byte nibble units [m][q][kg] (NIB) or widened to
-// bytes, group 1 as bytes [m][q][kg] at nbase.  A unit is loaded as 16
-// bytes through a buffer resource over the activation buffer (group 0
-// units use the first half); indexes past the last unit read as zero.
+// Activation staging: rows 0..M-1 of block 0 of both groups go to LDS.
+// For a nibble-path block (NIB): group 0 as packed 8-byte nibble units
+// [m][q][kg], group 1 as bytes [m][q - ng0][kg] at nbase = M*ng0*32.
+// Otherwise every unit as bytes [m][q][kg] (group 0 widened).  A unit is
+// loaded as 16 bytes through a buffer resource over the activation buffer
+// (group 0 units use the first half); indexes past the last unit read as
+// zero.
 template <int MT>
 constexpr int gemv_xr() { return MT == 1 ? 2 : MT == 2 ? 3 : MT <= 4 ? 5 : 9; }
 
@@ -2169,9 +2183,11 @@ __device__ __forceinline__ void gemv_store_x(const GemmArgs& a, int u0,
       const int m = gemv_row_of<MT>(u, d), rest = u - m * d;
       if (rest < d0 && NIB) {
         *reinterpret_cast<uint2*>(xs + m * d0 * 8 + rest * 8) = make_uint2(xl[i].x, xl[i].y);
+      } else if (NIB) {
+        *reinterpret_cast<uint4*>(xs + nbase + (m * (d - d0) + rest - d0) * 16) = xl[i];
       } else {
         const uint4 v = rest < d0 ? unpack4(xl[i].x, xl[i].y) : xl[i];
-        *reinterpret_cast<uint4*>(xs + nbase + (m * d + rest) * 16) = v;
+        *reinterpret_cast<uint4*>(xs + (m * d + rest) * 16) = v;
       }
     }
   }
@@ -2235,7 +2251,10 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
 #pragma unroll
     for (int mm = 0; mm < MT; ++mm) {
       if (mm < M) {
-        const uint4 x = *reinterpret_cast<const uint4*>(xs + nbase + (mm * ngt + xq) * 64 + kg * 16);
+        // NIB blocks read group 1 only, staged from granule ng0 on
+        const uint4 x = *reinterpret_cast<const uint4*>(
+            NIB ? xs + nbase + (mm * (ngt - ng0) + xq - ng0) * 64 + kg * 16
+                : xs + (mm * ngt + xq) * 64 + kg * 16);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const int v = dot16(chunk_bytes<CW>(raw, u), x, 0);
@@ -2354,7 +2373,7 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
   }
 }
 
-// Dynamic LDS: M * (Kp + 32 * ng0) bytes.
+// Dynamic LDS: the staged rows (see gemv_lds).
 template <int MT>
 __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
   extern __shared__ __align__(16) uint8_t xs[];
@@ -2364,7 +2383,10 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
   if (c == 2) gemv4_block<MT, 2, true>(a, xs, blk, red);
   else if (c == 4) gemv4_block<MT, 4, true>(a, xs, blk, red);
   else if (c == 8) gemv4_block<MT, 8, false>(a, xs, blk, red);
-  else gemv4_block<MT, 1, false>(a, xs, blk, red);
+  // 1-bit blocks keep eight row accumulators per lane and batch row; the
+  // host sends them here only for batches of at most 4 rows, so larger
+  // instances are compiled without that path (and its registers)
+  else if constexpr (MT <= 4) gemv4_block<MT, 1, false>(a, xs, blk, red);
 }
 
 
@@ -2479,18 +2501,28 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   const bool aligned = (K % 4 == 0) && (lda % 4 == 0) &&
                        (reinterpret_cast<uintptr_t>(A) % 16 == 0);
   const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
-  if (aligned && M == 1 && !sign && K / 4 <= 256 * 16) {
+  // batches of one row (up to 16 float4 per thread) or up to 8 rows (up
+  // to 4 float4 per thread and row): every row loaded once
+  if (aligned && !sign && ((M == 1 && K / 4 <= 256 * 16) || (M <= 8 && K / 4 <= 256 * 4))) {
     const int K4 = (int)(K / 4);
     const int J = (K4 + 255) / 256;
-#define SONIQ_ROW1(J_)                                                                          \
-  hipLaunchKernelGGL((k_act_row1<J_>), dim3(1), dim3(256), (size_t)ap.Kp, stream, A, K4, pos_dev, \
-                     ap, s_a, packed)
-    if (J <= 1) SONIQ_ROW1(1);
-    else if (J <= 2) SONIQ_ROW1(2);
-    else if (J <= 4) SONIQ_ROW1(4);
-    else if (J <= 8) SONIQ_ROW1(8);
-    else SONIQ_ROW1(16);
-#undef SONIQ_ROW1
+#define SONIQ_ROWS(J_, MT_)                                                                       \
+  hipLaunchKernelGGL((k_act_row1<J_, MT_>), dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A, \
+                     (int)M, K4, lda, pos_dev, ap, s_a, packed)
+    if (M == 1) {
+      if (J <= 1) SONIQ_ROWS(1, 1);
+      else if (J <= 2) SONIQ_ROWS(2, 1);
+      else if (J <= 4) SONIQ_ROWS(4, 1);
+      else if (J <= 8) SONIQ_ROWS(8, 1);
+      else SONIQ_ROWS(16, 1);
+    } else if (M <= 2) {
+      if (J <= 2) SONIQ_ROWS(2, 2); else SONIQ_ROWS(4, 2);
+    } else if (M <= 4) {
+      if (J <= 2) SONIQ_ROWS(2, 4); else SONIQ_ROWS(4, 4);
+    } else {
+      if (J <= 2) SONIQ_ROWS(2, 8); else SONIQ_ROWS(4, 8);
+    }
+#undef SONIQ_ROWS
     return hipGetLastError();
   }
   if (aligned && M <= 64 && M * K <= kSmallElems) {
@@ -2643,12 +2675,12 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
   return hipGetLastError();
 }
 
-static size_t gemv_lds(int64_t M, const ActPlan& ap);
+static size_t gemv_lds(int64_t M, const ActPlan& ap, const WPlan& wp);
 
 bool gemv_fits(int64_t M, const ActPlan& ap, const WPlan& wp) {
   if (M < 1 || M > 8) return false;
   // dynamic LDS (activation rows) plus the static reduction buffer
-  if (gemv_lds(M, ap) + (size_t)2048 * 8 > 64 * 1024) return false;
+  if (gemv_lds(M, ap, wp) + (size_t)2048 * 8 > 64 * 1024) return false;
   // 1-bit weight blocks keep 8 rows per lane: at most 4 activation rows.
   if ((wp.c_lo == 1 || wp.c_hi == 1) && M > 4) return false;
   // buffer-resource offsets into the activation and weight buffers are 32-bit
@@ -2664,8 +2696,14 @@ static bool gemv_nibble_plan(const ActPlan& ap) {
   return ap.c[0] == 4 && (ap.S == 1 || ap.c[1] == 8);
 }
 
-static size_t gemv_lds(int64_t M, const ActPlan& ap) {
-  return gemv_nibble_plan(ap) ? (size_t)M * (ap.Kp + 32 * ap.ng[0]) : (size_t)M * ap.Kp;
+// Staged rows: M*Kp bytes as bytes; a nibble-path block needs
+// M*(32*ng0 + 64*ng1) <= M*Kp, which is all a launch needs when every
+// weight block takes the nibble path (2- and 4-bit containers).
+static size_t gemv_lds(int64_t M, const ActPlan& ap, const WPlan& wp) {
+  const bool all_nib = gemv_nibble_plan(ap) && (wp.c_lo == 2 || wp.c_lo == 4) &&
+                       (wp.c_hi == 2 || wp.c_hi == 4);
+  const int ng1 = ap.S == 2 ? ap.ng[1] : 0;
+  return all_nib ? (size_t)M * (32 * ap.ng[0] + 64 * ng1) : (size_t)M * ap.Kp;
 }
 
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
@@ -2673,7 +2711,7 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
   const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   dim3 grid((unsigned)wp.nblk);
-  const size_t lds = gemv_lds(M, ap);
+  const size_t lds = gemv_lds(M, ap, wp);
   if (gemv_nibble_plan(ap)) {
     if (M == 1) hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
     else if (M == 2) hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), lds, stream, a);
