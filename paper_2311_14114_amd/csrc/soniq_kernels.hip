@@ -19,6 +19,8 @@
 //   k_gemv          batch <= 8 without matrix cores: one workgroup streams
 //                   one 16-row weight block, v_dot8_i32_i4 on nibbles or
 //                   v_dot4_i32_i8 on bytes against activations in LDS
+//   k_gemv_mfma     batch 2..8: one workgroup per weight block, the batch
+//                   rows as the MFMA A operand, straight from global memory
 //
 // Paper passages: Sec. 2.4 C1/C2/C5; Sec. 3 codec (group max-abs scale,
 // unsigned codes, Eq. 1 weight codes); Alg. 1 channel permutation and Phase
@@ -2390,6 +2392,124 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
 }
 
 
+// ----------------------------------------------------------- k_gemv_mfma --
+// Batches of 2..8 rows with activation containers 4 (group 0) and 8
+// (group 1): one workgroup per 16-row weight block, as in k_gemv, but the
+// products run on v_mfma_i32_16x16x64_i8 with the batch rows as the A
+// operand (rows past M are never read out) and the block's 16 weight rows
+// as B.  The block's bytes go global -> LDS in 16-byte chunks, all in
+// flight at once; both buffers are fragment-major, so lane l reads unit l
+// of a granule as its operand (the activations straight from global
+// memory, where every workgroup finds them in L2).  Wave w takes granules
+// w, w + 4, ... of each group in batches of kMB; the four partial 16x16
+// sums per group meet in LDS and the block's 16 columns get the GEMM's
+// exact epilogue.  Dynamic LDS: the largest block (ngt * 128 * c_hi bytes)
+// rounded up to 1 KB.
+constexpr int kMB = 4;
+
+template <int CW>
+__device__ __forceinline__ void gemv_mfma_block(const GemmArgs& a, int blk, uint8_t* wl,
+                                                int (&red)[4][2][4][64]) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const ActPlan& ap = a.ap;
+  const int ngt = a.wp.ngt, ng0 = ap.ng[0], ng1 = ngt - ng0;
+  {
+    const int nch = ngt * 8 * CW;  // 16-byte chunks of the block
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.wd.packed + wblk_off(a.wp, blk)), (short)0, nch * 16, 0x00020000);
+    const uint32_t base = lds_off(wl);
+    // a wave's 64 chunks land at base + 16 * (256i + 64 wid + lane); waves
+    // wholly past the block skip, the last partial one writes zeros up to
+    // the next 64-chunk boundary (the allocation covers it)
+    for (int i = 0; 256 * i < nch; ++i) {
+      const int ch = 256 * i + tid;
+      if (256 * i + 64 * wid < nch)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            wr, (__attribute__((address_space(3))) void*)(uintptr_t)(base + (256 * i + 64 * wid) * 16),
+            16, ch < nch ? (uint32_t)ch * 16 : kOOB, 0, 0, 0);
+    }
+  }
+  const uint8_t* x0 = a.act + ap.seg_off[0] + lane * 8;
+  const uint8_t* x1 = a.act + (ap.S == 2 ? ap.seg_off[1] : 0) + lane * 16;
+  // epilogue inputs, requested before the stream lands
+  const int pc = blk * kBlk + (lane & 15);
+  const ColInfo ci = a.wd.colinfo[pc];
+  const uint8_t shw = a.wd.shw[pc];
+  const float sa0 = a.s_a[0], sa1 = ap.S == 2 ? a.s_a[1] : 0.0f;
+  wait_vm<0>();
+  __syncthreads();
+
+  auto wunit = [&](int q) __attribute__((always_inline)) {
+    uint4 r = make_uint4(0u, 0u, 0u, 0u);
+    const uint8_t* p = wl + (q * 64 + lane) * 2 * CW;
+    if constexpr (CW == 8) r = *reinterpret_cast<const uint4*>(p);
+    else if constexpr (CW == 4) { const uint2 v = *reinterpret_cast<const uint2*>(p); r.x = v.x; r.y = v.y; }
+    else if constexpr (CW == 2) r.x = *reinterpret_cast<const uint32_t*>(p);
+    else r.x = *reinterpret_cast<const uint16_t*>(p);
+    return r;
+  };
+  v4i acc0 = v4i{0, 0, 0, 0}, acc1 = v4i{0, 0, 0, 0};
+  for (int q = wid; q < ng0; q += 4 * kMB) {
+    uint2 xa[kMB];
+#pragma unroll
+    for (int i = 0; i < kMB; ++i) xa[i] = *reinterpret_cast<const uint2*>(x0 + min(q + 4 * i, ng0 - 1) * 512);
+#pragma unroll
+    for (int i = 0; i < kMB; ++i)
+      if (q + 4 * i < ng0)
+        acc0 = __builtin_amdgcn_mfma_i32_16x16x64_i8(frag_of(unpack4(xa[i].x, xa[i].y)),
+                                                     frag_of(unpack_unit<CW>(wunit(q + 4 * i))),
+                                                     acc0, 0, 0, 0);
+  }
+  for (int q = wid; q < ng1; q += 4 * kMB) {
+    uint4 xa[kMB];
+#pragma unroll
+    for (int i = 0; i < kMB; ++i) xa[i] = *reinterpret_cast<const uint4*>(x1 + min(q + 4 * i, ng1 - 1) * 1024);
+#pragma unroll
+    for (int i = 0; i < kMB; ++i)
+      if (q + 4 * i < ng1)
+        acc1 = __builtin_amdgcn_mfma_i32_16x16x64_i8(frag_of(xa[i]),
+                                                     frag_of(unpack_unit<CW>(wunit(ng0 + q + 4 * i))),
+                                                     acc1, 0, 0, 0);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    red[wid][0][e][lane] = acc0[e];
+    red[wid][1][e][lane] = acc1[e];
+  }
+  __syncthreads();
+  if (wid == 0 && ci.n >= 0) {
+    const int sh0 = ap.sh[0] + (shw & 0x7F), sh1 = ap.sh[1] + (shw & 0x7F);
+    const int add0 = ap.zp[0] * ci.colsum[0], add1 = ap.zp[1] * ci.colsum[1];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = (lane >> 4) * 4 + e;  // batch row of this lane's sum e
+      if (m < a.M) {
+        const int r0 = red[0][0][e][lane] + red[1][0][e][lane] + red[2][0][e][lane] + red[3][0][e][lane];
+        const int r1 = red[0][1][e][lane] + red[1][1][e][lane] + red[2][1][e][lane] + red[3][1][e][lane];
+        const int t0 = (r0 >> sh0) + add0;
+        const int t1 = ap.S == 2 ? (r1 >> sh1) + add1 : 0;
+        a.Y[(int64_t)m * a.ldy + ci.n] = bf16_rne(epilogue(t0, t1, ap.S, sa0, sa1, ci.s_w));
+        if (a.acc) {
+          a.acc[(int64_t)m * a.N + ci.n] = t0;
+          if (ap.S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
+        }
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_gemv_mfma(GemmArgs a) {
+  extern __shared__ __align__(16) uint8_t wl[];
+  __shared__ int red[4][2][4][64];
+  const int blk = blockIdx.x;
+  const int c = wblk_c(a.wp, blk);
+  if (c == 2) gemv_mfma_block<2>(a, blk, wl, red);
+  else if (c == 4) gemv_mfma_block<4>(a, blk, wl, red);
+  else if (c == 8) gemv_mfma_block<8>(a, blk, wl, red);
+  else gemv_mfma_block<1>(a, blk, wl, red);
+}
+
 // ------------------------------------------------- single-pass quantize --
 // Batches of at least kCoopMinElems elements whose rows fit the registers
 // of one resident grid take k_act_coop: RB rows per workgroup (4, 8 or 16,
@@ -2712,7 +2832,16 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
   const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   dim3 grid((unsigned)wp.nblk);
   const size_t lds = gemv_lds(M, ap, wp);
-  if (gemv_nibble_plan(ap)) {
+  // Batches of 2..8 rows: the products on matrix cores.  SONIQ_GEMV_MFMA
+  // (0: never, 2: for single rows too) overrides the choice for
+  // measurement; results are the same.
+  bool mfma = M >= 2;
+  if (const char* env = getenv("SONIQ_GEMV_MFMA")) mfma = atoi(env) == 2 || (mfma && atoi(env) != 0);
+  // largest weight block, in whole 64-chunk (1 KB) wave batches
+  const size_t wblock = (size_t)(wp.ngt * 8 * wp.c_hi + 63) / 64 * 1024;
+  if (gemv_nibble_plan(ap) && mfma && wblock + sizeof(int) * 2048 <= 64 * 1024) {
+    hipLaunchKernelGGL(k_gemv_mfma, grid, dim3(256), wblock, stream, a);
+  } else if (gemv_nibble_plan(ap)) {
     if (M == 1) hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
     else if (M == 2) hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), lds, stream, a);
     else if (M <= 4) hipLaunchKernelGGL(k_gemv<4>, grid, dim3(256), lds, stream, a);
