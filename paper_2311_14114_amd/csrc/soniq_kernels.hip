@@ -615,10 +615,13 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
 // One group's units of a 16-row block whose stored codes sit in LDS (row r
 // at codes + r*Kp + gbase): granule q holds units l = kg*16 + r of 2C bytes
 // (128C contiguous bytes); 16-byte piece w holds units w*U .. w*U+U-1
-// (U = 8/C), i.e. rows of one 16-channel group.
+// (U = 8/C), i.e. rows of one 16-channel group.  zx (a byte replicated)
+// is XORed into every code byte first: codes held without their zero
+// point get it applied here.
 template <int C, int RB>
 __device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int Kp, int gbase, int ng,
-                                                   int r0, uint8_t* __restrict__ dst) {
+                                                   int r0, uint8_t* __restrict__ dst,
+                                                   uint32_t zx = 0u) {
   constexpr int U = 8 / C;            // units per piece
   constexpr int PK = RB / U > 0 ? RB / U : 1;  // pieces per 16-channel group
   static_assert(RB % U == 0, "row range covers whole pieces");
@@ -632,7 +635,7 @@ __device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int Kp,
     for (int u = 0; u < U; ++u) {
       const int l = w * U + u, r = (l & 15) - r0;
       const uint4 d = *reinterpret_cast<const uint4*>(codes + r * Kp + gbase + q * kGran + kg * 16);
-      const uint4 pk = pack_unit(d.x, d.y, d.z, d.w, C);
+      const uint4 pk = pack_unit(d.x ^ zx, d.y ^ zx, d.z ^ zx, d.w ^ zx, C);
       if constexpr (C == 8) {
         wd[0] = pk.x; wd[1] = pk.y; wd[2] = pk.z; wd[3] = pk.w;
       } else if constexpr (C == 4) {
@@ -732,6 +735,23 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt(SONIQ_VMCNT_IMM(N));
 }
 
+// Workgroup barrier without a memory fence, for LDS filled by direct
+// loads whose completion each wave has already awaited with wait_vm; the
+// compiler fences keep LDS accesses on their side.
+__device__ __forceinline__ void bar_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// All but the last N loads of this wave have landed, direct-to-LDS ones
+// included; LDS reads stay after it.
+template <int N>
+__device__ __forceinline__ void lds_dma_wait() {
+  wait_vm<N>();
+  asm volatile("" ::: "memory");
+}
+
 // Buffer-resource offset past any buffer: the load returns zero without
 // touching memory.
 constexpr uint32_t kOOB = 0x7FFFFFF0u;
@@ -794,8 +814,8 @@ __device__ __forceinline__ void bar_after(unsigned v) {
   asm volatile("" ::"v"(v) : "memory");
 }
 
-// This workgroup's generation word; read it (thread 0) when the kernel
-// starts, since it cannot move before every workgroup has arrived.
+// This workgroup's generation word; thread 0 reads it before arriving (it
+// cannot move before every workgroup has arrived).
 __device__ __forceinline__ unsigned* grid_gen_word(unsigned* st) {
   return st + kBarGen + 32 * (blockIdx.x & 7);
 }
@@ -958,6 +978,63 @@ __device__ __forceinline__ void qstore4g(const float4& v, const bool (&h)[4], co
   row[p.w] = (uint8_t)c[3];
 }
 
+// Codes without the zero point, for the single pass: a group's zero point
+// (0 or 2^(c-1) there, c >= 2) is applied as an XOR of each code byte when
+// its units are packed.  Unsigned codes lie in [0, hi], signed ones in
+// [-hi, hi]; the single pass never has a sign (1-bit) group.
+//
+// The shortcut: t = fma(x, rcp(s), kShift) rounds the exact product
+// x * rcp(s) to the nearest integer n, held as kShift + n, and the low
+// byte of t's bits is the code (clamped below at kShift, i.e. code 0, when
+// unsigned).  No upper clamp is needed: |x| is at most the group's
+// maximum m, s = m / hi rounded, and rcp(s) is within an ulp, so
+// |x * rcp(s)| <= hi * (1 + 2^-22) < hi + 1/2.  The product differs from
+// x/s by at most 2^-15 (|x/s| <= 256); its residue d = x * rcp(s) - n
+// (|d| <= 1/2, one more fma) is checked for the four elements together:
+// any one within kTieBand of a tie sends that element to the exact
+// division.
+template <bool SIGNED>
+__device__ __forceinline__ void qcodes4(const float4& v, int4 p, int kp0, float rs0, float rs1,
+                                        float s0, float s1, float hi0, float hi1, uint8_t* row) {
+  const float xs[4] = {v.x, v.y, v.z, v.w};
+  const int pp[4] = {p.x, p.y, p.z, p.w};
+  int c[4];
+  float d[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float rs = pp[e] >= kp0 ? rs1 : rs0;
+    const float t = __builtin_fmaf(xs[e], rs, kShift);
+    c[e] = __float_as_int(SIGNED ? t : fmaxf(t, kShift));
+    d[e] = __builtin_fmaf(xs[e], rs, kShift - t);
+  }
+  const float dm = fmaxf(fmaxf(fabsf(d[0]), fabsf(d[1])), fmaxf(fabsf(d[2]), fabsf(d[3])));
+  if (dm >= 0.5f - kTieBand) [[unlikely]] {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (fabsf(d[e]) >= 0.5f - kTieBand) {
+        const bool g1 = pp[e] >= kp0;
+        const float hi = g1 ? hi1 : hi0;
+        c[e] = qexact(xs[e], SIGNED ? -hi : 0.0f, hi, 0.0f, g1 ? s1 : s0);
+      }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) row[pp[e]] = (uint8_t)c[e];
+}
+
+// The same codes by exact division alone (a scale outside the shortcut's
+// range).
+__device__ __forceinline__ void qcodes4_exact(const float4& v, int4 p, int kp0, float s0, float s1,
+                                              float lo0, float lo1, float hi0, float hi1,
+                                              uint8_t* row) {
+  const float xs[4] = {v.x, v.y, v.z, v.w};
+  const int pp[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bool g1 = pp[e] >= kp0;
+    row[pp[e]] = (uint8_t)qexact(xs[e], g1 ? lo1 : lo0, g1 ? hi1 : hi0, 0.0f, g1 ? s1 : s0);
+  }
+}
+
 // Waves per SIMD the register budget must allow: T <= 9 keeps seven
 // workgroups per CU resident (1568 four-row workgroups on 256 CUs), more
 // float4 per thread four.  TL of the T float4 per thread wait in LDS.
@@ -974,12 +1051,16 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
   const int64_t m0 = (int64_t)blockIdx.x * RB;
   const int rows = (int)min((int64_t)RB, M - m0);
   const int nf = RB * K4;  // flat positions of this workgroup (T*256 >= nf)
-  const int q256 = 256 / K4, r256 = 256 - q256 * K4;
+  // uniform: kept in SGPRs (the division runs on the vector unit)
+  const int q256 = __builtin_amdgcn_readfirstlane(256 / K4);
+  const int r256 = 256 - q256 * K4;
   const int kp0 = ap.kpad[0];  // planned positions >= kp0 belong to group 1
-  const float* A0 = A + m0 * lda;
-  int4* pos4 = reinterpret_cast<int4*>(codes + RB * ap.Kp);
+  // The generation word first (thread 0 of wave 0): its wait then rides on
+  // the table's, long before the maxima are folded.
   unsigned gen = 0;
   if (tid == 0) gen = bar_load(grid_gen_word(st));
+  const float* A0 = A + m0 * lda;
+  int4* pos4 = reinterpret_cast<int4*>(codes + RB * ap.Kp);
   // The position table goes global -> LDS directly (no registers), ahead
   // of the row loads: entry k of wave wid's chunk j (k = 256j + 64wid +
   // lane) lands at pos4[k]; lanes past K4 read zeros into the padding of
@@ -1002,9 +1083,11 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     }
     asm volatile("" ::: "memory");
   }
-  // slots i < TV in registers; the last TL slots go global -> LDS (lane l
-  // of wave w: vlds + (i - TV)*4096 + (64w + l)*16) where the register
-  // budget cannot hold them
+  // The first TL slots go global -> LDS (lane l of wave w: vlds + i*4096 +
+  // (64w + l)*16) where the register budget cannot hold them, slots
+  // i >= TL to registers.  Issued first, the LDS slots are what the first
+  // LDS read after the barrier waits for (any LDS read waits for the
+  // direct loads before it), and slot 0 is the first one the maxima need.
   constexpr int TV = T - TL;
   float4 v[TV];
   float4* vlds = reinterpret_cast<float4*>(codes + RB * ap.Kp + 16 * ((K4 + 63) / 64 * 64));
@@ -1024,23 +1107,33 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
       const int rc = in ? min(r, rows - 1) : rows - 1;
       const int kc = in ? k : K4 - 1;
       const uint32_t off = (uint32_t)rc * ld4 + 16u * (uint32_t)kc;
-      if (i < TV)
-        v[i < TV ? i : 0] =
+      if (i >= TL)
+        v[i >= TL ? i - TL : 0] =
             __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(ar, off, 0, 0));
       else
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            ar, (__attribute__((address_space(3))) void*)(uintptr_t)(vb + (i - TV) * 4096), 16, off,
-            0, 0, 0);
+            ar, (__attribute__((address_space(3))) void*)(uintptr_t)(vb + i * 4096), 16, off, 0, 0,
+            0);
       coop_step(r, k, K4, q256, r256);
     }
   }
-  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
-  for (int i = tid; i < RB * ap.Kp / 4; i += 256) codes32[i] = 0;
-  wait_vm<T>();  // this wave's table chunks (issued before the T row loads)
-  __syncthreads();
+  // Codes start as each group's zero point, which packs to a stored zero
+  // (the padding channels and rows no element writes).
+  {
+    uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+    const int kw = ap.Kp / 4, kw0 = kp0 / 4;
+    const uint32_t z0 = 0x01010101u * (uint32_t)ap.zp[0], z1 = 0x01010101u * (uint32_t)ap.zp[1];
+    for (int r = 0; r < RB; ++r)
+      for (int i = tid; i < kw; i += 256) codes32[r * kw + i] = i < kw0 ? z0 : z1;
+  }
+  // This wave's generation read and table chunks (issued before the T row
+  // loads) have landed; a barrier without a fence, so the row loads stay
+  // in flight and the maxima below fold each slot as it arrives.
+  wait_vm<T>();
+  bar_nofence();
   // slot i's float4 (the LDS ones are read where they are used)
   auto val = [&](int i) __attribute__((always_inline)) {
-    return i < TV ? v[i < TV ? i : 0] : vlds[(i - TV) * 256 + tid];
+    return i < TL ? vlds[i * 256 + tid] : v[i >= TL ? i - TL : 0];
   };
   float mx0 = 0.0f, mx1 = 0.0f;
   {
@@ -1048,6 +1141,7 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     coop_first(r, k, K4);
 #pragma unroll
     for (int i = 0; i < T; ++i) {
+      if (i == 0 && TL > 0) lds_dma_wait<TV>();  // the LDS slots, issued before the TV others
       const int4 p = pos4[tid + 256 * i < nf ? k : K4 - 1];
       max4(val(i), make_uchar4(p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0), mx0, mx1);
       coop_step(r, k, K4, q256, r256);
@@ -1071,18 +1165,41 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     s_a_out[0] = s0;
     s_a_out[1] = s1;
   }
-  const QPair q = qpair(qelem(s0, ap.q[0], ap.zp[0]), qelem(s1, ap.q[1], ap.zp[1]));
   {
-    int r, k;
-    coop_first(r, k, K4);
+    const float hi0 = (float)ap.q[0].hi, hi1 = (float)ap.q[1].hi;
+    const float lo0 = (float)ap.q[0].lo, lo1 = (float)ap.q[1].lo;
+    const bool fast = fast_ok(s0) && (ap.S == 1 || fast_ok(s1));
+    float rs0 = fast ? __builtin_amdgcn_rcpf(s0) : 0.0f;
+    float rs1 = fast && ap.S == 2 ? __builtin_amdgcn_rcpf(s1) : 0.0f;
+    auto each = [&](auto&& f) __attribute__((always_inline)) {
+      int r, k;
+      coop_first(r, k, K4);
+      int ro = r * ap.Kp;  // row r's codes; the row is stepped through ro alone
+      const int qk = __builtin_amdgcn_readfirstlane(q256 * ap.Kp);
+      const int lim = __builtin_amdgcn_readfirstlane(rows * ap.Kp);
 #pragma unroll
-    for (int i = 0; i < T; ++i) {
-      if (tid + 256 * i < nf && r < rows) {
-        const int4 p = pos4[k];
-        const bool h[4] = {p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0};
-        qstore4g(val(i), h, q, codes + r * ap.Kp, p);
+      for (int i = 0; i < T; ++i) {
+        if (tid + 256 * i < nf && ro < lim) f(val(i), pos4[k], codes + ro);
+        k += r256;
+        ro += qk;
+        if (k >= K4) {
+          k -= K4;
+          ro += ap.Kp;
+        }
       }
-      coop_step(r, k, K4, q256, r256);
+    };
+    if (!fast) {
+      each([&](const float4& x, int4 p, uint8_t* row) __attribute__((always_inline)) {
+        qcodes4_exact(x, p, kp0, s0, s1, lo0, lo1, hi0, hi1, row);
+      });
+    } else if (ap.q[0].lo < 0) {
+      each([&](const float4& x, int4 p, uint8_t* row) __attribute__((always_inline)) {
+        qcodes4<true>(x, p, kp0, rs0, rs1, s0, s1, hi0, hi1, row);
+      });
+    } else {
+      each([&](const float4& x, int4 p, uint8_t* row) __attribute__((always_inline)) {
+        qcodes4<false>(x, p, kp0, rs0, rs1, s0, s1, hi0, hi1, row);
+      });
     }
   }
   __syncthreads();
@@ -1093,10 +1210,11 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     const int gbase = gi ? ap.kpad[0] : 0;
     uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
                    (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
-#define SONIQ_PIECES(RB_)                                                         \
-  if (c == 8) write_block_pieces<8, RB_>(codes, ap.Kp, gbase, ng, r0, dst);        \
-  else if (c == 4) write_block_pieces<4, RB_>(codes, ap.Kp, gbase, ng, r0, dst);   \
-  else write_block_pieces<2, RB_>(codes, ap.Kp, gbase, ng, r0, dst)
+    const uint32_t zx = 0x01010101u * (uint32_t)(gi ? ap.zp[1] : ap.zp[0]);
+#define SONIQ_PIECES(RB_)                                                             \
+  if (c == 8) write_block_pieces<8, RB_>(codes, ap.Kp, gbase, ng, r0, dst, zx);        \
+  else if (c == 4) write_block_pieces<4, RB_>(codes, ap.Kp, gbase, ng, r0, dst, zx);   \
+  else write_block_pieces<2, RB_>(codes, ap.Kp, gbase, ng, r0, dst, zx)
     if (RB == 4) { SONIQ_PIECES(4); }
     else if (RB == 8) { SONIQ_PIECES(8); }
     else { SONIQ_PIECES(16); }
@@ -1247,15 +1365,6 @@ struct GemmArgs {
   int32_t* acc;
   int xcd_tiles;  // GEMM: give each XCD a contiguous range of tiles
 };
-
-// Workgroup barrier without a memory fence: the LDS ring is filled by
-// direct loads whose completion each wave has already awaited with
-// wait_vmcnt; the compiler fences keep LDS accesses on their side.
-__device__ __forceinline__ void bar_nofence() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 // 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
 __device__ __forceinline__ void load_lds16(const uint8_t* src, uint8_t* lds_dst_uniform) {
