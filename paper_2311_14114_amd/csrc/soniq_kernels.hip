@@ -1906,10 +1906,24 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   }
   const uint8_t* wtile = a.wd.packed + wblk_off(a.wp, jb0);
 
-  // The activation scales (written by the quantize launch just before) are
-  // requested now, so that they have arrived when the epilogue needs them.
+  // The activation scales (written by the quantize launch just before) and,
+  // on 64-row tiles, the wave's four columns of epilogue data are requested
+  // now, so that they have arrived when the epilogue needs them (the
+  // 128-row tiles have no registers to spare for the latter: two waves per
+  // SIMD need at most 256).
   const float sa0 = a.s_a[0];
   const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
+  ColInfo cinf[4];
+  uint8_t cshw[4], crank[4];
+  if constexpr (WFM <= 2) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
+      cinf[jj] = a.wd.colinfo[pc];
+      cshw[jj] = a.wd.shw[pc];
+      crank[jj] = a.wd.colrank[pc];
+    }
+  }
 
   v4i acc0[WFM][4];
 #pragma unroll
@@ -1961,18 +1975,18 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
-    const ColInfo ci = a.wd.colinfo[pc];
+    const ColInfo ci = WFM <= 2 ? cinf[jj] : a.wd.colinfo[pc];
     if (ci.n < 0) continue;
     // Exact accumulator of group g: (raw >> sh_g) + add_g, where add_g folds
     // the zero-point term and the sign x sign padding products (padcnt
     // products of +1 each, exact multiples of 2^sh_g in the raw sum).
-    const uint8_t shw = a.wd.shw[pc];
+    const uint8_t shw = WFM <= 2 ? cshw[jj] : a.wd.shw[pc];
     const bool sgn = (shw & kShwSign) != 0;
     const int sh0 = ap.sh[0] + (shw & 0x7F);
     const int add0 = ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
     const int sh1 = ap.sh[1] + (shw & 0x7F);
     const int add1 = ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0);
-    uint16_t* ycol = ys + a.wd.colrank[pc];
+    uint16_t* ycol = ys + (WFM <= 2 ? crank[jj] : a.wd.colrank[pc]);
 #pragma unroll
     for (int i = 0; i < WFM; ++i) {
       const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
