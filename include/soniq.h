@@ -135,6 +135,31 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
                                 void* stream);
 
 /*
+ * soniq_quantize_act_conv3x3 -- the activations of a stride-1, pad-1 3x3
+ * convolution, quantized straight from its input tensor with no lowered
+ * fp32 matrix.  Passages: as soniq_quantize_act; the fusion of convolution
+ * input handling with quantization to cut memory traffic (Sec. 4, software
+ * optimizations, CPU SIMD item 2).
+ *
+ * The result (packed codes and s_a) is exactly that of soniq_quantize_act
+ * on the lowered matrix A[M = B*H*W, K = 9*C]: row m = (b*H + y)*W + x,
+ * column k = c*9 + kh*3 + kw holding X[b][c][y+kh-1][x+kw-1], or 0 where
+ * that lies outside the image (the order of a 3x3 unfold; the weights are
+ * the [N][C][3][3] filter viewed as [N][9C]).
+ *
+ *   X_dev   device, float32 [B][C][H][W], contiguous.  Finite values only.
+ *   B, C, H, W  >= 1; 9*C must equal the K of the handle's weights and
+ *           B*H*W must not exceed max_M; B*C*H*W < 2^31.
+ * The nine columns of every channel must share one activation width
+ * (UNSUPPORTED otherwise), and 16 rows of the handle's padded channel plan
+ * must fit 64 KB of LDS (K up to about 4000; UNSUPPORTED otherwise).
+ * Enqueued on `stream`, like soniq_quantize_act; X_dev is only read.
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64_t B, int64_t C,
+                                        int64_t H, int64_t W, void* stream);
+
+/*
  * soniq_mp_gemm -- Y = bf16(s_w * sum_g s_a[g] * ACC[g]) for the M rows last
  * quantized into `act` (Alg. 1 Phase II integer MAC forward; C2: the scales
  * are applied once per output, after the exact integer sums).

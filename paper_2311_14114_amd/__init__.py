@@ -29,7 +29,7 @@ SONIQ_MAX_K = 65536
 # Every symbol include/soniq.h declares.
 EXPORTED = [
     "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_act_create",
-    "soniq_quantize_act", "soniq_mp_gemm", "soniq_weights_info",
+    "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
     "soniq_act_unpack_debug", "soniq_weights_destroy", "soniq_act_destroy",
     "soniq_last_error",
@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_act_create.argtypes = [vp, i64, ctypes.POINTER(vp)]
         L.soniq_quantize_act.restype = st
         L.soniq_quantize_act.argtypes = [vp, vp, i64, i64, vp]
+        L.soniq_quantize_act_conv3x3.restype = st
+        L.soniq_quantize_act_conv3x3.argtypes = [vp, vp, i64, i64, i64, i64, vp]
         L.soniq_mp_gemm.restype = st
         L.soniq_mp_gemm.argtypes = [vp, vp, vp, i64, vp, vp]
         L.soniq_weights_info.restype = st
@@ -193,6 +195,19 @@ def soniq_quantize_act(act: Activations, A, stream=None) -> None:
     _check(lib().soniq_quantize_act(act.handle, _dev(A, "float32"), A.shape[0], A.stride(0),
                                     _stream(stream)))
     act.M = A.shape[0]
+
+
+def soniq_quantize_act_conv3x3(act: Activations, X, stream=None) -> None:
+    """Quantize and pack the activations of a stride-1, pad-1 3x3 convolution
+    straight from its input X (device float32 [B, C, H, W], contiguous); the
+    handle's weights are the [N, C, 3, 3] filter viewed as [N, 9C]."""
+    import torch
+    if X.dtype != torch.float32 or X.dim() != 4 or not X.is_contiguous():
+        raise TypeError("X must be a contiguous 4-D float32 device tensor")
+    B, C, H, W = X.shape
+    _check(lib().soniq_quantize_act_conv3x3(act.handle, _dev(X, "float32"), B, C, H, W,
+                                            _stream(stream)))
+    act.M = B * H * W
 
 
 def soniq_mp_gemm(act: Activations, weights: Weights, out=None, acc=None, stream=None):

@@ -556,6 +556,37 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
   return SONIQ_OK;
 }
 
+soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64_t B, int64_t C,
+                                        int64_t H, int64_t W, void* stream) {
+  if (!live_a(act) || !X_dev)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: bad handle or null");
+  const soniq_weights w = act->w;
+  if (B < 1 || C < 1 || H < 1 || W < 1)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: B, C, H, W must be >= 1");
+  if (9 * C != w->K)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: 9*C=%lld != K=%lld",
+                (long long)(9 * C), (long long)w->K);
+  if (B * C * H * W >= ((int64_t)1 << 31))
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: input has 2^31 elements or more");
+  const int64_t M = B * H * W;
+  if (M > act->max_M)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: B*H*W=%lld > max_M=%lld",
+                (long long)M, (long long)act->max_M);
+  for (int64_t c = 0; c < C; ++c)
+    for (int t = 1; t < 9; ++t)
+      if (w->kp.seg[9 * c + t] != w->kp.seg[9 * c])
+        return fail(SONIQ_ERR_UNSUPPORTED,
+                    "soniq_quantize_act_conv3x3: the taps of channel %lld have different widths",
+                    (long long)c);
+  if (!conv_quant_fits(act->ap))
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_quantize_act_conv3x3: K=%lld too large for one block",
+                (long long)w->K);
+  HIP_TRY(launch_conv_quant(X_dev, B, C, H, W, act->ap, w->pos, w->seg, act->partial, act->s_a,
+                            act->packed, reinterpret_cast<hipStream_t>(stream)));
+  act->M = M;
+  return SONIQ_OK;
+}
+
 soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int64_t ldy,
                            int32_t* acc_dev, void* stream) {
   if (!live_a(act) || !live_w(w) || !Y_dev)

@@ -112,6 +112,22 @@ hipError_t launch_wpack(const float* W, int64_t N, int64_t K, int64_t ldw,
                         QParam q_hi, int b_lo, int Kp, uint8_t* packed, ColInfo* colinfo,
                         hipStream_t stream);
 
+// Row stride (bytes) of the conv quantizer's LDS code rows, and whether a
+// 16-row block of them fits the 64 KB a workgroup may hold.
+inline int conv_quant_ldc(const ActPlan& ap) { return ap.Kp + 16; }
+inline bool conv_quant_fits(const ActPlan& ap) { return kBlk * (int64_t)conv_quant_ldc(ap) <= 64 * 1024; }
+// LDS of the window form: 16 code rows, the input rows a 16-pixel block
+// touches (at most (15 + W - 1) / W + 1 image rows, one above, one below),
+// then each channel's group byte and planned run start, then each window
+// row's start index.  The form takes images at most 256 wide.
+__host__ __device__ inline int64_t conv_win_rows(int64_t W) { return (15 + W - 1) / W + 1 + 2; }
+inline size_t conv_win_lds(const ActPlan& ap, int64_t C, int64_t W) {
+  return (size_t)(kBlk * (int64_t)conv_quant_ldc(ap) + ((conv_win_rows(W) * C * W + 15) & ~(int64_t)15) +
+                  ((C + 15) & ~(int64_t)15) + 4 * C + 4 * conv_win_rows(W) * C);
+}
+hipError_t launch_conv_quant(const float* X, int64_t B, int64_t C, int64_t H, int64_t W,
+                             const ActPlan& ap, const int32_t* pos_dev, const uint8_t* seg_dev,
+                             float* partial, float* s_a, uint8_t* packed, hipStream_t stream);
 hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const ActPlan& ap, const int32_t* pos_dev,
                             const uint8_t* seg_dev, float* partial,

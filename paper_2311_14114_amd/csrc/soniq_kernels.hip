@@ -613,13 +613,13 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
 }
 
 // One group's units of a 16-row block whose stored codes sit in LDS (row r
-// at codes + r*Kp + gbase): granule q holds units l = kg*16 + r of 2C bytes
+// at codes + r*ldc + gbase): granule q holds units l = kg*16 + r of 2C bytes
 // (128C contiguous bytes); 16-byte piece w holds units w*U .. w*U+U-1
 // (U = 8/C), i.e. rows of one 16-channel group.  zx (a byte replicated)
 // is XORed into every code byte first: codes held without their zero
 // point get it applied here.
 template <int C, int RB>
-__device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int Kp, int gbase, int ng,
+__device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int ldc, int gbase, int ng,
                                                    int r0, uint8_t* __restrict__ dst,
                                                    uint32_t zx = 0u) {
   constexpr int U = 8 / C;            // units per piece
@@ -634,7 +634,7 @@ __device__ __forceinline__ void write_block_pieces(const uint8_t* codes, int Kp,
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int l = w * U + u, r = (l & 15) - r0;
-      const uint4 d = *reinterpret_cast<const uint4*>(codes + r * Kp + gbase + q * kGran + kg * 16);
+      const uint4 d = *reinterpret_cast<const uint4*>(codes + r * ldc + gbase + q * kGran + kg * 16);
       const uint4 pk = pack_unit(d.x ^ zx, d.y ^ zx, d.z ^ zx, d.w ^ zx, C);
       if constexpr (C == 8) {
         wd[0] = pk.x; wd[1] = pk.y; wd[2] = pk.z; wd[3] = pk.w;
@@ -2733,6 +2733,394 @@ hipError_t launch_wpack(const float* W, int64_t N, int64_t K, int64_t ldw,
   hipLaunchKernelGGL(k_wpack, dim3((unsigned)N), dim3(256), (size_t)Kp, stream, W, K, ldw,
                      w_bits_dev, pos_dev, seg_dev, phys_dev, blk_off, blk_c, q_lo, q_hi, b_lo,
                      Kp, packed, colinfo);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ conv 3x3 --
+// Activations of a stride-1, pad-1 3x3 convolution taken straight from its
+// input X[B][C][H][W] (fp32, contiguous), with no lowered fp32 matrix: row
+// m = (b*H + y)*W + x of the lowered matrix holds, at column
+// k = c*9 + kh*3 + kw, the value X[b][c][y+kh-1][x+kw-1] (zero outside the
+// image), the column order of a 3x3 unfold.  The host requires the nine
+// columns of a channel to share one width, so the group maxima are maxima
+// over X's channels, and (the plan keeps original order within a group)
+// channel c's nine columns sit at the consecutive planned positions
+// pos[9c] .. pos[9c] + 8.
+
+// The conv kernels run a few waves per SIMD (a grid of a few hundred
+// workgroups) and need their loads in flight together: the waves-per-EU
+// bound lets the compiler keep a batch in registers rather than trade it
+// for an occupancy the grid never reaches.
+// Group maxima of X, one partial pair per workgroup.  Wave w of workgroup
+// b takes the kAbsR rows (b*4 + w)*kAbsR .. of the [B*C][H*W] view (then
+// every 4*kAbsR*grid rows on), kAbsJ 64-column strips per row at once: all
+// of a batch's loads are in flight together.
+constexpr int kAbsR = 8, kAbsJ = 4;
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void k_conv_absmax(const float* __restrict__ X, int BC, int C,
+                                                     int HW, const uint8_t* __restrict__ seg,
+                                                     float* __restrict__ partial) {
+  __shared__ float red[8];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  float m0 = 0.0f, m1 = 0.0f;
+  for (int rb = ((int)blockIdx.x * 4 + wid) * kAbsR; rb < BC; rb += (int)gridDim.x * 4 * kAbsR) {
+    // the batch's channels (row = b*C + c), stepped from one division
+    int cr[kAbsR];
+    cr[0] = rb % C;
+#pragma unroll
+    for (int rr = 1; rr < kAbsR; ++rr) cr[rr] = cr[rr - 1] + 1 == C ? 0 : cr[rr - 1] + 1;
+    uint8_t g[kAbsR];
+#pragma unroll
+    for (int rr = 0; rr < kAbsR; ++rr) g[rr] = seg[9 * cr[rr]];
+    for (int j0 = 0; j0 < HW; j0 += 64 * kAbsJ) {
+      float v[kAbsR][kAbsJ];
+#pragma unroll
+      for (int rr = 0; rr < kAbsR; ++rr)
+#pragma unroll
+        for (int jj = 0; jj < kAbsJ; ++jj) {
+          // clamped indices stay in bounds; what they add is masked out
+          const int row = rb + rr < BC ? rb + rr : BC - 1;
+          const int col = j0 + jj * 64 + lane;
+          const float x = X[(int64_t)row * HW + (col < HW ? col : HW - 1)];
+          v[rr][jj] = rb + rr < BC && col < HW ? fabsf(x) : 0.0f;
+        }
+#pragma unroll
+      for (int rr = 0; rr < kAbsR; ++rr) {
+        const float m = fmaxf(fmaxf(v[rr][0], v[rr][1]), fmaxf(v[rr][2], v[rr][3]));
+        if (g[rr] != 0) m1 = fmaxf(m1, m);
+        else m0 = fmaxf(m0, m);
+      }
+    }
+  }
+  const float2 r = block_max2(make_float2(m0, m1), red);
+  if (threadIdx.x == 0) reinterpret_cast<float2*>(partial)[blockIdx.x] = r;
+}
+
+// RB = 8 rows of the lowered matrix per workgroup (half a 16-row block).
+// Thread t takes row r = t % 8 and channels c = t / 8 + 32j: batches of
+// kConvCB channels, each batch's nine taps per channel (and the channels'
+// planned positions and groups) all loaded before any is quantized, the
+// 8 rows of a tap being neighbouring pixels.  FAST (no sign group): codes
+// without the zero point (the shortcut of qcodes4 with a per-tap tie
+// check), applied as a byte XOR when the units are packed; otherwise the
+// generic stored codes.  Dynamic LDS: 8 rows of ldc bytes (ldc = Kp + 16
+// keeps the rows' byte writes in different banks).
+constexpr int kConvRB = 8, kConvCB = 8;
+
+template <bool FAST>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_conv_quant(const float* __restrict__ X, int B, int C, int H,
+                                                    int W, const int32_t* __restrict__ pos,
+                                                    const uint8_t* __restrict__ seg,
+                                                    const float* __restrict__ partial, int nparts,
+                                                    ActPlan ap, int ldc, float* __restrict__ s_a_out,
+                                                    uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  __shared__ float red[8];
+  const int tid = threadIdx.x;
+  const int HW = H * W;
+  const int64_t M = (int64_t)B * HW;
+  const int64_t m0 = (int64_t)blockIdx.x * kConvRB;
+  {
+    // each group's zero point (FAST) or zero: the padding packs to zeros
+    uint32_t* c32 = reinterpret_cast<uint32_t*>(codes);
+    const int kw = ldc / 4, kw0 = ap.kpad[0] / 4;
+    const uint32_t z0 = FAST ? 0x01010101u * (uint32_t)ap.zp[0] : 0u;
+    const uint32_t z1 = FAST ? 0x01010101u * (uint32_t)ap.zp[1] : 0u;
+    for (int r = 0; r < kConvRB; ++r)
+      for (int j = tid; j < kw; j += 256) c32[r * kw + j] = j < kw0 ? z0 : z1;
+  }
+  float s0, s1;
+  scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
+  const int r = tid % kConvRB, cl = tid / kConvRB;
+  constexpr int kLanes = 256 / kConvRB;  // channel lanes
+  const int64_t m = m0 + r;
+  if (m < M) {
+    const int b = (int)(m / HW), yx = (int)(m - (int64_t)b * HW);
+    const int y = yx / W, x = yx - y * W;
+    // tap t reads xc[off[t]]; a tap outside the image reads xc[0] (always
+    // in bounds) and takes zero instead
+    int off[9];
+    unsigned valid = 0;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int dy = t / 3 - 1, dx = t % 3 - 1;
+      const bool in = y + dy >= 0 && y + dy < H && x + dx >= 0 && x + dx < W;
+      off[t] = in ? dy * W + dx : 0;
+      valid |= in ? 1u << t : 0u;
+    }
+    const float* xb = X + (int64_t)b * C * HW + (int64_t)y * W + x;
+    uint8_t* crow = codes + r * ldc;
+    const bool sgn = ap.q[0].lo < 0;
+    const bool fast = fast_ok(s0) && (ap.S == 1 || fast_ok(s1));
+    const float rs0 = fast ? __builtin_amdgcn_rcpf(s0) : 0.0f;
+    const float rs1 = fast && ap.S == 2 ? __builtin_amdgcn_rcpf(s1) : 0.0f;
+    const float hi0 = (float)ap.q[0].hi, hi1 = (float)ap.q[1].hi;
+    const ActQ aq = make_actq(ap, s0, s1);
+    for (int c0 = cl; c0 < C; c0 += kLanes * kConvCB) {
+      float v[kConvCB][9];
+      int pj[kConvCB];
+      uint8_t gj[kConvCB];
+#pragma unroll
+      for (int j = 0; j < kConvCB; ++j) {
+        const int c = c0 + kLanes * j;
+        const int cc = c < C ? c : C - 1;  // in bounds; its codes are not stored
+        const float* xc = xb + (int64_t)cc * HW;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) v[j][t] = xc[off[t]];
+        pj[j] = pos[9 * cc];
+        gj[j] = seg[9 * cc];
+      }
+#pragma unroll
+      for (int j = 0; j < kConvCB; ++j) {
+        if (c0 + kLanes * j >= C) break;
+        uint8_t* dst = crow + pj[j];
+        const bool g1 = gj[j] != 0;
+        if constexpr (FAST) {
+          const float rs = g1 ? rs1 : rs0, sc = g1 ? s1 : s0, hi = g1 ? hi1 : hi0;
+          const float lo = sgn ? -hi : 0.0f;
+#pragma unroll
+          for (int t = 0; t < 9; ++t) {
+            const float xv = (valid >> t) & 1u ? v[j][t] : 0.0f;
+            int code;
+            if (fast) {
+              const float tt = __builtin_fmaf(xv, rs, kShift);
+              code = __float_as_int(sgn ? tt : fmaxf(tt, kShift));
+              const float d = __builtin_fmaf(xv, rs, kShift - tt);
+              if (fabsf(d) >= 0.5f - kTieBand) [[unlikely]]
+                code = qexact(xv, lo, hi, 0.0f, sc);
+            } else {
+              code = qexact(xv, lo, hi, 0.0f, sc);
+            }
+            dst[t] = (uint8_t)code;
+          }
+        } else {
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+            dst[t] = store_code((valid >> t) & 1u ? v[j][t] : 0.0f, g1 ? 1 : 0, aq);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int r0 = (int)(m0 % kBlk);
+  for (int gi = 0; gi < ap.S; ++gi) {
+    const int c = gi ? ap.c[1] : ap.c[0];
+    const int ng = gi ? ap.ng[1] : ap.ng[0];
+    const int gbase = gi ? ap.kpad[0] : 0;
+    const uint32_t zx = FAST ? 0x01010101u * (uint32_t)(gi ? ap.zp[1] : ap.zp[0]) : 0u;
+    uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
+                   (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
+    if (c == 8) write_block_pieces<8, kConvRB>(codes, ldc, gbase, ng, r0, dst, zx);
+    else if (c == 4) write_block_pieces<4, kConvRB>(codes, ldc, gbase, ng, r0, dst, zx);
+    else if (c == 2) write_block_pieces<2, kConvRB>(codes, ldc, gbase, ng, r0, dst, zx);
+    else write_block_pieces<1, kConvRB>(codes, ldc, gbase, ng, r0, dst, zx);
+  }
+}
+
+// The same result from an LDS window: workgroup b takes the 16 rows of
+// block b (pixels m0 .. m0 + 15, global image rows R = b*H + y from
+// m0 / W to (m0 + 15) / W) and first quantizes, once each, every input
+// value of the global image rows R0 - 1 .. R1 + 1 (all channels) into
+// win[row][c][x] (one code byte each), with coalesced loads.  A pixel's
+// nine taps are then byte copies out of the window into its code row
+// (taps outside the image take the code of 0.0).  Dynamic LDS: 16 code
+// rows of ldc bytes, then the window (nr * C * W bytes, nr <= 19).
+template <bool FAST>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_conv_quant_win(const float* __restrict__ X, int B, int C,
+                                                        int H, int W, const int32_t* __restrict__ pos,
+                                                        const uint8_t* __restrict__ seg,
+                                                        const float* __restrict__ partial, int nparts,
+                                                        ActPlan ap, int ldc, float* __restrict__ s_a_out,
+                                                        uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  __shared__ float red[8];
+  const int tid = threadIdx.x;
+  const int HW = H * W;
+  const int64_t M = (int64_t)B * HW;
+  const int64_t m0 = (int64_t)blockIdx.x * kBlk;
+  const int64_t mlast = min(m0 + kBlk, M) - 1;
+  const int R0 = (int)(m0 / W), R1 = (int)(mlast / W);
+  const int wr0 = max(R0 - 1, 0), wr1 = min(R1 + 1, B * H - 1);
+  const int nr = wr1 - wr0 + 1;
+  uint8_t* win = codes + kBlk * ldc;
+  {
+    uint32_t* c32 = reinterpret_cast<uint32_t*>(codes);
+    const int kw = ldc / 4, kw0 = ap.kpad[0] / 4;
+    const uint32_t z0 = FAST ? 0x01010101u * (uint32_t)ap.zp[0] : 0u;
+    const uint32_t z1 = FAST ? 0x01010101u * (uint32_t)ap.zp[1] : 0u;
+    for (int r = 0; r < kBlk; ++r)
+      for (int j = tid; j < kw; j += 256) c32[r * kw + j] = j < kw0 ? z0 : z1;
+  }
+  // Each channel's group and planned run start, in LDS.
+  uint8_t* cg = win + ((conv_win_rows(W) * C * W + 15) & ~(int64_t)15);
+  int32_t* cp = reinterpret_cast<int32_t*>(cg + ((C + 15) & ~15));
+  for (int c = tid; c < C; c += 256) {
+    cg[c] = seg[9 * c];
+    cp[c] = pos[9 * c];
+  }
+  __syncthreads();
+  // Window row rc = c*nr + i is X[b][c][y][:] for the global image row
+  // wr0 + i = b*H + y (a channel's rows are neighbours in memory within an
+  // image): its start index (group of c in bit 31), in LDS.
+  int32_t* rbase = cp + C;
+  for (int rc = tid; rc < nr * C; rc += 256) {
+    const int c = rc / nr, i = rc - c * nr;
+    const int gr = wr0 + i, b = gr / H, y = gr - b * H;
+    rbase[rc] = (((b * C + c) * H + y) * W) | (cg[c] != 0 ? (int)0x80000000u : 0);
+  }
+  __syncthreads();
+  // Window element rc*W + x: thread t keeps column x = t % W and takes rows
+  // t / W + P*j (P = 256 / W rows per pass; the last 256 - P*W threads
+  // idle), kWinU loads at a time.  The first batch is issued before the
+  // scales are reduced, so that both wait together.
+  constexpr int kWinU = 64;
+  const int P = 256 / W, nrc = nr * C;
+  const int wx = tid % W, rq = tid / W;
+  const bool active = rq < P;
+  float xv[kWinU];
+  int meta[kWinU];
+  auto issue = [&](int j0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < kWinU; ++u) {
+      const int rc = rq + P * (j0 + u);
+      const bool ok = active && rc < nrc;
+      const int m = rbase[ok ? rc : 0];  // row 0 keeps the load in bounds
+      meta[u] = m;
+      xv[u] = X[(m & 0x7FFFFFFF) + (ok ? wx : 0)];
+    }
+  };
+  issue(0);
+  float s0, s1;
+  scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
+  const ActQ aq = make_actq(ap, s0, s1);
+  const bool sgn = ap.q[0].lo < 0;
+  const bool fast = fast_ok(s0) && (ap.S == 1 || fast_ok(s1));
+  const float rs0 = fast ? __builtin_amdgcn_rcpf(s0) : 0.0f;
+  const float rs1 = fast && ap.S == 2 ? __builtin_amdgcn_rcpf(s1) : 0.0f;
+  const float hi0 = (float)ap.q[0].hi, hi1 = (float)ap.q[1].hi;
+  auto code_of = [&](float xv, bool g1) __attribute__((always_inline)) -> uint8_t {
+    if constexpr (FAST) {
+      const float rs = g1 ? rs1 : rs0, hi = g1 ? hi1 : hi0;
+      const float lo = sgn ? -hi : 0.0f;
+      if (fast) {
+        const float tt = __builtin_fmaf(xv, rs, kShift);
+        const int code = __float_as_int(sgn ? tt : fmaxf(tt, kShift));
+        const float d = __builtin_fmaf(xv, rs, kShift - tt);
+        if (fabsf(d) < 0.5f - kTieBand) [[likely]]
+          return (uint8_t)code;
+      }
+      return (uint8_t)qexact(xv, lo, hi, 0.0f, g1 ? s1 : s0);
+    } else {
+      return store_code(xv, g1 ? 1 : 0, aq);
+    }
+  };
+  for (int j0 = 0;;) {
+#pragma unroll
+    for (int u = 0; u < kWinU; ++u) {
+      const int rc = rq + P * (j0 + u);
+      if (active && rc < nrc) win[rc * W + wx] = code_of(xv[u], meta[u] < 0);
+    }
+    j0 += kWinU;
+    if (rq + P * j0 >= nrc) break;
+    issue(j0);
+  }
+  __syncthreads();
+  // Taps: thread t takes pixel r = t % 16 and channels t / 16 + 16j.
+  {
+    const int r = tid & 15, cl = tid >> 4;
+    const int64_t m = m0 + r;
+    if (m < M) {
+      const int R = (int)(m / W), x = (int)(m - (int64_t)R * W);
+      const int y = R % H;
+      int off[9];
+      unsigned valid = 0;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int dy = t / 3 - 1, dx = t % 3 - 1;
+        const bool in = y + dy >= 0 && y + dy < H && x + dx >= 0 && x + dx < W;
+        // window row R + dy - wr0 of the channel, column x + dx
+        off[t] = in ? (R + dy - wr0) * W + x + dx : 0;
+        valid |= in ? 1u << t : 0u;
+      }
+      const uint8_t zc0 = code_of(0.0f, false), zc1 = code_of(0.0f, true);
+      uint8_t* crow = codes + r * ldc;
+      // kTapCB channels at a time: their table entries, then all their
+      // window bytes, then all their code bytes
+      constexpr int kTapCB = 4;
+      for (int c0 = cl; c0 < C; c0 += 16 * kTapCB) {
+        int pj[kTapCB];
+        uint8_t gj[kTapCB], bj[kTapCB][9];
+#pragma unroll
+        for (int j = 0; j < kTapCB; ++j) {
+          const int c = min(c0 + 16 * j, C - 1);
+          pj[j] = cp[c];
+          gj[j] = cg[c];
+          const uint8_t* wc = win + c * nr * W;
+#pragma unroll
+          for (int t = 0; t < 9; ++t) bj[j][t] = wc[off[t]];
+        }
+#pragma unroll
+        for (int j = 0; j < kTapCB; ++j) {
+          if (c0 + 16 * j >= C) break;
+          const uint8_t zc = gj[j] != 0 ? zc1 : zc0;
+          uint8_t* dst = crow + pj[j];
+#pragma unroll
+          for (int t = 0; t < 9; ++t) dst[t] = (valid >> t) & 1u ? bj[j][t] : zc;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int gi = 0; gi < ap.S; ++gi) {
+    const int c = gi ? ap.c[1] : ap.c[0];
+    const int ng = gi ? ap.ng[1] : ap.ng[0];
+    const int gbase = gi ? ap.kpad[0] : 0;
+    const uint32_t zx = FAST ? 0x01010101u * (uint32_t)(gi ? ap.zp[1] : ap.zp[0]) : 0u;
+    uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
+                   (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
+    if (c == 8) write_block_pieces<8, kBlk>(codes, ldc, gbase, ng, 0, dst, zx);
+    else if (c == 4) write_block_pieces<4, kBlk>(codes, ldc, gbase, ng, 0, dst, zx);
+    else if (c == 2) write_block_pieces<2, kBlk>(codes, ldc, gbase, ng, 0, dst, zx);
+    else write_block_pieces<1, kBlk>(codes, ldc, gbase, ng, 0, dst, zx);
+  }
+}
+
+hipError_t launch_conv_quant(const float* X, int64_t B, int64_t C, int64_t H, int64_t W,
+                             const ActPlan& ap, const int32_t* pos_dev, const uint8_t* seg_dev,
+                             float* partial, float* s_a, uint8_t* packed, hipStream_t stream) {
+  const int64_t BC = B * C;
+  const int64_t rows_per_block = 4 * kAbsR;
+  const int64_t nparts = (BC + rows_per_block - 1) / rows_per_block < kAbsmaxBlocks
+                             ? (BC + rows_per_block - 1) / rows_per_block
+                             : kAbsmaxBlocks;
+  hipLaunchKernelGGL(k_conv_absmax, dim3((unsigned)nparts), dim3(256), 0, stream, X, (int)BC, (int)C,
+                     (int)(H * W), seg_dev, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
+  const int ldc = conv_quant_ldc(ap);
+  const size_t wlds = conv_win_lds(ap, C, W);
+  if (W <= 256 && wlds <= 64 * 1024) {
+    const int64_t wblocks = (B * H * W + kBlk - 1) / kBlk;
+    if (!sign)
+      hipLaunchKernelGGL(k_conv_quant_win<true>, dim3((unsigned)wblocks), dim3(256), wlds, stream, X,
+                         (int)B, (int)C, (int)H, (int)W, pos_dev, seg_dev, partial, (int)nparts, ap,
+                         ldc, s_a, packed);
+    else
+      hipLaunchKernelGGL(k_conv_quant_win<false>, dim3((unsigned)wblocks), dim3(256), wlds, stream, X,
+                         (int)B, (int)C, (int)H, (int)W, pos_dev, seg_dev, partial, (int)nparts, ap,
+                         ldc, s_a, packed);
+    return hipGetLastError();
+  }
+  const int64_t blocks = (B * H * W + kConvRB - 1) / kConvRB;
+  if (!sign)
+    hipLaunchKernelGGL(k_conv_quant<true>, dim3((unsigned)blocks), dim3(256), (size_t)(kConvRB * ldc),
+                       stream, X, (int)B, (int)C, (int)H, (int)W, pos_dev, seg_dev, partial,
+                       (int)nparts, ap, ldc, s_a, packed);
+  else
+    hipLaunchKernelGGL(k_conv_quant<false>, dim3((unsigned)blocks), dim3(256), (size_t)(kConvRB * ldc),
+                       stream, X, (int)B, (int)C, (int)H, (int)W, pos_dev, seg_dev, partial,
+                       (int)nparts, ap, ldc, s_a, packed);
   return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ def L():
 def declared_symbols():
     text = open(os.path.join(ROOT, "include", "soniq.h")).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(soniq_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(soniq_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol(L):
@@ -72,6 +72,7 @@ def test_null_handles_are_rejected(L):
     h = ctypes.c_void_p()
     assert L.soniq_act_create(None, 4, ctypes.byref(h)) == sq.SONIQ_ERR_INVALID_ARGUMENT
     assert L.soniq_quantize_act(None, ctypes.c_void_p(0x1000), 1, 1, None) == sq.SONIQ_ERR_INVALID_ARGUMENT
+    assert L.soniq_quantize_act_conv3x3(None, ctypes.c_void_p(0x1000), 1, 1, 1, 1, None) == sq.SONIQ_ERR_INVALID_ARGUMENT
     assert L.soniq_mp_gemm(None, None, ctypes.c_void_p(0x1000), 1, None, None) == sq.SONIQ_ERR_INVALID_ARGUMENT
     assert L.soniq_weights_info(None, None) == sq.SONIQ_ERR_INVALID_ARGUMENT
     assert L.soniq_weights_unpack_debug(None, None, None) == sq.SONIQ_ERR_INVALID_ARGUMENT

@@ -395,3 +395,31 @@ def test_uniform_noise_model_variance(ab, wb):
             + K * da ** 2 * dw[None, :] ** 2 / 144)
     ratio = ((y_hat - y) ** 2).mean() / pred.mean()
     assert 0.5 < ratio < 2.0, ratio
+
+
+def test_im2col_lowering_is_the_convolution():
+    """The 3x3 stride-1 pad-1 lowering the convolution path is defined by:
+    the lowered matrix times the flattened filters equals a convolution
+    computed by direct loops over output pixels, channels and taps (fp64),
+    on shapes with borders on every side and a 1x1 image."""
+    import workloads
+    rng = np.random.default_rng(11)
+    for (B, C, H, W, N) in [(2, 3, 4, 5, 4), (1, 2, 1, 1, 3), (1, 1, 3, 1, 2)]:
+        X = rng.standard_normal((B, C, H, W)).astype(np.float32)
+        F = rng.standard_normal((N, C, 3, 3))
+        direct = np.zeros((B, H, W, N))
+        for b in range(B):
+            for y in range(H):
+                for x in range(W):
+                    for n in range(N):
+                        v = 0.0
+                        for c in range(C):
+                            for kh in range(3):
+                                for kw in range(3):
+                                    yy, xx = y + kh - 1, x + kw - 1
+                                    if 0 <= yy < H and 0 <= xx < W:
+                                        v += float(X[b, c, yy, xx]) * F[n, c, kh, kw]
+                        direct[b, y, x, n] = v
+        A = workloads.im2col_3x3(X).astype(np.float64)
+        got = A @ F.reshape(N, C * 9).T
+        np.testing.assert_allclose(got, direct.reshape(B * H * W, N), rtol=1e-12, atol=1e-12)

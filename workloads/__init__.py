@@ -102,7 +102,29 @@ def conv3x3_im2col(batch: int = 32, channels: int = 256, hw: int = 14) -> dict:
     W = np.ascontiguousarray(Wt.reshape(channels, channels * 9))
     a_bits = np.repeat(ch_bits, 9)
     return dict(name="conv3x3_im2col", seed=BASE_SEED + 2, M=A.shape[0], N=channels,
-                K=A.shape[1], A=A, W=W, a_bits=a_bits, w_bits=w_bits, a_signed=False)
+                K=A.shape[1], A=A, W=W, a_bits=a_bits, w_bits=w_bits, a_signed=False, X=X)
+
+
+def conv3x3(batch: int, channels: int, h: int, w: int, n_out: int, *, a_lo: int = 4,
+            a_hi: int = 8, a_frac_lo: float = 0.6, w_lo: int = 1, w_hi: int = 4,
+            w_frac_lo: float = 0.8, a_signed: bool = False, seed: int = 0,
+            name: str = "conv3x3") -> dict:
+    """A 3x3 stride-1 pad-1 convolution X[batch, channels, h, w] -> n_out
+    channels, in the draw order of conv3x3_im2col: X (|N(0,1)| when unsigned,
+    else N(0,1)), filters ~N(0,0.05), per-input-channel widths (shared by the
+    channel's 9 taps), per-output-channel widths.  Carries X and its lowering
+    A = im2col_3x3(X)."""
+    rng = _rng(seed)
+    X = rng.standard_normal((batch, channels, h, w), dtype=np.float32)
+    if not a_signed:
+        X = np.abs(X)
+    Wt = rng.standard_normal((n_out, channels, 3, 3), dtype=np.float32) * np.float32(0.05)
+    ch_bits = _split(rng, channels, a_frac_lo, a_lo, a_hi)
+    w_bits = _split(rng, n_out, w_frac_lo, w_lo, w_hi)
+    A = im2col_3x3(X)
+    return dict(name=name, seed=seed, M=A.shape[0], N=n_out, K=A.shape[1], A=A,
+                W=np.ascontiguousarray(Wt.reshape(n_out, channels * 9)),
+                a_bits=np.repeat(ch_bits, 9), w_bits=w_bits, a_signed=a_signed, X=X)
 
 
 def _xfmr(K: int, N: int, seed_id: int, name: str, M: int = 4096) -> dict:
