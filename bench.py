@@ -68,7 +68,7 @@ def uses_gemv(case) -> bool:
     return case["M"] <= 8
 
 
-def run_gpu(case, steps, warmup, rotate=True, graph=True):
+def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     import torch
     import paper_2311_14114_amd as sq
 
@@ -93,13 +93,19 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True):
     for _ in range(nw - 1):
         ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"]))
     acts = [sq.soniq_act_create(w, M) for w in ws]
-    na = max(1, min(8, math.ceil(ROTATE_A_BYTES / (A0.numel() * 4)))) if rotate else 1
-    As = [A0] + [A0.clone() for _ in range(na - 1)]
+    # the quantizer's input: the lowered matrix A, or (conv_input) the
+    # convolution's NCHW tensor X, whose 3x3 lowering A is
+    src0 = torch.from_numpy(case["X"]).to(dev) if conv_input else A0
+    na = max(1, min(8, math.ceil(ROTATE_A_BYTES / (src0.numel() * 4)))) if rotate else 1
+    As = [src0] + [src0.clone() for _ in range(na - 1)]
     Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
 
     def step(i):
         act = acts[i % nw]
-        sq.soniq_quantize_act(act, As[i % na])
+        if conv_input:
+            sq.soniq_quantize_act_conv3x3(act, As[i % na])
+        else:
+            sq.soniq_quantize_act(act, As[i % na])
         return act, ws[i % nw]
 
     for i in range(warmup):
@@ -156,16 +162,19 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True):
 
     # bf16 comparator: torch's GEMM (hipBLASLt) on the same shapes, the same
     # protocol, operands rotated the same way.
-    Ab = [a.to(torch.bfloat16) for a in As]
+    # (always on the lowered matrix A: a bf16 GEMM has no other input form)
+    del As
+    nab = max(1, min(8, math.ceil(ROTATE_A_BYTES / (A0.numel() * 4)))) if rotate else 1
+    Ab = [A0.to(torch.bfloat16) for _ in range(nab)]
     nwb = max(1, min(nw, math.ceil(ROTATE_W_BYTES / (N * K * 2))))
     Wb = [W.to(torch.bfloat16) for _ in range(nwb)]
     for i in range(warmup):
-        torch.nn.functional.linear(Ab[i % na], Wb[i % nwb])
+        torch.nn.functional.linear(Ab[i % nab], Wb[i % nwb])
     torch.cuda.synchronize()
     s2, t2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s2.record(stream)
     for i in range(steps):
-        torch.nn.functional.linear(Ab[i % na], Wb[i % nwb])
+        torch.nn.functional.linear(Ab[i % nab], Wb[i % nwb])
     t2.record(stream)
     torch.cuda.synchronize()
     bf16_ms = s2.elapsed_time(t2) / steps
@@ -278,6 +287,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--conv-input", action="store_true",
+                    help="conv workloads: quantize from the NCHW input tensor "
+                         "(soniq_quantize_act_conv3x3) instead of the lowered matrix")
     ap.add_argument("--launch", choices=["graph", "eager"], default="graph",
                     help="replay the timed steps as one captured HIP graph (default) or "
                          "launch every call from the host")
@@ -293,9 +305,15 @@ def main():
 
     import workloads
     case = workloads.make(args.workload)
+    if args.conv_input and "X" not in case:
+        print(f"--conv-input needs a convolution workload; {args.workload} has no input tensor",
+              file=sys.stderr)
+        sys.exit(2)
     r = run_gpu(case, args.steps, args.warmup, rotate=not args.no_rotate,
-                graph=args.launch == "graph")
+                graph=args.launch == "graph", conv_input=args.conv_input)
     alg = algorithmic(case, r["info"])
+    if args.conv_input:
+        alg["a_fp32"] = int(case["X"].nbytes)  # the quantizer reads X, not its lowering
     ms = r["total_ms"] / args.steps
     tops = alg["ops"] / (ms * 1e-3) / 1e12
 
@@ -308,7 +326,7 @@ def main():
                    "w_bits": sorted(set(case["w_bits"].tolist())),
                    "a_signed": bool(case["a_signed"]),
                    "activation_copies": r["na"], "weight_copies": r["nw"],
-                   "launch": args.launch},
+                   "launch": args.launch, "input": "nchw" if args.conv_input else "lowered"},
         "roofline": roofline(case, alg, r),
         "breakdown_ms": {"quantize_act": r["q_ms"], "mp_gemm": r["g_ms"],
                          "pack_weights_once": r["pack_ms"]},
@@ -318,6 +336,8 @@ def main():
         "bf16_linear_ms": r["bf16_ms"],
         "speedup_vs_bf16": {"gemm": r["bf16_ms"] / r["g_ms"], "step": r["bf16_ms"] / ms},
     }
+    if args.conv_input and rec["roofline"]["kernel"] == "soniq_quantize_act":
+        rec["roofline"]["traffic"] = None  # the counters on file are the lowered path's
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(rec))
