@@ -2389,24 +2389,36 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
     }
   };
   auto consume0 = [&](int s0, const uint4 (&raw)[NB0]) __attribute__((always_inline)) {
+    if constexpr (NIB) {
+      // every slot's staged activations first (one LDS round trip), then
+      // the products slot by slot as the chunks land
+      uint2 xv[NB0][MT];
 #pragma unroll
-    for (int b = 0; b < NB0; ++b) {
-      if (256 * (s0 + b) >= nch0) break;  // the same for the whole workgroup
-      const int q = min(q0 + QS * (s0 + b), ng0 - 1);
-      if constexpr (NIB) {
+      for (int b = 0; b < NB0; ++b) {
+        const int q = min(q0 + QS * (s0 + b), ng0 - 1);
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm)
+          xv[b][mm] = *reinterpret_cast<const uint2*>(xs + (min(mm, M - 1) * ng0 + q) * 32 + kg * 8);
+      }
+#pragma unroll
+      for (int b = 0; b < NB0; ++b) {
+        if (256 * (s0 + b) >= nch0) break;  // the same for the whole workgroup
 #pragma unroll
         for (int mm = 0; mm < MT; ++mm) {
           if (mm < M) {
-            const uint2 x = *reinterpret_cast<const uint2*>(xs + (mm * ng0 + q) * 32 + kg * 8);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
               const uint2 w = chunk_nibbles<CW>(raw[b], u);
-              acc0[u][mm] = dot16n(w.x, w.y, x, acc0[u][mm]);
+              acc0[u][mm] = dot16n(w.x, w.y, xv[b][mm], acc0[u][mm]);
             }
           }
         }
-      } else {
-        bytes_into(acc0, raw[b], q, tid + 256 * (s0 + b) < nch0);
+      }
+    } else {
+#pragma unroll
+      for (int b = 0; b < NB0; ++b) {
+        if (256 * (s0 + b) >= nch0) break;  // the same for the whole workgroup
+        bytes_into(acc0, raw[b], min(q0 + QS * (s0 + b), ng0 - 1), tid + 256 * (s0 + b) < nch0);
       }
     }
   };
@@ -2428,14 +2440,21 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
     uint4 xl[gemv_xr<MT>()];
     gemv_load_x<MT>(a, xr, 0, xl);
     uint4 raw0[NB0], raw1[NB1];
+    const int total_x = M * ngt * 4;
+    const bool more_x = total_x > 256 * gemv_xr<MT>();
+    if (more_x) {
+      // rows too long for one round: stage them all before the chunk loads
+      // (waits inside the staging loop would otherwise drain the chunks)
+      gemv_store_x<MT, NIB>(a, 0, xl, xs, nbase);
+      for (int u0 = 256 * gemv_xr<MT>(); u0 < total_x; u0 += 256 * gemv_xr<MT>()) {
+        gemv_load_x<MT>(a, xr, u0, xl);
+        gemv_store_x<MT, NIB>(a, u0, xl, xs, nbase);
+      }
+    }
+    // one place for the chunk loads: their registers need no copies at a join
     issue0(0, raw0);
     issue1(0, raw1);
-    gemv_store_x<MT, NIB>(a, 0, xl, xs, nbase);
-    const int total_x = M * ngt * 4;
-    for (int u0 = 256 * gemv_xr<MT>(); u0 < total_x; u0 += 256 * gemv_xr<MT>()) {
-      gemv_load_x<MT>(a, xr, u0, xl);
-      gemv_store_x<MT, NIB>(a, u0, xl, xs, nbase);
-    }
+    if (!more_x) gemv_store_x<MT, NIB>(a, 0, xl, xs, nbase);
     // The staged rows must be visible to every wave, but the weight chunks
     // may still be in flight: wait for LDS writes only, then a plain
     // barrier (a full __syncthreads would also drain every chunk load).
