@@ -114,8 +114,13 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     torch.cuda.synchronize()
 
     def full(i):
-        act, w = step(i)
-        sq.soniq_mp_gemm(act, w, out=Y)
+        # one layer: the conv entry point then the GEMM, or the one-call
+        # quantize + GEMM (a single launch for a batch of one row)
+        if conv_input:
+            act, w = step(i)
+            sq.soniq_mp_gemm(act, w, out=Y)
+        else:
+            sq.soniq_quantize_mp_gemm(acts[i % nw], ws[i % nw], As[i % na], out=Y)
 
     def gemm_only(i):
         sq.soniq_mp_gemm(acts[i % nw], ws[i % nw], out=Y)
@@ -326,7 +331,9 @@ def main():
                    "w_bits": sorted(set(case["w_bits"].tolist())),
                    "a_signed": bool(case["a_signed"]),
                    "activation_copies": r["na"], "weight_copies": r["nw"],
-                   "launch": args.launch, "input": "nchw" if args.conv_input else "lowered"},
+                   "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
+                   "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input
+                             else "soniq_quantize_mp_gemm")},
         "roofline": roofline(case, alg, r),
         "breakdown_ms": {"quantize_act": r["q_ms"], "mp_gemm": r["g_ms"],
                          "pack_weights_once": r["pack_ms"]},

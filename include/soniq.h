@@ -179,6 +179,25 @@ soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64
 soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int64_t ldy,
                            int32_t* acc_dev, void* stream);
 
+/*
+ * soniq_quantize_mp_gemm -- soniq_quantize_act followed by soniq_mp_gemm
+ * in one call, with the same results (Y, the optional accumulators, and
+ * the packed rows and scales left in the handle).  Passages: those of the
+ * two calls.  A batch of one row (the decode case) is quantized inside
+ * the GEMV launch, with no launch of its own, when its plan allows it
+ * (4-bit and 8-bit activation containers, no 1-bit sign group, K a
+ * multiple of 4 up to 4096, A_dev 16-byte aligned); other batches run the
+ * two calls.
+ *
+ *   act, w  a handle made for w, and w.
+ *   A_dev   device, float32 [M, lda], as for soniq_quantize_act.
+ *   Y_dev, ldy, acc_dev  as for soniq_mp_gemm.
+ * Enqueued on `stream`.  Errors: INVALID_ARGUMENT, HIP.
+ */
+soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float* A_dev, int64_t M,
+                                    int64_t lda, uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,
+                                    void* stream);
+
 /* Description of a packed weights handle. */
 typedef struct {
   int64_t N, K;               /* logical sizes */

@@ -29,7 +29,8 @@ SONIQ_MAX_K = 65536
 # Every symbol include/soniq.h declares.
 EXPORTED = [
     "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_act_create",
-    "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_weights_info",
+    "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_quantize_mp_gemm",
+    "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
     "soniq_act_unpack_debug", "soniq_weights_destroy", "soniq_act_destroy",
     "soniq_last_error",
@@ -77,6 +78,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_quantize_act_conv3x3.argtypes = [vp, vp, i64, i64, i64, i64, vp]
         L.soniq_mp_gemm.restype = st
         L.soniq_mp_gemm.argtypes = [vp, vp, vp, i64, vp, vp]
+        L.soniq_quantize_mp_gemm.restype = st
+        L.soniq_quantize_mp_gemm.argtypes = [vp, vp, vp, i64, i64, vp, i64, vp, vp]
         L.soniq_weights_info.restype = st
         L.soniq_weights_info.argtypes = [vp, ctypes.POINTER(WeightsInfo)]
         L.soniq_plan_input_channels.restype = st
@@ -228,6 +231,30 @@ def soniq_mp_gemm(act: Activations, weights: Weights, out=None, acc=None, stream
                                accp, _stream(stream)))
     return out
 
+
+
+def soniq_quantize_mp_gemm(act: Activations, weights: Weights, A, out=None, acc=None, stream=None):
+    """soniq_quantize_act(act, A) then soniq_mp_gemm(act, weights) in one call
+    (a single launch for a batch of one row).  Returns Y."""
+    import torch
+    if A.dtype != torch.float32 or A.dim() != 2 or A.stride(1) != 1:
+        raise TypeError("A must be a 2-D float32 device tensor with unit column stride")
+    if A.shape[1] != act.weights.K:
+        raise ValueError("A has the wrong number of input channels")
+    M, N = A.shape[0], weights.N
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or out.shape[0] < M:
+        raise TypeError("out must be a bf16 [M, >=N] device tensor with unit column stride")
+    accp = None
+    if acc is not None:
+        if acc.dtype != torch.int32 or not acc.is_contiguous() or tuple(acc.shape) != (weights.S, M, N):
+            raise TypeError("acc must be a contiguous int32 [S, M, N] device tensor")
+        accp = _dev(acc, "int32")
+    _check(lib().soniq_quantize_mp_gemm(act.handle, weights.handle, _dev(A, "float32"), M, A.stride(0),
+                                        _dev(out, "bf16"), out.stride(0), accp, _stream(stream)))
+    act.M = M
+    return out
 
 def soniq_weights_info(weights: Weights) -> WeightsInfo:
     info = WeightsInfo()

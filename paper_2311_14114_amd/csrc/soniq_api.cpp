@@ -611,6 +611,31 @@ soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int6
   return SONIQ_OK;
 }
 
+soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float* A_dev, int64_t M,
+                                    int64_t lda, uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,
+                                    void* stream) {
+  if (!live_a(act) || !live_w(w) || !A_dev || !Y_dev)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: bad handle or null");
+  if (act->w != w)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_quantize_mp_gemm: activation handle belongs to other weights");
+  if (M < 1 || M > act->max_M)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: M=%lld outside [1, %lld]",
+                (long long)M, (long long)act->max_M);
+  if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: lda < K");
+  if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: ldy < N");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (M == 1 && gemv_fused_fits(A_dev, w->K, act->ap, w->wp)) {
+    HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos, act->packed, act->s_a, act->ap, w->dev(), w->wp,
+                              w->N, Y_dev, acc_dev, st));
+    act->M = 1;
+    return SONIQ_OK;
+  }
+  const soniq_status q = soniq_quantize_act(act, A_dev, M, lda, stream);
+  if (q != SONIQ_OK) return q;
+  return soniq_mp_gemm(act, w, Y_dev, ldy, acc_dev, stream);
+}
+
 soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* s_w) {
   if (!live_w(w)) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_weights_unpack_debug: bad handle");
   HIP_TRY(hipDeviceSynchronize());

@@ -128,6 +128,13 @@ inline size_t conv_win_lds(const ActPlan& ap, int64_t C, int64_t W) {
 hipError_t launch_conv_quant(const float* X, int64_t B, int64_t C, int64_t H, int64_t W,
                              const ActPlan& ap, const int32_t* pos_dev, const uint8_t* seg_dev,
                              float* partial, float* s_a, uint8_t* packed, hipStream_t stream);
+// Batch of one row quantized inside the GEMV (soniq_quantize_mp_gemm): when
+// it applies, its LDS, and the launch.
+size_t gemv_fused_lds(const ActPlan& ap, const WPlan& wp);
+bool gemv_fused_fits(const float* A, int64_t K, const ActPlan& ap, const WPlan& wp);
+hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, uint8_t* act_packed,
+                             float* s_a, const ActPlan& ap, const WDev& wd, const WPlan& wp,
+                             int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream);
 hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const ActPlan& ap, const int32_t* pos_dev,
                             const uint8_t* seg_dev, float* partial,

@@ -744,6 +744,29 @@ __device__ __forceinline__ void bar_nofence() {
   asm volatile("" ::: "memory");
 }
 
+// block_max2 with fence-free barriers, for workgroups whose global loads
+// must stay in flight across it; red is used once.
+__device__ __forceinline__ float2 block_max2_nofence(float2 v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    v.x = fmaxf(v.x, __shfl_xor(v.x, o, 64));
+    v.y = fmaxf(v.y, __shfl_xor(v.y, o, 64));
+  }
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  if (lane == 0) {
+    red[2 * wid] = v.x;
+    red[2 * wid + 1] = v.y;
+  }
+  __builtin_amdgcn_s_waitcnt(SONIQ_LGKMCNT0_IMM);
+  bar_nofence();
+  float2 r = make_float2(red[0], red[1]);
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) {
+    r.x = fmaxf(r.x, red[2 * i]);
+    r.y = fmaxf(r.y, red[2 * i + 1]);
+  }
+  return r;
+}
+
 // All but the last N loads of this wave have landed, direct-to-LDS ones
 // included; LDS reads stay after it.
 template <int N>
@@ -1364,6 +1387,14 @@ struct GemmArgs {
   int64_t ldy;
   int32_t* acc;
   int xcd_tiles;  // GEMM: give each XCD a contiguous range of tiles
+  // fused batch-1 path (k_gemv_fused): the fp32 row, its planned
+  // positions, where the handle's scales and packed row go, the row's
+  // length in float4 and the staging bytes ahead of the code row in LDS
+  const float* a32;
+  const int32_t* apos;
+  float* s_a_out;
+  uint8_t* act_out;
+  int K4, xs_bytes;
 };
 
 // 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
@@ -2318,9 +2349,12 @@ __device__ __forceinline__ void gemv_store_x(const GemmArgs& a, int u0,
   }
 }
 
-template <int MT, int CW, bool NIB>
+// FJ > 0 (batch of one row only): the fused form, which quantizes the fp32
+// row itself (FJ float4 per thread) instead of staging packed units.
+template <int MT, int CW, bool NIB, int FJ = 0>
 __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int blk,
                                             int (&red)[4][4][kBlk][2][MT]) {
+  static_assert(FJ == 0 || MT == 1, "the fused form takes one row");
   constexpr int U = 8 / CW;
   constexpr int CPG = 8 * CW;    // chunks per granule
   constexpr int QS = 256 / CPG;  // granules per slot of the workgroup
@@ -2344,7 +2378,11 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
   const int ep = blk * kBlk + er;
   const ColInfo eci = a.wd.colinfo[ep];
   const uint8_t eshw = a.wd.shw[ep];
-  const float sa0 = a.s_a[0], sa1 = ap.S == 2 ? a.s_a[1] : 0.0f;
+  float sa0 = 0.0f, sa1 = 0.0f;
+  if constexpr (FJ == 0) {
+    sa0 = a.s_a[0];
+    sa1 = ap.S == 2 ? a.s_a[1] : 0.0f;
+  }
 
   int acc0[U][MT], acc1[U][MT];
 #pragma unroll
@@ -2432,7 +2470,70 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
 
   // The activation loads go first (they hit L2), then the first batch of
   // both groups' chunks; staging waits only for the former.
-  {
+  if constexpr (FJ > 0) {
+    // Fused: the row's float4 and planned positions first, then the
+    // chunks; the group maxima (every workgroup computes the same ones
+    // from the same row), codes and staged units are done while the chunks
+    // are in flight (fence-free barriers), with the arithmetic of the
+    // one-row quantizer, so the codes are those of soniq_quantize_act.
+    const int K4 = a.K4, kp0 = ap.kpad[0];
+    float4 v[FJ];
+    int4 p[FJ];
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) {
+      const int k4 = min(tid + 256 * j, K4 - 1);  // repeats change no max
+      p[j] = reinterpret_cast<const int4*>(a.apos)[k4];
+      v[j] = reinterpret_cast<const float4*>(a.a32)[k4];
+    }
+    uint4 raw0[NB0], raw1[NB1];
+    issue0(0, raw0);
+    issue1(0, raw1);
+    uint8_t* codes = xs + a.xs_bytes;
+    uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+    for (int i = tid; i < ap.Kp / 4; i += 256) codes32[i] = 0;
+    float mx0 = 0.0f, mx1 = 0.0f;
+#pragma unroll
+    for (int j = 0; j < FJ; ++j)
+      max4(v[j], make_uchar4(p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0), mx0, mx1);
+    const float2 mm = block_max2_nofence(make_float2(mx0, mx1),
+                                         reinterpret_cast<float*>(&red[0][0][0][0][0]));
+    const float s0 = group_scale(mm.x, ap.q[0]);
+    const float s1 = ap.S == 2 ? group_scale(mm.y, ap.q[1]) : 0.0f;
+    sa0 = s0;
+    sa1 = s1;
+    if (blk == 0 && tid == 0) {
+      a.s_a_out[0] = s0;
+      a.s_a_out[1] = s1;
+    }
+    const QPair q = qpair(qelem(s0, ap.q[0], ap.zp[0]), qelem(s1, ap.q[1], ap.zp[1]));
+#pragma unroll
+    for (int j = 0; j < FJ; ++j)
+      if (tid + 256 * j < K4) {
+        const bool h[4] = {p[j].x >= kp0, p[j].y >= kp0, p[j].z >= kp0, p[j].w >= kp0};
+        qstore4g(v[j], h, q, codes, p[j]);
+      }
+    __builtin_amdgcn_s_waitcnt(SONIQ_LGKMCNT0_IMM);
+    bar_nofence();
+    // unit u = planned positions 16u .. 16u + 15 (granule u / 4, group u % 4
+    // of 16), staged as gemv_store_x stages the packed unit
+    for (int u = tid; u < 4 * ngt; u += 256) {
+      const uint4 d = *reinterpret_cast<const uint4*>(codes + 16 * u);
+      const bool g0 = u < 4 * ng0;
+      const uint4 pk = pack_unit(d.x, d.y, d.z, d.w, 4);
+      if constexpr (NIB) {
+        if (g0) *reinterpret_cast<uint2*>(xs + 8 * u) = make_uint2(pk.x, pk.y);
+        else *reinterpret_cast<uint4*>(xs + nbase + 16 * (u - 4 * ng0)) = d;
+      } else {
+        *reinterpret_cast<uint4*>(xs + 16 * u) = g0 ? unpack4(pk.x, pk.y) : d;
+      }
+    }
+    // the handle's packed row and scales, as soniq_quantize_act leaves them
+    if (blk == 0) write_act_units(codes, 1, 0, ap, a.act_out);
+    __builtin_amdgcn_s_waitcnt(SONIQ_LGKMCNT0_IMM);
+    bar_nofence();
+    consume0(0, raw0);
+    if (nch1 > 0) consume1(0, raw1);
+  } else {
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)a.act, (short)0,
         (int)(ap.S == 2 ? ap.seg_off[1] + ap.mblk_bytes[1] : ap.seg_off[0] + ap.mblk_bytes[0]),
@@ -2533,6 +2634,23 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
   else if constexpr (MT <= 4) gemv4_block<MT, 1, false>(a, xs, blk, red);
 }
 
+
+// Batch of one row, quantized inside the GEMV: every workgroup computes
+// the row's group maxima and codes (J float4 per thread) while its weight
+// chunks stream in; workgroup 0 also leaves the packed row and the scales
+// in the handle.  Dynamic LDS: the staged row (xs_bytes), then Kp code
+// bytes.
+template <int J>
+__global__ __launch_bounds__(256) void k_gemv_fused(GemmArgs a) {
+  extern __shared__ __align__(16) uint8_t xs[];
+  __shared__ int red[4][4][kBlk][2][1];
+  const int blk = blockIdx.x;
+  const int c = wblk_c(a.wp, blk);
+  if (c == 2) gemv4_block<1, 2, true, J>(a, xs, blk, red);
+  else if (c == 4) gemv4_block<1, 4, true, J>(a, xs, blk, red);
+  else if (c == 8) gemv4_block<1, 8, false, J>(a, xs, blk, red);
+  else gemv4_block<1, 1, false, J>(a, xs, blk, red);
+}
 
 // ----------------------------------------------------------- k_gemv_mfma --
 // Batches of 2..8 rows with activation containers 4 (group 0) and 8
@@ -3270,6 +3388,12 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.ldy = ldy;
   a.acc = acc;
   a.xcd_tiles = 0;
+  a.a32 = nullptr;
+  a.apos = nullptr;
+  a.s_a_out = nullptr;
+  a.act_out = nullptr;
+  a.K4 = 0;
+  a.xs_bytes = 0;
   return a;
 }
 
@@ -3354,6 +3478,35 @@ static size_t gemv_lds(int64_t M, const ActPlan& ap, const WPlan& wp) {
                        (wp.c_hi == 2 || wp.c_hi == 4);
   const int ng1 = ap.S == 2 ? ap.ng[1] : 0;
   return all_nib ? (size_t)M * (32 * ap.ng[0] + 64 * ng1) : (size_t)M * ap.Kp;
+}
+
+bool gemv_fused_fits(const float* A, int64_t K, const ActPlan& ap, const WPlan& wp) {
+  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
+  return gemv_nibble_plan(ap) && !sign && K % 4 == 0 && K / 4 <= 4 * 256 &&
+         reinterpret_cast<uintptr_t>(A) % 16 == 0 && gemv_fits(1, ap, wp) &&
+         gemv_fused_lds(ap, wp) + (size_t)2048 * 8 <= 64 * 1024;
+}
+
+size_t gemv_fused_lds(const ActPlan& ap, const WPlan& wp) {
+  return (gemv_lds(1, ap, wp) + 15) / 16 * 16 + (size_t)ap.Kp;
+}
+
+hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, uint8_t* act_packed,
+                             float* s_a, const ActPlan& ap, const WDev& wd, const WPlan& wp,
+                             int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream) {
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, 1, N, Y, N, acc);
+  a.a32 = A;
+  a.apos = pos_dev;
+  a.s_a_out = s_a;
+  a.act_out = act_packed;
+  a.K4 = (int)(K / 4);
+  a.xs_bytes = (int)((gemv_lds(1, ap, wp) + 15) / 16 * 16);
+  const dim3 grid((unsigned)wp.nblk);
+  const size_t lds = gemv_fused_lds(ap, wp);
+  if (a.K4 <= 256) hipLaunchKernelGGL(k_gemv_fused<1>, grid, dim3(256), lds, stream, a);
+  else if (a.K4 <= 512) hipLaunchKernelGGL(k_gemv_fused<2>, grid, dim3(256), lds, stream, a);
+  else hipLaunchKernelGGL(k_gemv_fused<4>, grid, dim3(256), lds, stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
