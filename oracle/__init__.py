@@ -14,8 +14,11 @@ the paper it follows:
 * ``quantize_act`` -- one scale per activation precision group (Sec. 2.4 C2,
   Alg. 1 channel permutation); unsigned codec of codec item 2, or the signed
   symmetric grid.
+* ``quantize_act_grouped`` -- sub-group scales: blocks of GroupSize_act
+  bits inside each precision group (Sec. 3 design-space parameters; the
+  group-wise activation normalization of the transformer setup, Sec. 5).
 * ``mac`` -- integer multiply-accumulate, one int32 sum per activation group
-  (Alg. 1, Phase II integer forward).
+  or sub-group (Alg. 1, Phase II integer forward).
 * ``epilogue_ref`` -- y = bf16(s_w * sum_g s_a[g] * ACC[g]) in fp64.
 * ``run`` -- the whole path.
 """
@@ -69,6 +72,8 @@ def lib():
         L.orc_segments.argtypes = [vp, i64, vp, vp]
         L.orc_quantize_act.restype = i32
         L.orc_quantize_act.argtypes = [vp, i64, i64, i64, vp, i32, vp, vp, vp, vp]
+        L.orc_quantize_act_grouped.restype = i32
+        L.orc_quantize_act_grouped.argtypes = [vp, i64, i64, i64, vp, i32, i32, i32, vp, vp, vp, vp]
         L.orc_mac.restype = i32
         L.orc_mac.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp]
         L.orc_mac_at.restype = None
@@ -156,11 +161,33 @@ def quantize_act(A, a_bits, a_signed: bool):
     return q, s[:S].copy(), sb[:S].copy(), so
 
 
+def quantize_act_grouped(A, a_bits, a_signed: bool, group_bits: int):
+    """Sub-group scales: each precision group cut into blocks of
+    group_bits / container channels in the Alg. 1 order, one scale per
+    block.  Returns codes, scales[S], block widths[S], block of each
+    channel[K] (group_bits = 0: one block per precision group)."""
+    A = _c(A, np.float32)
+    M, K = A.shape
+    ab = _c(a_bits, np.uint8)
+    assert ab.shape == (K,)
+    cap = K + 2
+    q = np.empty((M, K), np.int32)
+    s = np.zeros(cap, np.float32)
+    sb = np.zeros(cap, np.uint8)
+    so = np.empty(K, np.int32)
+    S = lib().orc_quantize_act_grouped(_p(A), M, K, K, _p(ab), 1 if a_signed else 0,
+                                       int(group_bits), cap, _p(q), _p(s), _p(sb), _p(so))
+    if S < 0:
+        raise ValueError("bad widths or group size")
+    return q, s[:S].copy(), sb[:S].copy(), so
+
+
 def mac(q_a, q_w, seg_of, S: int):
-    """ACC[g][m][n] as int32; raises if a sum leaves int32."""
+    """ACC[g][m][n] as int32 (g = the scale group of each channel, seg_of);
+    raises if a sum leaves int32."""
     q_a = _c(q_a, np.int32)
     q_w = _c(q_w, np.int32)
-    so = _c(seg_of, np.uint8)
+    so = _c(seg_of, np.int32)
     M, K = q_a.shape
     N = q_w.shape[0]
     acc = np.empty((S, M, N), np.int32)
@@ -174,7 +201,7 @@ def mac_at(q_a, q_w, seg_of, S: int, ms, ns):
     """ACC[g] at sampled (m, n) pairs -> int64 [count, S]."""
     q_a = _c(q_a, np.int32)
     q_w = _c(q_w, np.int32)
-    so = _c(seg_of, np.uint8)
+    so = _c(seg_of, np.int32)
     ms = _c(ms, np.int64)
     ns = _c(ns, np.int64)
     out = np.empty((ms.shape[0], S), np.int64)

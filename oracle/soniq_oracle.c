@@ -160,41 +160,126 @@ int orc_quantize_act(const float* A, int64_t M, int64_t K, int64_t lda,
   return S;
 }
 
+/* ------------------------------------------------------------- O4/O5 ---
+ * Sub-group scales (GroupSize_act of the design-space parameters, Sec. 3,
+ * and the group-wise activation normalization of the transformer setup,
+ * Sec. 5).  Channels are put in the Alg. 1 order (narrow width first,
+ * original index order inside a width); each precision group is then cut
+ * into consecutive blocks of group_bits / c channels, c the container of
+ * its width (the next power of two >= b), so that one block fills
+ * group_bits of storage.  Each block has its own scale, from the max-abs
+ * over all rows and its channels.  Blocks are numbered in that order,
+ * group 0's first.  group_bits = 0 keeps one block per precision group.
+ * Outputs: codes q_a[M,K], scales s_a[S] (S = number of blocks, at most
+ * cap), the width of each block sub_bits[S], and the block of each channel
+ * sub_of[K].  Returns S, or -1 on bad widths, a group_bits that is not a
+ * positive multiple of every block's container, or more than cap blocks.
+ */
+static int orc_container_bits(int b) {
+  int c = 1;
+  while (c < b) c <<= 1;
+  return c;
+}
+
+int orc_quantize_act_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
+                             const uint8_t* a_bits, int a_signed, int group_bits,
+                             int cap, int32_t* q_a, float* s_a, uint8_t* sub_bits,
+                             int32_t* sub_of) {
+  uint8_t seg_bits[2];
+  uint8_t* seg_of = (uint8_t*)malloc((size_t)(K > 0 ? K : 1));
+  int S = orc_segments(a_bits, K, seg_bits, seg_of);
+  if (S < 0 || group_bits < 0) {
+    free(seg_of);
+    return -1;
+  }
+  int64_t len[2] = {0, 0}, per[2] = {0, 0}, nsub[2] = {0, 0};
+  for (int64_t k = 0; k < K; ++k) len[seg_of[k]]++;
+  for (int g = 0; g < S; ++g) {
+    int c = orc_container_bits(seg_bits[g]);
+    if (group_bits == 0) {
+      per[g] = len[g];
+    } else {
+      if (group_bits % c != 0) {
+        free(seg_of);
+        return -1;
+      }
+      per[g] = group_bits / c;
+    }
+    nsub[g] = (len[g] + per[g] - 1) / per[g];
+  }
+  int total = (int)(nsub[0] + (S == 2 ? nsub[1] : 0));
+  if (total > cap) {
+    free(seg_of);
+    return -1;
+  }
+  /* rank of each channel inside its precision group, in index order */
+  int64_t seen[2] = {0, 0};
+  for (int64_t k = 0; k < K; ++k) {
+    int g = seg_of[k];
+    int64_t r = seen[g]++;
+    sub_of[k] = (int32_t)((g == 1 ? nsub[0] : 0) + r / per[g]);
+  }
+  for (int j = 0; j < total; ++j) sub_bits[j] = seg_bits[j < nsub[0] ? 0 : 1];
+  int mode = a_signed ? ORC_SIGNED : ORC_UNSIGNED;
+  float* mx = (float*)calloc((size_t)total, sizeof(float));
+  for (int64_t m = 0; m < M; ++m)
+    for (int64_t k = 0; k < K; ++k) {
+      float a = fabsf(A[m * lda + k]);
+      if (a > mx[sub_of[k]]) mx[sub_of[k]] = a;
+    }
+  for (int j = 0; j < total; ++j) s_a[j] = orc_scale(mx[j], sub_bits[j], mode);
+  int64_t m;
+#pragma omp parallel for schedule(static)
+  for (m = 0; m < M; ++m)
+    for (int64_t k = 0; k < K; ++k) {
+      int j = sub_of[k];
+      q_a[m * K + k] = orc_code(A[m * lda + k], s_a[j], sub_bits[j], mode);
+    }
+  free(mx);
+  free(seg_of);
+  return total;
+}
+
 /* ------------------------------------------------------------------ O6 ---
  * Integer MAC: ACC[g][m][n] = sum over channels k of group g of
- * q_a[m,k] * q_w[n,k], summed in int64.  Returns 0, or -1 if a sum does
- * not fit int32 (the sums are then still stored, truncated).
+ * q_a[m,k] * q_w[n,k], summed in int64.  grp_of[k] is the scale group of
+ * channel k (0 .. S-1): a precision group, or a sub-group of one.  Returns
+ * 0, or -1 if a sum does not fit int32 (the sums are then still stored,
+ * truncated).
  */
-int orc_mac(const int32_t* q_a, const int32_t* q_w, const uint8_t* seg_of,
+int orc_mac(const int32_t* q_a, const int32_t* q_w, const int32_t* grp_of,
             int64_t M, int64_t N, int64_t K, int S, int32_t* acc) {
   int overflow = 0;
   int64_t m;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : overflow)
-  for (m = 0; m < M; ++m)
+  for (m = 0; m < M; ++m) {
+    int64_t* sum = (int64_t*)malloc(sizeof(int64_t) * (size_t)S);
     for (int64_t n = 0; n < N; ++n) {
-      int64_t sum[2] = {0, 0};
+      for (int g = 0; g < S; ++g) sum[g] = 0;
       for (int64_t k = 0; k < K; ++k)
-        sum[seg_of[k]] += (int64_t)q_a[m * K + k] * (int64_t)q_w[n * K + k];
+        sum[grp_of[k]] += (int64_t)q_a[m * K + k] * (int64_t)q_w[n * K + k];
       for (int g = 0; g < S; ++g) {
         if (sum[g] > INT32_MAX || sum[g] < INT32_MIN) overflow = 1;
         acc[((int64_t)g * M + m) * N + n] = (int32_t)sum[g];
       }
     }
+    free(sum);
+  }
   return overflow ? -1 : 0;
 }
 
 /* One output's accumulators, for sampled checks at full size. */
-void orc_mac_at(const int32_t* q_a, const int32_t* q_w, const uint8_t* seg_of,
+void orc_mac_at(const int32_t* q_a, const int32_t* q_w, const int32_t* grp_of,
                 int64_t K, int S, int64_t count, const int64_t* ms,
                 const int64_t* ns, int64_t* out /* [count][S] */) {
   int64_t i;
 #pragma omp parallel for schedule(static)
   for (i = 0; i < count; ++i) {
-    int64_t sum[2] = {0, 0};
+    int64_t* sum = out + i * S;
+    for (int g = 0; g < S; ++g) sum[g] = 0;
     const int32_t* a = q_a + ms[i] * K;
     const int32_t* w = q_w + ns[i] * K;
-    for (int64_t k = 0; k < K; ++k) sum[seg_of[k]] += (int64_t)a[k] * (int64_t)w[k];
-    for (int g = 0; g < S; ++g) out[i * S + g] = sum[g];
+    for (int64_t k = 0; k < K; ++k) sum[grp_of[k]] += (int64_t)a[k] * (int64_t)w[k];
   }
 }
 
@@ -246,7 +331,8 @@ void orc_epilogue_ref(const int32_t* acc, const float* s_a, const float* s_w,
 }
 
 /* Replay output: the same value in a fixed fp32 order -- t = f(ACC0)*s_a0;
- * t = t + f(ACC1)*s_a1 (separate multiply and add); t = t*s_w; bf16 RNE. */
+ * then for each later group g in order t = t + f(ACCg)*s_ag (separate
+ * multiply and add); t = t*s_w; bf16 RNE. */
 void orc_epilogue_replay(const int32_t* acc, const float* s_a, const float* s_w,
                          int64_t M, int64_t N, int S, uint16_t* y) {
   int64_t m;
@@ -254,8 +340,8 @@ void orc_epilogue_replay(const int32_t* acc, const float* s_a, const float* s_w,
   for (m = 0; m < M; ++m)
     for (int64_t n = 0; n < N; ++n) {
       float t = (float)acc[m * N + n] * s_a[0];
-      if (S == 2) {
-        float u = (float)acc[((int64_t)M + m) * N + n] * s_a[1];
+      for (int g = 1; g < S; ++g) {
+        float u = (float)acc[((int64_t)g * M + m) * N + n] * s_a[g];
         t = t + u;
       }
       t = t * s_w[n];

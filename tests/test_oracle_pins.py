@@ -423,3 +423,129 @@ def test_im2col_lowering_is_the_convolution():
         A = workloads.im2col_3x3(X).astype(np.float64)
         got = A @ F.reshape(N, C * 9).T
         np.testing.assert_allclose(got, direct.reshape(B * H * W, N), rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------- sub-group activation scales
+def test_grouped_without_blocks_is_the_precision_group_case():
+    """GroupSize_act large enough for a whole precision group (or 0) gives
+    one block per group: exactly the pinned per-group quantizer."""
+    rng = np.random.default_rng(21)
+    M, K = 9, 700
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    ab = np.where(rng.random(K) < 0.6, 4, 8).astype(np.uint8)
+    q0, s0, sb0, so0 = oracle.quantize_act(A, ab, True)
+    for gb in (0, 8 * 1024):
+        q, s, sb, so = oracle.quantize_act_grouped(A, ab, True, gb)
+        np.testing.assert_array_equal(q, q0)
+        np.testing.assert_array_equal(s, s0)
+        np.testing.assert_array_equal(sb, sb0)
+        np.testing.assert_array_equal(so, so0.astype(np.int32))
+
+
+@pytest.mark.parametrize("signed", [True, False])
+def test_grouped_blocks_are_independent_quantizations(signed):
+    """With the narrow channels first in index order, the Alg. 1 order is
+    the identity and every block is a contiguous column range: quantizing
+    each range alone with the (pinned) per-group quantizer must give the
+    block's codes and scale.  512-bit blocks: 128 channels at 4 bits, 64 at
+    8 bits (widths 3 and 5 share containers 4 and 8)."""
+    rng = np.random.default_rng(22 + signed)
+    M = 7
+    for lo, hi in ((4, 8), (3, 5)):
+        n_lo, n_hi = 300, 150
+        K = n_lo + n_hi
+        A = (rng.standard_normal((M, K)) * rng.uniform(0.1, 10, K)).astype(np.float32)
+        ab = np.array([lo] * n_lo + [hi] * n_hi, np.uint8)
+        q, s, sb, so = oracle.quantize_act_grouped(A, ab, signed, 512)
+        c_lo, c_hi = (4, 8)
+        edges = []
+        for start, n, c in ((0, n_lo, c_lo), (n_lo, n_hi, c_hi)):
+            per = 512 // c
+            edges += [(b, min(b + per, start + n)) for b in range(start, start + n, per)]
+        assert len(s) == len(edges)
+        for j, (b, e) in enumerate(edges):
+            qj, sj, _, _ = oracle.quantize_act(A[:, b:e], ab[b:e], signed)
+            np.testing.assert_array_equal(q[:, b:e], qj)
+            assert s[j] == sj[0]
+            assert (so[b:e] == j).all()
+            assert sb[j] == ab[b]
+
+
+def test_grouped_block_scale_is_equivariant():
+    """Doubling every input of one block doubles that block's scale exactly
+    and leaves all codes and every other scale unchanged; a channel put in
+    the wrong block breaks this."""
+    rng = np.random.default_rng(24)
+    M, K = 6, 520
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    ab = np.where(rng.random(K) < 0.7, 4, 8).astype(np.uint8)
+    q, s, sb, so = oracle.quantize_act_grouped(A, ab, True, 512)
+    for j in range(len(s)):
+        B = A.copy()
+        B[:, so == j] *= 2
+        q2, s2, _, so2 = oracle.quantize_act_grouped(B, ab, True, 512)
+        np.testing.assert_array_equal(q2, q)
+        np.testing.assert_array_equal(so2, so)
+        want = s.copy()
+        want[j] *= 2
+        np.testing.assert_array_equal(s2, want)
+
+
+def test_grouped_block_maximum_maps_to_the_top_code():
+    rng = np.random.default_rng(25)
+    M, K = 5, 400
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    ab = np.where(rng.random(K) < 0.5, 4, 8).astype(np.uint8)
+    q, s, sb, so = oracle.quantize_act_grouped(A, ab, True, 512)
+    for j in range(len(s)):
+        cols = so == j
+        blk = A[:, cols]
+        i = np.unravel_index(np.argmax(np.abs(blk)), blk.shape)
+        top = 2 ** (int(sb[j]) - 1) - 1
+        assert abs(q[:, cols][i]) == top
+        assert (np.abs(q[:, cols]) <= top).all()
+
+
+def test_grouped_mac_is_the_blockwise_product():
+    """ACC of block j is the integer product over the block's channels
+    alone (numpy int64 matmul), and the blocks of a precision group add up
+    to that group's accumulator."""
+    rng = np.random.default_rng(26)
+    M, N, K = 8, 12, 600
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    ab = np.where(rng.random(K) < 0.6, 4, 8).astype(np.uint8)
+    wb = np.where(rng.random(N) < 0.5, 2, 8).astype(np.uint8)
+    q_w, s_w = oracle.quantize_weights(W, wb)
+    q, s, sb, so = oracle.quantize_act_grouped(A, ab, True, 512)
+    acc = oracle.mac(q, q_w, so, len(s))
+    for j in range(len(s)):
+        cols = so == j
+        want = q[:, cols].astype(np.int64) @ q_w[:, cols].astype(np.int64).T
+        np.testing.assert_array_equal(acc[j], want)
+    # the same codes summed per precision group instead of per block
+    _, _, seg_bits, seg_of = oracle.quantize_act(A, ab, True)
+    acc_seg = oracle.mac(q, q_w, seg_of, len(seg_bits))
+    for g in range(len(seg_bits)):
+        np.testing.assert_array_equal(acc[sb == seg_bits[g]].sum(0), acc_seg[g])
+
+
+def test_grouped_epilogue_replay_matches_ref_within_rounding():
+    """Many groups: the fixed-order fp32 replay stays within the bf16
+    rounding of the fp64 reference (each product and sum adds at most
+    2^-24 relative to the running magnitude)."""
+    rng = np.random.default_rng(27)
+    S = 25
+    acc = rng.integers(-2 ** 18, 2 ** 18, (S, 20, 30)).astype(np.int32)
+    s_a = rng.uniform(1e-3, 1e-1, S).astype(np.float32)
+    s_w = rng.uniform(1e-3, 1.0, 30).astype(np.float32)
+    yr = oracle.bf16_to_f32(oracle.epilogue_ref(acc, s_a, s_w)).astype(np.float64)
+    yp = oracle.bf16_to_f32(oracle.epilogue_replay(acc, s_a, s_w)).astype(np.float64)
+    terms = np.abs(s_a[:, None, None].astype(np.float64) * acc).sum(0) * s_w[None, :]
+    assert (np.abs(yp - yr) <= np.abs(yr) * 2.0 ** -7 + terms * 2.0 ** -15).all()
+    # two groups: the general replay is the two-group order of O7
+    y2 = oracle.epilogue_replay(acc[:2], s_a[:2], s_w)
+    t = (acc[0].astype(np.float32) * s_a[0]) + (acc[1].astype(np.float32) * s_a[1])
+    t = t * s_w[None, :]
+    np.testing.assert_array_equal(oracle.bf16_to_f32(y2), oracle.bf16_to_f32(
+        np.array([[oracle.bf16_from_f32(v) for v in row] for row in t], np.uint16)))
