@@ -65,7 +65,8 @@ def algorithmic(case, info):
 
 
 def uses_gemv(case) -> bool:
-    return case["M"] <= 8
+    # sub-group scales run the MFMA tiles at every batch size
+    return case["M"] <= 8 and not case.get("act_group_bits", 0)
 
 
 def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
@@ -82,7 +83,9 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
-    ws = [sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"])]
+    gbits = case.get("act_group_bits", 0)
+    ws = [sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
+                                act_group_bits=gbits)]
     e1.record(stream)
     torch.cuda.synchronize()
     pack_ms = e0.elapsed_time(e1)
@@ -91,7 +94,8 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     if rotate:
         nw = max(1, min(MAX_W_COPIES, math.ceil(ROTATE_W_BYTES / int(info.packed_w_bytes))))
     for _ in range(nw - 1):
-        ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"]))
+        ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
+                                        act_group_bits=gbits))
     acts = [sq.soniq_act_create(w, M) for w in ws]
     # the quantizer's input: the lowered matrix A, or (conv_input) the
     # convolution's NCHW tensor X, whose 3x3 lowering A is
@@ -224,7 +228,8 @@ def roofline(case, alg, r):
                     kernel=kernel, algorithmic_bytes=byt, launch_us=t * 1e6)
     t = r["g_ms"] * 1e-3
     byt = alg["a_packed"] + alg["w_packed"] + alg["w_side"] + alg["y"]
-    kernel = "k_gemv" if uses_gemv(case) else "k_gemm"
+    kernel = ("k_gemv" if uses_gemv(case) else
+              "k_gemm_g" if case.get("act_group_bits", 0) else "k_gemm")
     traffic = measured_traffic(kernel, case["name"])
     # the bound is whichever resource needs longer at its peak
     if uses_gemv(case) or byt / (HBM_PEAK_GBS * 1e9) >= alg["ops"] / (INT8_PEAK_TOPS * 1e12):
@@ -251,7 +256,11 @@ def cpu_baseline(case, budget_s=12.0):
     def one(rows):
         A = np.ascontiguousarray(case["A"][:rows])
         t0 = time.perf_counter()
-        q_a, s_a, seg_bits, seg_of = oracle.quantize_act(A, case["a_bits"], case["a_signed"])
+        if case.get("act_group_bits", 0):
+            q_a, s_a, seg_bits, seg_of = oracle.quantize_act_grouped(
+                A, case["a_bits"], case["a_signed"], case["act_group_bits"])
+        else:
+            q_a, s_a, seg_bits, seg_of = oracle.quantize_act(A, case["a_bits"], case["a_signed"])
         acc = oracle.mac(q_a, q_w, seg_of, len(seg_bits))
         oracle.epilogue_replay(acc, s_a, s_w)
         return time.perf_counter() - t0
@@ -330,6 +339,7 @@ def main():
                    "a_bits": sorted(set(case["a_bits"].tolist())),
                    "w_bits": sorted(set(case["w_bits"].tolist())),
                    "a_signed": bool(case["a_signed"]),
+                   "act_group_bits": int(case.get("act_group_bits", 0)),
                    "activation_copies": r["na"], "weight_copies": r["nw"],
                    "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
                    "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input

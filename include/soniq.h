@@ -110,6 +110,38 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
                                    soniq_weights* out);
 
 /*
+ * soniq_pack_weights_grouped -- as soniq_pack_weights_ex, with sub-group
+ * activation scales: GroupSize_act of the design-space parameters (Sec. 3;
+ * Sec. 5 normalizes transformer activations in 512-bit groups).
+ *
+ *   act_group_bits  0: one activation scale per precision group (the
+ *       other pack calls).  Otherwise a positive multiple of 512: each
+ *       precision group, in the planned order (narrow width first, original
+ *       channel order inside a width), is cut into consecutive blocks of
+ *       act_group_bits / c channels, c the group's container (the next
+ *       power of two >= its width), so a block fills act_group_bits of
+ *       storage: 128 channels at 4 bits, 64 at 8 bits for 512.  Each block
+ *       has its own scale, max-abs over the batch and the block's channels
+ *       divided by the group's largest code; the GEMM keeps one exact int32
+ *       sum per block and scales it once:
+ *         Y = bf16(s_w * sum_j s_a[j] * ACC[j]),
+ *       summed in fp32 in block order (multiply, then add).  Blocks are
+ *       numbered group 0 first; soniq_weights_info reports their count.
+ * Grouped handles need a zero point of 0 in both activation groups (signed
+ * activations, or unsigned widths below their container: 3, 5, 6, 7 bits)
+ * and no 1-bit activation group, and at most 256 blocks; UNSUPPORTED
+ * otherwise.  Their activations are quantized from the lowered matrix only
+ * (soniq_quantize_act_conv3x3 returns UNSUPPORTED) and every batch size
+ * runs the MFMA GEMM.
+ * Errors: those of soniq_pack_weights_ex; INVALID_ARGUMENT for an
+ * act_group_bits that is negative or not a multiple of 512.
+ */
+soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                        const uint8_t* w_bits, const uint8_t* a_bits,
+                                        int a_signed, int wq_mode, int act_group_bits,
+                                        void* stream, soniq_weights* out);
+
+/*
  * soniq_act_create -- allocate a packed activation buffer for up to max_M
  * rows, laid out for the input-channel plan of `w` (activation groups,
  * permutation and padding are fixed at weight-packing time, Alg. 1).
@@ -168,9 +200,10 @@ soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64
  *   Y_dev    device, bf16 bit patterns (uint16) [M, ldy], columns in the
  *            original output-channel order; fully overwritten.
  *   ldy      row stride in elements, ldy >= N.
- *   acc_dev  optional device int32 [S][M][N] (S = number of activation
- *            groups, soniq_weights_info): receives the exact accumulators
- *            ACC[g][m][n] in original order.  NULL skips the dump.
+ *   acc_dev  optional device int32 [S][M][N] (S = act_scales of
+ *            soniq_weights_info: activation groups, or blocks for grouped
+ *            weights): receives the exact accumulators ACC[g][m][n] in
+ *            original order.  NULL skips the dump.
  * Enqueued on `stream`.  M <= 8 uses a bandwidth-bound kernel without matrix
  * cores; larger M uses int8 MFMA tiles.
  * Errors: INVALID_ARGUMENT (null, mismatched handles, nothing quantized),
@@ -210,6 +243,8 @@ typedef struct {
   int64_t w_count[2];         /* output channels per weight width */
   int64_t packed_w_bytes;     /* bytes of the packed weight buffer */
   int64_t packed_w_bytes_algorithmic; /* sum over rows of container*K/8 */
+  int32_t act_group_bits;     /* GroupSize_act in bits, 0 = one scale per group */
+  int32_t act_scales;         /* activation scales: blocks, or S when ungrouped */
 } soniq_weights_info_t;
 
 /* Fill *out.  Errors: INVALID_ARGUMENT. */
@@ -232,7 +267,7 @@ soniq_status soniq_plan_input_channels(const uint8_t* a_bits, int64_t K, int64_t
  * int32 in the original channel order; scales as float32.
  *   soniq_weights_unpack_debug: codes [N, K], s_w [N].
  *   soniq_act_unpack_debug:     codes [M, K] of the last soniq_quantize_act,
- *                               s_a [S].
+ *                               s_a [act_scales of soniq_weights_info].
  * Either output pointer may be NULL.  Errors: INVALID_ARGUMENT, HIP.
  */
 soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* s_w);

@@ -28,7 +28,8 @@ SONIQ_MAX_K = 65536
 
 # Every symbol include/soniq.h declares.
 EXPORTED = [
-    "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_act_create",
+    "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_pack_weights_grouped",
+    "soniq_act_create",
     "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_quantize_mp_gemm",
     "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
@@ -51,6 +52,7 @@ class WeightsInfo(ctypes.Structure):
         ("a_count", ctypes.c_int64 * 2), ("a_count_padded", ctypes.c_int64 * 2),
         ("w_count", ctypes.c_int64 * 2), ("packed_w_bytes", ctypes.c_int64),
         ("packed_w_bytes_algorithmic", ctypes.c_int64),
+        ("act_group_bits", ctypes.c_int32), ("act_scales", ctypes.c_int32),
     ]
 
 
@@ -70,6 +72,9 @@ def lib() -> ctypes.CDLL:
         L.soniq_pack_weights.argtypes = [vp, i64, i64, i64, vp, vp, i32, vp, ctypes.POINTER(vp)]
         L.soniq_pack_weights_ex.restype = st
         L.soniq_pack_weights_ex.argtypes = [vp, i64, i64, i64, vp, vp, i32, i32, vp, ctypes.POINTER(vp)]
+        L.soniq_pack_weights_grouped.restype = st
+        L.soniq_pack_weights_grouped.argtypes = [vp, i64, i64, i64, vp, vp, i32, i32, i32, vp,
+                                                 ctypes.POINTER(vp)]
         L.soniq_act_create.restype = st
         L.soniq_act_create.argtypes = [vp, i64, ctypes.POINTER(vp)]
         L.soniq_quantize_act.restype = st
@@ -128,7 +133,8 @@ class Weights:
         self.handle = handle
         self.N, self.K = N, K
         self.info = soniq_weights_info(self)
-        self.S = self.info.S
+        # accumulators per output: precision groups, or sub-group blocks
+        self.S = self.info.act_scales
 
     def close(self):
         if self.handle:
@@ -164,8 +170,10 @@ class Activations:
 
 
 def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_WQ_SYMMETRIC,
-                       stream=None) -> Weights:
-    """Quantize, re-order and bit-pack W (device float32 [N, K], row-major)."""
+                       stream=None, act_group_bits: int = 0) -> Weights:
+    """Quantize, re-order and bit-pack W (device float32 [N, K], row-major).
+    act_group_bits > 0 gives the activations sub-group scales (blocks of
+    that many bits of storage inside each precision group)."""
     import torch
     if W.dtype != torch.float32 or W.dim() != 2 or W.stride(1) != 1:
         raise TypeError("W must be a 2-D float32 device tensor with unit column stride")
@@ -174,11 +182,12 @@ def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_W
     if wb.shape != (N,) or ab.shape != (K,):
         raise ValueError("w_bits must have N entries and a_bits K entries")
     h = ctypes.c_void_p()
-    _check(lib().soniq_pack_weights_ex(_dev(W, "float32"), N, K, W.stride(0),
-                                       wb.ctypes.data_as(ctypes.c_void_p),
-                                       ab.ctypes.data_as(ctypes.c_void_p),
-                                       1 if a_signed else 0, int(wq_mode), _stream(stream),
-                                       ctypes.byref(h)))
+    _check(lib().soniq_pack_weights_grouped(_dev(W, "float32"), N, K, W.stride(0),
+                                            wb.ctypes.data_as(ctypes.c_void_p),
+                                            ab.ctypes.data_as(ctypes.c_void_p),
+                                            1 if a_signed else 0, int(wq_mode),
+                                            int(act_group_bits), _stream(stream),
+                                            ctypes.byref(h)))
     return Weights(h, N, K)
 
 
@@ -288,9 +297,10 @@ def soniq_weights_unpack_debug(weights: Weights):
 
 
 def soniq_act_unpack_debug(act: Activations):
-    """Codes int32 [M, K] (original order) and group scales float32 [S]."""
+    """Codes int32 [M, K] (original order) and scales float32 [S] (one per
+    precision group, or per sub-group block)."""
     codes = np.empty((act.M, act.weights.K), np.int32)
-    s_a = np.zeros(2, np.float32)
+    s_a = np.zeros(max(2, act.weights.S), np.float32)
     _check(lib().soniq_act_unpack_debug(act.handle, codes.ctypes.data_as(ctypes.c_void_p),
                                         s_a.ctypes.data_as(ctypes.c_void_p)))
     return codes, s_a[: act.weights.S].copy()

@@ -193,7 +193,13 @@ struct soniq_weights_s {
   uint8_t* colrank = nullptr;
   int32_t* pos = nullptr;
   uint8_t* seg = nullptr;
+  // sub-group activation scales (0 bits: one scale per precision group)
+  int act_group_bits = 0;
+  int gsub[2] = {0, 0};   // granules per block
+  int nsub[2] = {0, 0};   // blocks per precision group
+  int32_t* grp = nullptr;  // block of each original input channel
 
+  int scales() const { return act_group_bits ? nsub[0] + nsub[1] : kp.S; }
   WDev dev() const { return WDev{packed, blk_off, blk_c, colinfo, shw, tile_cols, colrank}; }
 };
 
@@ -222,6 +228,7 @@ void free_weights(soniq_weights w) {
   (void)hipFree(w->colrank);
   (void)hipFree(w->pos);
   (void)hipFree(w->seg);
+  (void)hipFree(w->grp);
   w->magic = kDead;
   delete w;
 }
@@ -256,6 +263,10 @@ ActPlan make_act_plan(const soniq_weights_s& w, int64_t M_alloc) {
     }
   }
   ap.Kp = (int)w.kp.Kp;
+  for (int g = 0; g < 2; ++g) {
+    ap.gsub[g] = w.gsub[g];
+    ap.nsub[g] = w.nsub[g];
+  }
   return ap;
 }
 
@@ -324,10 +335,10 @@ soniq_status soniq_plan_input_channels(const uint8_t* a_bits, int64_t K, int64_t
   return SONIQ_OK;
 }
 
-soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
-                                   const uint8_t* w_bits, const uint8_t* a_bits,
-                                   int a_signed, int wq_mode, void* stream,
-                                   soniq_weights* out) {
+soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                        const uint8_t* w_bits, const uint8_t* a_bits,
+                                        int a_signed, int wq_mode, int act_group_bits,
+                                        void* stream, soniq_weights* out) {
   if (!W_dev || !w_bits || !a_bits || !out)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: null pointer");
   if (N < 1 || K < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: N, K must be >= 1");
@@ -349,6 +360,32 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
                 (long long)kp.Kp, SONIQ_MAX_K);
   if (N > (int64_t)1 << 24)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_pack_weights: N %lld exceeds 2^24", (long long)N);
+  if (act_group_bits < 0 || act_group_bits % 512 != 0)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_pack_weights: act_group_bits %d is not 0 or a positive multiple of 512",
+                act_group_bits);
+  int gsub[2] = {0, 0}, nsub[2] = {0, 0};
+  if (act_group_bits > 0) {
+    for (int g = 0; g < kp.S; ++g) {
+      const int b = kp.bits[g];
+      const int c = a_container(b, a_signed);
+      if (a_qparam(b, a_signed).sign1 || a_zero_point(b, a_signed, c) != 0)
+        return fail(SONIQ_ERR_UNSUPPORTED,
+                    "soniq_pack_weights: sub-group scales need a zero point of 0 and no 1-bit "
+                    "group (activation width %d, %s)", b, a_signed ? "signed" : "unsigned");
+      const int per = act_group_bits / c;  // channels per block, a multiple of 64
+      gsub[g] = per / kGran;
+      nsub[g] = (int)((kp.len[g] + per - 1) / per);
+    }
+    if (nsub[0] + nsub[1] > kGSubMax)
+      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_pack_weights: %d activation blocks exceed %d",
+                  nsub[0] + nsub[1], kGSubMax);
+    // one code row and the block scales must fit a workgroup's 64 KB
+    if (kp.Kp + 8 * (int64_t)(nsub[0] + nsub[1]) > 64 * 1024)
+      return fail(SONIQ_ERR_UNSUPPORTED,
+                  "soniq_pack_weights: padded K %lld too large for sub-group scales",
+                  (long long)kp.Kp);
+  }
 
   soniq_weights w = new (std::nothrow) soniq_weights_s();
   if (!w) return fail(SONIQ_ERR_OUT_OF_MEMORY, "soniq_pack_weights: host allocation");
@@ -358,6 +395,11 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
   w->wq_mode = wq_mode;
   w->kp = std::move(kp);
   w->nw = nw;
+  w->act_group_bits = act_group_bits;
+  for (int g = 0; g < 2; ++g) {
+    w->gsub[g] = gsub[g];
+    w->nsub[g] = nsub[g];
+  }
   w->wb[0] = wb[0];
   w->wb[1] = nw == 2 ? wb[1] : 0;
 
@@ -450,6 +492,19 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
   STEP(dev_alloc(&w->colrank, (size_t)wp.Np));
   STEP(dev_alloc(&w->pos, (size_t)K));
   STEP(dev_alloc(&w->seg, (size_t)K));
+  std::vector<int32_t> grp_h;
+  if (act_group_bits > 0) {
+    // block of channel k: its rank inside its precision group over the
+    // channels per block, after the blocks of group 0
+    grp_h.resize(K);
+    for (int64_t k = 0; k < K; ++k) {
+      const int g = w->kp.seg[k];
+      const int64_t rank = w->kp.pos[k] - (g ? w->kp.pad[0] : 0);
+      grp_h[k] = (g ? nsub[0] : 0) + (int32_t)(rank / ((int64_t)gsub[g] * kGran));
+    }
+    STEP(dev_alloc(&w->grp, (size_t)K));
+    STEP(hipMemcpyAsync(w->grp, grp_h.data(), K * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  }
   STEP(dev_alloc(&wbits_dev, (size_t)N));
   STEP(dev_alloc(&phys_dev, (size_t)N));
   STEP(hipMemsetAsync(w->packed, 0, (size_t)w->packed_bytes, st));
@@ -479,6 +534,14 @@ soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int
   return SONIQ_OK;
 }
 
+soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                   const uint8_t* w_bits, const uint8_t* a_bits,
+                                   int a_signed, int wq_mode, void* stream,
+                                   soniq_weights* out) {
+  return soniq_pack_weights_grouped(W_dev, N, K, ldw, w_bits, a_bits, a_signed, wq_mode, 0,
+                                    stream, out);
+}
+
 soniq_status soniq_pack_weights(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
                                 const uint8_t* w_bits, const uint8_t* a_bits, int a_signed,
                                 void* stream, soniq_weights* out) {
@@ -504,6 +567,8 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out) {
   out->packed_w_bytes = w->packed_bytes;
   out->packed_w_bytes_algorithmic =
       (w->w_cnt[0] * w->wp.c_lo + w->w_cnt[1] * w->wp.c_hi) * w->K / 8;
+  out->act_group_bits = w->act_group_bits;
+  out->act_scales = w->scales();
   return SONIQ_OK;
 }
 
@@ -519,11 +584,14 @@ soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
   a->ap = make_act_plan(*w, a->M_alloc);
   a->packed_bytes = act_bytes(a->ap, a->M_alloc);
   hipError_t e = dev_alloc(&a->packed, (size_t)a->packed_bytes);
-  if (e == hipSuccess) e = dev_alloc(&a->partial, 2 * kAbsmaxBlocks);
+  const size_t nscale = (size_t)std::max(2, w->scales());
+  const size_t npart = std::max((size_t)2 * kAbsmaxBlocks,
+                                w->act_group_bits ? (size_t)kGAbsParts * nscale : 0);
+  if (e == hipSuccess) e = dev_alloc(&a->partial, npart);
   if (e == hipSuccess) e = dev_alloc(&a->counter, kActStateWords);
-  if (e == hipSuccess) e = dev_alloc(&a->s_a, 2);
+  if (e == hipSuccess) e = dev_alloc(&a->s_a, nscale);
   if (e == hipSuccess) e = hipMemset(a->counter, 0, kActStateWords * sizeof(unsigned int));
-  if (e == hipSuccess) e = hipMemset(a->s_a, 0, 2 * sizeof(float));
+  if (e == hipSuccess) e = hipMemset(a->s_a, 0, nscale * sizeof(float));
   if (e == hipSuccess) e = hipMemset(a->packed, 0, (size_t)a->packed_bytes);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
@@ -549,6 +617,12 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: M=%lld outside [1, %lld]",
                 (long long)M, (long long)act->max_M);
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: lda < K");
+  if (w->act_group_bits) {
+    HIP_TRY(launch_act_quant_grouped(A_dev, M, w->K, lda, act->ap, w->pos, w->grp, act->partial,
+                                     act->s_a, act->packed, reinterpret_cast<hipStream_t>(stream)));
+    act->M = M;
+    return SONIQ_OK;
+  }
   HIP_TRY(launch_act_quant(A_dev, M, w->K, lda, act->ap, w->pos, w->seg, act->partial,
                            act->counter, act->s_a, act->packed,
                            reinterpret_cast<hipStream_t>(stream)));
@@ -568,6 +642,9 @@ soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64
                 (long long)(9 * C), (long long)w->K);
   if (B * C * H * W >= ((int64_t)1 << 31))
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: input has 2^31 elements or more");
+  if (w->act_group_bits)
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_quantize_act_conv3x3: weights packed with sub-group activation scales");
   const int64_t M = B * H * W;
   if (M > act->max_M)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: B*H*W=%lld > max_M=%lld",
@@ -598,6 +675,14 @@ soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int6
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: ldy < N");
   const int64_t M = act->M;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (w->act_group_bits) {
+    const int64_t tiles = ((M + 63) / 64) * (w->wp.Np / kGemmBN);
+    if (tiles > 0x7FFFFFFFLL)
+      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
+    HIP_TRY(launch_mp_gemm_grouped(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev,
+                                   ldy, acc_dev, st));
+    return SONIQ_OK;
+  }
   if (gemv_fits(M, act->ap, w->wp)) {
     HIP_TRY(launch_mp_gemv(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                            acc_dev, st));
@@ -625,7 +710,7 @@ soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float*
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: lda < K");
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: ldy < N");
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (M == 1 && gemv_fused_fits(A_dev, w->K, act->ap, w->wp)) {
+  if (M == 1 && !w->act_group_bits && gemv_fused_fits(A_dev, w->K, act->ap, w->wp)) {
     HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos, act->packed, act->s_a, act->ap, w->dev(), w->wp,
                               w->N, Y_dev, acc_dev, st));
     act->M = 1;
@@ -663,9 +748,9 @@ soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a) {
   const ActPlan& ap = act->ap;
   const soniq_weights w = act->w;
   std::vector<uint8_t> packed(act->packed_bytes);
-  float sa[2] = {0, 0};
+  std::vector<float> sa((size_t)std::max(2, w->scales()), 0.0f);
   HIP_TRY(hipMemcpy(packed.data(), act->packed, act->packed_bytes, hipMemcpyDeviceToHost));
-  HIP_TRY(hipMemcpy(sa, act->s_a, sizeof sa, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(sa.data(), act->s_a, sa.size() * sizeof(float), hipMemcpyDeviceToHost));
   if (codes)
     for (int64_t m = 0; m < act->M; ++m)
       for (int64_t k = 0; k < w->K; ++k) {
@@ -675,7 +760,7 @@ soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a) {
         codes[m * w->K + k] = decode_signed(block_field(blk, (int)(m % kBlk), e, ap.c[g]), ap.c[g]) + ap.zp[g];
       }
   if (s_a)
-    for (int g = 0; g < ap.S; ++g) s_a[g] = sa[g];
+    for (int g = 0; g < w->scales(); ++g) s_a[g] = sa[g];
   return SONIQ_OK;
 }
 

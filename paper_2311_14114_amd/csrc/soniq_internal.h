@@ -72,6 +72,11 @@ struct ActPlan {
   int64_t seg_off[2];     // byte offset of each group's buffer
   int64_t mblk_bytes[2];  // bytes of one 16-row block over the group's granules
   QParam q[2];            // activation quantizer per group
+  // Sub-group scales (GroupSize_act): each group is cut into nsub blocks of
+  // gsub granules, each with its own scale; gsub = 0 keeps one scale per
+  // group.
+  int gsub[2];
+  int nsub[2];
 };
 
 struct WPlan {
@@ -140,6 +145,20 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const uint8_t* seg_dev, float* partial,
                             unsigned int* counter, float* s_a, uint8_t* packed,
                             hipStream_t stream);
+
+// Sub-group scales: block scales in s_a[block], blocks of group 0 first;
+// grp_dev[k] = block of original channel k.  At most kGAbsParts partial
+// rows of block maxima (the handle's partial buffer holds that many), and
+// at most kGSubMax blocks.
+constexpr int kGAbsParts = 256;
+constexpr int kGSubMax = 256;
+hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
+                                    const ActPlan& ap, const int32_t* pos_dev,
+                                    const int32_t* grp_dev, float* partial, float* s_a,
+                                    uint8_t* packed, hipStream_t stream);
+hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                  const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
+                                  uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,

@@ -1775,12 +1775,20 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
 // issues exactly WFM + kLB direct loads per stage (lanes past the data
 // re-load one valid chunk into an unused slot), so each wait is a
 // compile-time vmcnt.
-template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT>
+// The hook run after each granule's products (see k_gemm_g); the plain
+// GEMM passes this one, which does nothing.
+struct NoGranuleHook {
+  template <class T>
+  __device__ __forceinline__ void operator()(T&, int) const {}
+};
+
+template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT,
+          class Hook = NoGranuleHook>
 __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abase, int64_t mstride,
                                            int ca_rt, int ng, const uint8_t* wtile, int ngt,
                                            const int (&bc)[8], const int (&bpre)[9], int qbase,
                                            v4i (&acc)[WFM][4], int tid, int lane, int wid,
-                                           int wm, int wn) {
+                                           int wm, int wn, Hook&& hook = Hook{}) {
   constexpr int BM = 32 * WFM;
   static_assert(ASLOT == BM * 16 * 8 && SLOT == ASLOT + kBSlot, "runtime containers: 8-bit slots");
   constexpr int L = WFM + kLB;
@@ -1896,6 +1904,7 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj)
             acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[jj], acc[i][jj], 0, 0, 0);
+        hook(acc, 2 * st + kk);
       }
     }
   }
@@ -2858,6 +2867,244 @@ bool launch_act_coop(const float* A, int64_t M, int64_t K, int64_t lda, const Ac
   return false;
 }
 
+// ------------------------------------------------------ sub-group scales --
+// GroupSize_act blocks (the design-space parameters of Sec. 3; Sec. 5 uses
+// 512-bit activation groups for transformers): each precision group is cut
+// into blocks of gsub granules (64 channels each) in the planned order,
+// and each block has its own scale, the max-abs over the batch and the
+// block's channels.  Quantizing takes three launches (partial block maxima
+// per row range, block scales, codes); the GEMM folds each block's exact
+// int32 sum into fp32 as soon as the block ends.  grp[k] is the block of
+// original channel k; blocks of group 0 come first.  These paths run only
+// with a zero point of 0 in both groups (signed codes, or unsigned widths
+// below their container) and no 1-bit sign group.
+
+// Workgroup b takes rows [b*rpb, min(M, (b+1)*rpb)): each column's max-abs
+// over them goes into its block's LDS word (non-negative floats order as
+// their bits), then the block maxima go to part[b*nsub + j].  Dynamic LDS:
+// nsub words.
+__global__ __launch_bounds__(256) void k_gabsmax(const float* __restrict__ A, int64_t M, int64_t K,
+                                                 int64_t lda, int64_t rpb,
+                                                 const int32_t* __restrict__ grp, int nsub,
+                                                 float* __restrict__ part) {
+  extern __shared__ unsigned smax[];
+  const int tid = threadIdx.x;
+  for (int j = tid; j < nsub; j += 256) smax[j] = 0u;
+  __syncthreads();
+  const int64_t m0 = (int64_t)blockIdx.x * rpb;
+  const int64_t n = min(M, m0 + rpb) - m0;
+  for (int64_t k = tid; k < K; k += 256) {
+    const float* col = A + m0 * lda + k;
+    float m = 0.0f;
+    int64_t r = 0;
+    for (; r + 8 <= n; r += 8) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = fabsf(col[(r + i) * lda]);
+      m = fmaxf(m, fmaxf(fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])),
+                         fmaxf(fmaxf(v[4], v[5]), fmaxf(v[6], v[7]))));
+    }
+    for (; r < n; ++r) m = fmaxf(m, fabsf(col[r * lda]));
+    atomicMax(&smax[grp[k]], __float_as_uint(m));
+  }
+  __syncthreads();
+  for (int j = tid; j < nsub; j += 256) part[(int64_t)blockIdx.x * nsub + j] = __uint_as_float(smax[j]);
+}
+
+// Scale of block j (one workgroup per block) from the partial maxima.
+__global__ __launch_bounds__(256) void k_gscales(const float* __restrict__ part, int nparts,
+                                                 int nsub, ActPlan ap, float* __restrict__ s_a) {
+  __shared__ float red[8];
+  const int j = blockIdx.x;
+  float m = 0.0f;
+  for (int b = threadIdx.x; b < nparts; b += 256) m = fmaxf(m, part[(int64_t)b * nsub + j]);
+  m = block_max(m, red);
+  if (threadIdx.x == 0) s_a[j] = group_scale(m, j < ap.nsub[0] ? ap.q[0] : ap.q[1]);
+}
+
+// R rows per workgroup: each element's code with its block's scale goes to
+// LDS at its planned position, then the rows' units are written.  Codes
+// follow the per-group quantizer (reciprocal shortcut, exact division near
+// a tie or for scales outside the shortcut's range).  Dynamic LDS: R*Kp
+// code bytes, then nsub scales and nsub reciprocals.
+template <int R>
+__global__ __launch_bounds__(256) void k_gquant(const float* __restrict__ A, int64_t M, int64_t K,
+                                                int64_t lda, const int32_t* __restrict__ pos,
+                                                const int32_t* __restrict__ grp, ActPlan ap,
+                                                int nsub, const float* __restrict__ s_a,
+                                                uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  float* stab = reinterpret_cast<float*>(codes + R * ap.Kp);
+  float* rtab = stab + nsub;
+  const int tid = threadIdx.x;
+  const int64_t m0 = (int64_t)blockIdx.x * R;
+  const int rows = (int)min((int64_t)R, M - m0);
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < rows * ap.Kp / 4; i += 256) codes32[i] = 0u;
+  for (int j = tid; j < nsub; j += 256) {
+    const float sc = s_a[j];
+    stab[j] = sc;
+    rtab[j] = fast_ok(sc) ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+  }
+  __syncthreads();
+  const float lo0 = (float)ap.q[0].lo, hi0 = (float)ap.q[0].hi;
+  const float lo1 = (float)ap.q[1].lo, hi1 = (float)ap.q[1].hi;
+  for (int64_t k = tid; k < K; k += 256) {
+    const int j = grp[k], p = pos[k];
+    const bool g1 = j >= ap.nsub[0];
+    const float sc = stab[j], rs = rtab[j];
+    const float lo = g1 ? lo1 : lo0, hi = g1 ? hi1 : hi0;
+    float x[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = r < rows ? A[(m0 + r) * lda + k] : 0.0f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      float t = 0.0f;
+      if (sc != 0.0f) {
+        const float e = x[r] * rs;
+        t = __builtin_rintf(e);
+        if (rs == 0.0f || fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f) t = __builtin_rintf(__fdiv_rn(x[r], sc));
+        t = fminf(fmaxf(t, lo), hi);
+      }
+      if (r < rows) codes[r * ap.Kp + p] = (uint8_t)(int8_t)(int)t;
+    }
+  }
+  __syncthreads();
+  write_act_units(codes, rows, m0, ap, packed);
+}
+
+// Block scales a wave keeps in registers: lane l holds s_a[l + 64*i].
+constexpr int kGSubRegs = 4;
+static_assert(kGSubMax <= 64 * kGSubRegs, "every block scale has a lane");
+
+// The 64 x 128 tile of k_gemm (generic loop: containers read at run time)
+// with sub-group scales.  After the last granule of each block the tile
+// folds its int32 sums into fp32, y = y + f(acc >> sh) * s_a[j] (multiply,
+// then add, in block order), and restarts them at 0; the epilogue scales
+// by s_w and rounds to bf16.  With a zero point of 0, acc >> sh is the
+// block's exact sum (the unpack scales removed), which the optional int32
+// dump receives as [block][M][N].
+__global__ __launch_bounds__(256) void k_gemm_g(GemmArgs a) {
+  constexpr int WFM = 2, NST = 2, BM = 32 * WFM;
+  constexpr int SLOT = gemm_slot(2, 0, 0, 0, 0, WFM);
+  constexpr int ASLOT = gemm_aslot(2, 0, 0, 0, 0, WFM);
+  __shared__ __align__(16) uint8_t lds[NST * SLOT];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;
+  const ActPlan& ap = a.ap;
+  const int ntn = a.wp.Np / kGemmBN;
+  const int G = (int)gridDim.x, x = (int)(blockIdx.x & 7), l = (int)(blockIdx.x >> 3);
+  const int tile = a.xcd_tiles ? x * (G >> 3) + min(x, G & 7) + l : (int)blockIdx.x;
+  const int mt = tile / ntn, nt = tile - mt * ntn;
+  const int64_t m0 = (int64_t)mt * BM;
+  const int jb0 = nt * 8;
+
+  int bc[8], bpre[9];
+  bpre[0] = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    bc[j] = wblk_c(a.wp, jb0 + j);
+    bpre[j + 1] = bpre[j] + 16 * bc[j];
+  }
+  const uint8_t* wtile = a.wd.packed + wblk_off(a.wp, jb0);
+
+  const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
+  float sreg[kGSubRegs];
+#pragma unroll
+  for (int i = 0; i < kGSubRegs; ++i) sreg[i] = lane + 64 * i < nsub ? a.s_a[lane + 64 * i] : 0.0f;
+  ColInfo cinf[4];
+  uint8_t cshw[4], crank[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
+    cinf[jj] = a.wd.colinfo[pc];
+    cshw[jj] = a.wd.shw[pc];
+    crank[jj] = a.wd.colrank[pc];
+  }
+
+  v4i acc[WFM][4];
+  float yf[WFM][4][4];
+#pragma unroll
+  for (int i = 0; i < WFM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      acc[i][jj] = v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) yf[i][jj][r] = 0.0f;
+    }
+
+  // Fold block j of group g.
+  auto fold = [&](v4i (&ac)[WFM][4], int g, int j) __attribute__((always_inline)) {
+    const int jr = j >> 6;
+    const float sv = jr == 0 ? sreg[0] : jr == 1 ? sreg[1] : jr == 2 ? sreg[2] : sreg[3];
+    const float sj = __builtin_bit_cast(
+        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sv), j & 63));
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int sh = ap.sh[g] + (cshw[jj] & 0x7F);
+#pragma unroll
+      for (int i = 0; i < WFM; ++i) {
+        const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = ac[i][jj][r] >> sh;
+          yf[i][jj][r] = __fadd_rn(yf[i][jj][r], __fmul_rn((float)t, sj));
+          if (a.acc) {
+            const int64_t m = m0 + row0 + r;
+            if (m < a.M && cinf[jj].n >= 0) a.acc[((int64_t)j * a.M + m) * a.N + cinf[jj].n] = t;
+          }
+        }
+        ac[i][jj] = v4i{0, 0, 0, 0};
+      }
+    }
+  };
+  for (int g = 0; g < ap.S; ++g) {
+    const int ng = g ? ap.ng[1] : ap.ng[0];
+    const int gpg = g ? ap.gsub[1] : ap.gsub[0];
+    const int j0 = g ? ap.nsub[0] : 0;
+    auto hook = [&](v4i (&ac)[WFM][4], int q) __attribute__((always_inline)) {
+      if (q < ng && ((q + 1) % gpg == 0 || q == ng - 1)) fold(ac, g, j0 + q / gpg);
+    };
+    gemm_group_any<0, 0, 0, WFM, NST, ASLOT, SLOT>(
+        lds, a.act + (g ? ap.seg_off[1] : ap.seg_off[0]) + (m0 / kBlk) * (g ? ap.mblk_bytes[1] : ap.mblk_bytes[0]),
+        g ? ap.mblk_bytes[1] : ap.mblk_bytes[0], g ? ap.c[1] : ap.c[0], ng, wtile, a.wp.ngt, bc, bpre,
+        g ? ap.ng[0] : 0, acc, tid, lane, wid, wm, wn, hook);
+  }
+
+  // Epilogue: y * s_w, bf16, staged in LDS in ascending original column
+  // order (as in k_gemm), then stored row by row.
+  constexpr int YS = kGemmBN + 8;
+  uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
+  static_assert(BM * YS * 2 <= NST * SLOT, "output staging fits the ring");
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    const ColInfo ci = cinf[jj];
+    if (ci.n < 0) continue;
+    uint16_t* ycol = ys + crank[jj];
+#pragma unroll
+    for (int i = 0; i < WFM; ++i) {
+      const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
+#pragma unroll
+      for (int r = 0; r < 4; r += 2) {
+        const __hip_bfloat162 pr = __float22bfloat162_rn(
+            make_float2(__fmul_rn(yf[i][jj][r], ci.s_w), __fmul_rn(yf[i][jj][r + 1], ci.s_w)));
+        ycol[(row0 + r) * YS] = __builtin_bit_cast(uint16_t, pr.x);
+        ycol[(row0 + r + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
+      }
+    }
+  }
+  __syncthreads();
+  const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
+  if (n >= 0) {
+    const int mrem = (int)min((int64_t)BM, a.M - m0);
+    uint16_t* yout = a.Y + m0 * a.ldy + n;
+    for (int row = tid / kGemmBN; row < mrem; row += 256 / kGemmBN)
+      yout[(int64_t)row * a.ldy] = ys[row * YS + (tid & (kGemmBN - 1))];
+  }
+}
+
 }  // namespace
 
 // ------------------------------------------------------------- launchers --
@@ -3535,6 +3782,43 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
     else if (M <= 4) hipLaunchKernelGGL(k_gemv_any<4>, grid, dim3(256), lds, stream, a);
     else hipLaunchKernelGGL(k_gemv_any<8>, grid, dim3(256), lds, stream, a);
   }
+  return hipGetLastError();
+}
+
+// Sub-group scales: partial block maxima over row ranges of at least 8
+// rows (at most kGAbsParts of them), block scales, then codes.
+hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
+                                    const ActPlan& ap, const int32_t* pos_dev,
+                                    const int32_t* grp_dev, float* partial, float* s_a,
+                                    uint8_t* packed, hipStream_t stream) {
+  const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
+  const int64_t rpb = std::max<int64_t>(8, (M + kGAbsParts - 1) / kGAbsParts);
+  const int nparts = (int)((M + rpb - 1) / rpb);
+  hipLaunchKernelGGL(k_gabsmax, dim3((unsigned)nparts), dim3(256), (size_t)nsub * 4, stream, A, M, K,
+                     lda, rpb, grp_dev, nsub, partial);
+  hipLaunchKernelGGL(k_gscales, dim3((unsigned)nsub), dim3(256), 0, stream, partial, nparts, nsub, ap,
+                     s_a);
+  const size_t tab = (size_t)nsub * 8;
+  if (kBlk * (size_t)ap.Kp + tab <= 64 * 1024)
+    hipLaunchKernelGGL(k_gquant<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
+                       kBlk * (size_t)ap.Kp + tab, stream, A, M, K, lda, pos_dev, grp_dev, ap, nsub,
+                       s_a, packed);
+  else if (4 * (size_t)ap.Kp + tab <= 64 * 1024)
+    hipLaunchKernelGGL(k_gquant<4>, dim3((unsigned)((M + 3) / 4)), dim3(256), 4 * (size_t)ap.Kp + tab,
+                       stream, A, M, K, lda, pos_dev, grp_dev, ap, nsub, s_a, packed);
+  else
+    hipLaunchKernelGGL(k_gquant<1>, dim3((unsigned)M), dim3(256), (size_t)ap.Kp + tab, stream, A, M,
+                       K, lda, pos_dev, grp_dev, ap, nsub, s_a, packed);
+  return hipGetLastError();
+}
+
+hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                  const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
+                                  uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
+  a.xcd_tiles = tiles <= 2048;
+  hipLaunchKernelGGL(k_gemm_g, dim3((unsigned)tiles), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

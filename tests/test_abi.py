@@ -102,3 +102,27 @@ def test_input_channel_plan_matches_definition(L, seed):
     assert seg_len[0] == n0 and seg_pad[0] == pad0
     assert seg_len[1] == K - n0 and seg_pad[1] == -(-(K - n0) // 64) * 64
     assert len(set(pos.tolist())) == K
+
+
+def test_grouped_pack_validation(L):
+    """Sub-group scale requests are checked before any device work."""
+    fake = ctypes.c_void_p(0x1000)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    wb = np.full(4, 4, np.uint8)
+
+    def pack(ab, signed, bits):
+        h = ctypes.c_void_p()
+        K = ab.shape[0]
+        return L.soniq_pack_weights_grouped(fake, 4, K, K, p(wb), p(ab), signed, 0, bits, None,
+                                            ctypes.byref(h))
+    ab4 = np.full(256, 4, np.uint8)
+    assert pack(ab4, 1, 100) == sq.SONIQ_ERR_INVALID_ARGUMENT
+    assert b"512" in L.soniq_last_error()
+    assert pack(ab4, 1, -512) == sq.SONIQ_ERR_INVALID_ARGUMENT
+    # unsigned 4-bit codes fill their container: zero point, not supported
+    assert pack(ab4, 0, 512) == sq.SONIQ_ERR_UNSUPPORTED
+    assert b"zero point" in L.soniq_last_error()
+    assert pack(np.full(256, 1, np.uint8), 1, 512) == sq.SONIQ_ERR_UNSUPPORTED
+    # 300 blocks of 64 8-bit channels
+    assert pack(np.full(64 * 300, 8, np.uint8), 1, 512) == sq.SONIQ_ERR_UNSUPPORTED
+    assert b"blocks" in L.soniq_last_error()

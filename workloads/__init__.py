@@ -186,6 +186,24 @@ def square_8192(size: int = 8192) -> dict:
                    w_frac_lo=0.5, seed=BASE_SEED + 5, name="square_8192")
 
 
+def _grouped(base: dict, group_bits: int = 512) -> dict:
+    """The same inputs with sub-group activation scales: each precision
+    group cut into blocks of group_bits of storage (Sec. 5 normalizes
+    transformer activations in 512-bit groups)."""
+    case = dict(base)
+    case["name"] = f"{base['name']}_g{group_bits}"
+    case["act_group_bits"] = group_bits
+    return case
+
+
+def xfmr_qkv_g512() -> dict:
+    return _grouped(xfmr_qkv())
+
+
+def xfmr_ffn_down_g512() -> dict:
+    return _grouped(xfmr_ffn_down())
+
+
 BUILDERS = {
     "tiny_linear": tiny_linear,
     "conv3x3_im2col": conv3x3_im2col,
@@ -197,6 +215,8 @@ BUILDERS = {
     "decode_11008_m8": decode_11008_m8,
     "decode_4096_m8": decode_4096_m8,
     "square_8192": square_8192,
+    "xfmr_qkv_g512": xfmr_qkv_g512,
+    "xfmr_ffn_down_g512": xfmr_ffn_down_g512,
 }
 
 
