@@ -150,7 +150,7 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
 // grp_dev[k] = block of original channel k.  At most kGAbsParts partial
 // rows of block maxima (the handle's partial buffer holds that many), and
 // at most kGSubMax blocks.
-constexpr int kGAbsParts = 256;
+constexpr int kGAbsParts = 1024;
 constexpr int kGSubMax = 256;
 hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
                                     const ActPlan& ap, const int32_t* pos_dev,

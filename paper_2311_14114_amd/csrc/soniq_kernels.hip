@@ -1603,13 +1603,22 @@ __device__ __forceinline__ void mma_granule(v4i (&acc)[WFM][4], uint32_t a_addr,
   }
 }
 
+// The hook run after each granule's products, given the accumulators and
+// the granule's index in its group (see k_gemm_g); the plain GEMM passes
+// this one, which does nothing.
+struct NoGranuleHook {
+  template <class T>
+  __device__ __forceinline__ void operator()(T&, int) const {}
+};
+
 // Both granules of a stage on a tile of one weight width CB: every unit
 // read of the stage is issued first; granule 0 is widened and multiplied
 // once its reads have landed (the 4 + WFM reads of granule 1 may still be
-// in flight), then granule 1.
-template <int CA, int CB, int WFM>
+// in flight), then granule 1.  q0: index of granule 0 for the hook.
+template <int CA, int CB, int WFM, class Hook = NoGranuleHook>
 __device__ __forceinline__ void mma_stage(v4i (&acc)[WFM][4], uint32_t a_addr,
-                                          const uint32_t (&b_addr)[4]) {
+                                          const uint32_t (&b_addr)[4], Hook&& hook = Hook{},
+                                          int q0 = 0) {
   raw_t<CB> rb0[4], rb1[4];
   raw_t<CA> ra0[WFM], ra1[WFM];
 #pragma unroll
@@ -1636,6 +1645,7 @@ __device__ __forceinline__ void mma_stage(v4i (&acc)[WFM][4], uint32_t a_addr,
   };
   lds_wait_n<4 + WFM>();
   granule(rb0, ra0);
+  hook(acc, q0);
 #if defined(__HIP_DEVICE_COMPILE__)
   // keep granule 0's products ahead of the wait (MFMAs are not memory
   // operations, so the wait's memory clobber alone does not order them)
@@ -1643,6 +1653,7 @@ __device__ __forceinline__ void mma_stage(v4i (&acc)[WFM][4], uint32_t a_addr,
 #endif
   lds_wait();
   granule(rb1, ra1);
+  hook(acc, q0 + 1);
 }
 
 // One activation group's K loop for containers fixed at compile time (A in
@@ -1653,13 +1664,14 @@ __device__ __forceinline__ void mma_stage(v4i (&acc)[WFM][4], uint32_t a_addr,
 // fixed for the group and a scalar stage offset advances them (per lane on
 // the mixed-width tile); chunks past the data read as zero, which also
 // zeroes the second granule of a final half stage, so its products vanish.
-template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT>
+template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT,
+          class Hook = NoGranuleHook>
 __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* abase,
                                                 int64_t mstride, int ng, const uint8_t* wtile,
                                                 int wbytes, int ngt, const int (&bc)[8],
                                                 const int (&bpre)[9], int qbase,
                                                 v4i (&acc)[WFM][4], int tid, int lane, int wid,
-                                                int wm, int wn) {
+                                                int wm, int wn, Hook&& hook = Hook{}) {
 #if defined(__HIP_DEVICE_COMPILE__)  // GPU builtins; the host pass never runs it
   static_assert(CA == 4 || CA == 8, "activation container");
   constexpr int BM = 32 * WFM;
@@ -1757,10 +1769,12 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
     const uint32_t soff = (uint32_t)((st % NST) * SLOT);
     const uint32_t b_addr[4] = {b_lds[0] + soff, b_lds[1] + soff, b_lds[2] + soff, b_lds[3] + soff};
     if constexpr (UNI) {
-      mma_stage<CA, CBL, WFM>(acc, a_lds + soff, b_addr);
+      mma_stage<CA, CBL, WFM>(acc, a_lds + soff, b_addr, hook, 2 * st);
     } else {
       mma_granule<CA, CBL, CBH, WFM, 0>(acc, a_lds + soff, b_addr, wcj, false);
+      hook(acc, 2 * st);
       mma_granule<CA, CBL, CBH, WFM, 1>(acc, a_lds + soff, b_addr, wcj, false);
+      hook(acc, 2 * st + 1);
     }
   }
   // Everyone is done reading the ring before the next group refills it.
@@ -1775,13 +1789,6 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
 // issues exactly WFM + kLB direct loads per stage (lanes past the data
 // re-load one valid chunk into an unused slot), so each wait is a
 // compile-time vmcnt.
-// The hook run after each granule's products (see k_gemm_g); the plain
-// GEMM passes this one, which does nothing.
-struct NoGranuleHook {
-  template <class T>
-  __device__ __forceinline__ void operator()(T&, int) const {}
-};
-
 template <int CA, int CBL, int CBH, int WFM, int NST, int ASLOT, int SLOT,
           class Hook = NoGranuleHook>
 __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abase, int64_t mstride,
@@ -2973,21 +2980,150 @@ __global__ __launch_bounds__(256) void k_gquant(const float* __restrict__ A, int
   write_act_units(codes, rows, m0, ap, packed);
 }
 
+// float4 forms of the two passes above (K % 4 == 0, lda % 4 == 0, A
+// 16-byte aligned, K <= 1024*J): thread tid owns float4 columns
+// k4 = tid + 256*j (j < J) of every row; rows are loaded four at a time
+// for all its columns together.  Clamped rows and columns re-read data
+// already counted (a max ignores them; the quantizer skips them).
+template <int J>
+__global__ __launch_bounds__(256) void k_gabsmax4(const float4* __restrict__ A, int64_t M, int K4,
+                                                  int64_t lda4, int64_t rpb,
+                                                  const int4* __restrict__ grp4, int nsub,
+                                                  float* __restrict__ part) {
+  extern __shared__ unsigned smax[];
+  const int tid = threadIdx.x;
+  for (int j = tid; j < nsub; j += 256) smax[j] = 0u;
+  const int64_t m0 = (int64_t)blockIdx.x * rpb;
+  const int n = (int)(min(M, m0 + rpb) - m0);
+  float4 mx[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) mx[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int r = 0; r < n; r += 4) {
+    float4 v[4][J];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        v[rr][j] = A[(m0 + min(r + rr, n - 1)) * lda4 + min(tid + 256 * j, K4 - 1)];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        mx[j].x = fmaxf(mx[j].x, fabsf(v[rr][j].x));
+        mx[j].y = fmaxf(mx[j].y, fabsf(v[rr][j].y));
+        mx[j].z = fmaxf(mx[j].z, fabsf(v[rr][j].z));
+        mx[j].w = fmaxf(mx[j].w, fabsf(v[rr][j].w));
+      }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int k4 = tid + 256 * j;
+    if (k4 < K4) {
+      const int4 g = grp4[k4];
+      atomicMax(&smax[g.x], __float_as_uint(mx[j].x));
+      atomicMax(&smax[g.y], __float_as_uint(mx[j].y));
+      atomicMax(&smax[g.z], __float_as_uint(mx[j].z));
+      atomicMax(&smax[g.w], __float_as_uint(mx[j].w));
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < nsub; j += 256) part[(int64_t)blockIdx.x * nsub + j] = __uint_as_float(smax[j]);
+}
+
+template <int R, int J>
+__global__ __launch_bounds__(256) void k_gquant4(const float4* __restrict__ A, int64_t M, int K4,
+                                                 int64_t lda4, const int4* __restrict__ pos4,
+                                                 const int4* __restrict__ grp4, ActPlan ap,
+                                                 int nsub, const float* __restrict__ s_a,
+                                                 uint8_t* __restrict__ packed) {
+  static_assert(R % 4 == 0, "rows go four at a time");
+  extern __shared__ __align__(16) uint8_t codes[];
+  float* stab = reinterpret_cast<float*>(codes + R * ap.Kp);
+  float* rtab = stab + nsub;
+  const int tid = threadIdx.x;
+  const int64_t m0 = (int64_t)blockIdx.x * R;
+  const int rows = (int)min((int64_t)R, M - m0);
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < rows * ap.Kp / 4; i += 256) codes32[i] = 0u;
+  for (int j = tid; j < nsub; j += 256) {
+    const float sc = s_a[j];
+    stab[j] = sc;
+    rtab[j] = fast_ok(sc) ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+  }
+  int4 p[J], gb[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int k4 = min(tid + 256 * j, K4 - 1);
+    p[j] = pos4[k4];
+    gb[j] = grp4[k4];
+  }
+  __syncthreads();
+  const float lo0 = (float)ap.q[0].lo, hi0 = (float)ap.q[0].hi;
+  const float lo1 = (float)ap.q[1].lo, hi1 = (float)ap.q[1].hi;
+  float sc[J][4], rs[J][4];
+  bool g1[J][4];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int gg[4] = {gb[j].x, gb[j].y, gb[j].z, gb[j].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sc[j][e] = stab[gg[e]];
+      rs[j][e] = rtab[gg[e]];
+      g1[j][e] = gg[e] >= ap.nsub[0];
+    }
+  }
+  for (int r = 0; r < rows; r += 4) {
+    float4 v[4][J];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+        v[rr][j] = A[(m0 + min(r + rr, rows - 1)) * lda4 + min(tid + 256 * j, K4 - 1)];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      if (r + rr >= rows) break;
+      uint8_t* row = codes + (r + rr) * ap.Kp;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        if (tid + 256 * j >= K4) break;
+        const float xs[4] = {v[rr][j].x, v[rr][j].y, v[rr][j].z, v[rr][j].w};
+        const int pp[4] = {p[j].x, p[j].y, p[j].z, p[j].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float t = 0.0f;
+          if (sc[j][e] != 0.0f) {
+            const float ex = xs[e] * rs[j][e];
+            t = __builtin_rintf(ex);
+            if (rs[j][e] == 0.0f || fabsf(fabsf(ex - t) - 0.5f) <= 0x1p-9f)
+              t = __builtin_rintf(__fdiv_rn(xs[e], sc[j][e]));
+            t = fminf(fmaxf(t, g1[j][e] ? lo1 : lo0), g1[j][e] ? hi1 : hi0);
+          }
+          row[pp[e]] = (uint8_t)(int8_t)(int)t;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  write_act_units(codes, rows, m0, ap, packed);
+}
+
 // Block scales a wave keeps in registers: lane l holds s_a[l + 64*i].
 constexpr int kGSubRegs = 4;
 static_assert(kGSubMax <= 64 * kGSubRegs, "every block scale has a lane");
 
-// The 64 x 128 tile of k_gemm (generic loop: containers read at run time)
-// with sub-group scales.  After the last granule of each block the tile
-// folds its int32 sums into fp32, y = y + f(acc >> sh) * s_a[j] (multiply,
-// then add, in block order), and restarts them at 0; the epilogue scales
-// by s_w and rounds to bf16.  With a zero point of 0, acc >> sh is the
-// block's exact sum (the unpack scales removed), which the optional int32
-// dump receives as [block][M][N].
-__global__ __launch_bounds__(256) void k_gemm_g(GemmArgs a) {
+// The 64 x 128 tile of k_gemm with sub-group scales.  After the last
+// granule of each block the tile folds its int32 sums into fp32,
+// y = y + f(acc >> sh) * s_a[j] (multiply, then add, in block order), and
+// restarts them at 0; the epilogue scales by s_w and rounds to bf16.  With
+// a zero point of 0, acc >> sh is the block's exact sum (the unpack scales
+// removed), which the optional int32 dump receives as [block][M][N].
+template <int S, int CA0, int CA1, int CBL, int CBH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+void k_gemm_g(GemmArgs a) {
   constexpr int WFM = 2, NST = 2, BM = 32 * WFM;
-  constexpr int SLOT = gemm_slot(2, 0, 0, 0, 0, WFM);
-  constexpr int ASLOT = gemm_aslot(2, 0, 0, 0, 0, WFM);
+  constexpr int SLOT = gemm_slot(S, CA0, CA1, CBL, CBH, WFM);
+  constexpr int ASLOT = gemm_aslot(S, CA0, CA1, CBL, CBH, WFM);
   __shared__ __align__(16) uint8_t lds[NST * SLOT];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -3009,8 +3145,10 @@ __global__ __launch_bounds__(256) void k_gemm_g(GemmArgs a) {
     bpre[j + 1] = bpre[j] + 16 * bc[j];
   }
   const uint8_t* wtile = a.wd.packed + wblk_off(a.wp, jb0);
+  const int wbytes = (int)(wblk_off(a.wp, jb0 + 8) - wblk_off(a.wp, jb0));
+  const bool tile_lo = jb0 < a.wp.nlo;
 
-  const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
+  const int nsub = ap.nsub[0] + (S == 2 ? ap.nsub[1] : 0);
   float sreg[kGSubRegs];
 #pragma unroll
   for (int i = 0; i < kGSubRegs; ++i) sreg[i] = lane + 64 * i < nsub ? a.s_a[lane + 64 * i] : 0.0f;
@@ -3046,32 +3184,51 @@ __global__ __launch_bounds__(256) void k_gemm_g(GemmArgs a) {
       const int sh = ap.sh[g] + (cshw[jj] & 0x7F);
 #pragma unroll
       for (int i = 0; i < WFM; ++i) {
-        const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = ac[i][jj][r] >> sh;
-          yf[i][jj][r] = __fadd_rn(yf[i][jj][r], __fmul_rn((float)t, sj));
-          if (a.acc) {
+        for (int r = 0; r < 4; ++r)
+          yf[i][jj][r] = __fadd_rn(yf[i][jj][r], __fmul_rn((float)(ac[i][jj][r] >> sh), sj));
+        if (a.acc) {
+          const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
             const int64_t m = m0 + row0 + r;
-            if (m < a.M && cinf[jj].n >= 0) a.acc[((int64_t)j * a.M + m) * a.N + cinf[jj].n] = t;
+            if (m < a.M && cinf[jj].n >= 0)
+              a.acc[((int64_t)j * a.M + m) * a.N + cinf[jj].n] = ac[i][jj][r] >> sh;
           }
         }
         ac[i][jj] = v4i{0, 0, 0, 0};
       }
     }
   };
-  for (int g = 0; g < ap.S; ++g) {
+  auto run_group = [&](auto ca_tag, int g) __attribute__((always_inline)) {
+    constexpr int CA = decltype(ca_tag)::value;
     const int ng = g ? ap.ng[1] : ap.ng[0];
     const int gpg = g ? ap.gsub[1] : ap.gsub[0];
     const int j0 = g ? ap.nsub[0] : 0;
     auto hook = [&](v4i (&ac)[WFM][4], int q) __attribute__((always_inline)) {
       if (q < ng && ((q + 1) % gpg == 0 || q == ng - 1)) fold(ac, g, j0 + q / gpg);
     };
-    gemm_group_any<0, 0, 0, WFM, NST, ASLOT, SLOT>(
-        lds, a.act + (g ? ap.seg_off[1] : ap.seg_off[0]) + (m0 / kBlk) * (g ? ap.mblk_bytes[1] : ap.mblk_bytes[0]),
-        g ? ap.mblk_bytes[1] : ap.mblk_bytes[0], g ? ap.c[1] : ap.c[0], ng, wtile, a.wp.ngt, bc, bpre,
-        g ? ap.ng[0] : 0, acc, tid, lane, wid, wm, wn, hook);
-  }
+    const int64_t mstride = g ? ap.mblk_bytes[1] : ap.mblk_bytes[0];
+    const uint8_t* abase = a.act + (g ? ap.seg_off[1] : ap.seg_off[0]) + (m0 / kBlk) * mstride;
+    const int qbase = g ? ap.ng[0] : 0;
+    if constexpr (CA != 0 && CBL != 0 && CBH != 0) {
+      if (CBL == CBH || tile_lo)
+        gemm_group_fast<CA, CBL, CBL, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ng, wtile, wbytes,
+                                                             a.wp.ngt, bc, bpre, qbase, acc, tid,
+                                                             lane, wid, wm, wn, hook);
+      else
+        gemm_group_fast<CA, CBH, CBH, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ng, wtile, wbytes,
+                                                             a.wp.ngt, bc, bpre, qbase, acc, tid,
+                                                             lane, wid, wm, wn, hook);
+    } else {
+      gemm_group_any<CA, CBL, CBH, WFM, NST, ASLOT, SLOT>(lds, abase, mstride,
+                                                          g ? ap.c[1] : ap.c[0], ng, wtile,
+                                                          a.wp.ngt, bc, bpre, qbase, acc, tid,
+                                                          lane, wid, wm, wn, hook);
+    }
+  };
+  run_group(std::integral_constant<int, CA0>{}, 0);
+  if constexpr (S == 2) run_group(std::integral_constant<int, CA1>{}, 1);
 
   // Epilogue: y * s_w, bf16, staged in LDS in ascending original column
   // order (as in k_gemm), then stored row by row.
@@ -3792,13 +3949,48 @@ hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_
                                     const int32_t* grp_dev, float* partial, float* s_a,
                                     uint8_t* packed, hipStream_t stream) {
   const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
+  const size_t tab = (size_t)nsub * 8;
+  const bool aligned = (K % 4 == 0) && (lda % 4 == 0) && (reinterpret_cast<uintptr_t>(A) % 16 == 0);
+  const int K4 = (int)(K / 4);
+  const int J = (K4 + 255) / 256;
+  if (aligned && J <= 4) {
+    // four rows per workgroup at least, else up to kGAbsParts row ranges
+    const int64_t rpb = std::max<int64_t>(4, (M + kGAbsParts - 1) / kGAbsParts);
+    const int nparts = (int)((M + rpb - 1) / rpb);
+    const float4* A4 = reinterpret_cast<const float4*>(A);
+    const int4* g4 = reinterpret_cast<const int4*>(grp_dev);
+    const int4* p4 = reinterpret_cast<const int4*>(pos_dev);
+#define SONIQ_GABS(J_)                                                                              \
+  hipLaunchKernelGGL(k_gabsmax4<J_>, dim3((unsigned)nparts), dim3(256), (size_t)nsub * 4, stream, A4, \
+                     M, K4, lda / 4, rpb, g4, nsub, partial)
+    if (J == 1) SONIQ_GABS(1); else if (J == 2) SONIQ_GABS(2); else if (J == 3) SONIQ_GABS(3); else SONIQ_GABS(4);
+#undef SONIQ_GABS
+    hipLaunchKernelGGL(k_gscales, dim3((unsigned)nsub), dim3(256), 0, stream, partial, nparts, nsub,
+                       ap, s_a);
+    const int R = 8 * (size_t)ap.Kp + tab <= 64 * 1024 ? 8 : 4;
+    if (R * (size_t)ap.Kp + tab <= 64 * 1024) {
+      const size_t lds = R * (size_t)ap.Kp + tab;
+      const dim3 grid((unsigned)((M + R - 1) / R));
+#define SONIQ_GQ(R_, J_) \
+  hipLaunchKernelGGL((k_gquant4<R_, J_>), grid, dim3(256), lds, stream, A4, M, K4, lda / 4, p4, g4, ap, nsub, s_a, packed)
+      if (R == 8) {
+        if (J == 1) SONIQ_GQ(8, 1); else if (J == 2) SONIQ_GQ(8, 2); else if (J == 3) SONIQ_GQ(8, 3); else SONIQ_GQ(8, 4);
+      } else {
+        if (J == 1) SONIQ_GQ(4, 1); else if (J == 2) SONIQ_GQ(4, 2); else if (J == 3) SONIQ_GQ(4, 3); else SONIQ_GQ(4, 4);
+      }
+#undef SONIQ_GQ
+      return hipGetLastError();
+    }
+    hipLaunchKernelGGL(k_gquant<1>, dim3((unsigned)M), dim3(256), (size_t)ap.Kp + tab, stream, A, M,
+                       K, lda, pos_dev, grp_dev, ap, nsub, s_a, packed);
+    return hipGetLastError();
+  }
   const int64_t rpb = std::max<int64_t>(8, (M + kGAbsParts - 1) / kGAbsParts);
   const int nparts = (int)((M + rpb - 1) / rpb);
   hipLaunchKernelGGL(k_gabsmax, dim3((unsigned)nparts), dim3(256), (size_t)nsub * 4, stream, A, M, K,
                      lda, rpb, grp_dev, nsub, partial);
   hipLaunchKernelGGL(k_gscales, dim3((unsigned)nsub), dim3(256), 0, stream, partial, nparts, nsub, ap,
                      s_a);
-  const size_t tab = (size_t)nsub * 8;
   if (kBlk * (size_t)ap.Kp + tab <= 64 * 1024)
     hipLaunchKernelGGL(k_gquant<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
                        kBlk * (size_t)ap.Kp + tab, stream, A, M, K, lda, pos_dev, grp_dev, ap, nsub,
@@ -3818,7 +4010,19 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
   a.xcd_tiles = tiles <= 2048;
-  hipLaunchKernelGGL(k_gemm_g, dim3((unsigned)tiles), dim3(256), 0, stream, a);
+  const dim3 grid((unsigned)tiles), blk(256);
+  const int cl = wp.c_lo, ch = wp.c_hi;
+  if (ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8) {
+    if (cl == 4 && ch == 8) hipLaunchKernelGGL((k_gemm_g<2, 4, 8, 4, 8>), grid, blk, 0, stream, a);
+    else if (cl == 2 && ch == 8) hipLaunchKernelGGL((k_gemm_g<2, 4, 8, 2, 8>), grid, blk, 0, stream, a);
+    else if (cl == 1 && ch == 4) hipLaunchKernelGGL((k_gemm_g<2, 4, 8, 1, 4>), grid, blk, 0, stream, a);
+    else if (cl == 2 && ch == 4) hipLaunchKernelGGL((k_gemm_g<2, 4, 8, 2, 4>), grid, blk, 0, stream, a);
+    else hipLaunchKernelGGL((k_gemm_g<2, 4, 8, 0, 0>), grid, blk, 0, stream, a);
+  } else if (ap.S == 2) {
+    hipLaunchKernelGGL((k_gemm_g<2, 0, 0, 0, 0>), grid, blk, 0, stream, a);
+  } else {
+    hipLaunchKernelGGL((k_gemm_g<1, 0, 0, 0, 0>), grid, blk, 0, stream, a);
+  }
   return hipGetLastError();
 }
 
