@@ -216,8 +216,28 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
-def roofline(case, alg, r):
+def fused_one_row(case) -> bool:
+    """Whether soniq_quantize_mp_gemm runs the step as one k_gemv_fused
+    launch (its documented conditions: one row, one scale per precision
+    group, the narrow group in 4-bit containers and the wide one, if any,
+    in bytes, no 1-bit group, K a multiple of 4 up to 4096)."""
+    if case["M"] != 1 or case.get("act_group_bits", 0):
+        return False
+    widths = sorted(set(int(b) for b in case["a_bits"]))
+    return (case["K"] % 4 == 0 and case["K"] <= 4096 and 3 <= widths[0] <= 4
+            and (len(widths) == 1 or widths[1] >= 5))
+
+
+def roofline(case, alg, r, steps):
     """Roofline of the dominant kernel of one step."""
+    if fused_one_row(case):
+        # the step is one launch: the row's quantization and the GEMV
+        t = r["total_ms"] / steps * 1e-3
+        byt = alg["a_fp32"] + alg["w_packed"] + alg["w_side"] + alg["y"]
+        ach = byt / t / 1e9
+        return dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=ach / HBM_PEAK_GBS, traffic=measured_traffic("k_gemv_fused", case["name"]),
+                    kernel="k_gemv_fused", algorithmic_bytes=byt, launch_us=t * 1e6)
     if r["q_ms"] >= r["g_ms"]:
         kernel = "soniq_quantize_act"
         byt = alg["a_fp32"] + alg["a_packed"]
@@ -344,7 +364,7 @@ def main():
                    "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
                    "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input
                              else "soniq_quantize_mp_gemm")},
-        "roofline": roofline(case, alg, r),
+        "roofline": roofline(case, alg, r, args.steps),
         "breakdown_ms": {"quantize_act": r["q_ms"], "mp_gemm": r["g_ms"],
                          "pack_weights_once": r["pack_ms"]},
         "gemm_tops": alg["ops"] / (r["g_ms"] * 1e-3) / 1e12,
