@@ -68,6 +68,7 @@ SHAPES = [  # (M, N, K, a_lo, a_hi, w_lo, w_hi, a_signed, group_bits)
     (1, 64, 64, 8, 8, 8, 8, True, 512),         # one block
     (1030, 70, 333, 4, 7, 2, 8, True, 1536),    # blocks of 3 granules, ragged 16-row block
     (20, 64, 15000, 8, 8, 4, 4, True, 512),     # 235 blocks
+    (24, 130, 16384, 8, 8, 2, 8, True, 512),    # 256 blocks: the most a handle takes
 ]
 
 

@@ -193,6 +193,23 @@ def test_strides_and_unaligned_rows():
     compare_full(gpu_run(case, ldw_pad=1, lda_pad=1, ldy_pad=1), oracle_run(case))
 
 
+@pytest.mark.parametrize("extreme", [False, True], ids=["random", "all_max"])
+def test_largest_padded_k(extreme):
+    """K at the accumulator limit (65472 8-bit channels, padded K 65472 <=
+    SONIQ_MAX_K): every code at its maximum gives ACC = 127*127*K, just
+    under 2^31 / 2; the quantizer and GEMM take their wide-row forms."""
+    M, N, K = 20, 130, 65472
+    case = workloads.generic(M, N, K, a_lo=8, a_hi=8, a_frac_lo=1.0, w_lo=8, w_hi=8,
+                             w_frac_lo=1.0, a_signed=True, seed=77, name="kmax")
+    if extreme:
+        case["A"][:] = 1.0
+        case["W"][:] = 0.5
+    g, r = gpu_run(case), oracle_run(case)
+    if extreme:
+        assert r["acc"].max() == 127 * 127 * K
+    compare_full(g, r)
+
+
 def test_zero_inputs():
     case = workloads.generic(40, 70, 100, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=1, w_hi=4,
                              w_frac_lo=0.5, seed=9, name="zeros")
