@@ -251,6 +251,39 @@ typedef struct {
 soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
 
 /*
+ * soniq_mp_gemm_quantize_next -- soniq_mp_gemm whose epilogue also
+ * quantizes its outputs as the next layer's activations, so that layer
+ * needs no soniq_quantize_act call and no fp32 (or bf16) copy of them is
+ * read back.  Passages: Sec. 4 fuses quantization into the operation that
+ * produces the activations, to cut memory traffic; codec items 1-2 with
+ * static (calibrated) group scales in place of the batch maximum.
+ *
+ *   act, w   as for soniq_mp_gemm (act quantized, made for w).
+ *   next     an activation handle of the next layer's weights, whose K
+ *            equals this layer's N; act's M must not exceed its max_M.
+ *   s_next   host float [S of the next layer's weights]: the static scale
+ *            of each next-layer activation group (narrow width first),
+ *            finite and >= 0.  Copied during the call.
+ *   Y_dev    as for soniq_mp_gemm, or NULL to skip storing Y.
+ *   ldy, acc_dev  as for soniq_mp_gemm.
+ * Each output's code is taken from the fp32 value the epilogue rounds to
+ * bf16 (before that rounding): code = clamp(rint(y / s_next[g]), lo, hi)
+ * of its next-layer group g, exactly as soniq_quantize_act would with that
+ * scale.  On return (stream order) `next` holds M packed rows and its
+ * scales are s_next, ready for soniq_mp_gemm(next, next's weights).
+ * Every batch size runs the MFMA tiles.  The first call with a given
+ * (weights, next) pair allocates next's code image (max_M rows of its
+ * padded K, bytes) and a column table, synchronously; later calls with the
+ * same pair allocate nothing.
+ * Errors: INVALID_ARGUMENT (null, mismatched handles or sizes, bad
+ * scales), UNSUPPORTED (weights with sub-group activation scales on either
+ * side), OUT_OF_MEMORY, HIP.
+ */
+soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
+                                         const float* s_next, uint16_t* Y_dev, int64_t ldy,
+                                         int32_t* acc_dev, void* stream);
+
+/*
  * soniq_plan_input_channels -- the input-channel plan for a_bits, computed
  * on the host (no device needed): pos[k] receives the position of input
  * channel k in the packed, group-ordered and padded channel axis (group 0,

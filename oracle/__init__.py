@@ -19,7 +19,11 @@ the paper it follows:
   group-wise activation normalization of the transformer setup, Sec. 5).
 * ``mac`` -- integer multiply-accumulate, one int32 sum per activation group
   or sub-group (Alg. 1, Phase II integer forward).
-* ``epilogue_ref`` -- y = bf16(s_w * sum_g s_a[g] * ACC[g]) in fp64.
+* ``quantize_act_static`` -- the same codes with caller-given (calibrated)
+  group scales: what a producing kernel can quantize its own outputs with
+  (Sec. 4 fuses quantization into the preceding operation).
+* ``epilogue_ref`` -- y = bf16(s_w * sum_g s_a[g] * ACC[g]) in fp64;
+  ``epilogue_replay_f32`` the fixed-order fp32 value before rounding.
 * ``run`` -- the whole path.
 """
 from __future__ import annotations
@@ -86,6 +90,10 @@ def lib():
         L.orc_epilogue_ref.argtypes = [vp, vp, vp, i64, i64, i32, vp]
         L.orc_epilogue_replay.restype = None
         L.orc_epilogue_replay.argtypes = [vp, vp, vp, i64, i64, i32, vp]
+        L.orc_epilogue_replay_f32.restype = None
+        L.orc_epilogue_replay_f32.argtypes = [vp, vp, vp, i64, i64, i32, vp]
+        L.orc_quantize_act_static.restype = i32
+        L.orc_quantize_act_static.argtypes = [vp, i64, i64, i64, vp, i32, vp, vp]
         L.orc_container.restype = i32
         L.orc_container.argtypes = [i32]
         L.orc_pack.restype = i64
@@ -238,6 +246,31 @@ def epilogue_replay(acc, s_a, s_w):
     y = np.empty((M, N), np.uint16)
     lib().orc_epilogue_replay(_p(acc), _p(sa), _p(sw), M, N, S, _p(y))
     return y
+
+
+def epilogue_replay_f32(acc, s_a, s_w):
+    """The fixed-order fp32 epilogue value before its bf16 rounding."""
+    acc = _c(acc, np.int32)
+    S, M, N = acc.shape
+    sa = _c(s_a, np.float32)
+    sw = _c(s_w, np.float32)
+    y = np.empty((M, N), np.float32)
+    lib().orc_epilogue_replay_f32(_p(acc), _p(sa), _p(sw), M, N, S, _p(y))
+    return y
+
+
+def quantize_act_static(A, a_bits, a_signed: bool, s_a):
+    """Codes of A[M,K] with the caller's group scales (one per precision
+    group, narrow width first) instead of the batch maximum."""
+    A = _c(A, np.float32)
+    M, K = A.shape
+    ab = _c(a_bits, np.uint8)
+    sa = _c(s_a, np.float32)
+    q = np.empty((M, K), np.int32)
+    S = lib().orc_quantize_act_static(_p(A), M, K, K, _p(ab), 1 if a_signed else 0, _p(sa), _p(q))
+    if S < 0 or sa.shape[0] < S:
+        raise ValueError("bad widths or too few scales")
+    return q
 
 
 def container(bits: int) -> int:

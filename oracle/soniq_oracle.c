@@ -349,6 +349,52 @@ void orc_epilogue_replay(const int32_t* acc, const float* s_a, const float* s_w,
     }
 }
 
+/* Replay value before the bf16 rounding: the fp32 number the fixed-order
+ * epilogue produces, y_f32[m,n]. */
+void orc_epilogue_replay_f32(const int32_t* acc, const float* s_a, const float* s_w,
+                             int64_t M, int64_t N, int S, float* y) {
+  int64_t m;
+#pragma omp parallel for schedule(static)
+  for (m = 0; m < M; ++m)
+    for (int64_t n = 0; n < N; ++n) {
+      float t = (float)acc[m * N + n] * s_a[0];
+      for (int g = 1; g < S; ++g) {
+        float u = (float)acc[((int64_t)g * M + m) * N + n] * s_a[g];
+        t = t + u;
+      }
+      y[m * N + n] = t * s_w[n];
+    }
+}
+
+/* --------------------------------------------------------------- O4/O5 ---
+ * Activation codes with static (calibrated) group scales s_a[g] given by
+ * the caller instead of the batch maximum (the quantizer a producing
+ * kernel can run on its own outputs, Sec. 4's fusion of quantization into
+ * the preceding operation): q_a[m,k] = code(A[m,k], s_a[seg_of[k]]),
+ * clamped to the width's range.  Returns S, or -1 on bad widths.
+ */
+int orc_quantize_act_static(const float* A, int64_t M, int64_t K, int64_t lda,
+                            const uint8_t* a_bits, int a_signed, const float* s_a,
+                            int32_t* q_a) {
+  uint8_t seg_bits[2];
+  uint8_t* seg_of = (uint8_t*)malloc((size_t)(K > 0 ? K : 1));
+  int S = orc_segments(a_bits, K, seg_bits, seg_of);
+  if (S < 0) {
+    free(seg_of);
+    return -1;
+  }
+  int mode = a_signed ? ORC_SIGNED : ORC_UNSIGNED;
+  int64_t m;
+#pragma omp parallel for schedule(static)
+  for (m = 0; m < M; ++m)
+    for (int64_t k = 0; k < K; ++k) {
+      int g = seg_of[k];
+      q_a[m * K + k] = orc_code(A[m * lda + k], s_a[g], seg_bits[g], mode);
+    }
+  free(seg_of);
+  return S;
+}
+
 /* ------------------------------------------------------------------ O8 ---
  * Canonical dense packing of a run of codes, used to account bytes: element
  * j occupies bits [(j mod 32/c)*c, +c) of 32-bit word floor(j*c/32), with

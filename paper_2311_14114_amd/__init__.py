@@ -31,6 +31,7 @@ EXPORTED = [
     "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_pack_weights_grouped",
     "soniq_act_create",
     "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_quantize_mp_gemm",
+    "soniq_mp_gemm_quantize_next",
     "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
     "soniq_act_unpack_debug", "soniq_weights_destroy", "soniq_act_destroy",
@@ -83,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_quantize_act_conv3x3.argtypes = [vp, vp, i64, i64, i64, i64, vp]
         L.soniq_mp_gemm.restype = st
         L.soniq_mp_gemm.argtypes = [vp, vp, vp, i64, vp, vp]
+        L.soniq_mp_gemm_quantize_next.restype = st
+        L.soniq_mp_gemm_quantize_next.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp]
         L.soniq_quantize_mp_gemm.restype = st
         L.soniq_quantize_mp_gemm.argtypes = [vp, vp, vp, i64, i64, vp, i64, vp, vp]
         L.soniq_weights_info.restype = st
@@ -264,6 +267,33 @@ def soniq_quantize_mp_gemm(act: Activations, weights: Weights, A, out=None, acc=
                                         _dev(out, "bf16"), out.stride(0), accp, _stream(stream)))
     act.M = M
     return out
+
+def soniq_mp_gemm_quantize_next(act: Activations, weights: Weights, next_act: Activations,
+                                s_next, out=None, acc=None, stream=None):
+    """soniq_mp_gemm(act, weights) whose epilogue also quantizes the outputs
+    into next_act with the static group scales s_next (one per next-layer
+    activation group).  out=None skips Y; returns out."""
+    import torch
+    M, N = act.M, weights.N
+    sn = np.ascontiguousarray(np.asarray(s_next, np.float32).ravel())
+    if sn.shape[0] < next_act.weights.info.S:
+        raise ValueError("one static scale per next-layer activation group")
+    outp, ldy = None, N
+    if out is not None:
+        if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or out.shape[0] < M:
+            raise TypeError("out must be a bf16 [M, >=N] device tensor with unit column stride")
+        outp, ldy = _dev(out, "bf16"), out.stride(0)
+    accp = None
+    if acc is not None:
+        if acc.dtype != torch.int32 or not acc.is_contiguous() or tuple(acc.shape) != (weights.S, M, N):
+            raise TypeError("acc must be a contiguous int32 [S, M, N] device tensor")
+        accp = _dev(acc, "int32")
+    _check(lib().soniq_mp_gemm_quantize_next(act.handle, weights.handle, next_act.handle,
+                                             sn.ctypes.data_as(ctypes.c_void_p), outp, ldy, accp,
+                                             _stream(stream)))
+    next_act.M = M
+    return out
+
 
 def soniq_weights_info(weights: Weights) -> WeightsInfo:
     info = WeightsInfo()

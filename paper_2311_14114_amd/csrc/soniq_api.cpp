@@ -16,6 +16,8 @@
 // kernel derives any block's container and byte offset from the plan alone
 // (WPlan::nlo, c_lo, c_hi, ngt) without reading a table.
 #include <algorithm>
+#include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -55,6 +57,7 @@ soniq_status fail_hip(hipError_t e, const char* what) {
 
 constexpr uint32_t kMagicW = 0x57514E53u;  // live weights handle
 constexpr uint32_t kMagicA = 0x41514E53u;  // live activation handle
+std::atomic<uint64_t> g_serial{1};          // weights handles, in creation order
 constexpr uint32_t kDead = 0xDEADBEEFu;
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -194,6 +197,7 @@ struct soniq_weights_s {
   int32_t* pos = nullptr;
   uint8_t* seg = nullptr;
   // sub-group activation scales (0 bits: one scale per precision group)
+  uint64_t serial = 0;  // unique per handle (tables built for it are keyed by it)
   int act_group_bits = 0;
   int gsub[2] = {0, 0};   // granules per block
   int nsub[2] = {0, 0};   // blocks per precision group
@@ -213,6 +217,12 @@ struct soniq_act_s {
   float* partial = nullptr;
   unsigned int* counter = nullptr;  // kActStateWords words: the single-pass quantizer's grid state
   float* s_a = nullptr;
+  // filled by soniq_mp_gemm_quantize_next from the producing layer: its
+  // outputs' codes as bytes [M_alloc][Kp] (padding positions stay 0), and
+  // the producer's per-physical-column table (position | group << 16)
+  uint8_t* qn_img = nullptr;
+  int32_t* qn_tab = nullptr;
+  uint64_t qn_serial = 0;  // the producer weights the table was built for
 };
 
 namespace {
@@ -529,6 +539,7 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
     free_weights(w);
     return rc;
   }
+  w->serial = g_serial.fetch_add(1);
   w->magic = kMagicW;
   *out = w;
   return SONIQ_OK;
@@ -721,6 +732,69 @@ soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float*
   return soniq_mp_gemm(act, w, Y_dev, ldy, acc_dev, stream);
 }
 
+soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
+                                         const float* s_next, uint16_t* Y_dev, int64_t ldy,
+                                         int32_t* acc_dev, void* stream) {
+  if (!live_a(act) || !live_w(w) || !live_a(next) || !s_next)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: bad handle or null");
+  if (act->w != w)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_mp_gemm_quantize_next: activation handle belongs to other weights");
+  if (act->M < 1)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: no activations quantized yet");
+  const soniq_weights w2 = next->w;
+  if (w2->K != w->N)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_mp_gemm_quantize_next: next layer has K=%lld, this layer N=%lld",
+                (long long)w2->K, (long long)w->N);
+  const int64_t M = act->M;
+  if (M > next->max_M)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: M=%lld > next max_M=%lld",
+                (long long)M, (long long)next->max_M);
+  if (Y_dev && ldy < w->N)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: ldy < N");
+  if (w->act_group_bits || w2->act_group_bits)
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_mp_gemm_quantize_next: weights with sub-group activation scales");
+  for (int g = 0; g < w2->kp.S; ++g)
+    if (!(s_next[g] >= 0.0f) || !std::isfinite(s_next[g]))
+      return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                  "soniq_mp_gemm_quantize_next: static scale %d is negative or not finite", g);
+  const int64_t tiles = ((M + 63) / 64) * (w->wp.Np / kGemmBN);
+  if (tiles > 0x7FFFFFFFLL)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm_quantize_next: problem too large for one launch");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (!next->qn_img || next->qn_serial != w->serial) {
+    // first use of this (producer, next) pair: the code image and the
+    // producer's column table, built synchronously
+    if (!next->qn_img) {
+      uint8_t* img = nullptr;
+      const size_t bytes = (size_t)(next->M_alloc * w2->kp.Kp);
+      HIP_TRY(dev_alloc(&img, bytes));
+      const hipError_t e = hipMemset(img, 0, bytes);
+      if (e != hipSuccess) {
+        (void)hipFree(img);
+        return fail_hip(e, "soniq_mp_gemm_quantize_next: hipMemset");
+      }
+      next->qn_img = img;
+    }
+    std::vector<int32_t> tab((size_t)w->wp.Np, -1);
+    for (int64_t n = 0; n < w->N; ++n)
+      tab[w->phys_h[n]] = w2->kp.pos[n] | ((int32_t)w2->kp.seg[n] << 16);
+    (void)hipFree(next->qn_tab);
+    next->qn_tab = nullptr;
+    HIP_TRY(dev_alloc(&next->qn_tab, tab.size()));
+    HIP_TRY(hipMemcpy(next->qn_tab, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    next->qn_serial = w->serial;
+  }
+  const float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
+  HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                               acc_dev, next->qn_img, next->qn_tab, next->ap, s2, next->s_a,
+                               next->packed, st));
+  next->M = M;
+  return SONIQ_OK;
+}
+
 soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* s_w) {
   if (!live_w(w)) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_weights_unpack_debug: bad handle");
   HIP_TRY(hipDeviceSynchronize());
@@ -777,6 +851,8 @@ void soniq_act_destroy(soniq_act act) {
   (void)hipFree(act->partial);
   (void)hipFree(act->counter);
   (void)hipFree(act->s_a);
+  (void)hipFree(act->qn_img);
+  (void)hipFree(act->qn_tab);
   act->magic = kDead;
   soniq_weights w = act->w;
   delete act;

@@ -160,6 +160,17 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
                                   const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
                                   uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);
 
+// The GEMM whose epilogue also quantizes its outputs for the next layer
+// with static scales s_next (host, one per next-layer group): codes go to
+// the byte image img[m*ap2.Kp + position] (qtab[physical column] =
+// position | group << 16), then k_pack_img writes them as the next
+// handle's packed rows and its scales.  Y may be null.
+hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
+                                int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
+                                const ActPlan& ap2, const float s_next[2], float* s_a2,
+                                uint8_t* packed2, hipStream_t stream);
+
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);

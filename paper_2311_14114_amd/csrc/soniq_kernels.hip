@@ -1376,6 +1376,33 @@ __global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, i
 }
 
 // ------------------------------------------------------------ GEMM/GEMV --
+// Quantizer of the next layer's activation groups with static scales.
+struct QNext {
+  float s[2], rs[2];  // scale; its reciprocal, or 0 where the exact division decides
+  float lo[2], hi[2];
+  int zp[2], sign1[2];
+};
+
+// Stored next-layer code (code minus the zero point) of an fp32 output y
+// in group g: the per-group quantizer's rule with the given scale.
+__device__ __forceinline__ uint8_t qnext_code(float y, int g, const QNext& q) {
+  const float sc = g ? q.s[1] : q.s[0];
+  const float rs = g ? q.rs[1] : q.rs[0];
+  int code;
+  if (g ? q.sign1[1] : q.sign1[0]) {
+    code = y < 0.0f ? -1 : 1;
+  } else if (sc == 0.0f) {
+    code = 0;
+  } else {
+    const float e = y * rs;
+    float t = __builtin_rintf(e);
+    if (rs == 0.0f || fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f) t = __builtin_rintf(__fdiv_rn(y, sc));
+    t = fminf(fmaxf(t, g ? q.lo[1] : q.lo[0]), g ? q.hi[1] : q.hi[0]);
+    code = (int)t;
+  }
+  return (uint8_t)(int8_t)(code - (g ? q.zp[1] : q.zp[0]));
+}
+
 struct GemmArgs {
   const uint8_t* act;
   const float* s_a;
@@ -1395,6 +1422,14 @@ struct GemmArgs {
   float* s_a_out;
   uint8_t* act_out;
   int K4, xs_bytes;
+  // quantization of the outputs for the next layer (k_gemm<..., true>):
+  // the next layer's stored codes as bytes, qn_img[m*qn_ld + position],
+  // qn_tab[physical column] = position | group << 16 (-1 if empty), and the
+  // quantizer of each of its groups with its static scale
+  uint8_t* qn_img;
+  const int32_t* qn_tab;
+  int qn_ld;
+  QNext qn;
 };
 
 // 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
@@ -1919,8 +1954,10 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
   bar_nofence();
 }
 
-// (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).
-template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST>
+// (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).  QN:
+// the epilogue also quantizes every output for the next layer into qn_img
+// (and stores Y only when a.Y is set).
+template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, bool QN = false>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   constexpr int BM = 32 * WFM;
   constexpr int SLOT = gemm_slot(S, CA0, CA1, CBL, CBH, WFM);
@@ -2061,10 +2098,21 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
             }
           }
         }
+        if constexpr (QN) {
+          // the next layer's code of each output, at its planned position
+          const int qt = a.qn_tab[pc];
+          const int qpos = qt & 0xFFFF, qg = (qt >> 16) & 1;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int64_t m = m0 + row0 + r + h;
+            if (m < a.M) a.qn_img[m * a.qn_ld + qpos] = qnext_code(y[h], qg, a.qn);
+          }
+        }
       }
     }
   }
   __syncthreads();
+  if (QN && !a.Y) return;
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
     const int mrem = (int)min((int64_t)BM, a.M - m0);
@@ -2872,6 +2920,45 @@ bool launch_act_coop(const float* A, int64_t M, int64_t K, int64_t lda, const Ac
     if (done) return true;
   }
   return false;
+}
+
+// ------------------------------------------------------------ k_pack_img --
+// The next layer's packed rows from the byte image the GEMM's epilogue
+// wrote (stored codes at planned positions; padding positions stay 0):
+// R rows per workgroup go to LDS and out as units, whole 16-byte pieces
+// for a full 16-row block without 1-bit groups.  Workgroup 0 also stores
+// the static scales.  Dynamic LDS: R*Kp bytes.
+template <int R>
+__global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ img, int64_t M,
+                                                  ActPlan ap, float s0, float s1,
+                                                  float* __restrict__ s_a,
+                                                  uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  const int64_t m0 = (int64_t)blockIdx.x * R;
+  const int rows = (int)min((int64_t)R, M - m0);
+  const int n16 = rows * ap.Kp / 16;
+  const uint4* src = reinterpret_cast<const uint4*>(img + m0 * ap.Kp);
+  for (int i = threadIdx.x; i < n16; i += 256) reinterpret_cast<uint4*>(codes)[i] = src[i];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    s_a[0] = s0;
+    s_a[1] = s1;
+  }
+  __syncthreads();
+  const bool one_bit = ap.c[0] == 1 || (ap.S == 2 && ap.c[1] == 1);
+  if (R == kBlk && rows == kBlk && !one_bit) {
+    for (int gi = 0; gi < ap.S; ++gi) {
+      const int c = gi ? ap.c[1] : ap.c[0];
+      const int ng = gi ? ap.ng[1] : ap.ng[0];
+      const int gbase = gi ? ap.kpad[0] : 0;
+      uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
+                     (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
+      if (c == 8) write_block_pieces<8, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
+      else if (c == 4) write_block_pieces<4, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
+      else write_block_pieces<2, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
+    }
+  } else {
+    write_act_units(codes, rows, m0, ap, packed);
+  }
 }
 
 // ------------------------------------------------------ sub-group scales --
@@ -3798,6 +3885,10 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.act_out = nullptr;
   a.K4 = 0;
   a.xs_bytes = 0;
+  a.qn_img = nullptr;
+  a.qn_tab = nullptr;
+  a.qn_ld = 0;
+  a.qn = QNext{};
   return a;
 }
 
@@ -3850,6 +3941,61 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
   } else {
     launch_gemm_t<1, 0, 0, 0, 0>(a, M, shape, stream);
   }
+  return hipGetLastError();
+}
+
+// The GEMM with the next layer's quantization in its epilogue (64 x 128
+// tiles at every batch size), then the packing of that layer's rows.
+template <int S, int CA0, int CA1, int CBL, int CBH>
+static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, true>), dim3((unsigned)(((M + 63) / 64) * ntn)),
+                     dim3(256), 0, stream, a);
+}
+
+hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
+                                int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
+                                const ActPlan& ap2, const float s_next[2], float* s_a2,
+                                uint8_t* packed2, hipStream_t stream) {
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
+  a.xcd_tiles = tiles <= 2048;
+  a.qn_img = img;
+  a.qn_tab = qtab;
+  a.qn_ld = ap2.Kp;
+  for (int g = 0; g < 2; ++g) {
+    const float sc = g < ap2.S ? s_next[g] : 0.0f;
+    a.qn.s[g] = sc;
+    // the reciprocal shortcut under the same range rule as the device
+    // quantizers; IEEE division is within half an ulp of 1/s
+    a.qn.rs[g] = (sc >= 0x1p-100f && sc <= 0x1p100f) ? 1.0f / sc : 0.0f;
+    a.qn.lo[g] = (float)ap2.q[g].lo;
+    a.qn.hi[g] = (float)ap2.q[g].hi;
+    a.qn.zp[g] = ap2.zp[g];
+    a.qn.sign1[g] = ap2.q[g].sign1;
+  }
+  const int cl = wp.c_lo, ch = wp.c_hi;
+  if (ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8) {
+    if (cl == 4 && ch == 8) launch_gemm_qn_t<2, 4, 8, 4, 8>(a, M, stream);
+    else if (cl == 2 && ch == 8) launch_gemm_qn_t<2, 4, 8, 2, 8>(a, M, stream);
+    else if (cl == 1 && ch == 4) launch_gemm_qn_t<2, 4, 8, 1, 4>(a, M, stream);
+    else if (cl == 2 && ch == 4) launch_gemm_qn_t<2, 4, 8, 2, 4>(a, M, stream);
+    else launch_gemm_qn_t<2, 4, 8, 0, 0>(a, M, stream);
+  } else if (ap.S == 2) {
+    launch_gemm_qn_t<2, 0, 0, 0, 0>(a, M, stream);
+  } else {
+    launch_gemm_qn_t<1, 0, 0, 0, 0>(a, M, stream);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const float s0 = s_next[0], s1 = ap2.S == 2 ? s_next[1] : 0.0f;
+  if (kBlk * (size_t)ap2.Kp <= 64 * 1024)
+    hipLaunchKernelGGL(k_pack_img<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
+                       kBlk * (size_t)ap2.Kp, stream, img, M, ap2, s0, s1, s_a2, packed2);
+  else
+    hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)M), dim3(256), (size_t)ap2.Kp, stream, img, M,
+                       ap2, s0, s1, s_a2, packed2);
   return hipGetLastError();
 }
 

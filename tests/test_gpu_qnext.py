@@ -1,0 +1,107 @@
+"""GPU parity of quantization fused into the producing GEMM
+(soniq_mp_gemm_quantize_next; Sec. 4 fuses quantization into the operation
+that produces the activations): the next layer's codes equal the oracle's
+static-scale codes of this layer's fp32 outputs (before their bf16
+rounding), its scales are the static ones, and the next layer's GEMM on
+them matches the oracle bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2311_14114_amd as sq
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16_bits(t):
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def chain(M, K1, N1, N2, a1, w1, a2, w2, a2_signed, seed, scale_mul=1.0, with_y=True):
+    l1 = workloads.generic(M, N1, K1, a_lo=a1[0], a_hi=a1[1], a_frac_lo=0.6, w_lo=w1[0],
+                           w_hi=w1[1], w_frac_lo=0.7, a_signed=True, seed=seed, name="chain1")
+    l2 = workloads.generic(M, N2, N1, a_lo=a2[0], a_hi=a2[1], a_frac_lo=0.7, w_lo=w2[0],
+                           w_hi=w2[1], w_frac_lo=0.5, a_signed=a2_signed, seed=seed + 1,
+                           name="chain2")
+    print(f"[gpu] chain M={M} K1={K1} N1={N1} N2={N2} a2={a2} signed={a2_signed}", flush=True)
+    # oracle: layer 1, its fp32 outputs, static-scale codes for layer 2
+    r1 = oracle.run(l1["A"], l1["W"], l1["a_bits"], l1["w_bits"], True)
+    y1 = oracle.epilogue_replay_f32(r1["acc"], r1["s_a"], r1["s_w"])
+    # calibration: the scales the batch maximum of y1 would give, scaled
+    _, s_cal, _, _ = oracle.quantize_act(y1, l2["a_bits"], a2_signed)
+    s2 = (s_cal * np.float32(scale_mul)).astype(np.float32)
+    q2 = oracle.quantize_act_static(y1, l2["a_bits"], a2_signed, s2)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    S2, seg_bits2, seg_of2 = oracle.segments(l2["a_bits"])
+    acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+    # GPU
+    W1 = torch.from_numpy(l1["W"]).cuda()
+    W2 = torch.from_numpy(l2["W"]).cuda()
+    A1 = torch.from_numpy(l1["A"]).cuda()
+    wh1 = sq.soniq_pack_weights(W1, l1["w_bits"], l1["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(W2, l2["w_bits"], l2["a_bits"], a2_signed)
+    act1 = sq.soniq_act_create(wh1, M)
+    act2 = sq.soniq_act_create(wh2, M)
+    sq.soniq_quantize_act(act1, A1)
+    Y1 = torch.empty((M, N1), dtype=torch.bfloat16, device="cuda") if with_y else None
+    sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, s2, out=Y1)
+    acc = torch.empty((wh2.S, M, N2), dtype=torch.int32, device="cuda")
+    Y2 = sq.soniq_mp_gemm(act2, wh2, acc=acc)
+    torch.cuda.synchronize()
+    g_q2, g_s2 = sq.soniq_act_unpack_debug(act2)
+    np.testing.assert_array_equal(g_s2, s2[:S2])
+    np.testing.assert_array_equal(g_q2, q2)
+    if with_y:
+        np.testing.assert_array_equal(_bf16_bits(Y1), r1["y_replay"])
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+    np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2[:S2], s_w2))
+    return dict(act1=act1, act2=act2, wh1=wh1, wh2=wh2, s2=s2, a_bits2=l2["a_bits"])
+
+
+CHAINS = [  # (M, K1, N1, N2, a1, w1, a2, w2, a2_signed)
+    (64, 256, 256, 128, (4, 8), (2, 4), (4, 8), (2, 8), True),
+    (300, 200, 333, 70, (4, 8), (1, 4), (4, 8), (4, 8), False),   # unsigned next layer (zero point)
+    (1, 128, 130, 64, (4, 8), (2, 8), (3, 6), (2, 4), True),       # one row, 4- and 8-bit containers
+    (17, 96, 500, 100, (8, 8), (8, 8), (1, 8), (1, 4), True),      # 1-bit next-layer group
+    (129, 300, 1000, 64, (4, 8), (2, 8), (2, 8), (2, 8), True),    # 2-bit next-layer group
+    (70, 64, 5000, 16, (4, 8), (2, 4), (4, 8), (2, 4), True),      # 4-row packing (16 rows exceed 64 KB)
+]
+
+
+@pytest.mark.parametrize("c", CHAINS, ids=lambda c: f"M{c[0]}_K{c[1]}_N{c[2]}_a{c[6][0]}{c[6][1]}{'s' if c[8] else 'u'}")
+def test_chain(c):
+    chain(*c, seed=sum(c[:4]))
+
+
+def test_chain_clamps_and_skips_y():
+    """Scales below the calibrated ones clamp the largest outputs; no Y."""
+    chain(200, 256, 384, 96, (4, 8), (2, 8), (4, 8), (2, 8), True, seed=5, scale_mul=0.5,
+          with_y=False)
+
+
+def test_chain_repeat_and_other_producer():
+    """A second call with fewer rows, then a different producer layer (other
+    K, other weights) into the same next handle: its column table is
+    rebuilt and the codes follow the new producer's outputs."""
+    r = chain(150, 128, 256, 64, (4, 8), (2, 4), (4, 8), (2, 8), True, seed=9)
+    A = torch.from_numpy(np.random.default_rng(3).standard_normal((40, 128)).astype(np.float32)).cuda()
+    sq.soniq_quantize_act(r["act1"], A)
+    sq.soniq_mp_gemm_quantize_next(r["act1"], r["wh1"], r["act2"], r["s2"])
+    torch.cuda.synchronize()
+    assert r["act2"].M == 40
+    # another producer: K=96, N=256 (the next layer's K)
+    pb = workloads.generic(33, 256, 96, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.6, a_signed=True, seed=44, name="producer_b")
+    rb = oracle.run(pb["A"], pb["W"], pb["a_bits"], pb["w_bits"], True)
+    yb = oracle.epilogue_replay_f32(rb["acc"], rb["s_a"], rb["s_w"])
+    a_bits2 = r["a_bits2"]
+    qb = oracle.quantize_act_static(yb, a_bits2, True, r["s2"])
+    whb = sq.soniq_pack_weights(torch.from_numpy(pb["W"]).cuda(), pb["w_bits"], pb["a_bits"], True)
+    actb = sq.soniq_act_create(whb, 33)
+    sq.soniq_quantize_act(actb, torch.from_numpy(pb["A"]).cuda())
+    sq.soniq_mp_gemm_quantize_next(actb, whb, r["act2"], r["s2"])
+    torch.cuda.synchronize()
+    g_q, _ = sq.soniq_act_unpack_debug(r["act2"])
+    np.testing.assert_array_equal(g_q, qb)

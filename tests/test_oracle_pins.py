@@ -549,3 +549,38 @@ def test_grouped_epilogue_replay_matches_ref_within_rounding():
     t = t * s_w[None, :]
     np.testing.assert_array_equal(oracle.bf16_to_f32(y2), oracle.bf16_to_f32(
         np.array([[oracle.bf16_from_f32(v) for v in row] for row in t], np.uint16)))
+
+
+# ------------------------------------------- static scales (quantize in a producer)
+@pytest.mark.parametrize("signed", [True, False])
+def test_static_scales_equal_to_the_batch_ones_give_its_codes(signed):
+    """Given the scales the batch maximum produces, the static quantizer
+    returns the pinned dynamic quantizer's codes; halving a scale doubles
+    the pre-clamp ratio, so codes move to the clamp bound where they
+    exceed it and stay within range."""
+    rng = np.random.default_rng(31 + signed)
+    M, K = 11, 333
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    if not signed:
+        A = np.abs(A)
+    ab = np.where(rng.random(K) < 0.6, 4, 8).astype(np.uint8)
+    q, s, sb, so = oracle.quantize_act(A, ab, signed)
+    np.testing.assert_array_equal(oracle.quantize_act_static(A, ab, signed, s), q)
+    q2 = oracle.quantize_act_static(A, ab, signed, s / 2)
+    for g, b in enumerate(sb):
+        top = (2 ** (int(b) - 1) - 1) if signed else (2 ** int(b) - 1)
+        cols = so == g
+        assert np.abs(q2[:, cols]).max() == top
+        big = np.abs(A[:, cols]) / (s[g] / 2) >= top + 0.5
+        assert (np.abs(q2[:, cols])[big] == top).all()
+
+
+def test_replay_f32_rounds_to_the_replay():
+    rng = np.random.default_rng(33)
+    acc = rng.integers(-2 ** 20, 2 ** 20, (2, 17, 23)).astype(np.int32)
+    s_a = np.array([0.013, 0.0007], np.float32)
+    s_w = rng.uniform(1e-3, 1.0, 23).astype(np.float32)
+    y32 = oracle.epilogue_replay_f32(acc, s_a, s_w)
+    yb = oracle.epilogue_replay(acc, s_a, s_w)
+    np.testing.assert_array_equal(
+        np.array([[oracle.bf16_from_f32(v) for v in row] for row in y32], np.uint16), yb)
