@@ -312,6 +312,78 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
+def run_chain(steps, warmup):
+    """Two transformer linears in a row (FFN up, 4096x3072x768, then FFN
+    down, 4096x768x3072), timed two ways, each as `steps` steps captured
+    in one HIP graph: the next layer's activations quantized in the first
+    GEMM's epilogue with static scales (soniq_mp_gemm_quantize_next), and
+    the unfused form (bf16 Y of layer 1, widened to fp32 by torch, then
+    soniq_quantize_act with the batch maximum).  The static scales are
+    calibrated once, untimed, from the unfused form's batch maxima."""
+    import torch
+    import paper_2311_14114_amd as sq
+    import workloads
+
+    torch.cuda.set_device(0)
+    up, down = workloads.xfmr_ffn_up(), workloads.xfmr_ffn_down()
+    M = up["M"]
+    dev = torch.device("cuda")
+    A = torch.from_numpy(up["A"]).to(dev)
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(up["W"]).to(dev), up["w_bits"], up["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(down["W"]).to(dev), down["w_bits"], down["a_bits"],
+                                down["a_signed"])
+    act1, act2 = sq.soniq_act_create(wh1, M), sq.soniq_act_create(wh2, M)
+    Y1 = torch.empty((M, up["N"]), dtype=torch.bfloat16, device=dev)
+    Y1f = torch.empty((M, up["N"]), dtype=torch.float32, device=dev)
+    Y2 = torch.empty((M, down["N"]), dtype=torch.bfloat16, device=dev)
+
+    def unfused():
+        sq.soniq_quantize_act(act1, A)
+        sq.soniq_mp_gemm(act1, wh1, out=Y1)
+        Y1f.copy_(Y1)
+        sq.soniq_quantize_act(act2, Y1f)
+        sq.soniq_mp_gemm(act2, wh2, out=Y2)
+
+    unfused()
+    torch.cuda.synchronize()
+    s2 = sq.soniq_act_unpack_debug(act2)[1].copy()
+
+    def fused():
+        sq.soniq_quantize_act(act1, A)
+        sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, s2)
+        sq.soniq_mp_gemm(act2, wh2, out=Y2)
+
+    fused()  # prepares act2 for this producer (allocates outside the graph)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(steps):
+                fn()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    t_f, t_u = timed(fused), timed(unfused)
+    ops = 2 * M * (up["N"] * up["K"] + down["N"] * down["K"])
+    print(json.dumps({
+        "chain": "xfmr_ffn_up -> xfmr_ffn_down", "M": M, "steps": steps, "warmup": warmup,
+        "fused_us": t_f * 1e3, "unfused_us": t_u * 1e3, "fused_tops": ops / (t_f * 1e-3) / 1e12,
+        "unfused_tops": ops / (t_u * 1e-3) / 1e12, "static_scales": [float(v) for v in s2],
+        "data": "synthetic"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -321,6 +393,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--chain", action="store_true",
+                    help="time FFN up -> FFN down with the next layer quantized in the first "
+                         "GEMM's epilogue, against the unfused form")
     ap.add_argument("--conv-input", action="store_true",
                     help="conv workloads: quantize from the NCHW input tensor "
                          "(soniq_quantize_act_conv3x3) instead of the lowered matrix")
@@ -335,6 +410,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.chain:
+        run_chain(args.steps, args.warmup)
         return
 
     import workloads

@@ -778,9 +778,21 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
       }
       next->qn_img = img;
     }
-    std::vector<int32_t> tab((size_t)w->wp.Np, -1);
-    for (int64_t n = 0; n < w->N; ++n)
-      tab[w->phys_h[n]] = w2->kp.pos[n] | ((int32_t)w2->kp.seg[n] << 16);
+    // [0, Np): next-layer group of each physical column's channel;
+    // [Np, 2 Np): next-layer position of each tile's r-th column in
+    // ascending original order (the order the GEMM stages its outputs in)
+    const int Np = w->wp.Np;
+    std::vector<int32_t> tab(2 * (size_t)Np, -1);
+    std::vector<std::vector<int64_t>> cols(Np / kGemmBN);
+    for (int64_t n = 0; n < w->N; ++n) {
+      const int32_t p = w->phys_h[n];
+      tab[p] = w2->kp.seg[n];
+      cols[p / kGemmBN].push_back(n);
+    }
+    for (size_t t = 0; t < cols.size(); ++t) {
+      std::sort(cols[t].begin(), cols[t].end());
+      for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = w2->kp.pos[cols[t][r]];
+    }
     (void)hipFree(next->qn_tab);
     next->qn_tab = nullptr;
     HIP_TRY(dev_alloc(&next->qn_tab, tab.size()));

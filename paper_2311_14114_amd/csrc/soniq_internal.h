@@ -162,8 +162,9 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
 
 // The GEMM whose epilogue also quantizes its outputs for the next layer
 // with static scales s_next (host, one per next-layer group): codes go to
-// the byte image img[m*ap2.Kp + position] (qtab[physical column] =
-// position | group << 16), then k_pack_img writes them as the next
+// the byte image img[m*ap2.Kp + position] (qtab: [Np] next-layer group per
+// physical column, then [Np] next-layer position per tile column in
+// ascending original order), then k_pack_img writes them as the next
 // handle's packed rows and its scales.  Y may be null.
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,

@@ -1383,24 +1383,40 @@ struct QNext {
   int zp[2], sign1[2];
 };
 
-// Stored next-layer code (code minus the zero point) of an fp32 output y
-// in group g: the per-group quantizer's rule with the given scale.
-__device__ __forceinline__ uint8_t qnext_code(float y, int g, const QNext& q) {
-  const float sc = g ? q.s[1] : q.s[0];
-  const float rs = g ? q.rs[1] : q.rs[0];
-  int code;
-  if (g ? q.sign1[1] : q.sign1[0]) {
-    code = y < 0.0f ? -1 : 1;
-  } else if (sc == 0.0f) {
-    code = 0;
-  } else {
-    const float e = y * rs;
-    float t = __builtin_rintf(e);
-    if (rs == 0.0f || fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f) t = __builtin_rintf(__fdiv_rn(y, sc));
-    t = fminf(fmaxf(t, g ? q.lo[1] : q.lo[0]), g ? q.hi[1] : q.hi[0]);
-    code = (int)t;
-  }
-  return (uint8_t)(int8_t)(code - (g ? q.zp[1] : q.zp[0]));
+// The quantizer of one output column (its next-layer group's), selected
+// once per column; codes by the reciprocal shortcut, with `near` set where
+// the exact division must decide (near a tie, or a scale outside the
+// shortcut's range).
+struct QCol {
+  float sc, rs, lo, hi;
+  int zp;
+  bool sign1;
+};
+
+__device__ __forceinline__ QCol qnext_col(int g, const QNext& q) {
+  QCol c;
+  c.sc = g ? q.s[1] : q.s[0];
+  c.rs = g ? q.rs[1] : q.rs[0];
+  c.lo = g ? q.lo[1] : q.lo[0];
+  c.hi = g ? q.hi[1] : q.hi[0];
+  c.zp = g ? q.zp[1] : q.zp[0];
+  c.sign1 = (g ? q.sign1[1] : q.sign1[0]) != 0;
+  return c;
+}
+
+__device__ __forceinline__ int qnext_fast(float y, const QCol& c, bool& near) {
+  const float e = y * c.rs;
+  const float t = __builtin_rintf(e);
+  const bool plain = !c.sign1 && c.sc != 0.0f;
+  near = plain && (c.rs == 0.0f || fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f);
+  const int code = c.sign1 ? (y < 0.0f ? -1 : 1)
+                           : plain ? (int)__builtin_amdgcn_fmed3f(t, c.lo, c.hi) : 0;
+  return code - c.zp;
+}
+
+__device__ __forceinline__ int qnext_exact(float y, const QCol& c) {
+  const float t = __builtin_rintf(__fdiv_rn(y, c.sc));
+  return (int)__builtin_amdgcn_fmed3f(t, c.lo, c.hi) - c.zp;
 }
 
 struct GemmArgs {
@@ -1423,9 +1439,11 @@ struct GemmArgs {
   uint8_t* act_out;
   int K4, xs_bytes;
   // quantization of the outputs for the next layer (k_gemm<..., true>):
-  // the next layer's stored codes as bytes, qn_img[m*qn_ld + position],
-  // qn_tab[physical column] = position | group << 16 (-1 if empty), and the
-  // quantizer of each of its groups with its static scale
+  // the next layer's stored codes as bytes, qn_img[m*qn_ld + position];
+  // qn_tab[physical column] = the next-layer group of its channel, and
+  // qn_tab[Np + 128*tile + r] = the next-layer position of the tile's r-th
+  // column in ascending original order (-1 past the last); the quantizer
+  // of each next-layer group with its static scale
   uint8_t* qn_img;
   const int32_t* qn_tab;
   int qn_ld;
@@ -1999,6 +2017,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
   ColInfo cinf[4];
   uint8_t cshw[4], crank[4];
+  int cqg[4] = {0, 0, 0, 0};  // next-layer group of each column (QN)
   if constexpr (WFM <= 2) {
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
@@ -2006,6 +2025,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       cinf[jj] = a.wd.colinfo[pc];
       cshw[jj] = a.wd.shw[pc];
       crank[jj] = a.wd.colrank[pc];
+      if constexpr (QN) cqg[jj] = a.qn_tab[pc];
     }
   }
 
@@ -2099,20 +2119,36 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
           }
         }
         if constexpr (QN) {
-          // the next layer's code of each output, at its planned position
-          const int qt = a.qn_tab[pc];
-          const int qpos = qt & 0xFFFF, qg = (qt >> 16) & 1;
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int64_t m = m0 + row0 + r + h;
-            if (m < a.M) a.qn_img[m * a.qn_ld + qpos] = qnext_code(y[h], qg, a.qn);
+          // the next layer's code of each output, staged like Y
+          const QCol qc = qnext_col(WFM <= 2 ? cqg[jj] : a.qn_tab[pc], a.qn);
+          bool n0, n1;
+          int c0 = qnext_fast(y[0], qc, n0), c1 = qnext_fast(y[1], qc, n1);
+          if (__builtin_amdgcn_ballot_w64(n0 || n1) != 0) [[unlikely]] {
+            if (n0) c0 = qnext_exact(y[0], qc);
+            if (n1) c1 = qnext_exact(y[1], qc);
           }
+          uint8_t* qcol = reinterpret_cast<uint8_t*>(lds) + BM * YS * 2 + (WFM <= 2 ? crank[jj] : a.wd.colrank[pc]);
+          qcol[(row0 + r) * YS] = (uint8_t)(int8_t)c0;
+          qcol[(row0 + r + 1) * YS] = (uint8_t)(int8_t)c1;
         }
       }
     }
   }
   __syncthreads();
-  if (QN && !a.Y) return;
+  if constexpr (QN) {
+    // rows of codes, each thread one column of the tile in ascending
+    // original order: consecutive lanes write nearby planned positions
+    static_assert(BM * YS * 3 <= NST * SLOT, "code staging fits the ring");
+    const int qpos = a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))];
+    if (qpos >= 0) {
+      const uint8_t* qs = reinterpret_cast<const uint8_t*>(lds) + BM * YS * 2;
+      const int mrem = (int)min((int64_t)BM, a.M - m0);
+      uint8_t* qout = a.qn_img + m0 * a.qn_ld + qpos;
+      for (int row = tid / kGemmBN; row < mrem; row += 256 / kGemmBN)
+        qout[(int64_t)row * a.qn_ld] = qs[row * YS + (tid & (kGemmBN - 1))];
+    }
+    if (!a.Y) return;
+  }
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
     const int mrem = (int)min((int64_t)BM, a.M - m0);
