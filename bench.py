@@ -64,6 +64,12 @@ def algorithmic(case, info):
     )
 
 
+def sign_nibbles(case) -> bool:
+    """1-bit weight channels are packed in 4-bit containers where the MFMA
+    GEMM runs the layer (cheaper to widen; the GEMV keeps bits)."""
+    return bool((case["w_bits"] == 1).any()) and not uses_gemv(case)
+
+
 def uses_gemv(case) -> bool:
     # sub-group scales run the MFMA tiles at every batch size
     return case["M"] <= 8 and not case.get("act_group_bits", 0)
@@ -84,8 +90,9 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     torch.cuda.synchronize()
     e0.record(stream)
     gbits = case.get("act_group_bits", 0)
+    nib = sign_nibbles(case)
     ws = [sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                act_group_bits=gbits)]
+                                act_group_bits=gbits, sign_nibbles=nib)]
     e1.record(stream)
     torch.cuda.synchronize()
     pack_ms = e0.elapsed_time(e1)
@@ -95,7 +102,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
         nw = max(1, min(MAX_W_COPIES, math.ceil(ROTATE_W_BYTES / int(info.packed_w_bytes))))
     for _ in range(nw - 1):
         ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                        act_group_bits=gbits))
+                                        act_group_bits=gbits, sign_nibbles=nib))
     acts = [sq.soniq_act_create(w, M) for w in ws]
     # the quantizer's input: the lowered matrix A, or (conv_input) the
     # convolution's NCHW tensor X, whose 3x3 lowering A is
@@ -438,6 +445,7 @@ def main():
                    "w_bits": sorted(set(case["w_bits"].tolist())),
                    "a_signed": bool(case["a_signed"]),
                    "act_group_bits": int(case.get("act_group_bits", 0)),
+                   "sign_weights_container": 4 if sign_nibbles(case) else 1,
                    "activation_copies": r["na"], "weight_copies": r["nw"],
                    "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
                    "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input

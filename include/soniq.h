@@ -66,6 +66,15 @@ typedef struct soniq_act_s* soniq_act;
  *       codes in [-2^(b-1), 2^(b-1)-1], step max-abs/2^(b-1). */
 enum { SONIQ_WQ_SYMMETRIC = 0, SONIQ_WQ_TWOS_FRACTION = 1 };
 
+/* Packing flag, OR-ed into wq_mode: store 1-bit (sign, +-1) weight channels
+ * in 4-bit containers instead of single bits.  Same codes and results;
+ * four times those channels' bytes, but on gfx950 a nibble widens to the
+ * int8 MFMA operand in a shift and a mask where a bit takes a dozen
+ * instructions, so batches on the MFMA GEMM (more than 8 rows) run faster.
+ * The batch-1 GEMV, which is bound by weight bytes, is better served by
+ * the default bits. */
+#define SONIQ_WPACK_SIGN_NIBBLES 0x100
+
 /* Largest supported input-channel count (padded): keeps every int32
  * accumulator exact. */
 #define SONIQ_MAX_K 65536
@@ -103,7 +112,8 @@ soniq_status soniq_pack_weights(const float* W_dev, int64_t N, int64_t K, int64_
                                 int a_signed, void* stream, soniq_weights* out);
 
 /* As soniq_pack_weights, with the weight grid chosen by wq_mode
- * (SONIQ_WQ_SYMMETRIC or SONIQ_WQ_TWOS_FRACTION). */
+ * (SONIQ_WQ_SYMMETRIC or SONIQ_WQ_TWOS_FRACTION), optionally OR-ed with
+ * SONIQ_WPACK_SIGN_NIBBLES. */
 soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
                                    const uint8_t* w_bits, const uint8_t* a_bits,
                                    int a_signed, int wq_mode, void* stream,

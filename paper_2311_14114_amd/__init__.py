@@ -24,6 +24,7 @@ SONIQ_ERR_OUT_OF_MEMORY = 3
 SONIQ_ERR_HIP = 4
 SONIQ_WQ_SYMMETRIC = 0
 SONIQ_WQ_TWOS_FRACTION = 1
+SONIQ_WPACK_SIGN_NIBBLES = 0x100
 SONIQ_MAX_K = 65536
 
 # Every symbol include/soniq.h declares.
@@ -173,10 +174,11 @@ class Activations:
 
 
 def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_WQ_SYMMETRIC,
-                       stream=None, act_group_bits: int = 0) -> Weights:
+                       stream=None, act_group_bits: int = 0, sign_nibbles: bool = False) -> Weights:
     """Quantize, re-order and bit-pack W (device float32 [N, K], row-major).
     act_group_bits > 0 gives the activations sub-group scales (blocks of
-    that many bits of storage inside each precision group)."""
+    that many bits of storage inside each precision group); sign_nibbles
+    stores 1-bit channels in 4-bit containers (SONIQ_WPACK_SIGN_NIBBLES)."""
     import torch
     if W.dtype != torch.float32 or W.dim() != 2 or W.stride(1) != 1:
         raise TypeError("W must be a 2-D float32 device tensor with unit column stride")
@@ -188,7 +190,8 @@ def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_W
     _check(lib().soniq_pack_weights_grouped(_dev(W, "float32"), N, K, W.stride(0),
                                             wb.ctypes.data_as(ctypes.c_void_p),
                                             ab.ctypes.data_as(ctypes.c_void_p),
-                                            1 if a_signed else 0, int(wq_mode),
+                                            1 if a_signed else 0,
+                                            int(wq_mode) | (SONIQ_WPACK_SIGN_NIBBLES if sign_nibbles else 0),
                                             int(act_group_bits), _stream(stream),
                                             ctypes.byref(h)))
     return Weights(h, N, K)

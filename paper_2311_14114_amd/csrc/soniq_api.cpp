@@ -66,8 +66,10 @@ int pow2_container(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
 
 // Weight container: 1-bit symmetric channels are sign bits; the Eq. (1)
 // 1-bit grid {-1, 0} is two's complement and needs two bits.
-int w_container(int b, int wq_mode) {
-  if (b == 1) return wq_mode == SONIQ_WQ_TWOS_FRACTION ? 2 : 1;
+// 1-bit sign channels go in bits, or in nibbles when the handle asks for
+// SONIQ_WPACK_SIGN_NIBBLES (cheaper to widen for the MFMA GEMM).
+int w_container(int b, int wq_mode, bool sign_nibbles = false) {
+  if (b == 1) return wq_mode == SONIQ_WQ_TWOS_FRACTION ? 2 : sign_nibbles ? 4 : 1;
   return pow2_container(b);
 }
 
@@ -355,6 +357,8 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
   if (ldw < K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: ldw < K");
   if (a_signed != 0 && a_signed != 1)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: a_signed must be 0 or 1");
+  const bool sign_nibbles = (wq_mode & SONIQ_WPACK_SIGN_NIBBLES) != 0;
+  wq_mode &= ~SONIQ_WPACK_SIGN_NIBBLES;
   if (wq_mode != SONIQ_WQ_SYMMETRIC && wq_mode != SONIQ_WQ_TWOS_FRACTION)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: unknown wq_mode %d", wq_mode);
   int wb[2], nw = 0;
@@ -416,8 +420,8 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
   // Output-channel plan.
   const int b_lo = wb[0], b_hi = nw == 2 ? wb[1] : wb[0];
   WPlan& wp = w->wp;
-  wp.c_lo = w_container(b_lo, wq_mode);
-  wp.c_hi = w_container(b_hi, wq_mode);
+  wp.c_lo = w_container(b_lo, wq_mode, sign_nibbles);
+  wp.c_hi = w_container(b_hi, wq_mode, sign_nibbles);
   wp.ngt = (int)(w->kp.Kp / kGran);
   std::vector<int32_t> rows_lo, rows_hi;
   for (int64_t n = 0; n < N; ++n) (w_bits[n] == b_lo ? rows_lo : rows_hi).push_back((int32_t)n);

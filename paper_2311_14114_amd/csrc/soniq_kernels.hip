@@ -3968,6 +3968,7 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
   a.xcd_tiles = tiles <= 2048;  // a few rounds of two workgroups per CU
   if (ap.S == 2 && ca0 == 4 && ca1 == 8) {
     if (cl == 4 && ch == 8) launch_gemm_t<2, 4, 8, 4, 8>(a, M, shape, stream);
+    else if (cl == 4 && ch == 4) launch_gemm_t<2, 4, 8, 4, 4>(a, M, shape, stream);
     else if (cl == 2 && ch == 8) launch_gemm_t<2, 4, 8, 2, 8>(a, M, shape, stream);
     else if (cl == 1 && ch == 4) launch_gemm_t<2, 4, 8, 1, 4>(a, M, shape, stream);
     else if (cl == 2 && ch == 4) launch_gemm_t<2, 4, 8, 2, 4>(a, M, shape, stream);

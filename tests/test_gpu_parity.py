@@ -20,7 +20,8 @@ def _bf16_bits(t):
     return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def gpu_run(case, wq_mode=0, ldw_pad=0, lda_pad=0, ldy_pad=0, with_acc=True, debug=True):
+def gpu_run(case, wq_mode=0, ldw_pad=0, lda_pad=0, ldy_pad=0, with_acc=True, debug=True,
+            sign_nibbles=False):
     M, N, K = case["M"], case["N"], case["K"]
     print(f"[gpu] {case['name']} M={M} N={N} K={K} wq_mode={wq_mode}", flush=True)
     Wb = torch.zeros((N, K + ldw_pad), dtype=torch.float32, device="cuda")
@@ -28,7 +29,8 @@ def gpu_run(case, wq_mode=0, ldw_pad=0, lda_pad=0, ldy_pad=0, with_acc=True, deb
     Ab = torch.zeros((M, K + lda_pad), dtype=torch.float32, device="cuda")
     Ab[:, :K] = torch.from_numpy(case["A"]).cuda()
     W, A = Wb[:, :K], Ab[:, :K]
-    w = sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"], wq_mode)
+    w = sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"], wq_mode,
+                              sign_nibbles=sign_nibbles)
     act = sq.soniq_act_create(w, M)
     sq.soniq_quantize_act(act, A)
     Yb = torch.empty((M, N + ldy_pad), dtype=torch.bfloat16, device="cuda")
@@ -78,6 +80,31 @@ FULL = ["tiny_linear", "conv3x3_im2col", "xfmr_qkv", "xfmr_ffn_up", "xfmr_ffn_do
 def test_workload_parity_full(name):
     case = workloads.make(name)
     compare_full(gpu_run(case), oracle_run(case))
+
+
+NIBBLE_SIGN = [  # (M, N, K, a_lo, a_hi, w_lo, w_hi, a_signed): 1-bit weights in 4-bit containers
+    (200, 256, 2304, 4, 8, 1, 4, False),
+    (70, 130, 300, 4, 8, 1, 8, True),
+    (3, 64, 200, 4, 8, 1, 2, True),        # batch of 3 on the GEMV
+    (1, 100, 64, 4, 8, 1, 1, True),        # every output 1-bit, one row
+    (150, 100, 129, 1, 8, 1, 2, True),     # 1-bit activations too
+]
+
+
+@pytest.mark.parametrize("shape", NIBBLE_SIGN, ids=lambda s: "x".join(map(str, s[:3])) + f"_w{s[5]}{s[6]}")
+def test_sign_weights_in_nibbles(shape):
+    """SONIQ_WPACK_SIGN_NIBBLES changes only the storage of 1-bit channels:
+    the same codes, accumulators and outputs as the oracle."""
+    M, N, K, alo, ahi, wlo, whi, sgn = shape
+    case = workloads.generic(M, N, K, a_lo=alo, a_hi=ahi, a_frac_lo=0.6, w_lo=wlo, w_hi=whi,
+                             w_frac_lo=0.8, a_signed=sgn, seed=M + 3 * N + K, a_abs=not sgn,
+                             name="sign_nibbles")
+    compare_full(gpu_run(case, sign_nibbles=True), oracle_run(case))
+
+
+def test_conv_workload_sign_nibbles():
+    case = workloads.make("conv3x3_im2col")
+    compare_full(gpu_run(case, sign_nibbles=True), oracle_run(case))
 
 
 def test_square_8192_sampled():
