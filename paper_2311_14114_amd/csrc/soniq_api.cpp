@@ -204,6 +204,7 @@ struct soniq_weights_s {
   int gsub[2] = {0, 0};   // granules per block
   int nsub[2] = {0, 0};   // blocks per precision group
   int32_t* grp = nullptr;  // block of each original input channel
+  int32_t* posg = nullptr;  // planned position | block << 16
 
   int scales() const { return act_group_bits ? nsub[0] + nsub[1] : kp.S; }
   WDev dev() const { return WDev{packed, blk_off, blk_c, colinfo, shw, tile_cols, colrank}; }
@@ -241,6 +242,7 @@ void free_weights(soniq_weights w) {
   (void)hipFree(w->pos);
   (void)hipFree(w->seg);
   (void)hipFree(w->grp);
+  (void)hipFree(w->posg);
   w->magic = kDead;
   delete w;
 }
@@ -506,7 +508,7 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
   STEP(dev_alloc(&w->colrank, (size_t)wp.Np));
   STEP(dev_alloc(&w->pos, (size_t)K));
   STEP(dev_alloc(&w->seg, (size_t)K));
-  std::vector<int32_t> grp_h;
+  std::vector<int32_t> grp_h, posg_h;
   if (act_group_bits > 0) {
     // block of channel k: its rank inside its precision group over the
     // channels per block, after the blocks of group 0
@@ -518,6 +520,10 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
     }
     STEP(dev_alloc(&w->grp, (size_t)K));
     STEP(hipMemcpyAsync(w->grp, grp_h.data(), K * sizeof(int32_t), hipMemcpyHostToDevice, st));
+    posg_h.resize(K);
+    for (int64_t k = 0; k < K; ++k) posg_h[k] = w->kp.pos[k] | (grp_h[k] << 16);
+    STEP(dev_alloc(&w->posg, (size_t)K));
+    STEP(hipMemcpyAsync(w->posg, posg_h.data(), K * sizeof(int32_t), hipMemcpyHostToDevice, st));
   }
   STEP(dev_alloc(&wbits_dev, (size_t)N));
   STEP(dev_alloc(&phys_dev, (size_t)N));
@@ -633,8 +639,9 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
                 (long long)M, (long long)act->max_M);
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: lda < K");
   if (w->act_group_bits) {
-    HIP_TRY(launch_act_quant_grouped(A_dev, M, w->K, lda, act->ap, w->pos, w->grp, act->partial,
-                                     act->s_a, act->packed, reinterpret_cast<hipStream_t>(stream)));
+    HIP_TRY(launch_act_quant_grouped(A_dev, M, w->K, lda, act->ap, w->pos, w->grp, w->posg,
+                                     act->partial, act->counter, act->s_a, act->packed,
+                                     reinterpret_cast<hipStream_t>(stream)));
     act->M = M;
     return SONIQ_OK;
   }

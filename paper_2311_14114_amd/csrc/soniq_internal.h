@@ -38,7 +38,7 @@ constexpr int kMAlign = 256;  // activation rows are allocated in multiples of t
 constexpr int kAbsmaxBlocks = 1024;  // max partial maxima (pairs) per activation batch
 // 32-bit words of device state per activation handle (the single-pass
 // quantizer's grid counters and maxima); zero between calls.
-constexpr int kActStateWords = 2048;
+constexpr int kActStateWords = 8192;
 
 // Quantizer of one width: code = sign1 ? (x < 0 ? -1 : +1)
 //                                : clamp(rint(x / s), lo, hi), s = max/qdiv.
@@ -152,9 +152,12 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
 // at most kGSubMax blocks.
 constexpr int kGAbsParts = 1024;
 constexpr int kGSubMax = 256;
+// posg_dev[k] = pos_dev[k] | grp_dev[k] << 16 (the single pass's table);
+// counter: the handle's grid state.
 hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
                                     const ActPlan& ap, const int32_t* pos_dev,
-                                    const int32_t* grp_dev, float* partial, float* s_a,
+                                    const int32_t* grp_dev, const int32_t* posg_dev,
+                                    float* partial, unsigned int* counter, float* s_a,
                                     uint8_t* packed, hipStream_t stream);
 hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                   const WDev& wd, const WPlan& wp, int64_t M, int64_t N,

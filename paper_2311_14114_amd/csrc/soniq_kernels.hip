@@ -815,6 +815,11 @@ __device__ __forceinline__ uint32_t lds_off(const uint8_t* p) {
 constexpr int kBarTop = 256, kBarGen = 288, kBarMax = 544;
 constexpr int kBarWords = kBarMax + 32 * 16;
 static_assert(kBarWords <= kActStateWords, "grid state fits the handle's words");
+// Sub-group scales: block maxima maxg[p][x][j] at kBarMaxG + kGSubMax*(8p + x)
+// + j (the same counters and generation words as above).
+constexpr int kBarMaxG = 1088;
+static_assert(kBarMaxG >= kBarWords && kBarMaxG + 16 * kGSubMax <= kActStateWords,
+              "block maxima fit the handle's words");
 
 // Spin limit of the wait: far beyond any real wait (a few tenths of a
 // second).  A workgroup that times out (its grid was not resident after
@@ -899,6 +904,89 @@ __device__ __forceinline__ bool grid_fold_max(unsigned* st, unsigned gen, unsign
   g0 = __uint_as_float(m0);
   g1 = __uint_as_float(m1);
   return ok;
+}
+
+// Fold n block maxima (LDS words mx[0..n), n <= kGSubMax, non-negative
+// floats as bits) into the grid's and wait for every workgroup: run by all
+// of wave 0, gen = this call's generation in lane 0.  The same protocol as
+// grid_fold_max with the maxima spread over the wave's lanes; the last
+// arrival's whole wave clears the other parity's maxima.  On return mx[j]
+// holds the grid maximum of block j; false (every lane) when the wait
+// timed out.
+__device__ __forceinline__ bool grid_fold_max_n(unsigned* st, unsigned gen, unsigned spins,
+                                                unsigned* mx, int n) {
+  const int lane = threadIdx.x & 63;
+  gen = __builtin_amdgcn_readfirstlane(gen);
+  const unsigned x = blockIdx.x & 7;
+  const unsigned ngroups = gridDim.x < 8 ? gridDim.x : 8;
+  const unsigned nx = (gridDim.x - x + 7) / 8;
+  unsigned* cur = st + kBarMaxG + 8 * kGSubMax * (gen & 1);
+  unsigned done = gen;
+  for (int j = lane; j < n; j += 64)
+    done |= __hip_atomic_fetch_max(cur + x * kGSubMax + j, mx[j], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+  bar_after(done);
+  int last = 0, ok = 1;
+  if (lane == 0) {
+    const unsigned a1 = bar_add(st + 32 * x, 1u);
+    bar_after(a1);
+    if (a1 == nx - 1) {
+      bar_store(st + 32 * x, 0u);
+      const unsigned a2 = bar_add(st + kBarTop, 1u);
+      bar_after(a2);
+      if (a2 == ngroups - 1) {
+        bar_store(st + kBarTop, 0u);
+        last = 1;
+      }
+    }
+  }
+  last = __shfl(last, 0, 64);
+  if (last) {
+    // every fold came before its arrival: the other parity's maxima can be
+    // cleared for the next call, then the generation advances
+    unsigned* other = st + kBarMaxG + 8 * kGSubMax * ((gen & 1) ^ 1);
+    for (int xx = 0; xx < 8; ++xx)
+      for (int j = lane; j < n; j += 64) bar_store(other + xx * kGSubMax + j, 0u);
+    if (lane == 0)
+      for (int i = 0; i < 8; ++i) bar_add(st + kBarGen + 32 * i, 1u);
+  } else if (lane == 0) {
+    unsigned* genx = st + kBarGen + 32 * x;
+    unsigned c = 0, now;
+    while ((now = bar_load(genx)) == gen) {
+      if (++c > spins) {
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(20);
+    }
+    bar_after(now);
+  }
+  ok = __shfl(ok, 0, 64);
+  for (int j = lane; j < n; j += 64) {
+    unsigned m = 0;
+    for (int xx = 0; xx < 8; ++xx) m = max(m, bar_load(cur + xx * kGSubMax + j));
+    mx[j] = m;
+  }
+  return ok != 0;
+}
+
+// Block maxima of the whole batch, by this workgroup alone (the timed-out
+// wait only): block index in bits 16.. of the planned-position table.
+__device__ __forceinline__ void absmax_all_blocks(const float* __restrict__ A, int64_t M, int K4,
+                                                  int64_t lda, const int4* pos4, unsigned* mx,
+                                                  int n) {
+  for (int j = threadIdx.x; j < n; j += 256) mx[j] = 0u;
+  __syncthreads();
+  for (int64_t m = 0; m < M; ++m)
+    for (int k = threadIdx.x; k < K4; k += 256) {
+      const int4 p = pos4[k];
+      const float4 v = *reinterpret_cast<const float4*>(A + m * lda + 4 * k);
+      atomicMax(&mx[p.x >> 16], __float_as_uint(fabsf(v.x)));
+      atomicMax(&mx[p.y >> 16], __float_as_uint(fabsf(v.y)));
+      atomicMax(&mx[p.z >> 16], __float_as_uint(fabsf(v.z)));
+      atomicMax(&mx[p.w >> 16], __float_as_uint(fabsf(v.w)));
+    }
+  __syncthreads();
 }
 
 // Group maxima of the whole batch, by this workgroup alone (the timed-out
@@ -1058,10 +1146,51 @@ __device__ __forceinline__ void qcodes4_exact(const float4& v, int4 p, int kp0, 
   }
 }
 
+// The shortcut codes of qcodes4 with sub-group scales: element e's block
+// (bits 16.. of its table entry) selects its reciprocal from rtab (0 for a
+// scale outside the shortcut's range, which sends the element to the exact
+// division like a tie); hi per precision group (blocks >= nsub0 are group
+// 1's).  The block maximum bounds |x|, so the shortcut needs no upper
+// clamp, as in qcodes4.
+template <bool SIGNED>
+__device__ __forceinline__ void qcodes4g(const float4& v, int4 p, const float* stab,
+                                         const float* rtab, int nsub0, float hi0, float hi1,
+                                         uint8_t* row) {
+  const float xs[4] = {v.x, v.y, v.z, v.w};
+  const int pp[4] = {p.x, p.y, p.z, p.w};
+  int c[4];
+  float d[4];
+  bool slow = false;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float rs = rtab[pp[e] >> 16];
+    const float t = __builtin_fmaf(xs[e], rs, kShift);
+    c[e] = __float_as_int(SIGNED ? t : fmaxf(t, kShift));
+    d[e] = __builtin_fmaf(xs[e], rs, kShift - t);
+    slow |= rs == 0.0f;
+  }
+  const float dm = fmaxf(fmaxf(fabsf(d[0]), fabsf(d[1])), fmaxf(fabsf(d[2]), fabsf(d[3])));
+  if (slow || dm >= 0.5f - kTieBand) [[unlikely]] {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int b = pp[e] >> 16;
+      if (rtab[b] == 0.0f || fabsf(d[e]) >= 0.5f - kTieBand) {
+        const float hi = b >= nsub0 ? hi1 : hi0;
+        c[e] = qexact(xs[e], SIGNED ? -hi : 0.0f, hi, 0.0f, stab[b]);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) row[pp[e] & 0xFFFF] = (uint8_t)c[e];
+}
+
 // Waves per SIMD the register budget must allow: T <= 9 keeps seven
 // workgroups per CU resident (1568 four-row workgroups on 256 CUs), more
 // float4 per thread four.  TL of the T float4 per thread wait in LDS.
-template <int T, int TL>
+// GRP: sub-group scales (the planned-position table carries each
+// element's block in bits 16..; block maxima, scales and reciprocals sit in
+// LDS after the row slots: 3*nsub words).
+template <int T, int TL, bool GRP = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T <= 9 ? 7 : 4)))
 void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int RB,
                 const int32_t* __restrict__ pos, ActPlan ap, unsigned* __restrict__ st,
@@ -1149,6 +1278,12 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     for (int r = 0; r < RB; ++r)
       for (int i = tid; i < kw; i += 256) codes32[r * kw + i] = i < kw0 ? z0 : z1;
   }
+  const int nsub = GRP ? ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0) : 0;
+  unsigned* bmax = reinterpret_cast<unsigned*>(vlds + TL * 256);
+  float* stab = reinterpret_cast<float*>(bmax + nsub);
+  float* rtab = stab + nsub;
+  if constexpr (GRP)
+    for (int j = tid; j < nsub; j += 256) bmax[j] = 0u;
   // This wave's generation read and table chunks (issued before the T row
   // loads) have landed; a barrier without a fence, so the row loads stay
   // in flight and the maxima below fold each slot as it arrives.
@@ -1166,11 +1301,42 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
     for (int i = 0; i < T; ++i) {
       if (i == 0 && TL > 0) lds_dma_wait<TV>();  // the LDS slots, issued before the TV others
       const int4 p = pos4[tid + 256 * i < nf ? k : K4 - 1];
-      max4(val(i), make_uchar4(p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0), mx0, mx1);
+      if constexpr (GRP) {
+        // each element's |x| into its block's word; one atomic when the
+        // four share a block (the usual case)
+        const float4 x = val(i);
+        const float a0 = fabsf(x.x), a1 = fabsf(x.y), a2 = fabsf(x.z), a3 = fabsf(x.w);
+        const int b0 = p.x >> 16, b1 = p.y >> 16, b2 = p.z >> 16, b3 = p.w >> 16;
+        if (b0 == b1 && b0 == b2 && b0 == b3) {
+          atomicMax(&bmax[b0], __float_as_uint(fmaxf(fmaxf(a0, a1), fmaxf(a2, a3))));
+        } else {
+          atomicMax(&bmax[b0], __float_as_uint(a0));
+          atomicMax(&bmax[b1], __float_as_uint(a1));
+          atomicMax(&bmax[b2], __float_as_uint(a2));
+          atomicMax(&bmax[b3], __float_as_uint(a3));
+        }
+      } else {
+        max4(val(i), make_uchar4(p.x >= kp0, p.y >= kp0, p.z >= kp0, p.w >= kp0), mx0, mx1);
+      }
       coop_step(r, k, K4, q256, r256);
     }
   }
-  {
+  if constexpr (GRP) {
+    __syncthreads();
+    if (tid < 64) {
+      const bool ok = grid_fold_max_n(st, gen, spins, bmax, nsub);
+      if (tid == 0) flag = ok;
+    }
+    __syncthreads();
+    if (!flag) absmax_all_blocks(A, M, K4, lda, pos4, bmax, nsub);
+    for (int j = tid; j < nsub; j += 256) {
+      const float sc = group_scale(__uint_as_float(bmax[j]), j < ap.nsub[0] ? ap.q[0] : ap.q[1]);
+      stab[j] = sc;
+      rtab[j] = fast_ok(sc) ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+      if (blockIdx.x == 0) s_a_out[j] = sc;
+    }
+    __syncthreads();
+  } else {
     const float2 m = block_max2(make_float2(mx0, mx1), red);
     if (tid == 0) {
       float g0, g1;
@@ -1178,20 +1344,20 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
       gmax[0] = g0;
       gmax[1] = g1;
     }
+    __syncthreads();
   }
-  __syncthreads();
   float g0 = gmax[0], g1 = gmax[1];
-  if (!flag) absmax_all(A, M, K4, lda, pos4, kp0, red, g0, g1);
+  if (!GRP && !flag) absmax_all(A, M, K4, lda, pos4, kp0, red, g0, g1);
   const float s0 = group_scale(g0, ap.q[0]);
   const float s1 = ap.S == 2 ? group_scale(g1, ap.q[1]) : 0.0f;
-  if (blockIdx.x == 0 && tid == 0) {
+  if (!GRP && blockIdx.x == 0 && tid == 0) {
     s_a_out[0] = s0;
     s_a_out[1] = s1;
   }
   {
     const float hi0 = (float)ap.q[0].hi, hi1 = (float)ap.q[1].hi;
     const float lo0 = (float)ap.q[0].lo, lo1 = (float)ap.q[1].lo;
-    const bool fast = fast_ok(s0) && (ap.S == 1 || fast_ok(s1));
+    const bool fast = GRP || (fast_ok(s0) && (ap.S == 1 || fast_ok(s1)));
     float rs0 = fast ? __builtin_amdgcn_rcpf(s0) : 0.0f;
     float rs1 = fast && ap.S == 2 ? __builtin_amdgcn_rcpf(s1) : 0.0f;
     auto each = [&](auto&& f) __attribute__((always_inline)) {
@@ -1211,7 +1377,16 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
         }
       }
     };
-    if (!fast) {
+    if constexpr (GRP) {
+      if (ap.q[0].lo < 0)
+        each([&](const float4& x, int4 p, uint8_t* row) __attribute__((always_inline)) {
+          qcodes4g<true>(x, p, stab, rtab, ap.nsub[0], hi0, hi1, row);
+        });
+      else
+        each([&](const float4& x, int4 p, uint8_t* row) __attribute__((always_inline)) {
+          qcodes4g<false>(x, p, stab, rtab, ap.nsub[0], hi0, hi1, row);
+        });
+    } else if (!fast) {
       each([&](const float4& x, int4 p, uint8_t* row) __attribute__((always_inline)) {
         qcodes4_exact(x, p, kp0, s0, s1, lo0, lo1, hi0, hi1, row);
       });
@@ -2880,7 +3055,7 @@ __global__ __launch_bounds__(256) void k_gemv_mfma(GemmArgs a) {
 // depend on it.
 constexpr int64_t kCoopMinElems = (int64_t)1 << 20;
 
-template <int T, int TL>
+template <int T, int TL, bool GRP>
 int coop_capacity(size_t lds) {
   // resident workgroups per CU for this T and LDS size, cached per device
   struct Entry {
@@ -2894,7 +3069,7 @@ int coop_capacity(size_t lds) {
   if (cache.dev != dev || cache.lds != lds) {
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_act_coop<T, TL>, 256, lds) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_act_coop<T, TL, GRP>, 256, lds) != hipSuccess)
       return 0;
     cache.dev = dev;
     cache.lds = lds;
@@ -2904,26 +3079,29 @@ int coop_capacity(size_t lds) {
   return cache.per_cu * cache.cus;
 }
 
-template <int T, int TL>
+template <int T, int TL, bool GRP>
 bool coop_launch(const float* A, int64_t M, int64_t K, int64_t lda, int RB, const ActPlan& ap,
                  const int32_t* pos_dev, unsigned* bar, float* s_a,
                  uint8_t* packed, hipStream_t stream, hipError_t& e) {
-  const size_t lds = (size_t)RB * ap.Kp + 16 * (size_t)((K / 4 + 63) / 64 * 64) + 4096 * TL;
+  const int nsub = GRP ? ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0) : 0;
+  const size_t lds = (size_t)RB * ap.Kp + 16 * (size_t)((K / 4 + 63) / 64 * 64) + 4096 * TL +
+                     (size_t)(12 * nsub + 15) / 16 * 16;
   const int64_t blocks = (M + RB - 1) / RB;
   // a workgroup's rows are addressed with 32-bit byte offsets
   if ((int64_t)(RB - 1) * lda * 4 + K * 4 >= ((int64_t)1 << 31)) return false;
-  if (lds > 64 * 1024 || blocks > coop_capacity<T, TL>(lds)) return false;
+  if (lds > 64 * 1024 || blocks > coop_capacity<T, TL, GRP>(lds)) return false;
   unsigned spins = kBarrierSpins;
   if (const char* env = getenv("SONIQ_COOP_SPINS")) spins = (unsigned)strtoul(env, nullptr, 10);
-  hipLaunchKernelGGL((k_act_coop<T, TL>), dim3((unsigned)blocks), dim3(256), lds, stream, A, M,
+  hipLaunchKernelGGL((k_act_coop<T, TL, GRP>), dim3((unsigned)blocks), dim3(256), lds, stream, A, M,
                      (int)(K / 4), lda, RB, pos_dev, ap, bar, spins, s_a, packed);
   e = hipGetLastError();
   return true;
 }
 
+// grp: sub-group scales (pos_dev then holds position | block << 16).
 bool launch_act_coop(const float* A, int64_t M, int64_t K, int64_t lda, const ActPlan& ap,
                      const int32_t* pos_dev, unsigned* bar, float* s_a,
-                     uint8_t* packed, hipStream_t stream, hipError_t& e) {
+                     uint8_t* packed, hipStream_t stream, hipError_t& e, bool grp = false) {
   if (const char* env = getenv("SONIQ_ACT_COOP"))
     if (atoi(env) == 0) return false;
   const int64_t K4 = K / 4;
@@ -2945,14 +3123,14 @@ bool launch_act_coop(const float* A, int64_t M, int64_t K, int64_t lda, const Ac
   for (int i = 0; i < nc; ++i) {
     const Cand& c = cand[i];
     bool done = false;
-    if (c.t == 6)
-      done = coop_launch<6, 0>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
-    else if (c.t == 9)
-      done = coop_launch<9, 1>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
-    else if (c.t == 12)
-      done = coop_launch<12, 0>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
-    else
-      done = coop_launch<18, 0>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e);
+#define SONIQ_COOP(T_, TL_)                                                                         \
+  (grp ? coop_launch<T_, TL_, true>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e)  \
+       : coop_launch<T_, TL_, false>(A, M, K, lda, c.rb, ap, pos_dev, bar, s_a, packed, stream, e))
+    if (c.t == 6) done = SONIQ_COOP(6, 0);
+    else if (c.t == 9) done = SONIQ_COOP(9, 1);
+    else if (c.t == 12) done = SONIQ_COOP(12, 0);
+    else done = SONIQ_COOP(18, 0);
+#undef SONIQ_COOP
     if (done) return true;
   }
   return false;
@@ -4129,11 +4307,17 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
 // rows (at most kGAbsParts of them), block scales, then codes.
 hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
                                     const ActPlan& ap, const int32_t* pos_dev,
-                                    const int32_t* grp_dev, float* partial, float* s_a,
+                                    const int32_t* grp_dev, const int32_t* posg_dev,
+                                    float* partial, unsigned int* counter, float* s_a,
                                     uint8_t* packed, hipStream_t stream) {
   const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
   const size_t tab = (size_t)nsub * 8;
   const bool aligned = (K % 4 == 0) && (lda % 4 == 0) && (reinterpret_cast<uintptr_t>(A) % 16 == 0);
+  // one pass over the rows when the batch fits one resident grid
+  if (aligned && M * K >= kCoopMinElems) {
+    hipError_t e = hipSuccess;
+    if (launch_act_coop(A, M, K, lda, ap, posg_dev, counter, s_a, packed, stream, e, true)) return e;
+  }
   const int K4 = (int)(K / 4);
   const int J = (K4 + 255) / 256;
   if (aligned && J <= 4) {

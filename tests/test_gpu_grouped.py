@@ -137,3 +137,27 @@ def test_grouped_repeat_calls_and_rejections():
     X = torch.zeros((1, 4, 4, 4), dtype=torch.float32, device="cuda")
     with pytest.raises(sq.SoniqError):
         sq.soniq_quantize_act_conv3x3(g["act"], X)
+
+
+@pytest.mark.parametrize("mode", ["single_pass", "two_pass", "wait_timeout"])
+def test_grouped_quantizer_paths(mode, monkeypatch):
+    """A batch large enough for the single pass (M*K >= 2^20), through the
+    single pass, the two-pass form, and the single pass whose grid wait
+    gives up at once (every workgroup then takes the block maxima itself):
+    the same codes, scales and outputs as the oracle."""
+    if mode == "two_pass":
+        monkeypatch.setenv("SONIQ_ACT_COOP", "0")
+    if mode == "wait_timeout":
+        monkeypatch.setenv("SONIQ_COOP_SPINS", "0")
+    case = workloads.generic(1536, 256, 1024, a_lo=4, a_hi=8, a_frac_lo=0.7, w_lo=2, w_hi=8,
+                             w_frac_lo=0.7, a_signed=True, seed=31, name="grouped_paths")
+    rng = np.random.default_rng(1024)
+    case["A"] = (case["A"] * rng.uniform(0.05, 20.0, 1024).astype(np.float32)).astype(np.float32)
+    compare(gpu_run(case, 512), oracle_run(case, 512))
+    if mode == "single_pass":
+        # unsigned widths below their containers, and a second call
+        case2 = dict(case)
+        case2["A"] = np.abs(case["A"])
+        case2["a_bits"] = np.where(case["a_bits"] == 4, 3, 6).astype(np.uint8)
+        case2["a_signed"] = False
+        compare(gpu_run(case2, 1024), oracle_run(case2, 1024))
