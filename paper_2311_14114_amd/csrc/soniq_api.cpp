@@ -775,7 +775,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   if (tiles > 0x7FFFFFFFLL)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm_quantize_next: problem too large for one launch");
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (!next->qn_img || next->qn_serial != w->serial) {
+  if (!next->qn_img || !next->qn_tab || next->qn_serial != w->serial) {
     // first use of this (producer, next) pair: the code image and the
     // producer's column table, built synchronously
     if (!next->qn_img) {
@@ -806,6 +806,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     }
     (void)hipFree(next->qn_tab);
     next->qn_tab = nullptr;
+    next->qn_serial = 0;  // no table until the new one is complete
     HIP_TRY(dev_alloc(&next->qn_tab, tab.size()));
     HIP_TRY(hipMemcpy(next->qn_tab, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     next->qn_serial = w->serial;
