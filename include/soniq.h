@@ -163,7 +163,8 @@ soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out);
  * soniq_quantize_act -- quantize, re-order and pack M activation rows.
  * Passages: codec items 1 and 2 (group max-abs scale; unsigned codes) or the
  * symmetric signed grid; Sec. 2.4 C2 (one scale per precision group, shared
- * by all rows of the call); Alg. 1 channel permutation.
+ * by all rows of the call; one per block of a group for weights packed with
+ * soniq_pack_weights_grouped); Alg. 1 channel permutation.
  *
  *   A_dev   device, float32 [M, lda]; row m is one input vector over K
  *           channels in the original channel order.  Finite values only.
