@@ -105,3 +105,33 @@ def test_chain_repeat_and_other_producer():
     torch.cuda.synchronize()
     g_q, _ = sq.soniq_act_unpack_debug(r["act2"])
     np.testing.assert_array_equal(g_q, qb)
+
+
+def test_chain_at_benchmark_size():
+    """The two transformer linears bench.py --chain times (FFN up 4096 x 3072
+    x 768, then FFN down 4096 x 768 x 3072), in its launch configuration:
+    the layer-2 codes, scales, accumulators and outputs, bit for bit."""
+    up, down = workloads.xfmr_ffn_up(), workloads.xfmr_ffn_down()
+    M = up["M"]
+    print(f"[gpu] chain at benchmark size M={M}", flush=True)
+    r1 = oracle.run(up["A"], up["W"], up["a_bits"], up["w_bits"], True)
+    y1 = oracle.epilogue_replay_f32(r1["acc"], r1["s_a"], r1["s_w"])
+    _, s2, _, _ = oracle.quantize_act(y1, down["a_bits"], down["a_signed"])
+    q2 = oracle.quantize_act_static(y1, down["a_bits"], down["a_signed"], s2)
+    q_w2, s_w2 = oracle.quantize_weights(down["W"], down["w_bits"])
+    S2, _, seg_of2 = oracle.segments(down["a_bits"])
+    acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(up["W"]).cuda(), up["w_bits"], up["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(down["W"]).cuda(), down["w_bits"], down["a_bits"],
+                                down["a_signed"])
+    a1, a2 = sq.soniq_act_create(wh1, M), sq.soniq_act_create(wh2, M)
+    sq.soniq_quantize_act(a1, torch.from_numpy(up["A"]).cuda())
+    sq.soniq_mp_gemm_quantize_next(a1, wh1, a2, s2)
+    acc = torch.empty((S2, M, down["N"]), dtype=torch.int32, device="cuda")
+    Y2 = sq.soniq_mp_gemm(a2, wh2, acc=acc)
+    torch.cuda.synchronize()
+    g_q, g_s = sq.soniq_act_unpack_debug(a2)
+    np.testing.assert_array_equal(g_s, s2)
+    np.testing.assert_array_equal(g_q, q2)
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+    np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
