@@ -272,9 +272,11 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  *   act, w   as for soniq_mp_gemm (act quantized, made for w).
  *   next     an activation handle of the next layer's weights, whose K
  *            equals this layer's N; act's M must not exceed its max_M.
- *   s_next   host float [S of the next layer's weights]: the static scale
- *            of each next-layer activation group (narrow width first),
- *            finite and >= 0.  Copied during the call.
+ *   s_next   host float [act_scales of the next layer's weights]: the
+ *            static scale of each next-layer activation group (narrow width
+ *            first), or of each block when the next layer's weights were
+ *            packed with sub-group scales (blocks in their order), finite
+ *            and >= 0.  Copied during the call.
  *   Y_dev    as for soniq_mp_gemm, or NULL to skip storing Y.
  *   ldy, acc_dev  as for soniq_mp_gemm.
  * Each output's code is taken from the fp32 value the epilogue rounds to
@@ -287,8 +289,8 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * padded K, bytes) and a column table, synchronously; later calls with the
  * same pair allocate nothing.
  * Errors: INVALID_ARGUMENT (null, mismatched handles or sizes, bad
- * scales), UNSUPPORTED (weights with sub-group activation scales on either
- * side), OUT_OF_MEMORY, HIP.
+ * scales), UNSUPPORTED (producing weights packed with sub-group scales),
+ * OUT_OF_MEMORY, HIP.
  */
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
                                          const float* s_next, uint16_t* Y_dev, int64_t ldy,

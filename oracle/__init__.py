@@ -94,6 +94,8 @@ def lib():
         L.orc_epilogue_replay_f32.argtypes = [vp, vp, vp, i64, i64, i32, vp]
         L.orc_quantize_act_static.restype = i32
         L.orc_quantize_act_static.argtypes = [vp, i64, i64, i64, vp, i32, vp, vp]
+        L.orc_quantize_act_static_grouped.restype = i32
+        L.orc_quantize_act_static_grouped.argtypes = [vp, i64, i64, i64, vp, i32, i32, i32, vp, vp, vp]
         L.orc_container.restype = i32
         L.orc_container.argtypes = [i32]
         L.orc_pack.restype = i64
@@ -271,6 +273,23 @@ def quantize_act_static(A, a_bits, a_signed: bool, s_a):
     if S < 0 or sa.shape[0] < S:
         raise ValueError("bad widths or too few scales")
     return q
+
+
+def quantize_act_static_grouped(A, a_bits, a_signed: bool, group_bits: int, s_blocks):
+    """Codes of A[M,K] with the caller's scale per sub-group block (the
+    blocks of quantize_act_grouped).  Returns codes and the block of each
+    channel."""
+    A = _c(A, np.float32)
+    M, K = A.shape
+    ab = _c(a_bits, np.uint8)
+    sb = _c(s_blocks, np.float32)
+    q = np.empty((M, K), np.int32)
+    so = np.empty(K, np.int32)
+    S = lib().orc_quantize_act_static_grouped(_p(A), M, K, K, _p(ab), 1 if a_signed else 0,
+                                              int(group_bits), K + 2, _p(sb), _p(q), _p(so))
+    if S < 0 or sb.shape[0] < S:
+        raise ValueError("bad widths or group size, or too few scales")
+    return q, so
 
 
 def container(bits: int) -> int:

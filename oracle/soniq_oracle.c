@@ -395,6 +395,39 @@ int orc_quantize_act_static(const float* A, int64_t M, int64_t K, int64_t lda,
   return S;
 }
 
+/* Static block scales: the codes of orc_quantize_act_grouped's blocks with
+ * the caller's scale per block (s_blocks[S]) in place of the batch
+ * maximum.  Fills sub_of[K]; returns S, or -1 as orc_quantize_act_grouped. */
+int orc_quantize_act_static_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
+                                    const uint8_t* a_bits, int a_signed, int group_bits,
+                                    int cap, const float* s_blocks, int32_t* q_a,
+                                    int32_t* sub_of) {
+  /* the block plan: run the grouped quantizer on one row of zeros */
+  float* zero = (float*)calloc((size_t)(K > 0 ? K : 1), sizeof(float));
+  int32_t* qz = (int32_t*)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
+  float* sz = (float*)malloc(sizeof(float) * (size_t)(cap > 0 ? cap : 1));
+  uint8_t* bits = (uint8_t*)malloc((size_t)(cap > 0 ? cap : 1));
+  int S = orc_quantize_act_grouped(zero, 1, K, K, a_bits, a_signed, group_bits, cap, qz, sz, bits,
+                                   sub_of);
+  free(zero);
+  free(qz);
+  free(sz);
+  if (S < 0) {
+    free(bits);
+    return -1;
+  }
+  int mode = a_signed ? ORC_SIGNED : ORC_UNSIGNED;
+  int64_t m;
+#pragma omp parallel for schedule(static)
+  for (m = 0; m < M; ++m)
+    for (int64_t k = 0; k < K; ++k) {
+      int j = sub_of[k];
+      q_a[m * K + k] = orc_code(A[m * lda + k], s_blocks[j], bits[j], mode);
+    }
+  free(bits);
+  return S;
+}
+
 /* ------------------------------------------------------------------ O8 ---
  * Canonical dense packing of a run of codes, used to account bytes: element
  * j occupies bits [(j mod 32/c)*c, +c) of 32-bit word floor(j*c/32), with

@@ -274,13 +274,14 @@ def soniq_quantize_mp_gemm(act: Activations, weights: Weights, A, out=None, acc=
 def soniq_mp_gemm_quantize_next(act: Activations, weights: Weights, next_act: Activations,
                                 s_next, out=None, acc=None, stream=None):
     """soniq_mp_gemm(act, weights) whose epilogue also quantizes the outputs
-    into next_act with the static group scales s_next (one per next-layer
-    activation group).  out=None skips Y; returns out."""
+    into next_act with the static scales s_next (one per next-layer
+    activation group, or per block for sub-group weights).  out=None skips
+    Y; returns out."""
     import torch
     M, N = act.M, weights.N
     sn = np.ascontiguousarray(np.asarray(s_next, np.float32).ravel())
-    if sn.shape[0] < next_act.weights.info.S:
-        raise ValueError("one static scale per next-layer activation group")
+    if sn.shape[0] < next_act.weights.S:
+        raise ValueError("one static scale per next-layer activation group (or block)")
     outp, ldy = None, N
     if out is not None:
         if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or out.shape[0] < M:

@@ -205,6 +205,7 @@ struct soniq_weights_s {
   int nsub[2] = {0, 0};   // blocks per precision group
   int32_t* grp = nullptr;  // block of each original input channel
   int32_t* posg = nullptr;  // planned position | block << 16
+  std::vector<int32_t> grp_h;  // host copy of grp
 
   int scales() const { return act_group_bits ? nsub[0] + nsub[1] : kp.S; }
   WDev dev() const { return WDev{packed, blk_off, blk_c, colinfo, shw, tile_cols, colrank}; }
@@ -225,6 +226,7 @@ struct soniq_act_s {
   // the producer's per-physical-column table (position | group << 16)
   uint8_t* qn_img = nullptr;
   int32_t* qn_tab = nullptr;
+  float* qn_brs = nullptr;  // reciprocals of static block scales (sub-group weights)
   uint64_t qn_serial = 0;  // the producer weights the table was built for
 };
 
@@ -549,6 +551,7 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
     free_weights(w);
     return rc;
   }
+  w->grp_h = std::move(grp_h);
   w->serial = g_serial.fetch_add(1);
   w->magic = kMagicW;
   *out = w;
@@ -764,10 +767,10 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
                 (long long)M, (long long)next->max_M);
   if (Y_dev && ldy < w->N)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: ldy < N");
-  if (w->act_group_bits || w2->act_group_bits)
+  if (w->act_group_bits)
     return fail(SONIQ_ERR_UNSUPPORTED,
-                "soniq_mp_gemm_quantize_next: weights with sub-group activation scales");
-  for (int g = 0; g < w2->kp.S; ++g)
+                "soniq_mp_gemm_quantize_next: producing weights with sub-group activation scales");
+  for (int g = 0; g < w2->scales(); ++g)
     if (!(s_next[g] >= 0.0f) || !std::isfinite(s_next[g]))
       return fail(SONIQ_ERR_INVALID_ARGUMENT,
                   "soniq_mp_gemm_quantize_next: static scale %d is negative or not finite", g);
@@ -789,6 +792,8 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
       }
       next->qn_img = img;
     }
+    if (w2->act_group_bits && !next->qn_brs)
+      HIP_TRY(dev_alloc(&next->qn_brs, (size_t)w2->scales()));
     // [0, Np): next-layer group of each physical column's channel;
     // [Np, 2 Np): next-layer position of each tile's r-th column in
     // ascending original order (the order the GEMM stages its outputs in)
@@ -797,7 +802,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     std::vector<std::vector<int64_t>> cols(Np / kGemmBN);
     for (int64_t n = 0; n < w->N; ++n) {
       const int32_t p = w->phys_h[n];
-      tab[p] = w2->kp.seg[n];
+      tab[p] = w2->act_group_bits ? w2->grp_h[n] : w2->kp.seg[n];  // block, or group
       cols[p / kGemmBN].push_back(n);
     }
     for (size_t t = 0; t < cols.size(); ++t) {
@@ -811,9 +816,10 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     HIP_TRY(hipMemcpy(next->qn_tab, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice));
     next->qn_serial = w->serial;
   }
-  const float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
+  float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
   HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                               acc_dev, next->qn_img, next->qn_tab, next->ap, s2, next->s_a,
+                               acc_dev, next->qn_img, next->qn_tab, next->ap,
+                               w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
                                next->packed, st));
   next->M = M;
   return SONIQ_OK;
@@ -877,6 +883,7 @@ void soniq_act_destroy(soniq_act act) {
   (void)hipFree(act->s_a);
   (void)hipFree(act->qn_img);
   (void)hipFree(act->qn_tab);
+  (void)hipFree(act->qn_brs);
   act->magic = kDead;
   soniq_weights w = act->w;
   delete act;

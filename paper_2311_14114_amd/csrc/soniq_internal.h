@@ -169,11 +169,14 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
 // physical column, then [Np] next-layer position per tile column in
 // ascending original order), then k_pack_img writes them as the next
 // handle's packed rows and its scales.  Y may be null.
+// A next layer with sub-group scales takes one static scale per block
+// (s_next[nsub], qtab's groups are then blocks), stored with their
+// reciprocals (brs2, nsub floats) by a small launch before the GEMM.
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
-                                const ActPlan& ap2, const float s_next[2], float* s_a2,
-                                uint8_t* packed2, hipStream_t stream);
+                                const ActPlan& ap2, const float* s_next, float* s_a2,
+                                float* brs2, uint8_t* packed2, hipStream_t stream);
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,

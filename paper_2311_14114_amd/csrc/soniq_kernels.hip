@@ -1623,6 +1623,12 @@ struct GemmArgs {
   const int32_t* qn_tab;
   int qn_ld;
   QNext qn;
+  // a next layer with sub-group scales: qn_tab holds each column's block,
+  // whose static scale and reciprocal are qn_bs[b], qn_brs[b] (blocks
+  // >= qn_nsub0 belong to its group 1); null otherwise
+  const float* qn_bs;
+  const float* qn_brs;
+  int qn_nsub0;
 };
 
 // 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
@@ -2192,7 +2198,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const float sa1 = S == 2 ? a.s_a[1] : 0.0f;
   ColInfo cinf[4];
   uint8_t cshw[4], crank[4];
-  int cqg[4] = {0, 0, 0, 0};  // next-layer group of each column (QN)
+  int cqg[4] = {0, 0, 0, 0};  // next-layer group (or block) of each column (QN)
+  float cqs[4] = {0.0f, 0.0f, 0.0f, 0.0f}, cqr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if constexpr (WFM <= 2) {
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
@@ -2201,6 +2208,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       cshw[jj] = a.wd.shw[pc];
       crank[jj] = a.wd.colrank[pc];
       if constexpr (QN) cqg[jj] = a.qn_tab[pc];
+    }
+    if constexpr (QN) {
+      if (a.qn_bs) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          cqs[jj] = a.qn_bs[max(cqg[jj], 0)];
+          cqr[jj] = a.qn_brs[max(cqg[jj], 0)];
+        }
+      }
     }
   }
 
@@ -2295,7 +2311,20 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
         }
         if constexpr (QN) {
           // the next layer's code of each output, staged like Y
-          const QCol qc = qnext_col(WFM <= 2 ? cqg[jj] : a.qn_tab[pc], a.qn);
+          QCol qc;
+          if (a.qn_bs) {
+            // sub-group scales: the block's static scale, its group's range
+            const int b = WFM <= 2 ? cqg[jj] : a.qn_tab[pc];
+            const bool g1 = b >= a.qn_nsub0;
+            qc.sc = WFM <= 2 ? cqs[jj] : a.qn_bs[b];
+            qc.rs = WFM <= 2 ? cqr[jj] : a.qn_brs[b];
+            qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
+            qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
+            qc.zp = 0;
+            qc.sign1 = false;
+          } else {
+            qc = qnext_col(WFM <= 2 ? cqg[jj] : a.qn_tab[pc], a.qn);
+          }
           bool n0, n1;
           int c0 = qnext_fast(y[0], qc, n0), c1 = qnext_fast(y[1], qc, n1);
           if (__builtin_amdgcn_ballot_w64(n0 || n1) != 0) [[unlikely]] {
@@ -3136,6 +3165,23 @@ bool launch_act_coop(const float* A, int64_t M, int64_t K, int64_t lda, const Ac
   return false;
 }
 
+// Static scales of a next layer with sub-group blocks, passed by value (so
+// that a captured launch carries them): the handle's s_a and the
+// reciprocals the GEMM's epilogue uses (0 outside the shortcut's range).
+struct BlockScales {
+  float s[kGSubMax];
+  int n;
+};
+
+__global__ __launch_bounds__(256) void k_set_scales(BlockScales b, float* __restrict__ s_a,
+                                                    float* __restrict__ brs) {
+  for (int j = threadIdx.x; j < b.n; j += 256) {
+    const float sc = b.s[j];
+    s_a[j] = sc;
+    brs[j] = (sc >= 0x1p-100f && sc <= 0x1p100f) ? __fdiv_rn(1.0f, sc) : 0.0f;
+  }
+}
+
 // ------------------------------------------------------------ k_pack_img --
 // The next layer's packed rows from the byte image the GEMM's epilogue
 // wrote (stored codes at planned positions; padding positions stay 0):
@@ -3153,7 +3199,7 @@ __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ im
   const int n16 = rows * ap.Kp / 16;
   const uint4* src = reinterpret_cast<const uint4*>(img + m0 * ap.Kp);
   for (int i = threadIdx.x; i < n16; i += 256) reinterpret_cast<uint4*>(codes)[i] = src[i];
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (s_a && blockIdx.x == 0 && threadIdx.x == 0) {
     s_a[0] = s0;
     s_a[1] = s1;
   }
@@ -4103,6 +4149,9 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.qn_tab = nullptr;
   a.qn_ld = 0;
   a.qn = QNext{};
+  a.qn_bs = nullptr;
+  a.qn_brs = nullptr;
+  a.qn_nsub0 = 0;
   return a;
 }
 
@@ -4171,16 +4220,26 @@ static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
-                                const ActPlan& ap2, const float s_next[2], float* s_a2,
-                                uint8_t* packed2, hipStream_t stream) {
+                                const ActPlan& ap2, const float* s_next, float* s_a2,
+                                float* brs2, uint8_t* packed2, hipStream_t stream) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  const bool blocks = ap2.gsub[0] > 0;
+  if (blocks) {
+    BlockScales b{};
+    b.n = ap2.nsub[0] + (ap2.S == 2 ? ap2.nsub[1] : 0);
+    for (int j = 0; j < b.n; ++j) b.s[j] = s_next[j];
+    hipLaunchKernelGGL(k_set_scales, dim3(1), dim3(256), 0, stream, b, s_a2, brs2);
+    a.qn_bs = s_a2;
+    a.qn_brs = brs2;
+    a.qn_nsub0 = ap2.nsub[0];
+  }
   const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
   a.xcd_tiles = tiles <= 2048;
   a.qn_img = img;
   a.qn_tab = qtab;
   a.qn_ld = ap2.Kp;
   for (int g = 0; g < 2; ++g) {
-    const float sc = g < ap2.S ? s_next[g] : 0.0f;
+    const float sc = !blocks && g < ap2.S ? s_next[g] : 0.0f;
     a.qn.s[g] = sc;
     // the reciprocal shortcut under the same range rule as the device
     // quantizers; IEEE division is within half an ulp of 1/s
@@ -4204,13 +4263,15 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const float s0 = s_next[0], s1 = ap2.S == 2 ? s_next[1] : 0.0f;
+  const float s0 = blocks ? 0.0f : s_next[0];
+  const float s1 = !blocks && ap2.S == 2 ? s_next[1] : 0.0f;
+  float* s_out = blocks ? nullptr : s_a2;  // block scales were stored above
   if (kBlk * (size_t)ap2.Kp <= 64 * 1024)
     hipLaunchKernelGGL(k_pack_img<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
-                       kBlk * (size_t)ap2.Kp, stream, img, M, ap2, s0, s1, s_a2, packed2);
+                       kBlk * (size_t)ap2.Kp, stream, img, M, ap2, s0, s1, s_out, packed2);
   else
     hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)M), dim3(256), (size_t)ap2.Kp, stream, img, M,
-                       ap2, s0, s1, s_a2, packed2);
+                       ap2, s0, s1, s_out, packed2);
   return hipGetLastError();
 }
 

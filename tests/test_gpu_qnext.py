@@ -135,3 +135,42 @@ def test_chain_at_benchmark_size():
     np.testing.assert_array_equal(g_q, q2)
     np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
     np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
+
+
+@pytest.mark.parametrize("c", [
+    (64, 256, 768, 128, (4, 8), True, 512),
+    (300, 200, 1000, 70, (3, 6), False, 1024),   # unsigned widths below their containers
+    (5, 128, 600, 96, (4, 8), True, 512),
+    (33, 96, 4000, 40, (2, 8), True, 512),       # 2-bit blocks of 256 channels; 1-row packing
+], ids=lambda c: f"M{c[0]}_N{c[2]}_a{c[4][0]}{c[4][1]}_g{c[6]}")
+def test_chain_into_sub_group_scales(c):
+    """The next layer packed with sub-group scales: one static scale per
+    block; its codes, accumulators per block and outputs match the oracle."""
+    M, K1, N1, N2, a2, signed2, gbits = c
+    l1 = workloads.generic(M, N1, K1, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.7, a_signed=True, seed=M + N1, name="c1")
+    l2 = workloads.generic(M, N2, N1, a_lo=a2[0], a_hi=a2[1], a_frac_lo=0.7, w_lo=2, w_hi=4,
+                           w_frac_lo=0.5, a_signed=signed2, seed=M + N2, name="c2")
+    print(f"[gpu] chain into blocks M={M} N1={N1} N2={N2} a2={a2} signed={signed2} g={gbits}", flush=True)
+    r1 = oracle.run(l1["A"], l1["W"], l1["a_bits"], l1["w_bits"], True)
+    y1 = oracle.epilogue_replay_f32(r1["acc"], r1["s_a"], r1["s_w"])
+    _, s_cal, _, _ = oracle.quantize_act_grouped(y1, l2["a_bits"], signed2, gbits)
+    s2 = (s_cal * np.float32(0.8)).astype(np.float32)
+    q2, sub_of = oracle.quantize_act_static_grouped(y1, l2["a_bits"], signed2, gbits, s2)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    acc2 = oracle.mac(q2, q_w2, sub_of, len(s2))
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], signed2,
+                                act_group_bits=gbits)
+    assert wh2.S == len(s2)
+    a1, a2h = sq.soniq_act_create(wh1, M), sq.soniq_act_create(wh2, M)
+    sq.soniq_quantize_act(a1, torch.from_numpy(l1["A"]).cuda())
+    sq.soniq_mp_gemm_quantize_next(a1, wh1, a2h, s2)
+    acc = torch.empty((wh2.S, M, N2), dtype=torch.int32, device="cuda")
+    Y2 = sq.soniq_mp_gemm(a2h, wh2, acc=acc)
+    torch.cuda.synchronize()
+    g_q, g_s = sq.soniq_act_unpack_debug(a2h)
+    np.testing.assert_array_equal(g_s, s2)
+    np.testing.assert_array_equal(g_q, q2)
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+    np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))

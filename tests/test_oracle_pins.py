@@ -584,3 +584,22 @@ def test_replay_f32_rounds_to_the_replay():
     yb = oracle.epilogue_replay(acc, s_a, s_w)
     np.testing.assert_array_equal(
         np.array([[oracle.bf16_from_f32(v) for v in row] for row in y32], np.uint16), yb)
+
+
+def test_static_block_scales_equal_to_the_batch_ones_give_its_codes():
+    """Static scales per sub-group block, set to the blocks' batch scales,
+    reproduce the pinned grouped quantizer's codes and blocks; doubling one
+    block's static scale changes codes in that block only."""
+    rng = np.random.default_rng(34)
+    M, K = 9, 650
+    A = (rng.standard_normal((M, K)) * rng.uniform(0.1, 10, K)).astype(np.float32)
+    ab = np.where(rng.random(K) < 0.6, 4, 8).astype(np.uint8)
+    q, s, sb, so = oracle.quantize_act_grouped(A, ab, True, 512)
+    q2, so2 = oracle.quantize_act_static_grouped(A, ab, True, 512, s)
+    np.testing.assert_array_equal(q2, q)
+    np.testing.assert_array_equal(so2, so)
+    s3 = s.copy()
+    s3[1] *= 2
+    q3, _ = oracle.quantize_act_static_grouped(A, ab, True, 512, s3)
+    np.testing.assert_array_equal(q3[:, so != 1], q[:, so != 1])
+    assert (q3[:, so == 1] != q[:, so == 1]).any()
