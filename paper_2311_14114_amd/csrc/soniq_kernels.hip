@@ -2153,11 +2153,14 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
   bar_nofence();
 }
 
-// (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).  QN:
+// (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).  QN > 0:
 // the epilogue also quantizes every output for the next layer into qn_img
-// (and stores Y only when a.Y is set).
-template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, bool QN = false>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+// (and stores Y only when a.Y is set), with one static scale per
+// next-layer group (QN = 1) or per block of a next layer with sub-group
+// scales (QN = 2, asked to keep three waves per SIMD).
+template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QN == 2 ? 3 : 1)))
+void k_gemm(GemmArgs a) {
   constexpr int BM = 32 * WFM;
   constexpr int SLOT = gemm_slot(S, CA0, CA1, CBL, CBH, WFM);
   constexpr int ASLOT = gemm_aslot(S, CA0, CA1, CBL, CBH, WFM);
@@ -2199,7 +2202,6 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   ColInfo cinf[4];
   uint8_t cshw[4], crank[4];
   int cqg[4] = {0, 0, 0, 0};  // next-layer group (or block) of each column (QN)
-  float cqs[4] = {0.0f, 0.0f, 0.0f, 0.0f}, cqr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if constexpr (WFM <= 2) {
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
@@ -2207,16 +2209,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       cinf[jj] = a.wd.colinfo[pc];
       cshw[jj] = a.wd.shw[pc];
       crank[jj] = a.wd.colrank[pc];
-      if constexpr (QN) cqg[jj] = a.qn_tab[pc];
-    }
-    if constexpr (QN) {
-      if (a.qn_bs) {
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          cqs[jj] = a.qn_bs[max(cqg[jj], 0)];
-          cqr[jj] = a.qn_brs[max(cqg[jj], 0)];
-        }
-      }
+      if constexpr (QN > 0) cqg[jj] = a.qn_tab[pc];
     }
   }
 
@@ -2309,15 +2302,17 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
             }
           }
         }
-        if constexpr (QN) {
+        if constexpr (QN > 0) {
           // the next layer's code of each output, staged like Y
           QCol qc;
-          if (a.qn_bs) {
+          if constexpr (QN == 2) {
             // sub-group scales: the block's static scale, its group's range
             const int b = WFM <= 2 ? cqg[jj] : a.qn_tab[pc];
             const bool g1 = b >= a.qn_nsub0;
-            qc.sc = WFM <= 2 ? cqs[jj] : a.qn_bs[b];
-            qc.rs = WFM <= 2 ? cqr[jj] : a.qn_brs[b];
+            // (read here, not held through the K loop: registers decide
+            // this kernel's occupancy)
+            qc.sc = a.qn_bs[b];
+            qc.rs = a.qn_brs[b];
             qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
             qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
             qc.zp = 0;
@@ -2339,7 +2334,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     }
   }
   __syncthreads();
-  if constexpr (QN) {
+  if constexpr (QN > 0) {
     // rows of codes, each thread one column of the tile in ascending
     // original order: consecutive lanes write nearby planned positions
     static_assert(BM * YS * 3 <= NST * SLOT, "code staging fits the ring");
@@ -4213,8 +4208,11 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
 template <int S, int CA0, int CA1, int CBL, int CBH>
 static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
   const int ntn = a.wp.Np / kGemmBN;
-  hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, true>), dim3((unsigned)(((M + 63) / 64) * ntn)),
-                     dim3(256), 0, stream, a);
+  const dim3 grid((unsigned)(((M + 63) / 64) * ntn));
+  if (a.qn_bs)
+    hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 2>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 1>), grid, dim3(256), 0, stream, a);
 }
 
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
