@@ -319,14 +319,16 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
-def run_chain(steps, warmup):
+def run_chain(steps, warmup, group_bits=0):
     """Two transformer linears in a row (FFN up, 4096x3072x768, then FFN
     down, 4096x768x3072), timed two ways, each as `steps` steps captured
     in one HIP graph: the next layer's activations quantized in the first
     GEMM's epilogue with static scales (soniq_mp_gemm_quantize_next), and
     the unfused form (bf16 Y of layer 1, widened to fp32 by torch, then
     soniq_quantize_act with the batch maximum).  The static scales are
-    calibrated once, untimed, from the unfused form's batch maxima."""
+    calibrated once, untimed, from the unfused form's batch maxima.  With
+    group_bits > 0 both layers are packed with sub-group activation scales
+    of that many bits (one static scale per block)."""
     import torch
     import paper_2311_14114_amd as sq
     import workloads
@@ -336,9 +338,10 @@ def run_chain(steps, warmup):
     M = up["M"]
     dev = torch.device("cuda")
     A = torch.from_numpy(up["A"]).to(dev)
-    wh1 = sq.soniq_pack_weights(torch.from_numpy(up["W"]).to(dev), up["w_bits"], up["a_bits"], True)
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(up["W"]).to(dev), up["w_bits"], up["a_bits"], True,
+                                act_group_bits=group_bits)
     wh2 = sq.soniq_pack_weights(torch.from_numpy(down["W"]).to(dev), down["w_bits"], down["a_bits"],
-                                down["a_signed"])
+                                down["a_signed"], act_group_bits=group_bits)
     act1, act2 = sq.soniq_act_create(wh1, M), sq.soniq_act_create(wh2, M)
     Y1 = torch.empty((M, up["N"]), dtype=torch.bfloat16, device=dev)
     Y1f = torch.empty((M, up["N"]), dtype=torch.float32, device=dev)
@@ -385,7 +388,8 @@ def run_chain(steps, warmup):
     t_f, t_u = timed(fused), timed(unfused)
     ops = 2 * M * (up["N"] * up["K"] + down["N"] * down["K"])
     print(json.dumps({
-        "chain": "xfmr_ffn_up -> xfmr_ffn_down", "M": M, "steps": steps, "warmup": warmup,
+        "chain": "xfmr_ffn_up -> xfmr_ffn_down", "M": M, "act_group_bits": group_bits,
+        "steps": steps, "warmup": warmup,
         "fused_us": t_f * 1e3, "unfused_us": t_u * 1e3, "fused_tops": ops / (t_f * 1e-3) / 1e12,
         "unfused_tops": ops / (t_u * 1e-3) / 1e12, "static_scales": [float(v) for v in s2],
         "data": "synthetic"}), flush=True)
@@ -403,6 +407,9 @@ def main():
     ap.add_argument("--chain", action="store_true",
                     help="time FFN up -> FFN down with the next layer quantized in the first "
                          "GEMM's epilogue, against the unfused form")
+    ap.add_argument("--chain-group-bits", type=int, default=0,
+                    help="--chain with sub-group activation scales of this many bits "
+                         "(512: the transformer setting) in both layers")
     ap.add_argument("--conv-input", action="store_true",
                     help="conv workloads: quantize from the NCHW input tensor "
                          "(soniq_quantize_act_conv3x3) instead of the lowered matrix")
@@ -419,7 +426,7 @@ def main():
         copy_calibration()
         return
     if args.chain:
-        run_chain(args.steps, args.warmup)
+        run_chain(args.steps, args.warmup, args.chain_group_bits)
         return
 
     import workloads

@@ -284,13 +284,15 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * of its next-layer group g, exactly as soniq_quantize_act would with that
  * scale.  On return (stream order) `next` holds M packed rows and its
  * scales are s_next, ready for soniq_mp_gemm(next, next's weights).
- * Every batch size runs the MFMA tiles.  The first call with a given
+ * Every batch size runs the MFMA tiles; weights packed with sub-group
+ * scales produce through their per-block tiles (acc_dev then holds their
+ * per-block sums, as for soniq_mp_gemm).  The first call with a given
  * (weights, next) pair allocates next's code image (max_M rows of its
  * padded K, bytes) and a column table, synchronously; later calls with the
  * same pair allocate nothing.
  * Errors: INVALID_ARGUMENT (null, mismatched handles or sizes, bad
- * scales), UNSUPPORTED (producing weights packed with sub-group scales),
- * OUT_OF_MEMORY, HIP.
+ * scales), UNSUPPORTED (more tiles than one launch takes), OUT_OF_MEMORY,
+ * HIP.
  */
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
                                          const float* s_next, uint16_t* Y_dev, int64_t ldy,

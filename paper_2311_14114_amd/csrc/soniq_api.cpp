@@ -767,9 +767,6 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
                 (long long)M, (long long)next->max_M);
   if (Y_dev && ldy < w->N)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: ldy < N");
-  if (w->act_group_bits)
-    return fail(SONIQ_ERR_UNSUPPORTED,
-                "soniq_mp_gemm_quantize_next: producing weights with sub-group activation scales");
   for (int g = 0; g < w2->scales(); ++g)
     if (!(s_next[g] >= 0.0f) || !std::isfinite(s_next[g]))
       return fail(SONIQ_ERR_INVALID_ARGUMENT,

@@ -3460,7 +3460,9 @@ static_assert(kGSubMax <= 64 * kGSubRegs, "every block scale has a lane");
 // restarts them at 0; the epilogue scales by s_w and rounds to bf16.  With
 // a zero point of 0, acc >> sh is the block's exact sum (the unpack scales
 // removed), which the optional int32 dump receives as [block][M][N].
-template <int S, int CA0, int CA1, int CBL, int CBH>
+// QN > 0 quantizes each fp32 output for the next layer as k_gemm does (one
+// static scale per next-layer group, QN = 1, or per block, QN = 2).
+template <int S, int CA0, int CA1, int CBL, int CBH, int QN = 0>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void k_gemm_g(GemmArgs a) {
   constexpr int WFM = 2, NST = 2, BM = 32 * WFM;
@@ -3496,12 +3498,14 @@ void k_gemm_g(GemmArgs a) {
   for (int i = 0; i < kGSubRegs; ++i) sreg[i] = lane + 64 * i < nsub ? a.s_a[lane + 64 * i] : 0.0f;
   ColInfo cinf[4];
   uint8_t cshw[4], crank[4];
+  int cqg[4] = {0, 0, 0, 0};  // next-layer group (or block) of each column (QN)
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
     cinf[jj] = a.wd.colinfo[pc];
     cshw[jj] = a.wd.shw[pc];
     crank[jj] = a.wd.colrank[pc];
+    if constexpr (QN > 0) cqg[jj] = a.qn_tab[pc];
   }
 
   v4i acc[WFM][4];
@@ -3587,14 +3591,52 @@ void k_gemm_g(GemmArgs a) {
       const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
 #pragma unroll
       for (int r = 0; r < 4; r += 2) {
-        const __hip_bfloat162 pr = __float22bfloat162_rn(
-            make_float2(__fmul_rn(yf[i][jj][r], ci.s_w), __fmul_rn(yf[i][jj][r + 1], ci.s_w)));
+        const float y0 = __fmul_rn(yf[i][jj][r], ci.s_w), y1 = __fmul_rn(yf[i][jj][r + 1], ci.s_w);
+        const __hip_bfloat162 pr = __float22bfloat162_rn(make_float2(y0, y1));
         ycol[(row0 + r) * YS] = __builtin_bit_cast(uint16_t, pr.x);
         ycol[(row0 + r + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
+        if constexpr (QN > 0) {
+          // the next layer's code of each output, staged like Y
+          QCol qc;
+          if constexpr (QN == 2) {
+            const int b = cqg[jj];
+            const bool g1 = b >= a.qn_nsub0;
+            qc.sc = a.qn_bs[b];
+            qc.rs = a.qn_brs[b];
+            qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
+            qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
+            qc.zp = 0;
+            qc.sign1 = false;
+          } else {
+            qc = qnext_col(cqg[jj], a.qn);
+          }
+          bool n0, n1;
+          int c0 = qnext_fast(y0, qc, n0), c1 = qnext_fast(y1, qc, n1);
+          if (__builtin_amdgcn_ballot_w64(n0 || n1) != 0) [[unlikely]] {
+            if (n0) c0 = qnext_exact(y0, qc);
+            if (n1) c1 = qnext_exact(y1, qc);
+          }
+          uint8_t* qcol = reinterpret_cast<uint8_t*>(lds) + BM * YS * 2 + crank[jj];
+          qcol[(row0 + r) * YS] = (uint8_t)(int8_t)c0;
+          qcol[(row0 + r + 1) * YS] = (uint8_t)(int8_t)c1;
+        }
       }
     }
   }
   __syncthreads();
+  if constexpr (QN > 0) {
+    // rows of codes in ascending original column order, as in k_gemm
+    static_assert(BM * YS * 3 <= NST * SLOT, "code staging fits the ring");
+    const int qpos = a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))];
+    if (qpos >= 0) {
+      const uint8_t* qs = reinterpret_cast<const uint8_t*>(lds) + BM * YS * 2;
+      const int mrem = (int)min((int64_t)BM, a.M - m0);
+      uint8_t* qout = a.qn_img + m0 * a.qn_ld + qpos;
+      for (int row = tid / kGemmBN; row < mrem; row += 256 / kGemmBN)
+        qout[(int64_t)row * a.qn_ld] = qs[row * YS + (tid & (kGemmBN - 1))];
+    }
+    if (!a.Y) return;
+  }
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
     const int mrem = (int)min((int64_t)BM, a.M - m0);
@@ -4204,12 +4246,18 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
 }
 
 // The GEMM with the next layer's quantization in its epilogue (64 x 128
-// tiles at every batch size), then the packing of that layer's rows.
+// tiles at every batch size; k_gemm_g when the producer's activations have
+// sub-group scales), then the packing of that layer's rows.
 template <int S, int CA0, int CA1, int CBL, int CBH>
 static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
   const int ntn = a.wp.Np / kGemmBN;
   const dim3 grid((unsigned)(((M + 63) / 64) * ntn));
-  if (a.qn_bs)
+  if (a.ap.gsub[0] > 0) {  // the producer's own activations have blocks
+    if (a.qn_bs)
+      hipLaunchKernelGGL((k_gemm_g<S, CA0, CA1, CBL, CBH, 2>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_gemm_g<S, CA0, CA1, CBL, CBH, 1>), grid, dim3(256), 0, stream, a);
+  } else if (a.qn_bs)
     hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 2>), grid, dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 1>), grid, dim3(256), 0, stream, a);

@@ -174,3 +174,61 @@ def test_chain_into_sub_group_scales(c):
     np.testing.assert_array_equal(g_q, q2)
     np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
     np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
+
+
+@pytest.mark.parametrize("c", [
+    (64, 512, 256, 128, 512, 0, (4, 8), True),
+    (300, 1000, 333, 70, 512, 0, (4, 8), False),     # unsigned next layer (zero point)
+    (1, 768, 130, 64, 1024, 0, (2, 8), True),         # one row; 2-bit next-layer group
+    (129, 768, 768, 96, 512, 512, (4, 8), True),      # blocks on both sides
+    (33, 3072, 1000, 40, 512, 1024, (3, 6), False),   # 25 producer blocks; wide next blocks
+], ids=lambda c: f"M{c[0]}_K{c[1]}_N{c[2]}_g{c[4]}_next{c[5]}")
+def test_chain_from_sub_group_scales(c):
+    """The producing layer packed with sub-group scales (its per-block
+    tiles carry the epilogue): the next layer's codes come from the fp32
+    value (sum over blocks of f(ACC_j) s_a[j]) s_w, and its GEMM matches the
+    oracle; Y and the producer's per-block sums match too."""
+    M, K1, N1, N2, g1, g2, a2, signed2 = c
+    l1 = workloads.generic(M, N1, K1, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.7, a_signed=True, seed=M + K1, name="gp1")
+    l2 = workloads.generic(M, N2, N1, a_lo=a2[0], a_hi=a2[1], a_frac_lo=0.7, w_lo=2, w_hi=4,
+                           w_frac_lo=0.5, a_signed=signed2, seed=M + N2, name="gp2")
+    print(f"[gpu] chain from blocks M={M} K1={K1} N1={N1} N2={N2} g1={g1} g2={g2}", flush=True)
+    # oracle: the grouped producer, its fp32 outputs, then the next layer
+    q_a1, s_a1, _, sub1 = oracle.quantize_act_grouped(l1["A"], l1["a_bits"], True, g1)
+    q_w1, s_w1 = oracle.quantize_weights(l1["W"], l1["w_bits"])
+    acc1 = oracle.mac(q_a1, q_w1, sub1, len(s_a1))
+    y1 = oracle.epilogue_replay_f32(acc1, s_a1, s_w1)
+    if g2:
+        _, s_cal, _, _ = oracle.quantize_act_grouped(y1, l2["a_bits"], signed2, g2)
+        s2 = (s_cal * np.float32(0.8)).astype(np.float32)
+        q2, sub2 = oracle.quantize_act_static_grouped(y1, l2["a_bits"], signed2, g2, s2)
+    else:
+        _, s_cal, _, _ = oracle.quantize_act(y1, l2["a_bits"], signed2)
+        s2 = (s_cal * np.float32(0.8)).astype(np.float32)
+        q2 = oracle.quantize_act_static(y1, l2["a_bits"], signed2, s2)
+        S2, _, sub2 = oracle.segments(l2["a_bits"])
+        s2 = s2[:S2]
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    acc2 = oracle.mac(q2, q_w2, sub2, len(s2))
+    # GPU
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True,
+                                act_group_bits=g1)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], signed2,
+                                act_group_bits=g2)
+    assert wh1.S == len(s_a1) and wh2.S == len(s2)
+    h1, h2 = sq.soniq_act_create(wh1, M), sq.soniq_act_create(wh2, M)
+    sq.soniq_quantize_act(h1, torch.from_numpy(l1["A"]).cuda())
+    Y1 = torch.empty((M, N1), dtype=torch.bfloat16, device="cuda")
+    acc1_g = torch.empty((wh1.S, M, N1), dtype=torch.int32, device="cuda")
+    sq.soniq_mp_gemm_quantize_next(h1, wh1, h2, s2, out=Y1, acc=acc1_g)
+    acc2_g = torch.empty((wh2.S, M, N2), dtype=torch.int32, device="cuda")
+    Y2 = sq.soniq_mp_gemm(h2, wh2, acc=acc2_g)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(acc1_g.cpu().numpy(), acc1)
+    np.testing.assert_array_equal(_bf16_bits(Y1), oracle.epilogue_replay(acc1, s_a1, s_w1))
+    g_q, g_s = sq.soniq_act_unpack_debug(h2)
+    np.testing.assert_array_equal(g_s, s2)
+    np.testing.assert_array_equal(g_q, q2)
+    np.testing.assert_array_equal(acc2_g.cpu().numpy(), acc2)
+    np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
