@@ -104,17 +104,21 @@ def test_graph_replay_grouped(name):
         np.testing.assert_array_equal(_bits(Yg), _bits(Ye), err_msg=f"replay {r}")
 
 
-def test_graph_replay_quantize_next():
+@pytest.mark.parametrize("gbits", [0, 512])
+def test_graph_replay_quantize_next(gbits):
     """Two layers with the second's activations quantized in the first
-    GEMM's epilogue, replayed from a graph, checked against eager calls."""
+    GEMM's epilogue, replayed from a graph, checked against eager calls
+    (gbits > 0: both layers with sub-group activation scales)."""
     l1 = workloads.generic(256, 384, 256, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
                            w_frac_lo=0.6, a_signed=True, seed=3, name="l1")
     l2 = workloads.generic(256, 128, 384, a_lo=4, a_hi=8, a_frac_lo=0.7, w_lo=2, w_hi=4,
                            w_frac_lo=0.5, a_signed=True, seed=4, name="l2")
-    print("[gpu] graph replay quantize_next", flush=True)
-    w1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True)
-    w2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], True)
-    s2 = np.array([0.05, 0.2], np.float32)
+    print(f"[gpu] graph replay quantize_next gbits={gbits}", flush=True)
+    w1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True,
+                               act_group_bits=gbits)
+    w2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], True,
+                               act_group_bits=gbits)
+    s2 = np.linspace(0.05, 0.2, w2.S).astype(np.float32)
     A0 = torch.from_numpy(l1["A"]).cuda()
     A_buf = A0.clone()
     a1g, a2g = sq.soniq_act_create(w1, 256), sq.soniq_act_create(w2, 256)
