@@ -9,10 +9,16 @@ rotate over distinct copies (fp32 activations up to 512 MB, packed weights
 up to 1 GiB), so every step reads them from HBM rather than from the 256 MB
 Infinity Cache, as a layer of a real network would.
 
-Prints one JSON line.  `value` is TOPS: 2*M*N*K integer ops per step over
-the whole step.  `roofline` covers the dominant kernel of a step, timed with
-HIP events on the stream it runs on.  `cpu_baseline` is the CPU oracle on a
-bounded sample of the same workload.
+Prints one JSON line.  The metric has two halves, both measured in the
+default run: `value` is the TOPS of the large square GEMM step
+(8192 x 8192 x 8192, 4/8-bit operands; 2*M*N*K integer ops per step over
+the whole step), with `roofline` on its dominant kernel, timed with HIP
+events on the stream it runs on; `gemv` holds the batch-1 decode GEMV
+(W[11008, 4096], 2/4-bit weights) as HBM GB/s on the packed weight bytes,
+with its own roofline.  The bf16 comparators (torch's GEMM on the same
+shapes) are timed with the same protocol: operands rotated the same way,
+the timed calls replayed from one captured HIP graph.  `cpu_baseline` is
+the CPU oracle on a bounded sample of the headline workload.
 
 `--copy-calibration` instead runs a plain 1 GiB device copy, whose
 FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic figures.
@@ -33,7 +39,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "mixed-precision GEMM TOPS & GEMV HBM GB/s (1 MI355X); speedup vs bf16 GEMM"
-DEFAULT_WORKLOAD = "conv3x3_im2col"
+DEFAULT_WORKLOAD = "square_8192"
+DEFAULT_GEMV_WORKLOAD = "decode_11008_m1"
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA
 ROTATE_A_BYTES = 512 << 20
@@ -187,13 +194,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     for i in range(warmup):
         torch.nn.functional.linear(Ab[i % nab], Wb[i % nwb])
     torch.cuda.synchronize()
-    s2, t2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    s2.record(stream)
-    for i in range(steps):
-        torch.nn.functional.linear(Ab[i % nab], Wb[i % nwb])
-    t2.record(stream)
-    torch.cuda.synchronize()
-    bf16_ms = s2.elapsed_time(t2) / steps
+    bf16_ms = timed(lambda i: torch.nn.functional.linear(Ab[i % nab], Wb[i % nwb]))
     del Ab, Wb
     return dict(total_ms=total_ms, wall_s=wall, q_ms=q_ms, g_ms=g_ms, g_hot_ms=g_hot_ms,
                 pack_ms=pack_ms,
@@ -268,6 +269,44 @@ def roofline(case, alg, r, steps):
     return dict(bound="mfma", achieved=ach, peak=INT8_PEAK_TOPS, unit="TFLOP/s",
                 frac=ach / INT8_PEAK_TOPS, traffic=traffic, kernel=kernel,
                 algorithmic_ops=alg["ops"], launch_us=t * 1e6)
+
+
+def gemv_record(case, r, steps):
+    """The batch-1 (or batch-8) decode half of the metric: HBM GB/s on the
+    packed weight bytes, the GEMV kernel's roofline (soniq_mp_gemm alone,
+    after a separate quantize call) and the one-call step's (for a one-row
+    batch soniq_quantize_mp_gemm is one launch that also quantizes the row),
+    against torch's bf16 GEMM timed the same way."""
+    alg = algorithmic(case, r["info"])
+    step_s = r["total_ms"] / steps * 1e-3
+    g_s = r["g_ms"] * 1e-3
+    kbytes = alg["a_packed"] + alg["w_packed"] + alg["w_side"] + alg["y"]
+    kernel = "k_gemv" if case["M"] == 1 else "k_gemv_mfma"
+    ach = kbytes / g_s / 1e9
+    rec = {
+        "workload": case["name"], "M": case["M"], "N": case["N"], "K": case["K"],
+        "a_bits": sorted(set(case["a_bits"].tolist())),
+        "w_bits": sorted(set(case["w_bits"].tolist())),
+        "weight_copies": r["nw"], "packed_weight_bytes": alg["w_packed"],
+        "packed_weight_gbs": alg["w_packed"] / g_s / 1e9,
+        "step_packed_weight_gbs": alg["w_packed"] / step_s / 1e9,
+        "step_us": step_s * 1e6, "mp_gemm_us": g_s * 1e6, "quantize_act_us": r["q_ms"] * 1e3,
+        "mp_gemm_weights_cache_hot_us": r["g_hot_ms"] * 1e3,
+        "roofline": dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                         frac=ach / HBM_PEAK_GBS, traffic=measured_traffic(kernel, case["name"]),
+                         kernel=kernel, algorithmic_bytes=kbytes, launch_us=g_s * 1e6),
+        "bf16_linear_us": r["bf16_ms"] * 1e3,
+        "speedup_vs_bf16": {"gemv": r["bf16_ms"] / r["g_ms"], "step": r["bf16_ms"] * 1e-3 / step_s},
+    }
+    if fused_one_row(case):
+        sbytes = alg["a_fp32"] + alg["w_packed"] + alg["w_side"] + alg["y"]
+        sa = sbytes / step_s / 1e9
+        rec["roofline_step"] = dict(bound="hbm", achieved=sa, peak=HBM_PEAK_GBS, unit="GB/s",
+                                    frac=sa / HBM_PEAK_GBS,
+                                    traffic=measured_traffic("k_gemv_fused", case["name"]),
+                                    kernel="k_gemv_fused", algorithmic_bytes=sbytes,
+                                    launch_us=step_s * 1e6)
+    return rec
 
 
 def cpu_baseline(case, budget_s=12.0):
@@ -401,6 +440,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--gemv-workload", default=None,
+                    help="the decode GEMV measured in the same run (default: "
+                         f"{DEFAULT_GEMV_WORKLOAD} when --workload is the default; 'none' skips it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
@@ -468,6 +510,17 @@ def main():
     }
     if args.conv_input and rec["roofline"]["kernel"] == "soniq_quantize_act":
         rec["roofline"]["traffic"] = None  # the counters on file are the lowered path's
+    gname = args.gemv_workload
+    if gname is None:
+        gname = DEFAULT_GEMV_WORKLOAD if args.workload == DEFAULT_WORKLOAD else "none"
+    if gname != "none":
+        gcase = workloads.make(gname)
+        if gcase["M"] > 8:
+            print(f"--gemv-workload {gname} is not a decode batch (M > 8)", file=sys.stderr)
+            sys.exit(2)
+        gr = run_gpu(gcase, args.steps, args.warmup, rotate=not args.no_rotate,
+                     graph=args.launch == "graph")
+        rec["gemv"] = gemv_record(gcase, gr, args.steps)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(rec))

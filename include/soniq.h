@@ -289,9 +289,14 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * per-block sums, as for soniq_mp_gemm).  The first call with a given
  * (weights, next) pair allocates next's code image (max_M rows of its
  * padded K, bytes) and a column table, synchronously; later calls with the
- * same pair allocate nothing.
- * Errors: INVALID_ARGUMENT (null, mismatched handles or sizes, bad
- * scales), UNSUPPORTED (more tiles than one launch takes), OUT_OF_MEMORY,
+ * same pair allocate nothing, so make that first call before capturing the
+ * call in a HIP graph.  `next` keeps one table per producer weights handle
+ * until it is destroyed: a graph captured with one producer stays valid
+ * after other producers have fed the same `next`.
+ * `next` must not be `act` (its scales would be overwritten before the
+ * GEMM reads them).
+ * Errors: INVALID_ARGUMENT (null, next == act, mismatched handles or
+ * sizes, bad scales), UNSUPPORTED (more tiles than one launch takes), OUT_OF_MEMORY,
  * HIP.
  */
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
@@ -320,6 +325,19 @@ soniq_status soniq_plan_input_channels(const uint8_t* a_bits, int64_t K, int64_t
  */
 soniq_status soniq_weights_unpack_debug(soniq_weights w, int32_t* codes, float* s_w);
 soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a);
+
+/*
+ * soniq_act_wait_timeouts -- how many workgroups of the single-pass
+ * quantizer gave up waiting for the rest of their grid since `act` was
+ * made (synchronous: waits for the device).  The single pass (codec item 1:
+ * one max-abs per group over the whole batch, taken in the same pass that
+ * quantizes) sizes its grid so that every workgroup is resident; a
+ * workgroup whose wait times out anyway (e.g. other work held the compute
+ * units) takes the maxima from the whole batch itself, so results are
+ * unchanged but the call was slow.  A nonzero count says that happened.
+ * Errors: INVALID_ARGUMENT, HIP.
+ */
+soniq_status soniq_act_wait_timeouts(soniq_act act, uint64_t* count);
 
 /* Release a handle (NULL is ignored).  Waits for the device first. */
 void soniq_weights_destroy(soniq_weights w);

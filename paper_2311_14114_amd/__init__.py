@@ -35,7 +35,8 @@ EXPORTED = [
     "soniq_mp_gemm_quantize_next",
     "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
-    "soniq_act_unpack_debug", "soniq_weights_destroy", "soniq_act_destroy",
+    "soniq_act_unpack_debug", "soniq_act_wait_timeouts", "soniq_weights_destroy",
+    "soniq_act_destroy",
     "soniq_last_error",
 ]
 
@@ -97,6 +98,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_weights_unpack_debug.argtypes = [vp, vp, vp]
         L.soniq_act_unpack_debug.restype = st
         L.soniq_act_unpack_debug.argtypes = [vp, vp, vp]
+        L.soniq_act_wait_timeouts.restype = st
+        L.soniq_act_wait_timeouts.argtypes = [vp, ctypes.POINTER(ctypes.c_uint64)]
         L.soniq_weights_destroy.restype = None
         L.soniq_weights_destroy.argtypes = [vp]
         L.soniq_act_destroy.restype = None
@@ -271,6 +274,7 @@ def soniq_quantize_mp_gemm(act: Activations, weights: Weights, A, out=None, acc=
     act.M = M
     return out
 
+
 def soniq_mp_gemm_quantize_next(act: Activations, weights: Weights, next_act: Activations,
                                 s_next, out=None, acc=None, stream=None):
     """soniq_mp_gemm(act, weights) whose epilogue also quantizes the outputs
@@ -338,3 +342,11 @@ def soniq_act_unpack_debug(act: Activations):
     _check(lib().soniq_act_unpack_debug(act.handle, codes.ctypes.data_as(ctypes.c_void_p),
                                         s_a.ctypes.data_as(ctypes.c_void_p)))
     return codes, s_a[: act.weights.S].copy()
+
+
+def soniq_act_wait_timeouts(act: Activations) -> int:
+    """Workgroups of the single-pass quantizer whose grid wait timed out
+    since the handle was made (results unchanged; the call was slow)."""
+    n = ctypes.c_uint64(0)
+    _check(lib().soniq_act_wait_timeouts(act.handle, ctypes.byref(n)))
+    return int(n.value)

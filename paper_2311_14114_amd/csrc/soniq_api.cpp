@@ -225,9 +225,16 @@ struct soniq_act_s {
   // outputs' codes as bytes [M_alloc][Kp] (padding positions stay 0), and
   // the producer's per-physical-column table (position | group << 16)
   uint8_t* qn_img = nullptr;
-  int32_t* qn_tab = nullptr;
   float* qn_brs = nullptr;  // reciprocals of static block scales (sub-group weights)
-  uint64_t qn_serial = 0;  // the producer weights the table was built for
+  // one column table per producer weights handle (keyed by its serial),
+  // kept until this handle is destroyed: a captured graph may still hold a
+  // table's address after another producer has fed this handle
+  std::vector<std::pair<uint64_t, int32_t*>> qn_tabs;
+  int32_t* qn_table(uint64_t serial) const {
+    for (const auto& t : qn_tabs)
+      if (t.first == serial) return t.second;
+    return nullptr;
+  }
 };
 
 namespace {
@@ -325,6 +332,54 @@ uint32_t block_field(const uint8_t* blk, int r, int64_t e, int c) {
 int decode_signed(uint32_t f, int c) {
   if (c == 1) return f ? -1 : 1;
   return (f >> (c - 1)) ? (int)f - (1 << c) : (int)f;
+}
+
+// The launches behind the entry points, on validated arguments: an
+// activation handle's buffers.
+soniq_status run_quantize(soniq_act_s& act, const float* A_dev, int64_t M, int64_t lda,
+                          hipStream_t st) {
+  const soniq_weights w = act.w;
+  if (w->act_group_bits)
+    HIP_TRY(launch_act_quant_grouped(A_dev, M, w->K, lda, act.ap, w->pos, w->grp, w->posg,
+                                     act.partial, act.counter, act.s_a, act.packed, st));
+  else
+    HIP_TRY(launch_act_quant(A_dev, M, w->K, lda, act.ap, w->pos, w->seg, act.partial, act.counter,
+                             act.s_a, act.packed, st));
+  act.M = M;
+  return SONIQ_OK;
+}
+
+soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,
+                      hipStream_t st) {
+  const soniq_weights w = act.w;
+  const int64_t M = act.M;
+  const bool gemv = !w->act_group_bits && gemv_fits(M, act.ap, w->wp);
+  if (!gemv && ((M + 63) / 64) * (w->wp.Np / kGemmBN) > 0x7FFFFFFFLL)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
+  if (w->act_group_bits)
+    HIP_TRY(launch_mp_gemm_grouped(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                                   acc_dev, st));
+  else if (gemv)
+    HIP_TRY(launch_mp_gemv(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                           acc_dev, st));
+  else
+    HIP_TRY(launch_mp_gemm(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                           acc_dev, st));
+  return SONIQ_OK;
+}
+
+soniq_status run_quantize_gemm(soniq_act_s& act, const float* A_dev, int64_t M, int64_t lda,
+                               uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev, hipStream_t st) {
+  const soniq_weights w = act.w;
+  if (M == 1 && !w->act_group_bits && gemv_fused_fits(A_dev, w->K, act.ap, w->wp)) {
+    HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos, act.packed, act.s_a, act.ap, w->dev(), w->wp,
+                              w->N, Y_dev, acc_dev, st));
+    act.M = 1;
+    return SONIQ_OK;
+  }
+  const soniq_status q = run_quantize(act, A_dev, M, lda, st);
+  if (q != SONIQ_OK) return q;
+  return run_gemm(act, Y_dev, ldy, acc_dev, st);
 }
 
 }  // namespace
@@ -641,18 +696,7 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: M=%lld outside [1, %lld]",
                 (long long)M, (long long)act->max_M);
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: lda < K");
-  if (w->act_group_bits) {
-    HIP_TRY(launch_act_quant_grouped(A_dev, M, w->K, lda, act->ap, w->pos, w->grp, w->posg,
-                                     act->partial, act->counter, act->s_a, act->packed,
-                                     reinterpret_cast<hipStream_t>(stream)));
-    act->M = M;
-    return SONIQ_OK;
-  }
-  HIP_TRY(launch_act_quant(A_dev, M, w->K, lda, act->ap, w->pos, w->seg, act->partial,
-                           act->counter, act->s_a, act->packed,
-                           reinterpret_cast<hipStream_t>(stream)));
-  act->M = M;
-  return SONIQ_OK;
+  return run_quantize(*act, A_dev, M, lda, reinterpret_cast<hipStream_t>(stream));
 }
 
 soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64_t B, int64_t C,
@@ -698,27 +742,7 @@ soniq_status soniq_mp_gemm(soniq_act act, soniq_weights w, uint16_t* Y_dev, int6
   if (act->M < 1)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: no activations quantized yet");
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm: ldy < N");
-  const int64_t M = act->M;
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (w->act_group_bits) {
-    const int64_t tiles = ((M + 63) / 64) * (w->wp.Np / kGemmBN);
-    if (tiles > 0x7FFFFFFFLL)
-      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
-    HIP_TRY(launch_mp_gemm_grouped(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev,
-                                   ldy, acc_dev, st));
-    return SONIQ_OK;
-  }
-  if (gemv_fits(M, act->ap, w->wp)) {
-    HIP_TRY(launch_mp_gemv(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                           acc_dev, st));
-  } else {
-    const int64_t tiles = ((M + 63) / 64) * (w->wp.Np / kGemmBN);
-    if (tiles > 0x7FFFFFFFLL)
-      return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
-    HIP_TRY(launch_mp_gemm(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                           acc_dev, st));
-  }
-  return SONIQ_OK;
+  return run_gemm(*act, Y_dev, ldy, acc_dev, reinterpret_cast<hipStream_t>(stream));
 }
 
 soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float* A_dev, int64_t M,
@@ -734,16 +758,8 @@ soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float*
                 (long long)M, (long long)act->max_M);
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: lda < K");
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: ldy < N");
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (M == 1 && !w->act_group_bits && gemv_fused_fits(A_dev, w->K, act->ap, w->wp)) {
-    HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos, act->packed, act->s_a, act->ap, w->dev(), w->wp,
-                              w->N, Y_dev, acc_dev, st));
-    act->M = 1;
-    return SONIQ_OK;
-  }
-  const soniq_status q = soniq_quantize_act(act, A_dev, M, lda, stream);
-  if (q != SONIQ_OK) return q;
-  return soniq_mp_gemm(act, w, Y_dev, ldy, acc_dev, stream);
+  return run_quantize_gemm(*act, A_dev, M, lda, Y_dev, ldy, acc_dev,
+                           reinterpret_cast<hipStream_t>(stream));
 }
 
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
@@ -756,6 +772,9 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
                 "soniq_mp_gemm_quantize_next: activation handle belongs to other weights");
   if (act->M < 1)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: no activations quantized yet");
+  if (next == act)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_mp_gemm_quantize_next: next is the producer's own activation handle");
   const soniq_weights w2 = next->w;
   if (w2->K != w->N)
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
@@ -775,7 +794,8 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   if (tiles > 0x7FFFFFFFLL)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm_quantize_next: problem too large for one launch");
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (!next->qn_img || !next->qn_tab || next->qn_serial != w->serial) {
+  int32_t* qn_tab = next->qn_table(w->serial);
+  if (!next->qn_img || !qn_tab) {
     // first use of this (producer, next) pair: the code image and the
     // producer's column table, built synchronously
     if (!next->qn_img) {
@@ -806,16 +826,19 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
       std::sort(cols[t].begin(), cols[t].end());
       for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = w2->kp.pos[cols[t][r]];
     }
-    (void)hipFree(next->qn_tab);
-    next->qn_tab = nullptr;
-    next->qn_serial = 0;  // no table until the new one is complete
-    HIP_TRY(dev_alloc(&next->qn_tab, tab.size()));
-    HIP_TRY(hipMemcpy(next->qn_tab, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice));
-    next->qn_serial = w->serial;
+    int32_t* t = nullptr;
+    HIP_TRY(dev_alloc(&t, tab.size()));
+    const hipError_t e = hipMemcpy(t, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(t);
+      return fail_hip(e, "soniq_mp_gemm_quantize_next: hipMemcpy");
+    }
+    next->qn_tabs.emplace_back(w->serial, t);
+    qn_tab = t;
   }
   float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
   HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                               acc_dev, next->qn_img, next->qn_tab, next->ap,
+                               acc_dev, next->qn_img, qn_tab, next->ap,
                                w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
                                next->packed, st));
   next->M = M;
@@ -865,6 +888,16 @@ soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a) {
   return SONIQ_OK;
 }
 
+soniq_status soniq_act_wait_timeouts(soniq_act act, uint64_t* count) {
+  if (!live_a(act) || !count)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_wait_timeouts: bad handle or null");
+  HIP_TRY(hipDeviceSynchronize());
+  unsigned int v = 0;
+  HIP_TRY(hipMemcpy(&v, act->counter + kActStallWord, sizeof v, hipMemcpyDeviceToHost));
+  *count = v;
+  return SONIQ_OK;
+}
+
 void soniq_weights_destroy(soniq_weights w) {
   if (!live_w(w)) return;
   w->released = true;
@@ -879,7 +912,7 @@ void soniq_act_destroy(soniq_act act) {
   (void)hipFree(act->counter);
   (void)hipFree(act->s_a);
   (void)hipFree(act->qn_img);
-  (void)hipFree(act->qn_tab);
+  for (const auto& t : act->qn_tabs) (void)hipFree(t.second);
   (void)hipFree(act->qn_brs);
   act->magic = kDead;
   soniq_weights w = act->w;

@@ -39,6 +39,8 @@ constexpr int kAbsmaxBlocks = 1024;  // max partial maxima (pairs) per activatio
 // 32-bit words of device state per activation handle (the single-pass
 // quantizer's grid counters and maxima); zero between calls.
 constexpr int kActStateWords = 8192;
+// The word of that state that counts timed-out grid waits (never reset).
+constexpr int kActStallWord = kActStateWords - 32;
 
 // Quantizer of one width: code = sign1 ? (x < 0 ? -1 : +1)
 //                                : clamp(rint(x / s), lo, hi), s = max/qdiv.

@@ -827,6 +827,11 @@ static_assert(kBarMaxG >= kBarWords && kBarMaxG + 16 * kGSubMax <= kActStateWord
 // the same, only slower.  SONIQ_COOP_SPINS overrides the limit (tests set
 // it to 0 to run that path).
 constexpr unsigned kBarrierSpins = 1u << 18;
+// Count of workgroups whose wait timed out, kept for the handle's lifetime
+// (the barrier protocol never touches it): a grid that was not resident
+// after all is slow, not wrong, and this word makes that visible.
+static_assert(kBarMaxG + 16 * kGSubMax <= kActStallWord && kActStallWord < kActStateWords,
+              "the stall count has a word of its own");
 
 __device__ __forceinline__ unsigned bar_load(const unsigned* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1328,6 +1333,7 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
       if (tid == 0) flag = ok;
     }
     __syncthreads();
+    if (!flag && tid == 0) bar_add(st + kActStallWord, 1u);
     if (!flag) absmax_all_blocks(A, M, K4, lda, pos4, bmax, nsub);
     for (int j = tid; j < nsub; j += 256) {
       const float sc = group_scale(__uint_as_float(bmax[j]), j < ap.nsub[0] ? ap.q[0] : ap.q[1]);
@@ -1343,6 +1349,7 @@ void k_act_coop(const float* __restrict__ A, int64_t M, int K4, int64_t lda, int
       flag = grid_fold_max(st, gen, spins, m.x, m.y, g0, g1);
       gmax[0] = g0;
       gmax[1] = g1;
+      if (!flag) bar_add(st + kActStallWord, 1u);
     }
     __syncthreads();
   }

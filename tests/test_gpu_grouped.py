@@ -153,7 +153,10 @@ def test_grouped_quantizer_paths(mode, monkeypatch):
                              w_frac_lo=0.7, a_signed=True, seed=31, name="grouped_paths")
     rng = np.random.default_rng(1024)
     case["A"] = (case["A"] * rng.uniform(0.05, 20.0, 1024).astype(np.float32)).astype(np.float32)
-    compare(gpu_run(case, 512), oracle_run(case, 512))
+    g = gpu_run(case, 512)
+    compare(g, oracle_run(case, 512))
+    stalls = sq.soniq_act_wait_timeouts(g["act"])
+    assert stalls >= 1 if mode == "wait_timeout" else stalls == 0
     if mode == "single_pass":
         # unsigned widths below their containers, and a second call
         case2 = dict(case)

@@ -232,3 +232,65 @@ def test_chain_from_sub_group_scales(c):
     np.testing.assert_array_equal(g_q, q2)
     np.testing.assert_array_equal(acc2_g.cpu().numpy(), acc2)
     np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
+
+
+def test_graph_replay_after_another_producer():
+    """A graph captured with producer A into a next handle, then an eager
+    call from producer B into the same handle, then replays of A's graph:
+    each replay's codes follow A's outputs (A's column table is still the
+    one the graph holds), and a later eager call from B still follows B."""
+    M, K1, N1, N2 = 96, 128, 256, 64
+    la = workloads.generic(M, N1, K1, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.7, a_signed=True, seed=71, name="prod_a")
+    lb = workloads.generic(M, N1, 96, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
+                           w_frac_lo=0.4, a_signed=True, seed=72, name="prod_b")
+    l2 = workloads.generic(M, N2, N1, a_lo=4, a_hi=8, a_frac_lo=0.7, w_lo=2, w_hi=8,
+                           w_frac_lo=0.5, a_signed=True, seed=73, name="next")
+    print(f"[gpu] producer switch then replay M={M} N1={N1}", flush=True)
+
+    def static_codes(l):
+        r = oracle.run(l["A"], l["W"], l["a_bits"], l["w_bits"], True)
+        return oracle.epilogue_replay_f32(r["acc"], r["s_a"], r["s_w"])
+
+    ya, yb = static_codes(la), static_codes(lb)
+    _, s2, _, _ = oracle.quantize_act(ya, l2["a_bits"], True)
+    qa = oracle.quantize_act_static(ya, l2["a_bits"], True, s2)
+    qb = oracle.quantize_act_static(yb, l2["a_bits"], True, s2)
+    assert not np.array_equal(qa, qb)
+    wa = sq.soniq_pack_weights(torch.from_numpy(la["W"]).cuda(), la["w_bits"], la["a_bits"], True)
+    wb = sq.soniq_pack_weights(torch.from_numpy(lb["W"]).cuda(), lb["w_bits"], lb["a_bits"], True)
+    w2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], True)
+    ha, hb, h2 = sq.soniq_act_create(wa, M), sq.soniq_act_create(wb, M), sq.soniq_act_create(w2, M)
+    Aa, Ab = torch.from_numpy(la["A"]).cuda(), torch.from_numpy(lb["A"]).cuda()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm: builds A's table outside the capture
+        sq.soniq_quantize_act(ha, Aa)
+        sq.soniq_mp_gemm_quantize_next(ha, wa, h2, s2)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        sq.soniq_quantize_act(ha, Aa)
+        sq.soniq_mp_gemm_quantize_next(ha, wa, h2, s2)
+    torch.cuda.synchronize()
+    for r in range(3):
+        sq.soniq_quantize_act(hb, Ab)
+        sq.soniq_mp_gemm_quantize_next(hb, wb, h2, s2)   # eager, producer B
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(sq.soniq_act_unpack_debug(h2)[0], qb, err_msg=f"eager B {r}")
+        g.replay()                                        # producer A, captured
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(sq.soniq_act_unpack_debug(h2)[0], qa, err_msg=f"replay A {r}")
+
+
+def test_next_must_not_be_the_producers_handle():
+    """A square layer fed back into its own activation handle would have its
+    scales overwritten before the GEMM reads them: rejected, nothing run."""
+    l = workloads.generic(64, 256, 256, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                          w_frac_lo=0.7, a_signed=True, seed=74, name="square")
+    w = sq.soniq_pack_weights(torch.from_numpy(l["W"]).cuda(), l["w_bits"], l["a_bits"], True)
+    h = sq.soniq_act_create(w, 64)
+    sq.soniq_quantize_act(h, torch.from_numpy(l["A"]).cuda())
+    with pytest.raises(sq.SoniqError) as e:
+        sq.soniq_mp_gemm_quantize_next(h, w, h, np.ones(w.S, np.float32))
+    assert e.value.status == sq.SONIQ_ERR_INVALID_ARGUMENT

@@ -228,6 +228,36 @@ def test_acc_equals_fp64_blas_per_group():
         np.testing.assert_array_equal(r["acc"][g], ref.astype(np.int64))
 
 
+@pytest.mark.parametrize("S", [1, 2, 5])
+def test_sampled_mac_equals_integer_products(S):
+    """The sampled MAC (one output's sums at given (m, n) pairs, used to check
+    outputs one by one at sizes the full MAC cannot reach) against numpy
+    int64 products over each scale group's channels, and against the pinned
+    full MAC: corners, repeated pairs, a group with no channel, and a pair
+    whose row and column indices differ (catches swapped m and n)."""
+    rng = np.random.default_rng(40 + S)
+    M, N, K = 23, 37, 301
+    q_a = rng.integers(-128, 128, (M, K)).astype(np.int32)
+    q_w = rng.integers(-128, 128, (N, K)).astype(np.int32)
+    # scale group of each channel: S groups in a shuffled order, the last
+    # one empty when S > 2 (its sums must be 0)
+    used = max(1, S - 1) if S > 2 else S
+    grp = rng.integers(0, used, K).astype(np.int32)
+    ms = np.concatenate([rng.integers(0, M, 200), [0, 0, M - 1, M - 1, 3, 3]])
+    ns = np.concatenate([rng.integers(0, N, 200), [0, N - 1, 0, N - 1, 30, 30]])
+    got = oracle.mac_at(q_a, q_w, grp, S, ms, ns)
+    assert got.shape == (ms.shape[0], S)
+    for i, (m, n) in enumerate(zip(ms, ns)):
+        for g in range(S):
+            cols = grp == g
+            want = int(q_a[m, cols].astype(np.int64) @ q_w[n, cols].astype(np.int64))
+            assert got[i, g] == want, (i, g)
+    full = oracle.mac(q_a, q_w, grp, S)
+    np.testing.assert_array_equal(got, full[:, ms, ns].T.astype(np.int64))
+    if S > 2:
+        assert (got[:, S - 1] == 0).all()
+
+
 def _bit_extract(words, j, c):
     per = 32 // c
     return (int(words[j // per]) >> ((j % per) * c)) & ((1 << c) - 1)
