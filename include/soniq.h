@@ -242,6 +242,36 @@ soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float*
                                     int64_t lda, uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,
                                     void* stream);
 
+/*
+ * soniq_quantize_mp_gemm_scratch -- soniq_quantize_mp_gemm without an
+ * activation handle and without allocating: for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  The packed activations, their
+ * scales, the partial maxima and the single pass's grid state live in a
+ * per-device scratch array of the library (64 MiB, held by every device the
+ * library runs on until the process ends) instead of a handle's buffers.
+ * Same results as soniq_quantize_act + soniq_mp_gemm on a handle made for w
+ * (Y and the optional accumulators; the codes are not kept for a later
+ * call).  No hipMalloc, hipFree or other allocation happens in the call;
+ * the first call on a device looks up the scratch address and clears its
+ * grid state with a small kernel on `stream`.
+ *
+ *   w        packed weights (any packing).
+ *   A_dev    device, float32 [M, lda], as for soniq_quantize_act.
+ *   M        >= 1; the packed rows (M rounded up to 256) with the handle's
+ *            other buffers must fit the scratch: about M * K bytes at 8-bit
+ *            activations, e.g. M = 8192 at K = 8192 fits.
+ *   Y_dev, ldy, acc_dev  as for soniq_mp_gemm.
+ * Every call on a device shares that device's scratch: calls that overlap
+ * in time on one device (other streams, other threads) race and give wrong
+ * results; serialize them.  Enqueued on `stream`.
+ * Errors: INVALID_ARGUMENT (null, sizes), UNSUPPORTED (M too large for the
+ * scratch), HIP.
+ */
+soniq_status soniq_quantize_mp_gemm_scratch(soniq_weights w, const float* A_dev, int64_t M,
+                                            int64_t lda, uint16_t* Y_dev, int64_t ldy,
+                                            int32_t* acc_dev, void* stream);
+
 /* Description of a packed weights handle. */
 typedef struct {
   int64_t N, K;               /* logical sizes */

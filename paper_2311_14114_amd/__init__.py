@@ -32,6 +32,7 @@ EXPORTED = [
     "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_pack_weights_grouped",
     "soniq_act_create",
     "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_quantize_mp_gemm",
+    "soniq_quantize_mp_gemm_scratch",
     "soniq_mp_gemm_quantize_next",
     "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
@@ -90,6 +91,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_mp_gemm_quantize_next.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp]
         L.soniq_quantize_mp_gemm.restype = st
         L.soniq_quantize_mp_gemm.argtypes = [vp, vp, vp, i64, i64, vp, i64, vp, vp]
+        L.soniq_quantize_mp_gemm_scratch.restype = st
+        L.soniq_quantize_mp_gemm_scratch.argtypes = [vp, vp, i64, i64, vp, i64, vp, vp]
         L.soniq_weights_info.restype = st
         L.soniq_weights_info.argtypes = [vp, ctypes.POINTER(WeightsInfo)]
         L.soniq_plan_input_channels.restype = st
@@ -272,6 +275,31 @@ def soniq_quantize_mp_gemm(act: Activations, weights: Weights, A, out=None, acc=
     _check(lib().soniq_quantize_mp_gemm(act.handle, weights.handle, _dev(A, "float32"), M, A.stride(0),
                                         _dev(out, "bf16"), out.stride(0), accp, _stream(stream)))
     act.M = M
+    return out
+
+
+def soniq_quantize_mp_gemm_scratch(weights: Weights, A, out=None, acc=None, stream=None):
+    """soniq_quantize_mp_gemm without an activation handle: the library's
+    per-device scratch holds the packed activations, and the call allocates
+    nothing (pass `out` to keep the binding from allocating Y).  Returns Y."""
+    import torch
+    if A.dtype != torch.float32 or A.dim() != 2 or A.stride(1) != 1:
+        raise TypeError("A must be a 2-D float32 device tensor with unit column stride")
+    if A.shape[1] != weights.K:
+        raise ValueError("A has the wrong number of input channels")
+    M, N = A.shape[0], weights.N
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or out.shape[0] < M:
+        raise TypeError("out must be a bf16 [M, >=N] device tensor with unit column stride")
+    accp = None
+    if acc is not None:
+        if acc.dtype != torch.int32 or not acc.is_contiguous() or tuple(acc.shape) != (weights.S, M, N):
+            raise TypeError("acc must be a contiguous int32 [S, M, N] device tensor")
+        accp = _dev(acc, "int32")
+    _check(lib().soniq_quantize_mp_gemm_scratch(weights.handle, _dev(A, "float32"), M, A.stride(0),
+                                                _dev(out, "bf16"), out.stride(0), accp,
+                                                _stream(stream)))
     return out
 
 

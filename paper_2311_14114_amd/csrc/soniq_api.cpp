@@ -335,7 +335,7 @@ int decode_signed(uint32_t f, int c) {
 }
 
 // The launches behind the entry points, on validated arguments: an
-// activation handle's buffers.
+// activation handle's buffers (or their stand-ins in the device scratch).
 soniq_status run_quantize(soniq_act_s& act, const float* A_dev, int64_t M, int64_t lda,
                           hipStream_t st) {
   const soniq_weights w = act.w;
@@ -760,6 +760,48 @@ soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float*
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: ldy < N");
   return run_quantize_gemm(*act, A_dev, M, lda, Y_dev, ldy, acc_dev,
                            reinterpret_cast<hipStream_t>(stream));
+}
+
+soniq_status soniq_quantize_mp_gemm_scratch(soniq_weights w, const float* A_dev, int64_t M,
+                                            int64_t lda, uint16_t* Y_dev, int64_t ldy,
+                                            int32_t* acc_dev, void* stream) {
+  if (!live_w(w) || !A_dev || !Y_dev)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: bad handle or null");
+  if (M < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: M < 1");
+  if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: lda < K");
+  if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: ldy < N");
+  // The activation buffers an activation handle for M rows would own, laid
+  // out in the device's scratch: grid state, scales, partial maxima, packed
+  // rows.
+  if (M > ((int64_t)1 << 31) - kMAlign)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_quantize_mp_gemm_scratch: M=%lld too large",
+                (long long)M);
+  const int64_t M_alloc = round_up(M, kMAlign);
+  const ActPlan ap = make_act_plan(*w, M_alloc);
+  const size_t nscale = (size_t)std::max(2, w->scales());
+  const size_t npart = std::max((size_t)2 * kAbsmaxBlocks,
+                                w->act_group_bits ? (size_t)kGAbsParts * nscale : 0);
+  const size_t packed_off = (size_t)round_up((int64_t)(kScratchPartialOff + 4 * npart), 256);
+  const size_t need = packed_off + (size_t)act_bytes(ap, M_alloc);
+  if (4 * nscale > kScratchPartialOff - kScratchScalesOff || need > kScratchBytes)
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_quantize_mp_gemm_scratch: M=%lld needs %zu bytes of scratch, more than its "
+                "%zu (use an activation handle)",
+                (long long)M, need, kScratchBytes);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* base = nullptr;
+  HIP_TRY(scratch_device_ptr(st, &base));
+  soniq_act_s a;
+  a.w = w;
+  a.max_M = M;
+  a.M_alloc = M_alloc;
+  a.ap = ap;
+  a.packed_bytes = act_bytes(ap, M_alloc);
+  a.counter = reinterpret_cast<unsigned int*>(base);
+  a.s_a = reinterpret_cast<float*>(base + kScratchScalesOff);
+  a.partial = reinterpret_cast<float*>(base + kScratchPartialOff);
+  a.packed = base + packed_off;
+  return run_quantize_gemm(a, A_dev, M, lda, Y_dev, ldy, acc_dev, st);
 }
 
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,

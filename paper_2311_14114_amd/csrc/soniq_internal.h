@@ -41,6 +41,15 @@ constexpr int kAbsmaxBlocks = 1024;  // max partial maxima (pairs) per activatio
 constexpr int kActStateWords = 8192;
 // The word of that state that counts timed-out grid waits (never reset).
 constexpr int kActStallWord = kActStateWords - 32;
+// Device scratch of the allocation-free entry point: one per device, held
+// until the process ends.  Its layout for a call: the grid state, the
+// scales, the partial maxima, then the packed activations.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr size_t kScratchScalesOff = (size_t)kActStateWords * 4;
+constexpr size_t kScratchPartialOff = kScratchScalesOff + 4096;
+// Address of this device's scratch (set up on the first call per device,
+// with a fill kernel on `stream` that clears its grid state).
+hipError_t scratch_device_ptr(hipStream_t stream, uint8_t** out);
 
 // Quantizer of one width: code = sign1 ? (x < 0 ? -1 : +1)
 //                                : clamp(rint(x / s), lo, hi), s = max/qdiv.

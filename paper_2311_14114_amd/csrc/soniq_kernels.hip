@@ -34,6 +34,7 @@
 #include <utility>
 
 #include <cstdlib>
+#include <mutex>
 
 namespace soniq {
 namespace {
@@ -4505,6 +4506,47 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
     hipLaunchKernelGGL((k_gemm_g<1, 0, 0, 0, 0>), grid, blk, 0, stream, a);
   }
   return hipGetLastError();
+}
+
+// ------------------------------------------------------- scratch memory --
+// Working memory of the allocation-free entry point
+// (soniq_quantize_mp_gemm_scratch): the grid state, partial maxima, scales
+// and packed activations that an activation handle would own.  Each device
+// the library runs on holds its own copy until the process ends.  In host
+// code `scratch` names a host-side stand-in, not device memory: kernels get
+// the per-device address that hipGetSymbolAddress returns.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+__global__ __launch_bounds__(256) void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t v) {
+  for (int i = (int)(blockIdx.x * 256 + threadIdx.x); i < n; i += (int)(gridDim.x * 256)) p[i] = v;
+}
+
+hipError_t scratch_device_ptr(hipStream_t stream, uint8_t** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static uint8_t* ptr[kMaxDevices] = {};
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    // The grid-state words must start at zero; the barrier protocol leaves
+    // them at zero after every call, so they are cleared once, on the
+    // caller's stream ahead of the first call's kernels (a fill kernel, not
+    // a memset node, in case that call is being captured).
+    hipLaunchKernelGGL(k_fill_u32, dim3(8), dim3(256), 0, stream, reinterpret_cast<uint32_t*>(p),
+                       kActStateWords, 0u);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    ptr[dev] = static_cast<uint8_t*>(p);
+  }
+  *out = ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace soniq
