@@ -2024,6 +2024,212 @@ __device__ __forceinline__ void gemm_group_fast(uint8_t* lds, const uint8_t* aba
 #endif
 }
 
+// ----------------------------------------------------------- wide stages --
+// A stage of a tile of one weight width holds as many granules as its two
+// containers allow in the ring slot, so narrow operands (4-bit activations
+// against 2-bit weights, say) fill a slot with 4 or 6 granules instead of
+// 2: fewer stages per group, so fewer memory round trips and barriers on
+// short K.  A granule of a BM x 128 tile holds BM*8*CA activation bytes and
+// 1024*CB weight bytes; each side's stage region is a whole number of
+// 4 KB load rounds (256 lanes x 16 bytes).
+constexpr int wide_loads(int chunks) { return (chunks + 255) / 256; }
+constexpr int wide_bytes(int WFM, int CA, int CB, int g) {
+  return 4096 * (wide_loads(16 * WFM * g * CA) + wide_loads(64 * g * CB));
+}
+constexpr int wide_gps(int WFM, int CA, int CB, int slot) {
+  int best = 2;
+  for (int g = 4; g <= 8; g += 2)
+    if (wide_bytes(WFM, CA, CB, g) <= slot) best = g;
+  return best;
+}
+
+// Granule KK of a wide stage: B fragments of the wave's four blocks (block
+// jj at jj*GPS*128*CB from b_addr), A fragments of its WFM m-blocks (m-block
+// i at i*GPS*128*CA from a_addr), both at granule offset KK*128*C.
+template <int C, int GPS, int KK, int N, int... I>
+__device__ __forceinline__ void wide_units(raw_t<C> (&r)[N], uint32_t addr,
+                                           std::integer_sequence<int, I...>) {
+  ((r[I] = lds_unit<C, (I * GPS + KK) * 128 * C>(addr)), ...);
+}
+
+template <int CA, int CB, int WFM, int GPS, int KK>
+__device__ __forceinline__ void wide_read(raw_t<CB> (&rb)[4], raw_t<CA> (&ra)[WFM], uint32_t a_addr,
+                                          uint32_t b_addr) {
+  wide_units<CB, GPS, KK>(rb, b_addr, std::make_integer_sequence<int, 4>{});
+  wide_units<CA, GPS, KK>(ra, a_addr, std::make_integer_sequence<int, WFM>{});
+}
+
+template <int CA, int CB, int WFM>
+__device__ __forceinline__ void wide_mma(v4i (&acc)[WFM][4], raw_t<CB> (&rb)[4], raw_t<CA> (&ra)[WFM]) {
+  v4i bf[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    lds_touch(rb[jj]);
+    bf[jj] = unpack_frag<CB>(rb[jj]);
+  }
+#pragma unroll
+  for (int i = 0; i < WFM; ++i) {
+    lds_touch(ra[i]);
+    const v4i af = unpack_frag<CA>(ra[i]);
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      acc[i][jj] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf[jj], acc[i][jj], 0, 0, 0);
+  }
+}
+
+// R granules of one wide stage, straight-line: granule KK+1's reads are
+// issued before granule KK is widened and multiplied, so an LDS round trip
+// hides behind the products of the granule before.  The two register sets
+// alternate at compile time and no branch joins values of reads still in
+// flight (a join would let the register allocator copy such a register
+// before its wait).
+template <int CA, int CB, int WFM, int GPS, int R, int KK>
+__device__ __forceinline__ void wide_granules(v4i (&acc)[WFM][4], raw_t<CB> (&b0)[4],
+                                              raw_t<CA> (&a0)[WFM], raw_t<CB> (&b1)[4],
+                                              raw_t<CA> (&a1)[WFM], uint32_t a_addr,
+                                              uint32_t b_addr) {
+  if constexpr (KK < R) {
+    constexpr bool odd = (KK & 1) != 0;
+    if constexpr (KK + 1 < R) {
+      if constexpr (odd) wide_read<CA, CB, WFM, GPS, KK + 1>(b0, a0, a_addr, b_addr);
+      else wide_read<CA, CB, WFM, GPS, KK + 1>(b1, a1, a_addr, b_addr);
+      lds_wait_n<4 + WFM>();
+    } else {
+      lds_wait();
+    }
+    if constexpr (odd) wide_mma<CA, CB, WFM>(acc, b1, a1);
+    else wide_mma<CA, CB, WFM>(acc, b0, a0);
+#if defined(__HIP_DEVICE_COMPILE__)
+    // keep these products ahead of the next granule's wait
+    __builtin_amdgcn_sched_barrier(0);
+#endif
+    wide_granules<CA, CB, WFM, GPS, R, KK + 1>(acc, b0, a0, b1, a1, a_addr, b_addr);
+  }
+}
+
+template <int CA, int CB, int WFM, int GPS, int R>
+__device__ __forceinline__ void wide_stage(v4i (&acc)[WFM][4], uint32_t a_addr, uint32_t b_addr) {
+  raw_t<CB> b0[4], b1[4];
+  raw_t<CA> a0[WFM], a1[WFM];
+  wide_read<CA, CB, WFM, GPS, 0>(b0, a0, a_addr, b_addr);
+  wide_granules<CA, CB, WFM, GPS, R, 0>(acc, b0, a0, b1, a1, a_addr, b_addr);
+}
+
+// A stage with rem valid granules (rem >= GPS: a full one); each count is
+// its own straight-line body.
+template <int CA, int CB, int WFM, int GPS, int R = GPS>
+__device__ __forceinline__ void wide_stage_rem(v4i (&acc)[WFM][4], uint32_t a_addr, uint32_t b_addr,
+                                               int rem) {
+  if constexpr (R >= 1) {
+    if (rem >= R) wide_stage<CA, CB, WFM, GPS, R>(acc, a_addr, b_addr);
+    else wide_stage_rem<CA, CB, WFM, GPS, R - 1>(acc, a_addr, b_addr, rem);
+  }
+}
+
+// One activation group's K loop on a tile of one weight width (CA, CB
+// fixed), BM x 128 (BM = 32*WFM), waves 2 x 2, through an NST-deep ring of
+// SLOT-byte slots, GPS granules per stage (wide_gps).  Slot layout: the A
+// stage (m-block i, granule kk at (i*GPS + kk)*128*CA), then at ABYTES the
+// B stage (block j, granule kk at (j*GPS + kk)*128*CB).  Loads go through
+// buffer resources; chunks past the group's data, and lanes past a stage's
+// chunks, read as zero (their products vanish).
+template <int CA, int CB, int WFM, int NST, int SLOT>
+__device__ __forceinline__ void gemm_group_wide(uint8_t* lds, const uint8_t* abase, int64_t mstride,
+                                                int ng, const uint8_t* wtile, int wbytes, int ngt,
+                                                int qbase, v4i (&acc)[WFM][4], int tid, int lane,
+                                                int wid, int wm, int wn) {
+#if defined(__HIP_DEVICE_COMPILE__)  // GPU builtins; the host pass never runs it
+  constexpr int BM = 32 * WFM;
+  constexpr int GPS = wide_gps(WFM, CA, CB, SLOT);
+  constexpr int CHA = 16 * WFM * GPS * CA;  // A chunks per stage
+  constexpr int CHB = 64 * GPS * CB;        // B chunks per stage
+  constexpr int LA = wide_loads(CHA), LB = wide_loads(CHB);
+  constexpr int L = LA + LB;
+  constexpr int ABYTES = 4096 * LA;
+  static_assert(4096 * (LA + LB) <= SLOT, "a wide stage fits its slot");
+  static_assert((GPS - 1 + 3 * GPS) * 128 * CB + ABYTES < 65536 && (WFM * GPS) * 128 * CA < 65536,
+                "ds offsets");
+  const int nst = (ng + GPS - 1) / GPS;
+
+  const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)abase, (short)0, (int)min((int64_t)0x7FFFFFF0, (int64_t)(BM / kBlk) * mstride), 0x00020000);
+  const __amdgpu_buffer_rsrc_t br =
+      __builtin_amdgcn_make_buffer_rsrc((void*)wtile, (short)0, wbytes, 0x00020000);
+
+  // A chunk ci of a stage: m-block ci / (GPS*8*CA), granule-in-stage
+  // (ci mod GPS*8*CA) / (8*CA); B chunk ci: block ci / (GPS*8*CB).
+  // Lanes past a stage's chunks read zeros (kOOB) into the region's tail.
+  uint32_t aoff[LA], boff[LB];
+#pragma unroll
+  for (int i = 0; i < LA; ++i) {
+    const int ci = i * 256 + tid;
+    const int mb = ci / (GPS * 8 * CA), w = ci - mb * (GPS * 8 * CA);
+    aoff[i] = ci < CHA ? (uint32_t)(mb * mstride + w * 16) : kOOB;
+  }
+#pragma unroll
+  for (int i = 0; i < LB; ++i) {
+    const int ci = i * 256 + tid;
+    const int j = ci / (GPS * 8 * CB), w = ci - j * (GPS * 8 * CB);
+    boff[i] = ci < CHB ? (uint32_t)(j * ngt * 128 * CB + qbase * 128 * CB + w * 16) : kOOB;
+  }
+
+  // Stage st into ring slot `slot`; in a final partial stage (rem < GPS
+  // valid granules) the chunks of the missing granules read zeros, so
+  // their products vanish.
+  auto issue = [&](int st, int slot) __attribute__((always_inline)) {
+    const int rem = ng - st * GPS;
+    const uint32_t ldsb = lds_off(lds) + (uint32_t)(slot * SLOT);
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+      const int q = ((i * 256 + tid) % (GPS * 8 * CA)) / (8 * CA);  // granule in the stage
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ar, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + (i * 256 + wid * 64) * 16), 16,
+          rem >= GPS || q < rem ? aoff[i] : kOOB, st * GPS * 128 * CA, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+      const int q = ((i * 256 + tid) % (GPS * 8 * CB)) / (8 * CB);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          br, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + ABYTES + (i * 256 + wid * 64) * 16),
+          16, rem >= GPS || q < rem ? boff[i] : kOOB, st * GPS * 128 * CB, 0, 0);
+    }
+  };
+
+  const uint32_t b_lds = lds_off(lds) + (uint32_t)(ABYTES + wn * 4 * GPS * 128 * CB + lane * 2 * CB);
+  const uint32_t a_lds = lds_off(lds) + (uint32_t)(wm * WFM * GPS * 128 * CA + lane * 2 * CA);
+
+  int issued = 0;
+  for (; issued < NST - 1 && issued < nst; ++issued) issue(issued, issued);
+  // Stage st's loads have landed for every wave, and the next stage's
+  // loads are in flight.
+  auto ready = [&](int st) __attribute__((always_inline)) {
+    const int later = issued - st - 1;
+    if (NST >= 4 && later == 2) wait_vm<(NST >= 4 ? 2 * L : 0)>();
+    else if (NST >= 3 && later == 1) wait_vm<(NST >= 3 ? L : 0)>();
+    else wait_vm<0>();
+    bar_nofence();
+    if (issued < nst) {
+      issue(issued, issued % NST);
+      ++issued;
+    }
+    return (uint32_t)((st % NST) * SLOT);
+  };
+  // Full stages share one loop body (one path, so the accumulators stay
+  // in place); a final partial stage runs once after it.
+  const int nfull = ng / GPS;
+  for (int st = 0; st < nfull; ++st) {
+    const uint32_t soff = ready(st);
+    wide_stage<CA, CB, WFM, GPS, GPS>(acc, a_lds + soff, b_lds + soff);
+  }
+  if (nfull < nst) {
+    const uint32_t soff = ready(nfull);
+    wide_stage_rem<CA, CB, WFM, GPS, GPS - 1>(acc, a_lds + soff, b_lds + soff, ng - nfull * GPS);
+  }
+  // Everyone is done reading the ring before the next group refills it.
+  bar_nofence();
+#endif
+}
+
 // One activation group's K loop of a BM x 128 tile (BM = 32*WFM; waves 2x2,
 // wave tile (16*WFM) x 64), through an NST-deep LDS ring.  Stage = 2
 // granules.  A stage in LDS: m-block i granule kk at (2i + kk)*128*ca; B
@@ -2167,10 +2373,16 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
 // next-layer group (QN = 1) or per block of a next layer with sub-group
 // scales (QN = 2, asked to keep three waves per SIMD).
 template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QN == 2 ? 3 : 1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
+    QN == 2 ? 3 : QN == 1 ? 1 : WFM == 2 ? 3 : 2)))
 void k_gemm(GemmArgs a) {
   constexpr int BM = 32 * WFM;
-  constexpr int SLOT = gemm_slot(S, CA0, CA1, CBL, CBH, WFM);
+  // Instances whose containers are all known take at least 24 KB slots at
+  // 64-row tiles (three workgroups per CU still fit LDS), so narrow
+  // operands get wide stages (gemm_group_wide).
+  constexpr bool KNOWN = CA0 != 0 && (S == 1 || CA1 != 0) && CBL != 0 && CBH != 0;
+  constexpr int SLOT0 = gemm_slot(S, CA0, CA1, CBL, CBH, WFM);
+  constexpr int SLOT = KNOWN && WFM == 2 && SLOT0 < 24576 ? 24576 : SLOT0;
   constexpr int ASLOT = gemm_aslot(S, CA0, CA1, CBL, CBH, WFM);
   __shared__ __align__(16) uint8_t lds[NST * SLOT];
   const int tid = threadIdx.x;
@@ -2235,13 +2447,11 @@ void k_gemm(GemmArgs a) {
     constexpr int CA = decltype(ca_tag)::value;
     if constexpr (CA != 0 && CBL != 0 && CBH != 0) {
       if (CBL == CBH || tile_lo)
-        gemm_group_fast<CA, CBL, CBL, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ng, wtile, wbytes,
-                                                             a.wp.ngt, bc, bpre, qbase, acc, tid,
-                                                             lane, wid, wm, wn);
+        gemm_group_wide<CA, CBL, WFM, NST, SLOT>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
+                                                 qbase, acc, tid, lane, wid, wm, wn);
       else
-        gemm_group_fast<CA, CBH, CBH, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ng, wtile, wbytes,
-                                                             a.wp.ngt, bc, bpre, qbase, acc, tid,
-                                                             lane, wid, wm, wn);
+        gemm_group_wide<CA, CBH, WFM, NST, SLOT>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
+                                                 qbase, acc, tid, lane, wid, wm, wn);
     } else {
       gemm_group_any<CA, CBL, CBH, WFM, NST, ASLOT, SLOT>(lds, abase, mstride, ca_rt, ng, wtile,
                                                           a.wp.ngt, bc, bpre, qbase, acc, tid,
