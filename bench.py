@@ -82,7 +82,7 @@ def uses_gemv(case) -> bool:
     return case["M"] <= 8 and not case.get("act_group_bits", 0)
 
 
-def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
+def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6f4=False):
     import torch
     import paper_2311_14114_amd as sq
 
@@ -99,7 +99,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
     gbits = case.get("act_group_bits", 0)
     nib = sign_nibbles(case)
     ws = [sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                act_group_bits=gbits, sign_nibbles=nib)]
+                                act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4)]
     e1.record(stream)
     torch.cuda.synchronize()
     pack_ms = e0.elapsed_time(e1)
@@ -109,7 +109,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False):
         nw = max(1, min(MAX_W_COPIES, math.ceil(ROTATE_W_BYTES / int(info.packed_w_bytes))))
     for _ in range(nw - 1):
         ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                        act_group_bits=gbits, sign_nibbles=nib))
+                                        act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4))
     acts = [sq.soniq_act_create(w, M) for w in ws]
     # the quantizer's input: the lowered matrix A, or (conv_input) the
     # convolution's NCHW tensor X, whose 3x3 lowering A is
@@ -455,6 +455,9 @@ def main():
     ap.add_argument("--conv-input", action="store_true",
                     help="conv workloads: quantize from the NCHW input tensor "
                          "(soniq_quantize_act_conv3x3) instead of the lowered matrix")
+    ap.add_argument("--f8f6f4", action="store_true",
+                    help="pack the weights with SONIQ_WPACK_F8F6F4: narrow x narrow tiles run on the "
+                         "fp4/fp6 MFMA")
     ap.add_argument("--launch", choices=["graph", "eager"], default="graph",
                     help="replay the timed steps as one captured HIP graph (default) or "
                          "launch every call from the host")
@@ -478,7 +481,7 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     r = run_gpu(case, args.steps, args.warmup, rotate=not args.no_rotate,
-                graph=args.launch == "graph", conv_input=args.conv_input)
+                graph=args.launch == "graph", conv_input=args.conv_input, f8f6f4=args.f8f6f4)
     alg = algorithmic(case, r["info"])
     if args.conv_input:
         alg["a_fp32"] = int(case["X"].nbytes)  # the quantizer reads X, not its lowering
@@ -495,6 +498,7 @@ def main():
                    "a_signed": bool(case["a_signed"]),
                    "act_group_bits": int(case.get("act_group_bits", 0)),
                    "sign_weights_container": 4 if sign_nibbles(case) else 1,
+                   "f8f6f4_copies": bool(args.f8f6f4),
                    "activation_copies": r["na"], "weight_copies": r["nw"],
                    "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
                    "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input

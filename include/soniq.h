@@ -75,6 +75,23 @@ enum { SONIQ_WQ_SYMMETRIC = 0, SONIQ_WQ_TWOS_FRACTION = 1 };
  * the default bits. */
 #define SONIQ_WPACK_SIGN_NIBBLES 0x100
 
+/* Packing flag, OR-ed into wq_mode: also keep the narrow operands in the
+ * fp4 / fp6 operand formats of gfx950's v_mfma_scale_f32_16x16x128_f8f6f4,
+ * so tiles of narrow weights against narrow activations run on that
+ * instruction (128 channels per step, no widening to bytes) instead of the
+ * int8 MFMA.  1- and 2-bit containers map to fp4 (e2m1), 4-bit containers
+ * to fp6 (e3m2): every stored code is exactly representable, and with
+ * power-of-two block scales the fp32 sums equal the integer sums exactly
+ * (each partial sum is an integer multiple of the scale below 2^24 of it),
+ * so results are bit-identical to the integer path.  The low-precision MAC
+ * of the paper's hardware study (App. C; Sec. 7 findings on two-level
+ * palettes) is served by gfx950's narrow-float matrix instruction here.
+ * Costs a second copy of the narrow weights (fp4 or fp6 per element) and,
+ * per activation handle, of the narrow activation groups, refreshed before
+ * each MFMA GEMM.  Not combined with sub-group activation scales
+ * (UNSUPPORTED). */
+#define SONIQ_WPACK_F8F6F4 0x200
+
 /* Largest supported input-channel count (padded): keeps every int32
  * accumulator exact. */
 #define SONIQ_MAX_K 65536
@@ -286,6 +303,7 @@ typedef struct {
   int64_t packed_w_bytes_algorithmic; /* sum over rows of container*K/8 */
   int32_t act_group_bits;     /* GroupSize_act in bits, 0 = one scale per group */
   int32_t act_scales;         /* activation scales: blocks, or S when ungrouped */
+  int32_t f8f6f4;             /* 1: packed with SONIQ_WPACK_F8F6F4 */
 } soniq_weights_info_t;
 
 /* Fill *out.  Errors: INVALID_ARGUMENT. */

@@ -206,6 +206,11 @@ struct soniq_weights_s {
   int32_t* grp = nullptr;  // block of each original input channel
   int32_t* posg = nullptr;  // planned position | block << 16
   std::vector<int32_t> grp_h;  // host copy of grp
+  // MFMA-native copies (SONIQ_WPACK_F8F6F4): the weight side of the plan
+  // (formats, fgranule counts, region offsets) and the weight copy
+  bool f8f6f4 = false;
+  FPlan fplan{};
+  uint8_t* fw = nullptr;
 
   int scales() const { return act_group_bits ? nsub[0] + nsub[1] : kp.S; }
   WDev dev() const { return WDev{packed, blk_off, blk_c, colinfo, shw, tile_cols, colrank}; }
@@ -226,6 +231,11 @@ struct soniq_act_s {
   // the producer's per-physical-column table (position | group << 16)
   uint8_t* qn_img = nullptr;
   float* qn_brs = nullptr;  // reciprocals of static block scales (sub-group weights)
+  // MFMA-native copy of the narrow activation groups (weights packed with
+  // SONIQ_WPACK_F8F6F4), refreshed from the units before each MFMA GEMM;
+  // fplan = the weights' plan with this buffer's offsets
+  uint8_t* fa = nullptr;
+  FPlan fplan{};
   // one column table per producer weights handle (keyed by its serial),
   // kept until this handle is destroyed: a captured graph may still hold a
   // table's address after another producer has fed this handle
@@ -252,6 +262,7 @@ void free_weights(soniq_weights w) {
   (void)hipFree(w->seg);
   (void)hipFree(w->grp);
   (void)hipFree(w->posg);
+  (void)hipFree(w->fw);
   w->magic = kDead;
   delete w;
 }
@@ -296,6 +307,18 @@ ActPlan make_act_plan(const soniq_weights_s& w, int64_t M_alloc) {
 int64_t act_bytes(const ActPlan& ap, int64_t M_alloc) {
   int64_t off = 0;
   for (int g = 0; g < ap.S; ++g) off = round_up(off + (M_alloc / kBlk) * ap.mblk_bytes[g], 256);
+  return off;
+}
+
+// The activation side of an MFMA-native plan for M_alloc rows: each narrow
+// group's region in the activation copy; returns the copy's bytes.
+int64_t act_fplan(FPlan& fp, int64_t M_alloc) {
+  int64_t off = 0;
+  for (int g = 0; g < 2; ++g) {
+    fp.fa_off[g] = off;
+    fp.fa_mblk[g] = fp.fa[g] ? (int64_t)fp.nfg[g] * f_block_bytes(fp.fa[g]) : 0;
+    off = round_up(off + (M_alloc / kBlk) * fp.fa_mblk[g], 256);
+  }
   return off;
 }
 
@@ -362,7 +385,18 @@ soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* a
   else if (gemv)
     HIP_TRY(launch_mp_gemv(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                            acc_dev, st));
-  else
+  else if (act.fa) {
+    // refresh the MFMA-native copy of the narrow groups from the units the
+    // producer left, then the GEMM with both forms
+    const FPlan& fp = act.fplan;
+    for (int g = 0; g < act.ap.S; ++g)
+      if (fp.fa[g])
+        HIP_TRY(launch_to_fp(act.packed + act.ap.seg_off[g], act.ap.mblk_bytes[g], act.ap.c[g],
+                             act.ap.ng[g], (M + kBlk - 1) / kBlk, act.fa + fp.fa_off[g],
+                             fp.fa_mblk[g], fp.fa[g], st));
+    HIP_TRY(launch_mp_gemm(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                           acc_dev, st, &fp, act.fa, w->fw));
+  } else
     HIP_TRY(launch_mp_gemm(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                            acc_dev, st));
   return SONIQ_OK;
@@ -417,7 +451,11 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
   if (a_signed != 0 && a_signed != 1)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: a_signed must be 0 or 1");
   const bool sign_nibbles = (wq_mode & SONIQ_WPACK_SIGN_NIBBLES) != 0;
-  wq_mode &= ~SONIQ_WPACK_SIGN_NIBBLES;
+  const bool f8f6f4 = (wq_mode & SONIQ_WPACK_F8F6F4) != 0;
+  wq_mode &= ~(SONIQ_WPACK_SIGN_NIBBLES | SONIQ_WPACK_F8F6F4);
+  if (f8f6f4 && act_group_bits > 0)
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_pack_weights: SONIQ_WPACK_F8F6F4 with sub-group activation scales");
   if (wq_mode != SONIQ_WQ_SYMMETRIC && wq_mode != SONIQ_WQ_TWOS_FRACTION)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: unknown wq_mode %d", wq_mode);
   int wb[2], nw = 0;
@@ -598,6 +636,40 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
   STEP(launch_wpack(W_dev, N, K, ldw, wbits_dev, w->pos, w->seg, phys_dev, w->blk_off, w->blk_c,
                     w_qparam(b_lo, wq_mode), w_qparam(b_hi, wq_mode), b_lo, (int)w->kp.Kp,
                     w->packed, w->colinfo, st));
+  if (f8f6f4 && e == hipSuccess) {
+    // The MFMA-native copy of every (narrow activation group, narrow weight
+    // class) pair, converted from the units just packed.
+    FPlan& fp = w->fplan;
+    w->f8f6f4 = true;
+    const int ngr[2] = {(int)(w->kp.pad[0] / kGran), (int)(w->kp.pad[1] / kGran)};
+    for (int g = 0; g < 2; ++g) {
+      fp.fa[g] = g < w->kp.S ? f_fmt(a_container(w->kp.bits[g], a_signed)) : 0;
+      fp.nfg[g] = (ngr[g] + 1) / 2;
+    }
+    fp.fw[0] = f_fmt(wp.c_lo);
+    fp.fw[1] = f_fmt(wp.c_hi);
+    const int64_t cls_blocks[2] = {wp.nlo, wp.nblk - wp.nlo};
+    int64_t off = 0;
+    for (int g = 0; g < 2; ++g)
+      for (int k = 0; k < 2; ++k) {
+        fp.fw_off[g][k] = -1;
+        if (!fp.fa[g] || !fp.fw[k] || !cls_blocks[k]) continue;
+        fp.fw_off[g][k] = off;
+        off = round_up(off + cls_blocks[k] * fp.nfg[g] * f_block_bytes(fp.fw[k]), 256);
+      }
+    STEP(dev_alloc(&w->fw, (size_t)off));
+    for (int g = 0; g < 2; ++g)
+      for (int k = 0; k < 2; ++k) {
+        if (fp.fw_off[g][k] < 0 || e != hipSuccess) continue;
+        const int first = k ? wp.nlo : 0;
+        const int c = k ? wp.c_hi : wp.c_lo;
+        const int64_t qbase = g ? ngr[0] : 0;  // the group's first granule in a block
+        STEP(launch_to_fp(w->packed + wblk_off(wp, first) + qbase * 128 * c,
+                          (int64_t)wp.ngt * 128 * c, c, ngr[g], cls_blocks[k],
+                          w->fw + fp.fw_off[g][k], (int64_t)fp.nfg[g] * f_block_bytes(fp.fw[k]),
+                          fp.fw[k], st));
+      }
+  }
   STEP(hipStreamSynchronize(st));
 #undef STEP
   (void)hipFree(wbits_dev);
@@ -648,6 +720,7 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out) {
       (w->w_cnt[0] * w->wp.c_lo + w->w_cnt[1] * w->wp.c_hi) * w->K / 8;
   out->act_group_bits = w->act_group_bits;
   out->act_scales = w->scales();
+  out->f8f6f4 = w->f8f6f4 ? 1 : 0;
   return SONIQ_OK;
 }
 
@@ -672,9 +745,14 @@ soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
   if (e == hipSuccess) e = hipMemset(a->counter, 0, kActStateWords * sizeof(unsigned int));
   if (e == hipSuccess) e = hipMemset(a->s_a, 0, nscale * sizeof(float));
   if (e == hipSuccess) e = hipMemset(a->packed, 0, (size_t)a->packed_bytes);
+  if (e == hipSuccess && w->f8f6f4) {
+    a->fplan = w->fplan;
+    e = dev_alloc(&a->fa, (size_t)act_fplan(a->fplan, a->M_alloc));
+  }
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     soniq_status rc = fail_hip(e, "soniq_act_create");
+    (void)hipFree(a->fa);
     (void)hipFree(a->packed);
     (void)hipFree(a->partial);
     (void)hipFree(a->counter);
@@ -782,7 +860,10 @@ soniq_status soniq_quantize_mp_gemm_scratch(soniq_weights w, const float* A_dev,
   const size_t npart = std::max((size_t)2 * kAbsmaxBlocks,
                                 w->act_group_bits ? (size_t)kGAbsParts * nscale : 0);
   const size_t packed_off = (size_t)round_up((int64_t)(kScratchPartialOff + 4 * npart), 256);
-  const size_t need = packed_off + (size_t)act_bytes(ap, M_alloc);
+  FPlan fplan = w->fplan;
+  const size_t fa_off = packed_off + (size_t)round_up(act_bytes(ap, M_alloc), 256);
+  const size_t need = w->f8f6f4 ? fa_off + (size_t)act_fplan(fplan, M_alloc)
+                                : packed_off + (size_t)act_bytes(ap, M_alloc);
   if (4 * nscale > kScratchPartialOff - kScratchScalesOff || need > kScratchBytes)
     return fail(SONIQ_ERR_UNSUPPORTED,
                 "soniq_quantize_mp_gemm_scratch: M=%lld needs %zu bytes of scratch, more than its "
@@ -801,6 +882,10 @@ soniq_status soniq_quantize_mp_gemm_scratch(soniq_weights w, const float* A_dev,
   a.s_a = reinterpret_cast<float*>(base + kScratchScalesOff);
   a.partial = reinterpret_cast<float*>(base + kScratchPartialOff);
   a.packed = base + packed_off;
+  if (w->f8f6f4) {
+    a.fplan = fplan;
+    a.fa = base + fa_off;
+  }
   return run_quantize_gemm(a, A_dev, M, lda, Y_dev, ldy, acc_dev, st);
 }
 
@@ -956,6 +1041,7 @@ void soniq_act_destroy(soniq_act act) {
   (void)hipFree(act->qn_img);
   for (const auto& t : act->qn_tabs) (void)hipFree(t.second);
   (void)hipFree(act->qn_brs);
+  (void)hipFree(act->fa);
   act->magic = kDead;
   soniq_weights w = act->w;
   delete act;

@@ -108,6 +108,33 @@ __host__ __device__ inline uint64_t wblk_off(const WPlan& wp, int blk) {
   return ((uint64_t)lo * wp.c_lo + (uint64_t)(blk - lo) * wp.c_hi) * (uint64_t)wp.ngt * 128u;
 }
 
+// MFMA-native copies of narrow operands (handles packed with
+// SONIQ_WPACK_F8F6F4).  Beside the integer units above, a handle keeps the
+// codes of its narrow weight blocks and of its narrow activation groups in
+// the operand formats of v_mfma_scale_f32_16x16x128_f8f6f4, which takes
+// them straight from LDS with no widening: 1- and 2-bit containers as fp4
+// (e2m1), 4-bit containers as fp6 (e3m2); both hold every stored code
+// exactly (|code| <= 2, resp. <= 8).  The K axis of a precision group is
+// cut into "fgranules" of 128 channels (two granules; a final one of an
+// odd granule count is half zeros).  A 16-row block fgranule holds one unit
+// per lane: lane l = q*16 + r carries row r, channels [32q, 32q + 32), 16
+// bytes in fp4 (element e at bits 4e) or 24 bytes in fp6 (element e at bits
+// 6e of the 192-bit value), stored as the lane's first 16 bytes at 16*l and,
+// in fp6, its last 8 bytes at 1024 + 8*l.
+constexpr int kFmtFp6 = 3;  // MFMA operand format code of e3m2
+constexpr int kFmtFp4 = 4;  // of e2m1
+__host__ __device__ constexpr int f_fmt(int c) { return c <= 2 ? kFmtFp4 : c == 4 ? kFmtFp6 : 0; }
+__host__ __device__ constexpr int f_block_bytes(int fmt) { return fmt == kFmtFp4 ? 1024 : 1536; }
+
+struct FPlan {
+  int fa[2];            // format of activation group g's copy (0: none)
+  int nfg[2];           // fgranules of group g
+  int fw[2];            // format of the narrow / wide weight blocks' copy (0: none)
+  int64_t fw_off[2][2];  // [group][class] byte offset of that region in the weight copy
+  int64_t fa_off[2];     // byte offset of group g's region in the activation copy
+  int64_t fa_mblk[2];    // bytes of one 16-row block of that region
+};
+
 struct WDev {
   const uint8_t* packed;
   const uint64_t* blk_off;  // byte offset of each block
@@ -191,7 +218,15 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
-                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);
+                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream,
+                          const FPlan* fp = nullptr, const uint8_t* fa = nullptr,
+                          const uint8_t* fw = nullptr);
+
+// Converts integer units to their MFMA-native copy: `nblk` 16-row blocks,
+// block b's units at src + b*src_bstride (ng granules of container c),
+// its copy (fmt) at dst + b*dst_bstride.
+hipError_t launch_to_fp(const uint8_t* src, int64_t src_bstride, int c, int ng, int64_t nblk,
+                        uint8_t* dst, int64_t dst_bstride, int fmt, hipStream_t stream);
 
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,

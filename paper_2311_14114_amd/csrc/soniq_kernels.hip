@@ -1637,6 +1637,10 @@ struct GemmArgs {
   const float* qn_bs;
   const float* qn_brs;
   int qn_nsub0;
+  // MFMA-native copies of the narrow operands (null: none), and their plan
+  const uint8_t* fa;
+  const uint8_t* fw;
+  FPlan fp;
 };
 
 // 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
@@ -2367,12 +2371,180 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
   bar_nofence();
 }
 
+// ------------------------------------------------------ f8f6f4 tiles --
+// One unit of an MFMA-native copy in LDS, as the raw registers of its reads:
+// the lane's first 16 bytes at a + OFF, and for fp6 its last 8 bytes at
+// a8 + OFF (a8 = this lane's address in the fp6 tail region).  The operand
+// (8-dword type of the instruction; the unused dwords are never read by it)
+// is assembled only after the reads have landed (f_operand), so that no
+// register move can read a destination still in flight.
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+struct FRaw {
+  u32x4v lo;
+  u32x2v hi;
+};
+
+template <int FMT, int OFF>
+__device__ __forceinline__ FRaw lds_funit(uint32_t a, uint32_t a8) {
+  static_assert(OFF >= 0 && OFF + 1024 < 65536, "ds offset range");
+  FRaw r{};
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r.lo) : "v"(a), "i"(OFF));
+  if constexpr (FMT == kFmtFp6) asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(r.hi) : "v"(a8), "i"(OFF));
+#else
+  (void)a;
+  (void)a8;
+#endif
+  return r;
+}
+
+template <int FMT, int STRIDE, int N, int... I>
+__device__ __forceinline__ void lds_funits(FRaw (&r)[N], uint32_t a, uint32_t a8,
+                                           std::integer_sequence<int, I...>) {
+  ((r[I] = lds_funit<FMT, I * STRIDE>(a, a8)), ...);
+}
+
+// After the wait: pin the raw registers below it, then form the operand.
+template <int FMT>
+__device__ __forceinline__ v8i f_operand(FRaw& r) {
+  lds_touch(r.lo);
+  if constexpr (FMT == kFmtFp6) lds_touch(r.hi);
+  v8i o{};
+  o[0] = (int)r.lo.x;
+  o[1] = (int)r.lo.y;
+  o[2] = (int)r.lo.z;
+  o[3] = (int)r.lo.w;
+  if constexpr (FMT == kFmtFp6) {
+    o[4] = (int)r.hi.x;
+    o[5] = (int)r.hi.y;
+  }
+  return o;
+}
+
+constexpr int f_rounds(int bytes) { return (bytes / 16 + 255) / 256; }
+
+// One activation group's K loop on the MFMA-native copies: A (format FA)
+// against a tile of narrow weights (format FB), one fgranule (128
+// channels) per stage, through as deep a ring as LDSB bytes hold (at most
+// four).  Each wave multiplies its (16*WFM) x 64 block with
+// v_mfma_scale_f32_16x16x128_f8f6f4, block scales 2^sha and 2^shw (the
+// unpack exponents of the integer path, so each fp32 sum is that path's raw
+// integer sum exactly), and converts the sums to int32 at the end.
+// fa_tile: the group's copy at the tile's first row block (block stride
+// fa_mblk); fw_tile: the tile's first weight block (block stride
+// nfg*block bytes).
+template <int FA, int FB, int WFM, int LDSB>
+__device__ __forceinline__ void gemm_group_f(uint8_t* lds, const uint8_t* fa_tile, int64_t fa_mblk,
+                                             const uint8_t* fw_tile, int wblocks, int nfg, int sha,
+                                             int shw,
+                                             v4i (&acc)[WFM][4], int tid, int lane, int wid, int wm,
+                                             int wn) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int BM = 32 * WFM;
+  constexpr int FBA = f_block_bytes(FA), FBB = f_block_bytes(FB);
+  constexpr int CHA = (BM / kBlk) * FBA / 16, CHB = 8 * FBB / 16;  // chunks per stage
+  constexpr int LA = f_rounds((BM / kBlk) * FBA), LB = f_rounds(8 * FBB);
+  constexpr int L = LA + LB;
+  constexpr int ABYTES = 4096 * LA, SLOTF = 4096 * (LA + LB);
+  constexpr int NSTF = LDSB / SLOTF >= 4 ? 4 : LDSB / SLOTF;
+  static_assert(NSTF >= 2, "at least a double ring");
+
+  const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)fa_tile, (short)0, (int)min((int64_t)0x7FFFFFF0, (int64_t)(BM / kBlk) * fa_mblk), 0x00020000);
+  // the weight region ends after `wblocks` of the tile's blocks (a tile of
+  // a single-width handle may run past its class); beyond reads zeros
+  const int64_t wbytes = (int64_t)min(8, wblocks) * nfg * FBB;
+  const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)fw_tile, (short)0, (int)min((int64_t)0x7FFFFFF0, wbytes), 0x00020000);
+  uint32_t aoff[LA], boff[LB];
+#pragma unroll
+  for (int i = 0; i < LA; ++i) {
+    const int ci = i * 256 + tid;
+    const int mb = ci / (FBA / 16), w = ci - mb * (FBA / 16);
+    aoff[i] = ci < CHA ? (uint32_t)(mb * fa_mblk + w * 16) : kOOB;
+  }
+#pragma unroll
+  for (int i = 0; i < LB; ++i) {
+    const int ci = i * 256 + tid;
+    const int j = ci / (FBB / 16), w = ci - j * (FBB / 16);
+    boff[i] = ci < CHB ? (uint32_t)(j * nfg * FBB + w * 16) : kOOB;
+  }
+  auto issue = [&](int f, int slot) __attribute__((always_inline)) {
+    const uint32_t ldsb = lds_off(lds) + (uint32_t)(slot * SLOTF);
+#pragma unroll
+    for (int i = 0; i < LA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ar, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + (i * 256 + wid * 64) * 16), 16,
+          aoff[i], f * FBA, 0, 0);
+#pragma unroll
+    for (int i = 0; i < LB; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          br, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + ABYTES + (i * 256 + wid * 64) * 16),
+          16, boff[i], f * FBB, 0, 0);
+  };
+
+  const uint32_t base = lds_off(lds);
+  const uint32_t a_lds = base + (uint32_t)(wm * WFM * FBA + 16 * lane);
+  const uint32_t a8_lds = base + (uint32_t)(wm * WFM * FBA + 1024 + 8 * lane);
+  const uint32_t b_lds = base + (uint32_t)(ABYTES + wn * 4 * FBB + 16 * lane);
+  const uint32_t b8_lds = base + (uint32_t)(ABYTES + wn * 4 * FBB + 1024 + 8 * lane);
+  const int sa = 127 + sha, sb = 127 + shw;  // E8M0 block scales 2^sha, 2^shw
+
+  v4f accf[WFM][4];
+#pragma unroll
+  for (int i = 0; i < WFM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) accf[i][jj] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+
+  int issued = 0;
+  for (; issued < NSTF - 1 && issued < nfg; ++issued) issue(issued, issued);
+  for (int f = 0; f < nfg; ++f) {
+    const int later = issued - f - 1;
+    if (NSTF >= 4 && later == 2) wait_vm<(NSTF >= 4 ? 2 * L : 0)>();
+    else if (NSTF >= 3 && later == 1) wait_vm<(NSTF >= 3 ? L : 0)>();
+    else wait_vm<0>();
+    bar_nofence();
+    if (issued < nfg) {
+      issue(issued, issued % NSTF);
+      ++issued;
+    }
+    const uint32_t soff = (uint32_t)((f % NSTF) * SLOTF);
+    FRaw rb[4], ra[WFM];
+    lds_funits<FB, FBB>(rb, b_lds + soff, b8_lds + soff, std::make_integer_sequence<int, 4>{});
+    lds_funits<FA, FBA>(ra, a_lds + soff, a8_lds + soff, std::make_integer_sequence<int, WFM>{});
+    lds_wait();
+    v8i bf[4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) bf[jj] = f_operand<FB>(rb[jj]);
+#pragma unroll
+    for (int i = 0; i < WFM; ++i) {
+      const v8i af = f_operand<FA>(ra[i]);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        accf[i][jj] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf[jj], accf[i][jj], FA,
+                                                                      FB, 0, sa, 0, sb);
+    }
+  }
+  // Everyone is done reading the ring before it is reused.
+  bar_nofence();
+  // exact: integer multiples of 2^(sha+shw), below 2^24 of it
+#pragma unroll
+  for (int i = 0; i < WFM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[i][jj][r] = (int)accf[i][jj][r];
+#endif
+}
+
 // (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).  QN > 0:
 // the epilogue also quantizes every output for the next layer into qn_img
 // (and stores Y only when a.Y is set), with one static scale per
 // next-layer group (QN = 1) or per block of a next layer with sub-group
 // scales (QN = 2, asked to keep three waves per SIMD).
-template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0>
+template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0, bool F = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     QN == 2 ? 3 : QN == 1 ? 1 : WFM == 2 ? 3 : 2)))
 void k_gemm(GemmArgs a) {
@@ -2445,6 +2617,38 @@ void k_gemm(GemmArgs a) {
   auto run_group = [&](auto ca_tag, const uint8_t* abase, int64_t mstride, int ca_rt, int ng,
                        int qbase, v4i (&acc)[WFM][4]) __attribute__((always_inline)) {
     constexpr int CA = decltype(ca_tag)::value;
+    if constexpr (F && CA != 0 && CBL != 0 && CBH != 0) {
+      // narrow x narrow: the MFMA-native copies, when the handle has them
+      const int g = qbase ? 1 : 0;
+      const int k = tile_lo ? 0 : 1;
+      if (a.fa && a.fp.fa[g] && a.fp.fw_off[g][k] >= 0) {
+        constexpr int FA = f_fmt(CA);
+        constexpr int FBL = f_fmt(CBL), FBH = f_fmt(CBH);
+        const int nfg = a.fp.nfg[g];
+        const uint8_t* fat = a.fa + a.fp.fa_off[g] + (m0 / kBlk) * a.fp.fa_mblk[g];
+        const int first = k ? a.wp.nlo : 0;
+        const int wblocks = (k ? a.wp.nblk - a.wp.nlo : a.wp.nlo) - (jb0 - first);
+        const uint8_t* fwt = a.fw + a.fp.fw_off[g][k] +
+                             (int64_t)(jb0 - first) * nfg * f_block_bytes(k ? FBH : FBL);
+        const int sha = ap.sh[g];
+        if constexpr (FA != 0 && FBL != 0) {
+          if (k == 0) {
+            gemm_group_f<FA, FBL, WFM, NST * SLOT>(lds, fat, a.fp.fa_mblk[g], fwt, wblocks, nfg, sha,
+                                                   CBL == 8 ? 0 : CBL == 4 ? 4 : 6, acc, tid, lane,
+                                                   wid, wm, wn);
+            return;
+          }
+        }
+        if constexpr (FA != 0 && FBH != 0 && CBH != CBL) {
+          if (k == 1) {
+            gemm_group_f<FA, FBH, WFM, NST * SLOT>(lds, fat, a.fp.fa_mblk[g], fwt, wblocks, nfg, sha,
+                                                   CBH == 8 ? 0 : CBH == 4 ? 4 : 6, acc, tid, lane,
+                                                   wid, wm, wn);
+            return;
+          }
+        }
+      }
+    }
     if constexpr (CA != 0 && CBL != 0 && CBH != 0) {
       if (CBL == CBH || tile_lo)
         gemm_group_wide<CA, CBL, WFM, NST, SLOT>(lds, abase, mstride, ng, wtile, wbytes, a.wp.ngt,
@@ -4407,6 +4611,9 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.qn_bs = nullptr;
   a.qn_brs = nullptr;
   a.qn_nsub0 = 0;
+  a.fa = nullptr;
+  a.fw = nullptr;
+  a.fp = FPlan{};
   return a;
 }
 
@@ -4416,6 +4623,17 @@ template <int S, int CA0, int CA1, int CBL, int CBH>
 static void launch_gemm_t(const GemmArgs& a, int64_t M, int shape, hipStream_t stream) {
   const int ntn = a.wp.Np / kGemmBN;
   const dim3 blk(256);
+  constexpr bool FOK = CA0 != 0 && CBL != 0 && CBH != 0;
+  if (FOK && a.fa && shape != 2) {
+    // tiles with MFMA-native copies of the narrow operands
+    if (shape == 3)
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 4, 2, 0, FOK>),
+                         dim3((unsigned)(((M + 127) / 128) * ntn)), blk, 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 0, FOK>),
+                         dim3((unsigned)(((M + 63) / 64) * ntn)), blk, 0, stream, a);
+    return;
+  }
   switch (shape) {
     case 3:
       hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 4, 2>), dim3((unsigned)(((M + 127) / 128) * ntn)), blk, 0, stream, a);
@@ -4441,8 +4659,14 @@ static int gemm_shape(int64_t M, int ntn) {
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
-                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
+                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream,
+                          const FPlan* fp, const uint8_t* fa, const uint8_t* fw) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  if (fp && fa && fw) {
+    a.fp = *fp;
+    a.fa = fa;
+    a.fw = fw;
+  }
   const int ca0 = ap.c[0], ca1 = ap.S == 2 ? ap.c[1] : 0;
   const int cl = wp.c_lo, ch = wp.c_hi;
   const int shape = gemm_shape(M, wp.Np / kGemmBN);
@@ -4715,6 +4939,112 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
   } else {
     hipLaunchKernelGGL((k_gemm_g<1, 0, 0, 0, 0>), grid, blk, 0, stream, a);
   }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ k_to_fp --
+// Integer units -> MFMA-native copy.  One thread per (block, fgranule,
+// lane): lane l = q*16 + r takes row r, channels [32q, 32q + 32) of the
+// fgranule, which are elements of two units of granule 2f + q/2 (16-channel
+// groups 2(q%2) and 2(q%2) + 1); it decodes the 32 stored codes exactly as
+// the GEMM widens them (two's complement fields, or sign bits +-1) and
+// encodes each in fp4 (e2m1) or fp6 (e3m2).  Channels past the group's last
+// granule (half of a final fgranule) encode 0.
+__device__ __forceinline__ int unit_code(const uint32_t (&w)[2], int e, int c) {
+  if (c == 4) {
+    const int v = (int)((w[e >> 3] >> (8 * (e & 3) + 4 * ((e >> 2) & 1))) & 0xFu);
+    return v >= 8 ? v - 16 : v;
+  }
+  if (c == 2) {
+    const int j = e >> 2;
+    const int v = (int)((w[0] >> (8 * (e & 3) + 4 * (j & 1) + (j < 2 ? 2 : 0))) & 0x3u);
+    return v >= 2 ? v - 4 : v;
+  }
+  return ((w[0] >> (4 * (e & 3) + (e >> 2))) & 1u) ? -1 : 1;  // c == 1: sign bits
+}
+
+// e2m1: 0, 1 = 1.0 (exponent 1), 2 = 2.0 (exponent 2); bit 3 is the sign.
+__device__ __forceinline__ uint32_t enc_fp4(int v) {
+  const int m = v < 0 ? -v : v;
+  return (m == 0 ? 0u : m == 1 ? 0x2u : 0x4u) | (v < 0 ? 0x8u : 0u);
+}
+// e3m2 (exponent bias 3): |v| = 2^(E-3) * (1 + M/4) for |v| in 1..8; bit 5 is
+// the sign.
+__device__ __forceinline__ uint32_t enc_fp6(int v) {
+  const int m = v < 0 ? -v : v;
+  uint32_t code = 0;
+  if (m > 0) {
+    const int e = 31 - __builtin_clz((unsigned)m);     // 2^e <= m < 2^(e+1)
+    const int mant = ((m << 2) >> e) & 3;              // exact for m <= 8
+    code = (uint32_t)((e + 3) << 2 | mant);
+  }
+  return code | (v < 0 ? 0x20u : 0u);
+}
+
+// Four (block, fgranule) pairs per workgroup, one per wave; containers and
+// formats fixed at compile time, so each lane's 32 elements are a
+// straight-line sequence of shifts and masks.
+template <int C, int FMT>
+__global__ __launch_bounds__(256) void k_to_fp(const uint8_t* __restrict__ src, int64_t src_bstride,
+                                               int ng, int npairs, uint8_t* __restrict__ dst,
+                                               int64_t dst_bstride) {
+  const int nfg = (ng + 1) / 2;
+  const int p = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (p >= npairs) return;
+  const int lane = threadIdx.x & 63;
+  const int b = p / nfg, f = p - b * nfg;
+  const int q = lane >> 4, r = lane & 15;
+  const int gi = 2 * f + (q >> 1);
+  uint32_t d[6] = {0u, 0u, 0u, 0u, 0u, 0u};
+  if (gi < ng) {
+    const uint8_t* gbase = src + b * src_bstride + (int64_t)gi * 128 * C;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint8_t* u = gbase + ((2 * (q & 1) + h) * 16 + r) * 2 * C;
+      uint32_t w[2] = {0u, 0u};
+      if constexpr (C == 4) {
+        const uint2 v = *reinterpret_cast<const uint2*>(u);
+        w[0] = v.x;
+        w[1] = v.y;
+      } else if constexpr (C == 2) {
+        w[0] = *reinterpret_cast<const uint32_t*>(u);
+      } else {
+        w[0] = *reinterpret_cast<const uint16_t*>(u);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int v = unit_code(w, e, C);
+        const int el = 16 * h + e;  // element of the lane's 32
+        if constexpr (FMT == kFmtFp4) {
+          d[el >> 3] |= enc_fp4(v) << (4 * (el & 7));
+        } else {
+          const uint32_t code = enc_fp6(v);
+          const int pos = 6 * el, wd = pos >> 5, sh = pos & 31;
+          d[wd] |= code << sh;
+          if (sh > 26) d[wd + 1] |= code >> (32 - sh);
+        }
+      }
+    }
+  }
+  uint8_t* o = dst + b * dst_bstride + (int64_t)f * f_block_bytes(FMT);
+  *reinterpret_cast<uint4*>(o + 16 * lane) = make_uint4(d[0], d[1], d[2], d[3]);
+  if constexpr (FMT == kFmtFp6) *reinterpret_cast<uint2*>(o + 1024 + 8 * lane) = make_uint2(d[4], d[5]);
+}
+
+hipError_t launch_to_fp(const uint8_t* src, int64_t src_bstride, int c, int ng, int64_t nblk,
+                        uint8_t* dst, int64_t dst_bstride, int fmt, hipStream_t stream) {
+  const int64_t pairs = nblk * ((ng + 1) / 2);
+  if (pairs == 0) return hipSuccess;
+  if (pairs >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((pairs + 3) / 4)), blk(256);
+  if (c == 4 && fmt == kFmtFp6)
+    hipLaunchKernelGGL((k_to_fp<4, kFmtFp6>), grid, blk, 0, stream, src, src_bstride, ng, (int)pairs, dst, dst_bstride);
+  else if (c == 2 && fmt == kFmtFp4)
+    hipLaunchKernelGGL((k_to_fp<2, kFmtFp4>), grid, blk, 0, stream, src, src_bstride, ng, (int)pairs, dst, dst_bstride);
+  else if (c == 1 && fmt == kFmtFp4)
+    hipLaunchKernelGGL((k_to_fp<1, kFmtFp4>), grid, blk, 0, stream, src, src_bstride, ng, (int)pairs, dst, dst_bstride);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
