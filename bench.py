@@ -82,7 +82,8 @@ def uses_gemv(case) -> bool:
     return case["M"] <= 8 and not case.get("act_group_bits", 0)
 
 
-def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6f4=False):
+def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6f4=False,
+            implicit=False):
     import torch
     import paper_2311_14114_amd as sq
 
@@ -98,8 +99,20 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     e0.record(stream)
     gbits = case.get("act_group_bits", 0)
     nib = sign_nibbles(case)
-    ws = [sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4)]
+    if implicit:
+        # the filter as [N, C, 3, 3] and one width per input channel
+        Cin = case["X"].shape[1]
+        Wf = W.view(N, Cin, 3, 3)
+        ch_bits = case["a_bits"][::9]
+
+        def pack():
+            return sq.soniq_pack_weights_conv3x3(Wf, case["w_bits"], ch_bits, case["a_signed"],
+                                                 sign_nibbles=nib)
+    else:
+        def pack():
+            return sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
+                                         act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4)
+    ws = [pack()]
     e1.record(stream)
     torch.cuda.synchronize()
     pack_ms = e0.elapsed_time(e1)
@@ -108,9 +121,12 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     if rotate:
         nw = max(1, min(MAX_W_COPIES, math.ceil(ROTATE_W_BYTES / int(info.packed_w_bytes))))
     for _ in range(nw - 1):
-        ws.append(sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                        act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4))
-    acts = [sq.soniq_act_create(w, M) for w in ws]
+        ws.append(pack())
+    if implicit:
+        Bx, _, Hx, Wx = case["X"].shape
+        acts = [sq.soniq_act_create_conv3x3(w, Bx, Hx, Wx) for w in ws]
+    else:
+        acts = [sq.soniq_act_create(w, M) for w in ws]
     # the quantizer's input: the lowered matrix A, or (conv_input) the
     # convolution's NCHW tensor X, whose 3x3 lowering A is
     src0 = torch.from_numpy(case["X"]).to(dev) if conv_input else A0
@@ -134,7 +150,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     def full(i):
         # one layer: the conv entry point then the GEMM, or the one-call
         # quantize + GEMM (a single launch for a batch of one row)
-        if conv_input:
+        if conv_input or implicit:
             act, w = step(i)
             sq.soniq_mp_gemm(act, w, out=Y)
         else:
@@ -455,6 +471,10 @@ def main():
     ap.add_argument("--conv-input", action="store_true",
                     help="conv workloads: quantize from the NCHW input tensor "
                          "(soniq_quantize_act_conv3x3) instead of the lowered matrix")
+    ap.add_argument("--implicit-conv", action="store_true",
+                    help="conv workloads: the implicit-GEMM convolution (weights packed with "
+                         "soniq_pack_weights_conv3x3; the input quantized once into a code image "
+                         "whose taps the GEMM gathers)")
     ap.add_argument("--f8f6f4", action="store_true",
                     help="pack the weights with SONIQ_WPACK_F8F6F4: narrow x narrow tiles run on the "
                          "fp4/fp6 MFMA")
@@ -476,12 +496,15 @@ def main():
 
     import workloads
     case = workloads.make(args.workload)
+    if args.implicit_conv:
+        args.conv_input = True
     if args.conv_input and "X" not in case:
         print(f"--conv-input needs a convolution workload; {args.workload} has no input tensor",
               file=sys.stderr)
         sys.exit(2)
     r = run_gpu(case, args.steps, args.warmup, rotate=not args.no_rotate,
-                graph=args.launch == "graph", conv_input=args.conv_input, f8f6f4=args.f8f6f4)
+                graph=args.launch == "graph", conv_input=args.conv_input, f8f6f4=args.f8f6f4,
+                implicit=args.implicit_conv)
     alg = algorithmic(case, r["info"])
     if args.conv_input:
         alg["a_fp32"] = int(case["X"].nbytes)  # the quantizer reads X, not its lowering
@@ -501,6 +524,7 @@ def main():
                    "f8f6f4_copies": bool(args.f8f6f4),
                    "activation_copies": r["na"], "weight_copies": r["nw"],
                    "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
+                   "implicit_conv": bool(args.implicit_conv),
                    "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input
                              else "soniq_quantize_mp_gemm")},
         "roofline": roofline(case, alg, r, args.steps),

@@ -169,6 +169,53 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
                                         void* stream, soniq_weights* out);
 
 /*
+ * soniq_pack_weights_conv3x3 -- weights of a stride-1, pad-1 3x3
+ * convolution packed for the implicit GEMM (no lowered activation matrix
+ * exists anywhere).  Passages: as soniq_pack_weights; Sec. 4 (software
+ * optimizations for convolutions: a layout that lets the kernel read each
+ * input once, and input handling fused with quantization); per-channel
+ * precision (Sec. 3).
+ *
+ *   W_dev   device, float32 [N][C][3][3] contiguous (the filter; as a
+ *           matrix it is [N][9C] in the column order of a 3x3 unfold,
+ *           k = c*9 + kh*3 + kw).
+ *   N, C    output and input channels (9*C padded <= SONIQ_MAX_K).
+ *   w_bits  host uint8 [N] as for soniq_pack_weights.
+ *   c_bits  host uint8 [C]: width of each INPUT channel (shared by its nine
+ *           taps), 1..8, at most two values.
+ *   a_signed, wq_mode  as for soniq_pack_weights_ex (SONIQ_WPACK_SIGN_NIBBLES
+ *           allowed; SONIQ_WPACK_F8F6F4 not).
+ * Inside each precision group the K axis is tap-major (all channels of tap
+ * 0, then tap 1, ...), each tap's run padded to 16 channels, so that a
+ * GEMM fragment of one tap is one run of a pixel's codes.  Results are
+ * those of soniq_pack_weights on the lowered weights: the same codes and
+ * scales (soniq_weights_unpack_debug returns them in the k = c*9 + t order)
+ * and, through soniq_mp_gemm, the same accumulators and outputs.
+ * This build has instances for 4- and 8-bit activation containers (two
+ * widths) and weight containers 4/4, 1/4, 2/4, 2/8 and 4/8; UNSUPPORTED
+ * otherwise.  Activation handles: soniq_act_create_conv3x3.
+ * Errors: those of soniq_pack_weights, UNSUPPORTED.
+ */
+soniq_status soniq_pack_weights_conv3x3(const float* W_dev, int64_t N, int64_t C,
+                                        const uint8_t* w_bits, const uint8_t* c_bits,
+                                        int a_signed, int wq_mode, void* stream,
+                                        soniq_weights* out);
+
+/*
+ * soniq_act_create_conv3x3 -- the activation handle of weights from
+ * soniq_pack_weights_conv3x3, for inputs of up to B images of H x W.  It
+ * owns the input's code image: per precision group, (H+2) x (W+2) pixels
+ * per image (a one-pixel halo holding the code of 0.0), each pixel its
+ * channels of that group as packed codes, about 9x fewer bytes than a
+ * lowered matrix.  Quantize with soniq_quantize_act_conv3x3 (the same
+ * H and W, at most B images), multiply with soniq_mp_gemm; the other
+ * activation entry points return UNSUPPORTED for it.
+ * Errors: INVALID_ARGUMENT (other weights, sizes), OUT_OF_MEMORY, HIP.
+ */
+soniq_status soniq_act_create_conv3x3(soniq_weights w, int64_t B, int64_t H, int64_t W,
+                                      soniq_act* out);
+
+/*
  * soniq_act_create -- allocate a packed activation buffer for up to max_M
  * rows, laid out for the input-channel plan of `w` (activation groups,
  * permutation and padding are fixed at weight-packing time, Alg. 1).
@@ -213,6 +260,10 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
  * The nine columns of every channel must share one activation width
  * (UNSUPPORTED otherwise), and 16 rows of the handle's padded channel plan
  * must fit 64 KB of LDS (K up to about 4000; UNSUPPORTED otherwise).
+ * For a handle of soniq_act_create_conv3x3 (weights packed for the implicit
+ * GEMM) the call instead writes the handle's code image of X (H and W as
+ * created, B at most as created); codes and scales are the same as above,
+ * and soniq_act_unpack_debug returns them as the lowered matrix's.
  * Enqueued on `stream`, like soniq_quantize_act; X_dev is only read.
  * Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
  */

@@ -31,7 +31,7 @@ SONIQ_MAX_K = 65536
 # Every symbol include/soniq.h declares.
 EXPORTED = [
     "soniq_pack_weights", "soniq_pack_weights_ex", "soniq_pack_weights_grouped",
-    "soniq_act_create",
+    "soniq_pack_weights_conv3x3", "soniq_act_create", "soniq_act_create_conv3x3",
     "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_quantize_mp_gemm",
     "soniq_quantize_mp_gemm_scratch",
     "soniq_mp_gemm_quantize_next",
@@ -81,6 +81,11 @@ def lib() -> ctypes.CDLL:
         L.soniq_pack_weights_grouped.restype = st
         L.soniq_pack_weights_grouped.argtypes = [vp, i64, i64, i64, vp, vp, i32, i32, i32, vp,
                                                  ctypes.POINTER(vp)]
+        L.soniq_pack_weights_conv3x3.restype = st
+        L.soniq_pack_weights_conv3x3.argtypes = [vp, i64, i64, vp, vp, i32, i32, vp,
+                                                 ctypes.POINTER(vp)]
+        L.soniq_act_create_conv3x3.restype = st
+        L.soniq_act_create_conv3x3.argtypes = [vp, i64, i64, i64, ctypes.POINTER(vp)]
         L.soniq_act_create.restype = st
         L.soniq_act_create.argtypes = [vp, i64, ctypes.POINTER(vp)]
         L.soniq_quantize_act.restype = st
@@ -207,6 +212,36 @@ def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_W
                                             int(act_group_bits), _stream(stream),
                                             ctypes.byref(h)))
     return Weights(h, N, K)
+
+
+def soniq_pack_weights_conv3x3(Wf, w_bits, c_bits, a_signed: bool,
+                               wq_mode: int = SONIQ_WQ_SYMMETRIC, stream=None,
+                               sign_nibbles: bool = False) -> Weights:
+    """Pack a 3x3 filter (device float32 [N, C, 3, 3], contiguous) for the
+    implicit-GEMM convolution; c_bits holds one width per input channel.
+    The handle behaves as weights of K = 9*C columns (k = c*9 + kh*3 + kw)."""
+    import torch
+    if Wf.dtype != torch.float32 or Wf.dim() != 4 or tuple(Wf.shape[2:]) != (3, 3) \
+            or not Wf.is_contiguous():
+        raise TypeError("the filter must be a contiguous float32 [N, C, 3, 3] device tensor")
+    N, C = Wf.shape[0], Wf.shape[1]
+    wb, cb = _u8(w_bits), _u8(c_bits)
+    if wb.shape != (N,) or cb.shape != (C,):
+        raise ValueError("w_bits must have N entries and c_bits C entries")
+    h = ctypes.c_void_p()
+    _check(lib().soniq_pack_weights_conv3x3(_dev(Wf, "float32"), N, C,
+                                            wb.ctypes.data_as(ctypes.c_void_p),
+                                            cb.ctypes.data_as(ctypes.c_void_p),
+                                            1 if a_signed else 0,
+                                            int(wq_mode) | (SONIQ_WPACK_SIGN_NIBBLES if sign_nibbles else 0),
+                                            _stream(stream), ctypes.byref(h)))
+    return Weights(h, N, 9 * C)
+
+
+def soniq_act_create_conv3x3(weights: Weights, B: int, H: int, W: int) -> Activations:
+    h = ctypes.c_void_p()
+    _check(lib().soniq_act_create_conv3x3(weights.handle, int(B), int(H), int(W), ctypes.byref(h)))
+    return Activations(h, weights, int(B) * int(H) * int(W))
 
 
 def soniq_act_create(weights: Weights, max_M: int) -> Activations:

@@ -165,6 +165,38 @@ bool plan_k(const uint8_t* a_bits, int64_t K, KPlan& kp) {
   return true;
 }
 
+// Input-channel plan of a 3x3 convolution computed as an implicit GEMM:
+// column k = c*9 + t of the lowered matrix (t = kh*3 + kw) goes to tap-major
+// order inside its precision group: position t*cpad_g + rank of c in the
+// group, each tap's run padded to a multiple of 16 channels (one MFMA
+// fragment unit) and the group to a multiple of 64 (a granule).  The GEMM
+// then finds every 16-channel unit of a tap as one run of a pixel's codes.
+bool plan_k_conv(const uint8_t* c_bits, int64_t C, KPlan& kp, int64_t cpad[2]) {
+  if (!distinct_widths(c_bits, C, kp.bits, &kp.S)) return false;
+  int64_t cnt[2] = {0, 0};
+  std::vector<int64_t> rank(C);
+  for (int64_t c = 0; c < C; ++c) {
+    const int g = c_bits[c] == kp.bits[0] ? 0 : 1;
+    rank[c] = cnt[g]++;
+  }
+  for (int g = 0; g < 2; ++g) {
+    cpad[g] = round_up(cnt[g], 16);
+    kp.len[g] = 9 * cnt[g];
+    kp.pad[g] = round_up(9 * cpad[g], kGran);
+  }
+  kp.Kp = kp.pad[0] + kp.pad[1];
+  kp.pos.resize(9 * C);
+  kp.seg.resize(9 * C);
+  for (int64_t c = 0; c < C; ++c) {
+    const int g = c_bits[c] == kp.bits[0] ? 0 : 1;
+    for (int t = 0; t < 9; ++t) {
+      kp.seg[9 * c + t] = (uint8_t)g;
+      kp.pos[9 * c + t] = (int32_t)((g ? kp.pad[0] : 0) + t * cpad[g] + rank[c]);
+    }
+  }
+  return true;
+}
+
 template <class T>
 hipError_t dev_alloc(T** p, size_t count) {
   *p = nullptr;
@@ -211,6 +243,11 @@ struct soniq_weights_s {
   bool f8f6f4 = false;
   FPlan fplan{};
   uint8_t* fw = nullptr;
+  // 3x3 convolution packed for the implicit GEMM (tap-major channel plan)
+  bool conv = false;
+  int64_t C = 0;
+  int64_t cpad[2] = {0, 0};
+  int32_t* chan = nullptr;  // [2][max group size]: original channel of each rank
 
   int scales() const { return act_group_bits ? nsub[0] + nsub[1] : kp.S; }
   WDev dev() const { return WDev{packed, blk_off, blk_c, colinfo, shw, tile_cols, colrank}; }
@@ -236,6 +273,11 @@ struct soniq_act_s {
   // fplan = the weights' plan with this buffer's offsets
   uint8_t* fa = nullptr;
   FPlan fplan{};
+  // weights of an implicit 3x3 convolution: the haloed code image of its
+  // input, per precision group [B][H+2][W+2][cpad_g channels], for up to
+  // cg.B images of H x W
+  ConvGeo cg{};
+  uint8_t* img = nullptr;
   // one column table per producer weights handle (keyed by its serial),
   // kept until this handle is destroyed: a captured graph may still hold a
   // table's address after another producer has fed this handle
@@ -263,6 +305,7 @@ void free_weights(soniq_weights w) {
   (void)hipFree(w->grp);
   (void)hipFree(w->posg);
   (void)hipFree(w->fw);
+  (void)hipFree(w->chan);
   w->magic = kDead;
   delete w;
 }
@@ -376,6 +419,11 @@ soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* a
                       hipStream_t st) {
   const soniq_weights w = act.w;
   const int64_t M = act.M;
+  if (w->conv) {
+    HIP_TRY(launch_mp_gemm_conv(act.img, act.cg, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev,
+                                ldy, acc_dev, st));
+    return SONIQ_OK;
+  }
   const bool gemv = !w->act_group_bits && gemv_fits(M, act.ap, w->wp);
   if (!gemv && ((M + 63) / 64) * (w->wp.Np / kGemmBN) > 0x7FFFFFFFLL)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
@@ -440,11 +488,17 @@ soniq_status soniq_plan_input_channels(const uint8_t* a_bits, int64_t K, int64_t
   return SONIQ_OK;
 }
 
-soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
-                                        const uint8_t* w_bits, const uint8_t* a_bits,
-                                        int a_signed, int wq_mode, int act_group_bits,
-                                        void* stream, soniq_weights* out) {
-  if (!W_dev || !w_bits || !a_bits || !out)
+}  // extern "C"
+
+namespace {
+// Packing behind the entry points; c_bits (host, C widths) selects the
+// tap-major plan of a 3x3 convolution (K = 9*C), else a_bits gives the
+// plain plan.
+soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                       const uint8_t* w_bits, const uint8_t* a_bits, int a_signed, int wq_mode,
+                       int act_group_bits, void* stream, soniq_weights* out,
+                       const uint8_t* c_bits = nullptr, int64_t C = 0) {
+  if (!W_dev || !w_bits || (!a_bits && !c_bits) || !out)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: null pointer");
   if (N < 1 || K < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: N, K must be >= 1");
   if (ldw < K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: ldw < K");
@@ -463,9 +517,14 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
                 "soniq_pack_weights: w_bits must be 1..8 with at most two distinct values");
   KPlan kp;
-  if (!plan_k(a_bits, K, kp))
+  int64_t cpad[2] = {0, 0};
+  if (c_bits ? !plan_k_conv(c_bits, C, kp, cpad) : !plan_k(a_bits, K, kp))
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
-                "soniq_pack_weights: a_bits must be 1..8 with at most two distinct values");
+                "soniq_pack_weights: activation widths must be 1..8 with at most two distinct values");
+  if (c_bits && (f8f6f4 || act_group_bits))
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_pack_weights_conv3x3: SONIQ_WPACK_F8F6F4 and sub-group scales are not "
+                "available for the implicit convolution");
   if (kp.Kp > SONIQ_MAX_K)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_pack_weights: padded K %lld exceeds %d",
                 (long long)kp.Kp, SONIQ_MAX_K);
@@ -679,10 +738,59 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
     return rc;
   }
   w->grp_h = std::move(grp_h);
+  if (c_bits) {
+    if (!conv_gemm_supported(make_act_plan(*w, kMAlign), w->wp)) {
+      free_weights(w);
+      return fail(SONIQ_ERR_UNSUPPORTED,
+                  "soniq_pack_weights_conv3x3: the implicit convolution takes 4- and 8-bit "
+                  "activation containers and weight containers 4/4, 1/4, 2/4, 2/8 or 4/8");
+    }
+    // rank -> original channel, per group (the image quantizer's gather)
+    w->conv = true;
+    w->C = C;
+    w->cpad[0] = cpad[0];
+    w->cpad[1] = cpad[1];
+    const int64_t mx = std::max(cpad[0], cpad[1]);
+    std::vector<int32_t> chan(2 * (size_t)mx, -1);
+    int64_t cnt[2] = {0, 0};
+    for (int64_t c = 0; c < C; ++c) {
+      const int g = w->kp.seg[9 * c];
+      chan[g * mx + cnt[g]++] = (int32_t)c;
+    }
+    hipError_t e2 = dev_alloc(&w->chan, chan.size());
+    if (e2 == hipSuccess)
+      e2 = hipMemcpy(w->chan, chan.data(), chan.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e2 != hipSuccess) {
+      free_weights(w);
+      return fail_hip(e2, "soniq_pack_weights_conv3x3");
+    }
+  }
   w->serial = g_serial.fetch_add(1);
   w->magic = kMagicW;
   *out = w;
   return SONIQ_OK;
+}
+}  // namespace
+
+extern "C" {
+
+soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
+                                        const uint8_t* w_bits, const uint8_t* a_bits,
+                                        int a_signed, int wq_mode, int act_group_bits,
+                                        void* stream, soniq_weights* out) {
+  return pack_impl(W_dev, N, K, ldw, w_bits, a_bits, a_signed, wq_mode, act_group_bits, stream, out);
+}
+
+soniq_status soniq_pack_weights_conv3x3(const float* W_dev, int64_t N, int64_t C,
+                                        const uint8_t* w_bits, const uint8_t* c_bits,
+                                        int a_signed, int wq_mode, void* stream,
+                                        soniq_weights* out) {
+  if (!c_bits) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights_conv3x3: null pointer");
+  if (C < 1 || C > SONIQ_MAX_K / 9)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights_conv3x3: C=%lld out of range",
+                (long long)C);
+  return pack_impl(W_dev, N, 9 * C, 9 * C, w_bits, nullptr, a_signed, wq_mode, 0, stream, out,
+                   c_bits, C);
 }
 
 soniq_status soniq_pack_weights_ex(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
@@ -724,8 +832,58 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out) {
   return SONIQ_OK;
 }
 
+soniq_status soniq_act_create_conv3x3(soniq_weights w, int64_t B, int64_t H, int64_t W,
+                                      soniq_act* out) {
+  if (!live_w(w) || !out)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create_conv3x3: bad handle or null");
+  if (!w->conv)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_act_create_conv3x3: weights not packed with soniq_pack_weights_conv3x3");
+  if (B < 1 || H < 1 || W < 1 || B * H * W > ((int64_t)1 << 31) - kMAlign ||
+      B * (H + 2) * (W + 2) >= ((int64_t)1 << 31) / 256 || B * w->C * H * W >= ((int64_t)1 << 31))
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create_conv3x3: B, H, W out of range");
+  soniq_act a = new (std::nothrow) soniq_act_s();
+  if (!a) return fail(SONIQ_ERR_OUT_OF_MEMORY, "soniq_act_create_conv3x3: host allocation");
+  a->w = w;
+  a->max_M = B * H * W;
+  a->M_alloc = round_up(a->max_M, kMAlign);
+  a->ap = make_act_plan(*w, a->M_alloc);
+  ConvGeo& cg = a->cg;
+  cg.B = (int)B;
+  cg.H = (int)H;
+  cg.W = (int)W;
+  int64_t off = 0;
+  for (int g = 0; g < 2; ++g) {
+    cg.cpad[g] = (int)w->cpad[g];
+    cg.rowbytes[g] = g < w->kp.S ? (int)(w->cpad[g] * a->ap.c[g] / 8) : 0;
+    cg.img_off[g] = off;
+    off = round_up(off + B * (H + 2) * (W + 2) * (int64_t)cg.rowbytes[g], 256);
+  }
+  cg.chan_ld = (int)std::max(w->cpad[0], w->cpad[1]);
+  hipError_t e = dev_alloc(&a->img, (size_t)off);
+  if (e == hipSuccess) e = dev_alloc(&a->partial, (size_t)2 * kAbsmaxBlocks);
+  if (e == hipSuccess) e = dev_alloc(&a->s_a, 2);
+  if (e == hipSuccess) e = hipMemset(a->s_a, 0, 2 * sizeof(float));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    soniq_status rc = fail_hip(e, "soniq_act_create_conv3x3");
+    (void)hipFree(a->img);
+    (void)hipFree(a->partial);
+    (void)hipFree(a->s_a);
+    delete a;
+    return rc;
+  }
+  w->refs++;
+  a->magic = kMagicA;
+  *out = a;
+  return SONIQ_OK;
+}
+
 soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
   if (!live_w(w) || !out) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create: bad handle or null");
+  if (w->conv)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_act_create: convolution weights take soniq_act_create_conv3x3");
   if (max_M < 1 || max_M > ((int64_t)1 << 31) - kMAlign)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_act_create: max_M out of range");
   soniq_act a = new (std::nothrow) soniq_act_s();
@@ -774,6 +932,9 @@ soniq_status soniq_quantize_act(soniq_act act, const float* A_dev, int64_t M, in
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: M=%lld outside [1, %lld]",
                 (long long)M, (long long)act->max_M);
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act: lda < K");
+  if (w->conv)
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_quantize_act: implicit-convolution weights quantize with soniq_quantize_act_conv3x3");
   return run_quantize(*act, A_dev, M, lda, reinterpret_cast<hipStream_t>(stream));
 }
 
@@ -793,6 +954,17 @@ soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64
     return fail(SONIQ_ERR_UNSUPPORTED,
                 "soniq_quantize_act_conv3x3: weights packed with sub-group activation scales");
   const int64_t M = B * H * W;
+  if (w->conv) {
+    const ConvGeo& cg = act->cg;
+    if (H != cg.H || W != cg.W || B > cg.B)
+      return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                  "soniq_quantize_act_conv3x3: B=%lld H=%lld W=%lld do not fit the handle (B<=%d, "
+                  "H=%d, W=%d)", (long long)B, (long long)H, (long long)W, cg.B, cg.H, cg.W);
+    HIP_TRY(launch_conv_img(X_dev, B, C, H, W, act->ap, cg, w->seg, w->chan, act->partial, act->s_a,
+                            act->img, reinterpret_cast<hipStream_t>(stream)));
+    act->M = M;
+    return SONIQ_OK;
+  }
   if (M > act->max_M)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_act_conv3x3: B*H*W=%lld > max_M=%lld",
                 (long long)M, (long long)act->max_M);
@@ -836,6 +1008,8 @@ soniq_status soniq_quantize_mp_gemm(soniq_act act, soniq_weights w, const float*
                 (long long)M, (long long)act->max_M);
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: lda < K");
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm: ldy < N");
+  if (w->conv)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_quantize_mp_gemm: implicit-convolution weights");
   return run_quantize_gemm(*act, A_dev, M, lda, Y_dev, ldy, acc_dev,
                            reinterpret_cast<hipStream_t>(stream));
 }
@@ -848,6 +1022,8 @@ soniq_status soniq_quantize_mp_gemm_scratch(soniq_weights w, const float* A_dev,
   if (M < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: M < 1");
   if (lda < w->K) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: lda < K");
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_quantize_mp_gemm_scratch: ldy < N");
+  if (w->conv)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_quantize_mp_gemm_scratch: implicit-convolution weights");
   // The activation buffers an activation handle for M rows would own, laid
   // out in the device's scratch: grid state, scales, partial maxima, packed
   // rows.
@@ -902,6 +1078,8 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   if (next == act)
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
                 "soniq_mp_gemm_quantize_next: next is the producer's own activation handle");
+  if (w->conv || next->w->conv)
+    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm_quantize_next: implicit-convolution weights");
   const soniq_weights w2 = next->w;
   if (w2->K != w->N)
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
@@ -998,6 +1176,42 @@ soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a) {
   HIP_TRY(hipDeviceSynchronize());
   const ActPlan& ap = act->ap;
   const soniq_weights w = act->w;
+  if (w->conv) {
+    // codes of the lowered matrix, read back from the haloed image: column
+    // k = c*9 + t of row m = (b*H + y)*W + x is channel c of pixel
+    // (y + t/3 - 1, x + t%3 - 1), the halo holding the code of 0
+    const ConvGeo& cg = act->cg;
+    const int64_t Wp = cg.W + 2, Hp = cg.H + 2;
+    size_t bytes = 0;
+    for (int g = 0; g < ap.S; ++g)
+      bytes = std::max(bytes, (size_t)(cg.img_off[g] + cg.B * Hp * Wp * (int64_t)cg.rowbytes[g]));
+    std::vector<uint8_t> img(bytes);
+    float sa[2] = {0.0f, 0.0f};
+    HIP_TRY(hipMemcpy(img.data(), act->img, bytes, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(sa, act->s_a, sizeof sa, hipMemcpyDeviceToHost));
+    if (codes) {
+      std::vector<int64_t> rank(w->C);
+      int64_t cnt[2] = {0, 0};
+      for (int64_t c = 0; c < w->C; ++c) rank[c] = cnt[w->kp.seg[9 * c]]++;
+      for (int64_t m = 0; m < act->M; ++m) {
+        const int64_t b = m / (cg.H * cg.W), y = (m / cg.W) % cg.H, x = m % cg.W;
+        for (int64_t c = 0; c < w->C; ++c) {
+          const int g = w->kp.seg[9 * c];
+          const int cc = ap.c[g];
+          for (int t = 0; t < 9; ++t) {
+            const int64_t hp = (b * Hp + y + 1 + t / 3 - 1) * Wp + x + 1 + t % 3 - 1;
+            const uint8_t* unit =
+                img.data() + cg.img_off[g] + hp * cg.rowbytes[g] + (rank[c] / 16) * 2 * cc;
+            codes[m * w->K + 9 * c + t] =
+                decode_signed(unit_field(unit, (int)(rank[c] % 16), cc), cc) + ap.zp[g];
+          }
+        }
+      }
+    }
+    if (s_a)
+      for (int g = 0; g < w->kp.S; ++g) s_a[g] = sa[g];
+    return SONIQ_OK;
+  }
   std::vector<uint8_t> packed(act->packed_bytes);
   std::vector<float> sa((size_t)std::max(2, w->scales()), 0.0f);
   HIP_TRY(hipMemcpy(packed.data(), act->packed, act->packed_bytes, hipMemcpyDeviceToHost));
@@ -1042,6 +1256,7 @@ void soniq_act_destroy(soniq_act act) {
   for (const auto& t : act->qn_tabs) (void)hipFree(t.second);
   (void)hipFree(act->qn_brs);
   (void)hipFree(act->fa);
+  (void)hipFree(act->img);
   act->magic = kDead;
   soniq_weights w = act->w;
   delete act;

@@ -135,6 +135,20 @@ struct FPlan {
   int64_t fa_mblk[2];    // bytes of one 16-row block of that region
 };
 
+// Geometry of the code image of a 3x3 convolution's input (implicit GEMM):
+// per precision group g, B images of (H+2) x (W+2) pixels (a one-pixel halo
+// holding the code of 0), each pixel cpad[g] channels (the group's channels
+// in rank order, padded to 16) as rowbytes[g] bytes of 16-channel units in
+// the unit encoding above, at byte img_off[g] of the image buffer.
+// chan_ld: row length of the weights' rank -> channel table.
+struct ConvGeo {
+  int B, H, W;
+  int cpad[2];
+  int rowbytes[2];
+  int64_t img_off[2];
+  int chan_ld;
+};
+
 struct WDev {
   const uint8_t* packed;
   const uint64_t* blk_off;  // byte offset of each block
@@ -221,6 +235,21 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream,
                           const FPlan* fp = nullptr, const uint8_t* fa = nullptr,
                           const uint8_t* fw = nullptr);
+
+// Implicit 3x3 convolution: the group maxima of X and its haloed code image
+// (seg[9c] = group of channel c; chan[g*cg.chan_ld + rank] = channel), then
+// the GEMM that gathers each tap's units from the image.
+hipError_t launch_conv_img(const float* X, int64_t B, int64_t C, int64_t H, int64_t W,
+                           const ActPlan& ap, const ConvGeo& cg, const uint8_t* seg_dev,
+                           const int32_t* chan_dev, float* partial, float* s_a, uint8_t* img,
+                           hipStream_t stream);
+// Whether the implicit-convolution GEMM has an instance for these
+// containers (activations 4 + 8 bits; weights 4/4, 1/4, 2/4, 2/8 or 4/8).
+bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp);
+hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,
+                               const ActPlan& ap, const WDev& wd, const WPlan& wp, int64_t M,
+                               int64_t N, uint16_t* Y, int64_t ldy, int32_t* acc,
+                               hipStream_t stream);
 
 // Converts integer units to their MFMA-native copy: `nblk` 16-row blocks,
 // block b's units at src + b*src_bstride (ng granules of container c),

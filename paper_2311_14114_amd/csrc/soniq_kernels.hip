@@ -33,6 +33,7 @@
 #include <type_traits>
 #include <utility>
 
+#include <algorithm>
 #include <cstdlib>
 #include <mutex>
 
@@ -1641,6 +1642,9 @@ struct GemmArgs {
   const uint8_t* fa;
   const uint8_t* fw;
   FPlan fp;
+  // implicit 3x3 convolution: the input's haloed code image and geometry
+  const uint8_t* img;
+  ConvGeo cg;
 };
 
 // 16 bytes per lane, global -> LDS; lane l lands at lds_dst + 16*l.
@@ -2371,6 +2375,118 @@ __device__ __forceinline__ void gemm_group_any(uint8_t* lds, const uint8_t* abas
   bar_nofence();
 }
 
+// ---------------------------------------------------- implicit conv 3x3 --
+// One activation group's K loop of a 64 x 128 tile of an implicit 3x3
+// convolution: the weights as in gemm_group_wide (direct loads into the
+// ring); the activation units gathered from the haloed code image.  The
+// group's tap-major axis puts unit (granule q, 16-channel column kg) of an
+// output pixel at tap t = K'/cpad, channels K' mod cpad .. +16 (K' = 64q +
+// 16kg; past 9*cpad: padding, zero), which is one 2*CA-byte run of the
+// image at the pixel shifted by the tap.  Thread (wave kg, m-block
+// (tid/16)%4, row tid%16) loads its unit of every granule of a stage into
+// registers while the previous stage is multiplied, then writes them into
+// the stage's ring slot in the fragment-major layout the products read.
+template <int CA, int CB, int NST, int SLOT>
+__device__ __forceinline__ void gemm_group_conv(uint8_t* lds, const uint8_t* img, int rowbytes,
+                                                int cpad, int H, int W, int64_t M, int64_t m0,
+                                                int ng, const uint8_t* wtile, int wbytes, int ngt,
+                                                int qbase, v4i (&acc)[2][4], int tid, int lane,
+                                                int wid, int wm, int wn) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int WFM = 2;
+  constexpr int GPS = wide_gps(WFM, CA, CB, SLOT);
+  constexpr int CHB = 64 * GPS * CB;
+  constexpr int LA = wide_loads(16 * WFM * GPS * CA), LB = wide_loads(CHB);
+  constexpr int ABYTES = 4096 * LA;
+  static_assert(NST == 2, "two ring slots");
+  static_assert(4096 * (LA + LB) <= SLOT, "a stage fits its slot");
+  const int nst = (ng + GPS - 1) / GPS;
+
+  const __amdgpu_buffer_rsrc_t br =
+      __builtin_amdgcn_make_buffer_rsrc((void*)wtile, (short)0, wbytes, 0x00020000);
+  uint32_t boff[LB];
+#pragma unroll
+  for (int i = 0; i < LB; ++i) {
+    const int ci = i * 256 + tid;
+    const int j = ci / (GPS * 8 * CB), w = ci - j * (GPS * 8 * CB);
+    boff[i] = ci < CHB ? (uint32_t)(j * ngt * 128 * CB + qbase * 128 * CB + w * 16) : kOOB;
+  }
+  auto issue_b = [&](int st, int slot) __attribute__((always_inline)) {
+    const int rem = ng - st * GPS;
+    const uint32_t ldsb = lds_off(lds) + (uint32_t)(slot * SLOT) + ABYTES;
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+      const int q = ((i * 256 + tid) % (GPS * 8 * CB)) / (8 * CB);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          br, (__attribute__((address_space(3))) void*)(uintptr_t)(ldsb + (i * 256 + wid * 64) * 16),
+          16, rem >= GPS || q < rem ? boff[i] : kOOB, st * GPS * 128 * CB, 0, 0);
+    }
+  };
+
+  // this thread's output pixel (rows past M repeat the last one; their
+  // sums are never stored) and its haloed center
+  const int mb = (tid >> 4) & 3, r = tid & 15, kg = wid;
+  const int64_t P = min(m0 + 16 * mb + r, M - 1);
+  const int HW = H * W;
+  const int b = (int)(P / HW), rem0 = (int)(P - (int64_t)b * HW);
+  const int y = rem0 / W, x = rem0 - y * W;
+  const int Wp = W + 2;
+  const int hp0 = (b * (H + 2) + y + 1) * Wp + x + 1;
+  const int kend = 9 * cpad;
+  raw_t<CA> ua[GPS];
+  auto load_a = [&](int st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < GPS; ++q) {
+      const int gq = st * GPS + q;
+      const int kq = gq * 64 + 16 * kg;
+      raw_t<CA> v{};
+      if (gq < ng && kq < kend) {
+        const int t = kq / cpad, c16 = (kq - t * cpad) >> 4;
+        const int tr = t / 3;
+        const int hp = hp0 + (tr - 1) * Wp + (t - 3 * tr - 1);
+        v = *reinterpret_cast<const raw_t<CA>*>(img + (int64_t)hp * rowbytes + c16 * 2 * CA);
+      }
+      ua[q] = v;
+    }
+  };
+  const int aw = (mb * GPS) * 128 * CA + (kg * 16 + r) * 2 * CA;
+  auto write_a = [&](int slot) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < GPS; ++q)
+      *reinterpret_cast<raw_t<CA>*>(lds + slot * SLOT + aw + q * 128 * CA) = ua[q];
+  };
+
+  const uint32_t b_lds = lds_off(lds) + (uint32_t)(ABYTES + wn * 4 * GPS * 128 * CB + lane * 2 * CB);
+  const uint32_t a_lds = lds_off(lds) + (uint32_t)(wm * WFM * GPS * 128 * CA + lane * 2 * CA);
+
+  issue_b(0, 0);
+  load_a(0);
+  write_a(0);
+  auto ready = [&](int st) __attribute__((always_inline)) {
+    // this thread's unit writes and every wave's weight loads have landed
+    __builtin_amdgcn_s_waitcnt(0);
+    bar_nofence();
+    if (st + 1 < nst) {
+      issue_b(st + 1, (st + 1) & 1);
+      load_a(st + 1);
+    }
+    return (uint32_t)((st & 1) * SLOT);
+  };
+  const int nfull = ng / GPS;
+  for (int st = 0; st < nfull; ++st) {
+    const uint32_t soff = ready(st);
+    wide_stage<CA, CB, WFM, GPS, GPS>(acc, a_lds + soff, b_lds + soff);
+    if (st + 1 < nst) write_a((st + 1) & 1);
+  }
+  if (nfull < nst) {
+    const uint32_t soff = ready(nfull);
+    wide_stage_rem<CA, CB, WFM, GPS, GPS - 1>(acc, a_lds + soff, b_lds + soff, ng - nfull * GPS);
+  }
+  // Everyone is done reading the ring before the next group refills it.
+  bar_nofence();
+#endif
+}
+
 // ------------------------------------------------------ f8f6f4 tiles --
 // One unit of an MFMA-native copy in LDS, as the raw registers of its reads:
 // the lane's first 16 bytes at a + OFF, and for fp6 its last 8 bytes at
@@ -2544,7 +2660,8 @@ __device__ __forceinline__ void gemm_group_f(uint8_t* lds, const uint8_t* fa_til
 // (and stores Y only when a.Y is set), with one static scale per
 // next-layer group (QN = 1) or per block of a next layer with sub-group
 // scales (QN = 2, asked to keep three waves per SIMD).
-template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0, bool F = false>
+template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0, bool F = false,
+          bool CV = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     QN == 2 ? 3 : QN == 1 ? 1 : WFM == 2 ? 3 : 2)))
 void k_gemm(GemmArgs a) {
@@ -2617,6 +2734,20 @@ void k_gemm(GemmArgs a) {
   auto run_group = [&](auto ca_tag, const uint8_t* abase, int64_t mstride, int ca_rt, int ng,
                        int qbase, v4i (&acc)[WFM][4]) __attribute__((always_inline)) {
     constexpr int CA = decltype(ca_tag)::value;
+    if constexpr (CV) {
+      static_assert(WFM == 2 && CA != 0 && CBL != 0 && CBH != 0, "implicit conv instances");
+      const int g = qbase ? 1 : 0;
+      const uint8_t* img = a.img + a.cg.img_off[g];
+      if (CBL == CBH || tile_lo)
+        gemm_group_conv<CA, CBL, NST, SLOT>(lds, img, a.cg.rowbytes[g], a.cg.cpad[g], a.cg.H,
+                                            a.cg.W, a.M, m0, ng, wtile, wbytes, a.wp.ngt, qbase,
+                                            acc, tid, lane, wid, wm, wn);
+      else
+        gemm_group_conv<CA, CBH, NST, SLOT>(lds, img, a.cg.rowbytes[g], a.cg.cpad[g], a.cg.H,
+                                            a.cg.W, a.M, m0, ng, wtile, wbytes, a.wp.ngt, qbase,
+                                            acc, tid, lane, wid, wm, wn);
+      return;
+    }
     if constexpr (F && CA != 0 && CBL != 0 && CBH != 0) {
       // narrow x narrow: the MFMA-native copies, when the handle has them
       const int g = qbase ? 1 : 0;
@@ -4614,6 +4745,8 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.fa = nullptr;
   a.fw = nullptr;
   a.fp = FPlan{};
+  a.img = nullptr;
+  a.cg = ConvGeo{};
   return a;
 }
 
@@ -4939,6 +5072,105 @@ hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, c
   } else {
     hipLaunchKernelGGL((k_gemm_g<1, 0, 0, 0, 0>), grid, blk, 0, stream, a);
   }
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------- k_conv_img --
+// Haloed code image of a convolution input X[B][C][H][W] (implicit GEMM):
+// item j of group g is unit u = j / HP (channels of rank 16u .. 16u+15) of
+// haloed pixel hp = j % HP, so consecutive threads take consecutive pixels
+// and each of the 16 channel loads coalesces.  Halo pixels hold the stored
+// code of 0.0 and ranks past the group the stored 0 of padding; every code
+// is the group quantizer's (store_code) with the group scale reduced from
+// the partial maxima.
+__global__ __launch_bounds__(256) void k_conv_img(const float* __restrict__ X, int C, int H, int W,
+                                                  int HP, const int32_t* __restrict__ chan,
+                                                  const float* __restrict__ partial, int nparts,
+                                                  ActPlan ap, ConvGeo cg, uint8_t* __restrict__ img,
+                                                  float* __restrict__ s_a_out) {
+  __shared__ float red[8];
+  float s0, s1;
+  scales_from_partials(partial, nparts, ap, red, s0, s1, s_a_out);  // syncs
+  const ActQ aq = make_actq(ap, s0, s1);
+  const int u0 = cg.cpad[0] / 16, u1 = ap.S == 2 ? cg.cpad[1] / 16 : 0;
+  const int n0 = HP * u0, total = n0 + HP * u1;
+  const int Wp = W + 2, HPi = (H + 2) * Wp;
+  for (int i = (int)(blockIdx.x * 256 + threadIdx.x); i < total; i += (int)(gridDim.x * 256)) {
+    const int g = i >= n0 ? 1 : 0;
+    const int j = g ? i - n0 : i;
+    const int u = j / HP, hp = j - u * HP;
+    const int b = hp / HPi, rem = hp - b * HPi;
+    const int yh = rem / Wp, xh = rem - yh * Wp;
+    const bool halo = yh == 0 || yh == H + 1 || xh == 0 || xh == W + 1;
+    uint32_t d[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int c = chan[g * cg.chan_ld + 16 * u + e];
+      uint32_t byte = 0u;  // padding rank: stored 0
+      if (c >= 0) {
+        const float xv = halo ? 0.0f : X[(((int64_t)b * C + c) * H + (yh - 1)) * W + (xh - 1)];
+        byte = store_code(xv, g, aq);
+      }
+      d[e >> 2] |= byte << (8 * (e & 3));
+    }
+    const int c = ap.c[g];
+    uint8_t* dst = img + cg.img_off[g] + (int64_t)hp * cg.rowbytes[g] + u * 2 * c;
+    store_unit(dst, pack_unit(d[0], d[1], d[2], d[3], c), c);
+  }
+}
+
+hipError_t launch_conv_img(const float* X, int64_t B, int64_t C, int64_t H, int64_t W,
+                           const ActPlan& ap, const ConvGeo& cg, const uint8_t* seg_dev,
+                           const int32_t* chan_dev, float* partial, float* s_a, uint8_t* img,
+                           hipStream_t stream) {
+  const int64_t BC = B * C;
+  const int64_t rows_per_block = 4 * kAbsR;
+  const int64_t nparts = (BC + rows_per_block - 1) / rows_per_block < kAbsmaxBlocks
+                             ? (BC + rows_per_block - 1) / rows_per_block
+                             : kAbsmaxBlocks;
+  hipLaunchKernelGGL(k_conv_absmax, dim3((unsigned)nparts), dim3(256), 0, stream, X, (int)BC, (int)C,
+                     (int)(H * W), seg_dev, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t HP = B * (H + 2) * (W + 2);
+  const int64_t units = cg.cpad[0] / 16 + (ap.S == 2 ? cg.cpad[1] / 16 : 0);
+  const int64_t total = HP * units;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_conv_img, dim3((unsigned)blocks), dim3(256), 0, stream, X, (int)C, (int)H,
+                     (int)W, (int)HP, chan_dev, partial, (int)nparts, ap, cg, img, s_a);
+  return hipGetLastError();
+}
+
+template <int CBL, int CBH>
+static void launch_gemm_conv_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  hipLaunchKernelGGL((k_gemm<2, 4, 8, CBL, CBH, 2, 2, 0, false, true>),
+                     dim3((unsigned)(((M + 63) / 64) * ntn)), dim3(256), 0, stream, a);
+}
+
+bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp) {
+  if (!(ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8)) return false;
+  const int cl = wp.c_lo, ch = wp.c_hi;
+  return (cl == 4 && ch == 4) || (cl == 1 && ch == 4) || (cl == 2 && ch == 4) ||
+         (cl == 2 && ch == 8) || (cl == 4 && ch == 8);
+}
+
+hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,
+                               const ActPlan& ap, const WDev& wd, const WPlan& wp, int64_t M,
+                               int64_t N, uint16_t* Y, int64_t ldy, int32_t* acc,
+                               hipStream_t stream) {
+  if (!conv_gemm_supported(ap, wp)) return hipErrorInvalidValue;
+  GemmArgs a = make_args(nullptr, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  a.img = img;
+  a.cg = cg;
+  const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
+  a.xcd_tiles = tiles <= 2048;
+  const int cl = wp.c_lo, ch = wp.c_hi;
+  if (cl == 4 && ch == 4) launch_gemm_conv_t<4, 4>(a, M, stream);
+  else if (cl == 1 && ch == 4) launch_gemm_conv_t<1, 4>(a, M, stream);
+  else if (cl == 2 && ch == 4) launch_gemm_conv_t<2, 4>(a, M, stream);
+  else if (cl == 2 && ch == 8) launch_gemm_conv_t<2, 8>(a, M, stream);
+  else launch_gemm_conv_t<4, 8>(a, M, stream);
   return hipGetLastError();
 }
 
