@@ -2813,6 +2813,86 @@ void k_gemm(GemmArgs a) {
   constexpr int YS = kGemmBN + 8;
   uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
   static_assert(BM * YS * 2 <= NST * SLOT, "output staging fits the ring");
+  if constexpr (QN == 0) {
+    // Staged column-major (column rank c, row r at c*YT + r; YT odd in
+    // dwords, so consecutive ranks of one row sit in different banks): a
+    // lane's two pairs of rows go out as two 4-byte writes, and the stores
+    // read two rows of a column at once.  The raw sum is corrected in
+    // place, v = raw + add * 2^sh = (exact sum) * 2^sh, and scaled by
+    // s_a * 2^-sh: f(v) * (s_a 2^-sh) is exactly f(sum) * s_a, since a
+    // power of two changes no rounding (unless s_a 2^-sh is not a normal
+    // number: then the shifted sum is used).
+    constexpr int YT = BM + 2;
+    static_assert(kGemmBN * YT * 2 <= NST * SLOT, "output staging fits the ring");
+    static_assert(YT % 4 == 2, "odd dword stride");
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
+      const ColInfo ci = WFM <= 2 ? cinf[jj] : a.wd.colinfo[pc];
+      if (ci.n < 0) continue;
+      const uint8_t shw = WFM <= 2 ? cshw[jj] : a.wd.shw[pc];
+      const bool sgn = (shw & kShwSign) != 0;
+      const int sh0 = ap.sh[0] + (shw & 0x7F);
+      const int add0 = ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
+      const int sh1 = ap.sh[1] + (shw & 0x7F);
+      const int add1 = ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0);
+      const float sa0s = __builtin_ldexpf(sa0, -sh0);
+      const float sa1s = S == 2 ? __builtin_ldexpf(sa1, -sh1) : 0.0f;
+      const bool scaled = (sa0s == 0.0f || fabsf(sa0s) >= 0x1p-126f) &&
+                          (S == 1 || sa1s == 0.0f || fabsf(sa1s) >= 0x1p-126f);
+      const int add0s = add0 * (1 << sh0), add1s = S == 2 ? add1 * (1 << sh1) : 0;
+      uint32_t* ycol = reinterpret_cast<uint32_t*>(ys + (WFM <= 2 ? crank[jj] : a.wd.colrank[pc]) * YT);
+#pragma unroll
+      for (int i = 0; i < WFM; ++i) {
+        const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
+        float y[4];
+        if (scaled) [[likely]] {
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            float t = __fmul_rn((float)(acc0[i][jj][h] + add0s), sa0s);
+            if (S == 2) t = __fadd_rn(t, __fmul_rn((float)(acc1[i][jj][h] + add1s), sa1s));
+            y[h] = __fmul_rn(t, ci.s_w);
+          }
+        } else {
+#pragma unroll
+          for (int h = 0; h < 4; ++h)
+            y[h] = epilogue((acc0[i][jj][h] >> sh0) + add0,
+                            S == 2 ? (acc1[i][jj][h] >> sh1) + add1 : 0, S, sa0, sa1, ci.s_w);
+        }
+        // v_cvt_pk_bf16_f32: round to nearest even, as bf16_rne.
+        const __hip_bfloat162 p01 = __float22bfloat162_rn(make_float2(y[0], y[1]));
+        const __hip_bfloat162 p23 = __float22bfloat162_rn(make_float2(y[2], y[3]));
+        ycol[row0 / 2] = (uint32_t)__builtin_bit_cast(uint16_t, p01.x) |
+                         ((uint32_t)__builtin_bit_cast(uint16_t, p01.y) << 16);
+        ycol[row0 / 2 + 1] = (uint32_t)__builtin_bit_cast(uint16_t, p23.x) |
+                             ((uint32_t)__builtin_bit_cast(uint16_t, p23.y) << 16);
+        if (a.acc) {
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            const int64_t m = m0 + row0 + h;
+            if (m < a.M) {
+              a.acc[m * a.N + ci.n] = (acc0[i][jj][h] >> sh0) + add0;
+              if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = (acc1[i][jj][h] >> sh1) + add1;
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // thread: column rank tid % 128, rows 2*(tid / 128) + 4k and the next
+    const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
+    if (n >= 0) {
+      const int mrem = (int)min((int64_t)BM, a.M - m0);
+      uint16_t* yout = a.Y + m0 * a.ldy + n;
+      const uint32_t* yc = reinterpret_cast<const uint32_t*>(ys + (tid & (kGemmBN - 1)) * YT);
+      for (int row = 2 * (tid / kGemmBN); row < mrem; row += 512 / kGemmBN) {
+        const uint32_t v = yc[row / 2];
+        yout[(int64_t)row * a.ldy] = (uint16_t)(v & 0xFFFFu);
+        if (row + 1 < mrem) yout[(int64_t)(row + 1) * a.ldy] = (uint16_t)(v >> 16);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
