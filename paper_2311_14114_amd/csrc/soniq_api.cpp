@@ -278,6 +278,12 @@ struct soniq_act_s {
   // cg.B images of H x W
   ConvGeo cg{};
   uint8_t* img = nullptr;
+  // a single row's contiguous image for the batch-1 GEMV (plans with a
+  // 4-bit group 0 and an 8-bit or no group 1), and whether the last
+  // quantization into this handle left it (one row, by a path that writes
+  // it); the GEMV of one row reads it instead of the spread-out units
+  uint8_t* ximg = nullptr;
+  bool ximg_ok = false;
   // one column table per producer weights handle (keyed by its serial),
   // kept until this handle is destroyed: a captured graph may still hold a
   // table's address after another producer has fed this handle
@@ -408,9 +414,11 @@ soniq_status run_quantize(soniq_act_s& act, const float* A_dev, int64_t M, int64
   if (w->act_group_bits)
     HIP_TRY(launch_act_quant_grouped(A_dev, M, w->K, lda, act.ap, w->pos, w->grp, w->posg,
                                      act.partial, act.counter, act.s_a, act.packed, st));
-  else
+  bool ximg = false;
+  if (!w->act_group_bits)
     HIP_TRY(launch_act_quant(A_dev, M, w->K, lda, act.ap, w->pos, w->seg, act.partial, act.counter,
-                             act.s_a, act.packed, st));
+                             act.s_a, act.packed, st, act.ximg, &ximg));
+  act.ximg_ok = ximg;
   act.M = M;
   return SONIQ_OK;
 }
@@ -432,7 +440,7 @@ soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* a
                                    acc_dev, st));
   else if (gemv)
     HIP_TRY(launch_mp_gemv(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                           acc_dev, st));
+                           acc_dev, st, act.ximg_ok ? act.ximg : nullptr));
   else if (act.fa) {
     // refresh the MFMA-native copy of the narrow groups from the units the
     // producer left, then the GEMM with both forms
@@ -455,7 +463,8 @@ soniq_status run_quantize_gemm(soniq_act_s& act, const float* A_dev, int64_t M, 
   const soniq_weights w = act.w;
   if (M == 1 && !w->act_group_bits && gemv_fused_fits(A_dev, w->K, act.ap, w->wp)) {
     HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos, act.packed, act.s_a, act.ap, w->dev(), w->wp,
-                              w->N, Y_dev, acc_dev, st));
+                              w->N, Y_dev, acc_dev, st, act.ximg));
+    act.ximg_ok = act.ximg != nullptr;
     act.M = 1;
     return SONIQ_OK;
   }
@@ -907,9 +916,13 @@ soniq_status soniq_act_create(soniq_weights w, int64_t max_M, soniq_act* out) {
     a->fplan = w->fplan;
     e = dev_alloc(&a->fa, (size_t)act_fplan(a->fplan, a->M_alloc));
   }
+  const ActPlan& ap = a->ap;
+  if (e == hipSuccess && !w->act_group_bits && ap.c[0] == 4 && (ap.S == 1 || ap.c[1] == 8))
+    e = dev_alloc(&a->ximg, (size_t)round_up(32 * (int64_t)ap.ng[0] + 64 * (int64_t)ap.ng[1], 256));
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     soniq_status rc = fail_hip(e, "soniq_act_create");
+    (void)hipFree(a->ximg);
     (void)hipFree(a->fa);
     (void)hipFree(a->packed);
     (void)hipFree(a->partial);
@@ -962,6 +975,7 @@ soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64
                   "H=%d, W=%d)", (long long)B, (long long)H, (long long)W, cg.B, cg.H, cg.W);
     HIP_TRY(launch_conv_img(X_dev, B, C, H, W, act->ap, cg, w->seg, w->chan, act->partial, act->s_a,
                             act->img, reinterpret_cast<hipStream_t>(stream)));
+    act->ximg_ok = false;
     act->M = M;
     return SONIQ_OK;
   }
@@ -979,6 +993,7 @@ soniq_status soniq_quantize_act_conv3x3(soniq_act act, const float* X_dev, int64
                 (long long)w->K);
   HIP_TRY(launch_conv_quant(X_dev, B, C, H, W, act->ap, w->pos, w->seg, act->partial, act->s_a,
                             act->packed, reinterpret_cast<hipStream_t>(stream)));
+  act->ximg_ok = false;
   act->M = M;
   return SONIQ_OK;
 }
@@ -1145,7 +1160,8 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                                acc_dev, next->qn_img, qn_tab, next->ap,
                                w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
-                               next->packed, st));
+                               next->packed, st, next->ximg));
+  next->ximg_ok = M == 1 && next->ximg != nullptr;
   next->M = M;
   return SONIQ_OK;
 }
@@ -1257,6 +1273,7 @@ void soniq_act_destroy(soniq_act act) {
   (void)hipFree(act->qn_brs);
   (void)hipFree(act->fa);
   (void)hipFree(act->img);
+  (void)hipFree(act->ximg);
   act->magic = kDead;
   soniq_weights w = act->w;
   delete act;

@@ -186,17 +186,22 @@ hipError_t launch_conv_quant(const float* X, int64_t B, int64_t C, int64_t H, in
                              const ActPlan& ap, const int32_t* pos_dev, const uint8_t* seg_dev,
                              float* partial, float* s_a, uint8_t* packed, hipStream_t stream);
 // Batch of one row quantized inside the GEMV (soniq_quantize_mp_gemm): when
-// it applies, its LDS, and the launch.
+// it applies, its LDS, and the launch (ximg: the handle's row image).
 size_t gemv_fused_lds(const ActPlan& ap, const WPlan& wp);
 bool gemv_fused_fits(const float* A, int64_t K, const ActPlan& ap, const WPlan& wp);
 hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, uint8_t* act_packed,
                              float* s_a, const ActPlan& ap, const WDev& wd, const WPlan& wp,
-                             int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream);
+                             int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream,
+                             uint8_t* ximg);
+// ximg (null: none): where a batch of one row also leaves its contiguous
+// image for the batch-1 GEMV (a plan with a 4-bit group 0 and an 8-bit
+// group 1 only); *ximg_done tells whether the launched path wrote it.
 hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const ActPlan& ap, const int32_t* pos_dev,
                             const uint8_t* seg_dev, float* partial,
                             unsigned int* counter, float* s_a, uint8_t* packed,
-                            hipStream_t stream);
+                            hipStream_t stream, uint8_t* ximg = nullptr,
+                            bool* ximg_done = nullptr);
 
 // Sub-group scales: block scales in s_a[block], blocks of group 0 first;
 // grp_dev[k] = block of original channel k.  At most kGAbsParts partial
@@ -228,7 +233,8 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
                                 const ActPlan& ap2, const float* s_next, float* s_a2,
-                                float* brs2, uint8_t* packed2, hipStream_t stream);
+                                float* brs2, uint8_t* packed2, hipStream_t stream,
+                                uint8_t* ximg2 = nullptr);
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
@@ -257,9 +263,11 @@ hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const floa
 hipError_t launch_to_fp(const uint8_t* src, int64_t src_bstride, int c, int ng, int64_t nblk,
                         uint8_t* dst, int64_t dst_bstride, int fmt, hipStream_t stream);
 
+// ximg: a single row's contiguous image (see launch_act_quant), or null.
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
-                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);
+                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream,
+                          const uint8_t* ximg = nullptr);
 
 // Whether the GEMV kernel handles M rows for this plan.
 bool gemv_fits(int64_t M, const ActPlan& ap, const WPlan& wp);

@@ -418,11 +418,14 @@ __device__ __forceinline__ uint8_t store_code(float x, int g, const ActQ& a) {
 
 // Write the units of `nrows` rows whose stored codes sit in LDS (row r at
 // codes + r*Kp) to rows m0.. of the packed activation buffer, one 2*c-byte
-// unit per store.  Used when a workgroup holds fewer than 16 rows.
+// unit per store.  Used when a workgroup holds fewer than 16 rows.  Row 0
+// of the batch also goes, unit after unit, to xdst when that is given (the
+// batch-1 GEMV's contiguous row image).
 template <int C>
 __device__ __forceinline__ void write_group_units(const uint8_t* codes, int nrows, int64_t m0,
                                                   int Kp, int ng, int gbase, int64_t mblk,
-                                                  uint8_t* __restrict__ dst0) {
+                                                  uint8_t* __restrict__ dst0,
+                                                  uint8_t* __restrict__ xdst) {
   const int per_row = ng * 4;
   for (int r = 0; r < nrows; ++r) {
     const int64_t m = m0 + r;
@@ -431,23 +434,31 @@ __device__ __forceinline__ void write_group_units(const uint8_t* codes, int nrow
     for (int rest = threadIdx.x; rest < per_row; rest += blockDim.x) {
       const int qg = rest >> 2, kg = rest & 3;
       const uint4 d = *reinterpret_cast<const uint4*>(src + rest * 16);
-      store_unit(dst + qg * 128 * C + kg * 32 * C, pack_unit(d.x, d.y, d.z, d.w, C), C);
+      const uint4 u = pack_unit(d.x, d.y, d.z, d.w, C);
+      store_unit(dst + qg * 128 * C + kg * 32 * C, u, C);
+      if (xdst != nullptr && m == 0) store_unit(xdst + rest * 2 * C, u, C);
     }
   }
 }
 
+// ximg (null: none): the batch-1 GEMV's image of row 0, written beside the
+// units when the plan has the 4-bit group 0 and 8-bit group 1 that the
+// GEMV stages: group 0's 8-byte units in planned order, then group 1's
+// 16-byte units (at 32 bytes per granule of group 0).
 __device__ __forceinline__ void write_act_units(const uint8_t* codes, int nrows, int64_t m0,
-                                                const ActPlan& ap, uint8_t* __restrict__ packed) {
+                                                const ActPlan& ap, uint8_t* __restrict__ packed,
+                                                uint8_t* __restrict__ ximg = nullptr) {
   for (int g = 0; g < ap.S; ++g) {
     const int c = g ? ap.c[1] : ap.c[0];
     const int ng = g ? ap.ng[1] : ap.ng[0];
     const int gbase = g ? ap.kpad[0] : 0;
     const int64_t mblk = g ? ap.mblk_bytes[1] : ap.mblk_bytes[0];
     uint8_t* dst0 = packed + (g ? ap.seg_off[1] : ap.seg_off[0]);
-    if (c == 8) write_group_units<8>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
-    else if (c == 4) write_group_units<4>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
-    else if (c == 2) write_group_units<2>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
-    else write_group_units<1>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0);
+    uint8_t* xdst = ximg != nullptr && c == (g ? 8 : 4) ? ximg + (g ? ap.ng[0] * 32 : 0) : nullptr;
+    if (c == 8) write_group_units<8>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0, xdst);
+    else if (c == 4) write_group_units<4>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0, xdst);
+    else if (c == 2) write_group_units<2>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0, nullptr);
+    else write_group_units<1>(codes, nrows, m0, ap.Kp, ng, gbase, mblk, dst0, nullptr);
   }
 }
 
@@ -578,7 +589,8 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
                                                   const uint8_t* __restrict__ seg, ActPlan ap,
                                                   const float* __restrict__ partial, int nparts,
                                                   float* __restrict__ s_a_out,
-                                                  uint8_t* __restrict__ packed) {
+                                                  uint8_t* __restrict__ packed,
+                                                  uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
   const int64_t m0 = (int64_t)blockIdx.x * R;
@@ -611,7 +623,7 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
         codes[(int64_t)r * ap.Kp + pos[k]] = store_code(A[(m0 + r) * lda + k], seg[k], aq);
   }
   __syncthreads();
-  write_act_units(codes, rows, m0, ap, packed);
+  write_act_units(codes, rows, m0, ap, packed, ximg);
 }
 
 // One group's units of a 16-row block whose stored codes sit in LDS (row r
@@ -1441,7 +1453,8 @@ __global__ __launch_bounds__(256) void k_act_small(const float* __restrict__ A, 
                                                    int64_t lda, const int32_t* __restrict__ pos,
                                                    const uint8_t* __restrict__ seg, ActPlan ap,
                                                    float* __restrict__ s_a_out,
-                                                   uint8_t* __restrict__ packed) {
+                                                   uint8_t* __restrict__ packed,
+                                                   uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
   const int tid = threadIdx.x;
@@ -1496,7 +1509,7 @@ __global__ __launch_bounds__(256) void k_act_small(const float* __restrict__ A, 
     }
   }
   __syncthreads();
-  write_act_units(codes, 1, m, ap, packed);
+  write_act_units(codes, 1, m, ap, packed, ximg);
 }
 
 // ------------------------------------------------------------ k_act_row1 --
@@ -1512,7 +1525,8 @@ template <int J, int MT>
 __global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, int M, int K4,
                                                   int64_t lda, const int32_t* __restrict__ pos,
                                                   ActPlan ap, float* __restrict__ s_a_out,
-                                                  uint8_t* __restrict__ packed) {
+                                                  uint8_t* __restrict__ packed,
+                                                  uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
   const int tid = threadIdx.x;
@@ -1556,7 +1570,7 @@ __global__ __launch_bounds__(256) void k_act_row1(const float* __restrict__ A, i
       qstore4g(x, h, q, codes, p[j]);
     }
   __syncthreads();
-  write_act_units(codes, 1, m, ap, packed);
+  write_act_units(codes, 1, m, ap, packed, ximg);
 }
 
 // ------------------------------------------------------------ GEMM/GEMV --
@@ -1622,6 +1636,9 @@ struct GemmArgs {
   float* s_a_out;
   uint8_t* act_out;
   int K4, xs_bytes;
+  // batch-1 GEMV: the activation row's contiguous image (null: stage the
+  // row from the units); the fused form writes it
+  uint8_t* ximg;
   // quantization of the outputs for the next layer (k_gemm<..., true>):
   // the next layer's stored codes as bytes, qn_img[m*qn_ld + position];
   // qn_tab[physical column] = the next-layer group of its channel, and
@@ -3234,29 +3251,11 @@ __device__ __forceinline__ int gemv_row_of(int u, int d) {
 // Otherwise every unit as bytes [m][q][kg] (group 0 widened).  A unit is
 // loaded as 16 bytes through a buffer resource over the activation buffer
 // (group 0 units use the first half); indexes past the last unit read as
-// zero.
+// zero.  A single row whose quantizer also left its contiguous image (the
+// nibble-path layout itself) loads 16-byte pieces of that instead: a
+// fraction of the cache lines the row's units are spread over.
 template <int MT>
 constexpr int gemv_xr() { return MT == 1 ? 2 : MT == 2 ? 3 : MT <= 4 ? 5 : 9; }
-
-template <int MT>
-__device__ __forceinline__ void gemv_load_x(const GemmArgs& a, __amdgpu_buffer_rsrc_t xr, int u0,
-                                            uint4 (&xl)[gemv_xr<MT>()]) {
-  const ActPlan& ap = a.ap;
-  const int d = a.wp.ngt * 4, d0 = ap.ng[0] * 4;
-  const int total = (int)a.M * d;
-  const uint32_t o0 = (uint32_t)ap.seg_off[0], o1 = (uint32_t)ap.seg_off[1];
-#pragma unroll
-  for (int i = 0; i < gemv_xr<MT>(); ++i) {
-    // unit rest = 4q + kg of row m: at rest*128 + 8m (4-bit group) or
-    // (rest - 4*ng0)*256 + 16m (byte group) from the group's base
-    const int u = u0 + i * 256 + (int)threadIdx.x;
-    const int m = gemv_row_of<MT>(u, d), rest = u - m * d;
-    const uint32_t off = rest < d0 ? o0 + (uint32_t)(rest * 128 + m * 8)
-                                   : o1 + (uint32_t)((rest - d0) * 256 + m * 16);
-    xl[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                          xr, u < total ? off : kOOB, 0, 0));
-  }
-}
 
 template <int MT, bool NIB>
 __device__ __forceinline__ void gemv_store_x(const GemmArgs& a, int u0,
@@ -3460,34 +3459,83 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
       }
     }
     // the handle's packed row and scales, as soniq_quantize_act leaves them
-    if (blk == 0) write_act_units(codes, 1, 0, ap, a.act_out);
+    if (blk == 0) write_act_units(codes, 1, 0, ap, a.act_out, a.ximg);
     __builtin_amdgcn_s_waitcnt(SONIQ_LGKMCNT0_IMM);
     bar_nofence();
     consume0(0, raw0);
     if (nch1 > 0) consume1(0, raw1);
   } else {
-    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)a.act, (short)0,
-        (int)(ap.S == 2 ? ap.seg_off[1] + ap.mblk_bytes[1] : ap.seg_off[0] + ap.mblk_bytes[0]),
-        0x00020000);
+    // A single row with its contiguous image (cx): 16-byte pieces of it, as
+    // many as the row's units take at 8 (group 0) and 16 bytes (group 1).
+    // Otherwise the units of the batch's rows from the packed buffer.
+    const bool cx = MT == 1 && a.ximg != nullptr;
+    const int total_x = cx ? 2 * ng0 + 4 * ng1 : M * ngt * 4;
+    const __amdgpu_buffer_rsrc_t xr =
+        cx ? __builtin_amdgcn_make_buffer_rsrc((void*)a.ximg, (short)0, total_x * 16, 0x00020000)
+           : __builtin_amdgcn_make_buffer_rsrc(
+                 (void*)a.act, (short)0,
+                 (int)(ap.S == 2 ? ap.seg_off[1] + ap.mblk_bytes[1]
+                                 : ap.seg_off[0] + ap.mblk_bytes[0]),
+                 0x00020000);
     uint4 xl[gemv_xr<MT>()];
-    gemv_load_x<MT>(a, xr, 0, xl);
+    // one load per piece whichever the source (loads on both sides of a
+    // branch would be joined by copies that wait for them)
+    const int d = ngt * 4, d0 = ng0 * 4;
+    const uint32_t o0 = (uint32_t)ap.seg_off[0], o1 = (uint32_t)ap.seg_off[1];
+    auto load_x = [&](int u0) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < gemv_xr<MT>(); ++i) {
+        const int u = u0 + i * 256 + tid;
+        uint32_t off = (uint32_t)u * 16;
+        if (!cx) {
+          // unit rest = 4q + kg of row m: at rest*128 + 8m (4-bit group) or
+          // (rest - 4*ng0)*256 + 16m (byte group) from the group's base
+          const int m = gemv_row_of<MT>(u, d), rest = u - m * d;
+          off = rest < d0 ? o0 + (uint32_t)(rest * 128 + m * 8)
+                          : o1 + (uint32_t)((rest - d0) * 256 + m * 16);
+        }
+        xl[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              xr, u < total_x ? off : kOOB, 0, 0));
+      }
+    };
+    // the image is the staged layout of a nibble-path block; other blocks
+    // widen group 0's units to bytes
+    auto store_x = [&](int u0) __attribute__((always_inline)) {
+      if (cx) {
+#pragma unroll
+        for (int i = 0; i < gemv_xr<MT>(); ++i) {
+          const int c = u0 + i * 256 + tid;
+          if (c < total_x) {
+            if (NIB) {
+              *reinterpret_cast<uint4*>(xs + 16 * c) = xl[i];
+            } else if (c < 2 * ng0) {
+              *reinterpret_cast<uint4*>(xs + 32 * c) = unpack4(xl[i].x, xl[i].y);
+              *reinterpret_cast<uint4*>(xs + 32 * c + 16) = unpack4(xl[i].z, xl[i].w);
+            } else {
+              *reinterpret_cast<uint4*>(xs + 16 * (c + 2 * ng0)) = xl[i];
+            }
+          }
+        }
+      } else {
+        gemv_store_x<MT, NIB>(a, u0, xl, xs, nbase);
+      }
+    };
+    load_x(0);
     uint4 raw0[NB0], raw1[NB1];
-    const int total_x = M * ngt * 4;
     const bool more_x = total_x > 256 * gemv_xr<MT>();
     if (more_x) {
       // rows too long for one round: stage them all before the chunk loads
       // (waits inside the staging loop would otherwise drain the chunks)
-      gemv_store_x<MT, NIB>(a, 0, xl, xs, nbase);
+      store_x(0);
       for (int u0 = 256 * gemv_xr<MT>(); u0 < total_x; u0 += 256 * gemv_xr<MT>()) {
-        gemv_load_x<MT>(a, xr, u0, xl);
-        gemv_store_x<MT, NIB>(a, u0, xl, xs, nbase);
+        load_x(u0);
+        store_x(u0);
       }
     }
     // one place for the chunk loads: their registers need no copies at a join
     issue0(0, raw0);
     issue1(0, raw1);
-    if (!more_x) gemv_store_x<MT, NIB>(a, 0, xl, xs, nbase);
+    if (!more_x) store_x(0);
     // The staged rows must be visible to every wave, but the weight chunks
     // may still be in flight: wait for LDS writes only, then a plain
     // barrier (a full __syncthreads would also drain every chunk load).
@@ -3569,9 +3617,9 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
 
 // Batch of one row, quantized inside the GEMV: every workgroup computes
 // the row's group maxima and codes (J float4 per thread) while its weight
-// chunks stream in; workgroup 0 also leaves the packed row and the scales
-// in the handle.  Dynamic LDS: the staged row (xs_bytes), then Kp code
-// bytes.
+// chunks stream in; workgroup 0 also leaves the packed row, its image and
+// the scales in the handle.  Dynamic LDS: the staged row (xs_bytes), then
+// Kp code bytes.
 template <int J>
 __global__ __launch_bounds__(256) void k_gemv_fused(GemmArgs a) {
   extern __shared__ __align__(16) uint8_t xs[];
@@ -3820,7 +3868,8 @@ template <int R>
 __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ img, int64_t M,
                                                   ActPlan ap, float s0, float s1,
                                                   float* __restrict__ s_a,
-                                                  uint8_t* __restrict__ packed) {
+                                                  uint8_t* __restrict__ packed,
+                                                  uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
   const int64_t m0 = (int64_t)blockIdx.x * R;
   const int rows = (int)min((int64_t)R, M - m0);
@@ -3845,7 +3894,7 @@ __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ im
       else write_block_pieces<2, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
     }
   } else {
-    write_act_units(codes, rows, m0, ap, packed);
+    write_act_units(codes, rows, m0, ap, packed, ximg);
   }
 }
 
@@ -4686,7 +4735,10 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
                             const ActPlan& ap, const int32_t* pos_dev,
                             const uint8_t* seg_dev, float* partial,
                             unsigned int* counter, float* s_a, uint8_t* packed,
-                            hipStream_t stream) {
+                            hipStream_t stream, uint8_t* ximg, bool* ximg_done) {
+  // the row image is written by the per-row quantizers below, for one row
+  if (M != 1) ximg = nullptr;
+  if (ximg_done) *ximg_done = false;
   const bool aligned = (K % 4 == 0) && (lda % 4 == 0) &&
                        (reinterpret_cast<uintptr_t>(A) % 16 == 0);
   const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
@@ -4697,7 +4749,7 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
     const int J = (K4 + 255) / 256;
 #define SONIQ_ROWS(J_, MT_)                                                                       \
   hipLaunchKernelGGL((k_act_row1<J_, MT_>), dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A, \
-                     (int)M, K4, lda, pos_dev, ap, s_a, packed)
+                     (int)M, K4, lda, pos_dev, ap, s_a, packed, ximg)
     if (M == 1) {
       if (J <= 1) SONIQ_ROWS(1, 1);
       else if (J <= 2) SONIQ_ROWS(2, 1);
@@ -4712,11 +4764,13 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
       if (J <= 2) SONIQ_ROWS(2, 8); else SONIQ_ROWS(4, 8);
     }
 #undef SONIQ_ROWS
+    if (ximg_done) *ximg_done = ximg != nullptr;
     return hipGetLastError();
   }
   if (aligned && M <= 64 && M * K <= kSmallElems) {
     hipLaunchKernelGGL(k_act_small, dim3((unsigned)M), dim3(256), (size_t)ap.Kp, stream, A,
-                       (int)M, (int)K, lda, pos_dev, seg_dev, ap, s_a, packed);
+                       (int)M, (int)K, lda, pos_dev, seg_dev, ap, s_a, packed, ximg);
+    if (ximg_done) *ximg_done = ximg != nullptr;
     return hipGetLastError();
   }
   if (aligned && !sign && M * K >= kCoopMinElems) {
@@ -4760,7 +4814,7 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
 #define SONIQ_ACT_ROWS(R_, J_)                                                                  \
   hipLaunchKernelGGL((k_act_rows<R_, J_>), dim3((unsigned)((M + R_ - 1) / R_)), dim3(256),      \
                      (size_t)R_ * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,    \
-                     nparts, s_a, packed)
+                     nparts, s_a, packed, ximg)
   // whole 8- or 16-row block slices per workgroup for larger batches
   // 16 rows per workgroup once that still gives ~1.5 workgroups per CU,
   // else 8 (more workgroups in flight)
@@ -4791,6 +4845,8 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
     }
   }
 #undef SONIQ_ACT_ROWS
+  // a single row never takes the block form (M >= 1024)
+  if (ximg_done) *ximg_done = ximg != nullptr;
   return hipGetLastError();
 }
 
@@ -4813,6 +4869,7 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.apos = nullptr;
   a.s_a_out = nullptr;
   a.act_out = nullptr;
+  a.ximg = nullptr;
   a.K4 = 0;
   a.xs_bytes = 0;
   a.qn_img = nullptr;
@@ -4922,7 +4979,7 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
                                 const ActPlan& ap2, const float* s_next, float* s_a2,
-                                float* brs2, uint8_t* packed2, hipStream_t stream) {
+                                float* brs2, uint8_t* packed2, hipStream_t stream, uint8_t* ximg2) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const bool blocks = ap2.gsub[0] > 0;
   if (blocks) {
@@ -4969,10 +5026,11 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   float* s_out = blocks ? nullptr : s_a2;  // block scales were stored above
   if (kBlk * (size_t)ap2.Kp <= 64 * 1024)
     hipLaunchKernelGGL(k_pack_img<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
-                       kBlk * (size_t)ap2.Kp, stream, img, M, ap2, s0, s1, s_out, packed2);
+                       kBlk * (size_t)ap2.Kp, stream, img, M, ap2, s0, s1, s_out, packed2,
+                       M == 1 ? ximg2 : nullptr);
   else
     hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)M), dim3(256), (size_t)ap2.Kp, stream, img, M,
-                       ap2, s0, s1, s_out, packed2);
+                       ap2, s0, s1, s_out, packed2, M == 1 ? ximg2 : nullptr);
   return hipGetLastError();
 }
 
@@ -5020,8 +5078,10 @@ size_t gemv_fused_lds(const ActPlan& ap, const WPlan& wp) {
 
 hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, uint8_t* act_packed,
                              float* s_a, const ActPlan& ap, const WDev& wd, const WPlan& wp,
-                             int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream) {
+                             int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream,
+                             uint8_t* ximg) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, 1, N, Y, N, acc);
+  a.ximg = ximg;
   a.a32 = A;
   a.apos = pos_dev;
   a.s_a_out = s_a;
@@ -5038,8 +5098,10 @@ hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, 
 
 hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
-                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
-  const GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+                          uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream,
+                          const uint8_t* ximg) {
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  if (M == 1) a.ximg = const_cast<uint8_t*>(ximg);
   dim3 grid((unsigned)wp.nblk);
   const size_t lds = gemv_lds(M, ap, wp);
   // Batches of 2..8 rows: the products on matrix cores.  SONIQ_GEMV_MFMA

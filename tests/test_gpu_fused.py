@@ -82,3 +82,61 @@ def test_fused_repeat_calls():
     act = sq.soniq_act_create(w, 1)
     for case in (a, b, a):
         compare_full(run_fused(case, act=act, w=w), oracle_run(case))
+
+
+def test_fused_many_calls_one_handle():
+    """Successive one-row calls through one handle, each on new data, equal
+    the two calls they stand for (packed row, image and scales included)."""
+    case = G(1, 512, 2048, 4, 8, 0.7, 2, 4, 0.6, True, 9, "fused_seq")
+    w = sq.soniq_pack_weights(torch.from_numpy(case["W"]).cuda(), case["w_bits"], case["a_bits"],
+                              True)
+    act = sq.soniq_act_create(w, 1)
+    rng = np.random.default_rng(9)
+    for i in range(24):
+        c = dict(case)
+        c["A"] = np.ascontiguousarray(case["A"] * np.float32(rng.uniform(-3, 3)) +
+                                      rng.standard_normal(case["A"].shape).astype(np.float32))
+        c["name"] = f"fused_seq_{i}"
+        g = run_fused(c, act=act, w=w)
+        y2, acc2, q2, s2 = two_calls(c, w)
+        np.testing.assert_array_equal(g["acc"], acc2, err_msg=f"call {i}")
+        np.testing.assert_array_equal(g["y"], y2, err_msg=f"call {i}")
+        np.testing.assert_array_equal(g["q_a"], q2, err_msg=f"call {i}")
+        np.testing.assert_array_equal(g["s_a"], s2, err_msg=f"call {i}")
+
+
+def test_fused_graph_replay():
+    """The one-launch call captured in a HIP graph and replayed on new rows,
+    with eager work between the replays, equals eager calls bit for bit."""
+    case = workloads.make("decode_11008_m1")
+    N = case["N"]
+    w = sq.soniq_pack_weights(torch.from_numpy(case["W"]).cuda(), case["w_bits"], case["a_bits"],
+                              case["a_signed"])
+    act_g = sq.soniq_act_create(w, 1)
+    act_e = sq.soniq_act_create(w, 1)
+    A0 = torch.from_numpy(case["A"]).cuda()
+    inputs = [A0 * s for s in (1.0, -0.5, 3.0, 1.0, 0.01)]
+    A_buf = inputs[0].clone()
+    Yg = torch.empty((1, N), dtype=torch.bfloat16, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        sq.soniq_quantize_mp_gemm(act_g, w, A_buf, out=Yg)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        sq.soniq_quantize_mp_gemm(act_g, w, A_buf, out=Yg)
+    torch.cuda.synchronize()
+    for r, A in enumerate(inputs):
+        A_buf.copy_(A)
+        Yg.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        Ye = sq.soniq_quantize_mp_gemm(act_e, w, A)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(_bf16_bits(Yg), _bf16_bits(Ye), err_msg=f"replay {r}")
+        # the handle keeps the row the replay quantized
+        q_g, s_g = sq.soniq_act_unpack_debug(act_g)
+        q_e, s_e = sq.soniq_act_unpack_debug(act_e)
+        np.testing.assert_array_equal(q_g, q_e, err_msg=f"replay {r} codes")
+        np.testing.assert_array_equal(s_g, s_e, err_msg=f"replay {r} scales")

@@ -214,6 +214,51 @@ def test_small_batch_long_rows(M, K):
     compare_full(gpu_run(case), oracle_run(case))
 
 
+@pytest.mark.parametrize("K,lda_pad,wlo,whi", [
+    (1000, 0, 2, 4),    # per-row quantizer; nibble-path blocks
+    (1000, 0, 4, 8),    # byte-path blocks widen the image's 4-bit units
+    (1000, 0, 1, 4),    # sign-bit blocks
+    (20000, 0, 2, 8),   # small-batch quantizer; several staging rounds
+    (1001, 3, 2, 4),    # unaligned row: two-pass quantizer
+])
+def test_single_row_image(K, lda_pad, wlo, whi):
+    """A GEMV of one row stages the contiguous row image its quantizer left
+    beside the units; every quantizer of one row writes it."""
+    case = workloads.generic(1, 200, K, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=wlo, w_hi=whi,
+                             w_frac_lo=0.5, seed=K + wlo + lda_pad, name="row_image")
+    compare_full(gpu_run(case, lda_pad=lda_pad), oracle_run(case))
+
+
+def test_single_row_image_after_other_writers():
+    """The image follows whatever last quantized the handle: larger batches
+    (which leave no image), the fused one-call form, and one row again."""
+    big = workloads.generic(24, 300, 2000, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=4,
+                            w_frac_lo=0.5, seed=77, name="row_image_seq")
+    W = torch.from_numpy(big["W"]).cuda()
+    w = sq.soniq_pack_weights(W, big["w_bits"], big["a_bits"], True)
+    act = sq.soniq_act_create(w, 24)
+    for step, (M, lo, fused) in enumerate([(1, 0, False), (24, 0, False), (1, 5, False),
+                                           (3, 2, False), (1, 9, True), (1, 9, False),
+                                           (1, 11, True)]):
+        print(f"[gpu] row image step {step}: M={M} row {lo} fused={fused}", flush=True)
+        A_np = big["A"][lo:lo + M].copy()
+        A = torch.from_numpy(A_np).cuda()
+        acc = torch.empty((w.S, M, 300), dtype=torch.int32, device="cuda")
+        if fused:
+            Y = sq.soniq_quantize_mp_gemm(act, w, A, acc=acc)
+        else:
+            sq.soniq_quantize_act(act, A)
+            Y = sq.soniq_mp_gemm(act, w, acc=acc)
+        torch.cuda.synchronize()
+        r = oracle.run(A_np, big["W"], big["a_bits"], big["w_bits"], True)
+        np.testing.assert_array_equal(acc.cpu().numpy(), r["acc"])
+        np.testing.assert_array_equal(_bf16_bits(Y), r["y_replay"])
+    # a GEMV after the fused call reads the image the fused call left
+    Y2 = sq.soniq_mp_gemm(act, w)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_bf16_bits(Y2), r["y_replay"])
+
+
 def test_strides_and_unaligned_rows():
     case = workloads.generic(70, 100, 131, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
                              w_frac_lo=0.5, seed=5, name="strides")
