@@ -197,6 +197,19 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     # the same calls on one weight copy, which then stays in the 256 MB
     # Infinity Cache (reported beside the rotated figure, never as it)
     g_hot_ms = timed(lambda i: sq.soniq_mp_gemm(acts[0], ws[0], out=Y))
+    # Decode batches are bandwidth-bound: the plain-read time of the same
+    # packed weight bytes (one trivial read per call, rotated over 1 GiB
+    # like the weights, timed the same way) is the ceiling the GEMV is held
+    # against.
+    read_ms = None
+    if M <= 8:
+        nbytes = int(info.packed_w_bytes) // 16 * 16
+        rbuf = torch.empty(ROTATE_W_BYTES, dtype=torch.uint8, device=dev)
+        nsl = max(1, ROTATE_W_BYTES // nbytes) if rotate else 1
+        sink = torch.empty((nbytes + 8191) // 8192, dtype=torch.int32, device=dev)
+        read_ms = timed(lambda i: sq.soniq_debug_stream_read(rbuf, nbytes, sink,
+                                                             offset=(i % nsl) * nbytes))
+        del rbuf, sink
     del acts, ws
 
     # bf16 comparator: torch's GEMM (hipBLASLt) on the same shapes, the same
@@ -213,7 +226,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     bf16_ms = timed(lambda i: torch.nn.functional.linear(Ab[i % nab], Wb[i % nwb]))
     del Ab, Wb
     return dict(total_ms=total_ms, wall_s=wall, q_ms=q_ms, g_ms=g_ms, g_hot_ms=g_hot_ms,
-                pack_ms=pack_ms,
+                pack_ms=pack_ms, read_ms=read_ms,
                 bf16_ms=bf16_ms, info=info, na=na, nw=nw)
 
 
@@ -308,6 +321,11 @@ def gemv_record(case, r, steps):
         "step_packed_weight_gbs": alg["w_packed"] / step_s / 1e9,
         "step_us": step_s * 1e6, "mp_gemm_us": g_s * 1e6, "quantize_act_us": r["q_ms"] * 1e3,
         "mp_gemm_weights_cache_hot_us": r["g_hot_ms"] * 1e3,
+        # a plain read of the packed weight bytes, rotated and timed the same
+        # way, and the GEMV's time as a fraction of it
+        "plain_read_us": r["read_ms"] * 1e3,
+        "plain_read_gbs": alg["w_packed"] / (r["read_ms"] * 1e-3) / 1e9,
+        "of_plain_read": r["read_ms"] / r["g_ms"],
         "roofline": dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
                          frac=ach / HBM_PEAK_GBS, traffic=measured_traffic(kernel, case["name"]),
                          kernel=kernel, algorithmic_bytes=kbytes, launch_us=g_s * 1e6),
@@ -533,6 +551,7 @@ def main():
         "gemm_tops": alg["ops"] / (r["g_ms"] * 1e-3) / 1e12,
         "packed_weight_gbs": alg["w_packed"] / (r["g_ms"] * 1e-3) / 1e9,
         "mp_gemm_weights_cache_hot_ms": r["g_hot_ms"],
+        "plain_read_weights_ms": r["read_ms"],
         "bf16_linear_ms": r["bf16_ms"],
         "speedup_vs_bf16": {"gemm": r["bf16_ms"] / r["g_ms"], "step": r["bf16_ms"] / ms},
     }

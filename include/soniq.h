@@ -438,6 +438,20 @@ soniq_status soniq_act_unpack_debug(soniq_act act, int32_t* codes, float* s_a);
  */
 soniq_status soniq_act_wait_timeouts(soniq_act act, uint64_t* count);
 
+/*
+ * soniq_debug_stream_read -- a measurement aid, not part of the method:
+ * reads `bytes` bytes at src_dev (device, 16-byte aligned; bytes a positive
+ * multiple of 16, below 2^31) once, in 16-byte loads, two per thread and
+ * 8 KB per workgroup, and writes the XOR of each workgroup's words to
+ * sink_dev[workgroup] (ceil(bytes / 8192) words, device).  Its duration on
+ * the packed weights of a batch-1 GEMV is the plain-read time of those
+ * bytes on this device, the ceiling the GEMV is measured against.
+ * Asynchronous on `stream` (NULL = default stream).
+ * Errors: INVALID_ARGUMENT, HIP.
+ */
+soniq_status soniq_debug_stream_read(const void* src_dev, int64_t bytes, uint32_t* sink_dev,
+                                     void* stream);
+
 /* Release a handle (NULL is ignored).  Waits for the device first. */
 void soniq_weights_destroy(soniq_weights w);
 void soniq_act_destroy(soniq_act act);

@@ -37,7 +37,8 @@ EXPORTED = [
     "soniq_mp_gemm_quantize_next",
     "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
-    "soniq_act_unpack_debug", "soniq_act_wait_timeouts", "soniq_weights_destroy",
+    "soniq_act_unpack_debug", "soniq_act_wait_timeouts", "soniq_debug_stream_read",
+    "soniq_weights_destroy",
     "soniq_act_destroy",
     "soniq_last_error",
 ]
@@ -110,6 +111,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_act_unpack_debug.argtypes = [vp, vp, vp]
         L.soniq_act_wait_timeouts.restype = st
         L.soniq_act_wait_timeouts.argtypes = [vp, ctypes.POINTER(ctypes.c_uint64)]
+        L.soniq_debug_stream_read.restype = st
+        L.soniq_debug_stream_read.argtypes = [vp, i64, vp, vp]
         L.soniq_weights_destroy.restype = None
         L.soniq_weights_destroy.argtypes = [vp]
         L.soniq_act_destroy.restype = None
@@ -411,6 +414,22 @@ def soniq_act_unpack_debug(act: Activations):
     _check(lib().soniq_act_unpack_debug(act.handle, codes.ctypes.data_as(ctypes.c_void_p),
                                         s_a.ctypes.data_as(ctypes.c_void_p)))
     return codes, s_a[: act.weights.S].copy()
+
+
+def soniq_debug_stream_read(src, nbytes: int, sink, offset: int = 0, stream=None) -> None:
+    """One plain read of nbytes of the device tensor src from byte offset
+    `offset` (a measurement aid: the ceiling a bandwidth-bound kernel is
+    held against); sink, an int32 device tensor of at least
+    ceil(nbytes / 8192) elements, receives one XOR per workgroup."""
+    import torch
+    if not (isinstance(src, torch.Tensor) and src.is_cuda and src.is_contiguous()):
+        raise TypeError("src must be a contiguous device tensor")
+    if offset < 0 or offset + nbytes > src.numel() * src.element_size():
+        raise ValueError("the read lies outside src")
+    if sink.dtype != torch.int32 or not sink.is_cuda or sink.numel() < (nbytes + 8191) // 8192:
+        raise TypeError("sink must be an int32 device tensor of ceil(nbytes / 8192) elements")
+    _check(lib().soniq_debug_stream_read(ctypes.c_void_p(src.data_ptr() + offset), nbytes,
+                                         _dev(sink, "int32"), _stream(stream)))
 
 
 def soniq_act_wait_timeouts(act: Activations) -> int:

@@ -1255,6 +1255,16 @@ soniq_status soniq_act_wait_timeouts(soniq_act act, uint64_t* count) {
   return SONIQ_OK;
 }
 
+soniq_status soniq_debug_stream_read(const void* src_dev, int64_t bytes, uint32_t* sink_dev,
+                                     void* stream) {
+  if (!src_dev || !sink_dev || bytes < 16 || bytes % 16 != 0 || bytes >= ((int64_t)1 << 31) ||
+      reinterpret_cast<uintptr_t>(src_dev) % 16 != 0)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                "soniq_debug_stream_read: null pointer, unaligned source or bad byte count");
+  HIP_TRY(launch_stream_read(src_dev, bytes, sink_dev, reinterpret_cast<hipStream_t>(stream)));
+  return SONIQ_OK;
+}
+
 void soniq_weights_destroy(soniq_weights w) {
   if (!live_w(w)) return;
   w->released = true;

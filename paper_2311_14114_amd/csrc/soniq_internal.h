@@ -269,6 +269,10 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
                           uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream,
                           const uint8_t* ximg = nullptr);
 
+// One plain read of `bytes` (a multiple of 16) at src: 8 KB per workgroup,
+// the XOR of its words to sink[workgroup] (a measurement aid).
+hipError_t launch_stream_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream);
+
 // Whether the GEMV kernel handles M rows for this plan.
 bool gemv_fits(int64_t M, const ActPlan& ap, const WPlan& wp);
 

@@ -5435,6 +5435,34 @@ __global__ __launch_bounds__(256) void k_fill_u32(uint32_t* __restrict__ p, int 
   for (int i = (int)(blockIdx.x * 256 + threadIdx.x); i < n; i += (int)(gridDim.x * 256)) p[i] = v;
 }
 
+// ---------------------------------------------------------- k_stream_read --
+// A plain read, the ceiling a bandwidth-bound kernel is measured against:
+// 8 KB per workgroup in two 16-byte loads per thread, both issued before
+// either is used; the XOR of the workgroup's words is its one output.
+__global__ __launch_bounds__(256) void k_stream_read(const uint8_t* __restrict__ src, int bytes,
+                                                     uint32_t* __restrict__ sink) {
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc((void*)src, (short)0, bytes, 0x00020000);
+  const uint32_t base = blockIdx.x * 8192u + threadIdx.x * 16u;
+  const uint4 v0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, base, 0, 0));
+  const uint4 v1 =
+      __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, base + 4096u, 0, 0));
+  uint32_t x = v0.x ^ v0.y ^ v0.z ^ v0.w ^ v1.x ^ v1.y ^ v1.z ^ v1.w;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x ^= (uint32_t)__shfl_xor((int)x, o, 64);
+  __shared__ uint32_t red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
+hipError_t launch_stream_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream) {
+  const unsigned grid = (unsigned)((bytes + 8191) / 8192);
+  hipLaunchKernelGGL(k_stream_read, dim3(grid), dim3(256), 0, stream,
+                     static_cast<const uint8_t*>(src), (int)bytes, sink);
+  return hipGetLastError();
+}
+
 hipError_t scratch_device_ptr(hipStream_t stream, uint8_t** out) {
   constexpr int kMaxDevices = 64;
   static std::mutex mu;

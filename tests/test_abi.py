@@ -36,6 +36,14 @@ def test_exports_every_declared_symbol(L):
         assert hasattr(L, name), name
 
 
+def test_stream_read_validation(L):
+    fake = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+    for src, n, sink in ((None, 64, fake), (fake, 64, None), (fake, 0, fake), (fake, 24, fake),
+                         (ctypes.c_void_p(0x1008), 64, fake), (fake, 1 << 31, fake)):
+        assert L.soniq_debug_stream_read(src, n, sink, None) == sq.SONIQ_ERR_INVALID_ARGUMENT
+    assert b"soniq_debug_stream_read" in L.soniq_last_error()
+
+
 def _pack(L, W, N, K, ldw, wb, ab, a_signed=1, mode=0):
     h = ctypes.c_void_p()
     rc = L.soniq_pack_weights_ex(W, N, K, ldw, wb, ab, a_signed, mode, None, ctypes.byref(h))

@@ -259,6 +259,20 @@ def test_single_row_image_after_other_writers():
     np.testing.assert_array_equal(_bf16_bits(Y2), r["y_replay"])
 
 
+def test_stream_read_probe():
+    """The plain-read probe bench.py holds the GEMV against reads every byte:
+    its per-workgroup XORs equal the host's, ragged last workgroup included."""
+    n = 8192 * 37 + 48
+    src = torch.randint(0, 256, (n + 64,), dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(38, dtype=torch.int32, device="cuda")
+    sq.soniq_debug_stream_read(src, n, sink, offset=16)
+    torch.cuda.synchronize()
+    words = np.zeros((38 * 8192) // 4, np.uint32)
+    words.view(np.uint8)[:n] = src.cpu().numpy()[16:16 + n]
+    ref = np.bitwise_xor.reduce(words.reshape(38, 2048), axis=1)
+    np.testing.assert_array_equal(sink.cpu().numpy().view(np.uint32), ref)
+
+
 def test_strides_and_unaligned_rows():
     case = workloads.generic(70, 100, 131, a_lo=4, a_hi=8, a_frac_lo=0.5, w_lo=2, w_hi=4,
                              w_frac_lo=0.5, seed=5, name="strides")
