@@ -20,6 +20,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -435,7 +436,10 @@ soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* a
   const bool gemv = !w->act_group_bits && gemv_fits(M, act.ap, w->wp);
   if (!gemv && ((M + 63) / 64) * (w->wp.Np / kGemmBN) > 0x7FFFFFFFLL)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm: problem too large for one launch");
-  if (w->act_group_bits)
+  if (w->act_group_bits && gemv_g_fits(M, act.ap, w->wp) && !getenv("SONIQ_GROUPED_MFMA"))
+    HIP_TRY(launch_mp_gemv_grouped(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev,
+                                   ldy, acc_dev, st));
+  else if (w->act_group_bits)
     HIP_TRY(launch_mp_gemm_grouped(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                                    acc_dev, st));
   else if (gemv)

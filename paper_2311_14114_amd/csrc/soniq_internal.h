@@ -219,6 +219,13 @@ hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_
 hipError_t launch_mp_gemm_grouped(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                   const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
                                   uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);
+// The same for batches of at most 8 rows without matrix cores: one exact
+// int32 sum per activation block and output, folded in block order; where
+// it applies (activation containers 4 and 8, weight containers 2, 4, 8).
+bool gemv_g_fits(int64_t M, const ActPlan& ap, const WPlan& wp);
+hipError_t launch_mp_gemv_grouped(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                  const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
+                                  uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream);
 
 // The GEMM whose epilogue also quantizes its outputs for the next layer
 // with static scales s_next (host, one per next-layer group): codes go to

@@ -3282,10 +3282,15 @@ __device__ __forceinline__ void gemv_store_x(const GemmArgs& a, int u0,
 
 // FJ > 0 (batch of one row only): the fused form, which quantizes the fp32
 // row itself (FJ float4 per thread) instead of staging packed units.
-template <int MT, int CW, bool NIB, int FJ = 0>
+// GB: sub-group activation scales (zero points 0, no 1-bit weights): each
+// slot's products are summed over the lanes of its rows and added into one
+// exact int32 sum per activation block in LDS (after the staged rows), and
+// the epilogue folds the blocks in order as the MFMA GEMM does.
+template <int MT, int CW, bool NIB, int FJ = 0, bool GB = false>
 __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int blk,
                                             int (&red)[4][4][kBlk][2][MT]) {
   static_assert(FJ == 0 || MT == 1, "the fused form takes one row");
+  static_assert(!GB || (FJ == 0 && CW != 1), "block sums: no fused form, no sign-bit weights");
   constexpr int U = 8 / CW;
   constexpr int CPG = 8 * CW;    // chunks per granule
   constexpr int QS = 256 / CPG;  // granules per slot of the workgroup
@@ -3357,7 +3362,56 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
       }
     }
   };
+  // GB: exact per-block sums in LDS, [block][batch row][block row]
+  int* gacc = reinterpret_cast<int*>(xs + a.xs_bytes);
+  const int gl16 = lane & 15;
+  auto gadd = [&](int j, int (&v)[U][MT]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) v[u][mm] = dpp_row_sum<CW>(v[u][mm]);
+    if (gl16 < 2 * CW) {
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm)
+        if (mm < M)
+#pragma unroll
+          for (int u = 0; u < U; ++u) atomicAdd(&gacc[(j * MT + mm) * kBlk + U * gl16 + u], v[u][mm]);
+    }
+  };
   auto consume0 = [&](int s0, const uint4 (&raw)[NB0]) __attribute__((always_inline)) {
+    if constexpr (GB) {
+      // one slot's granule lies in one block; a 16-lane row of lanes never
+      // spans two granules (CW >= 2)
+      const int gpg = ap.gsub[0];
+#pragma unroll
+      for (int b = 0; b < NB0; ++b) {
+        if (256 * (s0 + b) >= nch0) break;  // the same for the whole workgroup
+        const int q = q0 + QS * (s0 + b);
+        int v[U][MT];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int mm = 0; mm < MT; ++mm) v[u][mm] = 0;
+        if constexpr (NIB) {
+#pragma unroll
+          for (int mm = 0; mm < MT; ++mm) {
+            if (mm < M) {
+              const uint2 xq = *reinterpret_cast<const uint2*>(
+                  xs + (mm * ng0 + min(q, ng0 - 1)) * 32 + kg * 8);
+#pragma unroll
+              for (int u = 0; u < U; ++u) {
+                const uint2 w = chunk_nibbles<CW>(raw[b], u);
+                v[u][mm] = dot16n(w.x, w.y, xq, 0);
+              }
+            }
+          }
+        } else {
+          bytes_into(v, raw[b], min(q, ng0 - 1), true);
+        }
+        if (q < ng0) gadd(q / gpg, v);
+      }
+      return;
+    }
     if constexpr (NIB) {
       // every slot's staged activations first (one LDS round trip), then
       // the products slot by slot as the chunks land
@@ -3392,6 +3446,22 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
     }
   };
   auto consume1 = [&](int s0, const uint4 (&raw)[NB1]) __attribute__((always_inline)) {
+    if constexpr (GB) {
+      const int gpg = ap.gsub[1];
+#pragma unroll
+      for (int b = 0; b < NB1; ++b) {
+        if (256 * (s0 + b) >= nch1) break;  // the same for the whole workgroup
+        const int q = q0 + QS * (s0 + b);
+        int v[U][MT];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int mm = 0; mm < MT; ++mm) v[u][mm] = 0;
+        bytes_into(v, raw[b], ng0 + min(q, ng1 - 1), true);
+        if (q < ng1) gadd(ap.nsub[0] + q / gpg, v);
+      }
+      return;
+    }
 #pragma unroll
     for (int b = 0; b < NB1; ++b) {
       if (256 * (s0 + b) >= nch1) break;  // the same for the whole workgroup
@@ -3536,6 +3606,10 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
     issue0(0, raw0);
     issue1(0, raw1);
     if (!more_x) store_x(0);
+    if constexpr (GB) {
+      const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
+      for (int i = tid; i < nsub * MT * kBlk; i += 256) gacc[i] = 0;
+    }
     // The staged rows must be visible to every wave, but the weight chunks
     // may still be in flight: wait for LDS writes only, then a plain
     // barrier (a full __syncthreads would also drain every chunk load).
@@ -3555,6 +3629,24 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
     consume1(s0, raw);
   }
 
+  if constexpr (GB) {
+    // every block sum is in LDS: fold the blocks in order, multiply then
+    // add (y = sum_j f(ACC_j) * s_a[j]), then scale by s_w
+    __syncthreads();
+    if (tid < kBlk * M && eci.n >= 0) {
+      const int nsub0 = ap.nsub[0], nsub = nsub0 + (ap.S == 2 ? ap.nsub[1] : 0);
+      const int shb0 = NIB ? (CW == 2 ? 2 : 0) : ap.sh[0] + (eshw & 0x7F);
+      const int shb1 = ap.sh[1] + (eshw & 0x7F);
+      float y = 0.0f;
+      for (int j = 0; j < nsub; ++j) {
+        const int t = gacc[(j * MT + em) * kBlk + er] >> (j < nsub0 ? shb0 : shb1);
+        y = __fadd_rn(y, __fmul_rn((float)t, a.s_a[j]));
+        if (a.acc) a.acc[((int64_t)j * a.M + em) * a.N + eci.n] = t;
+      }
+      a.Y[(int64_t)em * a.ldy + eci.n] = bf16_rne(__fmul_rn(y, eci.s_w));
+    }
+    return;
+  }
   // Within each 16-lane row, then rows and waves through LDS.
   const int row16 = lane >> 4, l16 = lane & 15;
 #pragma unroll
@@ -3614,6 +3706,20 @@ __global__ __launch_bounds__(256) void k_gemv(GemmArgs a) {
   else if constexpr (MT <= 4) gemv4_block<MT, 1, false>(a, xs, blk, red);
 }
 
+
+// Batches of at most 8 rows whose activations have sub-group scales: the
+// GEMV with one exact int32 sum per activation block.  Dynamic LDS: the
+// staged rows (xs_bytes), then the block sums [nsub][MT][16].
+template <int MT>
+__global__ __launch_bounds__(256) void k_gemv_g(GemmArgs a) {
+  extern __shared__ __align__(16) uint8_t xs[];
+  __shared__ int red[4][4][kBlk][2][MT];
+  const int blk = blockIdx.x;
+  const int c = wblk_c(a.wp, blk);
+  if (c == 2) gemv4_block<MT, 2, true, 0, true>(a, xs, blk, red);
+  else if (c == 4) gemv4_block<MT, 4, true, 0, true>(a, xs, blk, red);
+  else gemv4_block<MT, 8, false, 0, true>(a, xs, blk, red);
+}
 
 // Batch of one row, quantized inside the GEMV: every workgroup computes
 // the row's group maxima and codes (J float4 per thread) while its weight
@@ -4053,6 +4159,92 @@ __global__ __launch_bounds__(256) void k_gabsmax4(const float4* __restrict__ A, 
   }
   __syncthreads();
   for (int j = tid; j < nsub; j += 256) part[(int64_t)blockIdx.x * nsub + j] = __uint_as_float(smax[j]);
+}
+
+// Sub-group scales for batches of at most MT <= 8 rows in one launch:
+// workgroup m loads every row of the batch once (J float4 per thread and
+// row), folds their block maxima into LDS, turns them into the block
+// scales, and quantizes its own row m with them, with the arithmetic of
+// k_gabsmax4, k_gscales and k_gquant4 (so the codes and scales are
+// theirs).  Workgroup 0 stores the scales.  Dynamic LDS: Kp code bytes,
+// then nsub maxima, scales and reciprocals.
+template <int J, int MT>
+__global__ __launch_bounds__(256) void k_gact_rows(const float4* __restrict__ A, int M, int K4,
+                                                   int64_t lda4, const int4* __restrict__ pos4,
+                                                   const int4* __restrict__ grp4, ActPlan ap,
+                                                   int nsub, float* __restrict__ s_a,
+                                                   uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  unsigned* smax = reinterpret_cast<unsigned*>(codes + ap.Kp);
+  float* stab = reinterpret_cast<float*>(smax + nsub);
+  float* rtab = stab + nsub;
+  const int tid = threadIdx.x;
+  const int m = blockIdx.x;
+  float4 v[MT][J];
+  int4 p[J], gb[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int k4 = min(tid + 256 * j, K4 - 1);  // repeats change no max
+    p[j] = pos4[k4];
+    gb[j] = grp4[k4];
+#pragma unroll
+    for (int r = 0; r < MT; ++r) v[r][j] = A[(int64_t)min(r, M - 1) * lda4 + k4];
+  }
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < ap.Kp / 4; i += 256) codes32[i] = 0u;
+  for (int j = tid; j < nsub; j += 256) smax[j] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    float4 mx = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+    for (int r = 0; r < MT; ++r) {
+      mx.x = fmaxf(mx.x, fabsf(v[r][j].x));
+      mx.y = fmaxf(mx.y, fabsf(v[r][j].y));
+      mx.z = fmaxf(mx.z, fabsf(v[r][j].z));
+      mx.w = fmaxf(mx.w, fabsf(v[r][j].w));
+    }
+    atomicMax(&smax[gb[j].x], __float_as_uint(mx.x));
+    atomicMax(&smax[gb[j].y], __float_as_uint(mx.y));
+    atomicMax(&smax[gb[j].z], __float_as_uint(mx.z));
+    atomicMax(&smax[gb[j].w], __float_as_uint(mx.w));
+  }
+  __syncthreads();
+  for (int j = tid; j < nsub; j += 256) {
+    const float sc = group_scale(__uint_as_float(smax[j]), j < ap.nsub[0] ? ap.q[0] : ap.q[1]);
+    stab[j] = sc;
+    rtab[j] = fast_ok(sc) ? __builtin_amdgcn_rcpf(sc) : 0.0f;
+    if (m == 0) s_a[j] = sc;
+  }
+  __syncthreads();
+  const float lo0 = (float)ap.q[0].lo, hi0 = (float)ap.q[0].hi;
+  const float lo1 = (float)ap.q[1].lo, hi1 = (float)ap.q[1].hi;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    if (tid + 256 * j >= K4) break;
+    float4 x = v[0][j];
+#pragma unroll
+    for (int r = 1; r < MT; ++r)
+      if (r == m) x = v[r][j];
+    const float xs[4] = {x.x, x.y, x.z, x.w};
+    const int pp[4] = {p[j].x, p[j].y, p[j].z, p[j].w};
+    const int gg[4] = {gb[j].x, gb[j].y, gb[j].z, gb[j].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float sc = stab[gg[e]], rs = rtab[gg[e]];
+      const bool g1 = gg[e] >= ap.nsub[0];
+      float t = 0.0f;
+      if (sc != 0.0f) {
+        const float ex = xs[e] * rs;
+        t = __builtin_rintf(ex);
+        if (rs == 0.0f || fabsf(fabsf(ex - t) - 0.5f) <= 0x1p-9f) t = __builtin_rintf(__fdiv_rn(xs[e], sc));
+        t = fminf(fmaxf(t, g1 ? lo1 : lo0), g1 ? hi1 : hi0);
+      }
+      codes[pp[e]] = (uint8_t)(int8_t)(int)t;
+    }
+  }
+  __syncthreads();
+  write_act_units(codes, 1, m, ap, packed);
 }
 
 template <int R, int J>
@@ -5127,6 +5319,35 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
   return hipGetLastError();
 }
 
+// The block-sum GEMV (sub-group scales, batches of at most 8 rows): a
+// 4-bit group 0 and an 8-bit group 1, weight containers 2, 4 or 8, and
+// the staged rows plus the block sums within 64 KB of LDS.
+static size_t gemv_g_lds(int64_t M, const ActPlan& ap, const WPlan& wp) {
+  const int64_t MT = M == 1 ? 1 : M == 2 ? 2 : M <= 4 ? 4 : 8;
+  const int nsub = ap.nsub[0] + (ap.S == 2 ? ap.nsub[1] : 0);
+  return (gemv_lds(M, ap, wp) + 15) / 16 * 16 + (size_t)nsub * MT * kBlk * 4;
+}
+
+bool gemv_g_fits(int64_t M, const ActPlan& ap, const WPlan& wp) {
+  return gemv_fits(M, ap, wp) && gemv_nibble_plan(ap) && ap.zp[0] == 0 &&
+         (ap.S == 1 || ap.zp[1] == 0) && wp.c_lo != 1 && wp.c_hi != 1 &&
+         gemv_g_lds(M, ap, wp) + (size_t)2048 * 8 <= 64 * 1024;
+}
+
+hipError_t launch_mp_gemv_grouped(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                  const WDev& wd, const WPlan& wp, int64_t M, int64_t N,
+                                  uint16_t* Y, int64_t ldy, int32_t* acc, hipStream_t stream) {
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  a.xs_bytes = (int)((gemv_lds(M, ap, wp) + 15) / 16 * 16);
+  const dim3 grid((unsigned)wp.nblk);
+  const size_t lds = gemv_g_lds(M, ap, wp);
+  if (M == 1) hipLaunchKernelGGL(k_gemv_g<1>, grid, dim3(256), lds, stream, a);
+  else if (M == 2) hipLaunchKernelGGL(k_gemv_g<2>, grid, dim3(256), lds, stream, a);
+  else if (M <= 4) hipLaunchKernelGGL(k_gemv_g<4>, grid, dim3(256), lds, stream, a);
+  else hipLaunchKernelGGL(k_gemv_g<8>, grid, dim3(256), lds, stream, a);
+  return hipGetLastError();
+}
+
 // Sub-group scales: partial block maxima over row ranges of at least 8
 // rows (at most kGAbsParts of them), block scales, then codes.
 hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_t lda,
@@ -5144,6 +5365,26 @@ hipError_t launch_act_quant_grouped(const float* A, int64_t M, int64_t K, int64_
   }
   const int K4 = (int)(K / 4);
   const int J = (K4 + 255) / 256;
+  if (aligned && J <= 4 && M <= 8 && (size_t)ap.Kp + 3 * tab / 2 <= 64 * 1024) {
+    // decode batches: one launch, every row loaded once per workgroup
+    const size_t lds = (size_t)ap.Kp + (size_t)nsub * 12;
+    const float4* A4 = reinterpret_cast<const float4*>(A);
+    const int4* g4 = reinterpret_cast<const int4*>(grp_dev);
+    const int4* p4 = reinterpret_cast<const int4*>(pos_dev);
+#define SONIQ_GR(J_, MT_)                                                                      \
+  hipLaunchKernelGGL((k_gact_rows<J_, MT_>), dim3((unsigned)M), dim3(256), lds, stream, A4, (int)M, \
+                     K4, lda / 4, p4, g4, ap, nsub, s_a, packed)
+#define SONIQ_GR_J(MT_)                                                                     \
+  if (J == 1) SONIQ_GR(1, MT_); else if (J == 2) SONIQ_GR(2, MT_); else if (J == 3) SONIQ_GR(3, MT_); \
+  else SONIQ_GR(4, MT_)
+    if (M == 1) { SONIQ_GR_J(1); }
+    else if (M == 2) { SONIQ_GR_J(2); }
+    else if (M <= 4) { SONIQ_GR_J(4); }
+    else { SONIQ_GR_J(8); }
+#undef SONIQ_GR_J
+#undef SONIQ_GR
+    return hipGetLastError();
+  }
   if (aligned && J <= 4) {
     // four rows per workgroup at least, else up to kGAbsParts row ranges
     const int64_t rpb = std::max<int64_t>(4, (M + kGAbsParts - 1) / kGAbsParts);

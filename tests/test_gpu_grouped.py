@@ -62,7 +62,7 @@ SHAPES = [  # (M, N, K, a_lo, a_hi, w_lo, w_hi, a_signed, group_bits)
     (64, 256, 768, 4, 8, 2, 8, True, 512),
     (37, 130, 600, 4, 8, 1, 4, True, 512),      # ragged rows, 1-bit weights
     (300, 200, 1000, 3, 5, 2, 4, False, 512),   # unsigned widths below their containers
-    (5, 70, 129, 4, 8, 4, 8, True, 1024),       # a few rows still take the MFMA tiles
+    (5, 70, 129, 4, 8, 4, 8, True, 1024),       # a few rows: the block-sum GEMV
     (129, 300, 2000, 2, 8, 2, 8, True, 512),    # 2-bit activations: 256-channel blocks
     (260, 128, 4096, 4, 8, 2, 4, True, 512),    # 4-row quantizer (16 code rows exceed 64 KB)
     (1, 64, 64, 8, 8, 8, 8, True, 512),         # one block
@@ -95,7 +95,41 @@ def test_grouped_zero_block():
     compare(g, r)
 
 
-@pytest.mark.parametrize("name", ["xfmr_qkv_g512", "xfmr_ffn_down_g512"])
+GEMV_SHAPES = [  # (M, N, K, w_lo, w_hi, group_bits): batches of up to 8 rows
+    (1, 200, 1000, 2, 4, 512),
+    (1, 130, 4100, 2, 8, 512),
+    (1, 96, 2000, 4, 8, 1024),
+    (1, 64, 700, 8, 8, 512),
+    (1, 70, 20000, 2, 4, 512),     # several staging rounds, 157 blocks
+    (2, 150, 1500, 2, 8, 512),
+    (3, 100, 900, 4, 8, 1536),     # blocks of three granules
+    (5, 333, 1200, 2, 4, 512),
+    (8, 128, 3000, 2, 8, 512),
+]
+
+
+@pytest.mark.parametrize("shape", GEMV_SHAPES, ids=lambda s: "x".join(map(str, s[:3])) + f"_w{s[3]}{s[4]}_g{s[5]}")
+def test_grouped_gemv(shape, monkeypatch):
+    """Batches of at most 8 rows take the block-sum GEMV: every per-block
+    accumulator and output against the oracle, and bit for bit against the
+    MFMA tiles on the same handles."""
+    M, N, K, wlo, whi, gb = shape
+    case = workloads.generic(M, N, K, a_lo=4, a_hi=8, a_frac_lo=0.7, w_lo=wlo, w_hi=whi,
+                             w_frac_lo=0.6, a_signed=True, seed=M * 13 + N + K, name="grouped_gemv")
+    rng = np.random.default_rng(K + M)
+    case["A"] = (case["A"] * rng.uniform(0.05, 20.0, K).astype(np.float32)).astype(np.float32)
+    g = gpu_run(case, gb)
+    compare(g, oracle_run(case, gb))
+    monkeypatch.setenv("SONIQ_GROUPED_MFMA", "1")
+    acc = torch.empty_like(torch.from_numpy(g["acc"])).cuda()
+    Y = sq.soniq_mp_gemm(g["act"], g["w"], acc=acc)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_bf16_bits(Y), g["y"])
+    np.testing.assert_array_equal(acc.cpu().numpy(), g["acc"])
+
+
+@pytest.mark.parametrize("name", ["xfmr_qkv_g512", "xfmr_ffn_down_g512", "decode_11008_m1_g512",
+                                  "decode_11008_m8_g512"])
 def test_grouped_workload_parity(name):
     case = workloads.make(name)
     compare(gpu_run(case, case["act_group_bits"]), oracle_run(case, case["act_group_bits"]))

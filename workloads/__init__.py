@@ -204,6 +204,14 @@ def xfmr_ffn_down_g512() -> dict:
     return _grouped(xfmr_ffn_down())
 
 
+def decode_11008_m1_g512() -> dict:
+    return _grouped(decode_11008_m1())
+
+
+def decode_11008_m8_g512() -> dict:
+    return _grouped(decode_11008_m8())
+
+
 BUILDERS = {
     "tiny_linear": tiny_linear,
     "conv3x3_im2col": conv3x3_im2col,
@@ -217,6 +225,8 @@ BUILDERS = {
     "square_8192": square_8192,
     "xfmr_qkv_g512": xfmr_qkv_g512,
     "xfmr_ffn_down_g512": xfmr_ffn_down_g512,
+    "decode_11008_m1_g512": decode_11008_m1_g512,
+    "decode_11008_m8_g512": decode_11008_m8_g512,
 }
 
 
