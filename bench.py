@@ -392,7 +392,7 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
-def run_chain(steps, warmup, group_bits=0):
+def run_chain(steps, warmup, group_bits=0, rows=0):
     """Two transformer linears in a row (FFN up, 4096x3072x768, then FFN
     down, 4096x768x3072), timed two ways, each as `steps` steps captured
     in one HIP graph: the next layer's activations quantized in the first
@@ -401,13 +401,18 @@ def run_chain(steps, warmup, group_bits=0):
     soniq_quantize_act with the batch maximum).  The static scales are
     calibrated once, untimed, from the unfused form's batch maxima.  With
     group_bits > 0 both layers are packed with sub-group activation scales
-    of that many bits (one static scale per block)."""
+    of that many bits (one static scale per block).  rows > 0 takes only
+    the first `rows` rows (a decode batch: the GEMV forms carry the
+    epilogue)."""
     import torch
     import paper_2311_14114_amd as sq
     import workloads
 
     torch.cuda.set_device(0)
     up, down = workloads.xfmr_ffn_up(), workloads.xfmr_ffn_down()
+    if rows > 0:
+        up["A"] = np.ascontiguousarray(up["A"][:rows])
+        up["M"] = down["M"] = rows
     M = up["M"]
     dev = torch.device("cuda")
     A = torch.from_numpy(up["A"]).to(dev)
@@ -462,6 +467,7 @@ def run_chain(steps, warmup, group_bits=0):
     ops = 2 * M * (up["N"] * up["K"] + down["N"] * down["K"])
     print(json.dumps({
         "chain": "xfmr_ffn_up -> xfmr_ffn_down", "M": M, "act_group_bits": group_bits,
+        "launch": "graph",
         "steps": steps, "warmup": warmup,
         "fused_us": t_f * 1e3, "unfused_us": t_u * 1e3, "fused_tops": ops / (t_f * 1e-3) / 1e12,
         "unfused_tops": ops / (t_u * 1e-3) / 1e12, "static_scales": [float(v) for v in s2],
@@ -483,6 +489,8 @@ def main():
     ap.add_argument("--chain", action="store_true",
                     help="time FFN up -> FFN down with the next layer quantized in the first "
                          "GEMM's epilogue, against the unfused form")
+    ap.add_argument("--chain-rows", type=int, default=0,
+                    help="--chain: only the first ROWS activation rows (a decode batch)")
     ap.add_argument("--chain-group-bits", type=int, default=0,
                     help="--chain with sub-group activation scales of this many bits "
                          "(512: the transformer setting) in both layers")
@@ -509,7 +517,7 @@ def main():
         copy_calibration()
         return
     if args.chain:
-        run_chain(args.steps, args.warmup, args.chain_group_bits)
+        run_chain(args.steps, args.warmup, args.chain_group_bits, args.chain_rows)
         return
 
     import workloads

@@ -383,9 +383,11 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * of its next-layer group g, exactly as soniq_quantize_act would with that
  * scale.  On return (stream order) `next` holds M packed rows and its
  * scales are s_next, ready for soniq_mp_gemm(next, next's weights).
- * Every batch size runs the MFMA tiles; weights packed with sub-group
- * scales produce through their per-block tiles (acc_dev then holds their
- * per-block sums, as for soniq_mp_gemm).  The first call with a given
+ * Batches of more than 8 rows run the MFMA tiles, smaller ones the GEMV
+ * forms of soniq_mp_gemm (activation containers 4 and 8) with the same
+ * quantizing epilogue; weights packed with sub-group scales produce through
+ * their per-block kernels (acc_dev then holds their per-block sums, as for
+ * soniq_mp_gemm).  The first call with a given
  * (weights, next) pair allocates next's code image (max_M rows of its
  * padded K, bytes) and a column table, synchronously; later calls with the
  * same pair allocate nothing, so make that first call before capturing the

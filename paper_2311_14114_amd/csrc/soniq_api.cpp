@@ -1137,13 +1137,15 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
       HIP_TRY(dev_alloc(&next->qn_brs, (size_t)w2->scales()));
     // [0, Np): next-layer group of each physical column's channel;
     // [Np, 2 Np): next-layer position of each tile's r-th column in
-    // ascending original order (the order the GEMM stages its outputs in)
+    // ascending original order (the order the GEMM stages its outputs in);
+    // [2 Np, 3 Np): next-layer position of each physical column (the GEMV)
     const int Np = w->wp.Np;
-    std::vector<int32_t> tab(2 * (size_t)Np, -1);
+    std::vector<int32_t> tab(3 * (size_t)Np, -1);
     std::vector<std::vector<int64_t>> cols(Np / kGemmBN);
     for (int64_t n = 0; n < w->N; ++n) {
       const int32_t p = w->phys_h[n];
       tab[p] = w2->act_group_bits ? w2->grp_h[n] : w2->kp.seg[n];  // block, or group
+      tab[2 * (size_t)Np + p] = w2->kp.pos[n];  // [2 Np, 3 Np): position by physical column
       cols[p / kGemmBN].push_back(n);
     }
     for (size_t t = 0; t < cols.size(); ++t) {
@@ -1164,7 +1166,8 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                                acc_dev, next->qn_img, qn_tab, next->ap,
                                w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
-                               next->packed, st, next->ximg));
+                               next->packed, st, next->ximg,
+                               act->ximg_ok ? act->ximg : nullptr));
   next->ximg_ok = M == 1 && next->ximg != nullptr;
   next->M = M;
   return SONIQ_OK;

@@ -236,12 +236,16 @@ hipError_t launch_mp_gemv_grouped(const uint8_t* act_packed, const float* s_a, c
 // A next layer with sub-group scales takes one static scale per block
 // (s_next[nsub], qtab's groups are then blocks), stored with their
 // reciprocals (brs2, nsub floats) by a small launch before the GEMM.
+// Batches of at most 8 rows run the GEMV forms with the same epilogue
+// (qtab then also holds, at [2 Np, 3 Np), the next-layer position of each
+// physical column); ximg2 receives the next layer's row image for one row,
+// ximg is this layer's (or null).
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
                                 const ActPlan& ap2, const float* s_next, float* s_a2,
                                 float* brs2, uint8_t* packed2, hipStream_t stream,
-                                uint8_t* ximg2 = nullptr);
+                                uint8_t* ximg2, const uint8_t* ximg);
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,

@@ -3280,6 +3280,35 @@ __device__ __forceinline__ void gemv_store_x(const GemmArgs& a, int u0,
   }
 }
 
+// One output of a GEMV workgroup: physical column p, batch row m, fp32
+// value v (what the epilogue rounds to bf16).  Y only where it is asked
+// for; with a next layer (qn_img) also its code, by the quantizer of the
+// column's next-layer group (or block, with sub-group scales), written at
+// the column's planned position in the next layer's byte image.
+__device__ __forceinline__ void gemv_store_out(const GemmArgs& a, int p, int64_t m, int n, float v) {
+  if (a.Y) a.Y[m * a.ldy + n] = bf16_rne(v);
+  if (a.qn_img) {
+    const int qg = a.qn_tab[p];
+    const int qpos = a.qn_tab[2 * a.wp.Np + p];
+    QCol qc;
+    if (a.qn_bs) {
+      const bool g1 = qg >= a.qn_nsub0;
+      qc.sc = a.qn_bs[qg];
+      qc.rs = a.qn_brs[qg];
+      qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
+      qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
+      qc.zp = 0;
+      qc.sign1 = false;
+    } else {
+      qc = qnext_col(qg, a.qn);
+    }
+    bool near;
+    int c = qnext_fast(v, qc, near);
+    if (near) c = qnext_exact(v, qc);
+    if (qpos >= 0) a.qn_img[m * a.qn_ld + qpos] = (uint8_t)(int8_t)c;
+  }
+}
+
 // FJ > 0 (batch of one row only): the fused form, which quantizes the fp32
 // row itself (FJ float4 per thread) instead of staging packed units.
 // GB: sub-group activation scales (zero points 0, no 1-bit weights): each
@@ -3643,7 +3672,7 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
         y = __fadd_rn(y, __fmul_rn((float)t, a.s_a[j]));
         if (a.acc) a.acc[((int64_t)j * a.M + em) * a.N + eci.n] = t;
       }
-      a.Y[(int64_t)em * a.ldy + eci.n] = bf16_rne(__fmul_rn(y, eci.s_w));
+      gemv_store_out(a, ep, em, eci.n, __fmul_rn(y, eci.s_w));
     }
     return;
   }
@@ -3682,7 +3711,7 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
                        : true_acc(s0, ap.sh[0], ap.c[0], ap.padcnt[0], ap.zp[0], eshw, eci.colsum[0]);
     const int t1 = S == 2 ? true_acc(s1, ap.sh[1], ap.c[1], ap.padcnt[1], ap.zp[1], eshw, eci.colsum[1])
                           : 0;
-    a.Y[(int64_t)em * a.ldy + eci.n] = bf16_rne(epilogue(t0, t1, S, sa0, sa1, eci.s_w));
+    gemv_store_out(a, ep, em, eci.n, epilogue(t0, t1, S, sa0, sa1, eci.s_w));
     if (a.acc) {
       a.acc[(int64_t)em * a.N + eci.n] = t0;
       if (S == 2) a.acc[(a.M + em) * a.N + eci.n] = t1;
@@ -3835,7 +3864,7 @@ __device__ __forceinline__ void gemv_mfma_block(const GemmArgs& a, int blk, uint
         const int r1 = red[0][1][e][lane] + red[1][1][e][lane] + red[2][1][e][lane] + red[3][1][e][lane];
         const int t0 = (r0 >> sh0) + add0;
         const int t1 = ap.S == 2 ? (r1 >> sh1) + add1 : 0;
-        a.Y[(int64_t)m * a.ldy + ci.n] = bf16_rne(epilogue(t0, t1, ap.S, sa0, sa1, ci.s_w));
+        gemv_store_out(a, pc, m, ci.n, epilogue(t0, t1, ap.S, sa0, sa1, ci.s_w));
         if (a.acc) {
           a.acc[(int64_t)m * a.N + ci.n] = t0;
           if (ap.S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
@@ -5152,6 +5181,20 @@ hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const Act
 // The GEMM with the next layer's quantization in its epilogue (64 x 128
 // tiles at every batch size; k_gemm_g when the producer's activations have
 // sub-group scales), then the packing of that layer's rows.
+static size_t gemv_lds(int64_t M, const ActPlan& ap, const WPlan& wp);
+static size_t gemv_g_lds(int64_t M, const ActPlan& ap, const WPlan& wp);
+static bool gemv_nibble_plan(const ActPlan& ap);
+
+// k_gemv_mfma's dynamic LDS: the largest weight block in whole 64-chunk
+// (1 KB) wave batches; it applies when that and the static reduction
+// buffer (8 KB) fit in 64 KB.
+static size_t gemv_mfma_lds(const WPlan& wp) {
+  return (size_t)(wp.ngt * 8 * wp.c_hi + 63) / 64 * 1024;
+}
+static bool gemv_mfma_fits(const WPlan& wp) {
+  return gemv_mfma_lds(wp) + sizeof(int) * 2048 <= 64 * 1024;
+}
+
 template <int S, int CA0, int CA1, int CBL, int CBH>
 static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
   const int ntn = a.wp.Np / kGemmBN;
@@ -5171,7 +5214,8 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
                                 const ActPlan& ap2, const float* s_next, float* s_a2,
-                                float* brs2, uint8_t* packed2, hipStream_t stream, uint8_t* ximg2) {
+                                float* brs2, uint8_t* packed2, hipStream_t stream, uint8_t* ximg2,
+                                const uint8_t* ximg) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const bool blocks = ap2.gsub[0] > 0;
   if (blocks) {
@@ -5199,8 +5243,31 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
     a.qn.zp[g] = ap2.zp[g];
     a.qn.sign1[g] = ap2.q[g].sign1;
   }
+  // batches of at most 8 rows: the GEMV forms, whose epilogue quantizes
+  // each output the same way
+  const bool gv_g = ap.gsub[0] > 0 && gemv_g_fits(M, ap, wp);
+  const bool gv = ap.gsub[0] == 0 && gemv_nibble_plan(ap) && gemv_fits(M, ap, wp);
   const int cl = wp.c_lo, ch = wp.c_hi;
-  if (ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8) {
+  if (gv || gv_g) {
+    a.xs_bytes = (int)((gemv_lds(M, ap, wp) + 15) / 16 * 16);
+    if (M == 1 && gv) a.ximg = const_cast<uint8_t*>(ximg);
+    const dim3 grid((unsigned)wp.nblk);
+    if (gv_g) {
+      const size_t lds = gemv_g_lds(M, ap, wp);
+      if (M == 1) hipLaunchKernelGGL(k_gemv_g<1>, grid, dim3(256), lds, stream, a);
+      else if (M == 2) hipLaunchKernelGGL(k_gemv_g<2>, grid, dim3(256), lds, stream, a);
+      else if (M <= 4) hipLaunchKernelGGL(k_gemv_g<4>, grid, dim3(256), lds, stream, a);
+      else hipLaunchKernelGGL(k_gemv_g<8>, grid, dim3(256), lds, stream, a);
+    } else if (M >= 2 && gemv_mfma_fits(wp)) {
+      hipLaunchKernelGGL(k_gemv_mfma, grid, dim3(256), gemv_mfma_lds(wp), stream, a);
+    } else {
+      const size_t lds = gemv_lds(M, ap, wp);
+      if (M == 1) hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
+      else if (M == 2) hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), lds, stream, a);
+      else if (M <= 4) hipLaunchKernelGGL(k_gemv<4>, grid, dim3(256), lds, stream, a);
+      else hipLaunchKernelGGL(k_gemv<8>, grid, dim3(256), lds, stream, a);
+    }
+  } else if (ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8) {
     if (cl == 4 && ch == 8) launch_gemm_qn_t<2, 4, 8, 4, 8>(a, M, stream);
     else if (cl == 2 && ch == 8) launch_gemm_qn_t<2, 4, 8, 2, 8>(a, M, stream);
     else if (cl == 1 && ch == 4) launch_gemm_qn_t<2, 4, 8, 1, 4>(a, M, stream);
@@ -5225,8 +5292,6 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
                        ap2, s0, s1, s_out, packed2, M == 1 ? ximg2 : nullptr);
   return hipGetLastError();
 }
-
-static size_t gemv_lds(int64_t M, const ActPlan& ap, const WPlan& wp);
 
 bool gemv_fits(int64_t M, const ActPlan& ap, const WPlan& wp) {
   if (M < 1 || M > 8) return false;
@@ -5301,10 +5366,8 @@ hipError_t launch_mp_gemv(const uint8_t* act_packed, const float* s_a, const Act
   // measurement; results are the same.
   bool mfma = M >= 2;
   if (const char* env = getenv("SONIQ_GEMV_MFMA")) mfma = atoi(env) == 2 || (mfma && atoi(env) != 0);
-  // largest weight block, in whole 64-chunk (1 KB) wave batches
-  const size_t wblock = (size_t)(wp.ngt * 8 * wp.c_hi + 63) / 64 * 1024;
-  if (gemv_nibble_plan(ap) && mfma && wblock + sizeof(int) * 2048 <= 64 * 1024) {
-    hipLaunchKernelGGL(k_gemv_mfma, grid, dim3(256), wblock, stream, a);
+  if (gemv_nibble_plan(ap) && mfma && gemv_mfma_fits(wp)) {
+    hipLaunchKernelGGL(k_gemv_mfma, grid, dim3(256), gemv_mfma_lds(wp), stream, a);
   } else if (gemv_nibble_plan(ap)) {
     if (M == 1) hipLaunchKernelGGL(k_gemv<1>, grid, dim3(256), lds, stream, a);
     else if (M == 2) hipLaunchKernelGGL(k_gemv<2>, grid, dim3(256), lds, stream, a);

@@ -67,6 +67,11 @@ CHAINS = [  # (M, K1, N1, N2, a1, w1, a2, w2, a2_signed)
     (17, 96, 500, 100, (8, 8), (8, 8), (1, 8), (1, 4), True),      # 1-bit next-layer group
     (129, 300, 1000, 64, (4, 8), (2, 8), (2, 8), (2, 8), True),    # 2-bit next-layer group
     (70, 64, 5000, 16, (4, 8), (2, 4), (4, 8), (2, 4), True),      # 4-row packing (16 rows exceed 64 KB)
+    # batches of at most 8 rows: the GEMV forms carry the epilogue
+    (1, 4096, 1000, 300, (4, 8), (2, 4), (4, 8), (2, 4), True),    # decode row, nibble blocks
+    (3, 700, 500, 100, (4, 8), (4, 8), (4, 8), (2, 8), False),     # byte blocks, unsigned next
+    (8, 1000, 640, 96, (4, 8), (2, 8), (1, 8), (1, 4), True),      # 8 rows, 1-bit next group
+    (1, 300, 200, 64, (4, 8), (1, 4), (4, 8), (2, 4), True),       # sign-bit producer weights
 ]
 
 
@@ -78,6 +83,12 @@ def test_chain(c):
 def test_chain_clamps_and_skips_y():
     """Scales below the calibrated ones clamp the largest outputs; no Y."""
     chain(200, 256, 384, 96, (4, 8), (2, 8), (4, 8), (2, 8), True, seed=5, scale_mul=0.5,
+          with_y=False)
+
+
+def test_chain_small_batch_skips_y():
+    """A GEMV producer without Y, with scales below the calibrated ones."""
+    chain(2, 640, 384, 96, (4, 8), (2, 8), (4, 8), (2, 8), True, seed=6, scale_mul=0.5,
           with_y=False)
 
 
@@ -142,6 +153,7 @@ def test_chain_at_benchmark_size():
     (300, 200, 1000, 70, (3, 6), False, 1024),   # unsigned widths below their containers
     (5, 128, 600, 96, (4, 8), True, 512),
     (33, 96, 4000, 40, (2, 8), True, 512),       # 2-bit blocks of 256 channels; 1-row packing
+    (1, 512, 900, 64, (4, 8), True, 512),        # one row through the GEMV into blocks
 ], ids=lambda c: f"M{c[0]}_N{c[2]}_a{c[4][0]}{c[4][1]}_g{c[6]}")
 def test_chain_into_sub_group_scales(c):
     """The next layer packed with sub-group scales: one static scale per
@@ -182,6 +194,7 @@ def test_chain_into_sub_group_scales(c):
     (1, 768, 130, 64, 1024, 0, (2, 8), True),         # one row; 2-bit next-layer group
     (129, 768, 768, 96, 512, 512, (4, 8), True),      # blocks on both sides
     (33, 3072, 1000, 40, 512, 1024, (3, 6), False),   # 25 producer blocks; wide next blocks
+    (6, 1024, 700, 80, 512, 512, (4, 8), True),       # block-sum GEMV producer into blocks
 ], ids=lambda c: f"M{c[0]}_K{c[1]}_N{c[2]}_g{c[4]}_next{c[5]}")
 def test_chain_from_sub_group_scales(c):
     """The producing layer packed with sub-group scales (its per-block
