@@ -73,13 +73,22 @@ def algorithmic(case, info):
 
 def sign_nibbles(case) -> bool:
     """1-bit weight channels are packed in 4-bit containers where the MFMA
-    GEMM runs the layer (cheaper to widen; the GEMV keeps bits)."""
-    return bool((case["w_bits"] == 1).any()) and not uses_gemv(case)
+    GEMM or the block-sum GEMV (which takes containers of 2 bits and up)
+    runs the layer; the plain GEMV keeps bits."""
+    return bool((case["w_bits"] == 1).any()) and (not uses_gemv(case) or
+                                                  bool(case.get("act_group_bits", 0)))
 
 
 def uses_gemv(case) -> bool:
-    # sub-group scales run the MFMA tiles at every batch size
-    return case["M"] <= 8 and not case.get("act_group_bits", 0)
+    # batches of at most 8 rows run a GEMV form (with sub-group scales the
+    # block-sum GEMV)
+    return case["M"] <= 8
+
+
+def gemv_kernel(case) -> str:
+    if case.get("act_group_bits", 0):
+        return "k_gemv_g"
+    return "k_gemv" if case["M"] == 1 else "k_gemv_mfma"
 
 
 def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6f4=False,
@@ -285,7 +294,7 @@ def roofline(case, alg, r, steps):
                     kernel=kernel, algorithmic_bytes=byt, launch_us=t * 1e6)
     t = r["g_ms"] * 1e-3
     byt = alg["a_packed"] + alg["w_packed"] + alg["w_side"] + alg["y"]
-    kernel = ("k_gemv" if uses_gemv(case) else
+    kernel = (gemv_kernel(case) if uses_gemv(case) else
               "k_gemm_g" if case.get("act_group_bits", 0) else "k_gemm")
     traffic = measured_traffic(kernel, case["name"])
     # the bound is whichever resource needs longer at its peak
@@ -310,7 +319,7 @@ def gemv_record(case, r, steps):
     step_s = r["total_ms"] / steps * 1e-3
     g_s = r["g_ms"] * 1e-3
     kbytes = alg["a_packed"] + alg["w_packed"] + alg["w_side"] + alg["y"]
-    kernel = "k_gemv" if case["M"] == 1 else "k_gemv_mfma"
+    kernel = gemv_kernel(case)
     ach = kbytes / g_s / 1e9
     rec = {
         "workload": case["name"], "M": case["M"], "N": case["N"], "K": case["K"],
