@@ -3300,7 +3300,19 @@ __device__ __forceinline__ void gemv_store_out(const GemmArgs& a, int p, int64_t
       qc.zp = 0;
       qc.sign1 = false;
     } else {
-      qc = qnext_col(qg, a.qn);
+      // each field through readfirstlane, so the choice of group is a
+      // select between registers (selecting the fields' addresses instead
+      // made the compiler copy the kernel-argument quantizer to scratch in
+      // every thread)
+      const bool g1 = qg != 0;
+      auto rf = [](float x) { return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x))); };
+      auto ri = [](int x) { return __builtin_amdgcn_readfirstlane(x); };
+      qc.sc = g1 ? rf(a.qn.s[1]) : rf(a.qn.s[0]);
+      qc.rs = g1 ? rf(a.qn.rs[1]) : rf(a.qn.rs[0]);
+      qc.lo = g1 ? rf(a.qn.lo[1]) : rf(a.qn.lo[0]);
+      qc.hi = g1 ? rf(a.qn.hi[1]) : rf(a.qn.hi[0]);
+      qc.zp = g1 ? ri(a.qn.zp[1]) : ri(a.qn.zp[0]);
+      qc.sign1 = (g1 ? ri(a.qn.sign1[1]) : ri(a.qn.sign1[0])) != 0;
     }
     bool near;
     int c = qnext_fast(v, qc, near);
