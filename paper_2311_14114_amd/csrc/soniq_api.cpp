@@ -230,6 +230,7 @@ struct soniq_weights_s {
   int32_t* tile_cols = nullptr;
   uint8_t* colrank = nullptr;
   int32_t* pos = nullptr;
+  uint16_t* pos16 = nullptr;  // the same positions in 16 bits (planned K <= 65536)
   uint8_t* seg = nullptr;
   // sub-group activation scales (0 bits: one scale per precision group)
   uint64_t serial = 0;  // unique per handle (tables built for it are keyed by it)
@@ -308,6 +309,7 @@ void free_weights(soniq_weights w) {
   (void)hipFree(w->tile_cols);
   (void)hipFree(w->colrank);
   (void)hipFree(w->pos);
+  (void)hipFree(w->pos16);
   (void)hipFree(w->seg);
   (void)hipFree(w->grp);
   (void)hipFree(w->posg);
@@ -466,7 +468,7 @@ soniq_status run_quantize_gemm(soniq_act_s& act, const float* A_dev, int64_t M, 
                                uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev, hipStream_t st) {
   const soniq_weights w = act.w;
   if (M == 1 && !w->act_group_bits && gemv_fused_fits(A_dev, w->K, act.ap, w->wp)) {
-    HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos, act.packed, act.s_a, act.ap, w->dev(), w->wp,
+    HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos16, act.packed, act.s_a, act.ap, w->dev(), w->wp,
                               w->N, Y_dev, acc_dev, st, act.ximg));
     act.ximg_ok = act.ximg != nullptr;
     act.M = 1;
@@ -674,7 +676,9 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
   STEP(dev_alloc(&w->tile_cols, (size_t)wp.Np));
   STEP(dev_alloc(&w->colrank, (size_t)wp.Np));
   STEP(dev_alloc(&w->pos, (size_t)K));
+  STEP(dev_alloc(&w->pos16, (size_t)K));
   STEP(dev_alloc(&w->seg, (size_t)K));
+  const std::vector<uint16_t> pos16_h(w->kp.pos.begin(), w->kp.pos.end());
   std::vector<int32_t> grp_h, posg_h;
   if (act_group_bits > 0) {
     // block of channel k: its rank inside its precision group over the
@@ -702,6 +706,7 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
   STEP(hipMemcpyAsync(w->tile_cols, tile_cols_h.data(), wp.Np * sizeof(int32_t), hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->colrank, colrank_h.data(), wp.Np, hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->pos, w->kp.pos.data(), K * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  STEP(hipMemcpyAsync(w->pos16, pos16_h.data(), K * sizeof(uint16_t), hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(w->seg, w->kp.seg.data(), K, hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(wbits_dev, w_bits, N, hipMemcpyHostToDevice, st));
   STEP(hipMemcpyAsync(phys_dev, w->phys_h.data(), N * sizeof(int32_t), hipMemcpyHostToDevice, st));

@@ -189,7 +189,7 @@ hipError_t launch_conv_quant(const float* X, int64_t B, int64_t C, int64_t H, in
 // it applies, its LDS, and the launch (ximg: the handle's row image).
 size_t gemv_fused_lds(const ActPlan& ap, const WPlan& wp);
 bool gemv_fused_fits(const float* A, int64_t K, const ActPlan& ap, const WPlan& wp);
-hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, uint8_t* act_packed,
+hipError_t launch_gemv_fused(const float* A, int64_t K, const uint16_t* pos16_dev, uint8_t* act_packed,
                              float* s_a, const ActPlan& ap, const WDev& wd, const WPlan& wp,
                              int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream,
                              uint8_t* ximg);

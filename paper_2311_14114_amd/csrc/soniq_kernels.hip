@@ -1632,7 +1632,7 @@ struct GemmArgs {
   // positions, where the handle's scales and packed row go, the row's
   // length in float4 and the staging bytes ahead of the code row in LDS
   const float* a32;
-  const int32_t* apos;
+  const uint16_t* apos16;  // planned positions, 16 bits each
   float* s_a_out;
   uint8_t* act_out;
   int K4, xs_bytes;
@@ -3524,7 +3524,8 @@ __device__ __forceinline__ void gemv4_block(const GemmArgs& a, uint8_t* xs, int 
 #pragma unroll
     for (int j = 0; j < FJ; ++j) {
       const int k4 = min(tid + 256 * j, K4 - 1);  // repeats change no max
-      p[j] = reinterpret_cast<const int4*>(a.apos)[k4];
+      const uint2 pq = reinterpret_cast<const uint2*>(a.apos16)[k4];  // half the bytes of int32
+      p[j] = make_int4((int)(pq.x & 0xFFFFu), (int)(pq.x >> 16), (int)(pq.y & 0xFFFFu), (int)(pq.y >> 16));
       v[j] = reinterpret_cast<const float4*>(a.a32)[k4];
     }
     uint4 raw0[NB0], raw1[NB1];
@@ -5099,7 +5100,7 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.acc = acc;
   a.xcd_tiles = 0;
   a.a32 = nullptr;
-  a.apos = nullptr;
+  a.apos16 = nullptr;
   a.s_a_out = nullptr;
   a.act_out = nullptr;
   a.ximg = nullptr;
@@ -5345,14 +5346,14 @@ size_t gemv_fused_lds(const ActPlan& ap, const WPlan& wp) {
   return (gemv_lds(1, ap, wp) + 15) / 16 * 16 + (size_t)ap.Kp;
 }
 
-hipError_t launch_gemv_fused(const float* A, int64_t K, const int32_t* pos_dev, uint8_t* act_packed,
+hipError_t launch_gemv_fused(const float* A, int64_t K, const uint16_t* pos16_dev, uint8_t* act_packed,
                              float* s_a, const ActPlan& ap, const WDev& wd, const WPlan& wp,
                              int64_t N, uint16_t* Y, int32_t* acc, hipStream_t stream,
                              uint8_t* ximg) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, 1, N, Y, N, acc);
   a.ximg = ximg;
   a.a32 = A;
-  a.apos = pos_dev;
+  a.apos16 = pos16_dev;
   a.s_a_out = s_a;
   a.act_out = act_packed;
   a.K4 = (int)(K / 4);
