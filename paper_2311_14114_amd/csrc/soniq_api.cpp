@@ -599,9 +599,17 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
   w->w_cnt[0] = (int64_t)rows_lo.size();
   w->w_cnt[1] = (int64_t)rows_hi.size();
   const int64_t nb_lo = (w->w_cnt[0] + kBlk - 1) / kBlk, nb_hi = (w->w_cnt[1] + kBlk - 1) / kBlk;
-  // with two widths the narrow blocks are padded to whole tiles
-  const int64_t nlo = nw == 2 ? round_up(nb_lo, kGemmBN / kBlk) : nb_lo;
-  const int64_t nblk = round_up(nlo + nb_hi, kGemmBN / kBlk);
+  // With two containers the narrow blocks are padded to whole tiles, so that
+  // a tile holds one container.  Two widths in one container (1-bit channels
+  // in nibbles beside 3- or 4-bit ones, or 5..8 bits) need no such padding:
+  // the columns run on, narrow first, and a block may hold both widths (a
+  // block needs one container; codes and scales are per column).
+  const bool one_container = nw == 2 && wp.c_lo == wp.c_hi && !f8f6f4;
+  const int64_t nb_all = (N + kBlk - 1) / kBlk;
+  const int64_t nlo = one_container ? round_up(nb_all, kGemmBN / kBlk)
+                      : nw == 2    ? round_up(nb_lo, kGemmBN / kBlk)
+                                   : nb_lo;
+  const int64_t nblk = one_container ? nlo : round_up(nlo + nb_hi, kGemmBN / kBlk);
   wp.nblk = (int)nblk;
   wp.nlo = (int)nlo;
   wp.Np = (int)(nblk * kBlk);
@@ -629,10 +637,17 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
       ++b;
     };
     static const std::vector<int32_t> none;
-    while (il < nb_lo) place(rows_lo, il++, wp.c_lo);
-    while (b < nlo) place(none, 0, wp.c_lo);
-    while (ih < nb_hi) place(rows_hi, ih++, wp.c_hi);
-    while (b < nblk) place(none, 0, wp.c_hi);
+    if (one_container) {
+      std::vector<int32_t> rows_all(rows_lo);
+      rows_all.insert(rows_all.end(), rows_hi.begin(), rows_hi.end());
+      while (il < nb_all) place(rows_all, il++, wp.c_lo);
+      while (b < nblk) place(none, 0, wp.c_lo);
+    } else {
+      while (il < nb_lo) place(rows_lo, il++, wp.c_lo);
+      while (b < nlo) place(none, 0, wp.c_lo);
+      while (ih < nb_hi) place(rows_hi, ih++, wp.c_hi);
+      while (b < nblk) place(none, 0, wp.c_hi);
+    }
     w->packed_bytes = (int64_t)off;
     // Kernels derive block offsets from the plan; the table must agree.
     for (int64_t i = 0; i < nblk; ++i)
