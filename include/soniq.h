@@ -388,8 +388,8 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * quantizing epilogue; weights packed with sub-group scales produce through
  * their per-block kernels (acc_dev then holds their per-block sums, as for
  * soniq_mp_gemm).  The first call with a given
- * (weights, next) pair allocates next's code image (max_M rows of its
- * padded K, bytes) and a column table, synchronously; later calls with the
+ * (weights, next) pair allocates next's code image (max_M rounded up to
+ * 256, plus 8, rows of its padded K, bytes) and a column table, synchronously; later calls with the
  * same pair allocate nothing, so make that first call before capturing the
  * call in a HIP graph.  `next` keeps one table per producer weights handle
  * until it is destroyed: a graph captured with one producer stays valid

@@ -266,7 +266,9 @@ struct soniq_act_s {
   unsigned int* counter = nullptr;  // kActStateWords words: the single-pass quantizer's grid state
   float* s_a = nullptr;
   // filled by soniq_mp_gemm_quantize_next from the producing layer: its
-  // outputs' codes as bytes [M_alloc][Kp] (padding positions stay 0), and
+  // outputs' codes as bytes: M_alloc * Kp in 16-row blocks of 16-byte
+  // columns from the GEMM tiles, then 8 * Kp row-major from the GEMV forms
+  // (padding positions stay 0), and
   // the producer's per-physical-column table (position | group << 16)
   uint8_t* qn_img = nullptr;
   float* qn_brs = nullptr;  // reciprocals of static block scales (sub-group weights)
@@ -1144,7 +1146,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     // producer's column table, built synchronously
     if (!next->qn_img) {
       uint8_t* img = nullptr;
-      const size_t bytes = (size_t)(next->M_alloc * w2->kp.Kp);
+      const size_t bytes = (size_t)((next->M_alloc + 8) * w2->kp.Kp);
       HIP_TRY(dev_alloc(&img, bytes));
       const hipError_t e = hipMemset(img, 0, bytes);
       if (e != hipSuccess) {
@@ -1184,7 +1186,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   }
   float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
   HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                               acc_dev, next->qn_img, qn_tab, next->ap,
+                               acc_dev, next->qn_img, next->M_alloc, qn_tab, next->ap,
                                w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
                                next->packed, st, next->ximg,
                                act->ximg_ok ? act->ximg : nullptr));

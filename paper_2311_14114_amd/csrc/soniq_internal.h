@@ -229,7 +229,11 @@ hipError_t launch_mp_gemv_grouped(const uint8_t* act_packed, const float* s_a, c
 
 // The GEMM whose epilogue also quantizes its outputs for the next layer
 // with static scales s_next (host, one per next-layer group): codes go to
-// the byte image img[m*ap2.Kp + position] (qtab: [Np] next-layer group per
+// the byte image img ((img_rows + 8) * ap2.Kp bytes: from the GEMM tiles
+// in 16-row blocks of 16-byte columns, row m and position p at
+// img[(m/16)*16*ap2.Kp + 16*p + m%16]; from the GEMV forms row-major after
+// those img_rows rows, img[(img_rows + m)*ap2.Kp + p]; qtab: [Np] next-layer
+// group per
 // physical column, then [Np] next-layer position per tile column in
 // ascending original order), then k_pack_img writes them as the next
 // handle's packed rows and its scales.  Y may be null.
@@ -242,9 +246,9 @@ hipError_t launch_mp_gemv_grouped(const uint8_t* act_packed, const float* s_a, c
 // ximg is this layer's (or null).
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
-                                int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
-                                const ActPlan& ap2, const float* s_next, float* s_a2,
-                                float* brs2, uint8_t* packed2, hipStream_t stream,
+                                int64_t ldy, int32_t* acc, uint8_t* img, int64_t img_rows,
+                                const int32_t* qtab, const ActPlan& ap2, const float* s_next,
+                                float* s_a2, float* brs2, uint8_t* packed2, hipStream_t stream,
                                 uint8_t* ximg2, const uint8_t* ximg);
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,

@@ -1602,11 +1602,15 @@ __device__ __forceinline__ QCol qnext_col(int g, const QNext& q) {
   return c;
 }
 
+// rs is the correctly rounded reciprocal (0 outside [2^-100, 2^100]), so
+// y * rs lies within 2^-22.4 |y/s| of the exact quotient: kTieBand's
+// argument holds wherever the code is not clamped (|y/s| <= 256), and
+// beyond that both quotients clamp to the same bound.
 __device__ __forceinline__ int qnext_fast(float y, const QCol& c, bool& near) {
   const float e = y * c.rs;
   const float t = __builtin_rintf(e);
   const bool plain = !c.sign1 && c.sc != 0.0f;
-  near = plain && (c.rs == 0.0f || fabsf(fabsf(e - t) - 0.5f) <= 0x1p-9f);
+  near = plain && (c.rs == 0.0f || !(fabsf(fabsf(e - t) - 0.5f) > kTieBand));
   const int code = c.sign1 ? (y < 0.0f ? -1 : 1)
                            : plain ? (int)__builtin_amdgcn_fmed3f(t, c.lo, c.hi) : 0;
   return code - c.zp;
@@ -1640,14 +1644,17 @@ struct GemmArgs {
   // row from the units); the fused form writes it
   uint8_t* ximg;
   // quantization of the outputs for the next layer (k_gemm<..., true>):
-  // the next layer's stored codes as bytes, qn_img[m*qn_ld + position];
+  // the next layer's stored codes as bytes; from the GEMM tiles in 16-row
+  // blocks of 16-byte columns, row m and position p at
+  // qn_img[(m/16)*qn_ld + 16*p + m%16] (qn_ld = 16 * the next plan's Kp),
+  // from the GEMV forms row-major at qn_img[m*qn_ld + p] (qn_ld = Kp);
   // qn_tab[physical column] = the next-layer group of its channel, and
   // qn_tab[Np + 128*tile + r] = the next-layer position of the tile's r-th
   // column in ascending original order (-1 past the last); the quantizer
   // of each next-layer group with its static scale
   uint8_t* qn_img;
   const int32_t* qn_tab;
-  int qn_ld;
+  int64_t qn_ld;
   QNext qn;
   // a next layer with sub-group scales: qn_tab holds each column's block,
   // whose static scale and reciprocal are qn_bs[b], qn_brs[b] (blocks
@@ -2672,6 +2679,31 @@ __device__ __forceinline__ void gemm_group_f(uint8_t* lds, const uint8_t* fa_til
 #endif
 }
 
+
+// Next-layer codes of a tile, staged column-major in LDS: column rank c at
+// c * (BM + 16), its BM rows in order, four rows per 32-bit write.
+template <int BM>
+__device__ __forceinline__ void qn_stage4(uint8_t* qs, int rank, int row0, const int (&c)[4]) {
+  *reinterpret_cast<uint32_t*>(qs + rank * (BM + 16) + row0) =
+      (uint32_t)(c[0] & 0xFF) | ((uint32_t)(c[1] & 0xFF) << 8) | ((uint32_t)(c[2] & 0xFF) << 16) |
+      ((uint32_t)(c[3] & 0xFF) << 24);
+}
+
+// The staged codes to the image: the thread of column rank c writes each
+// 16-row block's 16 codes of its position as one 16-byte store (rows past M
+// land in the image's padding rows, which nothing packs).
+template <int BM>
+__device__ __forceinline__ void qn_store(const GemmArgs& a, const uint8_t* qs, int nt, int64_t m0,
+                                         int tid) {
+  const int c = tid & (kGemmBN - 1);
+  const int qpos = a.qn_tab[a.wp.Np + nt * kGemmBN + c];
+  if (qpos < 0) return;
+  uint8_t* out = a.qn_img + (m0 / kBlk) * a.qn_ld + (int64_t)qpos * 16;
+  for (int ch = tid / kGemmBN; ch < BM / 16; ch += 256 / kGemmBN)
+    *reinterpret_cast<uint4*>(out + ch * a.qn_ld) =
+        *reinterpret_cast<const uint4*>(qs + c * (BM + 16) + ch * 16);
+}
+
 // (32*WFM) x 128 output tile per workgroup of four waves (2 x 2).  QN > 0:
 // the epilogue also quantizes every output for the next layer into qn_img
 // (and stores Y only when a.Y is set), with one static scale per
@@ -2680,7 +2712,7 @@ __device__ __forceinline__ void gemm_group_f(uint8_t* lds, const uint8_t* fa_til
 template <int S, int CA0, int CA1, int CBL, int CBH, int WFM, int NST, int QN = 0, bool F = false,
           bool CV = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
-    QN == 2 ? 3 : QN == 1 ? 1 : WFM == 2 ? 3 : 2)))
+    QN == 2 ? 3 : WFM == 2 ? 3 : 2)))
 void k_gemm(GemmArgs a) {
   constexpr int BM = 32 * WFM;
   // Instances whose containers are all known take at least 24 KB slots at
@@ -2910,6 +2942,12 @@ void k_gemm(GemmArgs a) {
     }
     return;
   }
+  // QN > 0: the same scaling as above, Y staged row-major (when asked
+  // for), and each output's next-layer code staged column-major.
+  uint8_t* qs = reinterpret_cast<uint8_t*>(lds) + BM * YS * 2;
+  static_assert(QN == 0 || BM * YS * 2 + kGemmBN * (BM + 16) <= NST * SLOT,
+                "code staging fits the ring");
+  const bool want_y = a.Y != nullptr;
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const int pc = (jb0 + wn * 4 + jj) * kBlk + (lane & 15);
@@ -2917,87 +2955,88 @@ void k_gemm(GemmArgs a) {
     if (ci.n < 0) continue;
     // Exact accumulator of group g: (raw >> sh_g) + add_g, where add_g folds
     // the zero-point term and the sign x sign padding products (padcnt
-    // products of +1 each, exact multiples of 2^sh_g in the raw sum).
+    // products of +1 each, exact multiples of 2^sh_g in the raw sum); the
+    // scaled form is the one above.
     const uint8_t shw = WFM <= 2 ? cshw[jj] : a.wd.shw[pc];
     const bool sgn = (shw & kShwSign) != 0;
     const int sh0 = ap.sh[0] + (shw & 0x7F);
     const int add0 = ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
     const int sh1 = ap.sh[1] + (shw & 0x7F);
     const int add1 = ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0);
-    uint16_t* ycol = ys + (WFM <= 2 ? crank[jj] : a.wd.colrank[pc]);
+    const float sa0s = __builtin_ldexpf(sa0, -sh0);
+    const float sa1s = S == 2 ? __builtin_ldexpf(sa1, -sh1) : 0.0f;
+    const bool scaled = (sa0s == 0.0f || fabsf(sa0s) >= 0x1p-126f) &&
+                        (S == 1 || sa1s == 0.0f || fabsf(sa1s) >= 0x1p-126f);
+    const int add0s = add0 * (1 << sh0), add1s = S == 2 ? add1 * (1 << sh1) : 0;
+    const int rank = WFM <= 2 ? crank[jj] : a.wd.colrank[pc];
+    uint16_t* ycol = ys + rank;
+    QCol qc;
+    if constexpr (QN == 2) {
+      // sub-group scales: the block's static scale, its group's range
+      const int b = WFM <= 2 ? cqg[jj] : a.qn_tab[pc];
+      const bool g1 = b >= a.qn_nsub0;
+      // (read here, not held through the K loop: registers decide
+      // this kernel's occupancy)
+      qc.sc = a.qn_bs[b];
+      qc.rs = a.qn_brs[b];
+      qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
+      qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
+      qc.zp = 0;
+      qc.sign1 = false;
+    } else {
+      qc = qnext_col(WFM <= 2 ? cqg[jj] : a.qn_tab[pc], a.qn);
+    }
 #pragma unroll
     for (int i = 0; i < WFM; ++i) {
       const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
+      float y[4];
+      if (scaled) [[likely]] {
 #pragma unroll
-      for (int r = 0; r < 4; r += 2) {
-        int t0[2], t1[2];
-        float y[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          t0[h] = (acc0[i][jj][r + h] >> sh0) + add0;
-          t1[h] = S == 2 ? (acc1[i][jj][r + h] >> sh1) + add1 : 0;
-          y[h] = epilogue(t0[h], t1[h], S, sa0, sa1, ci.s_w);
+        for (int h = 0; h < 4; ++h) {
+          float t = __fmul_rn((float)(acc0[i][jj][h] + add0s), sa0s);
+          if (S == 2) t = __fadd_rn(t, __fmul_rn((float)(acc1[i][jj][h] + add1s), sa1s));
+          y[h] = __fmul_rn(t, ci.s_w);
         }
-        // v_cvt_pk_bf16_f32: round to nearest even, as bf16_rne.
-        const __hip_bfloat162 pr = __float22bfloat162_rn(make_float2(y[0], y[1]));
-        ycol[(row0 + r) * YS] = __builtin_bit_cast(uint16_t, pr.x);
-        ycol[(row0 + r + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
-        if (a.acc) {
+      } else {
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int64_t m = m0 + row0 + r + h;
-            if (m < a.M) {
-              a.acc[m * a.N + ci.n] = t0[h];
-              if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1[h];
-            }
-          }
-        }
-        if constexpr (QN > 0) {
-          // the next layer's code of each output, staged like Y
-          QCol qc;
-          if constexpr (QN == 2) {
-            // sub-group scales: the block's static scale, its group's range
-            const int b = WFM <= 2 ? cqg[jj] : a.qn_tab[pc];
-            const bool g1 = b >= a.qn_nsub0;
-            // (read here, not held through the K loop: registers decide
-            // this kernel's occupancy)
-            qc.sc = a.qn_bs[b];
-            qc.rs = a.qn_brs[b];
-            qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
-            qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
-            qc.zp = 0;
-            qc.sign1 = false;
-          } else {
-            qc = qnext_col(WFM <= 2 ? cqg[jj] : a.qn_tab[pc], a.qn);
-          }
-          bool n0, n1;
-          int c0 = qnext_fast(y[0], qc, n0), c1 = qnext_fast(y[1], qc, n1);
-          if (__builtin_amdgcn_ballot_w64(n0 || n1) != 0) [[unlikely]] {
-            if (n0) c0 = qnext_exact(y[0], qc);
-            if (n1) c1 = qnext_exact(y[1], qc);
-          }
-          uint8_t* qcol = reinterpret_cast<uint8_t*>(lds) + BM * YS * 2 + (WFM <= 2 ? crank[jj] : a.wd.colrank[pc]);
-          qcol[(row0 + r) * YS] = (uint8_t)(int8_t)c0;
-          qcol[(row0 + r + 1) * YS] = (uint8_t)(int8_t)c1;
+        for (int h = 0; h < 4; ++h)
+          y[h] = epilogue((acc0[i][jj][h] >> sh0) + add0,
+                          S == 2 ? (acc1[i][jj][h] >> sh1) + add1 : 0, S, sa0, sa1, ci.s_w);
+      }
+      if (want_y) {
+#pragma unroll
+        for (int h = 0; h < 4; h += 2) {
+          // v_cvt_pk_bf16_f32: round to nearest even, as bf16_rne.
+          const __hip_bfloat162 pr = __float22bfloat162_rn(make_float2(y[h], y[h + 1]));
+          ycol[(row0 + h) * YS] = __builtin_bit_cast(uint16_t, pr.x);
+          ycol[(row0 + h + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
         }
       }
+      if (a.acc) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const int64_t m = m0 + row0 + h;
+          if (m < a.M) {
+            a.acc[m * a.N + ci.n] = (acc0[i][jj][h] >> sh0) + add0;
+            if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = (acc1[i][jj][h] >> sh1) + add1;
+          }
+        }
+      }
+      int c[4];
+      bool nr[4];
+#pragma unroll
+      for (int h = 0; h < 4; ++h) c[h] = qnext_fast(y[h], qc, nr[h]);
+      if (__builtin_amdgcn_ballot_w64(nr[0] || nr[1] || nr[2] || nr[3]) != 0) [[unlikely]] {
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+          if (nr[h]) c[h] = qnext_exact(y[h], qc);
+      }
+      qn_stage4<BM>(qs, rank, row0, c);
     }
   }
   __syncthreads();
-  if constexpr (QN > 0) {
-    // rows of codes, each thread one column of the tile in ascending
-    // original order: consecutive lanes write nearby planned positions
-    static_assert(BM * YS * 3 <= NST * SLOT, "code staging fits the ring");
-    const int qpos = a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))];
-    if (qpos >= 0) {
-      const uint8_t* qs = reinterpret_cast<const uint8_t*>(lds) + BM * YS * 2;
-      const int mrem = (int)min((int64_t)BM, a.M - m0);
-      uint8_t* qout = a.qn_img + m0 * a.qn_ld + qpos;
-      for (int row = tid / kGemmBN; row < mrem; row += 256 / kGemmBN)
-        qout[(int64_t)row * a.qn_ld] = qs[row * YS + (tid & (kGemmBN - 1))];
-    }
-    if (!a.Y) return;
-  }
+  qn_store<BM>(a, qs, nt, m0, tid);
+  if (!want_y) return;
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
     const int mrem = (int)min((int64_t)BM, a.M - m0);
@@ -4007,23 +4046,61 @@ __global__ __launch_bounds__(256) void k_set_scales(BlockScales b, float* __rest
 }
 
 // ------------------------------------------------------------ k_pack_img --
-// The next layer's packed rows from the byte image the GEMM's epilogue
-// wrote (stored codes at planned positions; padding positions stay 0):
-// R rows per workgroup go to LDS and out as units, whole 16-byte pieces
-// for a full 16-row block without 1-bit groups.  Workgroup 0 also stores
-// the static scales.  Dynamic LDS: R*Kp bytes.
+// The next layer's packed rows from the byte image the producer's epilogue
+// wrote (stored codes; padding positions stay 0): in 16-row blocks of
+// 16-byte columns (row m, position p at img[(m/16)*ld + 16*p + m%16]) when
+// `blocked` (the GEMM tiles), else row-major (img[m*ld + p], the GEMV
+// forms).  R rows per workgroup go to LDS as rows of planned positions and
+// out as units, whole 16-byte pieces for a full 16-row block without 1-bit
+// groups.  Workgroup 0 also stores the static scales.  Dynamic LDS: R*Kp
+// bytes.
 template <int R>
-__global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ img, int64_t M,
-                                                  ActPlan ap, float s0, float s1,
+__global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ img, int64_t ld,
+                                                  bool blocked, int64_t M, ActPlan ap, float s0,
+                                                  float s1,
                                                   float* __restrict__ s_a,
                                                   uint8_t* __restrict__ packed,
                                                   uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
   const int64_t m0 = (int64_t)blockIdx.x * R;
   const int rows = (int)min((int64_t)R, M - m0);
-  const int n16 = rows * ap.Kp / 16;
-  const uint4* src = reinterpret_cast<const uint4*>(img + m0 * ap.Kp);
-  for (int i = threadIdx.x; i < n16; i += 256) reinterpret_cast<uint4*>(codes)[i] = src[i];
+  if (!blocked) {
+    for (int r = 0; r < rows; ++r) {
+      const uint4* src = reinterpret_cast<const uint4*>(img + (m0 + r) * ld);
+      for (int i = threadIdx.x; i < ap.Kp / 16; i += 256)
+        reinterpret_cast<uint4*>(codes + r * ap.Kp)[i] = src[i];
+    }
+  } else if (R == kBlk && rows == kBlk) {
+    // thread: four positions, 16 rows each (16-byte loads), turned into
+    // four-position words of each row
+    const int K4 = ap.Kp / 4;
+    const uint4* blk = reinterpret_cast<const uint4*>(img + (m0 / kBlk) * ld);
+    for (int p4 = threadIdx.x; p4 < K4; p4 += 256) {
+      uint4 v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = blk[4 * p4 + j];
+      const uint32_t w[4][4] = {{v[0].x, v[0].y, v[0].z, v[0].w}, {v[1].x, v[1].y, v[1].z, v[1].w},
+                                {v[2].x, v[2].y, v[2].z, v[2].w}, {v[3].x, v[3].y, v[3].z, v[3].w}};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // rows 4q .. 4q+3: bytes of positions 0,1 (x01) and 2,3 (x23)
+        const uint32_t x01lo = __builtin_amdgcn_perm(w[1][q], w[0][q], 0x05010400u);
+        const uint32_t x01hi = __builtin_amdgcn_perm(w[1][q], w[0][q], 0x07030602u);
+        const uint32_t x23lo = __builtin_amdgcn_perm(w[3][q], w[2][q], 0x05010400u);
+        const uint32_t x23hi = __builtin_amdgcn_perm(w[3][q], w[2][q], 0x07030602u);
+        uint32_t* c32 = reinterpret_cast<uint32_t*>(codes) + p4;
+        c32[(4 * q + 0) * K4] = __builtin_amdgcn_perm(x23lo, x01lo, 0x05040100u);
+        c32[(4 * q + 1) * K4] = __builtin_amdgcn_perm(x23lo, x01lo, 0x07060302u);
+        c32[(4 * q + 2) * K4] = __builtin_amdgcn_perm(x23hi, x01hi, 0x05040100u);
+        c32[(4 * q + 3) * K4] = __builtin_amdgcn_perm(x23hi, x01hi, 0x07060302u);
+      }
+    }
+  } else {
+    // the last block of a batch, or one row: only its rows' bytes
+    const uint8_t* blk = img + (m0 / kBlk) * ld + m0 % kBlk;
+    for (int r = 0; r < rows; ++r)
+      for (int p = threadIdx.x; p < ap.Kp; p += 256) codes[r * ap.Kp + p] = blk[16 * p + r];
+  }
   if (s_a && blockIdx.x == 0 && threadIdx.x == 0) {
     s_a[0] = s0;
     s_a[1] = s1;
@@ -4497,6 +4574,11 @@ void k_gemm_g(GemmArgs a) {
   constexpr int YS = kGemmBN + 8;
   uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
   static_assert(BM * YS * 2 <= NST * SLOT, "output staging fits the ring");
+  // QN > 0: each output's next-layer code, staged column-major as in k_gemm
+  uint8_t* qs = reinterpret_cast<uint8_t*>(lds) + BM * YS * 2;
+  static_assert(QN == 0 || BM * YS * 2 + kGemmBN * (BM + 16) <= NST * SLOT,
+                "code staging fits the ring");
+  const bool want_y = QN == 0 || a.Y != nullptr;
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     const ColInfo ci = cinf[jj];
@@ -4505,53 +4587,48 @@ void k_gemm_g(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < WFM; ++i) {
       const int row0 = (wm * WFM + i) * 16 + (lane >> 4) * 4;
+      float y[4];
 #pragma unroll
-      for (int r = 0; r < 4; r += 2) {
-        const float y0 = __fmul_rn(yf[i][jj][r], ci.s_w), y1 = __fmul_rn(yf[i][jj][r + 1], ci.s_w);
-        const __hip_bfloat162 pr = __float22bfloat162_rn(make_float2(y0, y1));
-        ycol[(row0 + r) * YS] = __builtin_bit_cast(uint16_t, pr.x);
-        ycol[(row0 + r + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
-        if constexpr (QN > 0) {
-          // the next layer's code of each output, staged like Y
-          QCol qc;
-          if constexpr (QN == 2) {
-            const int b = cqg[jj];
-            const bool g1 = b >= a.qn_nsub0;
-            qc.sc = a.qn_bs[b];
-            qc.rs = a.qn_brs[b];
-            qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
-            qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
-            qc.zp = 0;
-            qc.sign1 = false;
-          } else {
-            qc = qnext_col(cqg[jj], a.qn);
-          }
-          bool n0, n1;
-          int c0 = qnext_fast(y0, qc, n0), c1 = qnext_fast(y1, qc, n1);
-          if (__builtin_amdgcn_ballot_w64(n0 || n1) != 0) [[unlikely]] {
-            if (n0) c0 = qnext_exact(y0, qc);
-            if (n1) c1 = qnext_exact(y1, qc);
-          }
-          uint8_t* qcol = reinterpret_cast<uint8_t*>(lds) + BM * YS * 2 + crank[jj];
-          qcol[(row0 + r) * YS] = (uint8_t)(int8_t)c0;
-          qcol[(row0 + r + 1) * YS] = (uint8_t)(int8_t)c1;
+      for (int h = 0; h < 4; ++h) y[h] = __fmul_rn(yf[i][jj][h], ci.s_w);
+      if (want_y) {
+#pragma unroll
+        for (int h = 0; h < 4; h += 2) {
+          const __hip_bfloat162 pr = __float22bfloat162_rn(make_float2(y[h], y[h + 1]));
+          ycol[(row0 + h) * YS] = __builtin_bit_cast(uint16_t, pr.x);
+          ycol[(row0 + h + 1) * YS] = __builtin_bit_cast(uint16_t, pr.y);
         }
+      }
+      if constexpr (QN > 0) {
+        QCol qc;
+        if constexpr (QN == 2) {
+          const int b = cqg[jj];
+          const bool g1 = b >= a.qn_nsub0;
+          qc.sc = a.qn_bs[b];
+          qc.rs = a.qn_brs[b];
+          qc.lo = g1 ? a.qn.lo[1] : a.qn.lo[0];
+          qc.hi = g1 ? a.qn.hi[1] : a.qn.hi[0];
+          qc.zp = 0;
+          qc.sign1 = false;
+        } else {
+          qc = qnext_col(cqg[jj], a.qn);
+        }
+        int c[4];
+        bool nr[4];
+#pragma unroll
+        for (int h = 0; h < 4; ++h) c[h] = qnext_fast(y[h], qc, nr[h]);
+        if (__builtin_amdgcn_ballot_w64(nr[0] || nr[1] || nr[2] || nr[3]) != 0) [[unlikely]] {
+#pragma unroll
+          for (int h = 0; h < 4; ++h)
+            if (nr[h]) c[h] = qnext_exact(y[h], qc);
+        }
+        qn_stage4<BM>(qs, crank[jj], row0, c);
       }
     }
   }
   __syncthreads();
   if constexpr (QN > 0) {
-    // rows of codes in ascending original column order, as in k_gemm
-    static_assert(BM * YS * 3 <= NST * SLOT, "code staging fits the ring");
-    const int qpos = a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))];
-    if (qpos >= 0) {
-      const uint8_t* qs = reinterpret_cast<const uint8_t*>(lds) + BM * YS * 2;
-      const int mrem = (int)min((int64_t)BM, a.M - m0);
-      uint8_t* qout = a.qn_img + m0 * a.qn_ld + qpos;
-      for (int row = tid / kGemmBN; row < mrem; row += 256 / kGemmBN)
-        qout[(int64_t)row * a.qn_ld] = qs[row * YS + (tid & (kGemmBN - 1))];
-    }
-    if (!a.Y) return;
+    qn_store<BM>(a, qs, nt, m0, tid);
+    if (!want_y) return;
   }
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
@@ -5225,10 +5302,10 @@ static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
 
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
-                                int64_t ldy, int32_t* acc, uint8_t* img, const int32_t* qtab,
-                                const ActPlan& ap2, const float* s_next, float* s_a2,
-                                float* brs2, uint8_t* packed2, hipStream_t stream, uint8_t* ximg2,
-                                const uint8_t* ximg) {
+                                int64_t ldy, int32_t* acc, uint8_t* img, int64_t img_rows,
+                                const int32_t* qtab, const ActPlan& ap2, const float* s_next,
+                                float* s_a2, float* brs2, uint8_t* packed2, hipStream_t stream,
+                                uint8_t* ximg2, const uint8_t* ximg) {
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const bool blocks = ap2.gsub[0] > 0;
   if (blocks) {
@@ -5244,7 +5321,7 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   a.xcd_tiles = tiles <= 2048;
   a.qn_img = img;
   a.qn_tab = qtab;
-  a.qn_ld = ap2.Kp;
+  a.qn_ld = 0;  // set below with the producer's form
   for (int g = 0; g < 2; ++g) {
     const float sc = !blocks && g < ap2.S ? s_next[g] : 0.0f;
     a.qn.s[g] = sc;
@@ -5260,8 +5337,16 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   // each output the same way
   const bool gv_g = ap.gsub[0] > 0 && gemv_g_fits(M, ap, wp);
   const bool gv = ap.gsub[0] == 0 && gemv_nibble_plan(ap) && gemv_fits(M, ap, wp);
+  // The two forms keep separate images, so that neither writes a position
+  // that is padding in the other's layout (padding bytes stay 0).
+  const bool gemv_form = gv || gv_g;
+  a.qn_ld = gemv_form ? (int64_t)ap2.Kp : 16 * (int64_t)ap2.Kp;
+  if (gemv_form) {
+    img += img_rows * ap2.Kp;
+    a.qn_img = img;
+  }
   const int cl = wp.c_lo, ch = wp.c_hi;
-  if (gv || gv_g) {
+  if (gemv_form) {
     a.xs_bytes = (int)((gemv_lds(M, ap, wp) + 15) / 16 * 16);
     if (M == 1 && gv) a.ximg = const_cast<uint8_t*>(ximg);
     const dim3 grid((unsigned)wp.nblk);
@@ -5298,11 +5383,11 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   float* s_out = blocks ? nullptr : s_a2;  // block scales were stored above
   if (kBlk * (size_t)ap2.Kp <= 64 * 1024)
     hipLaunchKernelGGL(k_pack_img<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
-                       kBlk * (size_t)ap2.Kp, stream, img, M, ap2, s0, s1, s_out, packed2,
+                       kBlk * (size_t)ap2.Kp, stream, img, a.qn_ld, !gemv_form, M, ap2, s0, s1, s_out, packed2,
                        M == 1 ? ximg2 : nullptr);
   else
-    hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)M), dim3(256), (size_t)ap2.Kp, stream, img, M,
-                       ap2, s0, s1, s_out, packed2, M == 1 ? ximg2 : nullptr);
+    hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)M), dim3(256), (size_t)ap2.Kp, stream, img,
+                       a.qn_ld, !gemv_form, M, ap2, s0, s1, s_out, packed2, M == 1 ? ximg2 : nullptr);
   return hipGetLastError();
 }
 

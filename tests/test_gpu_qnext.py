@@ -118,6 +118,45 @@ def test_chain_repeat_and_other_producer():
     np.testing.assert_array_equal(g_q, qb)
 
 
+def test_chain_tiles_and_gemv_forms_share_next():
+    """One (producer, next) pair fed by the GEMM tiles (more than 8 rows) and
+    by the GEMV forms (8 or fewer) in turn: the two write their codes in
+    different layouts, and neither may leave a code where the other's
+    layout keeps padding.  The next layer has a sign group, 1-bit weights
+    and padded groups (K = 100), so a stray padding code would change its
+    accumulators."""
+    Mmax, K1, N1, N2 = 64, 192, 100, 48
+    l1 = workloads.generic(Mmax, N1, K1, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.7, a_signed=True, seed=71, name="share1")
+    l2 = workloads.generic(Mmax, N2, N1, a_lo=1, a_hi=8, a_frac_lo=0.7, w_lo=1, w_hi=4,
+                           w_frac_lo=0.5, a_signed=True, seed=72, name="share2")
+    r_all = oracle.run(l1["A"], l1["W"], l1["a_bits"], l1["w_bits"], True)
+    y_all = oracle.epilogue_replay_f32(r_all["acc"], r_all["s_a"], r_all["s_w"])
+    _, s2, _, _ = oracle.quantize_act(y_all, l2["a_bits"], True)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    S2, _, seg_of2 = oracle.segments(l2["a_bits"])
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], True)
+    act1 = sq.soniq_act_create(wh1, Mmax)
+    act2 = sq.soniq_act_create(wh2, Mmax)
+    for M in (64, 5, 40, 1, 64):
+        print(f"[gpu] shared next handle, M={M}", flush=True)
+        A = np.ascontiguousarray(l1["A"][:M])
+        r1 = oracle.run(A, l1["W"], l1["a_bits"], l1["w_bits"], True)
+        y1 = oracle.epilogue_replay_f32(r1["acc"], r1["s_a"], r1["s_w"])
+        q2 = oracle.quantize_act_static(y1, l2["a_bits"], True, s2)
+        acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+        sq.soniq_quantize_act(act1, torch.from_numpy(A).cuda())
+        sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, s2)
+        acc = torch.empty((S2, M, N2), dtype=torch.int32, device="cuda")
+        Y2 = sq.soniq_mp_gemm(act2, wh2, acc=acc)
+        torch.cuda.synchronize()
+        g_q, _ = sq.soniq_act_unpack_debug(act2)
+        np.testing.assert_array_equal(g_q, q2)
+        np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+        np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
+
+
 def test_chain_at_benchmark_size():
     """The two transformer linears bench.py --chain times (FFN up 4096 x 3072
     x 768, then FFN down 4096 x 768 x 3072), in its launch configuration:
