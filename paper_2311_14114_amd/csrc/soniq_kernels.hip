@@ -1621,6 +1621,37 @@ __device__ __forceinline__ int qnext_exact(float y, const QCol& c) {
   return (int)__builtin_amdgcn_fmed3f(t, c.lo, c.hi) - c.zp;
 }
 
+// Stored codes of four outputs of one column as the bytes of a word (byte
+// h: output h), by the shifted form of the quantizer (as qshift): y*rs +
+// (kShift - zp) rounds to kShift + rint(y*rs) - zp, clamped between
+// kShift + the stored-code bounds, whose low byte is the stored code.
+// Outputs within the tie band (or all, for a scale outside the shortcut's
+// range) take the exact division; the branch is taken by the wave.
+__device__ __forceinline__ uint32_t qnext4(const float (&y)[4], const QCol& c) {
+  const bool plain = !c.sign1 && c.sc != 0.0f;
+  const float zf = (float)c.zp;
+  const float mz = kShift - zf, lb = kShift + (c.lo - zf), hb = kShift + (c.hi - zf);
+  uint32_t b[4];
+  bool nr[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const float e = y[h] * c.rs;
+    const float t = e + mz;
+    nr[h] = plain && (c.rs == 0.0f || !(fabsf(e - (t - mz)) < 0.5f - kTieBand));
+    b[h] = __float_as_uint(__builtin_amdgcn_fmed3f(t, lb, hb));
+    if (c.sign1) b[h] = (uint32_t)((y[h] < 0.0f ? -1 : 1) - c.zp);
+  }
+  uint32_t w = __builtin_amdgcn_perm(b[1], b[0], 0x0C0C0400u) |
+               __builtin_amdgcn_perm(b[3], b[2], 0x04000C0Cu);
+  if (__builtin_amdgcn_ballot_w64(nr[0] || nr[1] || nr[2] || nr[3]) != 0) [[unlikely]] {
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      if (nr[h])
+        w = (w & ~(0xFFu << (8 * h))) | (((uint32_t)qnext_exact(y[h], c) & 0xFFu) << (8 * h));
+  }
+  return w;
+}
+
 struct GemmArgs {
   const uint8_t* act;
   const float* s_a;
@@ -2681,12 +2712,10 @@ __device__ __forceinline__ void gemm_group_f(uint8_t* lds, const uint8_t* fa_til
 
 
 // Next-layer codes of a tile, staged column-major in LDS: column rank c at
-// c * (BM + 16), its BM rows in order, four rows per 32-bit write.
+// c * (BM + 16), its BM rows in order, four rows (a qnext4 word) per write.
 template <int BM>
-__device__ __forceinline__ void qn_stage4(uint8_t* qs, int rank, int row0, const int (&c)[4]) {
-  *reinterpret_cast<uint32_t*>(qs + rank * (BM + 16) + row0) =
-      (uint32_t)(c[0] & 0xFF) | ((uint32_t)(c[1] & 0xFF) << 8) | ((uint32_t)(c[2] & 0xFF) << 16) |
-      ((uint32_t)(c[3] & 0xFF) << 24);
+__device__ __forceinline__ void qn_stage4(uint8_t* qs, int rank, int row0, uint32_t w) {
+  *reinterpret_cast<uint32_t*>(qs + rank * (BM + 16) + row0) = w;
 }
 
 // The staged codes to the image: the thread of column rank c writes each
@@ -3022,16 +3051,7 @@ void k_gemm(GemmArgs a) {
           }
         }
       }
-      int c[4];
-      bool nr[4];
-#pragma unroll
-      for (int h = 0; h < 4; ++h) c[h] = qnext_fast(y[h], qc, nr[h]);
-      if (__builtin_amdgcn_ballot_w64(nr[0] || nr[1] || nr[2] || nr[3]) != 0) [[unlikely]] {
-#pragma unroll
-        for (int h = 0; h < 4; ++h)
-          if (nr[h]) c[h] = qnext_exact(y[h], qc);
-      }
-      qn_stage4<BM>(qs, rank, row0, c);
+      qn_stage4<BM>(qs, rank, row0, qnext4(y, qc));
     }
   }
   __syncthreads();
@@ -4048,21 +4068,85 @@ __global__ __launch_bounds__(256) void k_set_scales(BlockScales b, float* __rest
 // ------------------------------------------------------------ k_pack_img --
 // The next layer's packed rows from the byte image the producer's epilogue
 // wrote (stored codes; padding positions stay 0): in 16-row blocks of
-// 16-byte columns (row m, position p at img[(m/16)*ld + 16*p + m%16]) when
-// `blocked` (the GEMM tiles), else row-major (img[m*ld + p], the GEMV
-// forms).  R rows per workgroup go to LDS as rows of planned positions and
-// out as units, whole 16-byte pieces for a full 16-row block without 1-bit
-// groups.  Workgroup 0 also stores the static scales.  Dynamic LDS: R*Kp
-// bytes.
+// 16-byte columns (row m, position p at img[(m/16)*ld + 16*p + m%16]) from
+// the GEMM tiles, row-major (img[m*ld + p]) from the GEMV forms.
+
+// Positions [p0, p0 + 4*n4) of a 16-row block of the blocked image into LDS
+// as rows of pitch 4*n4: thread = four positions, 16 rows each (16-byte
+// loads), turned into four-position words of each row by byte permutes.
+__device__ __forceinline__ void img_block_rows(const uint8_t* __restrict__ blk, int p0, int n4,
+                                               uint8_t* codes) {
+  const uint4* src = reinterpret_cast<const uint4*>(blk) + p0;
+  for (int p4 = threadIdx.x; p4 < n4; p4 += 256) {
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = src[4 * p4 + j];
+    const uint32_t w[4][4] = {{v[0].x, v[0].y, v[0].z, v[0].w}, {v[1].x, v[1].y, v[1].z, v[1].w},
+                              {v[2].x, v[2].y, v[2].z, v[2].w}, {v[3].x, v[3].y, v[3].z, v[3].w}};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      // rows 4q .. 4q+3: bytes of positions 0,1 (x01) and 2,3 (x23)
+      const uint32_t x01lo = __builtin_amdgcn_perm(w[1][q], w[0][q], 0x05010400u);
+      const uint32_t x01hi = __builtin_amdgcn_perm(w[1][q], w[0][q], 0x07030602u);
+      const uint32_t x23lo = __builtin_amdgcn_perm(w[3][q], w[2][q], 0x05010400u);
+      const uint32_t x23hi = __builtin_amdgcn_perm(w[3][q], w[2][q], 0x07030602u);
+      uint32_t* c32 = reinterpret_cast<uint32_t*>(codes) + p4;
+      c32[(4 * q + 0) * n4] = __builtin_amdgcn_perm(x23lo, x01lo, 0x05040100u);
+      c32[(4 * q + 1) * n4] = __builtin_amdgcn_perm(x23lo, x01lo, 0x07060302u);
+      c32[(4 * q + 2) * n4] = __builtin_amdgcn_perm(x23hi, x01hi, 0x05040100u);
+      c32[(4 * q + 3) * n4] = __builtin_amdgcn_perm(x23hi, x01hi, 0x07060302u);
+    }
+  }
+}
+
+// Full 16-row blocks of the blocked image, no 1-bit group: workgroup
+// (b, j) packs granules [j*ngr/P, (j+1)*ngr/P) of block b (P = gridDim.y),
+// so a batch's blocks spread over about a thousand workgroups.  Workgroup
+// (0, 0) also stores the static scales.  Dynamic LDS: 16 * 64 *
+// ceil(ngr/P) bytes.
+__global__ __launch_bounds__(256) void k_pack_img_split(const uint8_t* __restrict__ img, int64_t ld,
+                                                        ActPlan ap, float s0, float s1,
+                                                        float* __restrict__ s_a,
+                                                        uint8_t* __restrict__ packed) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  const int64_t b = blockIdx.x;
+  const int ngr = ap.Kp / kGran;
+  const int q0 = (int)((int64_t)blockIdx.y * ngr / gridDim.y);
+  const int q1 = (int)((int64_t)(blockIdx.y + 1) * ngr / gridDim.y);
+  if (s_a && b == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    s_a[0] = s0;
+    s_a[1] = s1;
+  }
+  if (q1 <= q0) return;
+  const int W = (q1 - q0) * kGran;
+  img_block_rows(img + b * ld, q0 * kGran, W / 4, codes);
+  __syncthreads();
+  for (int gi = 0; gi < ap.S; ++gi) {
+    const int c = gi ? ap.c[1] : ap.c[0];
+    const int gs = gi ? ap.ng[0] : 0;  // the group's first granule
+    const int g0 = max(q0, gs), g1 = min(q1, gs + (gi ? ap.ng[1] : ap.ng[0]));
+    if (g1 <= g0) continue;
+    uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
+                   b * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]) + (int64_t)(g0 - gs) * 128 * c;
+    const int lb = (g0 - q0) * kGran;
+    if (c == 8) write_block_pieces<8, kBlk>(codes, W, lb, g1 - g0, 0, dst);
+    else if (c == 4) write_block_pieces<4, kBlk>(codes, W, lb, g1 - g0, 0, dst);
+    else write_block_pieces<2, kBlk>(codes, W, lb, g1 - g0, 0, dst);
+  }
+}
+
+// Every other case (the GEMV forms' row-major image, a 1-bit group, the
+// last block of a batch): R rows per workgroup from block row blk0*R on go
+// to LDS as rows of planned positions and out as units.  Workgroup 0 also
+// stores the static scales (when s_a is set).  Dynamic LDS: R*Kp bytes.
 template <int R>
 __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ img, int64_t ld,
-                                                  bool blocked, int64_t M, ActPlan ap, float s0,
-                                                  float s1,
-                                                  float* __restrict__ s_a,
+                                                  bool blocked, int64_t blk0, int64_t M, ActPlan ap,
+                                                  float s0, float s1, float* __restrict__ s_a,
                                                   uint8_t* __restrict__ packed,
                                                   uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
-  const int64_t m0 = (int64_t)blockIdx.x * R;
+  const int64_t m0 = (blk0 + blockIdx.x) * R;
   const int rows = (int)min((int64_t)R, M - m0);
   if (!blocked) {
     for (int r = 0; r < rows; ++r) {
@@ -4071,30 +4155,7 @@ __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ im
         reinterpret_cast<uint4*>(codes + r * ap.Kp)[i] = src[i];
     }
   } else if (R == kBlk && rows == kBlk) {
-    // thread: four positions, 16 rows each (16-byte loads), turned into
-    // four-position words of each row
-    const int K4 = ap.Kp / 4;
-    const uint4* blk = reinterpret_cast<const uint4*>(img + (m0 / kBlk) * ld);
-    for (int p4 = threadIdx.x; p4 < K4; p4 += 256) {
-      uint4 v[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = blk[4 * p4 + j];
-      const uint32_t w[4][4] = {{v[0].x, v[0].y, v[0].z, v[0].w}, {v[1].x, v[1].y, v[1].z, v[1].w},
-                                {v[2].x, v[2].y, v[2].z, v[2].w}, {v[3].x, v[3].y, v[3].z, v[3].w}};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        // rows 4q .. 4q+3: bytes of positions 0,1 (x01) and 2,3 (x23)
-        const uint32_t x01lo = __builtin_amdgcn_perm(w[1][q], w[0][q], 0x05010400u);
-        const uint32_t x01hi = __builtin_amdgcn_perm(w[1][q], w[0][q], 0x07030602u);
-        const uint32_t x23lo = __builtin_amdgcn_perm(w[3][q], w[2][q], 0x05010400u);
-        const uint32_t x23hi = __builtin_amdgcn_perm(w[3][q], w[2][q], 0x07030602u);
-        uint32_t* c32 = reinterpret_cast<uint32_t*>(codes) + p4;
-        c32[(4 * q + 0) * K4] = __builtin_amdgcn_perm(x23lo, x01lo, 0x05040100u);
-        c32[(4 * q + 1) * K4] = __builtin_amdgcn_perm(x23lo, x01lo, 0x07060302u);
-        c32[(4 * q + 2) * K4] = __builtin_amdgcn_perm(x23hi, x01hi, 0x05040100u);
-        c32[(4 * q + 3) * K4] = __builtin_amdgcn_perm(x23hi, x01hi, 0x07060302u);
-      }
-    }
+    img_block_rows(img + (m0 / kBlk) * ld, 0, ap.Kp / 4, codes);
   } else {
     // the last block of a batch, or one row: only its rows' bytes
     const uint8_t* blk = img + (m0 / kBlk) * ld + m0 % kBlk;
@@ -4106,21 +4167,7 @@ __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ im
     s_a[1] = s1;
   }
   __syncthreads();
-  const bool one_bit = ap.c[0] == 1 || (ap.S == 2 && ap.c[1] == 1);
-  if (R == kBlk && rows == kBlk && !one_bit) {
-    for (int gi = 0; gi < ap.S; ++gi) {
-      const int c = gi ? ap.c[1] : ap.c[0];
-      const int ng = gi ? ap.ng[1] : ap.ng[0];
-      const int gbase = gi ? ap.kpad[0] : 0;
-      uint8_t* dst = packed + (gi ? ap.seg_off[1] : ap.seg_off[0]) +
-                     (m0 / kBlk) * (gi ? ap.mblk_bytes[1] : ap.mblk_bytes[0]);
-      if (c == 8) write_block_pieces<8, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
-      else if (c == 4) write_block_pieces<4, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
-      else write_block_pieces<2, kBlk>(codes, ap.Kp, gbase, ng, 0, dst);
-    }
-  } else {
-    write_act_units(codes, rows, m0, ap, packed, ximg);
-  }
+  write_act_units(codes, rows, m0, ap, packed, ximg);
 }
 
 // ------------------------------------------------------ sub-group scales --
@@ -4612,16 +4659,7 @@ void k_gemm_g(GemmArgs a) {
         } else {
           qc = qnext_col(cqg[jj], a.qn);
         }
-        int c[4];
-        bool nr[4];
-#pragma unroll
-        for (int h = 0; h < 4; ++h) c[h] = qnext_fast(y[h], qc, nr[h]);
-        if (__builtin_amdgcn_ballot_w64(nr[0] || nr[1] || nr[2] || nr[3]) != 0) [[unlikely]] {
-#pragma unroll
-          for (int h = 0; h < 4; ++h)
-            if (nr[h]) c[h] = qnext_exact(y[h], qc);
-        }
-        qn_stage4<BM>(qs, crank[jj], row0, c);
+        qn_stage4<BM>(qs, crank[jj], row0, qnext4(y, qc));
       }
     }
   }
@@ -5381,13 +5419,32 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   const float s0 = blocks ? 0.0f : s_next[0];
   const float s1 = !blocks && ap2.S == 2 ? s_next[1] : 0.0f;
   float* s_out = blocks ? nullptr : s_a2;  // block scales were stored above
-  if (kBlk * (size_t)ap2.Kp <= 64 * 1024)
-    hipLaunchKernelGGL(k_pack_img<kBlk>, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
-                       kBlk * (size_t)ap2.Kp, stream, img, a.qn_ld, !gemv_form, M, ap2, s0, s1, s_out, packed2,
-                       M == 1 ? ximg2 : nullptr);
-  else
-    hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)M), dim3(256), (size_t)ap2.Kp, stream, img,
-                       a.qn_ld, !gemv_form, M, ap2, s0, s1, s_out, packed2, M == 1 ? ximg2 : nullptr);
+  // Full 16-row blocks of the GEMM tiles' image (no 1-bit group) spread
+  // over about a thousand workgroups; the rest (the GEMV forms' rows, a
+  // 1-bit group, a last partial block) one block (or row) per workgroup.
+  const bool one_bit = ap2.c[0] == 1 || (ap2.S == 2 && ap2.c[1] == 1);
+  const int64_t nfull = !gemv_form && !one_bit ? M / kBlk : 0;
+  if (nfull > 0) {
+    const int ngr = ap2.Kp / kGran;
+    // at least enough parts to keep a part's LDS within 64 KB (64 granules)
+    const int parts = (int)std::max<int64_t>((ngr + 63) / 64,
+                                             std::min<int64_t>(ngr, (1024 + nfull - 1) / nfull));
+    const size_t lds = (size_t)kBlk * kGran * ((ngr + parts - 1) / parts);
+    hipLaunchKernelGGL(k_pack_img_split, dim3((unsigned)nfull, (unsigned)parts), dim3(256), lds,
+                       stream, img, a.qn_ld, ap2, s0, s1, s_out, packed2);
+    s_out = nullptr;  // stored
+  }
+  const int64_t rest = M - nfull * kBlk;
+  if (rest > 0) {
+    if (kBlk * (size_t)ap2.Kp <= 64 * 1024)
+      hipLaunchKernelGGL(k_pack_img<kBlk>, dim3((unsigned)((rest + kBlk - 1) / kBlk)), dim3(256),
+                         kBlk * (size_t)ap2.Kp, stream, img, a.qn_ld, !gemv_form, nfull, M, ap2, s0,
+                         s1, s_out, packed2, M == 1 ? ximg2 : nullptr);
+    else
+      hipLaunchKernelGGL(k_pack_img<1>, dim3((unsigned)rest), dim3(256), (size_t)ap2.Kp, stream, img,
+                         a.qn_ld, !gemv_form, nfull * kBlk, M, ap2, s0, s1, s_out, packed2,
+                         M == 1 ? ximg2 : nullptr);
+  }
   return hipGetLastError();
 }
 
