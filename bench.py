@@ -401,6 +401,91 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
+def graph_ms(fn, steps, warmup):
+    """Milliseconds per call of fn: `steps` calls captured in one HIP graph,
+    replayed once untimed and once between two events on the stream."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        fn()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(g, stream=side):
+        for _ in range(steps):
+            fn()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def run_conv_chain(steps, warmup):
+    """Two 3x3 convolutions in a row (the CNN workload's layer: 32 images of
+    256 x 14 x 14 -> 256 channels, then the same again), both as implicit
+    GEMMs, timed two ways as `steps` steps in one HIP graph: the second
+    convolution's input quantized in the first one's epilogue with static
+    scales straight into its haloed code image (soniq_mp_gemm_quantize_next),
+    and the unfused form (bf16 Y of layer 1, turned into an fp32 NCHW tensor
+    by torch, then soniq_quantize_act_conv3x3 with the batch maximum).  The
+    static scales are calibrated once, untimed, from the unfused form."""
+    import torch
+    import paper_2311_14114_amd as sq
+    import workloads
+
+    torch.cuda.set_device(0)
+    l1 = workloads.make("conv3x3_im2col")
+    B, C, H, W = l1["X"].shape
+    N = l1["N"]
+    l2 = workloads.conv3x3(B, N, H, W, N, seed=l1["seed"] + 100, name="conv3x3_second")
+    M = B * H * W
+    dev = torch.device("cuda")
+    X1 = torch.from_numpy(l1["X"]).to(dev)
+
+    def pack(case, cin):
+        Wf = torch.from_numpy(np.ascontiguousarray(case["W"].reshape(case["N"], cin, 3, 3))).to(dev)
+        return sq.soniq_pack_weights_conv3x3(Wf, case["w_bits"], case["a_bits"][::9], False,
+                                             sign_nibbles=True)
+
+    wh1, wh2 = pack(l1, C), pack(l2, N)
+    act1 = sq.soniq_act_create_conv3x3(wh1, B, H, W)
+    act2 = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    Y1 = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    X2 = torch.empty((B, N, H, W), dtype=torch.float32, device=dev)
+    Y2 = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+
+    def unfused():
+        sq.soniq_quantize_act_conv3x3(act1, X1)
+        sq.soniq_mp_gemm(act1, wh1, out=Y1)
+        X2.copy_(Y1.view(B, H, W, N).permute(0, 3, 1, 2))
+        sq.soniq_quantize_act_conv3x3(act2, X2)
+        sq.soniq_mp_gemm(act2, wh2, out=Y2)
+
+    unfused()
+    torch.cuda.synchronize()
+    s2 = sq.soniq_act_unpack_debug(act2)[1].copy()
+
+    def fused():
+        sq.soniq_quantize_act_conv3x3(act1, X1)
+        sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, s2)
+        sq.soniq_mp_gemm(act2, wh2, out=Y2)
+
+    fused()  # prepares act2 for this producer (allocates outside the graph)
+    t_f, t_u = graph_ms(fused, steps, warmup), graph_ms(unfused, steps, warmup)
+    ops = 2 * 2 * M * N * 9 * C
+    print(json.dumps({
+        "chain": "conv3x3 -> conv3x3 (implicit GEMM)", "input": [int(B), int(C), int(H), int(W)],
+        "N": int(N), "launch": "graph", "steps": steps, "warmup": warmup,
+        "fused_us": t_f * 1e3, "unfused_us": t_u * 1e3, "fused_tops": ops / (t_f * 1e-3) / 1e12,
+        "unfused_tops": ops / (t_u * 1e-3) / 1e12, "static_scales": [float(v) for v in s2],
+        "data": "synthetic"}), flush=True)
+
+
 def run_chain(steps, warmup, group_bits=0, rows=0):
     """Two transformer linears in a row (FFN up, 4096x3072x768, then FFN
     down, 4096x768x3072), timed two ways, each as `steps` steps captured
@@ -451,28 +536,7 @@ def run_chain(steps, warmup, group_bits=0, rows=0):
         sq.soniq_mp_gemm(act2, wh2, out=Y2)
 
     fused()  # prepares act2 for this producer (allocates outside the graph)
-    stream = torch.cuda.current_stream()
-
-    def timed(fn):
-        for _ in range(warmup):
-            fn()
-        g = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.graph(g, stream=side):
-            for _ in range(steps):
-                fn()
-        torch.cuda.synchronize()
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        g.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / steps
-
-    t_f, t_u = timed(fused), timed(unfused)
+    t_f, t_u = graph_ms(fused, steps, warmup), graph_ms(unfused, steps, warmup)
     ops = 2 * M * (up["N"] * up["K"] + down["N"] * down["K"])
     print(json.dumps({
         "chain": "xfmr_ffn_up -> xfmr_ffn_down", "M": M, "act_group_bits": group_bits,
@@ -498,6 +562,10 @@ def main():
     ap.add_argument("--chain", action="store_true",
                     help="time FFN up -> FFN down with the next layer quantized in the first "
                          "GEMM's epilogue, against the unfused form")
+    ap.add_argument("--conv-chain", action="store_true",
+                    help="time two 3x3 convolutions in a row (the CNN workload's layer twice, "
+                         "implicit GEMMs), the second's input quantized in the first's epilogue, "
+                         "against the unfused form")
     ap.add_argument("--chain-rows", type=int, default=0,
                     help="--chain: only the first ROWS activation rows (a decode batch)")
     ap.add_argument("--chain-group-bits", type=int, default=0,
@@ -527,6 +595,9 @@ def main():
         return
     if args.chain:
         run_chain(args.steps, args.warmup, args.chain_group_bits, args.chain_rows)
+        return
+    if args.conv_chain:
+        run_conv_chain(args.steps, args.warmup)
         return
 
     import workloads

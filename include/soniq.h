@@ -365,12 +365,23 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * quantizes its outputs as the next layer's activations, so that layer
  * needs no soniq_quantize_act call and no fp32 (or bf16) copy of them is
  * read back.  Passages: Sec. 4 fuses quantization into the operation that
- * produces the activations, to cut memory traffic; codec items 1-2 with
- * static (calibrated) group scales in place of the batch maximum.
+ * produces the activations (for CNNs, into the convolution), to cut memory
+ * traffic; codec items 1-2 with static (calibrated) group scales in place
+ * of the batch maximum.
  *
- *   act, w   as for soniq_mp_gemm (act quantized, made for w).
+ *   act, w   as for soniq_mp_gemm (act quantized, made for w); w may be an
+ *            implicit convolution's (soniq_pack_weights_conv3x3, act from
+ *            soniq_act_create_conv3x3), whose GEMM then carries the epilogue.
  *   next     an activation handle of the next layer's weights, whose K
- *            equals this layer's N; act's M must not exceed its max_M.
+ *            equals this layer's N; act's M must not exceed its max_M.  Or
+ *            a handle of soniq_act_create_conv3x3 (the next layer an
+ *            implicit 3x3 convolution): its input channels C equal this
+ *            layer's N, and this layer's M rows are the output pixels of
+ *            M / (H*W) <= B whole images in (image, y, x) order, as a
+ *            convolution's GEMM produces them (INVALID_ARGUMENT
+ *            otherwise).  The codes then go straight into next's haloed
+ *            code image (the halo holding the code of 0.0), as
+ *            soniq_quantize_act_conv3x3 would leave it for that input.
  *   s_next   host float [act_scales of the next layer's weights]: the
  *            static scale of each next-layer activation group (narrow width
  *            first), or of each block when the next layer's weights were
@@ -389,7 +400,8 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * their per-block kernels (acc_dev then holds their per-block sums, as for
  * soniq_mp_gemm).  The first call with a given
  * (weights, next) pair allocates next's code image (max_M rounded up to
- * 256, plus 8, rows of its padded K, bytes) and a column table, synchronously; later calls with the
+ * 256, plus 8, rows of its padded K, or of its two groups' padded channel
+ * counts for a convolution, bytes) and a column table, synchronously; later calls with the
  * same pair allocate nothing, so make that first call before capturing the
  * call in a HIP graph.  `next` keeps one table per producer weights handle
  * until it is destroyed: a graph captured with one producer stays valid
@@ -397,8 +409,10 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out);
  * `next` must not be `act` (its scales would be overwritten before the
  * GEMM reads them).
  * Errors: INVALID_ARGUMENT (null, next == act, mismatched handles or
- * sizes, bad scales), UNSUPPORTED (more tiles than one launch takes), OUT_OF_MEMORY,
- * HIP.
+ * sizes, bad scales, a batch that is not whole images of a convolution
+ * next), UNSUPPORTED (more tiles than one launch takes; an implicit
+ * convolution whose widths have no kernel, or feeding weights packed with
+ * sub-group scales), OUT_OF_MEMORY, HIP.
  */
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
                                          const float* s_next, uint16_t* Y_dev, int64_t ldy,

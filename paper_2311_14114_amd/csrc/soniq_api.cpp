@@ -1106,6 +1106,12 @@ soniq_status soniq_quantize_mp_gemm_scratch(soniq_weights w, const float* A_dev,
   return run_quantize_gemm(a, A_dev, M, lda, Y_dev, ldy, acc_dev, st);
 }
 
+// Positions of one row of a handle's next-layer byte image: its plan's
+// padded K, or for an implicit convolution the channel ranks of its groups.
+static int64_t qn_cols(const soniq_act_s& a) {
+  return a.w->conv ? a.cg.cpad[0] + (a.ap.S == 2 ? a.cg.cpad[1] : 0) : a.ap.Kp;
+}
+
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
                                          const float* s_next, uint16_t* Y_dev, int64_t ldy,
                                          int32_t* acc_dev, void* stream) {
@@ -1119,17 +1125,33 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   if (next == act)
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
                 "soniq_mp_gemm_quantize_next: next is the producer's own activation handle");
-  if (w->conv || next->w->conv)
-    return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm_quantize_next: implicit-convolution weights");
   const soniq_weights w2 = next->w;
-  if (w2->K != w->N)
+  // an implicit convolution as the next layer: its input channels are this
+  // layer's outputs, and this layer's rows its output pixels
+  const bool conv_next = w2->conv;
+  if (w->conv && !conv_gemm_supported(act->ap, w->wp))
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_mp_gemm_quantize_next: no implicit-convolution kernel for these widths");
+  if (w->conv && w2->act_group_bits)
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_mp_gemm_quantize_next: an implicit convolution into sub-group scales");
+  const int64_t K2 = conv_next ? w2->C : w2->K;
+  if (K2 != w->N)
     return fail(SONIQ_ERR_INVALID_ARGUMENT,
-                "soniq_mp_gemm_quantize_next: next layer has K=%lld, this layer N=%lld",
-                (long long)w2->K, (long long)w->N);
+                "soniq_mp_gemm_quantize_next: next layer has %lld input channels, this layer N=%lld",
+                (long long)K2, (long long)w->N);
   const int64_t M = act->M;
-  if (M > next->max_M)
+  if (conv_next) {
+    const ConvGeo& cg2 = next->cg;
+    const int64_t hw = (int64_t)cg2.H * cg2.W;
+    if (M % hw != 0 || M / hw > cg2.B)
+      return fail(SONIQ_ERR_INVALID_ARGUMENT,
+                  "soniq_mp_gemm_quantize_next: M=%lld is not a batch of at most %d images of %dx%d",
+                  (long long)M, cg2.B, cg2.H, cg2.W);
+  } else if (M > next->max_M) {
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: M=%lld > next max_M=%lld",
                 (long long)M, (long long)next->max_M);
+  }
   if (Y_dev && ldy < w->N)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_mp_gemm_quantize_next: ldy < N");
   for (int g = 0; g < w2->scales(); ++g)
@@ -1146,7 +1168,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     // producer's column table, built synchronously
     if (!next->qn_img) {
       uint8_t* img = nullptr;
-      const size_t bytes = (size_t)((next->M_alloc + 8) * w2->kp.Kp);
+      const size_t bytes = (size_t)((next->M_alloc + 8) * qn_cols(*next));
       HIP_TRY(dev_alloc(&img, bytes));
       const hipError_t e = hipMemset(img, 0, bytes);
       if (e != hipSuccess) {
@@ -1164,15 +1186,31 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     const int Np = w->wp.Np;
     std::vector<int32_t> tab(3 * (size_t)Np, -1);
     std::vector<std::vector<int64_t>> cols(Np / kGemmBN);
+    // next-layer position of input channel n: its planned position, or for a
+    // next convolution its rank within its group (group 1 after cpad[0])
+    std::vector<int32_t> npos(w->N), ngrp(w->N);
+    if (conv_next) {
+      int64_t cnt[2] = {0, 0};
+      for (int64_t n = 0; n < w->N; ++n) {
+        const int g = w2->kp.seg[9 * n];
+        ngrp[n] = g;
+        npos[n] = (int32_t)((g ? w2->cpad[0] : 0) + cnt[g]++);
+      }
+    } else {
+      for (int64_t n = 0; n < w->N; ++n) {
+        ngrp[n] = w2->act_group_bits ? w2->grp_h[n] : w2->kp.seg[n];  // block, or group
+        npos[n] = w2->kp.pos[n];
+      }
+    }
     for (int64_t n = 0; n < w->N; ++n) {
       const int32_t p = w->phys_h[n];
-      tab[p] = w2->act_group_bits ? w2->grp_h[n] : w2->kp.seg[n];  // block, or group
-      tab[2 * (size_t)Np + p] = w2->kp.pos[n];  // [2 Np, 3 Np): position by physical column
+      tab[p] = ngrp[n];
+      tab[2 * (size_t)Np + p] = npos[n];  // [2 Np, 3 Np): position by physical column
       cols[p / kGemmBN].push_back(n);
     }
     for (size_t t = 0; t < cols.size(); ++t) {
       std::sort(cols[t].begin(), cols[t].end());
-      for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = w2->kp.pos[cols[t][r]];
+      for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = npos[cols[t][r]];
     }
     int32_t* t = nullptr;
     HIP_TRY(dev_alloc(&t, tab.size()));
@@ -1185,12 +1223,25 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
     qn_tab = t;
   }
   float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
-  HIP_TRY(launch_mp_gemm_qnext(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                               acc_dev, next->qn_img, next->M_alloc, qn_tab, next->ap,
-                               w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
-                               next->packed, st, next->ximg,
-                               act->ximg_ok ? act->ximg : nullptr));
-  next->ximg_ok = M == 1 && next->ximg != nullptr;
+  QnConv qc{};
+  if (conv_next) {
+    qc.cg = next->cg;
+    qc.img = next->img;
+    qc.B = (int)(M / ((int64_t)next->cg.H * next->cg.W));
+    for (int64_t n = 0; n < w->N; ++n) qc.cnt[w2->kp.seg[9 * n]]++;
+    for (int g = 0; g < 2; ++g) {
+      // the stored code of 0.0: +1 in a sign group, else 0, less the zero point
+      const int code0 = next->ap.q[g].sign1 ? 1 : 0;
+      qc.halo[g] = code0 - next->ap.zp[g];
+    }
+  }
+  HIP_TRY(launch_mp_gemm_qnext(w->conv ? nullptr : act->packed, act->s_a, act->ap, w->dev(), w->wp,
+                               M, w->N, Y_dev, ldy, acc_dev, next->qn_img, next->M_alloc, qn_tab,
+                               next->ap, w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
+                               next->packed, st, next->ximg, act->ximg_ok ? act->ximg : nullptr,
+                               w->conv ? act->img : nullptr, w->conv ? &act->cg : nullptr,
+                               conv_next ? &qc : nullptr));
+  next->ximg_ok = !conv_next && M == 1 && next->ximg != nullptr;
   next->M = M;
   return SONIQ_OK;
 }

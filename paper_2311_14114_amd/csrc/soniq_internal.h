@@ -149,6 +149,18 @@ struct ConvGeo {
   int chan_ld;
 };
 
+// A next layer that is an implicit 3x3 convolution (quantization fused into
+// its producer): its code image and geometry, the channels of each
+// precision group (ranks past them are padding), the images in the batch,
+// and the stored code of 0.0 in each group (the halo's).
+struct QnConv {
+  ConvGeo cg;
+  uint8_t* img;
+  int cnt[2];
+  int B;
+  int halo[2];
+};
+
 struct WDev {
   const uint8_t* packed;
   const uint64_t* blk_off;  // byte offset of each block
@@ -243,13 +255,18 @@ hipError_t launch_mp_gemv_grouped(const uint8_t* act_packed, const float* s_a, c
 // Batches of at most 8 rows run the GEMV forms with the same epilogue
 // (qtab then also holds, at [2 Np, 3 Np), the next-layer position of each
 // physical column); ximg2 receives the next layer's row image for one row,
-// ximg is this layer's (or null).
+// ximg is this layer's (or null).  pimg/pcg: this layer is an implicit
+// convolution reading that code image (its tiles then carry the epilogue).
+// conv: the next layer is an implicit convolution, whose positions are its
+// channel ranks (qtab as above in that space) and whose haloed image
+// k_pack_conv_img writes instead of packed rows.
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, int64_t img_rows,
                                 const int32_t* qtab, const ActPlan& ap2, const float* s_next,
                                 float* s_a2, float* brs2, uint8_t* packed2, hipStream_t stream,
-                                uint8_t* ximg2, const uint8_t* ximg);
+                                uint8_t* ximg2, const uint8_t* ximg, const uint8_t* pimg = nullptr,
+                                const ConvGeo* pcg = nullptr, const QnConv* conv = nullptr);
 
 hipError_t launch_mp_gemm(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                           const WDev& wd, const WPlan& wp, int64_t M, int64_t N,

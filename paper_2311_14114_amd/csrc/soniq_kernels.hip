@@ -2718,14 +2718,14 @@ __device__ __forceinline__ void qn_stage4(uint8_t* qs, int rank, int row0, uint3
   *reinterpret_cast<uint32_t*>(qs + rank * (BM + 16) + row0) = w;
 }
 
-// The staged codes to the image: the thread of column rank c writes each
-// 16-row block's 16 codes of its position as one 16-byte store (rows past M
-// land in the image's padding rows, which nothing packs).
+// The staged codes to the image: the thread of column rank c (next-layer
+// position qpos, -1 for none) writes each 16-row block's 16 codes of its
+// position as one 16-byte store (rows past M land in the image's padding
+// rows, which nothing packs).
 template <int BM>
-__device__ __forceinline__ void qn_store(const GemmArgs& a, const uint8_t* qs, int nt, int64_t m0,
+__device__ __forceinline__ void qn_store(const GemmArgs& a, const uint8_t* qs, int qpos, int64_t m0,
                                          int tid) {
   const int c = tid & (kGemmBN - 1);
-  const int qpos = a.qn_tab[a.wp.Np + nt * kGemmBN + c];
   if (qpos < 0) return;
   uint8_t* out = a.qn_img + (m0 / kBlk) * a.qn_ld + (int64_t)qpos * 16;
   for (int ch = tid / kGemmBN; ch < BM / 16; ch += 256 / kGemmBN)
@@ -2799,6 +2799,11 @@ void k_gemm(GemmArgs a) {
       if constexpr (QN > 0) cqg[jj] = a.qn_tab[pc];
     }
   }
+  // The store phase's column of this thread (its original column, or its
+  // next-layer position), requested now rather than after the epilogue's
+  // barrier, where its latency would hold back every store of the tile.
+  const int st_col = QN > 0 ? a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))]
+                            : a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
 
   v4i acc0[WFM][4];
 #pragma unroll
@@ -2958,7 +2963,7 @@ void k_gemm(GemmArgs a) {
     }
     __syncthreads();
     // thread: column rank tid % 128, rows 2*(tid / 128) + 4k and the next
-    const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
+    const int n = st_col;
     if (n >= 0) {
       const int mrem = (int)min((int64_t)BM, a.M - m0);
       uint16_t* yout = a.Y + m0 * a.ldy + n;
@@ -3055,7 +3060,7 @@ void k_gemm(GemmArgs a) {
     }
   }
   __syncthreads();
-  qn_store<BM>(a, qs, nt, m0, tid);
+  qn_store<BM>(a, qs, st_col, m0, tid);
   if (!want_y) return;
   const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
   if (n >= 0) {
@@ -4170,6 +4175,85 @@ __global__ __launch_bounds__(256) void k_pack_img(const uint8_t* __restrict__ im
   write_act_units(codes, rows, m0, ap, packed, ximg);
 }
 
+// The next layer's haloed code image (an implicit 3x3 convolution's input,
+// geometry cg) from the byte image its producer's epilogue wrote: positions
+// are ranks within the precision groups (rank r of group g at
+// g ? cpad[0] + r : r, Cp positions a row), blocked from the GEMM tiles,
+// row-major from the GEMV forms, as for k_pack_img.  Output pixel m of the
+// producer is pixel (y, x) = ((m / W) % H, m % W) of image m / (H*W).
+// Workgroup b packs 16-row block b into its interior pixels, one unit
+// (16 ranks) per thread; every workgroup then takes a share of the halo
+// pixels, whose units hold the stored code of 0.0 (halo[g]) at the group's
+// ranks and the stored 0 of padding past them.  Workgroup 0 also stores
+// the static scales.  Dynamic LDS: 16 * Cp bytes.
+__global__ __launch_bounds__(256) void k_pack_conv_img(const uint8_t* __restrict__ bimg, int64_t ld,
+                                                       bool blocked, int64_t M, int nimg, int cnt0,
+                                                       int cnt1, int halo0, int halo1, ActPlan ap,
+                                                       ConvGeo cg, float s0, float s1,
+                                                       float* __restrict__ s_a,
+                                                       uint8_t* __restrict__ img) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  const int Cp = cg.cpad[0] + (ap.S == 2 ? cg.cpad[1] : 0);
+  const int U0 = cg.cpad[0] / 16, U = U0 + (ap.S == 2 ? cg.cpad[1] / 16 : 0);
+  const int Wp = cg.W + 2, Hp = cg.H + 2, HW = cg.H * cg.W;
+  const int64_t m0 = (int64_t)blockIdx.x * kBlk;
+  const int rows = (int)min((int64_t)kBlk, M - m0);
+  if (s_a && blockIdx.x == 0 && threadIdx.x == 0) {
+    s_a[0] = s0;
+    s_a[1] = s1;
+  }
+  if (blocked) {
+    img_block_rows(bimg + (m0 / kBlk) * ld, 0, Cp / 4, codes);
+  } else {
+    for (int r = 0; r < rows; ++r)
+      for (int i = threadIdx.x; i < Cp / 16; i += 256)
+        reinterpret_cast<uint4*>(codes + r * Cp)[i] = reinterpret_cast<const uint4*>(bimg + (m0 + r) * ld)[i];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < rows * U; i += 256) {
+    const int r = i / U, u = i - r * U;
+    const int g = u >= U0 ? 1 : 0, uu = g ? u - U0 : u;
+    const uint4 d = *reinterpret_cast<const uint4*>(codes + r * Cp + 16 * u);
+    const int64_t m = m0 + r;
+    const int b = (int)(m / HW), rem = (int)(m - (int64_t)b * HW);
+    const int y = rem / cg.W, x = rem - y * cg.W;
+    const int64_t hp = ((int64_t)b * Hp + y + 1) * Wp + x + 1;
+    const int c = ap.c[g];
+    store_unit(img + cg.img_off[g] + hp * cg.rowbytes[g] + uu * 2 * c, pack_unit(d.x, d.y, d.z, d.w, c), c);
+  }
+  // halo pixels: the top and bottom rows, then the left and right columns
+  const int nh = 2 * Wp + 2 * cg.H;
+  const int64_t hitems = (int64_t)nimg * nh * U;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < hitems; i += (int64_t)gridDim.x * 256) {
+    const int u = (int)(i % U);
+    const int64_t q = i / U;
+    const int b = (int)(q / nh), h = (int)(q - (int64_t)b * nh);
+    int yh, xh;
+    if (h < 2 * Wp) {
+      yh = h < Wp ? 0 : Hp - 1;
+      xh = h < Wp ? h : h - Wp;
+    } else {
+      const int v = h - 2 * Wp;
+      yh = 1 + (v >> 1);
+      xh = (v & 1) ? Wp - 1 : 0;
+    }
+    const int g = u >= U0 ? 1 : 0, uu = g ? u - U0 : u;
+    const int cnt = g ? cnt1 : cnt0;
+    const uint32_t hb = (uint32_t)(g ? halo1 : halo0) & 0xFFu;
+    uint32_t dw[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dw[j] = 0u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (16 * uu + 4 * j + e < cnt) dw[j] |= hb << (8 * e);
+    }
+    const int64_t hp = ((int64_t)b * Hp + yh) * Wp + xh;
+    const int c = ap.c[g];
+    store_unit(img + cg.img_off[g] + hp * cg.rowbytes[g] + uu * 2 * c, pack_unit(dw[0], dw[1], dw[2], dw[3], c), c);
+  }
+}
+
 // ------------------------------------------------------ sub-group scales --
 // GroupSize_act blocks (the design-space parameters of Sec. 3; Sec. 5 uses
 // 512-bit activation groups for transformers): each precision group is cut
@@ -4547,6 +4631,9 @@ void k_gemm_g(GemmArgs a) {
     crank[jj] = a.wd.colrank[pc];
     if constexpr (QN > 0) cqg[jj] = a.qn_tab[pc];
   }
+  // the store phase's column of this thread, requested early (as k_gemm)
+  const int st_col = QN > 0 ? a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))]
+                            : a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
 
   v4i acc[WFM][4];
   float yf[WFM][4][4];
@@ -4665,10 +4752,10 @@ void k_gemm_g(GemmArgs a) {
   }
   __syncthreads();
   if constexpr (QN > 0) {
-    qn_store<BM>(a, qs, nt, m0, tid);
+    qn_store<BM>(a, qs, st_col, m0, tid);
     if (!want_y) return;
   }
-  const int n = a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
+  const int n = QN > 0 ? a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))] : st_col;
   if (n >= 0) {
     const int mrem = (int)min((int64_t)BM, a.M - m0);
     uint16_t* yout = a.Y + m0 * a.ldy + n;
@@ -5338,13 +5425,31 @@ static void launch_gemm_qn_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
     hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 1>), grid, dim3(256), 0, stream, a);
 }
 
+// The implicit convolution's tiles with the next layer's quantization.
+template <int CBL, int CBH>
+static void launch_gemm_qn_conv_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  hipLaunchKernelGGL((k_gemm<2, 4, 8, CBL, CBH, 2, 2, 1, false, true>),
+                     dim3((unsigned)(((M + 63) / 64) * ntn)), dim3(256), 0, stream, a);
+}
+
 hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                 const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                 int64_t ldy, int32_t* acc, uint8_t* img, int64_t img_rows,
                                 const int32_t* qtab, const ActPlan& ap2, const float* s_next,
                                 float* s_a2, float* brs2, uint8_t* packed2, hipStream_t stream,
-                                uint8_t* ximg2, const uint8_t* ximg) {
+                                uint8_t* ximg2, const uint8_t* ximg, const uint8_t* pimg,
+                                const ConvGeo* pcg, const QnConv* conv) {
+  if (pimg && (!conv_gemm_supported(ap, wp) || ap2.gsub[0] > 0)) return hipErrorInvalidValue;
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  if (pimg) {
+    a.img = pimg;
+    a.cg = *pcg;
+  }
+  // positions of one row of the byte image: the next plan's, or the ranks
+  // of a next convolution's two groups
+  const int64_t qcols = conv ? (int64_t)conv->cg.cpad[0] + (ap2.S == 2 ? conv->cg.cpad[1] : 0)
+                             : (int64_t)ap2.Kp;
   const bool blocks = ap2.gsub[0] > 0;
   if (blocks) {
     BlockScales b{};
@@ -5373,18 +5478,24 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   }
   // batches of at most 8 rows: the GEMV forms, whose epilogue quantizes
   // each output the same way
-  const bool gv_g = ap.gsub[0] > 0 && gemv_g_fits(M, ap, wp);
-  const bool gv = ap.gsub[0] == 0 && gemv_nibble_plan(ap) && gemv_fits(M, ap, wp);
+  const bool gv_g = !pimg && ap.gsub[0] > 0 && gemv_g_fits(M, ap, wp);
+  const bool gv = !pimg && ap.gsub[0] == 0 && gemv_nibble_plan(ap) && gemv_fits(M, ap, wp);
   // The two forms keep separate images, so that neither writes a position
   // that is padding in the other's layout (padding bytes stay 0).
   const bool gemv_form = gv || gv_g;
-  a.qn_ld = gemv_form ? (int64_t)ap2.Kp : 16 * (int64_t)ap2.Kp;
+  a.qn_ld = gemv_form ? qcols : 16 * qcols;
   if (gemv_form) {
-    img += img_rows * ap2.Kp;
+    img += img_rows * qcols;
     a.qn_img = img;
   }
   const int cl = wp.c_lo, ch = wp.c_hi;
-  if (gemv_form) {
+  if (pimg) {
+    if (cl == 4 && ch == 4) launch_gemm_qn_conv_t<4, 4>(a, M, stream);
+    else if (cl == 1 && ch == 4) launch_gemm_qn_conv_t<1, 4>(a, M, stream);
+    else if (cl == 2 && ch == 4) launch_gemm_qn_conv_t<2, 4>(a, M, stream);
+    else if (cl == 2 && ch == 8) launch_gemm_qn_conv_t<2, 8>(a, M, stream);
+    else launch_gemm_qn_conv_t<4, 8>(a, M, stream);
+  } else if (gemv_form) {
     a.xs_bytes = (int)((gemv_lds(M, ap, wp) + 15) / 16 * 16);
     if (M == 1 && gv) a.ximg = const_cast<uint8_t*>(ximg);
     const dim3 grid((unsigned)wp.nblk);
@@ -5419,6 +5530,14 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
   const float s0 = blocks ? 0.0f : s_next[0];
   const float s1 = !blocks && ap2.S == 2 ? s_next[1] : 0.0f;
   float* s_out = blocks ? nullptr : s_a2;  // block scales were stored above
+  if (conv) {
+    // a next convolution: its haloed image, interior and halo
+    hipLaunchKernelGGL(k_pack_conv_img, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
+                       (size_t)kBlk * qcols, stream, img, a.qn_ld, !gemv_form, M, conv->B,
+                       conv->cnt[0], conv->cnt[1], conv->halo[0], conv->halo[1], ap2, conv->cg, s0,
+                       s1, s_out, conv->img);
+    return hipGetLastError();
+  }
   // Full 16-row blocks of the GEMM tiles' image (no 1-bit group) spread
   // over about a thousand workgroups; the rest (the GEMV forms' rows, a
   // 1-bit group, a last partial block) one block (or row) per workgroup.

@@ -346,3 +346,132 @@ def test_next_must_not_be_the_producers_handle():
     with pytest.raises(sq.SoniqError) as e:
         sq.soniq_mp_gemm_quantize_next(h, w, h, np.ones(w.S, np.float32))
     assert e.value.status == sq.SONIQ_ERR_INVALID_ARGUMENT
+
+
+def conv_chain(B, C1, H, W, N1, N2, a1, w1, a2, w2, a2_signed, implicit1, seed, with_y=False):
+    """Conv -> conv (Sec. 4 fuses quantization into the convolution that
+    produces the next one's input): layer 1 (implicit, or as a GEMM on its
+    lowered matrix) quantizes its fp32 outputs with static scales straight
+    into layer 2's haloed code image; layer 2 then runs as an implicit
+    convolution.  Against the oracle: layer 2's lowered codes (the halo and
+    border taps hold the code of 0.0), accumulators and outputs."""
+    l1 = workloads.conv3x3(B, C1, H, W, N1, a_lo=a1[0], a_hi=a1[1], a_frac_lo=0.6, w_lo=w1[0],
+                           w_hi=w1[1], w_frac_lo=0.7, a_signed=False, seed=seed)
+    l2 = workloads.conv3x3(B, N1, H, W, N2, a_lo=a2[0], a_hi=a2[1], a_frac_lo=0.6, w_lo=w2[0],
+                           w_hi=w2[1], w_frac_lo=0.5, a_signed=a2_signed, seed=seed + 1)
+    M = B * H * W
+    print(f"[gpu] conv chain B={B} C1={C1} {H}x{W} N1={N1} N2={N2} a2={a2} "
+          f"signed={a2_signed} implicit={implicit1}", flush=True)
+    r1 = oracle.run(l1["A"], l1["W"], l1["a_bits"], l1["w_bits"], False)
+    y1 = oracle.epilogue_replay_f32(r1["acc"], r1["s_a"], r1["s_w"])  # [M, N1], rows (b, y, x)
+    X2 = np.ascontiguousarray(y1.reshape(B, H, W, N1).transpose(0, 3, 1, 2))
+    A2 = workloads.im2col_3x3(X2)
+    _, s2, _, _ = oracle.quantize_act(A2, l2["a_bits"], a2_signed)
+    q2 = oracle.quantize_act_static(A2, l2["a_bits"], a2_signed, s2)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    S2, _, seg_of2 = oracle.segments(l2["a_bits"])
+    acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+    if implicit1:
+        W1 = torch.from_numpy(np.ascontiguousarray(l1["W"].reshape(N1, C1, 3, 3))).cuda()
+        wh1 = sq.soniq_pack_weights_conv3x3(W1, l1["w_bits"], l1["a_bits"][::9], False)
+        act1 = sq.soniq_act_create_conv3x3(wh1, B, H, W)
+        sq.soniq_quantize_act_conv3x3(act1, torch.from_numpy(l1["X"]).cuda())
+    else:
+        wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], False)
+        act1 = sq.soniq_act_create(wh1, M)
+        sq.soniq_quantize_act(act1, torch.from_numpy(l1["A"]).cuda())
+    W2 = torch.from_numpy(np.ascontiguousarray(l2["W"].reshape(N2, N1, 3, 3))).cuda()
+    wh2 = sq.soniq_pack_weights_conv3x3(W2, l2["w_bits"], l2["a_bits"][::9], a2_signed)
+    act2 = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    Y1 = torch.empty((M, N1), dtype=torch.bfloat16, device="cuda") if with_y else None
+    sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, s2, out=Y1)
+    acc = torch.empty((S2, M, N2), dtype=torch.int32, device="cuda")
+    Y2 = sq.soniq_mp_gemm(act2, wh2, acc=acc)
+    torch.cuda.synchronize()
+    g_q2, g_s2 = sq.soniq_act_unpack_debug(act2)
+    np.testing.assert_array_equal(g_s2, s2[:S2])
+    np.testing.assert_array_equal(g_q2, q2)
+    if with_y:
+        np.testing.assert_array_equal(_bf16_bits(Y1), r1["y_replay"])
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+    np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2[:S2], s_w2))
+
+
+CONV_CHAINS = [  # (B, C1, H, W, N1, N2, a1, w1, a2, w2, a2_signed, implicit1)
+    (2, 16, 5, 7, 32, 24, (4, 8), (1, 4), (4, 8), (2, 4), False, True),   # implicit -> implicit
+    (2, 16, 5, 7, 32, 24, (4, 8), (1, 4), (4, 8), (2, 4), False, False),  # lowered GEMM -> implicit
+    (1, 20, 6, 9, 40, 130, (4, 8), (2, 8), (3, 6), (4, 8), True, True),   # signed 3/6-bit next
+    (3, 8, 4, 4, 48, 16, (4, 8), (4, 8), (4, 8), (1, 4), False, True),    # 16 channels past a group
+    (1, 12, 2, 2, 24, 16, (4, 8), (2, 4), (4, 8), (2, 4), False, False),  # 4 pixels: a GEMV producer
+]
+
+
+@pytest.mark.parametrize("c", CONV_CHAINS,
+                         ids=lambda c: f"B{c[0]}_C{c[1]}_{c[2]}x{c[3]}_N{c[4]}_{'impl' if c[11] else 'gemm'}")
+def test_conv_chain(c):
+    conv_chain(*c, seed=sum(c[:6]))
+
+
+def test_conv_chain_with_y():
+    """The producer's Y as well as the next layer's codes."""
+    conv_chain(3, 16, 6, 6, 32, 32, (4, 8), (1, 4), (4, 8), (2, 4), False, True, seed=5, with_y=True)
+
+
+def test_conv_chain_smaller_batch_same_handles():
+    """Three images, then one new image through the same producer and next
+    handles: the second call's codes cover its one image (interior and
+    halo) and its next-layer GEMM matches the oracle."""
+    B, C1, H, W, N1, N2 = 3, 16, 5, 6, 32, 24
+    l1 = workloads.conv3x3(B, C1, H, W, N1, w_lo=1, w_hi=4, seed=31)
+    l2 = workloads.conv3x3(B, N1, H, W, N2, w_lo=2, w_hi=4, seed=77)
+    W1 = torch.from_numpy(np.ascontiguousarray(l1["W"].reshape(N1, C1, 3, 3))).cuda()
+    wh1 = sq.soniq_pack_weights_conv3x3(W1, l1["w_bits"], l1["a_bits"][::9], False)
+    act1 = sq.soniq_act_create_conv3x3(wh1, B, H, W)
+    W2 = torch.from_numpy(np.ascontiguousarray(l2["W"].reshape(N2, N1, 3, 3))).cuda()
+    wh2 = sq.soniq_pack_weights_conv3x3(W2, l2["w_bits"], l2["a_bits"][::9], False)
+    act2 = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    S2, _, seg_of2 = oracle.segments(l2["a_bits"])
+    s2 = np.array([0.05, 0.4], np.float32)
+    X_one = np.abs(np.random.default_rng(5).standard_normal((1, C1, H, W)).astype(np.float32))
+    for X in (l1["X"], X_one):
+        b = X.shape[0]
+        print(f"[gpu] conv chain on shared handles, {b} image(s)", flush=True)
+        A1 = workloads.im2col_3x3(X)
+        r1 = oracle.run(A1, l1["W"], l1["a_bits"], l1["w_bits"], False)
+        y1 = oracle.epilogue_replay_f32(r1["acc"], r1["s_a"], r1["s_w"])
+        A2 = workloads.im2col_3x3(np.ascontiguousarray(y1.reshape(b, H, W, N1).transpose(0, 3, 1, 2)))
+        q2 = oracle.quantize_act_static(A2, l2["a_bits"], False, s2)
+        acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+        sq.soniq_quantize_act_conv3x3(act1, torch.from_numpy(X).cuda())
+        sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, s2)
+        acc = torch.empty((S2, b * H * W, N2), dtype=torch.int32, device="cuda")
+        Y2 = sq.soniq_mp_gemm(act2, wh2, acc=acc)
+        torch.cuda.synchronize()
+        g_q2, _ = sq.soniq_act_unpack_debug(act2)
+        np.testing.assert_array_equal(g_q2, q2)
+        np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+        np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2[:S2], s_w2))
+
+
+def test_conv_chain_rejects_bad_batches():
+    """A producer whose rows are not whole images of the next handle, or more
+    images than it holds."""
+    l1 = workloads.conv3x3(2, 8, 4, 4, 16, seed=3)
+    l2 = workloads.conv3x3(1, 16, 4, 4, 16, seed=4)
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], False)
+    W2 = torch.from_numpy(np.ascontiguousarray(l2["W"].reshape(16, 16, 3, 3))).cuda()
+    wh2 = sq.soniq_pack_weights_conv3x3(W2, l2["w_bits"], l2["a_bits"][::9], False)
+    act2 = sq.soniq_act_create_conv3x3(wh2, 1, 4, 4)
+    act1 = sq.soniq_act_create(wh1, 32)
+    for rows in (20, 32):  # not whole 4x4 images; two images into a one-image handle
+        sq.soniq_quantize_act(act1, torch.from_numpy(l1["A"][:rows].copy()).cuda())
+        with pytest.raises(sq.SoniqError) as e:
+            sq.soniq_mp_gemm_quantize_next(act1, wh1, act2, [0.1, 0.2])
+        assert e.value.status == sq.SONIQ_ERR_INVALID_ARGUMENT
+
+
+def test_conv_chain_at_workload_size():
+    """Two 256 -> 256 3x3 layers at 14x14, batch 32 (the CNN workload's
+    shape), the first quantizing the second's input in its epilogue."""
+    conv_chain(32, 256, 14, 14, 256, 256, (4, 8), (1, 4), (4, 8), (1, 4), False, True, seed=11)
