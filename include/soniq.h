@@ -419,6 +419,37 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
                                          int32_t* acc_dev, void* stream);
 
 /*
+ * soniq_mp_gemm_quantize_next_max -- the two-pass form of quantization
+ * fused into the producer: soniq_mp_gemm(act, w) storing Y (required),
+ * whose epilogue also folds each next-layer activation group's largest |Y|
+ * (of the values as stored, bf16) per output tile; one pass over Y then
+ * quantizes it into `next` with the batch maxima of those.  Passages:
+ * Sec. 4 (quantization fused into the producing operation); codec items
+ * 1-2 (the group max-abs scale over the batch).
+ *
+ *   act, w, Y_dev, ldy, acc_dev  as for soniq_mp_gemm (Y_dev not NULL).
+ *   next     an activation handle of the next layer's weights (not a
+ *            convolution's), whose K equals this layer's N; act's M must
+ *            not exceed its max_M.
+ * On return (stream order) `next` holds exactly what
+ * soniq_quantize_act(next, float(Y)) would leave (codes and scales): no
+ * calibration, the fp32 copy of Y and the separate maximum pass are what
+ * it saves.  Batches of more than 8 rows fold the maxima in the GEMM
+ * tiles; smaller ones run the GEMV forms and reduce them in the quantizer.
+ * The first call with a given (weights, next) pair allocates as
+ * soniq_mp_gemm_quantize_next does (the same table), synchronously; make it
+ * before capturing the call in a HIP graph.  The tiles' maxima sit beside
+ * the pair's table, so calls with the same pair must not overlap.
+ * Errors: INVALID_ARGUMENT (null, next == act, mismatched handles or
+ * sizes), UNSUPPORTED (implicit-convolution weights or weights packed with
+ * sub-group scales on either side, more tiles than one launch takes),
+ * OUT_OF_MEMORY, HIP.
+ */
+soniq_status soniq_mp_gemm_quantize_next_max(soniq_act act, soniq_weights w, soniq_act next,
+                                             uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,
+                                             void* stream);
+
+/*
  * soniq_plan_input_channels -- the input-channel plan for a_bits, computed
  * on the host (no device needed): pos[k] receives the position of input
  * channel k in the packed, group-ordered and padded channel axis (group 0,

@@ -34,7 +34,7 @@ EXPORTED = [
     "soniq_pack_weights_conv3x3", "soniq_act_create", "soniq_act_create_conv3x3",
     "soniq_quantize_act", "soniq_quantize_act_conv3x3", "soniq_mp_gemm", "soniq_quantize_mp_gemm",
     "soniq_quantize_mp_gemm_scratch",
-    "soniq_mp_gemm_quantize_next",
+    "soniq_mp_gemm_quantize_next", "soniq_mp_gemm_quantize_next_max",
     "soniq_weights_info",
     "soniq_plan_input_channels", "soniq_weights_unpack_debug",
     "soniq_act_unpack_debug", "soniq_act_wait_timeouts", "soniq_debug_stream_read",
@@ -97,6 +97,8 @@ def lib() -> ctypes.CDLL:
         L.soniq_mp_gemm.argtypes = [vp, vp, vp, i64, vp, vp]
         L.soniq_mp_gemm_quantize_next.restype = st
         L.soniq_mp_gemm_quantize_next.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp]
+        L.soniq_mp_gemm_quantize_next_max.restype = st
+        L.soniq_mp_gemm_quantize_next_max.argtypes = [vp, vp, vp, vp, i64, vp, vp]
         L.soniq_quantize_mp_gemm.restype = st
         L.soniq_quantize_mp_gemm.argtypes = [vp, vp, vp, i64, i64, vp, i64, vp, vp]
         L.soniq_quantize_mp_gemm_scratch.restype = st
@@ -371,6 +373,30 @@ def soniq_mp_gemm_quantize_next(act: Activations, weights: Weights, next_act: Ac
     _check(lib().soniq_mp_gemm_quantize_next(act.handle, weights.handle, next_act.handle,
                                              sn.ctypes.data_as(ctypes.c_void_p), outp, ldy, accp,
                                              _stream(stream)))
+    next_act.M = M
+    return out
+
+
+def soniq_mp_gemm_quantize_next_max(act: Activations, weights: Weights, next_act: Activations,
+                                    out=None, acc=None, stream=None):
+    """soniq_mp_gemm(act, weights) storing Y (out, allocated when None) whose
+    epilogue also folds each next-layer group's largest |Y|; next_act then
+    holds soniq_quantize_act of float(Y) with that batch maximum.  Returns
+    out."""
+    import torch
+    M, N = act.M, weights.N
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or out.shape[0] < M:
+        raise TypeError("out must be a bf16 [M, >=N] device tensor with unit column stride")
+    accp = None
+    if acc is not None:
+        if acc.dtype != torch.int32 or not acc.is_contiguous() or tuple(acc.shape) != (weights.S, M, N):
+            raise TypeError("acc must be a contiguous int32 [S, M, N] device tensor")
+        accp = _dev(acc, "int32")
+    _check(lib().soniq_mp_gemm_quantize_next_max(act.handle, weights.handle, next_act.handle,
+                                                 _dev(out, "bf16"), out.stride(0), accp,
+                                                 _stream(stream)))
     next_act.M = M
     return out
 

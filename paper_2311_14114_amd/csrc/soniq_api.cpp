@@ -1112,6 +1112,78 @@ static int64_t qn_cols(const soniq_act_s& a) {
   return a.w->conv ? a.cg.cpad[0] + (a.ap.S == 2 ? a.cg.cpad[1] : 0) : a.ap.Kp;
 }
 
+// First use of a (producer weights, next) pair: next's code image and the
+// producer's column table, built synchronously (later calls find both).
+static soniq_status qn_prepare(soniq_act next, soniq_weights w, const char* who, int32_t** out) {
+  int32_t* qn_tab = next->qn_table(w->serial);
+  if (!next->qn_img || !qn_tab) {
+    const soniq_weights w2 = next->w;
+    const bool conv_next = w2->conv;
+    // first use of this (producer, next) pair: the code image and the
+    // producer's column table, built synchronously
+    if (!next->qn_img) {
+      uint8_t* img = nullptr;
+      const size_t bytes = (size_t)((next->M_alloc + 8) * qn_cols(*next));
+      HIP_TRY(dev_alloc(&img, bytes));
+      const hipError_t e = hipMemset(img, 0, bytes);
+      if (e != hipSuccess) {
+        (void)hipFree(img);
+        return fail_hip(e, (std::string(who) + ": hipMemset").c_str());
+      }
+      next->qn_img = img;
+    }
+    if (w2->act_group_bits && !next->qn_brs)
+      HIP_TRY(dev_alloc(&next->qn_brs, (size_t)w2->scales()));
+    // [0, Np): next-layer group of each physical column's channel;
+    // [Np, 2 Np): next-layer position of each tile's r-th column in
+    // ascending original order (the order the GEMM stages its outputs in);
+    // [2 Np, 3 Np): next-layer position of each physical column (the GEMV)
+    const int Np = w->wp.Np;
+    std::vector<int32_t> tab(3 * (size_t)Np, -1);
+    std::vector<std::vector<int64_t>> cols(Np / kGemmBN);
+    // next-layer position of input channel n: its planned position, or for a
+    // next convolution its rank within its group (group 1 after cpad[0])
+    std::vector<int32_t> npos(w->N), ngrp(w->N);
+    if (conv_next) {
+      int64_t cnt[2] = {0, 0};
+      for (int64_t n = 0; n < w->N; ++n) {
+        const int g = w2->kp.seg[9 * n];
+        ngrp[n] = g;
+        npos[n] = (int32_t)((g ? w2->cpad[0] : 0) + cnt[g]++);
+      }
+    } else {
+      for (int64_t n = 0; n < w->N; ++n) {
+        ngrp[n] = w2->act_group_bits ? w2->grp_h[n] : w2->kp.seg[n];  // block, or group
+        npos[n] = w2->kp.pos[n];
+      }
+    }
+    for (int64_t n = 0; n < w->N; ++n) {
+      const int32_t p = w->phys_h[n];
+      tab[p] = ngrp[n];
+      tab[2 * (size_t)Np + p] = npos[n];  // [2 Np, 3 Np): position by physical column
+      cols[p / kGemmBN].push_back(n);
+    }
+    for (size_t t = 0; t < cols.size(); ++t) {
+      std::sort(cols[t].begin(), cols[t].end());
+      for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = npos[cols[t][r]];
+    }
+    // followed by one pair of floats per GEMM tile of a full batch: the
+    // tiles' maxima of the two-pass form (soniq_mp_gemm_quantize_next_max)
+    const size_t ymax_words = 2 * (size_t)(next->M_alloc / 64) * (size_t)(Np / kGemmBN);
+    int32_t* t = nullptr;
+    HIP_TRY(dev_alloc(&t, tab.size() + ymax_words));
+    const hipError_t e = hipMemcpy(t, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(t);
+      return fail_hip(e, (std::string(who) + ": hipMemcpy").c_str());
+    }
+    next->qn_tabs.emplace_back(w->serial, t);
+    qn_tab = t;
+  }
+  *out = qn_tab;
+  return SONIQ_OK;
+}
+
 soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_act next,
                                          const float* s_next, uint16_t* Y_dev, int64_t ldy,
                                          int32_t* acc_dev, void* stream) {
@@ -1162,65 +1234,10 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   if (tiles > 0x7FFFFFFFLL)
     return fail(SONIQ_ERR_UNSUPPORTED, "soniq_mp_gemm_quantize_next: problem too large for one launch");
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  int32_t* qn_tab = next->qn_table(w->serial);
-  if (!next->qn_img || !qn_tab) {
-    // first use of this (producer, next) pair: the code image and the
-    // producer's column table, built synchronously
-    if (!next->qn_img) {
-      uint8_t* img = nullptr;
-      const size_t bytes = (size_t)((next->M_alloc + 8) * qn_cols(*next));
-      HIP_TRY(dev_alloc(&img, bytes));
-      const hipError_t e = hipMemset(img, 0, bytes);
-      if (e != hipSuccess) {
-        (void)hipFree(img);
-        return fail_hip(e, "soniq_mp_gemm_quantize_next: hipMemset");
-      }
-      next->qn_img = img;
-    }
-    if (w2->act_group_bits && !next->qn_brs)
-      HIP_TRY(dev_alloc(&next->qn_brs, (size_t)w2->scales()));
-    // [0, Np): next-layer group of each physical column's channel;
-    // [Np, 2 Np): next-layer position of each tile's r-th column in
-    // ascending original order (the order the GEMM stages its outputs in);
-    // [2 Np, 3 Np): next-layer position of each physical column (the GEMV)
-    const int Np = w->wp.Np;
-    std::vector<int32_t> tab(3 * (size_t)Np, -1);
-    std::vector<std::vector<int64_t>> cols(Np / kGemmBN);
-    // next-layer position of input channel n: its planned position, or for a
-    // next convolution its rank within its group (group 1 after cpad[0])
-    std::vector<int32_t> npos(w->N), ngrp(w->N);
-    if (conv_next) {
-      int64_t cnt[2] = {0, 0};
-      for (int64_t n = 0; n < w->N; ++n) {
-        const int g = w2->kp.seg[9 * n];
-        ngrp[n] = g;
-        npos[n] = (int32_t)((g ? w2->cpad[0] : 0) + cnt[g]++);
-      }
-    } else {
-      for (int64_t n = 0; n < w->N; ++n) {
-        ngrp[n] = w2->act_group_bits ? w2->grp_h[n] : w2->kp.seg[n];  // block, or group
-        npos[n] = w2->kp.pos[n];
-      }
-    }
-    for (int64_t n = 0; n < w->N; ++n) {
-      const int32_t p = w->phys_h[n];
-      tab[p] = ngrp[n];
-      tab[2 * (size_t)Np + p] = npos[n];  // [2 Np, 3 Np): position by physical column
-      cols[p / kGemmBN].push_back(n);
-    }
-    for (size_t t = 0; t < cols.size(); ++t) {
-      std::sort(cols[t].begin(), cols[t].end());
-      for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = npos[cols[t][r]];
-    }
-    int32_t* t = nullptr;
-    HIP_TRY(dev_alloc(&t, tab.size()));
-    const hipError_t e = hipMemcpy(t, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-      (void)hipFree(t);
-      return fail_hip(e, "soniq_mp_gemm_quantize_next: hipMemcpy");
-    }
-    next->qn_tabs.emplace_back(w->serial, t);
-    qn_tab = t;
+  int32_t* qn_tab = nullptr;
+  {
+    const soniq_status rc = qn_prepare(next, w, "soniq_mp_gemm_quantize_next", &qn_tab);
+    if (rc != SONIQ_OK) return rc;
   }
   float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
   QnConv qc{};
@@ -1242,6 +1259,57 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
                                w->conv ? act->img : nullptr, w->conv ? &act->cg : nullptr,
                                conv_next ? &qc : nullptr));
   next->ximg_ok = !conv_next && M == 1 && next->ximg != nullptr;
+  next->M = M;
+  return SONIQ_OK;
+}
+
+soniq_status soniq_mp_gemm_quantize_next_max(soniq_act act, soniq_weights w, soniq_act next,
+                                             uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,
+                                             void* stream) {
+  const char* who = "soniq_mp_gemm_quantize_next_max";
+  if (!live_a(act) || !live_w(w) || !live_a(next) || !Y_dev)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: bad handle or null", who);
+  if (act->w != w)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: activation handle belongs to other weights", who);
+  if (act->M < 1) return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: no activations quantized yet", who);
+  if (next == act)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: next is the producer's own activation handle", who);
+  const soniq_weights w2 = next->w;
+  if (w->conv || w2->conv)
+    return fail(SONIQ_ERR_UNSUPPORTED, "%s: implicit-convolution weights", who);
+  if (w->act_group_bits || w2->act_group_bits)
+    return fail(SONIQ_ERR_UNSUPPORTED, "%s: weights packed with sub-group activation scales", who);
+  if (w2->K != w->N)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: next layer has K=%lld, this layer N=%lld", who,
+                (long long)w2->K, (long long)w->N);
+  const int64_t M = act->M;
+  if (M > next->max_M)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: M=%lld > next max_M=%lld", who, (long long)M,
+                (long long)next->max_M);
+  if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: ldy < N", who);
+  if (((M + 63) / 64) * (w->wp.Np / kGemmBN) > 0x7FFFFFFFLL)
+    return fail(SONIQ_ERR_UNSUPPORTED, "%s: problem too large for one launch", who);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  int32_t* qn_tab = nullptr;
+  {
+    const soniq_status rc = qn_prepare(next, w, who, &qn_tab);
+    if (rc != SONIQ_OK) return rc;
+  }
+  // the tiles' maxima, after the pair's column table
+  float* ymax = reinterpret_cast<float*>(qn_tab + 3 * (size_t)w->wp.Np);
+  int nslot = 0;
+  if (M <= 8) {
+    // the GEMV forms store Y; the quantizer reduces the small batch's maxima
+    const soniq_status rc = run_gemm(*act, Y_dev, ldy, acc_dev, st);
+    if (rc != SONIQ_OK) return rc;
+  } else {
+    HIP_TRY(launch_mp_gemm_ymax(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
+                                acc_dev, qn_tab, ymax, st));
+    nslot = (int)(((M + 63) / 64) * (w->wp.Np / kGemmBN));
+  }
+  HIP_TRY(launch_act_bf16(Y_dev, M, w2->K, ldy, next->ap, w2->pos, w2->seg, ymax, nslot, next->s_a,
+                          next->packed, next->ximg, st));
+  next->ximg_ok = M == 1 && next->ximg != nullptr;
   next->M = M;
   return SONIQ_OK;
 }

@@ -36,6 +36,7 @@ constexpr int kBlk = 16;      // rows per block
 constexpr int kGemmBN = 128;  // GEMM block tile columns (8 weight blocks)
 constexpr int kMAlign = 256;  // activation rows are allocated in multiples of this
 constexpr int kAbsmaxBlocks = 1024;  // max partial maxima (pairs) per activation batch
+
 // 32-bit words of device state per activation handle (the single-pass
 // quantizer's grid counters and maxima); zero between calls.
 constexpr int kActStateWords = 8192;
@@ -283,6 +284,21 @@ hipError_t launch_conv_img(const float* X, int64_t B, int64_t C, int64_t H, int6
                            hipStream_t stream);
 // Whether the implicit-convolution GEMM has an instance for these
 // containers (activations 4 + 8 bits; weights 4/4, 1/4, 2/4, 2/8 or 4/8).
+// The two-pass form of the fused quantization (batch maximum): the GEMM
+// tiles store Y and write each next-layer group's largest |Y| (qtab's
+// groups, as above) as one float pair per tile into slots; then
+// launch_act_bf16 quantizes the next layer's activations from the stored
+// bf16 Y exactly as launch_act_quant would from float(Y), with the maxima
+// of nslot pairs (nslot = 0: reduced from the batch itself).
+hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                               const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
+                               int64_t ldy, int32_t* acc, const int32_t* qtab, float* slots,
+                               hipStream_t stream);
+hipError_t launch_act_bf16(const uint16_t* Y, int64_t M, int64_t K, int64_t ldy, const ActPlan& ap,
+                           const int32_t* pos_dev, const uint8_t* seg_dev, const float* slots,
+                           int nslot, float* s_a, uint8_t* packed, uint8_t* ximg,
+                           hipStream_t stream);
+
 bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp);
 hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,
                                const ActPlan& ap, const WDev& wd, const WPlan& wp, int64_t M,

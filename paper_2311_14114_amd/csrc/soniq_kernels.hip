@@ -626,6 +626,93 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
   write_act_units(codes, rows, m0, ap, packed, ximg);
 }
 
+// ------------------------------------------------------------ k_act_bf16 --
+// Activations of the next layer from a producer's stored bf16 outputs Y
+// with the batch maximum (the two-pass form of quantization fused into the
+// producer): each group's maximum |Y| is the largest over nslot pairs
+// (one per producer tile, written by its epilogue), or with
+// nslot = 0 every workgroup reduces it from the whole batch itself (small
+// batches).  R rows per workgroup are then quantized exactly as k_act_rows
+// quantizes float rows (the bf16 values widened, which is exact), and
+// written as units.  J > 0: rows with K % 4 == 0 and ldy % 4 == 0, Y 8-byte
+// aligned, J bf16 quadruples per thread per pass; J = 0: any layout, one
+// element at a time.  Dynamic LDS: R*Kp bytes.
+__device__ __forceinline__ float4 bf16x4(const uint16_t* p) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u),
+                     __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xFFFF0000u));
+}
+
+template <int R, int J>
+__global__ __launch_bounds__(256) void k_act_bf16(const uint16_t* __restrict__ Y, int64_t M,
+                                                  int64_t K, int64_t ldy,
+                                                  const int32_t* __restrict__ pos,
+                                                  const uint8_t* __restrict__ seg, ActPlan ap,
+                                                  const float* __restrict__ slots, int nslot,
+                                                  float* __restrict__ s_a_out,
+                                                  uint8_t* __restrict__ packed,
+                                                  uint8_t* __restrict__ ximg) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  __shared__ float red[8];
+  const int64_t m0 = (int64_t)blockIdx.x * R;
+  const int rows = (int)min((int64_t)R, M - m0);
+  const int tid = threadIdx.x;
+  float r0 = 0.0f, r1 = 0.0f;
+  if (nslot > 0) {
+    for (int b = tid; b < nslot; b += 256) {
+      const float2 v = reinterpret_cast<const float2*>(slots)[b];
+      r0 = fmaxf(r0, v.x);
+      r1 = fmaxf(r1, v.y);
+    }
+  } else if (J > 0) {
+    const uchar4* s4 = reinterpret_cast<const uchar4*>(seg);
+    for (int64_t m = 0; m < M; ++m)
+      for (int k4 = tid; k4 < (int)(K / 4); k4 += 256) max4(bf16x4(Y + m * ldy + 4 * k4), s4[k4], r0, r1);
+  } else {
+    for (int64_t m = 0; m < M; ++m)
+      for (int64_t k = tid; k < K; k += 256) {
+        const float a = fabsf(__uint_as_float((uint32_t)Y[m * ldy + k] << 16));
+        if (seg[k]) r1 = fmaxf(r1, a); else r0 = fmaxf(r0, a);
+      }
+  }
+  const float2 rr = block_max2(make_float2(r0, r1), red);
+  const float s0 = group_scale(rr.x, ap.q[0]);
+  const float s1 = ap.S == 2 ? group_scale(rr.y, ap.q[1]) : 0.0f;
+  if (blockIdx.x == 0 && tid == 0) {
+    s_a_out[0] = s0;
+    s_a_out[1] = s1;
+  }
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < rows * ap.Kp / 4; i += 256) codes32[i] = 0;
+  __syncthreads();
+  if constexpr (J > 0) {
+    const QElem q0 = qelem(s0, ap.q[0], ap.zp[0]), q1 = qelem(s1, ap.q[1], ap.zp[1]);
+    const int K4 = (int)(K / 4);
+    for (int base = tid; base < K4; base += 256 * J) {
+      int4 p[J];
+      uchar4 g[J];
+      float4 v[R][J];
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int k4 = min(base + 256 * j, K4 - 1);
+        p[j] = reinterpret_cast<const int4*>(pos)[k4];
+        g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
+#pragma unroll
+        for (int r = 0; r < R; ++r) v[r][j] = bf16x4(Y + (m0 + min(r, rows - 1)) * ldy + 4 * k4);
+      }
+      act_rows_quant<R, J>(codes, ap.Kp, rows, K4, base, p, g, v, q0, q1);
+    }
+  } else {
+    const ActQ aq = make_actq(ap, s0, s1);
+    for (int r = 0; r < rows; ++r)
+      for (int64_t k = tid; k < K; k += 256)
+        codes[(int64_t)r * ap.Kp + pos[k]] =
+            store_code(__uint_as_float((uint32_t)Y[(m0 + r) * ldy + k] << 16), seg[k], aq);
+  }
+  __syncthreads();
+  write_act_units(codes, rows, m0, ap, packed, ximg);
+}
+
 // One group's units of a 16-row block whose stored codes sit in LDS (row r
 // at codes + r*ldc + gbase): granule q holds units l = kg*16 + r of 2C bytes
 // (128C contiguous bytes); 16-byte piece w holds units w*U .. w*U+U-1
@@ -1686,6 +1773,9 @@ struct GemmArgs {
   uint8_t* qn_img;
   const int32_t* qn_tab;
   int64_t qn_ld;
+  // QN = 3 (batch maximum): per next-layer group the largest |Y| the tile
+  // stores, as pair qn_max[2*tile], qn_max[2*tile + 1]
+  float* qn_max;
   QNext qn;
   // a next layer with sub-group scales: qn_tab holds each column's block,
   // whose static scale and reciprocal are qn_bs[b], qn_brs[b] (blocks
@@ -2799,11 +2889,12 @@ void k_gemm(GemmArgs a) {
       if constexpr (QN > 0) cqg[jj] = a.qn_tab[pc];
     }
   }
-  // The store phase's column of this thread (its original column, or its
-  // next-layer position), requested now rather than after the epilogue's
-  // barrier, where its latency would hold back every store of the tile.
-  const int st_col = QN > 0 ? a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))]
-                            : a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
+  // The store phase's column of this thread (its next-layer position when
+  // the tile stores codes, else its original column), requested now rather
+  // than after the epilogue's barrier, where its latency would hold back
+  // every store of the tile.
+  const int st_col = QN == 1 || QN == 2 ? a.qn_tab[a.wp.Np + nt * kGemmBN + (tid & (kGemmBN - 1))]
+                                        : a.wd.tile_cols[nt * kGemmBN + (tid & (kGemmBN - 1))];
 
   v4i acc0[WFM][4];
 #pragma unroll
@@ -2896,7 +2987,12 @@ void k_gemm(GemmArgs a) {
   constexpr int YS = kGemmBN + 8;
   uint16_t* ys = reinterpret_cast<uint16_t*>(lds);
   static_assert(BM * YS * 2 <= NST * SLOT, "output staging fits the ring");
-  if constexpr (QN == 0) {
+  if constexpr (QN == 0 || QN == 3) {
+    // QN = 3: the largest |y| per next-layer group over the tile's rows
+    // below M (the bf16 of the largest |y| is the largest |bf16(y)|, since
+    // rounding is monotonic and symmetric)
+    float ymax[2] = {0.0f, 0.0f};
+    const bool full_rows = m0 + BM <= a.M;
     // Staged column-major (column rank c, row r at c*YT + r; YT odd in
     // dwords, so consecutive ranks of one row sit in different banks): a
     // lane's two pairs of rows go out as two 4-byte writes, and the stores
@@ -2945,10 +3041,25 @@ void k_gemm(GemmArgs a) {
         // v_cvt_pk_bf16_f32: round to nearest even, as bf16_rne.
         const __hip_bfloat162 p01 = __float22bfloat162_rn(make_float2(y[0], y[1]));
         const __hip_bfloat162 p23 = __float22bfloat162_rn(make_float2(y[2], y[3]));
-        ycol[row0 / 2] = (uint32_t)__builtin_bit_cast(uint16_t, p01.x) |
-                         ((uint32_t)__builtin_bit_cast(uint16_t, p01.y) << 16);
-        ycol[row0 / 2 + 1] = (uint32_t)__builtin_bit_cast(uint16_t, p23.x) |
+        const uint32_t w01 = (uint32_t)__builtin_bit_cast(uint16_t, p01.x) |
+                             ((uint32_t)__builtin_bit_cast(uint16_t, p01.y) << 16);
+        const uint32_t w23 = (uint32_t)__builtin_bit_cast(uint16_t, p23.x) |
                              ((uint32_t)__builtin_bit_cast(uint16_t, p23.y) << 16);
+        ycol[row0 / 2] = w01;
+        ycol[row0 / 2 + 1] = w23;
+        if constexpr (QN == 3) {
+          float m4 = 0.0f;
+          if (full_rows) [[likely]] {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) m4 = fmaxf(m4, fabsf(y[h]));
+          } else {
+#pragma unroll
+            for (int h = 0; h < 4; ++h)
+              if (m0 + row0 + h < a.M) m4 = fmaxf(m4, fabsf(y[h]));
+          }
+          if (cqg[jj]) ymax[1] = fmaxf(ymax[1], m4);
+          else ymax[0] = fmaxf(ymax[0], m4);
+        }
         if (a.acc) {
 #pragma unroll
           for (int h = 0; h < 4; ++h) {
@@ -2959,6 +3070,18 @@ void k_gemm(GemmArgs a) {
             }
           }
         }
+      }
+    }
+    if constexpr (QN == 3) {
+      // the tile's maxima (over the wave, then the workgroup), rounded to
+      // bf16 as Y is, into the tile's own pair: no atomics, nothing to clear
+      __shared__ float qred[8];
+      const float2 mx = block_max2(make_float2(ymax[0], ymax[1]), qred);
+      if (tid == 0) {
+        // the same rounding as the stores' (v_cvt_pk_bf16_f32), widened back
+        const __hip_bfloat162 pm = __float22bfloat162_rn(mx);
+        a.qn_max[2 * blockIdx.x] = __uint_as_float((uint32_t)__builtin_bit_cast(uint16_t, pm.x) << 16);
+        a.qn_max[2 * blockIdx.x + 1] = __uint_as_float((uint32_t)__builtin_bit_cast(uint16_t, pm.y) << 16);
       }
     }
     __syncthreads();
@@ -5309,6 +5432,7 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.K4 = 0;
   a.xs_bytes = 0;
   a.qn_img = nullptr;
+  a.qn_max = nullptr;
   a.qn_tab = nullptr;
   a.qn_ld = 0;
   a.qn = QNext{};
@@ -5564,6 +5688,79 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
                          a.qn_ld, !gemv_form, nfull * kBlk, M, ap2, s0, s1, s_out, packed2,
                          M == 1 ? ximg2 : nullptr);
   }
+  return hipGetLastError();
+}
+
+// The GEMM tiles storing Y and folding each next-layer group's largest |Y|
+// into the slots (cleared first), for the two-pass fused quantization.
+template <int S, int CA0, int CA1, int CBL, int CBH>
+static void launch_gemm_ymax_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  hipLaunchKernelGGL((k_gemm<S, CA0, CA1, CBL, CBH, 2, 2, 3>), dim3((unsigned)(((M + 63) / 64) * ntn)),
+                     dim3(256), 0, stream, a);
+}
+
+hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                               const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
+                               int64_t ldy, int32_t* acc, const int32_t* qtab, float* slots,
+                               hipStream_t stream) {
+  if (ap.gsub[0] > 0) return hipErrorInvalidValue;
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
+  a.xcd_tiles = tiles <= 2048;
+  a.qn_tab = qtab;
+  a.qn_max = slots;
+  const int cl = wp.c_lo, ch = wp.c_hi;
+  if (ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8) {
+    if (cl == 4 && ch == 8) launch_gemm_ymax_t<2, 4, 8, 4, 8>(a, M, stream);
+    else if (cl == 2 && ch == 8) launch_gemm_ymax_t<2, 4, 8, 2, 8>(a, M, stream);
+    else if (cl == 1 && ch == 4) launch_gemm_ymax_t<2, 4, 8, 1, 4>(a, M, stream);
+    else if (cl == 2 && ch == 4) launch_gemm_ymax_t<2, 4, 8, 2, 4>(a, M, stream);
+    else launch_gemm_ymax_t<2, 4, 8, 0, 0>(a, M, stream);
+  } else if (ap.S == 2) {
+    launch_gemm_ymax_t<2, 0, 0, 0, 0>(a, M, stream);
+  } else {
+    launch_gemm_ymax_t<1, 0, 0, 0, 0>(a, M, stream);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_act_bf16(const uint16_t* Y, int64_t M, int64_t K, int64_t ldy, const ActPlan& ap,
+                           const int32_t* pos_dev, const uint8_t* seg_dev, const float* slots,
+                           int nslot, float* s_a, uint8_t* packed, uint8_t* ximg,
+                           hipStream_t stream) {
+  const bool aligned = K % 4 == 0 && ldy % 4 == 0 && (reinterpret_cast<uintptr_t>(Y) & 7) == 0;
+  // groups of 1-bit sign codes take the per-element quantizer, as in
+  // launch_act_quant
+  const bool sign = ap.q[0].sign1 || (ap.S == 2 && ap.q[1].sign1);
+  const int64_t K4 = K / 4;
+  const int J = (sign || !aligned) ? 0 : K4 <= 256 ? 1 : K4 <= 512 ? 2 : K4 <= 768 ? 3 : 4;
+  // four rows per workgroup, or one row (small batches, whose workgroups
+  // each reduce the whole batch's maxima; or rows too long for four)
+  const bool four = M > 8 && 4 * (int64_t)ap.Kp <= 64 * 1024;
+  uint8_t* xi = M == 1 ? ximg : nullptr;
+#define SONIQ_BF16(R_, J_)                                                                          \
+  hipLaunchKernelGGL((k_act_bf16<R_, J_>), dim3((unsigned)((M + R_ - 1) / R_)), dim3(256),          \
+                     (size_t)R_ * ap.Kp, stream, Y, M, K, ldy, pos_dev, seg_dev, ap, slots, nslot, s_a, \
+                     packed, xi)
+  if (four) {
+    switch (J) {
+      case 0: SONIQ_BF16(4, 0); break;
+      case 1: SONIQ_BF16(4, 1); break;
+      case 2: SONIQ_BF16(4, 2); break;
+      case 3: SONIQ_BF16(4, 3); break;
+      default: SONIQ_BF16(4, 4); break;
+    }
+  } else {
+    switch (J) {
+      case 0: SONIQ_BF16(1, 0); break;
+      case 1: SONIQ_BF16(1, 1); break;
+      case 2: SONIQ_BF16(1, 2); break;
+      case 3: SONIQ_BF16(1, 3); break;
+      default: SONIQ_BF16(1, 4); break;
+    }
+  }
+#undef SONIQ_BF16
   return hipGetLastError();
 }
 

@@ -475,3 +475,98 @@ def test_conv_chain_at_workload_size():
     """Two 256 -> 256 3x3 layers at 14x14, batch 32 (the CNN workload's
     shape), the first quantizing the second's input in its epilogue."""
     conv_chain(32, 256, 14, 14, 256, 256, (4, 8), (1, 4), (4, 8), (1, 4), False, True, seed=11)
+
+
+def bf16_to_f32(bits):
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+MAX_CHAINS = [  # (M, K1, N1, N2, a1, w1, a2, w2, a2_signed)
+    (300, 256, 384, 96, (4, 8), (2, 8), (4, 8), (2, 8), True),    # tiles, a partial last tile
+    (64, 200, 130, 70, (4, 8), (1, 4), (4, 8), (4, 8), False),    # unsigned next; K2 % 4 != 0
+    (129, 128, 256, 64, (4, 8), (2, 4), (1, 8), (1, 4), True),    # 1-bit next group
+    (1, 512, 300, 64, (4, 8), (2, 4), (4, 8), (2, 4), True),      # one row: the GEMV form
+    (8, 640, 384, 96, (4, 8), (2, 8), (3, 6), (2, 8), False),     # 8 rows, 3/6-bit next
+]
+
+
+@pytest.mark.parametrize("c", MAX_CHAINS, ids=lambda c: f"M{c[0]}_N{c[2]}_a{c[6][0]}{c[6][1]}{'s' if c[8] else 'u'}")
+def test_chain_batch_max(c):
+    """The two-pass form (soniq_mp_gemm_quantize_next_max): Y as
+    soniq_mp_gemm stores it, and the next handle exactly as
+    soniq_quantize_act would leave it for float(Y), against the oracle's
+    quantize_act on the stored values (codec items 1-2 with the batch
+    maximum), and the next layer's GEMM on them."""
+    M, K1, N1, N2, a1, w1, a2, w2, a2_signed = c
+    l1 = workloads.generic(M, N1, K1, a_lo=a1[0], a_hi=a1[1], a_frac_lo=0.6, w_lo=w1[0],
+                           w_hi=w1[1], w_frac_lo=0.7, a_signed=True, seed=sum(c[:4]), name="max1")
+    l2 = workloads.generic(M, N2, N1, a_lo=a2[0], a_hi=a2[1], a_frac_lo=0.7, w_lo=w2[0],
+                           w_hi=w2[1], w_frac_lo=0.5, a_signed=a2_signed, seed=sum(c[:4]) + 1,
+                           name="max2")
+    print(f"[gpu] batch-max chain M={M} K1={K1} N1={N1} N2={N2} a2={a2}", flush=True)
+    r1 = oracle.run(l1["A"], l1["W"], l1["a_bits"], l1["w_bits"], True)
+    Y1f = bf16_to_f32(r1["y_replay"])
+    q2, s2, _, _ = oracle.quantize_act(Y1f, l2["a_bits"], a2_signed)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    S2, _, seg_of2 = oracle.segments(l2["a_bits"])
+    acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], a2_signed)
+    act1, act2, ref = sq.soniq_act_create(wh1, M), sq.soniq_act_create(wh2, M), sq.soniq_act_create(wh2, M)
+    sq.soniq_quantize_act(act1, torch.from_numpy(l1["A"]).cuda())
+    Y1 = sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2)
+    acc = torch.empty((S2, M, N2), dtype=torch.int32, device="cuda")
+    Y2 = sq.soniq_mp_gemm(act2, wh2, acc=acc)
+    sq.soniq_quantize_act(ref, Y1.float())  # the unfused form on the same GPU
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_bf16_bits(Y1), r1["y_replay"])
+    g_q2, g_s2 = sq.soniq_act_unpack_debug(act2)
+    r_q2, r_s2 = sq.soniq_act_unpack_debug(ref)
+    np.testing.assert_array_equal(g_s2, s2)
+    np.testing.assert_array_equal(g_q2, q2)
+    np.testing.assert_array_equal(g_s2, r_s2)
+    np.testing.assert_array_equal(g_q2, r_q2)
+    np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+    np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
+
+
+def test_chain_batch_max_repeats_and_graph():
+    """Repeated calls (the slots are cleared each time, a smaller batch
+    second), then the call captured in a HIP graph and replayed three times
+    with eager work between the replays, each against the eager result."""
+    l1 = workloads.generic(200, 256, 192, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.7, a_signed=True, seed=91, name="maxg1")
+    l2 = workloads.generic(200, 64, 256, a_lo=4, a_hi=8, a_frac_lo=0.7, w_lo=2, w_hi=4,
+                           w_frac_lo=0.5, a_signed=True, seed=92, name="maxg2")
+    wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], True)
+    wh2 = sq.soniq_pack_weights(torch.from_numpy(l2["W"]).cuda(), l2["w_bits"], l2["a_bits"], True)
+    act1, act2, ref = sq.soniq_act_create(wh1, 200), sq.soniq_act_create(wh2, 200), sq.soniq_act_create(wh2, 200)
+    A = torch.from_numpy(l1["A"]).cuda()
+    for rows in (200, 70):
+        sq.soniq_quantize_act(act1, A[:rows].contiguous())
+        Y1 = sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2)
+        sq.soniq_quantize_act(ref, Y1.float())
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(sq.soniq_act_unpack_debug(act2)[0], sq.soniq_act_unpack_debug(ref)[0])
+        np.testing.assert_array_equal(sq.soniq_act_unpack_debug(act2)[1], sq.soniq_act_unpack_debug(ref)[1])
+    Ag = A[:150].contiguous()
+    Yg = torch.empty((150, 256), dtype=torch.bfloat16, device="cuda")
+    Y2 = torch.empty((150, 64), dtype=torch.bfloat16, device="cuda")
+    sq.soniq_quantize_act(act1, Ag)
+    sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2, out=Yg)
+    sq.soniq_mp_gemm(act2, wh2, out=Y2)
+    torch.cuda.synchronize()
+    eager = _bf16_bits(Y2).copy()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(g, stream=s):
+        sq.soniq_quantize_act(act1, Ag, stream=s.cuda_stream)
+        sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2, out=Yg, stream=s.cuda_stream)
+        sq.soniq_mp_gemm(act2, wh2, out=Y2, stream=s.cuda_stream)
+    for _ in range(3):
+        Y2.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(_bf16_bits(Y2), eager)
