@@ -92,6 +92,17 @@ enum { SONIQ_WQ_SYMMETRIC = 0, SONIQ_WQ_TWOS_FRACTION = 1 };
  * (UNSUPPORTED). */
 #define SONIQ_WPACK_F8F6F4 0x200
 
+/* Packing flag, OR-ed into wq_mode: also keep a dense copy of the weights,
+ * every code in exactly its channel's width (3, 5, 6 and 7 bits no longer
+ * take the next power-of-two container; 1, 2, 4 and 8 as before), which
+ * the GEMV forms (batches of at most 8 rows, M * padded K <= 56 K) read
+ * instead of the units: fewer bytes for the weight-bound decode path.  The
+ * channels of each 16-row block share one width (two widths in one
+ * container are not merged into shared blocks).  Same codes and results.
+ * Costs the dense copy's bytes beside the units.  Not combined with
+ * sub-group activation scales or the f8f6f4 copies (UNSUPPORTED). */
+#define SONIQ_WPACK_DENSE 0x400
+
 /* Largest supported input-channel count (padded): keeps every int32
  * accumulator exact. */
 #define SONIQ_MAX_K 65536
@@ -355,6 +366,7 @@ typedef struct {
   int32_t act_group_bits;     /* GroupSize_act in bits, 0 = one scale per group */
   int32_t act_scales;         /* activation scales: blocks, or S when ungrouped */
   int32_t f8f6f4;             /* 1: packed with SONIQ_WPACK_F8F6F4 */
+  int64_t dense_w_bytes;      /* bytes of the dense copy (SONIQ_WPACK_DENSE), else 0 */
 } soniq_weights_info_t;
 
 /* Fill *out.  Errors: INVALID_ARGUMENT. */

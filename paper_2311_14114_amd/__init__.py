@@ -26,6 +26,7 @@ SONIQ_WQ_SYMMETRIC = 0
 SONIQ_WQ_TWOS_FRACTION = 1
 SONIQ_WPACK_SIGN_NIBBLES = 0x100
 SONIQ_WPACK_F8F6F4 = 0x200
+SONIQ_WPACK_DENSE = 0x400
 SONIQ_MAX_K = 65536
 
 # Every symbol include/soniq.h declares.
@@ -59,7 +60,7 @@ class WeightsInfo(ctypes.Structure):
         ("w_count", ctypes.c_int64 * 2), ("packed_w_bytes", ctypes.c_int64),
         ("packed_w_bytes_algorithmic", ctypes.c_int64),
         ("act_group_bits", ctypes.c_int32), ("act_scales", ctypes.c_int32),
-        ("f8f6f4", ctypes.c_int32),
+        ("f8f6f4", ctypes.c_int32), ("dense_w_bytes", ctypes.c_int64),
     ]
 
 
@@ -193,13 +194,14 @@ class Activations:
 
 def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_WQ_SYMMETRIC,
                        stream=None, act_group_bits: int = 0, sign_nibbles: bool = False,
-                       f8f6f4: bool = False) -> Weights:
+                       f8f6f4: bool = False, dense: bool = False) -> Weights:
     """Quantize, re-order and bit-pack W (device float32 [N, K], row-major).
     act_group_bits > 0 gives the activations sub-group scales (blocks of
     that many bits of storage inside each precision group); sign_nibbles
     stores 1-bit channels in 4-bit containers (SONIQ_WPACK_SIGN_NIBBLES);
     f8f6f4 also keeps the narrow operands in fp4/fp6 MFMA operand formats
-    (SONIQ_WPACK_F8F6F4)."""
+    (SONIQ_WPACK_F8F6F4); dense also keeps every code in exactly its width
+    for the GEMV forms (SONIQ_WPACK_DENSE)."""
     import torch
     if W.dtype != torch.float32 or W.dim() != 2 or W.stride(1) != 1:
         raise TypeError("W must be a 2-D float32 device tensor with unit column stride")
@@ -213,7 +215,8 @@ def soniq_pack_weights(W, w_bits, a_bits, a_signed: bool, wq_mode: int = SONIQ_W
                                             ab.ctypes.data_as(ctypes.c_void_p),
                                             1 if a_signed else 0,
                                             int(wq_mode) | (SONIQ_WPACK_SIGN_NIBBLES if sign_nibbles else 0)
-                                            | (SONIQ_WPACK_F8F6F4 if f8f6f4 else 0),
+                                            | (SONIQ_WPACK_F8F6F4 if f8f6f4 else 0)
+                                            | (SONIQ_WPACK_DENSE if dense else 0),
                                             int(act_group_bits), _stream(stream),
                                             ctypes.byref(h)))
     return Weights(h, N, K)

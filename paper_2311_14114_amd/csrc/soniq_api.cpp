@@ -245,6 +245,9 @@ struct soniq_weights_s {
   bool f8f6f4 = false;
   FPlan fplan{};
   uint8_t* fw = nullptr;
+  // dense copy (SONIQ_WPACK_DENSE): every code in its width, for the GEMV
+  uint8_t* dense = nullptr;
+  int64_t dense_bytes = 0;
   // 3x3 convolution packed for the implicit GEMM (tap-major channel plan)
   bool conv = false;
   int64_t C = 0;
@@ -316,6 +319,7 @@ void free_weights(soniq_weights w) {
   (void)hipFree(w->grp);
   (void)hipFree(w->posg);
   (void)hipFree(w->fw);
+  (void)hipFree(w->dense);
   (void)hipFree(w->chan);
   w->magic = kDead;
   delete w;
@@ -446,6 +450,9 @@ soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* a
   else if (w->act_group_bits)
     HIP_TRY(launch_mp_gemm_grouped(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                                    acc_dev, st));
+  else if (w->dense && gemv_dense_fits(M, act.ap))
+    HIP_TRY(launch_mp_gemv_dense(act.packed, act.s_a, act.ap, w->dev(), w->wp, w->dense, w->wb[0],
+                                 w->nw == 2 ? w->wb[1] : w->wb[0], M, w->N, Y_dev, ldy, acc_dev, st));
   else if (gemv)
     HIP_TRY(launch_mp_gemv(act.packed, act.s_a, act.ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
                            acc_dev, st, act.ximg_ok ? act.ximg : nullptr));
@@ -469,7 +476,7 @@ soniq_status run_gemm(soniq_act_s& act, uint16_t* Y_dev, int64_t ldy, int32_t* a
 soniq_status run_quantize_gemm(soniq_act_s& act, const float* A_dev, int64_t M, int64_t lda,
                                uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev, hipStream_t st) {
   const soniq_weights w = act.w;
-  if (M == 1 && !w->act_group_bits && gemv_fused_fits(A_dev, w->K, act.ap, w->wp)) {
+  if (M == 1 && !w->act_group_bits && !w->dense && gemv_fused_fits(A_dev, w->K, act.ap, w->wp)) {
     HIP_TRY(launch_gemv_fused(A_dev, w->K, w->pos16, act.packed, act.s_a, act.ap, w->dev(), w->wp,
                               w->N, Y_dev, acc_dev, st, act.ximg));
     act.ximg_ok = act.ximg != nullptr;
@@ -523,10 +530,15 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: a_signed must be 0 or 1");
   const bool sign_nibbles = (wq_mode & SONIQ_WPACK_SIGN_NIBBLES) != 0;
   const bool f8f6f4 = (wq_mode & SONIQ_WPACK_F8F6F4) != 0;
-  wq_mode &= ~(SONIQ_WPACK_SIGN_NIBBLES | SONIQ_WPACK_F8F6F4);
+  const bool dense = (wq_mode & SONIQ_WPACK_DENSE) != 0;
+  wq_mode &= ~(SONIQ_WPACK_SIGN_NIBBLES | SONIQ_WPACK_F8F6F4 | SONIQ_WPACK_DENSE);
   if (f8f6f4 && act_group_bits > 0)
     return fail(SONIQ_ERR_UNSUPPORTED,
                 "soniq_pack_weights: SONIQ_WPACK_F8F6F4 with sub-group activation scales");
+  if (dense && (f8f6f4 || act_group_bits > 0 || c_bits))
+    return fail(SONIQ_ERR_UNSUPPORTED,
+                "soniq_pack_weights: SONIQ_WPACK_DENSE with f8f6f4 copies, sub-group scales or a "
+                "convolution");
   if (wq_mode != SONIQ_WQ_SYMMETRIC && wq_mode != SONIQ_WQ_TWOS_FRACTION)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "soniq_pack_weights: unknown wq_mode %d", wq_mode);
   int wb[2], nw = 0;
@@ -606,7 +618,7 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
   // in nibbles beside 3- or 4-bit ones, or 5..8 bits) need no such padding:
   // the columns run on, narrow first, and a block may hold both widths (a
   // block needs one container; codes and scales are per column).
-  const bool one_container = nw == 2 && wp.c_lo == wp.c_hi && !f8f6f4;
+  const bool one_container = nw == 2 && wp.c_lo == wp.c_hi && !f8f6f4 && !dense;
   const int64_t nb_all = (N + kBlk - 1) / kBlk;
   const int64_t nlo = one_container ? round_up(nb_all, kGemmBN / kBlk)
                       : nw == 2    ? round_up(nb_lo, kGemmBN / kBlk)
@@ -730,6 +742,12 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
   STEP(launch_wpack(W_dev, N, K, ldw, wbits_dev, w->pos, w->seg, phys_dev, w->blk_off, w->blk_c,
                     w_qparam(b_lo, wq_mode), w_qparam(b_hi, wq_mode), b_lo, (int)w->kp.Kp,
                     w->packed, w->colinfo, st));
+  if (dense && e == hipSuccess) {
+    // the dense copy, converted from the units just packed
+    w->dense_bytes = (int64_t)dense_off(wp, wp.nblk, b_lo, b_hi);
+    STEP(dev_alloc(&w->dense, (size_t)w->dense_bytes));
+    STEP(launch_dense_pack(w->packed, wp, b_lo, b_hi, w->dense, st));
+  }
   if (f8f6f4 && e == hipSuccess) {
     // The MFMA-native copy of every (narrow activation group, narrow weight
     // class) pair, converted from the units just packed.
@@ -864,6 +882,7 @@ soniq_status soniq_weights_info(soniq_weights w, soniq_weights_info_t* out) {
   out->act_group_bits = w->act_group_bits;
   out->act_scales = w->scales();
   out->f8f6f4 = w->f8f6f4 ? 1 : 0;
+  out->dense_w_bytes = w->dense_bytes;
   return SONIQ_OK;
 }
 

@@ -109,6 +109,23 @@ __host__ __device__ inline uint64_t wblk_off(const WPlan& wp, int blk) {
   return ((uint64_t)lo * wp.c_lo + (uint64_t)(blk - lo) * wp.c_hi) * (uint64_t)wp.ngt * 128u;
 }
 
+// Dense copies of the weights for the GEMV forms (handles packed with
+// SONIQ_WPACK_DENSE): every code in b bits, b being its block's width
+// (widths 3, 5, 6 and 7 no longer take the next power-of-two container).
+// Block j (width dense_b) holds, for each 32-channel run u of the planned K
+// and each of its 16 rows r, the run's 32 codes as a little-endian string
+// of 32*b bits (b words) at dense_off(j) + (16u + r) * 4b.  A field is the
+// code's b-bit two's complement (b = 1: the sign bit, set for -1).  Blocks
+// keep the plan's order; each holds one width (the plan does not merge
+// widths into shared blocks for these handles).
+__host__ __device__ inline int dense_b(const WPlan& wp, int blk, int b_lo, int b_hi) {
+  return blk < wp.nlo ? b_lo : b_hi;
+}
+__host__ __device__ inline uint64_t dense_off(const WPlan& wp, int blk, int b_lo, int b_hi) {
+  const int lo = blk < wp.nlo ? blk : wp.nlo;
+  return ((uint64_t)lo * b_lo + (uint64_t)(blk - lo) * b_hi) * (uint64_t)wp.ngt * 128u;
+}
+
 // MFMA-native copies of narrow operands (handles packed with
 // SONIQ_WPACK_F8F6F4).  Beside the integer units above, a handle keeps the
 // codes of its narrow weight blocks and of its narrow activation groups in
@@ -308,6 +325,16 @@ hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const floa
 // Converts integer units to their MFMA-native copy: `nblk` 16-row blocks,
 // block b's units at src + b*src_bstride (ng granules of container c),
 // its copy (fmt) at dst + b*dst_bstride.
+// The dense copy of a handle's weights (layout above) from its units.
+hipError_t launch_dense_pack(const uint8_t* packed, const WPlan& wp, int b_lo, int b_hi,
+                             uint8_t* dense, hipStream_t stream);
+// The GEMV forms on the dense copy: batches of at most 8 rows (when
+// gemv_dense_fits), results as launch_mp_gemv's.
+bool gemv_dense_fits(int64_t M, const ActPlan& ap);
+hipError_t launch_mp_gemv_dense(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                const WDev& wd, const WPlan& wp, const uint8_t* dense, int b_lo,
+                                int b_hi, int64_t M, int64_t N, uint16_t* Y, int64_t ldy,
+                                int32_t* acc, hipStream_t stream);
 hipError_t launch_to_fp(const uint8_t* src, int64_t src_bstride, int c, int ng, int64_t nblk,
                         uint8_t* dst, int64_t dst_bstride, int fmt, hipStream_t stream);
 

@@ -1750,6 +1750,9 @@ struct GemmArgs {
   int64_t ldy;
   int32_t* acc;
   int xcd_tiles;  // GEMM: give each XCD a contiguous range of tiles
+  // the dense weight copy (k_gemv_dense) and its two widths
+  const uint8_t* dense;
+  int db_lo, db_hi;
   // fused batch-1 path (k_gemv_fused): the fp32 row, its planned
   // positions, where the handle's scales and packed row go, the row's
   // length in float4 and the staging bytes ahead of the code row in LDS
@@ -5424,6 +5427,8 @@ static GemmArgs make_args(const uint8_t* act_packed, const float* s_a, const Act
   a.ldy = ldy;
   a.acc = acc;
   a.xcd_tiles = 0;
+  a.dense = nullptr;
+  a.db_lo = a.db_hi = 0;
   a.a32 = nullptr;
   a.apos16 = nullptr;
   a.s_a_out = nullptr;
@@ -6178,6 +6183,220 @@ __global__ __launch_bounds__(256) void k_to_fp(const uint8_t* __restrict__ src, 
   uint8_t* o = dst + b * dst_bstride + (int64_t)f * f_block_bytes(FMT);
   *reinterpret_cast<uint4*>(o + 16 * lane) = make_uint4(d[0], d[1], d[2], d[3]);
   if constexpr (FMT == kFmtFp6) *reinterpret_cast<uint2*>(o + 1024 + 8 * lane) = make_uint2(d[4], d[5]);
+}
+
+// ---------------------------------------------------------- dense weights --
+// The dense copy (layout in soniq_internal.h): thread (block, run u, row r)
+// reads the two 16-channel units of its run from the block's units, decodes
+// their codes and writes the run's b-bit fields as b words.
+__global__ __launch_bounds__(256) void k_dense_pack(const uint8_t* __restrict__ packed, WPlan wp,
+                                                    int b_lo, int b_hi, uint8_t* __restrict__ dense) {
+  const int64_t nrun = (int64_t)wp.ngt * 2;  // 32-channel runs per row
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nrun * kBlk * wp.nblk) return;
+  const int blk = (int)(i / (nrun * kBlk));
+  const int rem = (int)(i - (int64_t)blk * nrun * kBlk);
+  const int u = rem / kBlk, r = rem - u * kBlk;
+  const int c = wblk_c(wp, blk), b = dense_b(wp, blk, b_lo, b_hi);
+  const uint8_t* gran = packed + wblk_off(wp, blk) + (int64_t)(u >> 1) * 128 * c;
+  uint32_t out[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+  const uint32_t mask = b == 32 ? 0xFFFFFFFFu : (1u << b) - 1u;
+  for (int h = 0; h < 2; ++h) {
+    const uint8_t* unit = gran + ((u & 1) * 32 + h * 16 + r) * 2 * c;  // 16-channel group 2(u&1)+h
+    uint32_t w2[2] = {0u, 0u};
+    uint4 w8 = make_uint4(0u, 0u, 0u, 0u);
+    if (c == 8) w8 = *reinterpret_cast<const uint4*>(unit);
+    else if (c == 4) { const uint2 t = *reinterpret_cast<const uint2*>(unit); w2[0] = t.x; w2[1] = t.y; }
+    else if (c == 2) w2[0] = *reinterpret_cast<const uint32_t*>(unit);
+    else w2[0] = *reinterpret_cast<const uint16_t*>(unit);
+    const uint32_t w8a[4] = {w8.x, w8.y, w8.z, w8.w};
+    for (int e = 0; e < 16; ++e) {
+      const int code = c == 8 ? (int)(int8_t)(w8a[e >> 2] >> (8 * (e & 3))) : unit_code(w2, e, c);
+      const uint32_t f = b == 1 ? (code < 0 ? 1u : 0u) : ((uint32_t)code & mask);
+      const int bit = (16 * h + e) * b, wd = bit >> 5, sh = bit & 31;
+      out[wd] |= f << sh;
+      if (sh + b > 32) out[wd + 1] |= f >> (32 - sh);
+    }
+  }
+  uint32_t* dst = reinterpret_cast<uint32_t*>(dense + dense_off(wp, blk, b_lo, b_hi) +
+                                              (int64_t)(u * kBlk + r) * 4 * b);
+  for (int j = 0; j < b; ++j) dst[j] = out[j];
+}
+
+hipError_t launch_dense_pack(const uint8_t* packed, const WPlan& wp, int b_lo, int b_hi,
+                             uint8_t* dense, hipStream_t stream) {
+  const int64_t n = (int64_t)wp.ngt * 2 * kBlk * wp.nblk;
+  hipLaunchKernelGGL(k_dense_pack, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, packed, wp,
+                     b_lo, b_hi, dense);
+  return hipGetLastError();
+}
+
+// A run's 32 fields of width B (B words w, little-endian) as 8 words of
+// four int8 codes each (for v_dot4_i32_i8).
+template <int B>
+__device__ __forceinline__ void dense_codes(const uint32_t (&w)[B], uint32_t (&o)[8]) {
+  if constexpr (B == 8) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) o[q] = w[q];
+  } else {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      uint32_t d = 0u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int bit = (4 * q + e) * B, wd = bit >> 5, sh = bit & 31;
+        int v;
+        if constexpr (B == 1) {
+          v = ((w[wd] >> sh) & 1u) ? -1 : 1;
+        } else {
+          v = sh + B <= 32 ? __builtin_amdgcn_sbfe((int)w[wd], sh, B)
+                           : __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(w[wd + 1 < B ? wd + 1 : wd], w[wd], sh), 0, B);
+        }
+        d |= ((uint32_t)v & 0xFFu) << (8 * e);
+      }
+      o[q] = d;
+    }
+  }
+}
+
+// One block of width B: thread t takes row t % 16 and runs t/16, t/16 + 16,
+// ..., loads up to 8 runs' words at once, then decodes them and forms the
+// products with the staged activation bytes (per group: runs never straddle
+// the groups, each padded to 64 channels).
+template <int MT, int B>
+__device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, const uint8_t* xs, int blk,
+                                                 int (&acc0)[MT], int (&acc1)[MT]) {
+  const int tid = threadIdx.x, r = tid & (kBlk - 1), s = tid >> 4;
+  const int Kp = a.ap.Kp, nrun = Kp / 32, kp0 = a.ap.kpad[0];
+  const int M = (int)a.M;
+  const uint32_t* blkw = reinterpret_cast<const uint32_t*>(a.dense + dense_off(a.wp, blk, a.db_lo, a.db_hi));
+  for (int u0 = s; u0 < nrun; u0 += 16 * 8) {
+    uint32_t w[8][B];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int u = min(u0 + 16 * k, nrun - 1);
+      const uint32_t* src = blkw + (int64_t)(u * kBlk + r) * B;
+#pragma unroll
+      for (int j = 0; j < B; ++j) w[k][j] = src[j];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int u = u0 + 16 * k;
+      if (u >= nrun) break;
+      uint32_t o[8];
+      dense_codes<B>(w[k], o);
+      const bool g1 = 32 * u >= kp0;
+#pragma unroll
+      for (int mm = 0; mm < MT; ++mm) {
+        if (mm < M) {
+          const uint4* x = reinterpret_cast<const uint4*>(xs + (int64_t)mm * Kp + 32 * u);
+          const uint4 x0 = x[0], x1 = x[1];
+          int v = 0;
+          v = __builtin_amdgcn_sdot4((int)o[0], (int)x0.x, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[1], (int)x0.y, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[2], (int)x0.z, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[3], (int)x0.w, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[4], (int)x1.x, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[5], (int)x1.y, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[6], (int)x1.z, v, false);
+          v = __builtin_amdgcn_sdot4((int)o[7], (int)x1.w, v, false);
+          if (g1) acc1[mm] += v;
+          else acc0[mm] += v;
+        }
+      }
+    }
+  }
+}
+
+// The GEMV on the dense copy: one workgroup per 16-row block; the
+// activation rows staged as bytes (gemv_stage_x), the block's runs as
+// above, the 16 partial sums of each row reduced over the lanes and waves,
+// and the epilogue of k_gemv (the weights' codes carry no unpack shift).
+// Dynamic LDS: M*Kp bytes.
+template <int MT>
+__global__ __launch_bounds__(256) void k_gemv_dense(GemmArgs a) {
+  extern __shared__ __align__(16) uint8_t xs[];
+  __shared__ int red[4][kBlk][2][MT];
+  const int blk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const ActPlan& ap = a.ap;
+  gemv_stage_x(a, xs);
+  __syncthreads();
+  int acc0[MT], acc1[MT];
+#pragma unroll
+  for (int mm = 0; mm < MT; ++mm) acc0[mm] = acc1[mm] = 0;
+  const int b = dense_b(a.wp, blk, a.db_lo, a.db_hi);
+  switch (b) {
+    case 1: gemv_dense_block<MT, 1>(a, xs, blk, acc0, acc1); break;
+    case 2: gemv_dense_block<MT, 2>(a, xs, blk, acc0, acc1); break;
+    case 3: gemv_dense_block<MT, 3>(a, xs, blk, acc0, acc1); break;
+    case 4: gemv_dense_block<MT, 4>(a, xs, blk, acc0, acc1); break;
+    case 5: gemv_dense_block<MT, 5>(a, xs, blk, acc0, acc1); break;
+    case 6: gemv_dense_block<MT, 6>(a, xs, blk, acc0, acc1); break;
+    case 7: gemv_dense_block<MT, 7>(a, xs, blk, acc0, acc1); break;
+    default: gemv_dense_block<MT, 8>(a, xs, blk, acc0, acc1); break;
+  }
+  // lanes of one row: t, t^16, t^32, t^48 in the wave, then the 4 waves
+#pragma unroll
+  for (int mm = 0; mm < MT; ++mm) {
+    acc0[mm] += __shfl_xor(acc0[mm], 16, 64);
+    acc0[mm] += __shfl_xor(acc0[mm], 32, 64);
+    acc1[mm] += __shfl_xor(acc1[mm], 16, 64);
+    acc1[mm] += __shfl_xor(acc1[mm], 32, 64);
+  }
+  if (lane < kBlk) {
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm) {
+      red[wid][lane][0][mm] = acc0[mm];
+      red[wid][lane][1][mm] = acc1[mm];
+    }
+  }
+  __syncthreads();
+  const int er = tid & (kBlk - 1), em = tid >> 4;
+  if (em < MT && em < (int)a.M) {
+    int t0 = 0, t1 = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      t0 += red[w][er][0][em];
+      t1 += red[w][er][1][em];
+    }
+    const int p = blk * kBlk + er;
+    const ColInfo ci = a.wd.colinfo[p];
+    if (ci.n >= 0) {
+      const bool sgn = b == 1;
+      const int S = ap.S;
+      t0 = (t0 >> ap.sh[0]) + ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
+      t1 = S == 2 ? (t1 >> ap.sh[1]) + ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0)
+                  : 0;
+      if (a.acc) {
+        a.acc[(int64_t)em * a.N + ci.n] = t0;
+        if (S == 2) a.acc[(a.M + em) * a.N + ci.n] = t1;
+      }
+      const float sa0 = a.s_a[0], sa1 = S == 2 ? a.s_a[1] : 0.0f;
+      gemv_store_out(a, p, em, ci.n, epilogue(t0, t1, S, sa0, sa1, ci.s_w));
+    }
+  }
+}
+
+bool gemv_dense_fits(int64_t M, const ActPlan& ap) {
+  return M >= 1 && M <= 8 && M * (int64_t)ap.Kp <= 56 * 1024;
+}
+
+hipError_t launch_mp_gemv_dense(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
+                                const WDev& wd, const WPlan& wp, const uint8_t* dense, int b_lo,
+                                int b_hi, int64_t M, int64_t N, uint16_t* Y, int64_t ldy,
+                                int32_t* acc, hipStream_t stream) {
+  if (!gemv_dense_fits(M, ap)) return hipErrorInvalidValue;
+  GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
+  a.dense = dense;
+  a.db_lo = b_lo;
+  a.db_hi = b_hi;
+  const dim3 grid((unsigned)wp.nblk);
+  const size_t lds = (size_t)M * ap.Kp;
+  if (M == 1) hipLaunchKernelGGL(k_gemv_dense<1>, grid, dim3(256), lds, stream, a);
+  else if (M == 2) hipLaunchKernelGGL(k_gemv_dense<2>, grid, dim3(256), lds, stream, a);
+  else if (M <= 4) hipLaunchKernelGGL(k_gemv_dense<4>, grid, dim3(256), lds, stream, a);
+  else hipLaunchKernelGGL(k_gemv_dense<8>, grid, dim3(256), lds, stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_to_fp(const uint8_t* src, int64_t src_bstride, int c, int ng, int64_t nblk,
