@@ -64,7 +64,10 @@ def algorithmic(case, info):
         ops=2 * M * N * K,
         a_fp32=M * K * 4,
         a_packed=act_packed,
-        w_packed=int(info.packed_w_bytes_algorithmic),
+        # the dense copy holds each weight in its own width; the container
+        # layout rounds a width up to 1, 2, 4 or 8 bits
+        w_packed=(int(case["w_bits"].astype(np.int64).sum()) * K // 8 if case.get("dense")
+                  else int(info.packed_w_bytes_algorithmic)),
         # per output channel: scale and one code sum per activation group
         w_side=N * (4 + 4 * S),
         y=M * N * 2,
@@ -88,11 +91,15 @@ def uses_gemv(case) -> bool:
 def gemv_kernel(case) -> str:
     if case.get("act_group_bits", 0):
         return "k_gemv_g"
+    if case.get("dense"):
+        return "k_gemv_dense"
     return "k_gemv" if case["M"] == 1 else "k_gemv_mfma"
 
 
 def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6f4=False,
             implicit=False):
+    """Pack, quantize and time one workload; case["dense"] asks for the dense
+    weight copy (SONIQ_WPACK_DENSE), which the GEMV forms read."""
     import torch
     import paper_2311_14114_amd as sq
 
@@ -120,7 +127,8 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     else:
         def pack():
             return sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], case["a_signed"],
-                                         act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4)
+                                         act_group_bits=gbits, sign_nibbles=nib, f8f6f4=f8f6f4,
+                                         dense=bool(case.get("dense")))
     ws = [pack()]
     e1.record(stream)
     torch.cuda.synchronize()
@@ -212,7 +220,7 @@ def run_gpu(case, steps, warmup, rotate=True, graph=True, conv_input=False, f8f6
     # against.
     read_ms = None
     if M <= 8:
-        nbytes = int(info.packed_w_bytes) // 16 * 16
+        nbytes = int(info.dense_w_bytes if case.get("dense") else info.packed_w_bytes) // 16 * 16
         rbuf = torch.empty(ROTATE_W_BYTES, dtype=torch.uint8, device=dev)
         nsl = max(1, ROTATE_W_BYTES // nbytes) if rotate else 1
         sink = torch.empty((nbytes + 8191) // 8192, dtype=torch.int32, device=dev)
@@ -267,7 +275,7 @@ def fused_one_row(case) -> bool:
     launch (its documented conditions: one row, one scale per precision
     group, the narrow group in 4-bit containers and the wide one, if any,
     in bytes, no 1-bit group, K a multiple of 4 up to 4096)."""
-    if case["M"] != 1 or case.get("act_group_bits", 0):
+    if case["M"] != 1 or case.get("act_group_bits", 0) or case.get("dense"):
         return False
     widths = sorted(set(int(b) for b in case["a_bits"]))
     return (case["K"] % 4 == 0 and case["K"] <= 4096 and 3 <= widths[0] <= 4
@@ -326,6 +334,7 @@ def gemv_record(case, r, steps):
         "a_bits": sorted(set(case["a_bits"].tolist())),
         "w_bits": sorted(set(case["w_bits"].tolist())),
         "weight_copies": r["nw"], "packed_weight_bytes": alg["w_packed"],
+        "dense_weights": bool(case.get("dense")),
         "packed_weight_gbs": alg["w_packed"] / g_s / 1e9,
         "step_packed_weight_gbs": alg["w_packed"] / step_s / 1e9,
         "step_us": step_s * 1e6, "mp_gemm_us": g_s * 1e6, "quantize_act_us": r["q_ms"] * 1e3,
@@ -592,6 +601,9 @@ def main():
     ap.add_argument("--f8f6f4", action="store_true",
                     help="pack the weights with SONIQ_WPACK_F8F6F4: narrow x narrow tiles run on the "
                          "fp4/fp6 MFMA")
+    ap.add_argument("--dense", action="store_true",
+                    help="decode batches: pack the weights with SONIQ_WPACK_DENSE (every code in "
+                         "its own width) so the GEMV reads the dense copy")
     ap.add_argument("--launch", choices=["graph", "eager"], default="graph",
                     help="replay the timed steps as one captured HIP graph (default) or "
                          "launch every call from the host")
@@ -613,6 +625,12 @@ def main():
 
     import workloads
     case = workloads.make(args.workload)
+    if args.dense:
+        if case["M"] > 8 or args.f8f6f4 or args.implicit_conv or case.get("act_group_bits", 0):
+            print("--dense: the dense copy serves decode batches (M <= 8) of plain linear "
+                  "layers with one scale per precision group", file=sys.stderr)
+            sys.exit(2)
+        case["dense"] = True
     if args.implicit_conv:
         args.conv_input = True
     if args.conv_input and "X" not in case:
@@ -642,6 +660,7 @@ def main():
                    "activation_copies": r["na"], "weight_copies": r["nw"],
                    "launch": args.launch, "input": "nchw" if args.conv_input else "lowered",
                    "implicit_conv": bool(args.implicit_conv),
+                   "dense_weights": bool(case.get("dense")),
                    "entry": ("soniq_quantize_act_conv3x3 + soniq_mp_gemm" if args.conv_input
                              else "soniq_quantize_mp_gemm")},
         "roofline": roofline(case, alg, r, args.steps),
@@ -661,6 +680,8 @@ def main():
         gname = DEFAULT_GEMV_WORKLOAD if args.workload == DEFAULT_WORKLOAD else "none"
     if gname != "none":
         gcase = workloads.make(gname)
+        if args.dense and not gcase.get("act_group_bits", 0):
+            gcase["dense"] = True
         if gcase["M"] > 8:
             print(f"--gemv-workload {gname} is not a decode batch (M > 8)", file=sys.stderr)
             sys.exit(2)

@@ -112,18 +112,27 @@ __host__ __device__ inline uint64_t wblk_off(const WPlan& wp, int blk) {
 // Dense copies of the weights for the GEMV forms (handles packed with
 // SONIQ_WPACK_DENSE): every code in b bits, b being its block's width
 // (widths 3, 5, 6 and 7 no longer take the next power-of-two container).
-// Block j (width dense_b) holds, for each 32-channel run u of the planned K
-// and each of its 16 rows r, the run's 32 codes as a little-endian string
-// of 32*b bits (b words) at dense_off(j) + (16u + r) * 4b.  A field is the
-// code's b-bit two's complement (b = 1: the sign bit, set for -1).  Blocks
-// keep the plan's order; each holds one width (the plan does not merge
-// widths into shared blocks for these handles).
+// Block j (width b = dense_b) spans nquad = ceil(Kp / 128) quad-runs of 128
+// planned channels; quad-run v of row r is a record of 4b words, b for
+// each of its four 32-channel runs.  A run's 32 fields are byte-sliced:
+// field 4q + e (q = 0..7) is field q of byte lane e, and lane e's 8 fields
+// form a little-endian string of 8b bits whose byte k is byte e of the
+// run's word k.  A field is the code's b-bit two's complement (b = 1: the
+// bit set for -1).  Records are cut into b 16-byte chunks and interleaved
+// for the GEMV's loads: quad-runs go in batches of 16; in batch i, with
+// n_i = min(16, nquad - 16i) quad-runs, chunk k of the record of quad-run
+// 16i + w, row r, is chunk 256*b*i + 16*n_i*k + 16w + r of the block.  Runs
+// past Kp (half of the last quad-run when Kp / 64 is odd) are zero.
+// Blocks keep the plan's order, 256*b*nquad bytes each; each holds one
+// width (the plan does not merge widths into shared blocks for these
+// handles).
 __host__ __device__ inline int dense_b(const WPlan& wp, int blk, int b_lo, int b_hi) {
   return blk < wp.nlo ? b_lo : b_hi;
 }
+__host__ __device__ inline int dense_nquad(const WPlan& wp) { return (wp.ngt + 1) / 2; }
 __host__ __device__ inline uint64_t dense_off(const WPlan& wp, int blk, int b_lo, int b_hi) {
   const int lo = blk < wp.nlo ? blk : wp.nlo;
-  return ((uint64_t)lo * b_lo + (uint64_t)(blk - lo) * b_hi) * (uint64_t)wp.ngt * 128u;
+  return ((uint64_t)lo * b_lo + (uint64_t)(blk - lo) * b_hi) * (uint64_t)dense_nquad(wp) * 256u;
 }
 
 // MFMA-native copies of narrow operands (handles packed with

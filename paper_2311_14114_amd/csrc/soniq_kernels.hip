@@ -3243,6 +3243,15 @@ __device__ __forceinline__ void gemv_stage_x(const GemmArgs& a, uint8_t* xs) {
   }
 }
 
+// Bytes of the activation buffer up to the end of the last group's first
+// 16-row block (what a GEMV reads).
+__host__ __device__ inline int64_t gemv_dense_xbytes64(const ActPlan& ap) {
+  const int64_t e0 = ap.seg_off[0] + ap.mblk_bytes[0];
+  const int64_t e1 = ap.S == 2 ? ap.seg_off[1] + ap.mblk_bytes[1] : 0;
+  return e0 > e1 ? e0 : e1;
+}
+__device__ __forceinline__ int gemv_dense_xbytes(const ActPlan& ap) { return (int)gemv_dense_xbytes64(ap); }
+
 template <int MT, int C>
 __device__ __forceinline__ void gemv_block(const GemmArgs& a, uint8_t* xs, int blk,
                                            int (&red)[4][kBlk][2][8]) {
@@ -6188,197 +6197,277 @@ __global__ __launch_bounds__(256) void k_to_fp(const uint8_t* __restrict__ src, 
 // ---------------------------------------------------------- dense weights --
 // The dense copy (layout in soniq_internal.h): thread (block, run u, row r)
 // reads the two 16-channel units of its run from the block's units, decodes
-// their codes and writes the run's b-bit fields as b words.
+// their 32 codes, slices their b-bit fields into the four byte lanes and
+// writes the run's b words into its record's chunks.  Runs past the planned
+// K (the half of a last 128-channel quad-run) are written as zeros.
 __global__ __launch_bounds__(256) void k_dense_pack(const uint8_t* __restrict__ packed, WPlan wp,
                                                     int b_lo, int b_hi, uint8_t* __restrict__ dense) {
-  const int64_t nrun = (int64_t)wp.ngt * 2;  // 32-channel runs per row
+  const int nrun = wp.ngt * 2, nquad = dense_nquad(wp), nru = 4 * nquad;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= nrun * kBlk * wp.nblk) return;
-  const int blk = (int)(i / (nrun * kBlk));
-  const int rem = (int)(i - (int64_t)blk * nrun * kBlk);
+  if (i >= (int64_t)nru * kBlk * wp.nblk) return;
+  const int blk = (int)(i / ((int64_t)nru * kBlk));
+  const int rem = (int)(i - (int64_t)blk * nru * kBlk);
   const int u = rem / kBlk, r = rem - u * kBlk;
   const int c = wblk_c(wp, blk), b = dense_b(wp, blk, b_lo, b_hi);
-  const uint8_t* gran = packed + wblk_off(wp, blk) + (int64_t)(u >> 1) * 128 * c;
-  uint32_t out[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-  const uint32_t mask = b == 32 ? 0xFFFFFFFFu : (1u << b) - 1u;
-  for (int h = 0; h < 2; ++h) {
-    const uint8_t* unit = gran + ((u & 1) * 32 + h * 16 + r) * 2 * c;  // 16-channel group 2(u&1)+h
-    uint32_t w2[2] = {0u, 0u};
-    uint4 w8 = make_uint4(0u, 0u, 0u, 0u);
-    if (c == 8) w8 = *reinterpret_cast<const uint4*>(unit);
-    else if (c == 4) { const uint2 t = *reinterpret_cast<const uint2*>(unit); w2[0] = t.x; w2[1] = t.y; }
-    else if (c == 2) w2[0] = *reinterpret_cast<const uint32_t*>(unit);
-    else w2[0] = *reinterpret_cast<const uint16_t*>(unit);
-    const uint32_t w8a[4] = {w8.x, w8.y, w8.z, w8.w};
-    for (int e = 0; e < 16; ++e) {
-      const int code = c == 8 ? (int)(int8_t)(w8a[e >> 2] >> (8 * (e & 3))) : unit_code(w2, e, c);
-      const uint32_t f = b == 1 ? (code < 0 ? 1u : 0u) : ((uint32_t)code & mask);
-      const int bit = (16 * h + e) * b, wd = bit >> 5, sh = bit & 31;
-      out[wd] |= f << sh;
-      if (sh + b > 32) out[wd + 1] |= f >> (32 - sh);
+  int code[32];
+  for (int e = 0; e < 32; ++e) code[e] = 0;
+  if (u < nrun) {
+    const uint8_t* gran = packed + wblk_off(wp, blk) + (int64_t)(u >> 1) * 128 * c;
+    for (int h = 0; h < 2; ++h) {
+      const uint8_t* unit = gran + ((u & 1) * 32 + h * 16 + r) * 2 * c;  // 16-channel group 2(u&1)+h
+      uint32_t w2[2] = {0u, 0u};
+      uint4 w8 = make_uint4(0u, 0u, 0u, 0u);
+      if (c == 8) w8 = *reinterpret_cast<const uint4*>(unit);
+      else if (c == 4) { const uint2 t = *reinterpret_cast<const uint2*>(unit); w2[0] = t.x; w2[1] = t.y; }
+      else if (c == 2) w2[0] = *reinterpret_cast<const uint32_t*>(unit);
+      else w2[0] = *reinterpret_cast<const uint16_t*>(unit);
+      const uint32_t w8a[4] = {w8.x, w8.y, w8.z, w8.w};
+      for (int e = 0; e < 16; ++e)
+        code[16 * h + e] = c == 8 ? (int)(int8_t)(w8a[e >> 2] >> (8 * (e & 3))) : unit_code(w2, e, c);
     }
   }
-  uint32_t* dst = reinterpret_cast<uint32_t*>(dense + dense_off(wp, blk, b_lo, b_hi) +
-                                              (int64_t)(u * kBlk + r) * 4 * b);
-  for (int j = 0; j < b; ++j) dst[j] = out[j];
+  // field 4q + e is field q of byte lane e; lane e's 8 fields form a string
+  // of 8b bits whose byte k goes to byte e of word k
+  uint32_t out[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+  const uint32_t mask = (1u << b) - 1u;
+  if (u < nrun) {
+    for (int e = 0; e < 4; ++e)
+      for (int q = 0; q < 8; ++q) {
+        const int cd = code[4 * q + e];
+        const uint32_t f = b == 1 ? (cd < 0 ? 1u : 0u) : ((uint32_t)cd & mask);
+        const int bit = q * b, k = bit >> 3, off = bit & 7;
+        out[k] |= ((f << off) & 0xFFu) << (8 * e);
+        if (off + b > 8) out[k + 1] |= (f >> (8 - off)) << (8 * e);
+      }
+  }
+  // record (quad-run v, row r): word w = (u % 4) * b + j of its 4b words
+  const int v = u >> 2, bi = v >> 4, vl = v & 15, ni = min(16, nquad - 16 * bi);
+  uint8_t* base = dense + dense_off(wp, blk, b_lo, b_hi);
+  for (int j = 0; j < b; ++j) {
+    const int w = (u & 3) * b + j;
+    const int64_t chunk = (int64_t)256 * b * bi + 16 * ni * (w >> 2) + 16 * vl + r;
+    *reinterpret_cast<uint32_t*>(base + chunk * 16 + (w & 3) * 4) = out[j];
+  }
 }
 
 hipError_t launch_dense_pack(const uint8_t* packed, const WPlan& wp, int b_lo, int b_hi,
                              uint8_t* dense, hipStream_t stream) {
-  const int64_t n = (int64_t)wp.ngt * 2 * kBlk * wp.nblk;
+  const int64_t n = (int64_t)4 * dense_nquad(wp) * kBlk * wp.nblk;
+  if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(k_dense_pack, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, packed, wp,
                      b_lo, b_hi, dense);
   return hipGetLastError();
 }
 
-// A run's 32 fields of width B (B words w, little-endian) as 8 words of
-// four int8 codes each (for v_dot4_i32_i8).
+// Bits lo .. hi-1 of every byte.
+__host__ __device__ constexpr uint32_t byte_bits(int lo, int hi) {
+  return ((((1u << hi) - 1u) & ~((1u << lo) - 1u)) & 0xFFu) * 0x01010101u;
+}
+
+// Exponent of the scale the dense products carry: every field sits in the
+// top bits of its byte (b = 1 as the two-bit string 01 or 11, i.e. +1 or -1
+// times 64), so a dot4 product is 2^dense_wsh times the true one.
+__host__ __device__ constexpr int dense_wsh(int b) { return b == 1 ? 6 : 8 - b; }
+
+// A run's 32 fields (b words w, byte-sliced) as 8 words of four int8 values
+// for v_dot4_i32_i8, word q holding fields 4q .. 4q+3: one shift and mask
+// for a field that lies in one byte of its lane's string, two of each for
+// one that straddles two bytes; the byte lanes never mix.
 template <int B>
-__device__ __forceinline__ void dense_codes(const uint32_t (&w)[B], uint32_t (&o)[8]) {
+__device__ __forceinline__ void dense_top(const uint32_t* w, uint32_t (&o)[8]) {
   if constexpr (B == 8) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) o[q] = w[q];
+  } else if constexpr (B == 1) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) o[q] = ((w[0] << (7 - q)) & 0x80808080u) | 0x40404040u;
   } else {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      uint32_t d = 0u;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int bit = (4 * q + e) * B, wd = bit >> 5, sh = bit & 31;
-        int v;
-        if constexpr (B == 1) {
-          v = ((w[wd] >> sh) & 1u) ? -1 : 1;
-        } else {
-          v = sh + B <= 32 ? __builtin_amdgcn_sbfe((int)w[wd], sh, B)
-                           : __builtin_amdgcn_sbfe((int)__builtin_amdgcn_alignbit(w[wd + 1 < B ? wd + 1 : wd], w[wd], sh), 0, B);
-        }
-        d |= ((uint32_t)v & 0xFFu) << (8 * e);
+      const int bit = q * B, k = bit >> 3, off = bit & 7;
+      if (off + B <= 8) {
+        o[q] = (w[k] << (8 - B - off)) & byte_bits(8 - B, 8);
+      } else {
+        const int s1 = off + B - 8, s2 = 16 - B - off;
+        o[q] = ((w[k] >> s1) & byte_bits(8 - B, s2)) | ((w[k + 1] << s2) & byte_bits(s2, 8));
       }
-      o[q] = d;
     }
   }
 }
 
-// One block of width B: thread t takes row t % 16 and runs t/16, t/16 + 16,
-// ..., loads up to 8 runs' words at once, then decodes them and forms the
-// products with the staged activation bytes (per group: runs never straddle
-// the groups, each padded to 64 channels).
+// One block of width B.  Thread t takes row t % 16 and quad-run t / 16 of
+// each batch of 16 quad-runs (its b 16-byte chunks, coalesced across the
+// workgroup).  The activation units are loaded first, then the first two
+// batches of chunks, so staging the units (rows xld bytes apart, then 32
+// zero bytes) waits for the units only; later batches are issued as a
+// batch's registers free up.  Products run on v_mfma_i32_16x16x64_i8 with
+// the block's decoded rows as B (lane l: row l % 16, its run of lane group
+// g = l / 16) and as A row c = 2m + j the staged channels of batch row m
+// that lie in activation group j, zeros elsewhere: lane l reads the run's
+// bytes of batch row (l % 16) / 2 where the run is in group (l % 16) % 2,
+// else the zero bytes.  So one accumulator holds both groups' sums and
+// every lane group contributes its own run.
 template <int MT, int B>
-__device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, const uint8_t* xs, int blk,
-                                                 int (&acc0)[MT], int (&acc1)[MT]) {
-  const int tid = threadIdx.x, r = tid & (kBlk - 1), s = tid >> 4;
-  const int Kp = a.ap.Kp, nrun = Kp / 32, kp0 = a.ap.kpad[0];
+__device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs, int xld, int blk,
+                                                 v4i& acc) {
+  const int tid = threadIdx.x, lane = tid & 63, vl = tid >> 4;
+  const int nrun = a.ap.Kp >> 5, kp0 = a.ap.kpad[0];
+  const int nquad = dense_nquad(a.wp), nbat = (nquad + 15) >> 4;
   const int M = (int)a.M;
-  const uint32_t* blkw = reinterpret_cast<const uint32_t*>(a.dense + dense_off(a.wp, blk, a.db_lo, a.db_hi));
-  for (int u0 = s; u0 < nrun; u0 += 16 * 8) {
-    uint32_t w[8][B];
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.dense + dense_off(a.wp, blk, a.db_lo, a.db_hi)), (short)0, 256 * B * nquad, 0x00020000);
+  auto issue = [&](int i, uint4 (&c)[B]) __attribute__((always_inline)) {
+    const int ni = i < nbat ? min(16, nquad - 16 * i) : 0;
+    const bool ok = vl < ni;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int u = min(u0 + 16 * k, nrun - 1);
-      const uint32_t* src = blkw + (int64_t)(u * kBlk + r) * B;
+    for (int j = 0; j < B; ++j)
+      c[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           wr, ok ? (uint32_t)(256 * B * i + 16 * ni * j + tid) * 16 : kOOB,
+                                           0, 0));
+  };
+  const int xm = (lane & 15) >> 1, xg = lane & 1;
+  const int xrow = xm < M ? xm * xld : -1;
+  const int xzero = M * xld;
+  auto consume = [&](int i, const uint4 (&c)[B]) __attribute__((always_inline)) {
+    uint32_t w[4 * B];
 #pragma unroll
-      for (int j = 0; j < B; ++j) w[k][j] = src[j];
+    for (int j = 0; j < B; ++j) {
+      w[4 * j] = c[j].x;
+      w[4 * j + 1] = c[j].y;
+      w[4 * j + 2] = c[j].z;
+      w[4 * j + 3] = c[j].w;
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int u = u0 + 16 * k;
-      if (u >= nrun) break;
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int u = 4 * (16 * i + vl) + q4;
+      // runs past the planned K, rows past the batch and the other
+      // group's lanes read the zero bytes
+      const bool on = u < nrun && xrow >= 0 && (32 * u >= kp0 ? 1 : 0) == xg;
+      const int xoff = on ? xrow + 32 * u : xzero;
       uint32_t o[8];
-      dense_codes<B>(w[k], o);
-      const bool g1 = 32 * u >= kp0;
+      dense_top<B>(w + q4 * B, o);
 #pragma unroll
-      for (int mm = 0; mm < MT; ++mm) {
-        if (mm < M) {
-          const uint4* x = reinterpret_cast<const uint4*>(xs + (int64_t)mm * Kp + 32 * u);
-          const uint4 x0 = x[0], x1 = x[1];
-          int v = 0;
-          v = __builtin_amdgcn_sdot4((int)o[0], (int)x0.x, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[1], (int)x0.y, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[2], (int)x0.z, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[3], (int)x0.w, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[4], (int)x1.x, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[5], (int)x1.y, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[6], (int)x1.z, v, false);
-          v = __builtin_amdgcn_sdot4((int)o[7], (int)x1.w, v, false);
-          if (g1) acc1[mm] += v;
-          else acc0[mm] += v;
-        }
+      for (int h = 0; h < 2; ++h) {
+        const uint4 x = *reinterpret_cast<const uint4*>(xs + xoff + 16 * h);
+        const v4i wf = v4i{(int)o[4 * h], (int)o[4 * h + 1], (int)o[4 * h + 2], (int)o[4 * h + 3]};
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(frag_of(x), wf, acc, 0, 0, 0);
       }
+    }
+  };
+  // Every unit is read as 16 bytes (its 2c bytes used) through a buffer
+  // over both groups' first 16-row blocks: one load per unit whatever its
+  // container, past the end read as zero.
+  constexpr int XR = gemv_xr<MT>();
+  const int ngt = a.wp.ngt, xd = ngt * 4, xtotal = M * xd, ng0 = a.ap.ng[0];
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)a.act, (short)0, gemv_dense_xbytes(a.ap), 0x00020000);
+  // unit u (< xtotal): batch row m, granule q, 16-channel group kg; its
+  // byte offset in the activation buffer, container and staged offset
+  auto xunit = [&](int u, uint32_t& off, int& c, int& dst) __attribute__((always_inline)) {
+    const int m = MT == 1 ? 0 : gemv_row_of<MT>(u, xd);
+    const int rest = u - m * xd, q = rest >> 2, kg = rest & 3;
+    const bool g1 = q >= ng0;
+    c = g1 ? a.ap.c[1] : a.ap.c[0];
+    off = (uint32_t)((g1 ? a.ap.seg_off[1] : a.ap.seg_off[0]) + (g1 ? q - ng0 : q) * 128 * c +
+                     (kg * 16 + m) * 2 * c);
+    dst = m * xld + q * kGran + kg * 16;
+  };
+  uint4 xr[XR];
+  int xc[XR], xdst[XR];
+#pragma unroll
+  for (int k = 0; k < XR; ++k) {
+    const int u = tid + 256 * k;
+    uint32_t off = 0;
+    xunit(min(u, xtotal - 1), off, xc[k], xdst[k]);
+    xr[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, u < xtotal ? off : kOOB, 0, 0));
+  }
+  // keep the units' loads ahead of the weights' in the issue order
+  __builtin_amdgcn_sched_barrier(0);
+  uint4 c0[B], c1[B];
+  issue(0, c0);
+  issue(1, c1);
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < 2) *reinterpret_cast<uint4*>(xs + xzero + 16 * tid) = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+  for (int k = 0; k < XR; ++k)
+    if (tid + 256 * k < xtotal) *reinterpret_cast<uint4*>(xs + xdst[k]) = unpack_unit_rt(xr[k], xc[k]);
+  for (int u = tid + 256 * XR; u < xtotal; u += 256) {
+    uint32_t off = 0;
+    int c = 0, dst = 0;
+    xunit(u, off, c, dst);
+    *reinterpret_cast<uint4*>(xs + dst) = unpack_unit_rt(load_unit(a.act + off, c), c);
+  }
+  __syncthreads();
+  for (int i = 0; i < nbat; i += 2) {
+    consume(i, c0);
+    if (i + 2 < nbat) issue(i + 2, c0);
+    if (i + 1 < nbat) {
+      consume(i + 1, c1);
+      if (i + 3 < nbat) issue(i + 3, c1);
     }
   }
 }
 
-// The GEMV on the dense copy: one workgroup per 16-row block; the
-// activation rows staged as bytes (gemv_stage_x), the block's runs as
-// above, the 16 partial sums of each row reduced over the lanes and waves,
-// and the epilogue of k_gemv (the weights' codes carry no unpack shift).
-// Dynamic LDS: M*Kp bytes.
+// The GEMV on the dense copy: one workgroup per 16-row block, batches of
+// up to 8 rows; the block's quad-runs as above, the four waves' 16x16 sums
+// met in LDS (sum row 2m + j: batch row m, activation group j) and the
+// epilogue of k_gemv (the field scale 2^dense_wsh taken out with the
+// activations' unpack shift).  Dynamic LDS: M rows of Kp + 16 bytes (the
+// pad spreads the rows over the banks) and 32 zero bytes.
 template <int MT>
-__global__ __launch_bounds__(256) void k_gemv_dense(GemmArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT >= 4 ? 3 : 4))) void k_gemv_dense(GemmArgs a) {
   extern __shared__ __align__(16) uint8_t xs[];
-  __shared__ int red[4][kBlk][2][MT];
-  const int blk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  __shared__ int red[4][4][64];
+  const int blk = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const ActPlan& ap = a.ap;
-  gemv_stage_x(a, xs);
-  __syncthreads();
-  int acc0[MT], acc1[MT];
-#pragma unroll
-  for (int mm = 0; mm < MT; ++mm) acc0[mm] = acc1[mm] = 0;
+  const int xld = ap.Kp + 16;
+  // the epilogue's column, fetched before the weights arrive
+  const int pc = blk * kBlk + (lane & 15);
+  const ColInfo ci = a.wd.colinfo[pc];
+  v4i acc = v4i{0, 0, 0, 0};
   const int b = dense_b(a.wp, blk, a.db_lo, a.db_hi);
   switch (b) {
-    case 1: gemv_dense_block<MT, 1>(a, xs, blk, acc0, acc1); break;
-    case 2: gemv_dense_block<MT, 2>(a, xs, blk, acc0, acc1); break;
-    case 3: gemv_dense_block<MT, 3>(a, xs, blk, acc0, acc1); break;
-    case 4: gemv_dense_block<MT, 4>(a, xs, blk, acc0, acc1); break;
-    case 5: gemv_dense_block<MT, 5>(a, xs, blk, acc0, acc1); break;
-    case 6: gemv_dense_block<MT, 6>(a, xs, blk, acc0, acc1); break;
-    case 7: gemv_dense_block<MT, 7>(a, xs, blk, acc0, acc1); break;
-    default: gemv_dense_block<MT, 8>(a, xs, blk, acc0, acc1); break;
+    case 1: gemv_dense_block<MT, 1>(a, xs, xld, blk, acc); break;
+    case 2: gemv_dense_block<MT, 2>(a, xs, xld, blk, acc); break;
+    case 3: gemv_dense_block<MT, 3>(a, xs, xld, blk, acc); break;
+    case 4: gemv_dense_block<MT, 4>(a, xs, xld, blk, acc); break;
+    case 5: gemv_dense_block<MT, 5>(a, xs, xld, blk, acc); break;
+    case 6: gemv_dense_block<MT, 6>(a, xs, xld, blk, acc); break;
+    case 7: gemv_dense_block<MT, 7>(a, xs, xld, blk, acc); break;
+    default: gemv_dense_block<MT, 8>(a, xs, xld, blk, acc); break;
   }
-  // lanes of one row: t, t^16, t^32, t^48 in the wave, then the 4 waves
 #pragma unroll
-  for (int mm = 0; mm < MT; ++mm) {
-    acc0[mm] += __shfl_xor(acc0[mm], 16, 64);
-    acc0[mm] += __shfl_xor(acc0[mm], 32, 64);
-    acc1[mm] += __shfl_xor(acc1[mm], 16, 64);
-    acc1[mm] += __shfl_xor(acc1[mm], 32, 64);
-  }
-  if (lane < kBlk) {
-#pragma unroll
-    for (int mm = 0; mm < MT; ++mm) {
-      red[wid][lane][0][mm] = acc0[mm];
-      red[wid][lane][1][mm] = acc1[mm];
-    }
-  }
+  for (int e = 0; e < 4; ++e) red[wid][e][lane] = acc[e];
   __syncthreads();
-  const int er = tid & (kBlk - 1), em = tid >> 4;
-  if (em < MT && em < (int)a.M) {
-    int t0 = 0, t1 = 0;
+  if (wid == 0 && ci.n >= 0) {
+    const bool sgn = b == 1;
+    const int S = ap.S, ws = dense_wsh(b);
+    const int sh0 = ap.sh[0] + ws, sh1 = ap.sh[1] + ws;
+    const int add0 = ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
+    const int add1 = ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0);
+    const float sa0 = a.s_a[0], sa1 = S == 2 ? a.s_a[1] : 0.0f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      t0 += red[w][er][0][em];
-      t1 += red[w][er][1][em];
-    }
-    const int p = blk * kBlk + er;
-    const ColInfo ci = a.wd.colinfo[p];
-    if (ci.n >= 0) {
-      const bool sgn = b == 1;
-      const int S = ap.S;
-      t0 = (t0 >> ap.sh[0]) + ap.zp[0] * ci.colsum[0] - (ap.c[0] == 1 && sgn ? ap.padcnt[0] : 0);
-      t1 = S == 2 ? (t1 >> ap.sh[1]) + ap.zp[1] * ci.colsum[1] - (ap.c[1] == 1 && sgn ? ap.padcnt[1] : 0)
-                  : 0;
-      if (a.acc) {
-        a.acc[(int64_t)em * a.N + ci.n] = t0;
-        if (S == 2) a.acc[(a.M + em) * a.N + ci.n] = t1;
+    for (int e = 0; e < 4; e += 2) {
+      const int m = (lane >> 4) * 2 + (e >> 1);  // sums e, e + 1: batch row m, groups 0 and 1
+      if (m < a.M) {
+        const int r0 = red[0][e][lane] + red[1][e][lane] + red[2][e][lane] + red[3][e][lane];
+        const int r1 = red[0][e + 1][lane] + red[1][e + 1][lane] + red[2][e + 1][lane] + red[3][e + 1][lane];
+        const int t0 = (r0 >> sh0) + add0;
+        const int t1 = S == 2 ? (r1 >> sh1) + add1 : 0;
+        if (a.acc) {
+          a.acc[(int64_t)m * a.N + ci.n] = t0;
+          if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
+        }
+        gemv_store_out(a, pc, m, ci.n, epilogue(t0, t1, S, sa0, sa1, ci.s_w));
       }
-      const float sa0 = a.s_a[0], sa1 = S == 2 ? a.s_a[1] : 0.0f;
-      gemv_store_out(a, p, em, ci.n, epilogue(t0, t1, S, sa0, sa1, ci.s_w));
     }
   }
 }
 
 bool gemv_dense_fits(int64_t M, const ActPlan& ap) {
-  return M >= 1 && M <= 8 && M * (int64_t)ap.Kp <= 56 * 1024;
+  return M >= 1 && M <= 8 && M * (int64_t)ap.Kp <= 56 * 1024 &&
+         gemv_dense_xbytes64(ap) < ((int64_t)1 << 31);
 }
 
 hipError_t launch_mp_gemv_dense(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
@@ -6390,8 +6479,8 @@ hipError_t launch_mp_gemv_dense(const uint8_t* act_packed, const float* s_a, con
   a.dense = dense;
   a.db_lo = b_lo;
   a.db_hi = b_hi;
+  const size_t lds = (size_t)M * (ap.Kp + 16) + 32;
   const dim3 grid((unsigned)wp.nblk);
-  const size_t lds = (size_t)M * ap.Kp;
   if (M == 1) hipLaunchKernelGGL(k_gemv_dense<1>, grid, dim3(256), lds, stream, a);
   else if (M == 2) hipLaunchKernelGGL(k_gemv_dense<2>, grid, dim3(256), lds, stream, a);
   else if (M <= 4) hipLaunchKernelGGL(k_gemv_dense<4>, grid, dim3(256), lds, stream, a);

@@ -59,7 +59,8 @@ def test_dense_gemv(c):
 
 
 def test_dense_bytes_and_batches_above_8():
-    """The dense copy holds 2*Kp*b bytes per 16-row block (b its width);
+    """The dense copy holds 256*b bytes per 128-channel quad-run of each
+    16-row block (b its width, Kp rounded up to 128 channels);
     batches above 8 rows run the GEMM tiles on the units, bit-exact."""
     case = workloads.generic(40, 200, 500, a_lo=4, a_hi=8, a_frac_lo=0.7, w_lo=3, w_hi=6,
                              w_frac_lo=0.6, a_signed=True, seed=3, name="dense40")
@@ -73,7 +74,8 @@ def test_dense_bytes_and_batches_above_8():
     # blocks in plan order: the narrow class padded to whole 128-column tiles
     nb_lo = -(-blocks(n_lo) // 8) * 8
     nb_all = -(-(nb_lo + blocks(n_hi)) // 8) * 8
-    expect = 2 * Kp * (3 * nb_lo + 6 * (nb_all - nb_lo))
+    nquad = -(-Kp // 128)
+    expect = 256 * nquad * (3 * nb_lo + 6 * (nb_all - nb_lo))
     assert info.dense_w_bytes == expect
     assert info.dense_w_bytes < info.packed_w_bytes
 

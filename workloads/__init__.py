@@ -36,6 +36,8 @@ CONFIGS = {
     "decode_4096_m1": 42,
     "decode_11008_m8": 43,
     "decode_4096_m8": 44,
+    "decode_11008_m1_w36": 45,
+    "decode_11008_m8_w36": 46,
     "square_8192": 5,
 }
 
@@ -179,6 +181,22 @@ def decode_4096_m8() -> dict:
     return _decode(4096, 8, 44, "decode_4096_m8")
 
 
+def _decode_w36(M: int, seed_id: int, name: str) -> dict:
+    """Decode GEMV with weight widths off the container sizes: x[M,4096]
+    ~N(0,1), 80% 4b / 20% 8b signed; W[11008,4096] ~N(0,0.02), 75% 3b /
+    25% 6b (any width from 1 to 8 bits is a valid SONIQ precision)."""
+    return generic(M, 11008, 4096, a_lo=4, a_hi=8, a_frac_lo=0.8, w_lo=3, w_hi=6,
+                   w_frac_lo=0.75, seed=BASE_SEED + seed_id, name=name)
+
+
+def decode_11008_m1_w36() -> dict:
+    return _decode_w36(1, 45, "decode_11008_m1_w36")
+
+
+def decode_11008_m8_w36() -> dict:
+    return _decode_w36(8, 46, "decode_11008_m8_w36")
+
+
 def square_8192(size: int = 8192) -> dict:
     """M = N = K = 8192, A ~N(0,1), W ~N(0,0.02), 50% 4b / 50% 8b on both
     operands with seeded interleaving."""
@@ -222,6 +240,8 @@ BUILDERS = {
     "decode_4096_m1": decode_4096_m1,
     "decode_11008_m8": decode_11008_m8,
     "decode_4096_m8": decode_4096_m8,
+    "decode_11008_m1_w36": decode_11008_m1_w36,
+    "decode_11008_m8_w36": decode_11008_m8_w36,
     "square_8192": square_8192,
     "xfmr_qkv_g512": xfmr_qkv_g512,
     "xfmr_ffn_down_g512": xfmr_ffn_down_g512,
