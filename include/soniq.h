@@ -95,10 +95,14 @@ enum { SONIQ_WQ_SYMMETRIC = 0, SONIQ_WQ_TWOS_FRACTION = 1 };
 /* Packing flag, OR-ed into wq_mode: also keep a dense copy of the weights,
  * every code in exactly its channel's width (3, 5, 6 and 7 bits no longer
  * take the next power-of-two container; 1, 2, 4 and 8 as before), which
- * the GEMV forms (batches of at most 8 rows, M * padded K <= 56 K) read
- * instead of the units: fewer bytes for the weight-bound decode path.  The
- * channels of each 16-row block share one width (two widths in one
- * container are not merged into shared blocks).  Same codes and results.
+ * the GEMV forms (batches of at most 8 rows with M * (1.25 * padded K +
+ * 16) + 32 <= 64 KiB, i.e. M * padded K up to about 52 K; larger batches
+ * read the units) read instead of the units: fewer bytes for the
+ * weight-bound decode path.  Sign (1-bit) weights against a sign
+ * activation group take XNOR-popcount products there (Sec. 4.2, Hardware
+ * Support).  The channels of each 16-row block share one width (two widths
+ * in one container are not merged into shared blocks).  Same codes and
+ * results.
  * Costs the dense copy's bytes beside the units.  Not combined with
  * sub-group activation scales or the f8f6f4 copies (UNSUPPORTED). */
 #define SONIQ_WPACK_DENSE 0x400

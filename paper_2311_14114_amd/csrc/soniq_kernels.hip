@@ -6307,9 +6307,16 @@ __device__ __forceinline__ void dense_top(const uint32_t* w, uint32_t (&o)[8]) {
 // bytes of batch row (l % 16) / 2 where the run is in group (l % 16) % 2,
 // else the zero bytes.  So one accumulator holds both groups' sums and
 // every lane group contributes its own run.
+// Sign weights (B = 1) against a sign activation group: the run's product
+// is 32 - 2 popcount(X ^ W), X and W the runs' 32 sign bits (set for -1)
+// in the same byte-sliced order, summed per thread in xacc (true units);
+// those lanes feed zeros to the matrix product.  X is staged beside the
+// byte rows as two words per run and batch row (one per 16-channel unit:
+// its nibbles spread to the low halves of four bytes, shifted by 4 for
+// the run's second unit), at xbits.
 template <int MT, int B>
 __device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs, int xld, int blk,
-                                                 v4i& acc) {
+                                                 int xbits, v4i& acc, int (&xacc)[MT]) {
   const int tid = threadIdx.x, lane = tid & 63, vl = tid >> 4;
   const int nrun = a.ap.Kp >> 5, kp0 = a.ap.kpad[0];
   const int nquad = dense_nquad(a.wp), nbat = (nquad + 15) >> 4;
@@ -6328,6 +6335,9 @@ __device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs,
   const int xm = (lane & 15) >> 1, xg = lane & 1;
   const int xrow = xm < M ? xm * xld : -1;
   const int xzero = M * xld;
+  // the sign activation group, if any (XNOR runs need B = 1 weights)
+  const int sgrp = B != 1 ? -1 : a.ap.c[0] == 1 ? 0 : a.ap.S == 2 && a.ap.c[1] == 1 ? 1 : -1;
+  const uint2* xb2 = reinterpret_cast<const uint2*>(xs + xbits);
   auto consume = [&](int i, const uint4 (&c)[B]) __attribute__((always_inline)) {
     uint32_t w[4 * B];
 #pragma unroll
@@ -6340,9 +6350,22 @@ __device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs,
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
       const int u = 4 * (16 * i + vl) + q4;
-      // runs past the planned K, rows past the batch and the other
-      // group's lanes read the zero bytes
-      const bool on = u < nrun && xrow >= 0 && (32 * u >= kp0 ? 1 : 0) == xg;
+      const int ug = 32 * u >= kp0 ? 1 : 0;
+      const bool xn = B == 1 && u < nrun && ug == sgrp;
+      if constexpr (B == 1) {
+        if (xn) {
+#pragma unroll
+          for (int mm = 0; mm < MT; ++mm) {
+            if (mm < M) {
+              const uint2 xw = xb2[mm * nrun + u];
+              xacc[mm] += 32 - 2 * (int)__popc((xw.x | xw.y) ^ w[q4]);
+            }
+          }
+        }
+      }
+      // runs past the planned K, rows past the batch, the other group's
+      // lanes and the sign runs read the zero bytes
+      const bool on = u < nrun && xrow >= 0 && ug == xg && !xn;
       const int xoff = on ? xrow + 32 * u : xzero;
       uint32_t o[8];
       dense_top<B>(w + q4 * B, o);
@@ -6363,7 +6386,8 @@ __device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs,
       (void*)a.act, (short)0, gemv_dense_xbytes(a.ap), 0x00020000);
   // unit u (< xtotal): batch row m, granule q, 16-channel group kg; its
   // byte offset in the activation buffer, container and staged offset
-  auto xunit = [&](int u, uint32_t& off, int& c, int& dst) __attribute__((always_inline)) {
+  // and, for sign runs, the offset of its bit word
+  auto xunit = [&](int u, uint32_t& off, int& c, int& dst, int& bdst) __attribute__((always_inline)) {
     const int m = MT == 1 ? 0 : gemv_row_of<MT>(u, xd);
     const int rest = u - m * xd, q = rest >> 2, kg = rest & 3;
     const bool g1 = q >= ng0;
@@ -6371,14 +6395,24 @@ __device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs,
     off = (uint32_t)((g1 ? a.ap.seg_off[1] : a.ap.seg_off[0]) + (g1 ? q - ng0 : q) * 128 * c +
                      (kg * 16 + m) * 2 * c);
     dst = m * xld + q * kGran + kg * 16;
+    bdst = xbits + 8 * (m * nrun + 2 * q + (kg >> 1)) + 4 * (kg & 1);
+  };
+  auto stage = [&](uint4 raw, int c, int dst, int bdst) __attribute__((always_inline)) {
+    *reinterpret_cast<uint4*>(xs + dst) = unpack_unit_rt(raw, c);
+    if (B == 1 && c == 1 && sgrp >= 0) {
+      const uint32_t h = raw.x & 0xFFFFu;
+      const uint32_t t = (h | (h << 8)) & 0x00FF00FFu;
+      const uint32_t y = (t | (t << 4)) & 0x0F0F0F0Fu;  // byte b = nibble b of the unit
+      *reinterpret_cast<uint32_t*>(xs + bdst) = (bdst & 4) ? y << 4 : y;
+    }
   };
   uint4 xr[XR];
-  int xc[XR], xdst[XR];
+  int xc[XR], xdst[XR], xbd[XR];
 #pragma unroll
   for (int k = 0; k < XR; ++k) {
     const int u = tid + 256 * k;
     uint32_t off = 0;
-    xunit(min(u, xtotal - 1), off, xc[k], xdst[k]);
+    xunit(min(u, xtotal - 1), off, xc[k], xdst[k], xbd[k]);
     xr[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, u < xtotal ? off : kOOB, 0, 0));
   }
   // keep the units' loads ahead of the weights' in the issue order
@@ -6390,12 +6424,12 @@ __device__ __forceinline__ void gemv_dense_block(const GemmArgs& a, uint8_t* xs,
   if (tid < 2) *reinterpret_cast<uint4*>(xs + xzero + 16 * tid) = make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
   for (int k = 0; k < XR; ++k)
-    if (tid + 256 * k < xtotal) *reinterpret_cast<uint4*>(xs + xdst[k]) = unpack_unit_rt(xr[k], xc[k]);
+    if (tid + 256 * k < xtotal) stage(xr[k], xc[k], xdst[k], xbd[k]);
   for (int u = tid + 256 * XR; u < xtotal; u += 256) {
     uint32_t off = 0;
-    int c = 0, dst = 0;
-    xunit(u, off, c, dst);
-    *reinterpret_cast<uint4*>(xs + dst) = unpack_unit_rt(load_unit(a.act + off, c), c);
+    int c = 0, dst = 0, bdst = 0;
+    xunit(u, off, c, dst, bdst);
+    stage(load_unit(a.act + off, c), c, dst, bdst);
   }
   __syncthreads();
   for (int i = 0; i < nbat; i += 2) {
@@ -6418,27 +6452,43 @@ template <int MT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT >= 4 ? 3 : 4))) void k_gemv_dense(GemmArgs a) {
   extern __shared__ __align__(16) uint8_t xs[];
   __shared__ int red[4][4][64];
+  __shared__ int redx[4][MT][kBlk];
   const int blk = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const ActPlan& ap = a.ap;
   const int xld = ap.Kp + 16;
+  const int xbits = (int)a.M * xld + 32;
   // the epilogue's column, fetched before the weights arrive
   const int pc = blk * kBlk + (lane & 15);
   const ColInfo ci = a.wd.colinfo[pc];
   v4i acc = v4i{0, 0, 0, 0};
+  int xacc[MT];
+#pragma unroll
+  for (int mm = 0; mm < MT; ++mm) xacc[mm] = 0;
   const int b = dense_b(a.wp, blk, a.db_lo, a.db_hi);
   switch (b) {
-    case 1: gemv_dense_block<MT, 1>(a, xs, xld, blk, acc); break;
-    case 2: gemv_dense_block<MT, 2>(a, xs, xld, blk, acc); break;
-    case 3: gemv_dense_block<MT, 3>(a, xs, xld, blk, acc); break;
-    case 4: gemv_dense_block<MT, 4>(a, xs, xld, blk, acc); break;
-    case 5: gemv_dense_block<MT, 5>(a, xs, xld, blk, acc); break;
-    case 6: gemv_dense_block<MT, 6>(a, xs, xld, blk, acc); break;
-    case 7: gemv_dense_block<MT, 7>(a, xs, xld, blk, acc); break;
-    default: gemv_dense_block<MT, 8>(a, xs, xld, blk, acc); break;
+    case 1: gemv_dense_block<MT, 1>(a, xs, xld, blk, xbits, acc, xacc); break;
+    case 2: gemv_dense_block<MT, 2>(a, xs, xld, blk, xbits, acc, xacc); break;
+    case 3: gemv_dense_block<MT, 3>(a, xs, xld, blk, xbits, acc, xacc); break;
+    case 4: gemv_dense_block<MT, 4>(a, xs, xld, blk, xbits, acc, xacc); break;
+    case 5: gemv_dense_block<MT, 5>(a, xs, xld, blk, xbits, acc, xacc); break;
+    case 6: gemv_dense_block<MT, 6>(a, xs, xld, blk, xbits, acc, xacc); break;
+    case 7: gemv_dense_block<MT, 7>(a, xs, xld, blk, xbits, acc, xacc); break;
+    default: gemv_dense_block<MT, 8>(a, xs, xld, blk, xbits, acc, xacc); break;
   }
 #pragma unroll
   for (int e = 0; e < 4; ++e) red[wid][e][lane] = acc[e];
+  // the sign runs' sums: the lanes of one row (l, l^16, l^32, l^48), then
+  // the waves in the epilogue
+  const int sgrp = b != 1 ? -1 : ap.c[0] == 1 ? 0 : ap.S == 2 && ap.c[1] == 1 ? 1 : -1;
+  if (sgrp >= 0) {
+#pragma unroll
+    for (int mm = 0; mm < MT; ++mm) {
+      xacc[mm] += __shfl_xor(xacc[mm], 16, 64);
+      xacc[mm] += __shfl_xor(xacc[mm], 32, 64);
+      if (lane < kBlk) redx[wid][mm][lane] = xacc[mm];
+    }
+  }
   __syncthreads();
   if (wid == 0 && ci.n >= 0) {
     const bool sgn = b == 1;
@@ -6453,8 +6503,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT >= 4 ? 3
       if (m < a.M) {
         const int r0 = red[0][e][lane] + red[1][e][lane] + red[2][e][lane] + red[3][e][lane];
         const int r1 = red[0][e + 1][lane] + red[1][e + 1][lane] + red[2][e + 1][lane] + red[3][e + 1][lane];
-        const int t0 = (r0 >> sh0) + add0;
-        const int t1 = S == 2 ? (r1 >> sh1) + add1 : 0;
+        int xsum = 0;
+        if (sgrp >= 0) {
+          const int r = lane & 15;
+          xsum = redx[0][m][r] + redx[1][m][r] + redx[2][m][r] + redx[3][m][r];
+        }
+        const int t0 = (r0 >> sh0) + add0 + (sgrp == 0 ? xsum : 0);
+        const int t1 = S == 2 ? (r1 >> sh1) + add1 + (sgrp == 1 ? xsum : 0) : 0;
         if (a.acc) {
           a.acc[(int64_t)m * a.N + ci.n] = t0;
           if (S == 2) a.acc[(a.M + m) * a.N + ci.n] = t1;
@@ -6466,8 +6521,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT >= 4 ? 3
 }
 
 bool gemv_dense_fits(int64_t M, const ActPlan& ap) {
-  return M >= 1 && M <= 8 && M * (int64_t)ap.Kp <= 56 * 1024 &&
-         gemv_dense_xbytes64(ap) < ((int64_t)1 << 31);
+  const int64_t lds = M * (ap.Kp + 16) + 32 + M * (ap.Kp / 32) * 8;
+  return M >= 1 && M <= 8 && lds <= 64 * 1024 && gemv_dense_xbytes64(ap) < ((int64_t)1 << 31);
 }
 
 hipError_t launch_mp_gemv_dense(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
@@ -6479,7 +6534,8 @@ hipError_t launch_mp_gemv_dense(const uint8_t* act_packed, const float* s_a, con
   a.dense = dense;
   a.db_lo = b_lo;
   a.db_hi = b_hi;
-  const size_t lds = (size_t)M * (ap.Kp + 16) + 32;
+  // byte rows, 32 zero bytes, then two sign words per run and row
+  const size_t lds = (size_t)M * (ap.Kp + 16) + 32 + (size_t)M * (ap.Kp / 32) * 8;
   const dim3 grid((unsigned)wp.nblk);
   if (M == 1) hipLaunchKernelGGL(k_gemv_dense<1>, grid, dim3(256), lds, stream, a);
   else if (M == 2) hipLaunchKernelGGL(k_gemv_dense<2>, grid, dim3(256), lds, stream, a);

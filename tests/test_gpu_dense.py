@@ -42,6 +42,11 @@ CASES = [  # (M, N, K, a_lo, a_hi, w_lo, w_hi, a_signed)
     (1, 64, 256, 4, 8, 6, 6, True),      # one width
     (4, 100, 640, 4, 8, 4, 8, True),     # power-of-two widths through the dense path
     (1, 1000, 4096, 4, 8, 3, 6, True),   # a decode-like row
+    # sign weights against a sign activation group: XNOR-popcount runs
+    (1, 200, 1000, 1, 8, 1, 4, True),    # one row, beside an 8-bit group
+    (8, 160, 2048, 1, 4, 1, 2, True),    # eight rows
+    (3, 64, 700, 1, 1, 1, 1, True),      # sign x sign only, ragged K
+    (2, 48, 4160, 1, 8, 1, 6, True),     # K / 64 odd: half of the last quad-run past K
 ]
 
 

@@ -38,6 +38,7 @@ CONFIGS = {
     "decode_4096_m8": 44,
     "decode_11008_m1_w36": 45,
     "decode_11008_m8_w36": 46,
+    "decode_11008_m1_sign": 47,
     "square_8192": 5,
 }
 
@@ -197,6 +198,14 @@ def decode_11008_m8_w36() -> dict:
     return _decode_w36(8, 46, "decode_11008_m8_w36")
 
 
+def decode_11008_m1_sign() -> dict:
+    """Decode GEMV with sign (1-bit) channels on both sides: x[1,4096]
+    ~N(0,1), 75% 1b / 25% 4b signed; W[11008,4096] ~N(0,0.02), 75% 1b /
+    25% 4b (the sign x sign runs are XNOR-popcount products)."""
+    return generic(1, 11008, 4096, a_lo=1, a_hi=4, a_frac_lo=0.75, w_lo=1, w_hi=4,
+                   w_frac_lo=0.75, seed=BASE_SEED + 47, name="decode_11008_m1_sign")
+
+
 def square_8192(size: int = 8192) -> dict:
     """M = N = K = 8192, A ~N(0,1), W ~N(0,0.02), 50% 4b / 50% 8b on both
     operands with seeded interleaving."""
@@ -242,6 +251,7 @@ BUILDERS = {
     "decode_4096_m8": decode_4096_m8,
     "decode_11008_m1_w36": decode_11008_m1_w36,
     "decode_11008_m8_w36": decode_11008_m8_w36,
+    "decode_11008_m1_sign": decode_11008_m1_sign,
     "square_8192": square_8192,
     "xfmr_qkv_g512": xfmr_qkv_g512,
     "xfmr_ffn_down_g512": xfmr_ffn_down_g512,
