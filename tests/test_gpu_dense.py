@@ -93,3 +93,36 @@ def test_dense_rejects_other_copies():
         with pytest.raises(sq.SoniqError) as e:
             sq.soniq_pack_weights(W, case["w_bits"], case["a_bits"], True, dense=True, **kw)
         assert e.value.status == sq.SONIQ_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("name", ["decode_11008_m1_w36", "decode_11008_m8_w36", "decode_11008_m1_sign"])
+def test_dense_workload_full(name):
+    """The dense decode workloads at full size, as bench.py --dense runs
+    them (the same handles and entry points), compared in full."""
+    case = workloads.make(name)
+    print(f"[gpu] dense workload {name}", flush=True)
+    compare_full(run(case, True), oracle_run(case))
+
+
+@pytest.mark.parametrize("M", [1, 5])
+def test_dense_one_call_and_scratch(M):
+    """soniq_quantize_mp_gemm and the allocation-free entry point on a
+    dense handle (quantize, then the dense GEMV) give the two-call result."""
+    case = workloads.generic(M, 300, 1500, a_lo=4, a_hi=8, a_frac_lo=0.8, w_lo=3, w_hi=6,
+                             w_frac_lo=0.7, a_signed=True, seed=77 + M, name="dense_call")
+    print(f"[gpu] dense one-call M={M}", flush=True)
+    ref = run(case, True)
+    w = ref["w"]
+    A = torch.from_numpy(case["A"]).cuda()
+    act = sq.soniq_act_create(w, M)
+    for _ in range(2):
+        acc = torch.empty((w.S, M, case["N"]), dtype=torch.int32, device="cuda")
+        Y = sq.soniq_quantize_mp_gemm(act, w, A, acc=acc)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(acc.cpu().numpy(), ref["acc"])
+        np.testing.assert_array_equal(_bf16_bits(Y), ref["y"])
+        acc2 = torch.empty_like(acc)
+        Y2 = sq.soniq_quantize_mp_gemm_scratch(w, A, acc=acc2)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(acc2.cpu().numpy(), ref["acc"])
+        np.testing.assert_array_equal(_bf16_bits(Y2), ref["y"])
