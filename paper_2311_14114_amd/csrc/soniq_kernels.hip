@@ -593,7 +593,16 @@ __global__ __launch_bounds__(256) void k_act_rows(const float* __restrict__ A, i
                                                   uint8_t* __restrict__ ximg) {
   extern __shared__ __align__(16) uint8_t codes[];
   __shared__ float red[8];
-  const int64_t m0 = (int64_t)blockIdx.x * R;
+  // R = 4: the four workgroups of one 16-row block run on one XCD
+  // (workgroup i goes to XCD i mod 8), so its L2 joins their partial unit
+  // lines before they reach HBM; the grid is a multiple of 32 workgroups
+  int64_t wg = blockIdx.x;
+  if constexpr (R == 4) {
+    const int64_t x = wg & 7, j = wg >> 3;
+    wg = 4 * ((j >> 2) * 8 + x) + (j & 3);
+  }
+  const int64_t m0 = wg * R;
+  if (m0 >= M) return;
   const int rows = (int)min((int64_t)R, M - m0);
   const int tid = threadIdx.x;
   if constexpr (J > 0) {
@@ -5383,7 +5392,9 @@ hipError_t launch_act_quant(const float* A, int64_t M, int64_t K, int64_t lda,
   const int K4 = (int)(K / 4);
   const int J = (sign || !aligned) ? 0 : K4 <= 256 ? 1 : K4 <= 512 ? 2 : K4 <= 768 ? 3 : 4;
 #define SONIQ_ACT_ROWS(R_, J_)                                                                  \
-  hipLaunchKernelGGL((k_act_rows<R_, J_>), dim3((unsigned)((M + R_ - 1) / R_)), dim3(256),      \
+  hipLaunchKernelGGL((k_act_rows<R_, J_>),                                                      \
+                     dim3((unsigned)(R_ == 4 ? ((M + 127) / 128) * 32 : (M + R_ - 1) / R_)),    \
+                     dim3(256),                                                                 \
                      (size_t)R_ * ap.Kp, stream, A, M, K, lda, pos_dev, seg_dev, ap, partial,    \
                      nparts, s_a, packed, ximg)
   // whole 8- or 16-row block slices per workgroup for larger batches
