@@ -443,23 +443,28 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
  * Sec. 4 (quantization fused into the producing operation); codec items
  * 1-2 (the group max-abs scale over the batch).
  *
- *   act, w, Y_dev, ldy, acc_dev  as for soniq_mp_gemm (Y_dev not NULL).
- *   next     an activation handle of the next layer's weights (not a
- *            convolution's), whose K equals this layer's N; act's M must
- *            not exceed its max_M.
+ *   act, w, Y_dev, ldy, acc_dev  as for soniq_mp_gemm (Y_dev not NULL);
+ *            w may be an implicit convolution's weights (act then its
+ *            convolution handle).
+ *   next     an activation handle of the next layer's weights, whose K
+ *            equals this layer's N (act's M must not exceed its max_M), or
+ *            of a next implicit convolution with C = N (act's M output
+ *            pixels a batch of at most B of its H x W images).
  * On return (stream order) `next` holds exactly what
- * soniq_quantize_act(next, float(Y)) would leave (codes and scales): no
- * calibration, the fp32 copy of Y and the separate maximum pass are what
- * it saves.  Batches of more than 8 rows fold the maxima in the GEMM
- * tiles; smaller ones run the GEMV forms and reduce them in the quantizer.
+ * soniq_quantize_act(next, float(Y)) would leave (codes and scales; for a
+ * next convolution what soniq_quantize_act_conv3x3 would leave from Y as
+ * its NHWC input): no calibration, the fp32 copy of Y and the separate
+ * maximum pass are what it saves.  Batches of more than 8 rows (and every
+ * convolution producer) fold the maxima in the GEMM tiles; smaller ones
+ * run the GEMV forms and reduce them in the quantizer.
  * The first call with a given (weights, next) pair allocates as
  * soniq_mp_gemm_quantize_next does (the same table), synchronously; make it
  * before capturing the call in a HIP graph.  The tiles' maxima sit beside
  * the pair's table, so calls with the same pair must not overlap.
  * Errors: INVALID_ARGUMENT (null, next == act, mismatched handles or
- * sizes), UNSUPPORTED (implicit-convolution weights or weights packed with
- * sub-group scales on either side, more tiles than one launch takes),
- * OUT_OF_MEMORY, HIP.
+ * sizes), UNSUPPORTED (weights packed with sub-group scales on either
+ * side, an implicit convolution whose widths have no kernel, more tiles
+ * than one launch takes), OUT_OF_MEMORY, HIP.
  */
 soniq_status soniq_mp_gemm_quantize_next_max(soniq_act act, soniq_weights w, soniq_act next,
                                              uint16_t* Y_dev, int64_t ldy, int32_t* acc_dev,

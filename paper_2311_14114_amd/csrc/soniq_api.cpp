@@ -1131,6 +1131,27 @@ static int64_t qn_cols(const soniq_act_s& a) {
   return a.w->conv ? a.cg.cpad[0] + (a.ap.S == 2 ? a.cg.cpad[1] : 0) : a.ap.Kp;
 }
 
+// Words of a pair's table taken by the tiles' maxima of a full batch.
+static size_t qn_ymax_words(const soniq_act_s& next, const soniq_weights_s& w) {
+  return 2 * (size_t)((next.M_alloc + 63) / 64) * (size_t)(w.wp.Np / kGemmBN);
+}
+
+// The next-convolution description of a producer's M output pixels.
+static QnConv qn_conv(const soniq_act_s& next, const soniq_weights_s& w, int64_t M) {
+  QnConv qc{};
+  const soniq_weights w2 = next.w;
+  qc.cg = next.cg;
+  qc.img = next.img;
+  qc.B = (int)(M / ((int64_t)next.cg.H * next.cg.W));
+  for (int64_t n = 0; n < w.N; ++n) qc.cnt[w2->kp.seg[9 * n]]++;
+  for (int g = 0; g < 2; ++g) {
+    // the stored code of 0.0: +1 in a sign group, else 0, less the zero point
+    const int code0 = next.ap.q[g].sign1 ? 1 : 0;
+    qc.halo[g] = code0 - next.ap.zp[g];
+  }
+  return qc;
+}
+
 // First use of a (producer weights, next) pair: next's code image and the
 // producer's column table, built synchronously (later calls find both).
 static soniq_status qn_prepare(soniq_act next, soniq_weights w, const char* who, int32_t** out) {
@@ -1187,11 +1208,15 @@ static soniq_status qn_prepare(soniq_act next, soniq_weights w, const char* who,
       for (size_t r = 0; r < cols[t].size(); ++r) tab[Np + t * kGemmBN + r] = npos[cols[t][r]];
     }
     // followed by one pair of floats per GEMM tile of a full batch: the
-    // tiles' maxima of the two-pass form (soniq_mp_gemm_quantize_next_max)
-    const size_t ymax_words = 2 * (size_t)(next->M_alloc / 64) * (size_t)(Np / kGemmBN);
+    // tiles' maxima of the two-pass form (soniq_mp_gemm_quantize_next_max),
+    // then the next-layer position of each input channel n (npos)
+    const size_t ymax_words = qn_ymax_words(*next, *w);
     int32_t* t = nullptr;
-    HIP_TRY(dev_alloc(&t, tab.size() + ymax_words));
-    const hipError_t e = hipMemcpy(t, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    HIP_TRY(dev_alloc(&t, tab.size() + ymax_words + (size_t)w->N));
+    hipError_t e = hipMemcpy(t, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(t + tab.size() + ymax_words, npos.data(), npos.size() * sizeof(int32_t),
+                    hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       (void)hipFree(t);
       return fail_hip(e, (std::string(who) + ": hipMemcpy").c_str());
@@ -1260,17 +1285,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   }
   float s2[2] = {s_next[0], w2->kp.S == 2 ? s_next[1] : 0.0f};
   QnConv qc{};
-  if (conv_next) {
-    qc.cg = next->cg;
-    qc.img = next->img;
-    qc.B = (int)(M / ((int64_t)next->cg.H * next->cg.W));
-    for (int64_t n = 0; n < w->N; ++n) qc.cnt[w2->kp.seg[9 * n]]++;
-    for (int g = 0; g < 2; ++g) {
-      // the stored code of 0.0: +1 in a sign group, else 0, less the zero point
-      const int code0 = next->ap.q[g].sign1 ? 1 : 0;
-      qc.halo[g] = code0 - next->ap.zp[g];
-    }
-  }
+  if (conv_next) qc = qn_conv(*next, *w, M);
   HIP_TRY(launch_mp_gemm_qnext(w->conv ? nullptr : act->packed, act->s_a, act->ap, w->dev(), w->wp,
                                M, w->N, Y_dev, ldy, acc_dev, next->qn_img, next->M_alloc, qn_tab,
                                next->ap, w2->act_group_bits ? s_next : s2, next->s_a, next->qn_brs,
@@ -1294,17 +1309,25 @@ soniq_status soniq_mp_gemm_quantize_next_max(soniq_act act, soniq_weights w, son
   if (next == act)
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: next is the producer's own activation handle", who);
   const soniq_weights w2 = next->w;
-  if (w->conv || w2->conv)
-    return fail(SONIQ_ERR_UNSUPPORTED, "%s: implicit-convolution weights", who);
+  const bool conv_next = w2->conv;
+  if (w->conv && !conv_gemm_supported(act->ap, w->wp))
+    return fail(SONIQ_ERR_UNSUPPORTED, "%s: no implicit-convolution kernel for these widths", who);
   if (w->act_group_bits || w2->act_group_bits)
     return fail(SONIQ_ERR_UNSUPPORTED, "%s: weights packed with sub-group activation scales", who);
-  if (w2->K != w->N)
-    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: next layer has K=%lld, this layer N=%lld", who,
-                (long long)w2->K, (long long)w->N);
+  const int64_t K2 = conv_next ? w2->C : w2->K;
+  if (K2 != w->N)
+    return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: next layer has %lld input channels, this layer N=%lld",
+                who, (long long)K2, (long long)w->N);
   const int64_t M = act->M;
-  if (M > next->max_M)
+  if (conv_next) {
+    const int64_t hw = (int64_t)next->cg.H * next->cg.W;
+    if (M % hw != 0 || M / hw > next->cg.B)
+      return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: M=%lld is not a batch of at most %d images of %dx%d",
+                  who, (long long)M, next->cg.B, next->cg.H, next->cg.W);
+  } else if (M > next->max_M) {
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: M=%lld > next max_M=%lld", who, (long long)M,
                 (long long)next->max_M);
+  }
   if (ldy < w->N) return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: ldy < N", who);
   if (((M + 63) / 64) * (w->wp.Np / kGemmBN) > 0x7FFFFFFFLL)
     return fail(SONIQ_ERR_UNSUPPORTED, "%s: problem too large for one launch", who);
@@ -1316,19 +1339,29 @@ soniq_status soniq_mp_gemm_quantize_next_max(soniq_act act, soniq_weights w, son
   }
   // the tiles' maxima, after the pair's column table
   float* ymax = reinterpret_cast<float*>(qn_tab + 3 * (size_t)w->wp.Np);
+  const int32_t* posn = qn_tab + 3 * (size_t)w->wp.Np + qn_ymax_words(*next, *w);
   int nslot = 0;
-  if (M <= 8) {
+  if (M <= 8 && !w->conv) {
     // the GEMV forms store Y; the quantizer reduces the small batch's maxima
     const soniq_status rc = run_gemm(*act, Y_dev, ldy, acc_dev, st);
     if (rc != SONIQ_OK) return rc;
   } else {
-    HIP_TRY(launch_mp_gemm_ymax(act->packed, act->s_a, act->ap, w->dev(), w->wp, M, w->N, Y_dev, ldy,
-                                acc_dev, qn_tab, ymax, st));
+    HIP_TRY(launch_mp_gemm_ymax(w->conv ? nullptr : act->packed, act->s_a, act->ap, w->dev(), w->wp,
+                                M, w->N, Y_dev, ldy, acc_dev, qn_tab, ymax, st,
+                                w->conv ? act->img : nullptr, w->conv ? &act->cg : nullptr));
     nslot = (int)(((M + 63) / 64) * (w->wp.Np / kGemmBN));
   }
-  HIP_TRY(launch_act_bf16(Y_dev, M, w2->K, ldy, next->ap, w2->pos, w2->seg, ymax, nslot, next->s_a,
-                          next->packed, next->ximg, st));
-  next->ximg_ok = M == 1 && next->ximg != nullptr;
+  if (conv_next) {
+    // the blocked byte image the tiles' epilogue would write, then the
+    // convolution's haloed code image
+    HIP_TRY(launch_img_bf16(Y_dev, M, (int)w->N, ldy, posn, next->ap, qn_conv(*next, *w, M), ymax,
+                            nslot, next->s_a, next->qn_img, st));
+    next->ximg_ok = false;
+  } else {
+    HIP_TRY(launch_act_bf16(Y_dev, M, w2->K, ldy, next->ap, w2->pos, w2->seg, ymax, nslot,
+                            next->s_a, next->packed, next->ximg, st));
+    next->ximg_ok = M == 1 && next->ximg != nullptr;
+  }
   next->M = M;
   return SONIQ_OK;
 }

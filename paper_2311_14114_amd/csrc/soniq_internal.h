@@ -316,14 +316,23 @@ hipError_t launch_conv_img(const float* X, int64_t B, int64_t C, int64_t H, int6
 // launch_act_bf16 quantizes the next layer's activations from the stored
 // bf16 Y exactly as launch_act_quant would from float(Y), with the maxima
 // of nslot pairs (nslot = 0: reduced from the batch itself).
+// (pimg, pcg: an implicit convolution's code image and geometry as the
+// producer's input.)
 hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                int64_t ldy, int32_t* acc, const int32_t* qtab, float* slots,
-                               hipStream_t stream);
+                               hipStream_t stream, const uint8_t* pimg = nullptr,
+                               const ConvGeo* pcg = nullptr);
 hipError_t launch_act_bf16(const uint16_t* Y, int64_t M, int64_t K, int64_t ldy, const ActPlan& ap,
                            const int32_t* pos_dev, const uint8_t* seg_dev, const float* slots,
                            int nslot, float* s_a, uint8_t* packed, uint8_t* ximg,
                            hipStream_t stream);
+// The same into a next implicit convolution (ap and conv describe it): the
+// blocked byte image bimg from Y with posn (each of the N producer
+// columns' rank-space position), then its haloed code image conv.img.
+hipError_t launch_img_bf16(const uint16_t* Y, int64_t M, int N, int64_t ldy, const int32_t* posn,
+                           const ActPlan& ap, const QnConv& conv, const float* slots, int nslot,
+                           float* s_a, uint8_t* bimg, hipStream_t stream);
 
 bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp);
 hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,

@@ -722,6 +722,63 @@ __global__ __launch_bounds__(256) void k_act_bf16(const uint16_t* __restrict__ Y
   write_act_units(codes, rows, m0, ap, packed, ximg);
 }
 
+// The two-pass form into a next convolution: its byte image (blocked: row
+// m, rank-space position p at (m/16)*16*Cp + 16p + m%16, as the GEMM tiles'
+// epilogue writes it) from the stored bf16 Y, with each group's maximum
+// from nslot tile pairs (nslot = 0: reduced from the whole batch).  posn
+// gives each producer column's position in rank space (group 1 from
+// cpad0).  Workgroup b quantizes 16-row block b into LDS (rank-major, 16
+// rows a position) with the arithmetic of soniq_quantize_act, then writes
+// the block's 16*Cp bytes; workgroup 0 also stores the scales.  Dynamic
+// LDS: 16 * Cp bytes.
+__global__ __launch_bounds__(256) void k_img_bf16(const uint16_t* __restrict__ Y, int64_t M, int N,
+                                                  int64_t ldy, const int32_t* __restrict__ posn,
+                                                  int cpad0, int Cp, ActPlan ap,
+                                                  const float* __restrict__ slots, int nslot,
+                                                  float* __restrict__ s_a_out,
+                                                  uint8_t* __restrict__ bimg) {
+  extern __shared__ __align__(16) uint8_t codes[];
+  __shared__ float red[8];
+  const int64_t m0 = (int64_t)blockIdx.x * kBlk;
+  const int rows = (int)min((int64_t)kBlk, M - m0);
+  const int tid = threadIdx.x;
+  float r0 = 0.0f, r1 = 0.0f;
+  if (nslot > 0) {
+    for (int b = tid; b < nslot; b += 256) {
+      const float2 v = reinterpret_cast<const float2*>(slots)[b];
+      r0 = fmaxf(r0, v.x);
+      r1 = fmaxf(r1, v.y);
+    }
+  } else {
+    for (int64_t i = tid; i < M * N; i += 256) {
+      const int64_t m = i / N;
+      const int n = (int)(i - m * N);
+      const float a = fabsf(__uint_as_float((uint32_t)Y[m * ldy + n] << 16));
+      if (posn[n] >= cpad0) r1 = fmaxf(r1, a); else r0 = fmaxf(r0, a);
+    }
+  }
+  const float2 rr = block_max2(make_float2(r0, r1), red);
+  const float s0 = group_scale(rr.x, ap.q[0]);
+  const float s1 = ap.S == 2 ? group_scale(rr.y, ap.q[1]) : 0.0f;
+  if (blockIdx.x == 0 && tid == 0) {
+    s_a_out[0] = s0;
+    s_a_out[1] = s1;
+  }
+  const ActQ aq = make_actq(ap, s0, s1);
+  uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
+  for (int i = tid; i < 4 * Cp; i += 256) codes32[i] = 0;
+  __syncthreads();
+  for (int i = tid; i < rows * N; i += 256) {
+    const int r = i / N, n = i - r * N;
+    const int p = posn[n];
+    codes[16 * p + r] =
+        store_code(__uint_as_float((uint32_t)Y[(m0 + r) * ldy + n] << 16), p >= cpad0 ? 1 : 0, aq);
+  }
+  __syncthreads();
+  uint4* dst = reinterpret_cast<uint4*>(bimg + (m0 / kBlk) * (int64_t)kBlk * Cp);
+  for (int i = tid; i < Cp; i += 256) dst[i] = reinterpret_cast<const uint4*>(codes)[i];
+}
+
 // One group's units of a 16-row block whose stored codes sit in LDS (row r
 // at codes + r*ldc + gbase): granule q holds units l = kg*16 + r of 2C bytes
 // (128C contiguous bytes); 16-byte piece w holds units w*U .. w*U+U-1
@@ -5725,17 +5782,36 @@ static void launch_gemm_ymax_t(const GemmArgs& a, int64_t M, hipStream_t stream)
                      dim3(256), 0, stream, a);
 }
 
+// The same for the implicit convolution's tiles.
+template <int CBL, int CBH>
+static void launch_gemm_ymax_conv_t(const GemmArgs& a, int64_t M, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  hipLaunchKernelGGL((k_gemm<2, 4, 8, CBL, CBH, 2, 2, 3, false, true>),
+                     dim3((unsigned)(((M + 63) / 64) * ntn)), dim3(256), 0, stream, a);
+}
+
 hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, const ActPlan& ap,
                                const WDev& wd, const WPlan& wp, int64_t M, int64_t N, uint16_t* Y,
                                int64_t ldy, int32_t* acc, const int32_t* qtab, float* slots,
-                               hipStream_t stream) {
+                               hipStream_t stream, const uint8_t* pimg, const ConvGeo* pcg) {
   if (ap.gsub[0] > 0) return hipErrorInvalidValue;
+  if (pimg && !conv_gemm_supported(ap, wp)) return hipErrorInvalidValue;
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
-  a.xcd_tiles = tiles <= 2048;
   a.qn_tab = qtab;
   a.qn_max = slots;
   const int cl = wp.c_lo, ch = wp.c_hi;
+  if (pimg) {
+    a.img = pimg;
+    a.cg = *pcg;
+    if (cl == 4 && ch == 4) launch_gemm_ymax_conv_t<4, 4>(a, M, stream);
+    else if (cl == 1 && ch == 4) launch_gemm_ymax_conv_t<1, 4>(a, M, stream);
+    else if (cl == 2 && ch == 4) launch_gemm_ymax_conv_t<2, 4>(a, M, stream);
+    else if (cl == 2 && ch == 8) launch_gemm_ymax_conv_t<2, 8>(a, M, stream);
+    else launch_gemm_ymax_conv_t<4, 8>(a, M, stream);
+    return hipGetLastError();
+  }
+  a.xcd_tiles = tiles <= 2048;
   if (ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8) {
     if (cl == 4 && ch == 8) launch_gemm_ymax_t<2, 4, 8, 4, 8>(a, M, stream);
     else if (cl == 2 && ch == 8) launch_gemm_ymax_t<2, 4, 8, 2, 8>(a, M, stream);
@@ -5747,6 +5823,25 @@ hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, cons
   } else {
     launch_gemm_ymax_t<1, 0, 0, 0, 0>(a, M, stream);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_img_bf16(const uint16_t* Y, int64_t M, int N, int64_t ldy, const int32_t* posn,
+                           const ActPlan& ap, const QnConv& conv, const float* slots, int nslot,
+                           float* s_a, uint8_t* bimg, hipStream_t stream) {
+  const int cpad0 = conv.cg.cpad[0];
+  const int Cp = cpad0 + (ap.S == 2 ? conv.cg.cpad[1] : 0);
+  if (M < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_img_bf16, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256), (size_t)kBlk * Cp,
+                     stream, Y, M, N, ldy, posn, cpad0, Cp, ap, slots, nslot, s_a, bimg);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // then the convolution's haloed image from the blocked byte image (the
+  // scales are stored above)
+  hipLaunchKernelGGL(k_pack_conv_img, dim3((unsigned)((M + kBlk - 1) / kBlk)), dim3(256),
+                     (size_t)kBlk * Cp, stream, bimg, (int64_t)kBlk * Cp, true, M, conv.B, conv.cnt[0],
+                     conv.cnt[1], conv.halo[0], conv.halo[1], ap, conv.cg, 0.0f, 0.0f, nullptr,
+                     conv.img);
   return hipGetLastError();
 }
 

@@ -530,6 +530,66 @@ def test_chain_batch_max(c):
     np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2, s_w2))
 
 
+def conv_chain_max(B, C1, H, W, N1, N2, a1, w1, a2, w2, a2_signed, implicit1, seed):
+    """The two-pass form into a next convolution: layer 1 (implicit, or a
+    GEMM on its lowered matrix) stores Y and folds its tiles' maxima, then
+    layer 2's haloed code image is quantized from the stored bf16 Y with the
+    batch maximum.  Against the oracle's quantize_act of the lowering of
+    float(Y) (the lowering's zeros change no maximum), layer 2's
+    accumulators and outputs, and the unfused form on the GPU
+    (soniq_quantize_act_conv3x3 of float(Y) as NCHW)."""
+    l1 = workloads.conv3x3(B, C1, H, W, N1, a_lo=a1[0], a_hi=a1[1], a_frac_lo=0.6, w_lo=w1[0],
+                           w_hi=w1[1], w_frac_lo=0.7, a_signed=False, seed=seed)
+    l2 = workloads.conv3x3(B, N1, H, W, N2, a_lo=a2[0], a_hi=a2[1], a_frac_lo=0.6, w_lo=w2[0],
+                           w_hi=w2[1], w_frac_lo=0.5, a_signed=a2_signed, seed=seed + 1)
+    M = B * H * W
+    print(f"[gpu] conv batch-max chain B={B} C1={C1} {H}x{W} N1={N1} N2={N2} a2={a2} "
+          f"signed={a2_signed} implicit={implicit1}", flush=True)
+    r1 = oracle.run(l1["A"], l1["W"], l1["a_bits"], l1["w_bits"], False)
+    Y1f = bf16_to_f32(r1["y_replay"])  # [M, N1], rows (b, y, x)
+    X2 = np.ascontiguousarray(Y1f.reshape(B, H, W, N1).transpose(0, 3, 1, 2))
+    A2 = workloads.im2col_3x3(X2)
+    q2, s2, _, _ = oracle.quantize_act(A2, l2["a_bits"], a2_signed)
+    q_w2, s_w2 = oracle.quantize_weights(l2["W"], l2["w_bits"])
+    S2, _, seg_of2 = oracle.segments(l2["a_bits"])
+    acc2 = oracle.mac(q2, q_w2, seg_of2, S2)
+    if implicit1:
+        W1 = torch.from_numpy(np.ascontiguousarray(l1["W"].reshape(N1, C1, 3, 3))).cuda()
+        wh1 = sq.soniq_pack_weights_conv3x3(W1, l1["w_bits"], l1["a_bits"][::9], False)
+        act1 = sq.soniq_act_create_conv3x3(wh1, B, H, W)
+        sq.soniq_quantize_act_conv3x3(act1, torch.from_numpy(l1["X"]).cuda())
+    else:
+        wh1 = sq.soniq_pack_weights(torch.from_numpy(l1["W"]).cuda(), l1["w_bits"], l1["a_bits"], False)
+        act1 = sq.soniq_act_create(wh1, M)
+        sq.soniq_quantize_act(act1, torch.from_numpy(l1["A"]).cuda())
+    W2 = torch.from_numpy(np.ascontiguousarray(l2["W"].reshape(N2, N1, 3, 3))).cuda()
+    wh2 = sq.soniq_pack_weights_conv3x3(W2, l2["w_bits"], l2["a_bits"][::9], a2_signed)
+    act2 = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    ref = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    for _ in range(2):  # the second call reuses the pair's table and image
+        Y1 = sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2)
+        acc = torch.empty((S2, M, N2), dtype=torch.int32, device="cuda")
+        Y2 = sq.soniq_mp_gemm(act2, wh2, acc=acc)
+        Xg = Y1.float().reshape(B, H, W, N1).permute(0, 3, 1, 2).contiguous()
+        sq.soniq_quantize_act_conv3x3(ref, Xg)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(_bf16_bits(Y1), r1["y_replay"])
+        g_q2, g_s2 = sq.soniq_act_unpack_debug(act2)
+        r_q2, r_s2 = sq.soniq_act_unpack_debug(ref)
+        np.testing.assert_array_equal(g_s2, s2[:S2])
+        np.testing.assert_array_equal(g_q2, q2)
+        np.testing.assert_array_equal(g_s2, r_s2)
+        np.testing.assert_array_equal(g_q2, r_q2)
+        np.testing.assert_array_equal(acc.cpu().numpy(), acc2)
+        np.testing.assert_array_equal(_bf16_bits(Y2), oracle.epilogue_replay(acc2, s2[:S2], s_w2))
+
+
+@pytest.mark.parametrize("c", CONV_CHAINS,
+                         ids=lambda c: f"B{c[0]}_C{c[1]}_{c[2]}x{c[3]}_N{c[4]}_{'impl' if c[11] else 'gemm'}")
+def test_conv_chain_batch_max(c):
+    conv_chain_max(*c, seed=sum(c[:6]) + 11)
+
+
 def test_chain_batch_max_repeats_and_graph():
     """Repeated calls (the slots are cleared each time, a smaller batch
     second), then the call captured in a HIP graph and replayed three times
