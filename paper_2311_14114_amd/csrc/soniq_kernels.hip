@@ -728,8 +728,9 @@ __global__ __launch_bounds__(256) void k_act_bf16(const uint16_t* __restrict__ Y
 // from nslot tile pairs (nslot = 0: reduced from the whole batch).  posn
 // gives each producer column's position in rank space (group 1 from
 // cpad0).  Workgroup b quantizes 16-row block b into LDS (rank-major, 16
-// rows a position) with the arithmetic of soniq_quantize_act, then writes
-// the block's 16*Cp bytes; workgroup 0 also stores the scales.  Dynamic
+// rows a position: one thread a channel) with the arithmetic of
+// soniq_quantize_act, then writes the block's 16*Cp bytes; workgroup 0
+// also stores the scales.  Dynamic
 // LDS: 16 * Cp bytes.
 __global__ __launch_bounds__(256) void k_img_bf16(const uint16_t* __restrict__ Y, int64_t M, int N,
                                                   int64_t ldy, const int32_t* __restrict__ posn,
@@ -768,11 +769,21 @@ __global__ __launch_bounds__(256) void k_img_bf16(const uint16_t* __restrict__ Y
   uint32_t* codes32 = reinterpret_cast<uint32_t*>(codes);
   for (int i = tid; i < 4 * Cp; i += 256) codes32[i] = 0;
   __syncthreads();
-  for (int i = tid; i < rows * N; i += 256) {
-    const int r = i / N, n = i - r * N;
+  // thread n takes channel n: its 16 rows' values (each row's loads
+  // coalesced across the threads), their codes as one 16-byte position
+  for (int n = tid; n < N; n += 256) {
     const int p = posn[n];
-    codes[16 * p + r] =
-        store_code(__uint_as_float((uint32_t)Y[(m0 + r) * ldy + n] << 16), p >= cpad0 ? 1 : 0, aq);
+    const int g = p >= cpad0 ? 1 : 0;
+    uint32_t yv[kBlk];
+#pragma unroll
+    for (int r = 0; r < kBlk; ++r) yv[r] = Y[(m0 + min(r, rows - 1)) * ldy + n];
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int r = 0; r < kBlk; ++r) {
+      const uint32_t c = r < rows ? store_code(__uint_as_float(yv[r] << 16), g, aq) : 0u;
+      w[r >> 2] |= c << (8 * (r & 3));
+    }
+    *reinterpret_cast<uint4*>(codes + 16 * p) = make_uint4(w[0], w[1], w[2], w[3]);
   }
   __syncthreads();
   uint4* dst = reinterpret_cast<uint4*>(bimg + (m0 / kBlk) * (int64_t)kBlk * Cp);
