@@ -666,17 +666,50 @@ __global__ __launch_bounds__(256) void k_act_bf16(const uint16_t* __restrict__ Y
   const int64_t m0 = (int64_t)blockIdx.x * R;
   const int rows = (int)min((int64_t)R, M - m0);
   const int tid = threadIdx.x;
+  // the first batch of the rows' values is loaded before the maxima are
+  // reduced, so the two latencies overlap
+  constexpr int JJ = J > 0 ? J : 1;
+  const int K4 = (int)(K / 4);
+  int4 p[JJ];
+  uchar4 g[JJ];
+  float4 v[R][JJ];
+  auto load = [&](int base) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < JJ; ++j) {
+      const int k4 = min(base + 256 * j, K4 - 1);
+      p[j] = reinterpret_cast<const int4*>(pos)[k4];
+      g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
+#pragma unroll
+      for (int r = 0; r < R; ++r) v[r][j] = bf16x4(Y + (m0 + min(r, rows - 1)) * ldy + 4 * k4);
+    }
+  };
+  if constexpr (J > 0) load(tid);
   float r0 = 0.0f, r1 = 0.0f;
   if (nslot > 0) {
     for (int b = tid; b < nslot; b += 256) {
-      const float2 v = reinterpret_cast<const float2*>(slots)[b];
-      r0 = fmaxf(r0, v.x);
-      r1 = fmaxf(r1, v.y);
+      const float2 sv = reinterpret_cast<const float2*>(slots)[b];
+      r0 = fmaxf(r0, sv.x);
+      r1 = fmaxf(r1, sv.y);
     }
   } else if (J > 0) {
+    // the whole (small) batch: eight loads in flight per thread, then their
+    // maxima (a clamped repeat changes no maximum)
     const uchar4* s4 = reinterpret_cast<const uchar4*>(seg);
-    for (int64_t m = 0; m < M; ++m)
-      for (int k4 = tid; k4 < (int)(K / 4); k4 += 256) max4(bf16x4(Y + m * ldy + 4 * k4), s4[k4], r0, r1);
+    const int64_t tot = M * K4;
+    for (int64_t f0 = tid; f0 < tot; f0 += 256 * 8) {
+      float4 yv[8];
+      uchar4 sv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t f = min(f0 + 256 * u, tot - 1);
+        const int64_t m = f / K4;
+        const int k4 = (int)(f - m * K4);
+        yv[u] = bf16x4(Y + m * ldy + 4 * k4);
+        sv[u] = s4[k4];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) max4(yv[u], sv[u], r0, r1);
+    }
   } else {
     for (int64_t m = 0; m < M; ++m)
       for (int64_t k = tid; k < K; k += 256) {
@@ -696,19 +729,8 @@ __global__ __launch_bounds__(256) void k_act_bf16(const uint16_t* __restrict__ Y
   __syncthreads();
   if constexpr (J > 0) {
     const QElem q0 = qelem(s0, ap.q[0], ap.zp[0]), q1 = qelem(s1, ap.q[1], ap.zp[1]);
-    const int K4 = (int)(K / 4);
     for (int base = tid; base < K4; base += 256 * J) {
-      int4 p[J];
-      uchar4 g[J];
-      float4 v[R][J];
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const int k4 = min(base + 256 * j, K4 - 1);
-        p[j] = reinterpret_cast<const int4*>(pos)[k4];
-        g[j] = reinterpret_cast<const uchar4*>(seg)[k4];
-#pragma unroll
-        for (int r = 0; r < R; ++r) v[r][j] = bf16x4(Y + (m0 + min(r, rows - 1)) * ldy + 4 * k4);
-      }
+      if (base != tid) load(base);
       act_rows_quant<R, J>(codes, ap.Kp, rows, K4, base, p, g, v, q0, q1);
     }
   } else {
