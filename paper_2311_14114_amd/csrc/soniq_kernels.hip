@@ -6172,15 +6172,21 @@ __global__ __launch_bounds__(256) void k_conv_img(const float* __restrict__ X, i
     const int b = hp / HPi, rem = hp - b * HPi;
     const int yh = rem / Wp, xh = rem - yh * Wp;
     const bool halo = yh == 0 || yh == H + 1 || xh == 0 || xh == W + 1;
+    // every load unconditional and in bounds (a halo pixel or a padding
+    // rank reads pixel (0, 0) of channel 0 and discards it), so all 16 are
+    // in flight at once
+    const int64_t pix = halo ? 0 : (int64_t)(yh - 1) * W + (xh - 1);
+    int cc[16];
+    float xv[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) cc[e] = chan[g * cg.chan_ld + 16 * u + e];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) xv[e] = X[((int64_t)b * C + max(cc[e], 0)) * H * W + pix];
     uint32_t d[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const int c = chan[g * cg.chan_ld + 16 * u + e];
-      uint32_t byte = 0u;  // padding rank: stored 0
-      if (c >= 0) {
-        const float xv = halo ? 0.0f : X[(((int64_t)b * C + c) * H + (yh - 1)) * W + (xh - 1)];
-        byte = store_code(xv, g, aq);
-      }
+      // padding rank: stored 0; halo: the code of 0.0
+      const uint32_t byte = cc[e] < 0 ? 0u : store_code(halo ? 0.0f : xv[e], g, aq);
       d[e >> 2] |= byte << (8 * (e & 3));
     }
     const int c = ap.c[g];
