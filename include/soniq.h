@@ -206,9 +206,10 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
  * those of soniq_pack_weights on the lowered weights: the same codes and
  * scales (soniq_weights_unpack_debug returns them in the k = c*9 + t order)
  * and, through soniq_mp_gemm, the same accumulators and outputs.
- * This build has instances for 4- and 8-bit activation containers (two
- * widths) and weight containers 4/4, 1/4, 2/4, 2/8 and 4/8; UNSUPPORTED
- * otherwise.  Activation handles: soniq_act_create_conv3x3.
+ * The implicit convolution takes 4- and 8-bit activation containers (two
+ * widths: one of at most 4 bits, one of 5 to 8) and any pair of weight
+ * containers; UNSUPPORTED otherwise.  Activation handles:
+ * soniq_act_create_conv3x3.
  * Errors: those of soniq_pack_weights, UNSUPPORTED.
  */
 soniq_status soniq_pack_weights_conv3x3(const float* W_dev, int64_t N, int64_t C,

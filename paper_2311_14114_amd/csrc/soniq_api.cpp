@@ -796,7 +796,7 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
       free_weights(w);
       return fail(SONIQ_ERR_UNSUPPORTED,
                   "soniq_pack_weights_conv3x3: the implicit convolution takes 4- and 8-bit "
-                  "activation containers and weight containers 4/4, 1/4, 2/4, 2/8 or 4/8");
+                  "activation containers (two widths)");
     }
     // rank -> original channel, per group (the image quantizer's gather)
     w->conv = true;

@@ -5733,6 +5733,11 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
     else if (cl == 1 && ch == 4) launch_gemm_qn_conv_t<1, 4>(a, M, stream);
     else if (cl == 2 && ch == 4) launch_gemm_qn_conv_t<2, 4>(a, M, stream);
     else if (cl == 2 && ch == 8) launch_gemm_qn_conv_t<2, 8>(a, M, stream);
+    else if (cl == 8 && ch == 8) launch_gemm_qn_conv_t<8, 8>(a, M, stream);
+    else if (cl == 1 && ch == 8) launch_gemm_qn_conv_t<1, 8>(a, M, stream);
+    else if (cl == 2 && ch == 2) launch_gemm_qn_conv_t<2, 2>(a, M, stream);
+    else if (cl == 1 && ch == 2) launch_gemm_qn_conv_t<1, 2>(a, M, stream);
+    else if (cl == 1 && ch == 1) launch_gemm_qn_conv_t<1, 1>(a, M, stream);
     else launch_gemm_qn_conv_t<4, 8>(a, M, stream);
   } else if (gemv_form) {
     a.xs_bytes = (int)((gemv_lds(M, ap, wp) + 15) / 16 * 16);
@@ -5841,6 +5846,11 @@ hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, cons
     else if (cl == 1 && ch == 4) launch_gemm_ymax_conv_t<1, 4>(a, M, stream);
     else if (cl == 2 && ch == 4) launch_gemm_ymax_conv_t<2, 4>(a, M, stream);
     else if (cl == 2 && ch == 8) launch_gemm_ymax_conv_t<2, 8>(a, M, stream);
+    else if (cl == 8 && ch == 8) launch_gemm_ymax_conv_t<8, 8>(a, M, stream);
+    else if (cl == 1 && ch == 8) launch_gemm_ymax_conv_t<1, 8>(a, M, stream);
+    else if (cl == 2 && ch == 2) launch_gemm_ymax_conv_t<2, 2>(a, M, stream);
+    else if (cl == 1 && ch == 2) launch_gemm_ymax_conv_t<1, 2>(a, M, stream);
+    else if (cl == 1 && ch == 1) launch_gemm_ymax_conv_t<1, 1>(a, M, stream);
     else launch_gemm_ymax_conv_t<4, 8>(a, M, stream);
     return hipGetLastError();
   }
@@ -6227,8 +6237,8 @@ static void launch_gemm_conv_t(const GemmArgs& a, int64_t M, hipStream_t stream)
 bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp) {
   if (!(ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8)) return false;
   const int cl = wp.c_lo, ch = wp.c_hi;
-  return (cl == 4 && ch == 4) || (cl == 1 && ch == 4) || (cl == 2 && ch == 4) ||
-         (cl == 2 && ch == 8) || (cl == 4 && ch == 8);
+  // every pair of weight containers (c_lo <= c_hi)
+  return cl >= 1 && ch >= cl && ch <= 8 && (cl & (cl - 1)) == 0 && (ch & (ch - 1)) == 0;
 }
 
 hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,
@@ -6246,6 +6256,11 @@ hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const floa
   else if (cl == 1 && ch == 4) launch_gemm_conv_t<1, 4>(a, M, stream);
   else if (cl == 2 && ch == 4) launch_gemm_conv_t<2, 4>(a, M, stream);
   else if (cl == 2 && ch == 8) launch_gemm_conv_t<2, 8>(a, M, stream);
+  else if (cl == 8 && ch == 8) launch_gemm_conv_t<8, 8>(a, M, stream);
+  else if (cl == 1 && ch == 8) launch_gemm_conv_t<1, 8>(a, M, stream);
+  else if (cl == 2 && ch == 2) launch_gemm_conv_t<2, 2>(a, M, stream);
+  else if (cl == 1 && ch == 2) launch_gemm_conv_t<1, 2>(a, M, stream);
+  else if (cl == 1 && ch == 1) launch_gemm_conv_t<1, 1>(a, M, stream);
   else launch_gemm_conv_t<4, 8>(a, M, stream);
   return hipGetLastError();
 }

@@ -48,6 +48,12 @@ SMALL = [
     (4, 64, 8, 8, 128, 4, 8, 0.6, 4, 8, False, False), # several blocks per image
     (2, 33, 6, 9, 130, 4, 8, 0.5, 4, 4, True, False),  # odd channel counts, N past a tile
     (2, 3, 1, 70, 8, 4, 8, 0.5, 2, 4, False, False),   # one image row wider than a wave
+    # the other weight container pairs
+    (2, 16, 5, 7, 48, 4, 8, 0.6, 5, 8, False, False),  # 8/8: two widths in one container
+    (2, 16, 5, 7, 40, 4, 8, 0.6, 1, 7, True, False),   # 1/8
+    (1, 24, 6, 6, 33, 3, 6, 0.5, 2, 2, False, False),  # 2/2: one width
+    (2, 16, 4, 5, 40, 4, 8, 0.6, 1, 2, True, False),   # 1/2
+    (1, 16, 5, 5, 20, 4, 8, 0.6, 1, 1, False, False),  # 1/1: sign weights only
 ]
 
 
