@@ -631,3 +631,56 @@ def test_chain_batch_max_repeats_and_graph():
         g.replay()
         torch.cuda.synchronize()
         np.testing.assert_array_equal(_bf16_bits(Y2), eager)
+
+
+def test_conv_chain_batch_max_smaller_batch_and_graph():
+    """The two-pass form into a next convolution on handles made for three
+    images, called with three then two (the unfused form on the same
+    stored Y as reference), then captured in a HIP graph and replayed three
+    times with eager work between the replays, each against the eager
+    result."""
+    B, C1, H, W, N1, N2 = 3, 16, 6, 7, 32, 24
+    l1 = workloads.conv3x3(B, C1, H, W, N1, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=1, w_hi=4,
+                           w_frac_lo=0.7, a_signed=False, seed=301)
+    l2 = workloads.conv3x3(B, N1, H, W, N2, a_lo=4, a_hi=8, a_frac_lo=0.6, w_lo=2, w_hi=8,
+                           w_frac_lo=0.5, a_signed=True, seed=302)
+    W1 = torch.from_numpy(np.ascontiguousarray(l1["W"].reshape(N1, C1, 3, 3))).cuda()
+    wh1 = sq.soniq_pack_weights_conv3x3(W1, l1["w_bits"], l1["a_bits"][::9], False)
+    W2 = torch.from_numpy(np.ascontiguousarray(l2["W"].reshape(N2, N1, 3, 3))).cuda()
+    wh2 = sq.soniq_pack_weights_conv3x3(W2, l2["w_bits"], l2["a_bits"][::9], True)
+    act1 = sq.soniq_act_create_conv3x3(wh1, B, H, W)
+    act2 = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    ref = sq.soniq_act_create_conv3x3(wh2, B, H, W)
+    X = torch.from_numpy(l1["X"]).cuda()
+    for nb in (3, 2):
+        print(f"[gpu] conv batch-max on {nb} of {B} images", flush=True)
+        sq.soniq_quantize_act_conv3x3(act1, X[:nb].contiguous())
+        Y1 = sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2)
+        sq.soniq_quantize_act_conv3x3(ref, Y1.float().reshape(nb, H, W, N1).permute(0, 3, 1, 2).contiguous())
+        torch.cuda.synchronize()
+        g_q, g_s = sq.soniq_act_unpack_debug(act2)
+        r_q, r_s = sq.soniq_act_unpack_debug(ref)
+        np.testing.assert_array_equal(g_s, r_s)
+        np.testing.assert_array_equal(g_q, r_q)
+    Xg = X[:2].contiguous()
+    M = 2 * H * W
+    Yg = torch.empty((M, N1), dtype=torch.bfloat16, device="cuda")
+    Y2 = torch.empty((M, N2), dtype=torch.bfloat16, device="cuda")
+    sq.soniq_quantize_act_conv3x3(act1, Xg)
+    sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2, out=Yg)
+    sq.soniq_mp_gemm(act2, wh2, out=Y2)
+    torch.cuda.synchronize()
+    eager = _bf16_bits(Y2).copy()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(g, stream=s):
+        sq.soniq_quantize_act_conv3x3(act1, Xg, stream=s.cuda_stream)
+        sq.soniq_mp_gemm_quantize_next_max(act1, wh1, act2, out=Yg, stream=s.cuda_stream)
+        sq.soniq_mp_gemm(act2, wh2, out=Y2, stream=s.cuda_stream)
+    for _ in range(3):
+        Y2.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(_bf16_bits(Y2), eager)
