@@ -206,9 +206,11 @@ soniq_status soniq_pack_weights_grouped(const float* W_dev, int64_t N, int64_t K
  * those of soniq_pack_weights on the lowered weights: the same codes and
  * scales (soniq_weights_unpack_debug returns them in the k = c*9 + t order)
  * and, through soniq_mp_gemm, the same accumulators and outputs.
- * The implicit convolution takes 4- and 8-bit activation containers (two
- * widths: one of at most 4 bits, one of 5 to 8) and any pair of weight
- * containers; UNSUPPORTED otherwise.  Activation handles:
+ * The implicit convolution takes two activation widths in 4- and 8-bit
+ * containers (one of at most 4 bits, one of 5 to 8) or one width of 3 to
+ * 8 bits, and any pair of weight containers; UNSUPPORTED otherwise (the
+ * next-layer epilogues of soniq_mp_gemm_quantize_next(_max) from a
+ * convolution take the two-width plans only).  Activation handles:
  * soniq_act_create_conv3x3.
  * Errors: those of soniq_pack_weights, UNSUPPORTED.
  */

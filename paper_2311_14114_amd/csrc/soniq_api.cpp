@@ -795,8 +795,8 @@ soniq_status pack_impl(const float* W_dev, int64_t N, int64_t K, int64_t ldw,
     if (!conv_gemm_supported(make_act_plan(*w, kMAlign), w->wp)) {
       free_weights(w);
       return fail(SONIQ_ERR_UNSUPPORTED,
-                  "soniq_pack_weights_conv3x3: the implicit convolution takes 4- and 8-bit "
-                  "activation containers (two widths)");
+                  "soniq_pack_weights_conv3x3: the implicit convolution takes activation "
+                  "widths in 4- and 8-bit containers (two widths, or one of 3 to 8 bits)");
     }
     // rank -> original channel, per group (the image quantizer's gather)
     w->conv = true;
@@ -1245,7 +1245,7 @@ soniq_status soniq_mp_gemm_quantize_next(soniq_act act, soniq_weights w, soniq_a
   // an implicit convolution as the next layer: its input channels are this
   // layer's outputs, and this layer's rows its output pixels
   const bool conv_next = w2->conv;
-  if (w->conv && !conv_gemm_supported(act->ap, w->wp))
+  if (w->conv && !conv_gemm_qn_supported(act->ap, w->wp))
     return fail(SONIQ_ERR_UNSUPPORTED,
                 "soniq_mp_gemm_quantize_next: no implicit-convolution kernel for these widths");
   if (w->conv && w2->act_group_bits)
@@ -1310,7 +1310,7 @@ soniq_status soniq_mp_gemm_quantize_next_max(soniq_act act, soniq_weights w, son
     return fail(SONIQ_ERR_INVALID_ARGUMENT, "%s: next is the producer's own activation handle", who);
   const soniq_weights w2 = next->w;
   const bool conv_next = w2->conv;
-  if (w->conv && !conv_gemm_supported(act->ap, w->wp))
+  if (w->conv && !conv_gemm_qn_supported(act->ap, w->wp))
     return fail(SONIQ_ERR_UNSUPPORTED, "%s: no implicit-convolution kernel for these widths", who);
   if (w->act_group_bits || w2->act_group_bits)
     return fail(SONIQ_ERR_UNSUPPORTED, "%s: weights packed with sub-group activation scales", who);

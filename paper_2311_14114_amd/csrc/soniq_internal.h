@@ -334,7 +334,12 @@ hipError_t launch_img_bf16(const uint16_t* Y, int64_t M, int N, int64_t ldy, con
                            const ActPlan& ap, const QnConv& conv, const float* slots, int nslot,
                            float* s_a, uint8_t* bimg, hipStream_t stream);
 
+// The implicit convolution's tiles: two activation widths in 4- and 8-bit
+// containers, or one width in a 4- or 8-bit container; any pair of weight
+// containers.  The next-layer and batch-maximum epilogues from a
+// convolution take the two-width plans only (conv_gemm_qn_supported).
 bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp);
+bool conv_gemm_qn_supported(const ActPlan& ap, const WPlan& wp);
 hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,
                                const ActPlan& ap, const WDev& wd, const WPlan& wp, int64_t M,
                                int64_t N, uint16_t* Y, int64_t ldy, int32_t* acc,

@@ -5679,7 +5679,7 @@ hipError_t launch_mp_gemm_qnext(const uint8_t* act_packed, const float* s_a, con
                                 float* s_a2, float* brs2, uint8_t* packed2, hipStream_t stream,
                                 uint8_t* ximg2, const uint8_t* ximg, const uint8_t* pimg,
                                 const ConvGeo* pcg, const QnConv* conv) {
-  if (pimg && (!conv_gemm_supported(ap, wp) || ap2.gsub[0] > 0)) return hipErrorInvalidValue;
+  if (pimg && (!conv_gemm_qn_supported(ap, wp) || ap2.gsub[0] > 0)) return hipErrorInvalidValue;
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   if (pimg) {
     a.img = pimg;
@@ -5833,7 +5833,7 @@ hipError_t launch_mp_gemm_ymax(const uint8_t* act_packed, const float* s_a, cons
                                int64_t ldy, int32_t* acc, const int32_t* qtab, float* slots,
                                hipStream_t stream, const uint8_t* pimg, const ConvGeo* pcg) {
   if (ap.gsub[0] > 0) return hipErrorInvalidValue;
-  if (pimg && !conv_gemm_supported(ap, wp)) return hipErrorInvalidValue;
+  if (pimg && !conv_gemm_qn_supported(ap, wp)) return hipErrorInvalidValue;
   GemmArgs a = make_args(act_packed, s_a, ap, wd, wp, M, N, Y, ldy, acc);
   const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
   a.qn_tab = qtab;
@@ -6234,11 +6234,39 @@ static void launch_gemm_conv_t(const GemmArgs& a, int64_t M, hipStream_t stream)
                      dim3((unsigned)(((M + 63) / 64) * ntn)), dim3(256), 0, stream, a);
 }
 
-bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp) {
-  if (!(ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8)) return false;
+// One activation width in 4- or 8-bit containers: the tiles with S = 1.
+template <int CA>
+static void launch_gemm_conv1(const GemmArgs& a, int64_t M, hipStream_t stream) {
+  const int ntn = a.wp.Np / kGemmBN;
+  const dim3 grid((unsigned)(((M + 63) / 64) * ntn));
+  const int cl = a.wp.c_lo, ch = a.wp.c_hi;
+#define SONIQ_CONV1(L_, H_) hipLaunchKernelGGL((k_gemm<1, CA, 0, L_, H_, 2, 2, 0, false, true>), grid, dim3(256), 0, stream, a)
+  if (cl == 4 && ch == 4) SONIQ_CONV1(4, 4);
+  else if (cl == 1 && ch == 4) SONIQ_CONV1(1, 4);
+  else if (cl == 2 && ch == 4) SONIQ_CONV1(2, 4);
+  else if (cl == 2 && ch == 8) SONIQ_CONV1(2, 8);
+  else if (cl == 8 && ch == 8) SONIQ_CONV1(8, 8);
+  else if (cl == 1 && ch == 8) SONIQ_CONV1(1, 8);
+  else if (cl == 2 && ch == 2) SONIQ_CONV1(2, 2);
+  else if (cl == 1 && ch == 2) SONIQ_CONV1(1, 2);
+  else if (cl == 1 && ch == 1) SONIQ_CONV1(1, 1);
+  else SONIQ_CONV1(4, 8);
+#undef SONIQ_CONV1
+}
+
+// Every pair of weight containers (c_lo <= c_hi, powers of two up to 8).
+static bool conv_wpair_ok(const WPlan& wp) {
   const int cl = wp.c_lo, ch = wp.c_hi;
-  // every pair of weight containers (c_lo <= c_hi)
   return cl >= 1 && ch >= cl && ch <= 8 && (cl & (cl - 1)) == 0 && (ch & (ch - 1)) == 0;
+}
+
+bool conv_gemm_qn_supported(const ActPlan& ap, const WPlan& wp) {
+  return ap.S == 2 && ap.c[0] == 4 && ap.c[1] == 8 && conv_wpair_ok(wp);
+}
+
+bool conv_gemm_supported(const ActPlan& ap, const WPlan& wp) {
+  return conv_gemm_qn_supported(ap, wp) ||
+         (ap.S == 1 && (ap.c[0] == 4 || ap.c[0] == 8) && conv_wpair_ok(wp));
 }
 
 hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const float* s_a,
@@ -6251,6 +6279,11 @@ hipError_t launch_mp_gemm_conv(const uint8_t* img, const ConvGeo& cg, const floa
   a.cg = cg;
   const int64_t tiles = ((M + 63) / 64) * (wp.Np / kGemmBN);
   a.xcd_tiles = tiles <= 2048;
+  if (ap.S == 1) {
+    if (ap.c[0] == 4) launch_gemm_conv1<4>(a, M, stream);
+    else launch_gemm_conv1<8>(a, M, stream);
+    return hipGetLastError();
+  }
   const int cl = wp.c_lo, ch = wp.c_hi;
   if (cl == 4 && ch == 4) launch_gemm_conv_t<4, 4>(a, M, stream);
   else if (cl == 1 && ch == 4) launch_gemm_conv_t<1, 4>(a, M, stream);

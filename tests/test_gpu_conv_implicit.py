@@ -54,6 +54,9 @@ SMALL = [
     (1, 24, 6, 6, 33, 3, 6, 0.5, 2, 2, False, False),  # 2/2: one width
     (2, 16, 4, 5, 40, 4, 8, 0.6, 1, 2, True, False),   # 1/2
     (1, 16, 5, 5, 20, 4, 8, 0.6, 1, 1, False, False),  # 1/1: sign weights only
+    # one activation width (S = 1)
+    (2, 16, 5, 7, 32, 8, 8, 0.6, 1, 4, False, False),  # 8-bit activations only
+    (2, 12, 4, 6, 40, 3, 3, 0.6, 2, 8, True, False),   # 3-bit signed activations only
 ]
 
 

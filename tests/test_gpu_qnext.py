@@ -404,6 +404,7 @@ CONV_CHAINS = [  # (B, C1, H, W, N1, N2, a1, w1, a2, w2, a2_signed, implicit1)
     (3, 8, 4, 4, 48, 16, (4, 8), (4, 8), (4, 8), (1, 4), False, True),    # 16 channels past a group
     (1, 12, 2, 2, 24, 16, (4, 8), (2, 4), (4, 8), (2, 4), False, False),  # 4 pixels: a GEMV producer
     (2, 16, 5, 7, 32, 24, (4, 8), (5, 8), (4, 8), (1, 8), True, True),    # 8/8 producer, 1/8 next
+    (2, 16, 5, 7, 32, 24, (4, 8), (2, 4), (6, 6), (2, 8), True, True),    # one-width next (S = 1)
 ]
 
 
